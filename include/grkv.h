@@ -1,0 +1,162 @@
+/*
+ * grkv.h - C ABI of the MI355X (gfx950) GRKV prefill-compression path.
+ *
+ * GRKV ("Global Regression for KV cache", arXiv 2605.31105) compresses each
+ * (layer, KV head) slice of a prefilled KV cache in two stages:
+ *
+ *   1. SnapKV-style span retention.  The last w prompt queries (the surrogate
+ *      query window, Sec. 3.2) attend to the whole cache; every prefix token
+ *      is scored by the attention it receives from the window, the scores are
+ *      pooled over a window of pool_kernel neighbouring tokens, and the
+ *      budget - w best prefix tokens are kept together with the w window
+ *      tokens (Sec. 1 and Sec. 2, SnapKV).
+ *   2. The value step of the global ridge-regression merge (Eq. 6-8;
+ *      Algorithm 1, value step; App. D.1 and D.3).  With X the window's
+ *      attention over the retained keys and Y its attention output over the
+ *      full cache (Eq. 4), the free retained values are moved to
+ *      V*_G = V0_G + X_G^T (X_G X_G^T + lambda I_m)^-1 (Y - X V0),
+ *      which minimises ||Y - X V||_F^2 + lambda ||V - V0||_F^2 over V_G.
+ *      Fixed tokens (sinks, the window, the top beta of the retained set,
+ *      Sec. 3.4 "Fixed tokens during optimization") keep their values.
+ *      Keys are not moved: K* = K0.
+ *
+ * A "unit" is one (layer, KV head) slice; units are independent and are
+ * processed in one batched call.  G query heads share each KV head (grouped
+ * query attention); their windows are stacked into m = G*w rows, row
+ * r = g*w + i holding query head g at window position i, which sits at token
+ * position n - w + i.
+ *
+ * Memory: every pointer argument is DEVICE memory owned by the caller.  The
+ * library allocates nothing and keeps no state between calls; calls with
+ * distinct workspaces may run concurrently on different streams.
+ * Calls are asynchronous on `stream`; results are valid once the stream has
+ * been synchronised.  No exception crosses this interface.
+ */
+#ifndef GRKV_H
+#define GRKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Return codes.  Argument errors are found on the host before anything is
+ * launched, and then nothing is written. */
+typedef enum {
+  GRKV_OK = 0,
+  GRKV_ERR_INVALID = -1,     /* bad argument (null pointer, size out of range) */
+  GRKV_ERR_WORKSPACE = -2,   /* workspace smaller than grkv_workspace_bytes() */
+  GRKV_ERR_UNSUPPORTED = -3, /* valid but not built: head_dim not 64/128, m = G*w > 256 */
+  GRKV_ERR_HIP = -4          /* a HIP launch failed */
+} grkv_status;
+
+/* Element type of q_obs, K, V and k_out. */
+typedef enum { GRKV_BF16 = 0, GRKV_F32 = 1 } grkv_dtype;
+
+/* Per-unit status in stats[u][3]. */
+#define GRKV_UNIT_OK 0
+#define GRKV_UNIT_SINGULAR 1 /* non-positive Cholesky pivot: v_out holds V0 */
+
+typedef struct {
+  int32_t units;    /* U >= 1: number of (layer, KV head) slices */
+  int32_t group;    /* G >= 1: query heads per KV head */
+  int32_t head_dim; /* d: 64 or 128 */
+  int32_t dtype;    /* grkv_dtype */
+} grkv_problem;
+
+/* Fixed-token and masking options.  NULL selects the defaults
+ * {n_sink = 4, beta = 0.10f, fix_window = 1, causal_window = 1}:
+ * the paper keeps sink tokens, the window tokens and the top 10% retained
+ * tokens fixed (Sec. 4.1 hyperparameters). */
+typedef struct {
+  int32_t n_sink;        /* retained positions below n_sink stay fixed (>= 0) */
+  float beta;            /* in [0, 1]: the first floor(beta * budget) prefix
+                            tokens of the selection order stay fixed */
+  int32_t fix_window;    /* nonzero: the w window tokens stay fixed */
+  int32_t causal_window; /* nonzero: window row at position p sees keys 0..p only */
+} grkv_options;
+
+/* Outputs, all device memory owned by the caller, c = budget:
+ *   idx   int32 [U][c]      retained positions, ascending; the last w entries
+ *                           are n-w .. n-1.  Ties in the pooled score go to the
+ *                           lower position.
+ *   k_out dtype [U][c][d]   K0 = K[idx], bit-exact copies of the input rows
+ *   v_out float [U][c][d]   merged values V*
+ *   stats float [U][4]      {||Y||_F^2, D_before, D_after, unit status}, where
+ *                           D = ||Y - X V||_F^2 / ||Y||_F^2 (the raw numerator
+ *                           when ||Y|| = 0) with V = V0 and V = V*; may be NULL
+ *   workspace               at least grkv_workspace_bytes() bytes, 256-byte
+ *                           aligned; its contents on return are described by
+ *                           grkv_workspace_layout(). */
+typedef struct {
+  int32_t* idx;
+  void* k_out;
+  float* v_out;
+  float* stats;
+  void* workspace;
+  size_t workspace_bytes;
+} grkv_outputs;
+
+/* Compress U units.
+ *   q_obs  dtype [U][G][w][d]  the window queries (post-RoPE), query head
+ *                               kv_head*G + g of unit u at [u][g]
+ *   K, V   dtype [U][n][d]     the full cache (post-RoPE keys)
+ *   n            tokens per unit, w <= budget <= n, n <= 2^30
+ *   window       w >= 1
+ *   budget       c: retained tokens including the w window tokens
+ *   pool_kernel  odd k >= 1: scores are summed over positions j-(k-1)/2 ..
+ *                j+(k-1)/2 (zero outside the prefix) before ranking
+ *   lambda       ridge coefficient lambda_v >= 0 (finite)
+ *   stream       hipStream_t, NULL for the default stream
+ * Errors: GRKV_ERR_INVALID for null pointers, units < 1, group < 1,
+ * window < 1, budget < window, budget > n, even or < 1 pool_kernel,
+ * negative or non-finite lambda, beta outside [0, 1], n_sink < 0, an unknown
+ * dtype; GRKV_ERR_UNSUPPORTED for head_dim not in {64, 128} or G*w > 256;
+ * GRKV_ERR_WORKSPACE when out->workspace_bytes is too small; GRKV_ERR_HIP
+ * when a launch fails (outputs are then undefined). */
+int grkv_compress(const void* q_obs, const void* K, const void* V, int64_t n,
+                  int32_t window, int32_t budget, int32_t pool_kernel,
+                  float lambda, void* stream, const grkv_problem* prob,
+                  const grkv_options* opt, const grkv_outputs* out);
+
+/* Workspace bytes grkv_compress needs for this shape; 0 if the shape is
+ * invalid or unsupported. */
+size_t grkv_workspace_bytes(const grkv_problem* prob, int64_t n,
+                            int32_t window, int32_t budget);
+
+/* Byte offsets, inside the workspace, of intermediates that remain readable
+ * after grkv_compress returns (mp = m rounded up to a multiple of 32; rows
+ * m..mp-1 are padding; P = n - w):
+ *   lse      double [U][mp]     natural log-sum-exp of each window row over the
+ *                               full cache (window attention normaliser)
+ *   y        float  [U][mp][d]  Y = A V, the full-cache window attention output
+ *   score    float  [U][P]      SnapKV score s_j = sum_r A[r][j]
+ *   pooled   float  [U][P]      pooled score p_j
+ *   fixed    uint8  [U][c]      1 where the retained slot is fixed
+ *   x        float  [U][mp][c]  X, window attention over the retained keys
+ *   resid    float  [U][mp][d]  R = Y - X V0
+ *   gram     float  [U][mp][mp] N = X_G X_G^T + lambda I (padding rows: identity)
+ *   z        float  [U][d][mp]  Z^T, Z = N^-1 R
+ * Returns GRKV_OK, or GRKV_ERR_INVALID / GRKV_ERR_UNSUPPORTED like
+ * grkv_compress. */
+typedef struct {
+  size_t lse, y, score, pooled, fixed, x, resid, gram, z;
+  size_t total;
+} grkv_layout;
+
+int grkv_workspace_layout(const grkv_problem* prob, int64_t n, int32_t window,
+                          int32_t budget, grkv_layout* layout);
+
+/* The default options (see grkv_options). */
+void grkv_default_options(grkv_options* opt);
+
+/* Static description of a return code; never NULL. */
+const char* grkv_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GRKV_H */

@@ -1,0 +1,204 @@
+"""MI355X (gfx950) GRKV prefill-compression path: Python binding.
+
+Argument marshalling only.  Every step of the computation runs in the HIP
+kernels of ``libgrkv.so`` behind the C ABI declared in ``include/grkv.h``;
+PyTorch supplies device memory and the stream.  Importing works without a GPU;
+calling ``compress`` requires the built library and a ROCm device, and raises
+if either is missing (there is no CPU fallback).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+__all__ = [
+    "GRKV_OK", "GRKV_ERR_INVALID", "GRKV_ERR_WORKSPACE", "GRKV_ERR_UNSUPPORTED",
+    "GRKV_ERR_HIP", "GrkvError", "lib", "lib_path", "Problem", "Options", "Outputs",
+    "Layout", "workspace_bytes", "workspace_layout", "compress", "Result",
+    "intermediates", "EXPORTED_SYMBOLS",
+]
+
+GRKV_OK, GRKV_ERR_INVALID, GRKV_ERR_WORKSPACE, GRKV_ERR_UNSUPPORTED, GRKV_ERR_HIP = 0, -1, -2, -3, -4
+GRKV_BF16, GRKV_F32 = 0, 1
+EXPORTED_SYMBOLS = ("grkv_compress", "grkv_workspace_bytes", "grkv_workspace_layout",
+                    "grkv_default_options", "grkv_status_string")
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+
+
+def lib_path() -> str:
+    return os.path.join(_PKG, "libgrkv.so")
+
+
+class GrkvError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__("grkv status %d: %s" % (status, msg))
+        self.status = status
+
+
+class Problem(ctypes.Structure):
+    _fields_ = [("units", ctypes.c_int32), ("group", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+class Options(ctypes.Structure):
+    _fields_ = [("n_sink", ctypes.c_int32), ("beta", ctypes.c_float),
+                ("fix_window", ctypes.c_int32), ("causal_window", ctypes.c_int32)]
+
+
+class Outputs(ctypes.Structure):
+    _fields_ = [("idx", ctypes.c_void_p), ("k_out", ctypes.c_void_p),
+                ("v_out", ctypes.c_void_p), ("stats", ctypes.c_void_p),
+                ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t)]
+
+
+class Layout(ctypes.Structure):
+    _fields_ = [(f, ctypes.c_size_t) for f in
+                ("lse", "y", "score", "pooled", "fixed", "x", "resid", "gram", "z", "total")]
+
+
+_LIB = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libgrkv.so (once).  Raises if it has not been built."""
+    global _LIB
+    if _LIB is None:
+        path = lib_path()
+        if not os.path.exists(path):
+            raise RuntimeError("libgrkv.so is not built: run `python -m paper_2605_31105_amd.build`")
+        L = ctypes.CDLL(path)
+        P = ctypes.POINTER
+        L.grkv_compress.restype = ctypes.c_int
+        L.grkv_compress.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                    ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                    ctypes.c_int32, ctypes.c_float, ctypes.c_void_p,
+                                    P(Problem), P(Options), P(Outputs)]
+        L.grkv_workspace_bytes.restype = ctypes.c_size_t
+        L.grkv_workspace_bytes.argtypes = [P(Problem), ctypes.c_int64, ctypes.c_int32, ctypes.c_int32]
+        L.grkv_workspace_layout.restype = ctypes.c_int
+        L.grkv_workspace_layout.argtypes = [P(Problem), ctypes.c_int64, ctypes.c_int32,
+                                            ctypes.c_int32, P(Layout)]
+        L.grkv_default_options.restype = None
+        L.grkv_default_options.argtypes = [P(Options)]
+        L.grkv_status_string.restype = ctypes.c_char_p
+        L.grkv_status_string.argtypes = [ctypes.c_int]
+        _LIB = L
+    return _LIB
+
+
+def status_string(status: int) -> str:
+    return lib().grkv_status_string(status).decode()
+
+
+def _check(status: int):
+    if status != GRKV_OK:
+        raise GrkvError(status, status_string(status))
+
+
+def workspace_bytes(units, group, head_dim, dtype, n, window, budget) -> int:
+    prob = Problem(units, group, head_dim, dtype)
+    return int(lib().grkv_workspace_bytes(ctypes.byref(prob), n, window, budget))
+
+
+def workspace_layout(units, group, head_dim, dtype, n, window, budget) -> Layout:
+    prob = Problem(units, group, head_dim, dtype)
+    lay = Layout()
+    _check(lib().grkv_workspace_layout(ctypes.byref(prob), n, window, budget, ctypes.byref(lay)))
+    return lay
+
+
+@dataclass
+class Result:
+    idx: "object"        # int32 [U, c]
+    k_out: "object"      # input dtype [U, c, d]
+    v_out: "object"      # float32 [U, c, d]
+    stats: "object"      # float32 [U, 4]
+    workspace: "object"  # uint8 workspace, see intermediates()
+    shape: tuple         # (U, G, d, dtype, n, window, budget)
+
+
+def compress(q_obs, K, V, window: int, budget: int, pool_kernel: int, lam: float, *,
+             n_sink: int = 4, beta: float = 0.10, fix_window: bool = True,
+             causal_window: bool = True, stream=None, workspace=None, out=None) -> Result:
+    """GRKV compression of U units on the GPU.
+
+    q_obs [U, G, w, d], K and V [U, n, d]: contiguous CUDA tensors of one dtype
+    (bfloat16 or float32).  Returns the retained indices, K0, the merged V*,
+    per-unit stats {||Y||^2, D_before, D_after, status} and the workspace.
+    ``workspace`` (uint8, >= workspace_bytes) and ``out`` (a Result whose
+    tensors are reused) avoid allocations in timed loops.
+    """
+    import torch
+
+    if not (q_obs.is_cuda and K.is_cuda and V.is_cuda):
+        raise ValueError("q_obs, K and V must be device tensors")
+    if not (q_obs.dtype == K.dtype == V.dtype) or K.dtype not in (torch.bfloat16, torch.float32):
+        raise ValueError("q_obs, K, V must share dtype bfloat16 or float32")
+    if not (q_obs.is_contiguous() and K.is_contiguous() and V.is_contiguous()):
+        raise ValueError("inputs must be contiguous")
+    U, G, w, d = q_obs.shape
+    if w != window or K.shape[0] != U or K.shape[2] != d or V.shape != K.shape:
+        raise ValueError("shape mismatch: q_obs %s K %s V %s window %d"
+                         % (tuple(q_obs.shape), tuple(K.shape), tuple(V.shape), window))
+    n = K.shape[1]
+    dt = GRKV_BF16 if K.dtype == torch.bfloat16 else GRKV_F32
+    dev = K.device
+    need = workspace_bytes(U, G, d, dt, n, window, budget)
+    if need == 0:
+        # let the library report the precise error
+        need = 256
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    if out is None:
+        out = Result(idx=torch.empty((U, budget), dtype=torch.int32, device=dev),
+                     k_out=torch.empty((U, budget, d), dtype=K.dtype, device=dev),
+                     v_out=torch.empty((U, budget, d), dtype=torch.float32, device=dev),
+                     stats=torch.empty((U, 4), dtype=torch.float32, device=dev),
+                     workspace=workspace, shape=())
+    out.workspace = workspace
+    out.shape = (U, G, d, dt, n, window, budget)
+    prob = Problem(U, G, d, dt)
+    opt = Options(n_sink, beta, 1 if fix_window else 0, 1 if causal_window else 0)
+    outs = Outputs(out.idx.data_ptr(), out.k_out.data_ptr(), out.v_out.data_ptr(),
+                   out.stats.data_ptr(), workspace.data_ptr(), workspace.numel())
+    if stream is None:
+        stream = torch.cuda.current_stream(dev)
+    handle = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+    st = lib().grkv_compress(q_obs.data_ptr(), K.data_ptr(), V.data_ptr(), n, window, budget,
+                             pool_kernel, float(lam), ctypes.c_void_p(handle),
+                             ctypes.byref(prob), ctypes.byref(opt), ctypes.byref(outs))
+    _check(st)
+    return out
+
+
+def intermediates(res: Result) -> dict:
+    """Views of the workspace intermediates of the last call (see grkv.h)."""
+    import torch
+
+    U, G, d, dt, n, w, c = res.shape
+    lay = workspace_layout(U, G, d, dt, n, w, c)
+    m = G * w
+    mp = (m + 31) // 32 * 32
+    P = n - w
+    ws = res.workspace
+
+    def view(off, dtype, shape):
+        count = 1
+        for s in shape:
+            count *= s
+        nbytes = count * torch.empty((), dtype=dtype).element_size()
+        return ws[off:off + nbytes].view(dtype).view(*shape)
+
+    return {
+        "lse": view(lay.lse, torch.float64, (U, mp))[:, :m],
+        "y": view(lay.y, torch.float32, (U, mp, d))[:, :m],
+        "score": view(lay.score, torch.float32, (U, P)),
+        "pooled": view(lay.pooled, torch.float32, (U, P)),
+        "fixed": view(lay.fixed, torch.uint8, (U, c)),
+        "x": view(lay.x, torch.float32, (U, mp, c))[:, :m],
+        "resid": view(lay.resid, torch.float32, (U, mp, d))[:, :m],
+        "gram": view(lay.gram, torch.float32, (U, mp, mp))[:, :m, :m],
+        "z": view(lay.z, torch.float32, (U, d, mp))[:, :, :m],
+    }

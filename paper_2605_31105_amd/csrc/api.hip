@@ -1,0 +1,203 @@
+// Host side of the C ABI: argument checks, the workspace plan and the launch
+// sequence of one grkv_compress call.  Everything is enqueued on the caller's
+// stream without a host synchronisation.
+#include <math.h>
+#include <string.h>
+
+#include "grkv_internal.h"
+
+namespace grkv {
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+static int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Split a key range of length len over at most `want` blocks of >= min_len keys,
+// each a whole number of key tiles.
+static void split_range(int64_t len, int64_t want, int64_t min_len, int* S, int* chunk) {
+  int64_t s = want < 1 ? 1 : want;
+  int64_t cap = ceil_div(len, min_len);
+  if (s > cap) s = cap;
+  if (s < 1) s = 1;
+  int64_t ch = ceil_div(len, s);
+  ch = ceil_div(ch, kKeyTile) * kKeyTile;
+  if (ch < kKeyTile) ch = kKeyTile;
+  *chunk = (int)ch;
+  *S = (int)(len > 0 ? ceil_div(len, ch) : 1);
+}
+
+int make_plan(const grkv_problem* prob, int64_t n, int32_t window, int32_t budget,
+              int32_t pool_kernel, float lambda, const grkv_options* opt, Plan* p) {
+  if (!prob) return GRKV_ERR_INVALID;
+  if (prob->units < 1 || prob->group < 1) return GRKV_ERR_INVALID;
+  if (prob->dtype != GRKV_BF16 && prob->dtype != GRKV_F32) return GRKV_ERR_INVALID;
+  if (window < 1 || budget < window || (int64_t)budget > n || n > (int64_t(1) << 30))
+    return GRKV_ERR_INVALID;
+  if (pool_kernel < 1 || pool_kernel % 2 == 0) return GRKV_ERR_INVALID;
+  if (!(lambda >= 0.f) || !isfinite(lambda)) return GRKV_ERR_INVALID;
+  grkv_options o;
+  grkv_default_options(&o);
+  if (opt) o = *opt;
+  if (o.n_sink < 0 || !(o.beta >= 0.f && o.beta <= 1.f)) return GRKV_ERR_INVALID;
+  if (prob->head_dim != 64 && prob->head_dim != 128) return GRKV_ERR_UNSUPPORTED;
+  int64_t m = (int64_t)prob->group * window;
+  if (m > 256) return GRKV_ERR_UNSUPPORTED;
+
+  memset(p, 0, sizeof(*p));
+  p->U = prob->units;
+  p->G = prob->group;
+  p->w = window;
+  p->m = (int)m;
+  p->mp = (int)ceil_div(m, kRowsPerWave) * kRowsPerWave;
+  p->waves = p->mp / kRowsPerWave;
+  p->d = prob->head_dim;
+  p->dtype = prob->dtype;
+  p->n = n;
+  p->c = budget;
+  p->s_sel = budget - window;
+  p->prefix = (int)(n - window);
+  p->k_pool = pool_kernel;
+  int64_t top = (int64_t)floor((double)o.beta * (double)budget);
+  p->n_top_fixed = (int)(top < p->s_sel ? top : p->s_sel);
+  p->lam = lambda;
+  p->opt = o;
+
+  // Target about 512 blocks per launch so every CU holds two.
+  const int64_t want = ceil_div(512, p->U);
+  split_range(n, want, 512, &p->S1, &p->chunk1);
+  split_range(budget, want, 128, &p->S2, &p->chunk2);
+  split_range(budget, ceil_div(256, p->U), 256, &p->S3, &p->chunk3);
+
+  const size_t U = p->U, mp = p->mp, d = p->d, c = budget, P = p->prefix;
+  const size_t esz = p->dtype == GRKV_BF16 ? 2 : 4;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o2 = off; off = align256(off + bytes); return o2; };
+  p->pmax1 = take(U * p->S1 * mp * sizeof(float));
+  p->psum1 = take(U * p->S1 * mp * sizeof(double));
+  p->lse1 = take(U * mp * sizeof(double));
+  p->lse1_log2 = take(U * mp * sizeof(float));
+  p->ypart = take(U * p->S1 * mp * d * sizeof(float));
+  p->y = take(U * mp * d * sizeof(float));
+  p->colsum = take(U * (P > 0 ? P : 1) * sizeof(float));
+  p->pooled = take(U * (P > 0 ? P : 1) * sizeof(float));
+  p->fixed = take(U * c);
+  p->v0c = take(U * c * d * esz);
+  p->pmax2 = take(U * p->S2 * mp * sizeof(float));
+  p->psum2 = take(U * p->S2 * mp * sizeof(double));
+  p->lse2 = take(U * mp * sizeof(double));
+  p->lse2_log2 = take(U * mp * sizeof(float));
+  p->xvpart = take(U * p->S2 * mp * d * sizeof(float));
+  p->x = take(U * mp * c * sizeof(float));
+  p->resid = take(U * mp * d * sizeof(float));
+  p->npart = take(U * p->S3 * mp * mp * sizeof(float));
+  p->gram = take(U * mp * mp * sizeof(float));
+  p->z = take(U * d * mp * sizeof(float));
+  p->stats_ws = take(U * 4 * sizeof(float));
+  p->total = off;
+  return GRKV_OK;
+}
+
+}  // namespace grkv
+
+using namespace grkv;
+
+extern "C" {
+
+void grkv_default_options(grkv_options* opt) {
+  if (!opt) return;
+  opt->n_sink = 4;
+  opt->beta = 0.10f;
+  opt->fix_window = 1;
+  opt->causal_window = 1;
+}
+
+const char* grkv_status_string(int status) {
+  switch (status) {
+    case GRKV_OK: return "ok";
+    case GRKV_ERR_INVALID: return "invalid argument";
+    case GRKV_ERR_WORKSPACE: return "workspace too small";
+    case GRKV_ERR_UNSUPPORTED: return "unsupported shape (head_dim must be 64 or 128, group*window <= 256)";
+    case GRKV_ERR_HIP: return "HIP launch failed";
+  }
+  return "unknown status";
+}
+
+size_t grkv_workspace_bytes(const grkv_problem* prob, int64_t n, int32_t window, int32_t budget) {
+  Plan p;
+  if (make_plan(prob, n, window, budget, 1, 0.f, nullptr, &p) != GRKV_OK) return 0;
+  return p.total;
+}
+
+int grkv_workspace_layout(const grkv_problem* prob, int64_t n, int32_t window, int32_t budget,
+                          grkv_layout* layout) {
+  if (!layout) return GRKV_ERR_INVALID;
+  Plan p;
+  int st = make_plan(prob, n, window, budget, 1, 0.f, nullptr, &p);
+  if (st != GRKV_OK) return st;
+  layout->lse = p.lse1;
+  layout->y = p.y;
+  layout->score = p.colsum;
+  layout->pooled = p.pooled;
+  layout->fixed = p.fixed;
+  layout->x = p.x;
+  layout->resid = p.resid;
+  layout->gram = p.gram;
+  layout->z = p.z;
+  layout->total = p.total;
+  return GRKV_OK;
+}
+
+int grkv_compress(const void* q_obs, const void* K, const void* V, int64_t n, int32_t window,
+                  int32_t budget, int32_t pool_kernel, float lambda, void* stream,
+                  const grkv_problem* prob, const grkv_options* opt, const grkv_outputs* out) {
+  if (!q_obs || !K || !V || !prob || !out) return GRKV_ERR_INVALID;
+  if (!out->idx || !out->k_out || !out->v_out || !out->workspace) return GRKV_ERR_INVALID;
+  Plan p;
+  int st = make_plan(prob, n, window, budget, pool_kernel, lambda, opt, &p);
+  if (st != GRKV_OK) return st;
+  if (out->workspace_bytes < p.total) return GRKV_ERR_WORKSPACE;
+  if (((uintptr_t)out->workspace & 255) != 0) return GRKV_ERR_INVALID;
+
+  hipStream_t s = (hipStream_t)stream;
+  char* ws = (char*)out->workspace;
+  auto F = [&](size_t o) { return (float*)(ws + o); };
+  auto Dd = [&](size_t o) { return (double*)(ws + o); };
+
+#define GRKV_TRY(x) do { if ((x) != hipSuccess) return GRKV_ERR_HIP; } while (0)
+  // 1. window attention over the full cache: LSE, then Y and the SnapKV scores
+  AttnPass full = {};
+  full.q = q_obs; full.k = K; full.v = V; full.kpos = nullptr; full.nk = (int)n;
+  full.S = p.S1; full.chunk = p.chunk1;
+  full.pmax = F(p.pmax1); full.psum = Dd(p.psum1);
+  full.lse = Dd(p.lse1); full.lse_log2 = F(p.lse1_log2);
+  full.ypart = F(p.ypart); full.colsum = p.prefix > 0 ? F(p.colsum) : nullptr;
+  full.prefix = p.prefix; full.xout = nullptr; full.split_p = true;
+  GRKV_TRY(launch_lse_pass(p, full, s));
+  GRKV_TRY(launch_lse_combine(p, full.pmax, full.psum, p.S1, Dd(p.lse1), F(p.lse1_log2), s));
+  GRKV_TRY(launch_prob_pass(p, full, s));
+  GRKV_TRY(launch_combine_rows(p, F(p.ypart), p.S1, nullptr, F(p.y), s));
+  // 2. pooled top-k retention and the fixed set; gather K0, V0
+  uint8_t* fixed = (uint8_t*)(ws + p.fixed);
+  GRKV_TRY(launch_select(p, F(p.colsum), F(p.pooled), out->idx, fixed, s));
+  GRKV_TRY(launch_gather(p, K, V, out->idx, out->k_out, ws + p.v0c, out->v_out, s));
+  // 3. window attention over the retained cache: X and X V0, then R = Y - X V0
+  AttnPass ret = {};
+  ret.q = q_obs; ret.k = out->k_out; ret.v = ws + p.v0c; ret.kpos = out->idx; ret.nk = p.c;
+  ret.S = p.S2; ret.chunk = p.chunk2;
+  ret.pmax = F(p.pmax2); ret.psum = Dd(p.psum2);
+  ret.lse = Dd(p.lse2); ret.lse_log2 = F(p.lse2_log2);
+  ret.ypart = F(p.xvpart); ret.colsum = nullptr; ret.prefix = 0; ret.xout = F(p.x);
+  ret.split_p = true;
+  GRKV_TRY(launch_lse_pass(p, ret, s));
+  GRKV_TRY(launch_lse_combine(p, ret.pmax, ret.psum, p.S2, Dd(p.lse2), F(p.lse2_log2), s));
+  GRKV_TRY(launch_prob_pass(p, ret, s));
+  GRKV_TRY(launch_combine_rows(p, F(p.xvpart), p.S2, F(p.y), F(p.resid), s));
+  // 4. value step: N, Cholesky solve for Z, V* = V0 + X_G^T Z
+  GRKV_TRY(launch_gram(p, F(p.x), fixed, F(p.npart), s));
+  GRKV_TRY(launch_cholesky_solve(p, F(p.npart), F(p.y), F(p.resid), F(p.gram), F(p.z),
+                                 F(p.stats_ws), out->stats, s));
+  GRKV_TRY(launch_update(p, F(p.x), fixed, F(p.z), F(p.stats_ws), out->v_out, s));
+#undef GRKV_TRY
+  return GRKV_OK;
+}
+
+}  // extern "C"

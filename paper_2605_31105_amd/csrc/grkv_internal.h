@@ -1,0 +1,86 @@
+// Internal declarations shared by the host API and the kernel launchers of the
+// gfx950 GRKV path.  Not installed; the public interface is include/grkv.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "grkv.h"
+
+namespace grkv {
+
+constexpr int kRowsPerWave = 32;   // each wave owns 32 stacked window rows
+constexpr int kKeyTile = 32;       // keys per streamed tile
+constexpr int kSelectThreads = 1024;
+
+// Everything a call needs, derived on the host from the arguments.
+struct Plan {
+  // shape
+  int U, G, w, m, mp, waves, d, dtype;
+  int64_t n;
+  int c, s_sel, prefix, k_pool, n_top_fixed;
+  float lam;
+  grkv_options opt;
+  // work split of the full-cache passes: S1 splits of chunk1 keys per unit
+  int S1, chunk1;
+  // retained-cache passes over the c retained keys
+  int S2, chunk2;
+  // Gram-matrix splits over the c retained columns
+  int S3, chunk3;
+  // workspace offsets (bytes)
+  size_t pmax1, psum1, lse1, lse1_log2, ypart, y, colsum, pooled, fixed, v0c;
+  size_t pmax2, psum2, lse2, lse2_log2, xvpart, x, resid, npart, gram, z, stats_ws;
+  size_t total;
+};
+
+// Fills `plan`; returns GRKV_OK or the error the call must report.
+int make_plan(const grkv_problem* prob, int64_t n, int32_t window,
+              int32_t budget, int32_t pool_kernel, float lambda,
+              const grkv_options* opt, Plan* plan);
+
+// One streamed attention pass over nk keys per unit.
+struct AttnPass {
+  const void* q;       // [U][m][d] stacked window rows
+  const void* k;       // [U][nk][d]
+  const void* v;       // [U][nk][d] (pass B only)
+  const int32_t* kpos; // [U][nk] token position of each key, or null (= key index)
+  int nk;              // keys per unit
+  int S, chunk;        // splits per unit and keys per split
+  float* pmax;         // pass A out [U][S][mp]: row max of log2-scaled logits
+  double* psum;        // pass A out [U][S][mp]: sum of 2^(t - max)
+  const double* lse;   // in: [U][mp] natural LSE (combine output)
+  const float* lse_log2; // pass B in: [U][mp] log2-domain LSE
+  float* ypart;        // pass B out [U][S][mp][d]
+  float* colsum;       // pass B out [U][prefix] column sums over rows, or null
+  int prefix;          // only keys < prefix get a column sum
+  float* xout;         // pass B out [U][mp][nk] probabilities, or null
+  bool split_p;        // P.V with P as a bf16 hi+lo pair (else bf16 P)
+};
+
+hipError_t launch_lse_pass(const Plan& p, const AttnPass& a, hipStream_t s);
+hipError_t launch_lse_combine(const Plan& p, const float* pmax,
+                              const double* psum, int S, double* lse,
+                              float* lse_log2, hipStream_t s);
+hipError_t launch_prob_pass(const Plan& p, const AttnPass& a, hipStream_t s);
+// out[u][r][c] = (base ? base[u][r][c] : 0) +/- sum_s part[u][s][r][c]
+hipError_t launch_combine_rows(const Plan& p, const float* part, int S,
+                               const float* base, float* out, hipStream_t s);
+
+hipError_t launch_select(const Plan& p, const float* colsum, float* pooled,
+                         int32_t* idx, uint8_t* fixed, hipStream_t s);
+hipError_t launch_gather(const Plan& p, const void* K, const void* V,
+                         const int32_t* idx, void* k_out, void* v0c,
+                         float* v_out, hipStream_t s);
+hipError_t launch_gram(const Plan& p, const float* x, const uint8_t* fixed,
+                       float* npart, hipStream_t s);
+// Writes the per-unit stats to stats_ws (always) and stats_user (if not null).
+hipError_t launch_cholesky_solve(const Plan& p, const float* npart,
+                                 const float* y, const float* resid,
+                                 float* gram, float* z, float* stats_ws,
+                                 float* stats_user, hipStream_t s);
+hipError_t launch_update(const Plan& p, const float* x, const uint8_t* fixed,
+                         const float* z, const float* stats_ws, float* v_out,
+                         hipStream_t s);
+
+}  // namespace grkv

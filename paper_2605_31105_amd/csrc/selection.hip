@@ -1,0 +1,185 @@
+// SnapKV-style span retention for each unit, one 1024-thread block per unit:
+//   1. pooling: p_j = sum_{t=j-h}^{j+h} s_t over the prefix (zero outside),
+//      summed left to right;
+//   2. radix select (4 passes of 8 bits on the fp32 bit patterns, which order
+//      like the values since p >= 0) of the (c-w)-th and of the
+//      floor(beta*c)-th largest pooled score;
+//   3. compaction in ascending position order: every prefix position above
+//      the threshold, plus the lowest-position ones equal to it until the
+//      count is met (ties go to the lower position), then the w window
+//      positions; the fixed flag marks sinks, window tokens and the top
+//      floor(beta*c) selections.
+// Then the gather of the retained K rows (bit-exact copy), of V0 in the input
+// type for the retained-cache passes, and of V0 in fp32 into v_out.
+#include "grkv_device.h"
+#include "grkv_internal.h"
+
+namespace grkv {
+namespace {
+
+struct SelK {
+  const float* colsum;
+  float* pooled;
+  int32_t* idx;
+  uint8_t* fixed;
+  int prefix, c, w, h, s_sel, n_top, n_sink, fix_window;
+  int64_t n;
+};
+
+__global__ __launch_bounds__(kSelectThreads) void select_kernel(SelK a) {
+  __shared__ uint32_t hist[2][256];
+  __shared__ uint32_t sh_state[4];
+  __shared__ uint32_t scan_scratch[16];
+
+  const int u = blockIdx.x, tid = threadIdx.x;
+  const int P = a.prefix;
+  const float* s = a.colsum + (size_t)u * P;
+  float* p = a.pooled + (size_t)u * P;
+  int32_t* idx = a.idx + (size_t)u * a.c;
+  uint8_t* fixed = a.fixed + (size_t)u * a.c;
+
+  for (int j = tid; j < P; j += blockDim.x) {
+    int lo = j - a.h < 0 ? 0 : j - a.h;
+    int hi = j + a.h > P - 1 ? P - 1 : j + a.h;
+    float acc = 0.f;
+    for (int t = lo; t <= hi; ++t) acc += s[t];
+    p[j] = acc;
+  }
+  __syncthreads();
+
+  // radix select of the k-th largest for k = s_sel (target 0) and n_top (1)
+  uint32_t prefix[2] = {0u, 0u}, krem[2] = {(uint32_t)a.s_sel, (uint32_t)a.n_top};
+  uint32_t mask = 0u;
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    for (int b = tid; b < 512; b += blockDim.x) (&hist[0][0])[b] = 0u;
+    __syncthreads();
+    for (int j = tid; j < P; j += blockDim.x) {
+      uint32_t key = __float_as_uint(p[j]);
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+        if (krem[t] > 0 && (key & mask) == prefix[t]) atomicAdd(&hist[t][(key >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    if (tid < 2 && krem[tid] > 0) {
+      uint32_t cum = 0;
+      int digit = 0;
+      for (int b = 255; b >= 0; --b) {
+        uint32_t hcount = hist[tid][b];
+        if (cum + hcount >= krem[tid]) { digit = b; break; }
+        cum += hcount;
+      }
+      sh_state[2 * tid] = prefix[tid] | ((uint32_t)digit << shift);
+      sh_state[2 * tid + 1] = krem[tid] - cum;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+      if (krem[t] > 0) { prefix[t] = sh_state[2 * t]; krem[t] = sh_state[2 * t + 1]; }
+    mask |= 255u << shift;
+    __syncthreads();
+  }
+  // prefix[t] = bits of the k-th largest score; krem[t] = how many scores
+  // equal to it are taken (lowest positions first); all larger ones are taken.
+  const uint32_t T0 = prefix[0], T1 = prefix[1];
+  const bool any0 = a.s_sel > 0, any1 = a.n_top > 0;
+
+  const int per = (P + blockDim.x - 1) / blockDim.x;
+  const int j0 = min(P, tid * per), j1 = min(P, j0 + per);
+  uint32_t eq0 = 0, eq1 = 0;
+  for (int j = j0; j < j1; ++j) {
+    uint32_t key = __float_as_uint(p[j]);
+    eq0 += (any0 && key == T0);
+    eq1 += (any1 && key == T1);
+  }
+  uint32_t tot;
+  uint32_t eqb0 = block_exclusive_scan(eq0, scan_scratch, &tot);
+  uint32_t eqb1 = block_exclusive_scan(eq1, scan_scratch, &tot);
+  uint32_t nsel = 0;
+  {
+    uint32_t e0 = eqb0;
+    for (int j = j0; j < j1; ++j) {
+      uint32_t key = __float_as_uint(p[j]);
+      bool sel = any0 && (key > T0 || (key == T0 && e0 < krem[0]));
+      e0 += (any0 && key == T0);
+      nsel += sel;
+    }
+  }
+  uint32_t off = block_exclusive_scan(nsel, scan_scratch, &tot);
+  {
+    uint32_t e0 = eqb0, e1 = eqb1;
+    for (int j = j0; j < j1; ++j) {
+      uint32_t key = __float_as_uint(p[j]);
+      bool sel = any0 && (key > T0 || (key == T0 && e0 < krem[0]));
+      bool top = any1 && (key > T1 || (key == T1 && e1 < krem[1]));
+      e0 += (any0 && key == T0);
+      e1 += (any1 && key == T1);
+      if (sel) {
+        idx[off] = j;
+        fixed[off] = (j < a.n_sink || top) ? 1 : 0;
+        ++off;
+      }
+    }
+  }
+  for (int i = tid; i < a.w; i += blockDim.x) {
+    int64_t pos = a.n - a.w + i;
+    idx[a.s_sel + i] = (int32_t)pos;
+    fixed[a.s_sel + i] = (a.fix_window || pos < a.n_sink) ? 1 : 0;
+  }
+}
+
+template <typename T>
+__global__ void gather_kernel(const T* K, const T* V, const int32_t* idx, T* k_out, T* v0c,
+                              float* v_out, int c, int64_t n, int D) {
+  // one 16-byte chunk of one retained row per thread
+  const int u = blockIdx.y;
+  const int epc = 16 / (int)sizeof(T);
+  const int cpr = D / epc;
+  const int64_t chunk = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (chunk >= (int64_t)c * cpr) return;
+  const int row = (int)(chunk / cpr), cc = (int)(chunk % cpr);
+  const int64_t src = idx[(size_t)u * c + row];
+  const size_t so = ((size_t)u * n + src) * D + (size_t)cc * epc;
+  const size_t dof = ((size_t)u * c + row) * D + (size_t)cc * epc;
+  uint4 kv = make_uint4(0, 0, 0, 0), vv = kv;
+  if (src >= 0 && src < n) {  // the selection always writes in-range positions
+    kv = *reinterpret_cast<const uint4*>(K + so);
+    vv = *reinterpret_cast<const uint4*>(V + so);
+  }
+  *reinterpret_cast<uint4*>(k_out + dof) = kv;
+  *reinterpret_cast<uint4*>(v0c + dof) = vv;
+  const T* ve = reinterpret_cast<const T*>(&vv);
+  for (int e = 0; e < epc; ++e) {
+    float f;
+    if constexpr (sizeof(T) == 2) f = bf16_to_f32(ve[e]); else f = ve[e];
+    v_out[dof + e] = f;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_select(const Plan& p, const float* colsum, float* pooled, int32_t* idx,
+                         uint8_t* fixed, hipStream_t s) {
+  SelK a;
+  a.colsum = colsum; a.pooled = pooled; a.idx = idx; a.fixed = fixed;
+  a.prefix = p.prefix; a.c = p.c; a.w = p.w; a.h = (p.k_pool - 1) / 2;
+  a.s_sel = p.s_sel; a.n_top = p.n_top_fixed; a.n_sink = p.opt.n_sink;
+  a.fix_window = p.opt.fix_window ? 1 : 0; a.n = p.n;
+  hipLaunchKernelGGL(select_kernel, dim3(p.U), dim3(kSelectThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather(const Plan& p, const void* K, const void* V, const int32_t* idx,
+                         void* k_out, void* v0c, float* v_out, hipStream_t s) {
+  const int esz = p.dtype == GRKV_BF16 ? 2 : 4;
+  const int64_t chunks = (int64_t)p.c * (p.d * esz / 16);
+  dim3 grid((unsigned)((chunks + 255) / 256), p.U);
+  if (p.dtype == GRKV_BF16)
+    hipLaunchKernelGGL(gather_kernel<u16>, grid, dim3(256), 0, s, (const u16*)K, (const u16*)V,
+                       idx, (u16*)k_out, (u16*)v0c, v_out, p.c, p.n, p.d);
+  else
+    hipLaunchKernelGGL(gather_kernel<float>, grid, dim3(256), 0, s, (const float*)K,
+                       (const float*)V, idx, (float*)k_out, (float*)v0c, v_out, p.c, p.n, p.d);
+  return hipGetLastError();
+}
+
+}  // namespace grkv

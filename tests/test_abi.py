@@ -1,0 +1,101 @@
+"""The C ABI library on the CPU: it loads, exports every declared symbol, and
+rejects bad arguments on the host before launching anything."""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+import paper_2605_31105_amd as G
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    text = open(os.path.join(ROOT, "include", "grkv.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(grkv_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(G.lib_path()):
+        pytest.skip("libgrkv.so not built")
+    return G.lib()
+
+
+def test_exports_every_declared_symbol(L):
+    names = _declared()
+    assert set(names) == set(G.EXPORTED_SYMBOLS)
+    for name in names:
+        assert hasattr(L, name), name
+
+
+def test_defaults_and_status_strings(L):
+    o = G.Options()
+    L.grkv_default_options(ctypes.byref(o))
+    assert (o.n_sink, o.fix_window, o.causal_window) == (4, 1, 1)
+    assert abs(o.beta - 0.1) < 1e-7
+    for st in (0, -1, -2, -3, -4, 7):
+        assert len(G.status_string(st)) > 0
+
+
+def _call(L, U=2, Gq=4, d=128, dt=0, n=8192, w=32, c=512, k=7, lam=1e-2, opt=None,
+          ws_bytes=None, ws_ptr=4096, nullq=False):
+    prob = G.Problem(U, Gq, d, dt)
+    fake = ctypes.c_void_p(4096)   # never dereferenced: validation fails first
+    need = L.grkv_workspace_bytes(ctypes.byref(prob), n, w, c)
+    outs = G.Outputs(4096, 4096, 4096, 0, ws_ptr,
+                     (need if ws_bytes is None else ws_bytes))
+    return L.grkv_compress(None if nullq else fake, fake, fake, n, w, c, k, lam, None,
+                           ctypes.byref(prob), ctypes.byref(opt) if opt else None,
+                           ctypes.byref(outs))
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(nullq=True), G.GRKV_ERR_INVALID),
+    (dict(U=0), G.GRKV_ERR_INVALID),
+    (dict(Gq=0), G.GRKV_ERR_INVALID),
+    (dict(dt=7), G.GRKV_ERR_INVALID),
+    (dict(w=0), G.GRKV_ERR_INVALID),
+    (dict(c=16), G.GRKV_ERR_INVALID),
+    (dict(c=9000), G.GRKV_ERR_INVALID),
+    (dict(k=4), G.GRKV_ERR_INVALID),
+    (dict(k=0), G.GRKV_ERR_INVALID),
+    (dict(lam=-1.0), G.GRKV_ERR_INVALID),
+    (dict(lam=math.nan), G.GRKV_ERR_INVALID),
+    (dict(lam=math.inf), G.GRKV_ERR_INVALID),
+    (dict(opt=G.Options(4, 1.5, 1, 1)), G.GRKV_ERR_INVALID),
+    (dict(opt=G.Options(-1, 0.1, 1, 1)), G.GRKV_ERR_INVALID),
+    (dict(d=96), G.GRKV_ERR_UNSUPPORTED),
+    (dict(Gq=8, w=64), G.GRKV_ERR_UNSUPPORTED),
+    (dict(ws_bytes=1024), G.GRKV_ERR_WORKSPACE),
+    (dict(ws_ptr=4096 + 8), G.GRKV_ERR_INVALID),
+])
+def test_invalid_arguments_rejected_before_launch(L, kw, code):
+    assert _call(L, **kw) == code
+
+
+def test_workspace_size_and_layout(L):
+    def wb(**kw):
+        a = dict(U=8, Gq=4, d=128, dt=0, n=8192, w=32, c=512)
+        a.update(kw)
+        return G.workspace_bytes(a["U"], a["Gq"], a["d"], a["dt"], a["n"], a["w"], a["c"])
+    base = wb()
+    assert base > 0
+    assert wb(n=32768) > base and wb(c=1024) > base and wb(U=16) > base
+    assert wb(d=96) == 0 and wb(c=4) == 0
+    lay = G.workspace_layout(8, 4, 128, 0, 8192, 32, 512)
+    offs = [lay.lse, lay.y, lay.score, lay.pooled, lay.fixed, lay.x, lay.resid, lay.gram, lay.z]
+    assert len(set(offs)) == len(offs)
+    assert all(o % 256 == 0 and o < lay.total for o in offs)
+    assert lay.total == base
+
+
+def test_binding_refuses_host_tensors():
+    torch = pytest.importorskip("torch")
+    q = torch.zeros(1, 1, 4, 64)
+    K = torch.zeros(1, 16, 64)
+    with pytest.raises(ValueError):
+        G.compress(q, K, K, 4, 8, 7, 1e-2)
