@@ -1,0 +1,234 @@
+#!/usr/bin/env python3
+"""Benchmark of the GRKV prefill-compression path on one MI355X.
+
+One step = one grkv_compress call over the whole workload: window attention
+over the full cache, pooled top-k retention, retained-cache attention and the
+ridge value merge, for every (layer, KV head) unit.  Default workload: a
+32-layer x 8-KV-head Llama-3-8B-shaped cache, 32 query heads (G = 4),
+head_dim 128, n = 32768 tokens, window 32, budget 2048, pool kernel 7,
+lambda 1e-2, bfloat16, synthetic seeded inputs resident in HBM.
+
+Prints one JSON line: heads/s (value), ms per step and per layer, the
+roofline of the dominant kernel (its duration measured with HIP events around
+its launches inside the timed steps), and the float64 oracle's CPU throughput
+on a bounded sample of the same workload.
+
+  python bench.py [--steps K] [--warmup W] [--config 4] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "compressed KV heads/sec (and ms per layer) at n=32k; % of HBM roofline"
+HBM_PEAK_GBS = 8000.0   # MI355X HBM3E peak
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=4)
+    ap.add_argument("--budget", type=int, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run only a 1 GiB device copy (for counter calibration)")
+    return ap.parse_args()
+
+
+class Hip:
+    """The few HIP runtime calls the benchmark needs for raw events."""
+
+    def __init__(self):
+        self.lib = ctypes.CDLL("libamdhip64.so")
+
+    def event(self):
+        ev = ctypes.c_void_p()
+        if self.lib.hipEventCreate(ctypes.byref(ev)) != 0:
+            raise RuntimeError("hipEventCreate failed")
+        return ev
+
+    def elapsed_ms(self, a, b):
+        ms = ctypes.c_float()
+        if self.lib.hipEventElapsedTime(ctypes.byref(ms), a, b) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return ms.value
+
+    def destroy(self, ev):
+        self.lib.hipEventDestroy(ev)
+
+
+def source_hash(files):
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def copy_calibration():
+    import torch
+    x = torch.ones(2 ** 30 // 4, dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    for _ in range(5):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": 2 ** 30, "launches": 5}), flush=True)
+
+
+def cpu_baseline(cfg, q, K, V, seconds):
+    """The oracle as it stands, on a bounded sample of whole units."""
+    import numpy as np
+    import workloads as W
+    from oracle import grkv_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = 1
+    done, t0 = 0, time.perf_counter()
+    while done < cfg.units and (done < 2 or time.perf_counter() - t0 < seconds):
+        u = done
+        qd, Kd, Vd = (W.decode(a[u], cfg.dtype) for a in (q, K, V))
+        O.compress_unit(qd, Kd, Vd, cfg.window, cfg.budget, cfg.pool_kernel, cfg.lam)
+        done += 1
+    el = time.perf_counter() - t0
+    return {"value": done / el, "unit": "heads/s", "cores": int(threads), "kind": "oracle",
+            "sample": "%d of %d units (whole units, float64 numpy oracle), %.1f s"
+                      % (done, cfg.units, el)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(units shard across GPUs with no communication; see the design notes)",
+              file=sys.stderr)
+        sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration()
+        return
+
+    import numpy as np
+    import torch
+
+    import paper_2605_31105_amd as G
+    import workloads as W
+
+    cfg = W.config(args.config)
+    if args.budget:
+        cfg = W.config(args.config, budget=args.budget)
+    U, Gq, w, d, n, c = cfg.units, cfg.group, cfg.window, cfg.head_dim, cfg.n, cfg.budget
+    m = Gq * w
+    print("bench: generating %s (%d units, n=%d)" % (cfg.name, U, n), file=sys.stderr, flush=True)
+    t_gen = time.perf_counter()
+    q, K, V = W.make_batch(cfg)
+    print("bench: generated in %.1f s" % (time.perf_counter() - t_gen), file=sys.stderr, flush=True)
+
+    def dev(a):
+        if cfg.dtype == "bf16":
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
+        return torch.from_numpy(a).cuda()
+
+    qd, Kd, Vd = dev(q), dev(K), dev(V)
+    torch.cuda.synchronize()
+    res = G.compress(qd, Kd, Vd, w, c, cfg.pool_kernel, cfg.lam)   # allocates outputs once
+    ws, out = res.workspace, res
+    for _ in range(args.warmup):
+        G.compress(qd, Kd, Vd, w, c, cfg.pool_kernel, cfg.lam, workspace=ws, out=out)
+    torch.cuda.synchronize()
+    print("bench: warmup done", file=sys.stderr, flush=True)
+
+    hip = Hip()
+    timed = {"full_prob": G.STAGES.index("full_prob"), "full_lse": G.STAGES.index("full_lse")}
+    slots = []
+    for _ in range(args.steps):
+        arr = (ctypes.c_void_p * (2 * G.NUM_STAGES))()
+        evs = {}
+        for name, s in timed.items():
+            a, b = hip.event(), hip.event()
+            arr[2 * s], arr[2 * s + 1] = a.value, b.value
+            evs[name] = (a, b)
+        slots.append((arr, evs))
+    stream = torch.cuda.current_stream()
+    e0, e1 = hip.event(), hip.event()
+
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    hip.lib.hipEventRecord(e0, ctypes.c_void_p(stream.cuda_stream))
+    for k in range(args.steps):
+        G.compress(qd, Kd, Vd, w, c, cfg.pool_kernel, cfg.lam, workspace=ws, out=out,
+                   stage_events=slots[k][0])
+    hip.lib.hipEventRecord(e1, ctypes.c_void_p(stream.cuda_stream))
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+
+    ms_wall = (t1 - t0) * 1e3 / args.steps
+    ms_events = hip.elapsed_ms(e0, e1) / args.steps
+    stage_ms = {name: float(np.mean([hip.elapsed_ms(*ev[name]) for _, ev in slots]))
+                for name in timed}
+    ms_step = ms_wall
+    heads_s = U / (ms_step / 1e3)
+
+    # algorithmic bytes (read once / written once), per unit
+    esz = 2 if cfg.dtype == "bf16" else 4
+    kv_bytes = 2 * n * d * esz
+    q_bytes = m * d * esz
+    path_bytes = kv_bytes + q_bytes + c * 4 + c * d * esz + c * d * 4
+    alg = {"full_prob": U * (kv_bytes + q_bytes), "full_lse": U * (n * d * esz + q_bytes)}
+    dom = max(stage_ms, key=stage_ms.get)
+    achieved = alg[dom] / (stage_ms[dom] / 1e3) / 1e9
+
+    traffic = None
+    tfile = os.path.join(ROOT, "profiles", "traffic_full_prob_llama3-8b-32layer-n32k.json")
+    if os.path.exists(tfile) and dom == "full_prob" and args.config == 4:
+        t = json.load(open(tfile))
+        if t.get("source_hash") == source_hash(t.get("sources", [])):
+            traffic = t.get("bytes_per_launch")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        print("bench: timing the oracle on the host", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(cfg, q, K, V, args.cpu_seconds)
+
+    line = {
+        "metric": METRIC,
+        "value": heads_s,
+        "unit": "heads/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "ms_per_layer": ms_step / cfg.layers,
+        "ms_per_step_events": ms_events,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "layers": cfg.layers, "kv_heads": cfg.kv_heads,
+                   "query_heads": cfg.kv_heads * Gq, "head_dim": d, "n": n, "window": w,
+                   "budget": c, "pool_kernel": cfg.pool_kernel, "lambda": cfg.lam,
+                   "units": U},
+        "path_hbm_frac": (U * path_bytes / (ms_step / 1e3) / 1e9) / HBM_PEAK_GBS,
+        "stage_ms": stage_ms,
+        "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": traffic},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

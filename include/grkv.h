@@ -97,7 +97,30 @@ typedef struct {
   float* stats;
   void* workspace;
   size_t workspace_bytes;
+  /* Optional timing hooks, may be NULL: an array of 2 * GRKV_NUM_STAGES
+   * hipEvent_t owned by the caller.  For every stage s whose two slots are both
+   * non-null, slot 2s is recorded on `stream` before the stage's kernels and
+   * slot 2s+1 after them, so hipEventElapsedTime gives the stage's duration. */
+  void** stage_events;
 } grkv_outputs;
+
+/* Stages of one call, in launch order (indices into stage_events / 2). */
+enum {
+  GRKV_STAGE_FULL_LSE = 0,     /* full-cache pass A: row max / sum-exp per split */
+  GRKV_STAGE_FULL_LSE_COMBINE, /* -> log-sum-exp of every window row */
+  GRKV_STAGE_FULL_PROB,        /* full-cache pass B: P.V partials, SnapKV column sums */
+  GRKV_STAGE_FULL_Y,           /* -> Y */
+  GRKV_STAGE_SELECT,           /* pooling, top-k, fixed set */
+  GRKV_STAGE_GATHER,           /* K0 -> k_out, V0 -> v_out */
+  GRKV_STAGE_RET_LSE,          /* retained-cache pass A */
+  GRKV_STAGE_RET_LSE_COMBINE,
+  GRKV_STAGE_RET_PROB,         /* retained-cache pass B: X and X V0 partials */
+  GRKV_STAGE_RESID,            /* R = Y - X V0 */
+  GRKV_STAGE_GRAM,             /* N partials */
+  GRKV_STAGE_SOLVE,            /* Cholesky, Z, stats */
+  GRKV_STAGE_UPDATE,           /* V* = V0 + X_G^T Z */
+  GRKV_NUM_STAGES
+};
 
 /* Compress U units.
  *   q_obs  dtype [U][G][w][d]  the window queries (post-RoPE), query head

@@ -21,6 +21,9 @@ __all__ = [
 
 GRKV_OK, GRKV_ERR_INVALID, GRKV_ERR_WORKSPACE, GRKV_ERR_UNSUPPORTED, GRKV_ERR_HIP = 0, -1, -2, -3, -4
 GRKV_BF16, GRKV_F32 = 0, 1
+STAGES = ("full_lse", "full_lse_combine", "full_prob", "full_y", "select", "gather",
+          "ret_lse", "ret_lse_combine", "ret_prob", "resid", "gram", "solve", "update")
+NUM_STAGES = len(STAGES)
 EXPORTED_SYMBOLS = ("grkv_compress", "grkv_workspace_bytes", "grkv_workspace_layout",
                     "grkv_default_options", "grkv_status_string")
 
@@ -50,7 +53,8 @@ class Options(ctypes.Structure):
 class Outputs(ctypes.Structure):
     _fields_ = [("idx", ctypes.c_void_p), ("k_out", ctypes.c_void_p),
                 ("v_out", ctypes.c_void_p), ("stats", ctypes.c_void_p),
-                ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t)]
+                ("workspace", ctypes.c_void_p), ("workspace_bytes", ctypes.c_size_t),
+                ("stage_events", ctypes.POINTER(ctypes.c_void_p))]
 
 
 class Layout(ctypes.Structure):
@@ -121,14 +125,16 @@ class Result:
 
 def compress(q_obs, K, V, window: int, budget: int, pool_kernel: int, lam: float, *,
              n_sink: int = 4, beta: float = 0.10, fix_window: bool = True,
-             causal_window: bool = True, stream=None, workspace=None, out=None) -> Result:
+             causal_window: bool = True, stream=None, workspace=None, out=None,
+             stage_events=None) -> Result:
     """GRKV compression of U units on the GPU.
 
     q_obs [U, G, w, d], K and V [U, n, d]: contiguous CUDA tensors of one dtype
     (bfloat16 or float32).  Returns the retained indices, K0, the merged V*,
     per-unit stats {||Y||^2, D_before, D_after, status} and the workspace.
     ``workspace`` (uint8, >= workspace_bytes) and ``out`` (a Result whose
-    tensors are reused) avoid allocations in timed loops.
+    tensors are reused) avoid allocations in timed loops.  ``stage_events`` is
+    an optional ctypes array of 2 * NUM_STAGES event handles (see grkv.h).
     """
     import torch
 
@@ -162,7 +168,8 @@ def compress(q_obs, K, V, window: int, budget: int, pool_kernel: int, lam: float
     prob = Problem(U, G, d, dt)
     opt = Options(n_sink, beta, 1 if fix_window else 0, 1 if causal_window else 0)
     outs = Outputs(out.idx.data_ptr(), out.k_out.data_ptr(), out.v_out.data_ptr(),
-                   out.stats.data_ptr(), workspace.data_ptr(), workspace.numel())
+                   out.stats.data_ptr(), workspace.data_ptr(), workspace.numel(),
+                   stage_events)
     if stream is None:
         stream = torch.cuda.current_stream(dev)
     handle = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)

@@ -163,6 +163,12 @@ int grkv_compress(const void* q_obs, const void* K, const void* V, int64_t n, in
   auto Dd = [&](size_t o) { return (double*)(ws + o); };
 
 #define GRKV_TRY(x) do { if ((x) != hipSuccess) return GRKV_ERR_HIP; } while (0)
+  void** ev = out->stage_events;
+  auto mark = [&](int stage, int end) -> hipError_t {
+    if (!ev || !ev[2 * stage] || !ev[2 * stage + 1]) return hipSuccess;
+    return hipEventRecord((hipEvent_t)ev[2 * stage + end], s);
+  };
+#define GRKV_STAGE(id, call) do { GRKV_TRY(mark(id, 0)); GRKV_TRY(call); GRKV_TRY(mark(id, 1)); } while (0)
   // 1. window attention over the full cache: LSE, then Y and the SnapKV scores
   AttnPass full = {};
   full.q = q_obs; full.k = K; full.v = V; full.kpos = nullptr; full.nk = (int)n;
@@ -171,14 +177,16 @@ int grkv_compress(const void* q_obs, const void* K, const void* V, int64_t n, in
   full.lse = Dd(p.lse1); full.lse_log2 = F(p.lse1_log2);
   full.ypart = F(p.ypart); full.colsum = p.prefix > 0 ? F(p.colsum) : nullptr;
   full.prefix = p.prefix; full.xout = nullptr; full.split_p = true;
-  GRKV_TRY(launch_lse_pass(p, full, s));
-  GRKV_TRY(launch_lse_combine(p, full.pmax, full.psum, p.S1, Dd(p.lse1), F(p.lse1_log2), s));
-  GRKV_TRY(launch_prob_pass(p, full, s));
-  GRKV_TRY(launch_combine_rows(p, F(p.ypart), p.S1, nullptr, F(p.y), s));
+  GRKV_STAGE(GRKV_STAGE_FULL_LSE, launch_lse_pass(p, full, s));
+  GRKV_STAGE(GRKV_STAGE_FULL_LSE_COMBINE,
+             launch_lse_combine(p, full.pmax, full.psum, p.S1, Dd(p.lse1), F(p.lse1_log2), s));
+  GRKV_STAGE(GRKV_STAGE_FULL_PROB, launch_prob_pass(p, full, s));
+  GRKV_STAGE(GRKV_STAGE_FULL_Y, launch_combine_rows(p, F(p.ypart), p.S1, nullptr, F(p.y), s));
   // 2. pooled top-k retention and the fixed set; gather K0, V0
   uint8_t* fixed = (uint8_t*)(ws + p.fixed);
-  GRKV_TRY(launch_select(p, F(p.colsum), F(p.pooled), out->idx, fixed, s));
-  GRKV_TRY(launch_gather(p, K, V, out->idx, out->k_out, ws + p.v0c, out->v_out, s));
+  GRKV_STAGE(GRKV_STAGE_SELECT, launch_select(p, F(p.colsum), F(p.pooled), out->idx, fixed, s));
+  GRKV_STAGE(GRKV_STAGE_GATHER,
+             launch_gather(p, K, V, out->idx, out->k_out, ws + p.v0c, out->v_out, s));
   // 3. window attention over the retained cache: X and X V0, then R = Y - X V0
   AttnPass ret = {};
   ret.q = q_obs; ret.k = out->k_out; ret.v = ws + p.v0c; ret.kpos = out->idx; ret.nk = p.c;
@@ -187,15 +195,18 @@ int grkv_compress(const void* q_obs, const void* K, const void* V, int64_t n, in
   ret.lse = Dd(p.lse2); ret.lse_log2 = F(p.lse2_log2);
   ret.ypart = F(p.xvpart); ret.colsum = nullptr; ret.prefix = 0; ret.xout = F(p.x);
   ret.split_p = true;
-  GRKV_TRY(launch_lse_pass(p, ret, s));
-  GRKV_TRY(launch_lse_combine(p, ret.pmax, ret.psum, p.S2, Dd(p.lse2), F(p.lse2_log2), s));
-  GRKV_TRY(launch_prob_pass(p, ret, s));
-  GRKV_TRY(launch_combine_rows(p, F(p.xvpart), p.S2, F(p.y), F(p.resid), s));
+  GRKV_STAGE(GRKV_STAGE_RET_LSE, launch_lse_pass(p, ret, s));
+  GRKV_STAGE(GRKV_STAGE_RET_LSE_COMBINE,
+             launch_lse_combine(p, ret.pmax, ret.psum, p.S2, Dd(p.lse2), F(p.lse2_log2), s));
+  GRKV_STAGE(GRKV_STAGE_RET_PROB, launch_prob_pass(p, ret, s));
+  GRKV_STAGE(GRKV_STAGE_RESID, launch_combine_rows(p, F(p.xvpart), p.S2, F(p.y), F(p.resid), s));
   // 4. value step: N, Cholesky solve for Z, V* = V0 + X_G^T Z
-  GRKV_TRY(launch_gram(p, F(p.x), fixed, F(p.npart), s));
-  GRKV_TRY(launch_cholesky_solve(p, F(p.npart), F(p.y), F(p.resid), F(p.gram), F(p.z),
-                                 F(p.stats_ws), out->stats, s));
-  GRKV_TRY(launch_update(p, F(p.x), fixed, F(p.z), F(p.stats_ws), out->v_out, s));
+  GRKV_STAGE(GRKV_STAGE_GRAM, launch_gram(p, F(p.x), fixed, F(p.npart), s));
+  GRKV_STAGE(GRKV_STAGE_SOLVE, launch_cholesky_solve(p, F(p.npart), F(p.y), F(p.resid), F(p.gram),
+                                                     F(p.z), F(p.stats_ws), out->stats, s));
+  GRKV_STAGE(GRKV_STAGE_UPDATE,
+             launch_update(p, F(p.x), fixed, F(p.z), F(p.stats_ws), out->v_out, s));
+#undef GRKV_STAGE
 #undef GRKV_TRY
   return GRKV_OK;
 }
