@@ -150,7 +150,7 @@ size_t grkv_workspace_bytes(const grkv_problem* prob, int64_t n,
                             int32_t window, int32_t budget);
 
 /* Byte offsets, inside the workspace, of intermediates that remain readable
- * after grkv_compress returns (mp = m rounded up to a multiple of 32; rows
+ * after grkv_compress returns (mp = m rounded up to 32, 64, 128 or 256; rows
  * m..mp-1 are padding; P = n - w):
  *   lse      double [U][mp]     natural log-sum-exp of each window row over the
  *                               full cache (window attention normaliser)

@@ -187,7 +187,9 @@ def intermediates(res: Result) -> dict:
     U, G, d, dt, n, w, c = res.shape
     lay = workspace_layout(U, G, d, dt, n, w, c)
     m = G * w
-    mp = (m + 31) // 32 * 32
+    mp = 32
+    while mp < m:
+        mp *= 2
     P = n - w
     ws = res.workspace
 

@@ -47,8 +47,11 @@ int make_plan(const grkv_problem* prob, int64_t n, int32_t window, int32_t budge
   p->G = prob->group;
   p->w = window;
   p->m = (int)m;
-  p->mp = (int)ceil_div(m, kRowsPerWave) * kRowsPerWave;
-  p->waves = p->mp / kRowsPerWave;
+  // one wave per 32 rows, a power of two of them (1, 2, 4 or 8)
+  int waves = 1;
+  while (waves * kRowsPerWave < m) waves *= 2;
+  p->waves = waves;
+  p->mp = waves * kRowsPerWave;
   p->d = prob->head_dim;
   p->dtype = prob->dtype;
   p->n = n;
@@ -91,6 +94,8 @@ int make_plan(const grkv_problem* prob, int64_t n, int32_t window, int32_t budge
   p->npart = take(U * p->S3 * mp * mp * sizeof(float));
   p->gram = take(U * mp * mp * sizeof(float));
   p->z = take(U * d * mp * sizeof(float));
+  p->zhi = take(U * d * mp * 2);
+  p->zlo = take(U * d * mp * 2);
   p->stats_ws = take(U * 4 * sizeof(float));
   p->total = off;
   return GRKV_OK;
@@ -177,16 +182,20 @@ int grkv_compress(const void* q_obs, const void* K, const void* V, int64_t n, in
   full.lse = Dd(p.lse1); full.lse_log2 = F(p.lse1_log2);
   full.ypart = F(p.ypart); full.colsum = p.prefix > 0 ? F(p.colsum) : nullptr;
   full.prefix = p.prefix; full.xout = nullptr; full.split_p = true;
-  GRKV_STAGE(GRKV_STAGE_FULL_LSE, launch_lse_pass(p, full, s));
+  const bool fast = stream_supported(p);
+  auto pass_a = [&](const AttnPass& a) { return fast ? launch_stream(p, a, false, s) : launch_lse_pass(p, a, s); };
+  auto pass_b = [&](const AttnPass& a) { return fast ? launch_stream(p, a, true, s) : launch_prob_pass(p, a, s); };
+  GRKV_STAGE(GRKV_STAGE_FULL_LSE, pass_a(full));
   GRKV_STAGE(GRKV_STAGE_FULL_LSE_COMBINE,
              launch_lse_combine(p, full.pmax, full.psum, p.S1, Dd(p.lse1), F(p.lse1_log2), s));
-  GRKV_STAGE(GRKV_STAGE_FULL_PROB, launch_prob_pass(p, full, s));
+  GRKV_STAGE(GRKV_STAGE_FULL_PROB, pass_b(full));
   GRKV_STAGE(GRKV_STAGE_FULL_Y, launch_combine_rows(p, F(p.ypart), p.S1, nullptr, F(p.y), s));
   // 2. pooled top-k retention and the fixed set; gather K0, V0
   uint8_t* fixed = (uint8_t*)(ws + p.fixed);
   GRKV_STAGE(GRKV_STAGE_SELECT, launch_select(p, F(p.colsum), F(p.pooled), out->idx, fixed, s));
-  GRKV_STAGE(GRKV_STAGE_GATHER,
-             launch_gather(p, K, V, out->idx, out->k_out, ws + p.v0c, out->v_out, s));
+  const bool fast_merge = merge_fast_supported(p);
+  GRKV_STAGE(GRKV_STAGE_GATHER, launch_gather(p, K, V, out->idx, out->k_out, ws + p.v0c,
+                                              fast_merge ? nullptr : out->v_out, s));
   // 3. window attention over the retained cache: X and X V0, then R = Y - X V0
   AttnPass ret = {};
   ret.q = q_obs; ret.k = out->k_out; ret.v = ws + p.v0c; ret.kpos = out->idx; ret.nk = p.c;
@@ -195,17 +204,29 @@ int grkv_compress(const void* q_obs, const void* K, const void* V, int64_t n, in
   ret.lse = Dd(p.lse2); ret.lse_log2 = F(p.lse2_log2);
   ret.ypart = F(p.xvpart); ret.colsum = nullptr; ret.prefix = 0; ret.xout = F(p.x);
   ret.split_p = true;
-  GRKV_STAGE(GRKV_STAGE_RET_LSE, launch_lse_pass(p, ret, s));
+  GRKV_STAGE(GRKV_STAGE_RET_LSE, pass_a(ret));
   GRKV_STAGE(GRKV_STAGE_RET_LSE_COMBINE,
              launch_lse_combine(p, ret.pmax, ret.psum, p.S2, Dd(p.lse2), F(p.lse2_log2), s));
-  GRKV_STAGE(GRKV_STAGE_RET_PROB, launch_prob_pass(p, ret, s));
+  GRKV_STAGE(GRKV_STAGE_RET_PROB, pass_b(ret));
   GRKV_STAGE(GRKV_STAGE_RESID, launch_combine_rows(p, F(p.xvpart), p.S2, F(p.y), F(p.resid), s));
   // 4. value step: N, Cholesky solve for Z, V* = V0 + X_G^T Z
   GRKV_STAGE(GRKV_STAGE_GRAM, launch_gram(p, F(p.x), fixed, F(p.npart), s));
-  GRKV_STAGE(GRKV_STAGE_SOLVE, launch_cholesky_solve(p, F(p.npart), F(p.y), F(p.resid), F(p.gram),
-                                                     F(p.z), F(p.stats_ws), out->stats, s));
-  GRKV_STAGE(GRKV_STAGE_UPDATE,
-             launch_update(p, F(p.x), fixed, F(p.z), F(p.stats_ws), out->v_out, s));
+  if (fast_merge) {
+    GRKV_STAGE(GRKV_STAGE_SOLVE,
+               launch_solve(p, F(p.npart), F(p.y), F(p.resid), F(p.gram), F(p.z),
+                            (uint16_t*)(ws + p.zhi), (uint16_t*)(ws + p.zlo), F(p.stats_ws),
+                            out->stats, s));
+    GRKV_STAGE(GRKV_STAGE_UPDATE,
+               launch_update(p, F(p.x), fixed, (const uint16_t*)(ws + p.zhi),
+                             (const uint16_t*)(ws + p.zlo), F(p.stats_ws),
+                             (const uint16_t*)(ws + p.v0c), out->v_out, s));
+  } else {
+    GRKV_STAGE(GRKV_STAGE_SOLVE, launch_cholesky_solve(p, F(p.npart), F(p.y), F(p.resid),
+                                                       F(p.gram), F(p.z), F(p.stats_ws),
+                                                       out->stats, s));
+    GRKV_STAGE(GRKV_STAGE_UPDATE,
+               launch_update_add(p, F(p.x), fixed, F(p.z), F(p.stats_ws), out->v_out, s));
+  }
 #undef GRKV_STAGE
 #undef GRKV_TRY
   return GRKV_OK;

@@ -54,6 +54,17 @@ __device__ __forceinline__ float sum16(float v) {
   return v;
 }
 
+// The same 16-lane sum on the VALU through DPP (no LDS traffic): swap within
+// pairs, within quads, mirror within half-rows, mirror within the row; every
+// lane of the 16-lane row ends with the row total.
+__device__ __forceinline__ float sum16_dpp(float v) {
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xF, 0xF, false));
+  v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x140, 0xF, 0xF, false));
+  return v;
+}
+
 // Reductions over the 4 lanes that share l%16 (lanes differing in bits 4..5).
 __device__ __forceinline__ float max_over_groups(float v) {
   v = fmaxf(v, __shfl_xor(v, 16));

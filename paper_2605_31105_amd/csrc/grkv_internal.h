@@ -30,7 +30,7 @@ struct Plan {
   int S3, chunk3;
   // workspace offsets (bytes)
   size_t pmax1, psum1, lse1, lse1_log2, ypart, y, colsum, pooled, fixed, v0c;
-  size_t pmax2, psum2, lse2, lse2_log2, xvpart, x, resid, npart, gram, z, stats_ws;
+  size_t pmax2, psum2, lse2, lse2_log2, xvpart, x, resid, npart, gram, z, zhi, zlo, stats_ws;
   size_t total;
 };
 
@@ -67,20 +67,40 @@ hipError_t launch_prob_pass(const Plan& p, const AttnPass& a, hipStream_t s);
 hipError_t launch_combine_rows(const Plan& p, const float* part, int S,
                                const float* base, float* out, hipStream_t s);
 
+// bf16 streaming passes (direct-to-LDS ring); used when stream_supported().
+bool stream_supported(const Plan& p);
+hipError_t launch_stream(const Plan& p, const AttnPass& a, bool pass_b, hipStream_t s);
+
 hipError_t launch_select(const Plan& p, const float* colsum, float* pooled,
                          int32_t* idx, uint8_t* fixed, hipStream_t s);
+// K0 -> k_out, V0 -> v0c (input dtype); V0 as fp32 -> v_out when v_out is not null.
 hipError_t launch_gather(const Plan& p, const void* K, const void* V,
                          const int32_t* idx, void* k_out, void* v0c,
                          float* v_out, hipStream_t s);
 hipError_t launch_gram(const Plan& p, const float* x, const uint8_t* fixed,
                        float* npart, hipStream_t s);
+
+// Fast value step (bf16, mp <= 128): elimination solve, then
+// v_out = V0 + X_G^T Z written in one pass from the compact V0 copy.
+bool merge_fast_supported(const Plan& p);
+hipError_t launch_solve(const Plan& p, const float* npart, const float* y,
+                        const float* resid, float* gram, float* z, uint16_t* zhi,
+                        uint16_t* zlo, float* stats_ws, float* stats_user,
+                        hipStream_t s);
+hipError_t launch_update(const Plan& p, const float* x, const uint8_t* fixed,
+                         const uint16_t* zhi, const uint16_t* zlo,
+                         const float* stats_ws, const uint16_t* v0c, float* v_out,
+                         hipStream_t s);
+
+// Generic value step (any dtype, mp up to 256): Cholesky in LDS; the update
+// adds X_G^T Z into v_out, which the gather filled with V0.
 // Writes the per-unit stats to stats_ws (always) and stats_user (if not null).
 hipError_t launch_cholesky_solve(const Plan& p, const float* npart,
                                  const float* y, const float* resid,
                                  float* gram, float* z, float* stats_ws,
                                  float* stats_user, hipStream_t s);
-hipError_t launch_update(const Plan& p, const float* x, const uint8_t* fixed,
-                         const float* z, const float* stats_ws, float* v_out,
-                         hipStream_t s);
+hipError_t launch_update_add(const Plan& p, const float* x, const uint8_t* fixed,
+                             const float* z, const float* stats_ws, float* v_out,
+                             hipStream_t s);
 
 }  // namespace grkv

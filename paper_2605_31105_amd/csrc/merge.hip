@@ -1,7 +1,7 @@
 // Value step of the ridge merge in its Woodbury dual form (Eq. 8; Algorithm 1,
 // value step; App. D.1, fixed tokens App. D.3):
 //   N = X_G X_G^T + lambda I_m   (gram: partial sums over column splits)
-//   Z = N^-1 R                   (cholesky_solve: Cholesky of N in LDS)
+//   Z = N^-1 R                   (solve: elimination in registers and LDS)
 //   V*_G = V0_G + X_G^T Z        (update: fixed columns keep V0)
 // X_G is X with the fixed columns zeroed.  The fp32 operands of the two
 // products go through the bf16 MFMA as hi+lo pairs (three products per tile),
@@ -12,28 +12,28 @@
 namespace grkv {
 namespace {
 
-// Loads 8 consecutive X_G entries of row `row` starting at column t (columns
-// past `t_end` and fixed columns read as zero).
-__device__ __forceinline__ void load_xg8(const float* xrow, const uint8_t* fixedu, int t, int t_end,
-                                         float* out) {
-#pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    int tt = t + e;
-    out[e] = (tt < t_end && !fixedu[tt]) ? xrow[tt] : 0.f;
-  }
-}
-
+// ------------------------------------------------------------------ gram ----
+// One block per (unit, column split).  Each 32-column slab of X_G (all mp rows)
+// is loaded with 16-byte loads, masked, split into bf16 hi/lo and staged in LDS
+// as [mp][32] (+8 pad) rows; every wave then forms its 32 rows of N against
+// all mp rows.  The next slab's loads are in flight during the MFMAs.
 template <int WAVES>
 __global__ __launch_bounds__(WAVES * 64) void gram_kernel(const float* x, const uint8_t* fixed,
-                                                          float* npart, int c, int mp, int S3,
-                                                          int chunk3) {
-  constexpr int NT = 2 * WAVES;  // 16-wide column tiles of N
-  const int s = blockIdx.x, u = blockIdx.y;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int l16 = lane & 15, g = lane >> 4;
+                                                          float* npart, int c, int S3, int chunk3) {
+  constexpr int MP = WAVES * 32;
+  constexpr int NT = MP / 16;              // 16-row tiles of N
+  constexpr int RS = 40;                   // LDS row stride in bf16 (32 + 8 pad)
+  constexpr int NTH = WAVES * 64;
+  constexpr int F4 = MP * 32 / 4 / NTH;    // float4 loads per thread per slab
+  __shared__ __attribute__((aligned(16))) u16 hi[MP * RS];
+  __shared__ __attribute__((aligned(16))) u16 lo[MP * RS];
+
+  const int s = blockIdx.x, u = blockIdx.y, tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6, l16 = lane & 15, g = lane >> 4;
   const int t0 = s * chunk3, t1 = min(t0 + chunk3, c);
-  const float* xu = x + (size_t)u * mp * c;
+  const float* xu = x + (size_t)u * MP * c;
   const uint8_t* fu = fixed + (size_t)u * c;
+  const bool vec = (c & 3) == 0;
 
   f32x4 acc[2][NT];
 #pragma unroll
@@ -41,130 +41,213 @@ __global__ __launch_bounds__(WAVES * 64) void gram_kernel(const float* x, const 
 #pragma unroll
     for (int bt = 0; bt < NT; ++bt) acc[rt][bt] = zero4();
 
+  float4 rg[F4];
+  auto load = [&](int tk) {
+#pragma unroll
+    for (int i = 0; i < F4; ++i) {
+      const int e = (tid + i * NTH) * 4;       // element in the [MP][32] slab
+      const int r = e / 32, cc = e % 32, t = tk + cc;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      const float* src = xu + (size_t)r * c + t;
+      if (vec && t + 3 < t1) {
+        v = *reinterpret_cast<const float4*>(src);
+      } else {
+        float tmp[4] = {0.f, 0.f, 0.f, 0.f};
+        for (int q = 0; q < 4; ++q)
+          if (t + q < t1) tmp[q] = src[q];
+        v = make_float4(tmp[0], tmp[1], tmp[2], tmp[3]);
+      }
+      rg[i] = v;
+    }
+  };
+  if (t0 < t1) load(t0);
   for (int tk = t0; tk < t1; tk += 32) {
-    bf16x8 ahi[2], alo[2];
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < F4; ++i) {
+      const int e = (tid + i * NTH) * 4;
+      const int r = e / 32, cc = e % 32, t = tk + cc;
+      float v[4] = {rg[i].x, rg[i].y, rg[i].z, rg[i].w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float xv = (t + q < t1 && !fu[t + q]) ? v[q] : 0.f;
+        const __bf16 h = (__bf16)xv;
+        const __bf16 l = (__bf16)(xv - (float)h);
+        hi[r * RS + cc + q] = __builtin_bit_cast(u16, h);
+        lo[r * RS + cc + q] = __builtin_bit_cast(u16, l);
+      }
+    }
+    __syncthreads();
+    if (tk + 32 < t1) load(tk + 32);
+    bf16x8 ah[2], al[2];
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) {
-      float v[8];
-      load_xg8(xu + (size_t)(wave * kRowsPerWave + rt * 16 + l16) * c, fu, tk + 8 * g, t1, v);
-      split8(v, ahi[rt], alo[rt]);
+      const int r = wave * 32 + rt * 16 + l16;
+      ah[rt] = as_bf16x8(*reinterpret_cast<const uint4*>(&hi[r * RS + 8 * g]));
+      al[rt] = as_bf16x8(*reinterpret_cast<const uint4*>(&lo[r * RS + 8 * g]));
     }
 #pragma unroll
     for (int bt = 0; bt < NT; ++bt) {
-      float v[8];
-      bf16x8 bhi, blo;
-      load_xg8(xu + (size_t)(bt * 16 + l16) * c, fu, tk + 8 * g, t1, v);
-      split8(v, bhi, blo);
+      const int r = bt * 16 + l16;
+      const bf16x8 bh = as_bf16x8(*reinterpret_cast<const uint4*>(&hi[r * RS + 8 * g]));
+      const bf16x8 bl = as_bf16x8(*reinterpret_cast<const uint4*>(&lo[r * RS + 8 * g]));
 #pragma unroll
       for (int rt = 0; rt < 2; ++rt) {
-        acc[rt][bt] = mfma_bf16(ahi[rt], bhi, acc[rt][bt]);
-        acc[rt][bt] = mfma_bf16(ahi[rt], blo, acc[rt][bt]);
-        acc[rt][bt] = mfma_bf16(alo[rt], bhi, acc[rt][bt]);
+        acc[rt][bt] = mfma_bf16(ah[rt], bh, acc[rt][bt]);
+        acc[rt][bt] = mfma_bf16(ah[rt], bl, acc[rt][bt]);
+        acc[rt][bt] = mfma_bf16(al[rt], bh, acc[rt][bt]);
       }
     }
   }
-  float* out = npart + ((size_t)u * S3 + s) * mp * mp;
+  float* out = npart + ((size_t)u * S3 + s) * MP * MP;
 #pragma unroll
   for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
     for (int bt = 0; bt < NT; ++bt)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        int row = wave * kRowsPerWave + rt * 16 + 4 * g + i;
-        out[(size_t)row * mp + bt * 16 + l16] = acc[rt][bt][i];
+        const int row = wave * 32 + rt * 16 + 4 * g + i;
+        out[(size_t)row * MP + bt * 16 + l16] = acc[rt][bt][i];
       }
 }
 
-__device__ __forceinline__ int tri(int i, int j) { return i * (i + 1) / 2 + j; }
-
-// One block per unit.  L (packed lower triangle) lives in LDS; the right-hand
-// sides W are in LDS when they fit (w_in_lds) and otherwise in the z buffer.
-__global__ __launch_bounds__(256) void chol_kernel(const float* npart, int S3, const float* y,
-                                                  const float* resid, float* gram, float* z,
-                                                  float* stats_ws, float* stats_user, int m,
-                                                  int mp, int D, float lam, int w_in_lds) {
-  extern __shared__ __attribute__((aligned(16))) float lds[];
+// ----------------------------------------------------------------- solve ----
+// One block per unit solves N Z = R for the d right-hand sides by Gaussian
+// elimination without pivoting (N is symmetric positive definite for
+// lambda > 0) followed by back substitution, in fp32.
+// Thread (rb, j) holds rows 32rb..32rb+31 of column j of the augmented matrix
+// [N | R] in registers (j < MP: N, j >= MP: right-hand side j - MP).  The
+// elimination step for pivot k publishes row k in LDS; since the trailing
+// block stays symmetric, the multipliers of the rows below k are that row's
+// own entries, A[i][k] = A[k][i].  The finished rows of U are kept in LDS,
+// transposed, for the back substitution.
+template <int MP, int D>
+__global__ __launch_bounds__(MP / 32 * 256) void solve_kernel(
+    const float* npart, int S3, const float* y, const float* resid, float* gram, float* z,
+    u16* zhi, u16* zlo, float* stats_ws, float* stats_user, int m, float lam) {
+  constexpr int RB = MP / 32;
+  constexpr int NC = MP + D;              // augmented columns (<= 256)
+  constexpr int US = MP + 4;              // Ucol row stride
+  __shared__ __attribute__((aligned(16))) float rowk[2][256];
+  __shared__ __attribute__((aligned(16))) float ucol[MP * US];   // ucol[k][i] = U[i][k]
+  __shared__ float zk[2][256];
   __shared__ int fail;
-  __shared__ double red[3][4];
+  __shared__ double red[3][RB * 4];
+
   const int u = blockIdx.x, tid = threadIdx.x;
-  float* L = lds;
-  const int ntri = mp * (mp + 1) / 2;
-  float* zu = z + (size_t)u * D * mp;  // Z^T [D][mp]
-  float* Wl = lds + ((ntri + 3) & ~3);
-  // W(i, col): LDS [mp][D] or global [D][mp]
-  float* Wb = w_in_lds ? Wl : zu;
-  const int si = w_in_lds ? D : 1, sc = w_in_lds ? 1 : mp;
+  const int rb = tid >> 8, j = tid & 255;
+  const bool active = j < NC;
+  const bool rhs = j >= MP && active;
+  const int r0 = rb * 32;
+  float a[32];
 
   if (tid == 0) fail = 0;
-  const float* np = npart + (size_t)u * S3 * mp * mp;
-  float* gu = gram + (size_t)u * mp * mp;
-  for (int e = tid; e < mp * mp; e += blockDim.x) {
-    int i = e / mp, j = e % mp;
-    float v = 0.f;
-    for (int s = 0; s < S3; ++s) v += np[(size_t)s * mp * mp + e];
-    if (i == j) v += (i < m) ? lam : 1.f;
-    gu[e] = v;
-    if (j <= i) L[tri(i, j)] = v;
+  // load: column j < MP is row j of the symmetric N; j >= MP is column j-MP of R
+  const float* np = npart + (size_t)u * S3 * MP * MP;
+  const float* ru = resid + (size_t)u * MP * D;
+  if (j < MP) {
+#pragma unroll
+    for (int ii = 0; ii < 32; ++ii) a[ii] = 0.f;
+    for (int s = 0; s < S3; ++s) {
+      const float4* src = reinterpret_cast<const float4*>(np + (size_t)s * MP * MP + (size_t)j * MP + r0);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        float4 v = src[q];
+        a[4 * q] += v.x; a[4 * q + 1] += v.y; a[4 * q + 2] += v.z; a[4 * q + 3] += v.w;
+      }
+    }
+#pragma unroll
+    for (int ii = 0; ii < 32; ++ii)
+      if (r0 + ii == j) a[ii] += (j < m) ? lam : 1.f;
+    float* gu = gram + (size_t)u * MP * MP + (size_t)j * MP + r0;
+#pragma unroll
+    for (int ii = 0; ii < 32; ++ii) gu[ii] = a[ii];
+  } else if (rhs) {
+#pragma unroll
+    for (int ii = 0; ii < 32; ++ii) a[ii] = ru[(size_t)(r0 + ii) * D + (j - MP)];
+  } else {
+#pragma unroll
+    for (int ii = 0; ii < 32; ++ii) a[ii] = 0.f;
   }
-  const float* ru = resid + (size_t)u * mp * D;
-  for (int e = tid; e < mp * D; e += blockDim.x) {
-    int i = e / D, col = e % D;
-    Wb[i * si + col * sc] = ru[e];
+
+  // forward elimination
+  for (int pb = 0; pb < RB; ++pb) {
+#pragma unroll
+    for (int kk = 0; kk < 32; ++kk) {
+      const int k = pb * 32 + kk;
+      float* rk = rowk[kk & 1];
+      if (rb == pb && active) {
+        rk[j] = a[kk];
+        if (j < MP) ucol[j * US + k] = a[kk];   // U[k][j], stored transposed
+      }
+      __syncthreads();
+      const float pk = rk[k];
+      if (tid == 0 && !(pk > 0.f && isfinite(pk))) fail = 1;
+      if (active && rb >= pb) {
+        const float f = rk[j] / pk;
+        if (rb > pb) {
+#pragma unroll
+          for (int ii = 0; ii < 32; ++ii) a[ii] -= rk[r0 + ii] * f;
+        } else {
+#pragma unroll
+          for (int ii = kk + 1; ii < 32; ++ii) a[ii] -= rk[r0 + ii] * f;
+        }
+      }
+    }
   }
   __syncthreads();
-
-  for (int k = 0; k < mp; ++k) {
-    if (tid == 0) {
-      float dkk = L[tri(k, k)];
-      if (!(dkk > 0.f) || !isfinite(dkk)) { fail = 1; dkk = 1.f; }
-      L[tri(k, k)] = sqrtf(dkk);
-    }
-    __syncthreads();
-    const float inv = 1.f / L[tri(k, k)];
-    for (int i = k + 1 + tid; i < mp; i += blockDim.x) L[tri(i, k)] *= inv;
-    __syncthreads();
-    const int rem = mp - k - 1;
-    for (int e = tid; e < rem * rem; e += blockDim.x) {
-      int i = k + 1 + e / rem, j = k + 1 + e % rem;
-      if (j <= i) L[tri(i, j)] -= L[tri(i, k)] * L[tri(j, k)];
-    }
-    __syncthreads();
-  }
   const bool ok = fail == 0;
 
-  // forward (L W = R) then backward (L^T Z = W), one right-hand side per thread
-  for (int col = tid; col < D; col += blockDim.x) {
-    if (!ok) {
-      for (int i = 0; i < mp; ++i) Wb[i * si + col * sc] = 0.f;
-      continue;
-    }
-    for (int i = 0; i < mp; ++i) {
-      float acc = Wb[i * si + col * sc];
-      for (int j = 0; j < i; ++j) acc -= L[tri(i, j)] * Wb[j * si + col * sc];
-      Wb[i * si + col * sc] = acc / L[tri(i, i)];
-    }
-    for (int i = mp - 1; i >= 0; --i) {
-      float acc = Wb[i * si + col * sc];
-      for (int j = i + 1; j < mp; ++j) acc -= L[tri(j, i)] * Wb[j * si + col * sc];
-      Wb[i * si + col * sc] = acc / L[tri(i, i)];
+  // back substitution: z[k] = w[k] / U[k][k], then w[i] -= U[i][k] z[k] for i < k
+  for (int pb = RB - 1; pb >= 0; --pb) {
+#pragma unroll
+    for (int kk = 31; kk >= 0; --kk) {
+      const int k = pb * 32 + kk;
+      float* zb = zk[kk & 1];
+      if (rb == pb && rhs) {
+        const float zv = a[kk] / ucol[k * US + k];
+        a[kk] = zv;
+        zb[j] = zv;
+      }
+      __syncthreads();
+      if (rhs && rb <= pb) {
+        const float zv = zb[j];
+        const float* uc = ucol + k * US + r0;
+        if (rb < pb) {
+#pragma unroll
+          for (int ii = 0; ii < 32; ++ii) a[ii] -= uc[ii] * zv;
+        } else {
+#pragma unroll
+          for (int ii = 0; ii < kk; ++ii) a[ii] -= uc[ii] * zv;
+        }
+      }
     }
   }
-  __syncthreads();
-  if (w_in_lds)
-    for (int e = tid; e < mp * D; e += blockDim.x) {
-      int col = e / mp, i = e % mp;
-      zu[e] = Wl[i * D + col];
-    }
 
-  // stats: ||Y||^2, ||R||^2, ||Z||^2 over the m real rows
-  const float* yu = y + (size_t)u * mp * D;
-  double sy = 0.0, sr = 0.0, sz = 0.0;
+  // outputs: Z^T in fp32 and as bf16 hi/lo pairs (the update's MFMA operand)
+  double sz = 0.0;
+  if (rhs) {
+    const int dd = j - MP;
+    float* zr = z + ((size_t)u * D + dd) * MP + r0;
+    u16* hr = zhi + ((size_t)u * D + dd) * MP + r0;
+    u16* lr = zlo + ((size_t)u * D + dd) * MP + r0;
+#pragma unroll
+    for (int ii = 0; ii < 32; ++ii) {
+      const float zv = ok ? a[ii] : 0.f;
+      zr[ii] = zv;
+      const __bf16 h = (__bf16)zv;
+      hr[ii] = __builtin_bit_cast(u16, h);
+      lr[ii] = __builtin_bit_cast(u16, (__bf16)(zv - (float)h));
+      if (r0 + ii < m) sz += (double)zv * zv;
+    }
+  }
+  // ||Y||^2 and ||R||^2 over the m real rows
+  const float* yu = y + (size_t)u * MP * D;
+  double sy = 0.0, sr = 0.0;
   for (int e = tid; e < m * D; e += blockDim.x) {
-    int i = e / D, col = e % D;
-    double yv = yu[e], rv = ru[e], zv = Wb[i * si + col * sc];
+    const double yv = yu[e], rv = ru[e];
     sy += yv * yv;
     sr += rv * rv;
-    sz += zv * zv;
   }
   for (int off = 32; off > 0; off >>= 1) {
     sy += __shfl_xor(sy, off);
@@ -175,11 +258,11 @@ __global__ __launch_bounds__(256) void chol_kernel(const float* npart, int S3, c
   __syncthreads();
   if (tid == 0) {
     double Y2 = 0, R2 = 0, Z2 = 0;
-    for (int k = 0; k < (int)(blockDim.x >> 6); ++k) { Y2 += red[0][k]; R2 += red[1][k]; Z2 += red[2][k]; }
-    double dn = Y2 > 0 ? Y2 : 1.0;
-    double dbefore = R2 / dn;
-    double dafter = ok ? (double)lam * lam * Z2 / dn : dbefore;
-    float st[4] = {(float)Y2, (float)dbefore, (float)dafter, ok ? 0.f : (float)GRKV_UNIT_SINGULAR};
+    for (int k = 0; k < RB * 4; ++k) { Y2 += red[0][k]; R2 += red[1][k]; Z2 += red[2][k]; }
+    const double dn = Y2 > 0 ? Y2 : 1.0;
+    const double dbefore = R2 / dn;
+    const double dafter = ok ? (double)lam * lam * Z2 / dn : dbefore;
+    const float st[4] = {(float)Y2, (float)dbefore, (float)dafter, ok ? 0.f : (float)GRKV_UNIT_SINGULAR};
     for (int k = 0; k < 4; ++k) {
       stats_ws[u * 4 + k] = st[k];
       if (stats_user) stats_user[u * 4 + k] = st[k];
@@ -187,55 +270,65 @@ __global__ __launch_bounds__(256) void chol_kernel(const float* npart, int S3, c
   }
 }
 
-// dV = X_G^T Z for 64 retained columns per block; adds into v_out (which holds V0).
+// ---------------------------------------------------------------- update ----
+// v_out = V0 + X_G^T Z for 64 retained slots per block (fixed slots and units
+// with a singular system get V0).  X_G^T is staged transposed in LDS as bf16
+// hi/lo; Z^T arrives pre-split from the solve.
+template <int MP, int D>
 __global__ __launch_bounds__(256) void update_kernel(const float* x, const uint8_t* fixed,
-                                                     const float* z, const float* stats_ws,
-                                                     float* v_out, int c, int mp, int D) {
-  extern __shared__ __attribute__((aligned(16))) float Xs[];  // [mp][68]
-  constexpr int XS = 68;
+                                                     const u16* zhi, const u16* zlo,
+                                                     const float* stats_ws, const u16* v0c,
+                                                     float* v_out, int c) {
+  constexpr int XS = MP + 8;   // LDS row stride (bf16) of X_G^T rows
+  __shared__ __attribute__((aligned(16))) u16 xh[64 * XS];
+  __shared__ __attribute__((aligned(16))) u16 xl[64 * XS];
   const int u = blockIdx.y, t0 = blockIdx.x * 64;
-  if (stats_ws[u * 4 + 3] != 0.f) return;  // singular: keep V0
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int l16 = lane & 15, g = lane >> 4;
-  const float* xu = x + (size_t)u * mp * c;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l16 = lane & 15, g = lane >> 4;
+  const bool singular = stats_ws[u * 4 + 3] != 0.f;
+  const float* xu = x + (size_t)u * MP * c;
   const uint8_t* fu = fixed + (size_t)u * c;
-  for (int e = tid; e < mp * 64; e += blockDim.x) {
-    int r = e / 64, tt = e % 64, t = t0 + tt;
-    Xs[r * XS + tt] = (t < c && !fu[t]) ? xu[(size_t)r * c + t] : 0.f;
-  }
-  __syncthreads();
-  const float* zu = z + (size_t)u * D * mp;
-  f32x4 acc[8];
+
+  f32x4 acc[D / 16];
 #pragma unroll
-  for (int dt = 0; dt < 8; ++dt) acc[dt] = zero4();
-  const int ndt = D / 16;
-  for (int ks = 0; ks < mp / 32; ++ks) {
-    float av[8];
+  for (int dt = 0; dt < D / 16; ++dt) acc[dt] = zero4();
+  if (!singular) {
+    for (int e = tid; e < MP * 64; e += 256) {
+      const int r = e / 64, tt = e % 64, t = t0 + tt;
+      const float xv = (t < c && !fu[t]) ? xu[(size_t)r * c + t] : 0.f;
+      const __bf16 h = (__bf16)xv;
+      xh[tt * XS + r] = __builtin_bit_cast(u16, h);
+      xl[tt * XS + r] = __builtin_bit_cast(u16, (__bf16)(xv - (float)h));
+    }
+    __syncthreads();
+    const u16* zh = zhi + (size_t)u * D * MP;
+    const u16* zl = zlo + (size_t)u * D * MP;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) av[e] = Xs[(ks * 32 + 8 * g + e) * XS + wave * 16 + l16];
-    bf16x8 ahi, alo;
-    split8(av, ahi, alo);
+    for (int ks = 0; ks < MP / 32; ++ks) {
+      const int tt = wave * 16 + l16;
+      const bf16x8 ah = as_bf16x8(*reinterpret_cast<const uint4*>(&xh[tt * XS + ks * 32 + 8 * g]));
+      const bf16x8 al = as_bf16x8(*reinterpret_cast<const uint4*>(&xl[tt * XS + ks * 32 + 8 * g]));
 #pragma unroll
-    for (int dt = 0; dt < 8; ++dt) {
-      if (dt >= ndt) break;
-      const float* zr = zu + (size_t)(dt * 16 + l16) * mp + ks * 32 + 8 * g;
-      float bv[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) bv[e] = zr[e];
-      bf16x8 bhi, blo;
-      split8(bv, bhi, blo);
-      acc[dt] = mfma_bf16(ahi, bhi, acc[dt]);
-      acc[dt] = mfma_bf16(ahi, blo, acc[dt]);
-      acc[dt] = mfma_bf16(alo, bhi, acc[dt]);
+      for (int dt = 0; dt < D / 16; ++dt) {
+        const size_t zo = (size_t)(dt * 16 + l16) * MP + ks * 32 + 8 * g;
+        const bf16x8 bh = as_bf16x8(*reinterpret_cast<const uint4*>(zh + zo));
+        const bf16x8 bl = as_bf16x8(*reinterpret_cast<const uint4*>(zl + zo));
+        acc[dt] = mfma_bf16(ah, bh, acc[dt]);
+        acc[dt] = mfma_bf16(ah, bl, acc[dt]);
+        acc[dt] = mfma_bf16(al, bh, acc[dt]);
+      }
     }
   }
+  // lane holds dV[t = t0 + 16*wave + 4g + i][dd = 16dt + l16]
 #pragma unroll
-  for (int dt = 0; dt < 8; ++dt) {
-    if (dt >= ndt) break;
+  for (int i = 0; i < 4; ++i) {
+    const int t = t0 + wave * 16 + 4 * g + i;
+    if (t >= c) continue;
+    const bool upd = !singular && !fu[t];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      int t = t0 + wave * 16 + 4 * g + i;
-      if (t < c && !fu[t]) v_out[((size_t)u * c + t) * D + dt * 16 + l16] += acc[dt][i];
+    for (int dt = 0; dt < D / 16; ++dt) {
+      const size_t o = ((size_t)u * c + t) * D + dt * 16 + l16;
+      const float v0 = bf16_to_f32(v0c[o]);
+      v_out[o] = upd ? v0 + acc[dt][i] : v0;
     }
   }
 }
@@ -244,57 +337,67 @@ template <int WAVES>
 hipError_t launch_gram_w(const Plan& p, const float* x, const uint8_t* fixed, float* npart,
                          hipStream_t s) {
   hipLaunchKernelGGL(gram_kernel<WAVES>, dim3(p.S3, p.U), dim3(WAVES * 64), 0, s, x, fixed, npart,
-                     p.c, p.mp, p.S3, p.chunk3);
+                     p.c, p.S3, p.chunk3);
+  return hipGetLastError();
+}
+
+template <int MP, int D>
+hipError_t launch_solve_t(const Plan& p, const float* npart, const float* y, const float* resid,
+                          float* gram, float* z, u16* zhi, u16* zlo, float* stats_ws,
+                          float* stats_user, hipStream_t s) {
+  hipLaunchKernelGGL((solve_kernel<MP, D>), dim3(p.U), dim3(MP / 32 * 256), 0, s, npart, p.S3, y,
+                     resid, gram, z, zhi, zlo, stats_ws, stats_user, p.m, p.lam);
+  return hipGetLastError();
+}
+
+template <int MP, int D>
+hipError_t launch_update_t(const Plan& p, const float* x, const uint8_t* fixed, const u16* zhi,
+                           const u16* zlo, const float* stats_ws, const u16* v0c, float* v_out,
+                           hipStream_t s) {
+  hipLaunchKernelGGL((update_kernel<MP, D>), dim3((p.c + 63) / 64, p.U), dim3(256), 0, s, x, fixed,
+                     zhi, zlo, stats_ws, v0c, v_out, p.c);
   return hipGetLastError();
 }
 
 }  // namespace
+
+bool merge_fast_supported(const Plan& p) {
+  return p.dtype == GRKV_BF16 && p.mp <= 128 && (p.d == 64 || p.d == 128);
+}
 
 hipError_t launch_gram(const Plan& p, const float* x, const uint8_t* fixed, float* npart,
                        hipStream_t s) {
   switch (p.waves) {
     case 1: return launch_gram_w<1>(p, x, fixed, npart, s);
     case 2: return launch_gram_w<2>(p, x, fixed, npart, s);
-    case 3: return launch_gram_w<3>(p, x, fixed, npart, s);
     case 4: return launch_gram_w<4>(p, x, fixed, npart, s);
-    case 5: return launch_gram_w<5>(p, x, fixed, npart, s);
-    case 6: return launch_gram_w<6>(p, x, fixed, npart, s);
-    case 7: return launch_gram_w<7>(p, x, fixed, npart, s);
     case 8: return launch_gram_w<8>(p, x, fixed, npart, s);
   }
   return hipErrorInvalidValue;
 }
 
-size_t chol_lds_bytes(int mp, int D, bool* w_in_lds) {
-  size_t tri_f = ((size_t)mp * (mp + 1) / 2 + 3) & ~(size_t)3;
-  size_t with_w = (tri_f + (size_t)mp * D) * sizeof(float);
-  if (with_w <= 150 * 1024) { *w_in_lds = true; return with_w; }
-  *w_in_lds = false;
-  return tri_f * sizeof(float);
+hipError_t launch_solve(const Plan& p, const float* npart, const float* y, const float* resid,
+                        float* gram, float* z, u16* zhi, u16* zlo, float* stats_ws,
+                        float* stats_user, hipStream_t s) {
+#define GRKV_SOLVE(MPV, DV)                                                                   \
+  if (p.mp == MPV && p.d == DV)                                                               \
+    return launch_solve_t<MPV, DV>(p, npart, y, resid, gram, z, zhi, zlo, stats_ws, stats_user, s);
+  GRKV_SOLVE(32, 64) GRKV_SOLVE(32, 128) GRKV_SOLVE(64, 64) GRKV_SOLVE(64, 128)
+  GRKV_SOLVE(128, 64) GRKV_SOLVE(128, 128)
+#undef GRKV_SOLVE
+  return hipErrorInvalidValue;
 }
 
-hipError_t launch_cholesky_solve(const Plan& p, const float* npart, const float* y,
-                                 const float* resid, float* gram, float* z, float* stats_ws,
-                                 float* stats_user, hipStream_t s) {
-  bool w_in_lds;
-  size_t lds = chol_lds_bytes(p.mp, p.d, &w_in_lds);
-  hipError_t e = hipFuncSetAttribute((const void*)chol_kernel,
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(chol_kernel, dim3(p.U), dim3(256), lds, s, npart, p.S3, y, resid, gram, z,
-                     stats_ws, stats_user, p.m, p.mp, p.d, p.lam, w_in_lds ? 1 : 0);
-  return hipGetLastError();
-}
-
-hipError_t launch_update(const Plan& p, const float* x, const uint8_t* fixed, const float* z,
-                         const float* stats_ws, float* v_out, hipStream_t s) {
-  size_t lds = (size_t)p.mp * 68 * sizeof(float);
-  hipError_t e = hipFuncSetAttribute((const void*)update_kernel,
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(update_kernel, dim3((p.c + 63) / 64, p.U), dim3(256), lds, s, x, fixed, z,
-                     stats_ws, v_out, p.c, p.mp, p.d);
-  return hipGetLastError();
+hipError_t launch_update(const Plan& p, const float* x, const uint8_t* fixed, const u16* zhi,
+                         const u16* zlo, const float* stats_ws, const u16* v0c, float* v_out,
+                         hipStream_t s) {
+#define GRKV_UPD(MPV, DV)                                                                     \
+  if (p.mp == MPV && p.d == DV)                                                               \
+    return launch_update_t<MPV, DV>(p, x, fixed, zhi, zlo, stats_ws, v0c, v_out, s);
+  GRKV_UPD(32, 64) GRKV_UPD(32, 128) GRKV_UPD(64, 64) GRKV_UPD(64, 128)
+  GRKV_UPD(128, 64) GRKV_UPD(128, 128)
+#undef GRKV_UPD
+  return hipErrorInvalidValue;
 }
 
 }  // namespace grkv

@@ -1,0 +1,211 @@
+// Generic value-step kernels for shapes outside the fast path (float32
+// inputs, or m > 128 rows): Cholesky of N in LDS (packed lower triangle, the
+// right-hand sides in LDS when they fit and in the z buffer otherwise), then
+// V* = V0 + X_G^T Z added into v_out, which the gather filled with V0.
+// Same arithmetic contract as merge.hip; slower, latency-bound per unit.
+#include "grkv_device.h"
+#include "grkv_internal.h"
+
+namespace grkv {
+namespace {
+
+__device__ __forceinline__ int tri(int i, int j) { return i * (i + 1) / 2 + j; }
+
+// One block per unit.  L (packed lower triangle) lives in LDS; the right-hand
+// sides W are in LDS when they fit (w_in_lds) and otherwise in the z buffer.
+__global__ __launch_bounds__(256) void chol_kernel(const float* npart, int S3, const float* y,
+                                                  const float* resid, float* gram, float* z,
+                                                  float* stats_ws, float* stats_user, int m,
+                                                  int mp, int D, float lam, int w_in_lds) {
+  extern __shared__ __attribute__((aligned(16))) float lds[];
+  __shared__ int fail;
+  __shared__ double red[3][4];
+  const int u = blockIdx.x, tid = threadIdx.x;
+  float* L = lds;
+  const int ntri = mp * (mp + 1) / 2;
+  float* zu = z + (size_t)u * D * mp;  // Z^T [D][mp]
+  float* Wl = lds + ((ntri + 3) & ~3);
+  // W(i, col): LDS [mp][D] or global [D][mp]
+  float* Wb = w_in_lds ? Wl : zu;
+  const int si = w_in_lds ? D : 1, sc = w_in_lds ? 1 : mp;
+
+  if (tid == 0) fail = 0;
+  const float* np = npart + (size_t)u * S3 * mp * mp;
+  float* gu = gram + (size_t)u * mp * mp;
+  for (int e = tid; e < mp * mp; e += blockDim.x) {
+    int i = e / mp, j = e % mp;
+    float v = 0.f;
+    for (int s = 0; s < S3; ++s) v += np[(size_t)s * mp * mp + e];
+    if (i == j) v += (i < m) ? lam : 1.f;
+    gu[e] = v;
+    if (j <= i) L[tri(i, j)] = v;
+  }
+  const float* ru = resid + (size_t)u * mp * D;
+  for (int e = tid; e < mp * D; e += blockDim.x) {
+    int i = e / D, col = e % D;
+    Wb[i * si + col * sc] = ru[e];
+  }
+  __syncthreads();
+
+  for (int k = 0; k < mp; ++k) {
+    if (tid == 0) {
+      float dkk = L[tri(k, k)];
+      if (!(dkk > 0.f) || !isfinite(dkk)) { fail = 1; dkk = 1.f; }
+      L[tri(k, k)] = sqrtf(dkk);
+    }
+    __syncthreads();
+    const float inv = 1.f / L[tri(k, k)];
+    for (int i = k + 1 + tid; i < mp; i += blockDim.x) L[tri(i, k)] *= inv;
+    __syncthreads();
+    const int rem = mp - k - 1;
+    for (int e = tid; e < rem * rem; e += blockDim.x) {
+      int i = k + 1 + e / rem, j = k + 1 + e % rem;
+      if (j <= i) L[tri(i, j)] -= L[tri(i, k)] * L[tri(j, k)];
+    }
+    __syncthreads();
+  }
+  const bool ok = fail == 0;
+
+  // forward (L W = R) then backward (L^T Z = W), one right-hand side per thread
+  for (int col = tid; col < D; col += blockDim.x) {
+    if (!ok) {
+      for (int i = 0; i < mp; ++i) Wb[i * si + col * sc] = 0.f;
+      continue;
+    }
+    for (int i = 0; i < mp; ++i) {
+      float acc = Wb[i * si + col * sc];
+      for (int j = 0; j < i; ++j) acc -= L[tri(i, j)] * Wb[j * si + col * sc];
+      Wb[i * si + col * sc] = acc / L[tri(i, i)];
+    }
+    for (int i = mp - 1; i >= 0; --i) {
+      float acc = Wb[i * si + col * sc];
+      for (int j = i + 1; j < mp; ++j) acc -= L[tri(j, i)] * Wb[j * si + col * sc];
+      Wb[i * si + col * sc] = acc / L[tri(i, i)];
+    }
+  }
+  __syncthreads();
+  if (w_in_lds)
+    for (int e = tid; e < mp * D; e += blockDim.x) {
+      int col = e / mp, i = e % mp;
+      zu[e] = Wl[i * D + col];
+    }
+
+  // stats: ||Y||^2, ||R||^2, ||Z||^2 over the m real rows
+  const float* yu = y + (size_t)u * mp * D;
+  double sy = 0.0, sr = 0.0, sz = 0.0;
+  for (int e = tid; e < m * D; e += blockDim.x) {
+    int i = e / D, col = e % D;
+    double yv = yu[e], rv = ru[e], zv = Wb[i * si + col * sc];
+    sy += yv * yv;
+    sr += rv * rv;
+    sz += zv * zv;
+  }
+  for (int off = 32; off > 0; off >>= 1) {
+    sy += __shfl_xor(sy, off);
+    sr += __shfl_xor(sr, off);
+    sz += __shfl_xor(sz, off);
+  }
+  if ((tid & 63) == 0) { red[0][tid >> 6] = sy; red[1][tid >> 6] = sr; red[2][tid >> 6] = sz; }
+  __syncthreads();
+  if (tid == 0) {
+    double Y2 = 0, R2 = 0, Z2 = 0;
+    for (int k = 0; k < (int)(blockDim.x >> 6); ++k) { Y2 += red[0][k]; R2 += red[1][k]; Z2 += red[2][k]; }
+    double dn = Y2 > 0 ? Y2 : 1.0;
+    double dbefore = R2 / dn;
+    double dafter = ok ? (double)lam * lam * Z2 / dn : dbefore;
+    float st[4] = {(float)Y2, (float)dbefore, (float)dafter, ok ? 0.f : (float)GRKV_UNIT_SINGULAR};
+    for (int k = 0; k < 4; ++k) {
+      stats_ws[u * 4 + k] = st[k];
+      if (stats_user) stats_user[u * 4 + k] = st[k];
+    }
+  }
+}
+
+// dV = X_G^T Z for 64 retained columns per block; adds into v_out (which holds V0).
+__global__ __launch_bounds__(256) void update_add_kernel(const float* x, const uint8_t* fixed,
+                                                     const float* z, const float* stats_ws,
+                                                     float* v_out, int c, int mp, int D) {
+  extern __shared__ __attribute__((aligned(16))) float Xs[];  // [mp][68]
+  constexpr int XS = 68;
+  const int u = blockIdx.y, t0 = blockIdx.x * 64;
+  if (stats_ws[u * 4 + 3] != 0.f) return;  // singular: keep V0
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l16 = lane & 15, g = lane >> 4;
+  const float* xu = x + (size_t)u * mp * c;
+  const uint8_t* fu = fixed + (size_t)u * c;
+  for (int e = tid; e < mp * 64; e += blockDim.x) {
+    int r = e / 64, tt = e % 64, t = t0 + tt;
+    Xs[r * XS + tt] = (t < c && !fu[t]) ? xu[(size_t)r * c + t] : 0.f;
+  }
+  __syncthreads();
+  const float* zu = z + (size_t)u * D * mp;
+  f32x4 acc[8];
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt) acc[dt] = zero4();
+  const int ndt = D / 16;
+  for (int ks = 0; ks < mp / 32; ++ks) {
+    float av[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) av[e] = Xs[(ks * 32 + 8 * g + e) * XS + wave * 16 + l16];
+    bf16x8 ahi, alo;
+    split8(av, ahi, alo);
+#pragma unroll
+    for (int dt = 0; dt < 8; ++dt) {
+      if (dt >= ndt) break;
+      const float* zr = zu + (size_t)(dt * 16 + l16) * mp + ks * 32 + 8 * g;
+      float bv[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) bv[e] = zr[e];
+      bf16x8 bhi, blo;
+      split8(bv, bhi, blo);
+      acc[dt] = mfma_bf16(ahi, bhi, acc[dt]);
+      acc[dt] = mfma_bf16(ahi, blo, acc[dt]);
+      acc[dt] = mfma_bf16(alo, bhi, acc[dt]);
+    }
+  }
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt) {
+    if (dt >= ndt) break;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      int t = t0 + wave * 16 + 4 * g + i;
+      if (t < c && !fu[t]) v_out[((size_t)u * c + t) * D + dt * 16 + l16] += acc[dt][i];
+    }
+  }
+}
+
+}  // namespace
+
+static size_t chol_lds_bytes(int mp, int D, bool* w_in_lds) {
+  size_t tri_f = ((size_t)mp * (mp + 1) / 2 + 3) & ~(size_t)3;
+  size_t with_w = (tri_f + (size_t)mp * D) * sizeof(float);
+  if (with_w <= 150 * 1024) { *w_in_lds = true; return with_w; }
+  *w_in_lds = false;
+  return tri_f * sizeof(float);
+}
+
+hipError_t launch_cholesky_solve(const Plan& p, const float* npart, const float* y,
+                                 const float* resid, float* gram, float* z, float* stats_ws,
+                                 float* stats_user, hipStream_t s) {
+  bool w_in_lds;
+  size_t lds = chol_lds_bytes(p.mp, p.d, &w_in_lds);
+  hipError_t e = hipFuncSetAttribute((const void*)chol_kernel,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(chol_kernel, dim3(p.U), dim3(256), lds, s, npart, p.S3, y, resid, gram, z,
+                     stats_ws, stats_user, p.m, p.mp, p.d, p.lam, w_in_lds ? 1 : 0);
+  return hipGetLastError();
+}
+
+hipError_t launch_update_add(const Plan& p, const float* x, const uint8_t* fixed, const float* z,
+                             const float* stats_ws, float* v_out, hipStream_t s) {
+  size_t lds = (size_t)p.mp * 68 * sizeof(float);
+  hipError_t e = hipFuncSetAttribute((const void*)update_add_kernel,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(update_add_kernel, dim3((p.c + 63) / 64, p.U), dim3(256), lds, s, x, fixed, z,
+                     stats_ws, v_out, p.c, p.mp, p.d);
+  return hipGetLastError();
+}
+
+}  // namespace grkv

@@ -147,6 +147,7 @@ __global__ void gather_kernel(const T* K, const T* V, const int32_t* idx, T* k_o
   }
   *reinterpret_cast<uint4*>(k_out + dof) = kv;
   *reinterpret_cast<uint4*>(v0c + dof) = vv;
+  if (!v_out) return;
   const T* ve = reinterpret_cast<const T*>(&vv);
   for (int e = 0; e < epc; ++e) {
     float f;

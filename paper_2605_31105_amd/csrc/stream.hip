@@ -1,0 +1,421 @@
+// bf16 streaming window attention for gfx950 (pass A: log-sum-exp partials,
+// pass B: P.V partials, SnapKV column sums, optional P).  Same contract as the
+// generic kernels in attention.hip, built for bandwidth:
+//
+//  * K and V tiles go from HBM straight into an LDS ring (global_load_lds,
+//    16 bytes per lane, no register staging).  Each ring stage is its own
+//    LDS array and the tile loop is unrolled by the ring depth, so every
+//    access names its stage at compile time; the compiler can then see that
+//    the loads refilling one stage do not alias the stage being read and does
+//    not stall on them.  NSTAGE-1 tiles stay in flight per block.
+//  * A tile is 4096 elements per tensor (32 keys of d=128, 64 keys of d=64),
+//    row-major with the 16-byte chunks of row r XOR-swizzled by r, which keeps
+//    the MFMA operand reads of K free of bank conflicts.
+//  * P.V uses P as a bf16 hi+lo pair (two MFMAs, about 16 bits of P).
+//  * The P.V B-operand (four consecutive keys of one d column per lane) is
+//    read from the row-major V tile with the LDS transpose read
+//    ds_read_b64_tr_b16: within a 16-lane group, lane 4e+q supplies the
+//    address of key row e, columns 4q..4q+3, and lane i receives column i of
+//    the four rows.
+//  * Pass A keeps a running max and sum per lane (its own keys of its row) and
+//    merges the four lanes of a row once at the end; pass B's column sums use
+//    DPP within 16-lane rows.  Neither touches the LDS for reductions inside
+//    the tile loop except one 32-float exchange per tile for column sums.
+//  * Window positions are the last w key slots of both key sets (the full
+//    cache, and the retained set whose last w entries are the window), so the
+//    causal rule needs no position array.
+#include "grkv_device.h"
+#include "grkv_internal.h"
+
+namespace grkv {
+namespace {
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef short v8i16 __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+
+struct StreamK {
+  const u16* q;
+  const u16* k;
+  const u16* v;
+  int m, mp, w;
+  int causal;
+  int nk, S, chunk;
+  float scale_log2;
+  float* pmax;
+  double* psum;
+  const float* lse_log2;
+  float* ypart;
+  float* colsum;
+  int prefix;
+  float* xout;
+};
+
+constexpr int kTileElems = 4096;   // elements of one tensor per tile
+constexpr int kTileBytes = kTileElems * 2;
+
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
+// vmcnt in bits 3:0 and 15:14, expcnt 6:4 and lgkmcnt 11:8 left at maximum).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// Workgroup barrier for the tile ring.  It waits for this wave's own LDS
+// reads and writes and synchronises the waves; it does not wait for the
+// vector-memory counter, so tile loads already in flight stay in flight (a
+// fence-based barrier counts the LDS writes of those loads as pending local
+// stores and would drain them).  The memory clobber keeps the compiler from
+// moving LDS accesses across it.  Completion of the tile about to be read is
+// established before the barrier by an explicit s_waitcnt on vmcnt.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+template <int D>
+struct Geo {
+  static constexpr int TK = kTileElems / D;           // keys per tile
+  static constexpr int CPR = D / 8;                   // 16-byte chunks per row
+  static constexpr int NKT = TK / 16;                 // 16-key MFMA tiles per tile
+  static constexpr int RPI = 64 / CPR;                // rows filled by one wave instruction
+  static constexpr int INSTR = kTileBytes / 1024;     // wave instructions per tensor per tile (8)
+};
+
+// Byte offset, inside a tile, of logical 16-byte chunk `ch` of row `r`.
+template <int D>
+__device__ __forceinline__ int swz(int r, int ch) {
+  return (r * Geo<D>::CPR + (ch ^ (r & (Geo<D>::CPR - 1)))) * 16;
+}
+
+// Issues this wave's share of the direct-to-LDS loads of one tensor tile.
+// Rows at or past key_end are clamped to key_end-1 (finite data, masked later).
+template <int D, int WAVES>
+__device__ __forceinline__ void load_tile(const u16* base, int tile0, int key_end, char* lds_tile,
+                                          int wave, int lane) {
+  using G = Geo<D>;
+  constexpr int PER = G::INSTR / WAVES;
+#pragma unroll
+  for (int it = 0; it < PER; ++it) {
+    const int instr = wave * PER + it;
+    const int r = instr * G::RPI + lane / G::CPR;       // row inside the tile
+    const int p = lane % G::CPR;                        // physical chunk in the row
+    const int ch = p ^ (r & (G::CPR - 1));              // logical chunk stored there
+    int key = tile0 + r;
+    key = key < key_end ? key : key_end - 1;
+    const u16* src = base + (size_t)key * D + ch * 8;
+    __builtin_amdgcn_global_load_lds(src, (lds_void*)(lds_tile + instr * 1024), 16, 0, 0);
+  }
+}
+
+// Per-block state of one (unit, split) stream.
+template <int D, bool PASS_B>
+struct State {
+  uint4 qb[2][D / 32];
+  int rowwin[2];
+  bool rowok[2];
+  float lse[2];
+  float mrun[2];   // pass A: per-lane running max of this lane's keys
+  double srun[2];  // pass A: per-lane running sum of 2^(t - mrun)
+  f32x4 y[2][PASS_B ? D / 16 : 1];
+};
+
+template <int D, int WAVES, bool PASS_B, int NSTAGE>
+struct Stream {
+  using G = Geo<D>;
+  static constexpr int TK = G::TK, NKT = G::NKT;
+  static constexpr int LOADS = (G::INSTR / WAVES) * (PASS_B ? 2 : 1);  // per thread per tile
+
+  const StreamK& a;
+  const u16* kbase;
+  const u16* vbase;
+  int u, key0, key_end, ntiles, win0, lane, wave, l16, g;
+  float (*colpart)[WAVES][TK];
+
+  __device__ __forceinline__ void issue(int t, char* stage) {
+    if (t < ntiles) {
+      load_tile<D, WAVES>(kbase, key0 + t * TK, key_end, stage, wave, lane);
+      if (PASS_B) load_tile<D, WAVES>(vbase, key0 + t * TK, key_end, stage + kTileBytes, wave, lane);
+    }
+  }
+
+  __device__ __forceinline__ void flush_colsum(int t) {
+    // column sums of tile t (every wave wrote its part before the last barrier)
+    if (threadIdx.x < TK) {
+      const int key = key0 + t * TK + threadIdx.x;
+      if (key < key_end && key < a.prefix) {
+        float c = 0.f;
+#pragma unroll
+        for (int wv = 0; wv < WAVES; ++wv) c += colpart[t & 1][wv][threadIdx.x];
+        a.colsum[(size_t)u * a.prefix + key] = c;
+      }
+    }
+  }
+
+  // One tile: wait for it, refill the stage freed last step, compute.
+  __device__ __forceinline__ void step(int t, const char* cur, char* refill, State<D, PASS_B>& S) {
+    if (t >= ntiles) return;
+    const int ahead = min(ntiles - 1 - t, NSTAGE - 2);
+    if (ahead >= 2) wait_vmcnt<2 * LOADS>();
+    else if (ahead == 1) wait_vmcnt<LOADS>();
+    else wait_vmcnt<0>();
+    lds_barrier();
+    if (PASS_B && a.colsum && t > 0) flush_colsum(t - 1);
+    issue(t + NSTAGE - 1, refill);
+
+    const int tile0 = key0 + t * TK;
+    f32x4 st[NKT][2];
+    uint4 kv[D / 32][NKT];
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks)
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt)
+        kv[ks][kt] = *reinterpret_cast<const uint4*>(cur + swz<D>(kt * 16 + l16, ks * 4 + g));
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt) st[kt][0] = st[kt][1] = zero4();
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks)
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt)
+          st[kt][rt] = mfma_bf16(as_bf16x8(kv[ks][kt]), as_bf16x8(S.qb[rt][ks]), st[kt][rt]);
+    bool ok[NKT][2][4];
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int key = tile0 + kt * 16 + 4 * g + i;
+        const int kw = key - win0;   // < 0 outside the window
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt) ok[kt][rt][i] = S.rowok[rt] && key < key_end && kw <= S.rowwin[rt];
+      }
+
+    if (!PASS_B) {
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt) {
+        float tv[NKT][4];
+        float tmax = -INFINITY;
+#pragma unroll
+        for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            tv[kt][i] = ok[kt][rt][i] ? st[kt][rt][i] * a.scale_log2 : -INFINITY;
+            tmax = fmaxf(tmax, tv[kt][i]);
+          }
+        if (tmax == -INFINITY) continue;
+        if (tmax > S.mrun[rt]) {
+          if (S.mrun[rt] != -INFINITY) S.srun[rt] *= exp2((double)S.mrun[rt] - (double)tmax);
+          S.mrun[rt] = tmax;
+        }
+        float acc = 0.f;
+#pragma unroll
+        for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc += exp2f(tv[kt][i] - S.mrun[rt]);
+        S.srun[rt] += (double)acc;
+      }
+      return;
+    }
+
+    float pv[NKT][2][4];
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          pv[kt][rt][i] = ok[kt][rt][i] ? exp2f(fmaf(st[kt][rt][i], a.scale_log2, -S.lse[rt])) : 0.f;
+    if (a.colsum) {
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float c = sum16_dpp(pv[kt][0][i] + pv[kt][1][i]);
+          if (l16 == 0) colpart[t & 1][wave][kt * 16 + 4 * g + i] = c;
+        }
+    }
+    if (a.xout) {
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt) {
+        const int row = wave * kRowsPerWave + rt * 16 + l16;
+        float* xr = a.xout + ((size_t)u * a.mp + row) * a.nk;
+#pragma unroll
+        for (int kt = 0; kt < NKT; ++kt) {
+          const int key = tile0 + kt * 16 + 4 * g;
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (key + i < key_end) xr[key + i] = pv[kt][rt][i];
+        }
+      }
+    }
+    const char* vt = cur + kTileBytes;
+    const int e = l16 >> 2, qq = l16 & 3;
+#pragma unroll
+    for (int kp = 0; kp < NKT / 2; ++kp) {
+      bf16x8 ahi[2], alo[2];
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt) {
+        float x8[8] = {pv[2 * kp][rt][0], pv[2 * kp][rt][1], pv[2 * kp][rt][2], pv[2 * kp][rt][3],
+                       pv[2 * kp + 1][rt][0], pv[2 * kp + 1][rt][1], pv[2 * kp + 1][rt][2],
+                       pv[2 * kp + 1][rt][3]};
+        split8(x8, ahi[rt], alo[rt]);
+      }
+      // lane 4e+q of group g supplies key row 32kp + 4g + e (and +16), columns dt*16 + 4q..+3
+      const int r0 = 32 * kp + 4 * g + e;
+      bf16x8 b[D / 16];
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt) {
+        const int col = dt * 16 + 4 * qq;
+        v4i16 b0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_v4i16*)(vt + swz<D>(r0, col >> 3) + (col & 7) * 2));
+        v4i16 b1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_v4i16*)(vt + swz<D>(r0 + 16, col >> 3) + (col & 7) * 2));
+        b[dt] = __builtin_bit_cast(bf16x8, (v8i16){b0[0], b0[1], b0[2], b0[3],
+                                                   b1[0], b1[1], b1[2], b1[3]});
+      }
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt)
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt) {
+          S.y[rt][dt] = mfma_bf16(ahi[rt], b[dt], S.y[rt][dt]);
+          S.y[rt][dt] = mfma_bf16(alo[rt], b[dt], S.y[rt][dt]);
+        }
+    }
+  }
+};
+
+template <int D, int WAVES, bool PASS_B>
+__global__ __launch_bounds__(WAVES * 64) void stream_kernel(StreamK a) {
+  using G = Geo<D>;
+  constexpr int TK = G::TK;
+  constexpr int NSTAGE = PASS_B ? 3 : 4;
+  constexpr int STAGE_BYTES = kTileBytes * (PASS_B ? 2 : 1);
+  __shared__ __attribute__((aligned(16))) char stg0[STAGE_BYTES];
+  __shared__ __attribute__((aligned(16))) char stg1[STAGE_BYTES];
+  __shared__ __attribute__((aligned(16))) char stg2[STAGE_BYTES];
+  __shared__ __attribute__((aligned(16))) char stg3[PASS_B ? 16 : STAGE_BYTES];
+  __shared__ float colpart[2][WAVES][TK];
+
+  Stream<D, WAVES, PASS_B, NSTAGE> sm{a};
+  sm.u = blockIdx.y;
+  const int s = blockIdx.x;
+  sm.lane = threadIdx.x & 63;
+  sm.wave = threadIdx.x >> 6;
+  sm.l16 = sm.lane & 15;
+  sm.g = sm.lane >> 4;
+  sm.key0 = s * a.chunk;
+  sm.key_end = min(sm.key0 + a.chunk, a.nk);
+  sm.ntiles = sm.key_end > sm.key0 ? (sm.key_end - sm.key0 + TK - 1) / TK : 0;
+  sm.kbase = a.k + (size_t)sm.u * a.nk * D;
+  sm.vbase = a.v + (size_t)sm.u * a.nk * D;
+  sm.win0 = a.nk - a.w;
+  sm.colpart = colpart;
+  const int u = sm.u, wave = sm.wave, l16 = sm.l16, g = sm.g;
+
+  State<D, PASS_B> S;
+#pragma unroll
+  for (int rt = 0; rt < 2; ++rt) {
+    const int row = wave * kRowsPerWave + rt * 16 + l16;
+    S.rowok[rt] = row < a.m;
+    S.rowwin[rt] = a.causal ? row % a.w : 0x3fffffff;
+    const u16* q = a.q + ((size_t)u * a.m + row) * D;
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks)
+      S.qb[rt][ks] = S.rowok[rt] ? *reinterpret_cast<const uint4*>(q + ks * 32 + 8 * g)
+                                 : make_uint4(0, 0, 0, 0);
+    S.lse[rt] = PASS_B ? a.lse_log2[(size_t)u * a.mp + row] : 0.f;
+    S.mrun[rt] = -INFINITY;
+    S.srun[rt] = 0.0;
+#pragma unroll
+    for (int dt = 0; dt < (PASS_B ? D / 16 : 1); ++dt) S.y[rt][dt] = zero4();
+  }
+
+  sm.issue(0, stg0);
+  sm.issue(1, stg1);
+  if (NSTAGE == 4) sm.issue(2, stg2);
+  for (int t = 0; t < sm.ntiles; t += NSTAGE) {
+    if (NSTAGE == 3) {
+      sm.step(t + 0, stg0, stg2, S);
+      sm.step(t + 1, stg1, stg0, S);
+      sm.step(t + 2, stg2, stg1, S);
+    } else {
+      sm.step(t + 0, stg0, stg3, S);
+      sm.step(t + 1, stg1, stg0, S);
+      sm.step(t + 2, stg2, stg1, S);
+      sm.step(t + 3, stg3, stg2, S);
+    }
+  }
+
+  const int s_idx = s;
+  if (PASS_B) {
+    if (a.colsum && sm.ntiles > 0) {
+      lds_barrier();
+      sm.flush_colsum(sm.ntiles - 1);
+    }
+    float* yp = a.ypart + ((size_t)u * a.S + s_idx) * a.mp * D;
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int row = wave * kRowsPerWave + rt * 16 + 4 * g + i;
+          yp[(size_t)row * D + dt * 16 + l16] = S.y[rt][dt][i];
+        }
+  } else {
+    // merge the four lanes of each row: M = max m_g, sum = sum_g s_g 2^(m_g - M)
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt) {
+      float M = max_over_groups(S.mrun[rt]);
+      double part = (S.mrun[rt] == -INFINITY) ? 0.0 : S.srun[rt] * exp2((double)S.mrun[rt] - (double)M);
+      const double tot = sum_over_groups(part);
+      const int row = wave * kRowsPerWave + rt * 16 + l16;
+      if (g == 0) {
+        const size_t o = ((size_t)u * a.S + s_idx) * a.mp + row;
+        a.pmax[o] = M;
+        a.psum[o] = M == -INFINITY ? 0.0 : tot;
+      }
+    }
+  }
+}
+
+template <int D, int WAVES, bool PASS_B>
+hipError_t launch_stream_t(const Plan& p, const AttnPass& a, hipStream_t s) {
+  StreamK k;
+  k.q = (const u16*)a.q; k.k = (const u16*)a.k; k.v = (const u16*)a.v;
+  k.m = p.m; k.mp = p.mp; k.w = p.w; k.causal = p.opt.causal_window ? 1 : 0;
+  k.nk = a.nk; k.S = a.S; k.chunk = a.chunk;
+  k.scale_log2 = (float)(1.4426950408889634 / __builtin_sqrt((double)D));
+  k.pmax = a.pmax; k.psum = a.psum; k.lse_log2 = a.lse_log2;
+  k.ypart = a.ypart; k.colsum = a.colsum; k.prefix = a.prefix; k.xout = a.xout;
+  hipLaunchKernelGGL((stream_kernel<D, WAVES, PASS_B>), dim3(a.S, p.U), dim3(WAVES * 64), 0, s, k);
+  return hipGetLastError();
+}
+
+template <int D, bool PASS_B>
+hipError_t launch_stream_w(const Plan& p, const AttnPass& a, hipStream_t s) {
+  switch (p.waves) {
+    case 1: return launch_stream_t<D, 1, PASS_B>(p, a, s);
+    case 2: return launch_stream_t<D, 2, PASS_B>(p, a, s);
+    case 4: return launch_stream_t<D, 4, PASS_B>(p, a, s);
+    case 8: return launch_stream_t<D, 8, PASS_B>(p, a, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+bool stream_supported(const Plan& p) {
+  return p.dtype == GRKV_BF16 && (p.d == 64 || p.d == 128) &&
+         (p.waves == 1 || p.waves == 2 || p.waves == 4 || p.waves == 8);
+}
+
+hipError_t launch_stream(const Plan& p, const AttnPass& a, bool pass_b, hipStream_t s) {
+  if (p.d == 128)
+    return pass_b ? launch_stream_w<128, true>(p, a, s) : launch_stream_w<128, false>(p, a, s);
+  return pass_b ? launch_stream_w<64, true>(p, a, s) : launch_stream_w<64, false>(p, a, s);
+}
+
+}  // namespace grkv
