@@ -127,6 +127,147 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(SelK a) {
   }
 }
 
+constexpr int kSmallThreads = 512;
+constexpr int kSmallPer = 64;   // pooled scores per thread: prefixes up to 32768
+
+// Block-wide sum of one value per thread (kSmallThreads threads); `part` holds
+// 2 x 8 words and alternates by `parity` so consecutive calls need one barrier.
+__device__ __forceinline__ uint32_t block_sum_small(uint32_t v, uint32_t (*part)[8], int parity) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+  if ((threadIdx.x & 63) == 0) part[parity][threadIdx.x >> 6] = v;
+  __syncthreads();
+  uint32_t tot = 0;
+#pragma unroll
+  for (int k = 0; k < kSmallThreads / 64; ++k) tot += part[parity][k];
+  return tot;
+}
+
+// Same selection for prefixes of at most 32768 tokens, with each thread
+// keeping 64 consecutive pooled scores in registers.  The k-th largest score
+// is found by bisection on the fp32 bit pattern (scores are >= 0, so bit
+// patterns order like values): 31 block-wide counts of "score >= mid", no
+// histograms and no atomics.
+__global__ __launch_bounds__(kSmallThreads) void select_small_kernel(SelK a) {
+  __shared__ float sl[kSmallThreads * kSmallPer];
+  __shared__ uint32_t part[2][8];
+  __shared__ uint32_t scan_scratch[16];
+  constexpr int PER = kSmallPer;
+  const int u = blockIdx.x, tid = threadIdx.x;
+  const int P = a.prefix;
+  const float* s = a.colsum + (size_t)u * P;
+  float* pg = a.pooled + (size_t)u * P;
+  int32_t* idx = a.idx + (size_t)u * a.c;
+  uint8_t* fixed = a.fixed + (size_t)u * a.c;
+  const int j0 = tid * PER;
+
+  // Positions past the prefix get key 0 (score 0.0): they rank after every
+  // real position with an equal score, so they are never taken while real
+  // positions are left.
+  // scores of the whole prefix into LDS (coalesced), then each thread pools
+  // its 64 consecutive positions, summing s[j-h..j+h] left to right
+  for (int t = tid; t < P; t += kSmallThreads) sl[t] = s[t];
+  __syncthreads();
+  uint32_t key[PER];
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    const int j = j0 + q;
+    float acc = 0.f;
+    const int lo = j - a.h < 0 ? 0 : j - a.h;
+    const int hi = j + a.h > P - 1 ? P - 1 : j + a.h;
+    for (int t = lo; t <= hi; ++t) acc += sl[t];
+    key[q] = j < P ? __float_as_uint(acc) : 0u;
+    if (j < P) pg[j] = acc;
+  }
+
+  // count of keys >= x over the block
+  int parity = 0;
+  auto count_ge = [&](uint32_t x0, uint32_t x1, uint32_t* c0, uint32_t* c1) {
+    uint32_t n0 = 0, n1 = 0;
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      n0 += key[q] >= x0;
+      n1 += key[q] >= x1;
+    }
+    *c0 = block_sum_small(n0 | (n1 << 16), part, parity);
+    parity ^= 1;
+    *c1 = *c0 >> 16;
+    *c0 &= 0xFFFF;
+  };
+  // largest T with count(>= T) >= k, for k = s_sel (0) and n_top (1)
+  uint32_t lo0 = 0, hi0 = 0x7F800001u, lo1 = 0, hi1 = 0x7F800001u;
+  const uint32_t k0 = (uint32_t)a.s_sel, k1 = (uint32_t)a.n_top;
+#pragma unroll 1
+  for (int it = 0; it < 32; ++it) {
+    const bool go0 = k0 > 0 && hi0 - lo0 > 1, go1 = k1 > 0 && hi1 - lo1 > 1;
+    if (!go0 && !go1) break;   // uniform: every thread holds the same bounds
+    const uint32_t m0 = lo0 + (hi0 - lo0) / 2, m1 = lo1 + (hi1 - lo1) / 2;
+    uint32_t c0, c1;
+    count_ge(m0, m1, &c0, &c1);
+    if (go0) { if (c0 >= k0) lo0 = m0; else hi0 = m0; }
+    if (go1) { if (c1 >= k1) lo1 = m1; else hi1 = m1; }
+  }
+  const uint32_t T0 = lo0, T1 = lo1;
+  uint32_t gt0, gt1;
+  count_ge(T0 + 1, T1 + 1, &gt0, &gt1);
+  const bool any0 = k0 > 0, any1 = k1 > 0;
+  const uint32_t krem0 = k0 - gt0, krem1 = k1 - gt1;   // ties taken, lowest positions first
+
+  uint32_t eq0 = 0, eq1 = 0;
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    eq0 += key[q] == T0;
+    eq1 += key[q] == T1;
+  }
+  if (!any0) eq0 = 0;
+  if (!any1) eq1 = 0;
+  uint32_t tot;
+  const uint32_t eqb0 = block_exclusive_scan(eq0, scan_scratch, &tot);
+  const uint32_t eqb1 = block_exclusive_scan(eq1, scan_scratch, &tot);
+  uint32_t nsel = 0;
+  {
+    uint32_t e0 = eqb0;
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      const bool sel = key[q] > T0 || (key[q] == T0 && e0 < krem0);
+      e0 += key[q] == T0;
+      nsel += sel;
+    }
+    if (!any0) nsel = 0;
+  }
+  uint32_t off = block_exclusive_scan(nsel, scan_scratch, &tot);
+  // selection and top-beta membership as bit masks over this thread's positions,
+  // then the selected positions in increasing order
+  uint64_t selm = 0, topm = 0;
+  {
+    uint32_t e0 = eqb0, e1 = eqb1;
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      const bool sel = key[q] > T0 || (key[q] == T0 && e0 < krem0);
+      const bool top = key[q] > T1 || (key[q] == T1 && e1 < krem1);
+      e0 += key[q] == T0;
+      e1 += key[q] == T1;
+      selm |= (uint64_t)sel << q;
+      topm |= (uint64_t)top << q;
+    }
+  }
+  if (!any0) selm = 0;
+  if (!any1) topm = 0;
+  while (selm) {
+    const int q = __builtin_ctzll(selm);
+    const int j = j0 + q;
+    idx[off] = j;
+    fixed[off] = (j < a.n_sink || ((topm >> q) & 1)) ? 1 : 0;
+    ++off;
+    selm &= selm - 1;
+  }
+  for (int i = tid; i < a.w; i += blockDim.x) {
+    const int64_t pos = a.n - a.w + i;
+    idx[a.s_sel + i] = (int32_t)pos;
+    fixed[a.s_sel + i] = (a.fix_window || pos < a.n_sink) ? 1 : 0;
+  }
+}
+
 template <typename T>
 __global__ void gather_kernel(const T* K, const T* V, const int32_t* idx, T* k_out, T* v0c,
                               float* v_out, int c, int64_t n, int D) {
@@ -165,7 +306,10 @@ hipError_t launch_select(const Plan& p, const float* colsum, float* pooled, int3
   a.prefix = p.prefix; a.c = p.c; a.w = p.w; a.h = (p.k_pool - 1) / 2;
   a.s_sel = p.s_sel; a.n_top = p.n_top_fixed; a.n_sink = p.opt.n_sink;
   a.fix_window = p.opt.fix_window ? 1 : 0; a.n = p.n;
-  hipLaunchKernelGGL(select_kernel, dim3(p.U), dim3(kSelectThreads), 0, s, a);
+  if (p.prefix <= kSmallThreads * kSmallPer && p.k_pool <= 17)
+    hipLaunchKernelGGL(select_small_kernel, dim3(p.U), dim3(kSmallThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL(select_kernel, dim3(p.U), dim3(kSelectThreads), 0, s, a);
   return hipGetLastError();
 }
 
