@@ -158,14 +158,13 @@ size_t grkv_workspace_bytes(const grkv_problem* prob, int64_t n,
  *   score    float  [U][P]      SnapKV score s_j = sum_r A[r][j]
  *   pooled   float  [U][P]      pooled score p_j
  *   fixed    uint8  [U][c]      1 where the retained slot is fixed
- *   x        float  [U][mp][c]  X, window attention over the retained keys
  *   resid    float  [U][mp][d]  R = Y - X V0
  *   gram     float  [U][mp][mp] N = X_G X_G^T + lambda I (padding rows: identity)
  *   z        float  [U][d][mp]  Z^T, Z = N^-1 R
  * Returns GRKV_OK, or GRKV_ERR_INVALID / GRKV_ERR_UNSUPPORTED like
  * grkv_compress. */
 typedef struct {
-  size_t lse, y, score, pooled, fixed, x, resid, gram, z;
+  size_t lse, y, score, pooled, fixed, resid, gram, z;
   size_t total;
 } grkv_layout;
 

@@ -59,7 +59,7 @@ class Outputs(ctypes.Structure):
 
 class Layout(ctypes.Structure):
     _fields_ = [(f, ctypes.c_size_t) for f in
-                ("lse", "y", "score", "pooled", "fixed", "x", "resid", "gram", "z", "total")]
+                ("lse", "y", "score", "pooled", "fixed", "resid", "gram", "z", "total")]
 
 
 _LIB = None
@@ -206,7 +206,6 @@ def intermediates(res: Result) -> dict:
         "score": view(lay.score, torch.float32, (U, P)),
         "pooled": view(lay.pooled, torch.float32, (U, P)),
         "fixed": view(lay.fixed, torch.uint8, (U, c)),
-        "x": view(lay.x, torch.float32, (U, mp, c))[:, :m],
         "resid": view(lay.resid, torch.float32, (U, mp, d))[:, :m],
         "gram": view(lay.gram, torch.float32, (U, mp, mp))[:, :m, :m],
         "z": view(lay.z, torch.float32, (U, d, mp))[:, :, :m],

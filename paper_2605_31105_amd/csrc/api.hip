@@ -68,7 +68,14 @@ int make_plan(const grkv_problem* prob, int64_t n, int32_t window, int32_t budge
   const int64_t want = ceil_div(512, p->U);
   split_range(n, want, 512, &p->S1, &p->chunk1);
   split_range(budget, want, 128, &p->S2, &p->chunk2);
-  split_range(budget, ceil_div(256, p->U), 256, &p->S3, &p->chunk3);
+  if (p->chunk2 > 8192) split_range(budget, ceil_div(budget, 8192), 128, &p->S2, &p->chunk2);
+  p->fast_merge = merge_fast_supported(*p);
+  if (p->fast_merge) {
+    p->S3 = p->S2;
+    p->chunk3 = p->chunk2;
+  } else {
+    split_range(budget, ceil_div(256, p->U), 256, &p->S3, &p->chunk3);
+  }
 
   const size_t U = p->U, mp = p->mp, d = p->d, c = budget, P = p->prefix;
   const size_t esz = p->dtype == GRKV_BF16 ? 2 : 4;
@@ -89,7 +96,7 @@ int make_plan(const grkv_problem* prob, int64_t n, int32_t window, int32_t budge
   p->lse2 = take(U * mp * sizeof(double));
   p->lse2_log2 = take(U * mp * sizeof(float));
   p->xvpart = take(U * p->S2 * mp * d * sizeof(float));
-  p->x = take(U * mp * c * sizeof(float));
+  p->x = take(p->fast_merge ? 0 : U * mp * c * sizeof(float));   // generic path only
   p->resid = take(U * mp * d * sizeof(float));
   p->npart = take(U * p->S3 * mp * mp * sizeof(float));
   p->gram = take(U * mp * mp * sizeof(float));
@@ -143,7 +150,6 @@ int grkv_workspace_layout(const grkv_problem* prob, int64_t n, int32_t window, i
   layout->score = p.colsum;
   layout->pooled = p.pooled;
   layout->fixed = p.fixed;
-  layout->x = p.x;
   layout->resid = p.resid;
   layout->gram = p.gram;
   layout->z = p.z;
@@ -183,8 +189,8 @@ int grkv_compress(const void* q_obs, const void* K, const void* V, int64_t n, in
   full.ypart = F(p.ypart); full.colsum = p.prefix > 0 ? F(p.colsum) : nullptr;
   full.prefix = p.prefix; full.xout = nullptr; full.split_p = true;
   const bool fast = stream_supported(p);
-  auto pass_a = [&](const AttnPass& a) { return fast ? launch_stream(p, a, false, s) : launch_lse_pass(p, a, s); };
-  auto pass_b = [&](const AttnPass& a) { return fast ? launch_stream(p, a, true, s) : launch_prob_pass(p, a, s); };
+  auto pass_a = [&](const AttnPass& a) { return fast ? launch_stream(p, a, 0, s) : launch_lse_pass(p, a, s); };
+  auto pass_b = [&](const AttnPass& a) { return fast ? launch_stream(p, a, 1, s) : launch_prob_pass(p, a, s); };
   GRKV_STAGE(GRKV_STAGE_FULL_LSE, pass_a(full));
   GRKV_STAGE(GRKV_STAGE_FULL_LSE_COMBINE,
              launch_lse_combine(p, full.pmax, full.psum, p.S1, Dd(p.lse1), F(p.lse1_log2), s));
@@ -193,7 +199,7 @@ int grkv_compress(const void* q_obs, const void* K, const void* V, int64_t n, in
   // 2. pooled top-k retention and the fixed set; gather K0, V0
   uint8_t* fixed = (uint8_t*)(ws + p.fixed);
   GRKV_STAGE(GRKV_STAGE_SELECT, launch_select(p, F(p.colsum), F(p.pooled), out->idx, fixed, s));
-  const bool fast_merge = merge_fast_supported(p);
+  const bool fast_merge = p.fast_merge;
   GRKV_STAGE(GRKV_STAGE_GATHER, launch_gather(p, K, V, out->idx, out->k_out, ws + p.v0c,
                                               fast_merge ? nullptr : out->v_out, s));
   // 3. window attention over the retained cache: X and X V0, then R = Y - X V0
@@ -202,22 +208,27 @@ int grkv_compress(const void* q_obs, const void* K, const void* V, int64_t n, in
   ret.S = p.S2; ret.chunk = p.chunk2;
   ret.pmax = F(p.pmax2); ret.psum = Dd(p.psum2);
   ret.lse = Dd(p.lse2); ret.lse_log2 = F(p.lse2_log2);
-  ret.ypart = F(p.xvpart); ret.colsum = nullptr; ret.prefix = 0; ret.xout = F(p.x);
+  ret.ypart = F(p.xvpart); ret.colsum = nullptr; ret.prefix = 0;
+  ret.xout = fast_merge ? nullptr : F(p.x);
   ret.split_p = true;
+  ret.fixed = fixed; ret.npart = F(p.npart);
   GRKV_STAGE(GRKV_STAGE_RET_LSE, pass_a(ret));
   GRKV_STAGE(GRKV_STAGE_RET_LSE_COMBINE,
              launch_lse_combine(p, ret.pmax, ret.psum, p.S2, Dd(p.lse2), F(p.lse2_log2), s));
-  GRKV_STAGE(GRKV_STAGE_RET_PROB, pass_b(ret));
+  // the generic value step needs X itself, which only the generic pass writes
+  GRKV_STAGE(GRKV_STAGE_RET_PROB,
+             fast_merge ? launch_stream(p, ret, 2, s) : launch_prob_pass(p, ret, s));
   GRKV_STAGE(GRKV_STAGE_RESID, launch_combine_rows(p, F(p.xvpart), p.S2, F(p.y), F(p.resid), s));
   // 4. value step: N, Cholesky solve for Z, V* = V0 + X_G^T Z
-  GRKV_STAGE(GRKV_STAGE_GRAM, launch_gram(p, F(p.x), fixed, F(p.npart), s));
+  if (!fast_merge) GRKV_STAGE(GRKV_STAGE_GRAM, launch_gram(p, F(p.x), fixed, F(p.npart), s));
   if (fast_merge) {
     GRKV_STAGE(GRKV_STAGE_SOLVE,
                launch_solve(p, F(p.npart), F(p.y), F(p.resid), F(p.gram), F(p.z),
                             (uint16_t*)(ws + p.zhi), (uint16_t*)(ws + p.zlo), F(p.stats_ws),
                             out->stats, s));
     GRKV_STAGE(GRKV_STAGE_UPDATE,
-               launch_update(p, F(p.x), fixed, (const uint16_t*)(ws + p.zhi),
+               launch_update(p, q_obs, out->k_out, F(p.lse2_log2), fixed,
+                             (const uint16_t*)(ws + p.zhi),
                              (const uint16_t*)(ws + p.zlo), F(p.stats_ws),
                              (const uint16_t*)(ws + p.v0c), out->v_out, s));
   } else {

@@ -26,8 +26,10 @@ struct Plan {
   int S1, chunk1;
   // retained-cache passes over the c retained keys
   int S2, chunk2;
-  // Gram-matrix splits over the c retained columns
+  // Gram-matrix splits over the c retained columns (the retained-pass splits
+  // on the fast value-step path, where that pass produces the Gram partials)
   int S3, chunk3;
+  bool fast_merge;
   // workspace offsets (bytes)
   size_t pmax1, psum1, lse1, lse1_log2, ypart, y, colsum, pooled, fixed, v0c;
   size_t pmax2, psum2, lse2, lse2_log2, xvpart, x, resid, npart, gram, z, zhi, zlo, stats_ws;
@@ -54,8 +56,10 @@ struct AttnPass {
   float* ypart;        // pass B out [U][S][mp][d]
   float* colsum;       // pass B out [U][prefix] column sums over rows, or null
   int prefix;          // only keys < prefix get a column sum
-  float* xout;         // pass B out [U][mp][nk] probabilities, or null
+  float* xout;         // pass B out [U][mp][nk] probabilities, or null (generic path)
   bool split_p;        // P.V with P as a bf16 hi+lo pair (else bf16 P)
+  const uint8_t* fixed; // retained pass B (fast path): fixed flags [U][nk]
+  float* npart;        // retained pass B (fast path): Gram partials [U][S][mp][mp]
 };
 
 hipError_t launch_lse_pass(const Plan& p, const AttnPass& a, hipStream_t s);
@@ -68,8 +72,10 @@ hipError_t launch_combine_rows(const Plan& p, const float* part, int S,
                                const float* base, float* out, hipStream_t s);
 
 // bf16 streaming passes (direct-to-LDS ring); used when stream_supported().
+// mode 0: pass A; 1: full-cache pass B (column sums); 2: retained pass B with
+// the Gram partials of the fixed-masked probabilities (needs mp <= 128).
 bool stream_supported(const Plan& p);
-hipError_t launch_stream(const Plan& p, const AttnPass& a, bool pass_b, hipStream_t s);
+hipError_t launch_stream(const Plan& p, const AttnPass& a, int mode, hipStream_t s);
 
 hipError_t launch_select(const Plan& p, const float* colsum, float* pooled,
                          int32_t* idx, uint8_t* fixed, hipStream_t s);
@@ -87,7 +93,9 @@ hipError_t launch_solve(const Plan& p, const float* npart, const float* y,
                         const float* resid, float* gram, float* z, uint16_t* zhi,
                         uint16_t* zlo, float* stats_ws, float* stats_user,
                         hipStream_t s);
-hipError_t launch_update(const Plan& p, const float* x, const uint8_t* fixed,
+// X is recomputed from q_obs, K0 (k_out) and the retained log-sum-exp.
+hipError_t launch_update(const Plan& p, const void* q, const void* k0,
+                         const float* lse_log2, const uint8_t* fixed,
                          const uint16_t* zhi, const uint16_t* zlo,
                          const float* stats_ws, const uint16_t* v0c, float* v_out,
                          hipStream_t s);

@@ -3,6 +3,8 @@
 //   N = X_G X_G^T + lambda I_m   (gram: partial sums over column splits)
 //   Z = N^-1 R                   (solve: elimination in registers and LDS)
 //   V*_G = V0_G + X_G^T Z        (update: fixed columns keep V0)
+// On this fast path the Gram partials come from the retained-cache pass
+// (stream.hip); the gram kernel here serves the generic path.
 // X_G is X with the fixed columns zeroed.  The fp32 operands of the two
 // products go through the bf16 MFMA as hi+lo pairs (three products per tile),
 // which keeps about 16 significant bits per term; accumulation is fp32.
@@ -271,64 +273,130 @@ __global__ __launch_bounds__(MP / 32 * 256) void solve_kernel(
 }
 
 // ---------------------------------------------------------------- update ----
-// v_out = V0 + X_G^T Z for 64 retained slots per block (fixed slots and units
-// with a singular system get V0).  X_G^T is staged transposed in LDS as bf16
-// hi/lo; Z^T arrives pre-split from the solve.
+// v_out = V0 + X_G^T Z for 256 retained slots per block (fixed slots, and every
+// slot of a unit whose system was singular, get V0).  X is recomputed from the
+// window queries, K0 and the retained-set log-sum-exp rather than stored:
+// S = Q K0^T on the MFMA leaves each lane holding eight rows (two groups of
+// four) of one key's column, which is exactly the A operand of X_G^T Z with
+// the rows as the contraction index; Z^T arrives as bf16 hi/lo from the solve.
+// Q and Z^T are staged in LDS once per block.
 template <int MP, int D>
-__global__ __launch_bounds__(256) void update_kernel(const float* x, const uint8_t* fixed,
+__global__ __launch_bounds__(256) void update_kernel(const u16* q, const u16* k0,
+                                                     const float* lse_log2, const uint8_t* fixed,
                                                      const u16* zhi, const u16* zlo,
                                                      const float* stats_ws, const u16* v0c,
-                                                     float* v_out, int c) {
-  constexpr int XS = MP + 8;   // LDS row stride (bf16) of X_G^T rows
-  __shared__ __attribute__((aligned(16))) u16 xh[64 * XS];
-  __shared__ __attribute__((aligned(16))) u16 xl[64 * XS];
-  const int u = blockIdx.y, t0 = blockIdx.x * 64;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l16 = lane & 15, g = lane >> 4;
+                                                     float* v_out, int m, int w, int c,
+                                                     int causal, float scale_log2) {
+  constexpr int QS = D + 8;    // LDS row stride (bf16) of Q rows
+  constexpr int ZS = MP + 8;   // LDS row stride (bf16) of Z^T rows
+  extern __shared__ __attribute__((aligned(16))) u16 sm[];
+  u16* qs = sm;                  // [MP][QS]
+  u16* zh = qs + MP * QS;        // [D][ZS]
+  u16* zl = zh + D * ZS;         // [D][ZS]
+  const int u = blockIdx.y, tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6, l16 = lane & 15, g = lane >> 4;
   const bool singular = stats_ws[u * 4 + 3] != 0.f;
-  const float* xu = x + (size_t)u * MP * c;
   const uint8_t* fu = fixed + (size_t)u * c;
+  const int win0 = c - w;   // first window slot of the retained set
 
-  f32x4 acc[D / 16];
-#pragma unroll
-  for (int dt = 0; dt < D / 16; ++dt) acc[dt] = zero4();
   if (!singular) {
-    for (int e = tid; e < MP * 64; e += 256) {
-      const int r = e / 64, tt = e % 64, t = t0 + tt;
-      const float xv = (t < c && !fu[t]) ? xu[(size_t)r * c + t] : 0.f;
-      const __bf16 h = (__bf16)xv;
-      xh[tt * XS + r] = __builtin_bit_cast(u16, h);
-      xl[tt * XS + r] = __builtin_bit_cast(u16, (__bf16)(xv - (float)h));
+    const u16* qu = q + (size_t)u * m * D;
+    for (int e = tid; e < MP * (D / 8); e += 256) {
+      const int r = e / (D / 8), ch = e % (D / 8);
+      const uint4 v = r < m ? *reinterpret_cast<const uint4*>(qu + (size_t)r * D + ch * 8)
+                            : make_uint4(0, 0, 0, 0);
+      *reinterpret_cast<uint4*>(qs + r * QS + ch * 8) = v;
+    }
+    const u16* zhu = zhi + (size_t)u * D * MP;
+    const u16* zlu = zlo + (size_t)u * D * MP;
+    for (int e = tid; e < D * (MP / 8); e += 256) {
+      const int r = e / (MP / 8), ch = e % (MP / 8);
+      *reinterpret_cast<uint4*>(zh + r * ZS + ch * 8) =
+          *reinterpret_cast<const uint4*>(zhu + (size_t)r * MP + ch * 8);
+      *reinterpret_cast<uint4*>(zl + r * ZS + ch * 8) =
+          *reinterpret_cast<const uint4*>(zlu + (size_t)r * MP + ch * 8);
     }
     __syncthreads();
-    const u16* zh = zhi + (size_t)u * D * MP;
-    const u16* zl = zlo + (size_t)u * D * MP;
+  }
+  float lse[MP / 16][4];
+  bool rowok[MP / 16][4];
+  int rowwin[MP / 16][4];
 #pragma unroll
-    for (int ks = 0; ks < MP / 32; ++ks) {
-      const int tt = wave * 16 + l16;
-      const bf16x8 ah = as_bf16x8(*reinterpret_cast<const uint4*>(&xh[tt * XS + ks * 32 + 8 * g]));
-      const bf16x8 al = as_bf16x8(*reinterpret_cast<const uint4*>(&xl[tt * XS + ks * 32 + 8 * g]));
+  for (int rt = 0; rt < MP / 16; ++rt)
 #pragma unroll
-      for (int dt = 0; dt < D / 16; ++dt) {
-        const size_t zo = (size_t)(dt * 16 + l16) * MP + ks * 32 + 8 * g;
-        const bf16x8 bh = as_bf16x8(*reinterpret_cast<const uint4*>(zh + zo));
-        const bf16x8 bl = as_bf16x8(*reinterpret_cast<const uint4*>(zl + zo));
-        acc[dt] = mfma_bf16(ah, bh, acc[dt]);
-        acc[dt] = mfma_bf16(ah, bl, acc[dt]);
-        acc[dt] = mfma_bf16(al, bh, acc[dt]);
+    for (int i = 0; i < 4; ++i) {
+      const int row = rt * 16 + 4 * g + i;
+      lse[rt][i] = lse_log2[(size_t)u * MP + row];
+      rowok[rt][i] = row < m;
+      rowwin[rt][i] = causal ? row % w : 0x3fffffff;
+    }
+
+  for (int kt = 0; kt < 4; ++kt) {
+    const int tbase = blockIdx.x * 256 + (kt * 4 + wave) * 16;   // this wave's 16 slots
+    if (tbase >= c) break;
+    const int t = tbase + l16;   // the slot whose column this lane holds
+    f32x4 acc[D / 16];
+#pragma unroll
+    for (int dt = 0; dt < D / 16; ++dt) acc[dt] = zero4();
+    const bool tok = t < c;
+    const bool free_slot = tok && !fu[t];
+    if (!singular) {
+      // K0 rows as the B operand of S = Q K0^T: lane holds K0[t][32ks + 8g .. +8]
+      uint4 kb[D / 32];
+      const u16* kr = k0 + ((size_t)u * c + (tok ? t : c - 1)) * D;
+#pragma unroll
+      for (int ks = 0; ks < D / 32; ++ks) kb[ks] = *reinterpret_cast<const uint4*>(kr + ks * 32 + 8 * g);
+      const int tw = t - win0;   // window index of slot t (< 0 outside the window)
+#pragma unroll
+      for (int rp = 0; rp < MP / 32; ++rp) {
+        float x8[8];
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int rt = 2 * rp + h;
+          f32x4 st = zero4();
+#pragma unroll
+          for (int ks = 0; ks < D / 32; ++ks) {
+            const bf16x8 qa = as_bf16x8(*reinterpret_cast<const uint4*>(qs + (rt * 16 + l16) * QS + ks * 32 + 8 * g));
+            st = mfma_bf16(qa, as_bf16x8(kb[ks]), st);
+          }
+          // st[i] = q_row . k_t for row = 16rt + 4g + i
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const bool ok = free_slot && rowok[rt][i] && tw <= rowwin[rt][i];
+            x8[4 * h + i] = ok ? exp2f(fmaf(st[i], scale_log2, -lse[rt][i])) : 0.f;
+          }
+        }
+        bf16x8 ah, al;
+        split8(x8, ah, al);
+        // Z rows {32rp + 4g + i, 32rp + 16 + 4g + i}, column dd = 16dt + l16
+#pragma unroll
+        for (int dt = 0; dt < D / 16; ++dt) {
+          const u16* zr = zh + (dt * 16 + l16) * ZS + 32 * rp + 4 * g;
+          const u16* zr2 = zl + (dt * 16 + l16) * ZS + 32 * rp + 4 * g;
+          const uint2 h0 = *reinterpret_cast<const uint2*>(zr);
+          const uint2 h1 = *reinterpret_cast<const uint2*>(zr + 16);
+          const uint2 l0 = *reinterpret_cast<const uint2*>(zr2);
+          const uint2 l1 = *reinterpret_cast<const uint2*>(zr2 + 16);
+          const bf16x8 bh = as_bf16x8(make_uint4(h0.x, h0.y, h1.x, h1.y));
+          const bf16x8 bl = as_bf16x8(make_uint4(l0.x, l0.y, l1.x, l1.y));
+          acc[dt] = mfma_bf16(ah, bh, acc[dt]);
+          acc[dt] = mfma_bf16(ah, bl, acc[dt]);
+          acc[dt] = mfma_bf16(al, bh, acc[dt]);
+        }
       }
     }
-  }
-  // lane holds dV[t = t0 + 16*wave + 4g + i][dd = 16dt + l16]
+    // lane holds dV[slot = tbase + 4g + i][dd = 16dt + l16]
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int t = t0 + wave * 16 + 4 * g + i;
-    if (t >= c) continue;
-    const bool upd = !singular && !fu[t];
+    for (int i = 0; i < 4; ++i) {
+      const int ts = tbase + 4 * g + i;
+      if (ts >= c) continue;
+      const bool upd = !singular && !fu[ts];
 #pragma unroll
-    for (int dt = 0; dt < D / 16; ++dt) {
-      const size_t o = ((size_t)u * c + t) * D + dt * 16 + l16;
-      const float v0 = bf16_to_f32(v0c[o]);
-      v_out[o] = upd ? v0 + acc[dt][i] : v0;
+      for (int dt = 0; dt < D / 16; ++dt) {
+        const size_t o = ((size_t)u * c + ts) * D + dt * 16 + l16;
+        const float v0 = bf16_to_f32(v0c[o]);
+        v_out[o] = upd ? v0 + acc[dt][i] : v0;
+      }
     }
   }
 }
@@ -351,11 +419,17 @@ hipError_t launch_solve_t(const Plan& p, const float* npart, const float* y, con
 }
 
 template <int MP, int D>
-hipError_t launch_update_t(const Plan& p, const float* x, const uint8_t* fixed, const u16* zhi,
-                           const u16* zlo, const float* stats_ws, const u16* v0c, float* v_out,
-                           hipStream_t s) {
-  hipLaunchKernelGGL((update_kernel<MP, D>), dim3((p.c + 63) / 64, p.U), dim3(256), 0, s, x, fixed,
-                     zhi, zlo, stats_ws, v0c, v_out, p.c);
+hipError_t launch_update_t(const Plan& p, const void* q, const void* k0, const float* lse_log2,
+                           const uint8_t* fixed, const u16* zhi, const u16* zlo,
+                           const float* stats_ws, const u16* v0c, float* v_out, hipStream_t s) {
+  const size_t lds = ((size_t)MP * (D + 8) + 2 * (size_t)D * (MP + 8)) * sizeof(u16);
+  hipError_t e = hipFuncSetAttribute((const void*)update_kernel<MP, D>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  const float scale_log2 = (float)(1.4426950408889634 / __builtin_sqrt((double)D));
+  hipLaunchKernelGGL((update_kernel<MP, D>), dim3((p.c + 255) / 256, p.U), dim3(256), lds, s,
+                     (const u16*)q, (const u16*)k0, lse_log2, fixed, zhi, zlo, stats_ws, v0c,
+                     v_out, p.m, p.w, p.c, p.opt.causal_window ? 1 : 0, scale_log2);
   return hipGetLastError();
 }
 
@@ -388,12 +462,12 @@ hipError_t launch_solve(const Plan& p, const float* npart, const float* y, const
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_update(const Plan& p, const float* x, const uint8_t* fixed, const u16* zhi,
-                         const u16* zlo, const float* stats_ws, const u16* v0c, float* v_out,
-                         hipStream_t s) {
+hipError_t launch_update(const Plan& p, const void* q, const void* k0, const float* lse_log2,
+                         const uint8_t* fixed, const u16* zhi, const u16* zlo,
+                         const float* stats_ws, const u16* v0c, float* v_out, hipStream_t s) {
 #define GRKV_UPD(MPV, DV)                                                                     \
   if (p.mp == MPV && p.d == DV)                                                               \
-    return launch_update_t<MPV, DV>(p, x, fixed, zhi, zlo, stats_ws, v0c, v_out, s);
+    return launch_update_t<MPV, DV>(p, q, k0, lse_log2, fixed, zhi, zlo, stats_ws, v0c, v_out, s);
   GRKV_UPD(32, 64) GRKV_UPD(32, 128) GRKV_UPD(64, 64) GRKV_UPD(64, 128)
   GRKV_UPD(128, 64) GRKV_UPD(128, 128)
 #undef GRKV_UPD

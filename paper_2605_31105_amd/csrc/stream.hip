@@ -49,7 +49,8 @@ struct StreamK {
   float* ypart;
   float* colsum;
   int prefix;
-  float* xout;
+  const uint8_t* fixed;   // retained pass: fixed flag per retained slot
+  float* npart;           // retained pass: Gram partials [U][S][mp][mp]
 };
 
 constexpr int kTileElems = 4096;   // elements of one tensor per tile
@@ -109,8 +110,13 @@ __device__ __forceinline__ void load_tile(const u16* base, int tile0, int key_en
   }
 }
 
+// Kernel modes: pass A (log-sum-exp partials), pass B over the full cache
+// (P.V partials and SnapKV column sums), pass B over the retained set (P.V
+// partials and the Gram matrix X_G X_G^T of the fixed-masked probabilities).
+enum { kModeLse = 0, kModeFull = 1, kModeRetained = 2 };
+
 // Per-block state of one (unit, split) stream.
-template <int D, bool PASS_B>
+template <int D, int MODE, int NT>
 struct State {
   uint4 qb[2][D / 32];
   int rowwin[2];
@@ -118,13 +124,15 @@ struct State {
   float lse[2];
   float mrun[2];   // pass A: per-lane running max of this lane's keys
   double srun[2];  // pass A: per-lane running sum of 2^(t - mrun)
-  f32x4 y[2][PASS_B ? D / 16 : 1];
+  f32x4 y[2][MODE != kModeLse ? D / 16 : 1];
+  f32x4 n[2][MODE == kModeRetained ? NT : 1];   // Gram rows of this wave
 };
 
-template <int D, int WAVES, bool PASS_B, int NSTAGE>
+template <int D, int WAVES, int MODE, int NSTAGE>
 struct Stream {
   using G = Geo<D>;
-  static constexpr int TK = G::TK, NKT = G::NKT;
+  static constexpr bool PASS_B = MODE != kModeLse;
+  static constexpr int TK = G::TK, NKT = G::NKT, NT = 2 * WAVES;
   static constexpr int LOADS = (G::INSTR / WAVES) * (PASS_B ? 2 : 1);  // per thread per tile
 
   const StreamK& a;
@@ -132,6 +140,8 @@ struct Stream {
   const u16* vbase;
   int u, key0, key_end, ntiles, win0, lane, wave, l16, g;
   float (*colpart)[WAVES][TK];
+  uint4* xg;                 // retained pass: [2][NT][2][64] fragment exchange
+  const uint8_t* fixs;       // retained pass: fixed flags of this split (LDS)
 
   __device__ __forceinline__ void issue(int t, char* stage) {
     if (t < ntiles) {
@@ -153,15 +163,53 @@ struct Stream {
     }
   }
 
+  // Gram contribution of 32 keys (16-key tiles 2kp, 2kp+1): this wave's
+  // X_G fragments (hi/lo) go to LDS, then every wave multiplies its two row
+  // tiles by all NT row tiles.  X_G is P with fixed slots zeroed.
+  __device__ __forceinline__ void gram_step(int t, int kp, const float (&pv)[NKT][2][4],
+                                            State<D, MODE, NT>& S) {
+    const int buf = (t * (NKT / 2) + kp) & 1;
+    uint4* xb = xg + buf * NT * 2 * 64;
+    const int tl = t * TK;   // key offset of this tile inside the split
+    bf16x8 fh[2], fl[2];
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt) {
+      float x8[8];
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int kl = tl + (2 * kp + h) * 16 + 4 * g + i;   // slot offset in the split
+          x8[4 * h + i] = fixs[kl] ? 0.f : pv[2 * kp + h][rt][i];
+        }
+      split8(x8, fh[rt], fl[rt]);
+      xb[((2 * wave + rt) * 2 + 0) * 64 + lane] = __builtin_bit_cast(uint4, fh[rt]);
+      xb[((2 * wave + rt) * 2 + 1) * 64 + lane] = __builtin_bit_cast(uint4, fl[rt]);
+    }
+    lds_barrier();
+#pragma unroll
+    for (int bt = 0; bt < NT; ++bt) {
+      const bf16x8 bh = __builtin_bit_cast(bf16x8, xb[(bt * 2 + 0) * 64 + lane]);
+      const bf16x8 bl = __builtin_bit_cast(bf16x8, xb[(bt * 2 + 1) * 64 + lane]);
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt) {
+        S.n[rt][bt] = mfma_bf16(fh[rt], bh, S.n[rt][bt]);
+        S.n[rt][bt] = mfma_bf16(fh[rt], bl, S.n[rt][bt]);
+        S.n[rt][bt] = mfma_bf16(fl[rt], bh, S.n[rt][bt]);
+      }
+    }
+  }
+
   // One tile: wait for it, refill the stage freed last step, compute.
-  __device__ __forceinline__ void step(int t, const char* cur, char* refill, State<D, PASS_B>& S) {
+  __device__ __forceinline__ void step(int t, const char* cur, char* refill,
+                                       State<D, MODE, NT>& S) {
     if (t >= ntiles) return;
     const int ahead = min(ntiles - 1 - t, NSTAGE - 2);
     if (ahead >= 2) wait_vmcnt<2 * LOADS>();
     else if (ahead == 1) wait_vmcnt<LOADS>();
     else wait_vmcnt<0>();
     lds_barrier();
-    if (PASS_B && a.colsum && t > 0) flush_colsum(t - 1);
+    if (MODE == kModeFull && a.colsum && t > 0) flush_colsum(t - 1);
     issue(t + NSTAGE - 1, refill);
 
     const int tile0 = key0 + t * TK;
@@ -227,7 +275,7 @@ struct Stream {
 #pragma unroll
         for (int i = 0; i < 4; ++i)
           pv[kt][rt][i] = ok[kt][rt][i] ? exp2f(fmaf(st[kt][rt][i], a.scale_log2, -S.lse[rt])) : 0.f;
-    if (a.colsum) {
+    if (MODE == kModeFull && a.colsum) {
 #pragma unroll
       for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
@@ -235,20 +283,6 @@ struct Stream {
           const float c = sum16_dpp(pv[kt][0][i] + pv[kt][1][i]);
           if (l16 == 0) colpart[t & 1][wave][kt * 16 + 4 * g + i] = c;
         }
-    }
-    if (a.xout) {
-#pragma unroll
-      for (int rt = 0; rt < 2; ++rt) {
-        const int row = wave * kRowsPerWave + rt * 16 + l16;
-        float* xr = a.xout + ((size_t)u * a.mp + row) * a.nk;
-#pragma unroll
-        for (int kt = 0; kt < NKT; ++kt) {
-          const int key = tile0 + kt * 16 + 4 * g;
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            if (key + i < key_end) xr[key + i] = pv[kt][rt][i];
-        }
-      }
     }
     const char* vt = cur + kTileBytes;
     const int e = l16 >> 2, qq = l16 & 3;
@@ -282,14 +316,16 @@ struct Stream {
           S.y[rt][dt] = mfma_bf16(ahi[rt], b[dt], S.y[rt][dt]);
           S.y[rt][dt] = mfma_bf16(alo[rt], b[dt], S.y[rt][dt]);
         }
+      if (MODE == kModeRetained) gram_step(t, kp, pv, S);
     }
   }
 };
 
-template <int D, int WAVES, bool PASS_B>
+template <int D, int WAVES, int MODE>
 __global__ __launch_bounds__(WAVES * 64) void stream_kernel(StreamK a) {
   using G = Geo<D>;
-  constexpr int TK = G::TK;
+  constexpr bool PASS_B = MODE != kModeLse;
+  constexpr int TK = G::TK, NT = 2 * WAVES;
   constexpr int NSTAGE = PASS_B ? 3 : 4;
   constexpr int STAGE_BYTES = kTileBytes * (PASS_B ? 2 : 1);
   __shared__ __attribute__((aligned(16))) char stg0[STAGE_BYTES];
@@ -297,8 +333,9 @@ __global__ __launch_bounds__(WAVES * 64) void stream_kernel(StreamK a) {
   __shared__ __attribute__((aligned(16))) char stg2[STAGE_BYTES];
   __shared__ __attribute__((aligned(16))) char stg3[PASS_B ? 16 : STAGE_BYTES];
   __shared__ float colpart[2][WAVES][TK];
+  extern __shared__ __attribute__((aligned(16))) uint4 dyn[];   // retained pass only
 
-  Stream<D, WAVES, PASS_B, NSTAGE> sm{a};
+  Stream<D, WAVES, MODE, NSTAGE> sm{a};
   sm.u = blockIdx.y;
   const int s = blockIdx.x;
   sm.lane = threadIdx.x & 63;
@@ -312,9 +349,22 @@ __global__ __launch_bounds__(WAVES * 64) void stream_kernel(StreamK a) {
   sm.vbase = a.v + (size_t)sm.u * a.nk * D;
   sm.win0 = a.nk - a.w;
   sm.colpart = colpart;
+  sm.xg = dyn;
+  sm.fixs = reinterpret_cast<const uint8_t*>(dyn + 2 * NT * 2 * 64);
   const int u = sm.u, wave = sm.wave, l16 = sm.l16, g = sm.g;
 
-  State<D, PASS_B> S;
+  if (MODE == kModeRetained) {
+    // fixed flags of this split's slots (padded with "fixed" past the end)
+    uint8_t* fl = reinterpret_cast<uint8_t*>(dyn + 2 * NT * 2 * 64);
+    const int nsl = sm.ntiles * TK;
+    for (int i = threadIdx.x; i < nsl; i += WAVES * 64) {
+      const int key = sm.key0 + i;
+      fl[i] = key < sm.key_end ? a.fixed[(size_t)u * a.nk + key] : 1;
+    }
+    __syncthreads();
+  }
+
+  State<D, MODE, NT> S;
 #pragma unroll
   for (int rt = 0; rt < 2; ++rt) {
     const int row = wave * kRowsPerWave + rt * 16 + l16;
@@ -330,6 +380,8 @@ __global__ __launch_bounds__(WAVES * 64) void stream_kernel(StreamK a) {
     S.srun[rt] = 0.0;
 #pragma unroll
     for (int dt = 0; dt < (PASS_B ? D / 16 : 1); ++dt) S.y[rt][dt] = zero4();
+#pragma unroll
+    for (int bt = 0; bt < (MODE == kModeRetained ? NT : 1); ++bt) S.n[rt][bt] = zero4();
   }
 
   sm.issue(0, stg0);
@@ -348,13 +400,12 @@ __global__ __launch_bounds__(WAVES * 64) void stream_kernel(StreamK a) {
     }
   }
 
-  const int s_idx = s;
   if (PASS_B) {
-    if (a.colsum && sm.ntiles > 0) {
+    if (MODE == kModeFull && a.colsum && sm.ntiles > 0) {
       lds_barrier();
       sm.flush_colsum(sm.ntiles - 1);
     }
-    float* yp = a.ypart + ((size_t)u * a.S + s_idx) * a.mp * D;
+    float* yp = a.ypart + ((size_t)u * a.S + s) * a.mp * D;
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
@@ -364,6 +415,18 @@ __global__ __launch_bounds__(WAVES * 64) void stream_kernel(StreamK a) {
           const int row = wave * kRowsPerWave + rt * 16 + 4 * g + i;
           yp[(size_t)row * D + dt * 16 + l16] = S.y[rt][dt][i];
         }
+    if (MODE == kModeRetained) {
+      float* np = a.npart + ((size_t)u * a.S + s) * a.mp * a.mp;
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+        for (int bt = 0; bt < (MODE == kModeRetained ? NT : 1); ++bt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int row = wave * kRowsPerWave + rt * 16 + 4 * g + i;
+            np[(size_t)row * a.mp + bt * 16 + l16] = S.n[rt][bt][i];
+          }
+    }
   } else {
     // merge the four lanes of each row: M = max m_g, sum = sum_g s_g 2^(m_g - M)
 #pragma unroll
@@ -373,7 +436,7 @@ __global__ __launch_bounds__(WAVES * 64) void stream_kernel(StreamK a) {
       const double tot = sum_over_groups(part);
       const int row = wave * kRowsPerWave + rt * 16 + l16;
       if (g == 0) {
-        const size_t o = ((size_t)u * a.S + s_idx) * a.mp + row;
+        const size_t o = ((size_t)u * a.S + s) * a.mp + row;
         a.pmax[o] = M;
         a.psum[o] = M == -INFINITY ? 0.0 : tot;
       }
@@ -381,7 +444,7 @@ __global__ __launch_bounds__(WAVES * 64) void stream_kernel(StreamK a) {
   }
 }
 
-template <int D, int WAVES, bool PASS_B>
+template <int D, int WAVES, int MODE>
 hipError_t launch_stream_t(const Plan& p, const AttnPass& a, hipStream_t s) {
   StreamK k;
   k.q = (const u16*)a.q; k.k = (const u16*)a.k; k.v = (const u16*)a.v;
@@ -389,20 +452,40 @@ hipError_t launch_stream_t(const Plan& p, const AttnPass& a, hipStream_t s) {
   k.nk = a.nk; k.S = a.S; k.chunk = a.chunk;
   k.scale_log2 = (float)(1.4426950408889634 / __builtin_sqrt((double)D));
   k.pmax = a.pmax; k.psum = a.psum; k.lse_log2 = a.lse_log2;
-  k.ypart = a.ypart; k.colsum = a.colsum; k.prefix = a.prefix; k.xout = a.xout;
-  hipLaunchKernelGGL((stream_kernel<D, WAVES, PASS_B>), dim3(a.S, p.U), dim3(WAVES * 64), 0, s, k);
+  k.ypart = a.ypart; k.colsum = a.colsum; k.prefix = a.prefix;
+  k.fixed = a.fixed; k.npart = a.npart;
+  size_t dyn = 0;
+  if (MODE == kModeRetained) {
+    const int tk = kTileElems / D;
+    const size_t slots = (size_t)((a.chunk + tk - 1) / tk) * tk;
+    dyn = (size_t)2 * (2 * WAVES) * 2 * 64 * sizeof(uint4) + ((slots + 15) & ~(size_t)15);
+    hipError_t e = hipFuncSetAttribute((const void*)stream_kernel<D, WAVES, MODE>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL((stream_kernel<D, WAVES, MODE>), dim3(a.S, p.U), dim3(WAVES * 64), dyn, s, k);
   return hipGetLastError();
 }
 
-template <int D, bool PASS_B>
+template <int D, int MODE>
 hipError_t launch_stream_w(const Plan& p, const AttnPass& a, hipStream_t s) {
   switch (p.waves) {
-    case 1: return launch_stream_t<D, 1, PASS_B>(p, a, s);
-    case 2: return launch_stream_t<D, 2, PASS_B>(p, a, s);
-    case 4: return launch_stream_t<D, 4, PASS_B>(p, a, s);
-    case 8: return launch_stream_t<D, 8, PASS_B>(p, a, s);
+    case 1: return launch_stream_t<D, 1, MODE>(p, a, s);
+    case 2: return launch_stream_t<D, 2, MODE>(p, a, s);
+    case 4: return launch_stream_t<D, 4, MODE>(p, a, s);
+    case 8:
+      // the retained pass accumulates the Gram matrix in registers: m <= 128 only
+      if constexpr (MODE != kModeRetained) return launch_stream_t<D, 8, MODE>(p, a, s);
+      break;
   }
   return hipErrorInvalidValue;
+}
+
+template <int D>
+hipError_t launch_stream_d(const Plan& p, const AttnPass& a, int mode, hipStream_t s) {
+  if (mode == kModeLse) return launch_stream_w<D, kModeLse>(p, a, s);
+  if (mode == kModeFull) return launch_stream_w<D, kModeFull>(p, a, s);
+  return launch_stream_w<D, kModeRetained>(p, a, s);
 }
 
 }  // namespace
@@ -412,10 +495,9 @@ bool stream_supported(const Plan& p) {
          (p.waves == 1 || p.waves == 2 || p.waves == 4 || p.waves == 8);
 }
 
-hipError_t launch_stream(const Plan& p, const AttnPass& a, bool pass_b, hipStream_t s) {
-  if (p.d == 128)
-    return pass_b ? launch_stream_w<128, true>(p, a, s) : launch_stream_w<128, false>(p, a, s);
-  return pass_b ? launch_stream_w<64, true>(p, a, s) : launch_stream_w<64, false>(p, a, s);
+hipError_t launch_stream(const Plan& p, const AttnPass& a, int mode, hipStream_t s) {
+  if (p.d == 128) return launch_stream_d<128>(p, a, mode, s);
+  return launch_stream_d<64>(p, a, mode, s);
 }
 
 }  // namespace grkv

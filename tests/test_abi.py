@@ -87,7 +87,7 @@ def test_workspace_size_and_layout(L):
     assert wb(n=32768) > base and wb(c=1024) > base and wb(U=16) > base
     assert wb(d=96) == 0 and wb(c=4) == 0
     lay = G.workspace_layout(8, 4, 128, 0, 8192, 32, 512)
-    offs = [lay.lse, lay.y, lay.score, lay.pooled, lay.fixed, lay.x, lay.resid, lay.gram, lay.z]
+    offs = [lay.lse, lay.y, lay.score, lay.pooled, lay.fixed, lay.resid, lay.gram, lay.z]
     assert len(set(offs)) == len(offs)
     assert all(o % 256 == 0 and o < lay.total for o in offs)
     assert lay.total == base
