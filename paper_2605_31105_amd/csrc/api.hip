@@ -2,6 +2,7 @@
 // sequence of one grkv_compress call.  Everything is enqueued on the caller's
 // stream without a host synchronisation.
 #include <math.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include "grkv_internal.h"
@@ -64,8 +65,10 @@ int make_plan(const grkv_problem* prob, int64_t n, int32_t window, int32_t budge
   p->lam = lambda;
   p->opt = o;
 
-  // Target about 512 blocks per launch so every CU holds two.
-  const int64_t want = ceil_div(512, p->U);
+  // Target about 1024 blocks per launch (four per CU) for the streaming passes.
+  int64_t target = 1024;
+  if (const char* e = getenv("GRKV_TARGET_BLOCKS")) target = atoll(e);   // tuning experiments
+  const int64_t want = ceil_div(target, p->U);
   split_range(n, want, 512, &p->S1, &p->chunk1);
   split_range(budget, want, 128, &p->S2, &p->chunk2);
   if (p->chunk2 > 8192) split_range(budget, ceil_div(budget, 8192), 128, &p->S2, &p->chunk2);

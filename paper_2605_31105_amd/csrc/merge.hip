@@ -363,7 +363,7 @@ __global__ __launch_bounds__(256) void update_kernel(const u16* q, const u16* k0
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const bool ok = free_slot && rowok[rt][i] && tw <= rowwin[rt][i];
-            x8[4 * h + i] = ok ? exp2f(fmaf(st[i], scale_log2, -lse[rt][i])) : 0.f;
+            x8[4 * h + i] = ok ? __builtin_amdgcn_exp2f(fmaf(st[i], scale_log2, -lse[rt][i])) : 0.f;
           }
         }
         bf16x8 ah, al;

@@ -75,6 +75,10 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+// 2^x on the transcendental unit (v_exp_f32).  Results below 2^-126 flush to
+// zero, far below the precision any probability here is used at.
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
 template <int D>
 struct Geo {
   static constexpr int TK = kTileElems / D;           // keys per tile
@@ -84,15 +88,25 @@ struct Geo {
   static constexpr int INSTR = kTileBytes / 1024;     // wave instructions per tensor per tile (8)
 };
 
+// Chunk permutation of row r.  K tiles are read as 16 rows x one chunk
+// (MFMA A operand) and use r mod 16; V tiles are read by the transpose read as
+// 4 rows x 2 adjacent chunks per 16 lanes (8 rows per half wave) and use
+// 2(r mod 4) + 8(floor(r/4) mod 2), which puts those 16 chunks on distinct
+// bank groups.
+template <int D, bool VT>
+__device__ __forceinline__ int swz_key(int r) {
+  return (VT ? ((r & 3) << 1) | (((r >> 2) & 1) << 3) : r) & (Geo<D>::CPR - 1);
+}
+
 // Byte offset, inside a tile, of logical 16-byte chunk `ch` of row `r`.
-template <int D>
+template <int D, bool VT = false>
 __device__ __forceinline__ int swz(int r, int ch) {
-  return (r * Geo<D>::CPR + (ch ^ (r & (Geo<D>::CPR - 1)))) * 16;
+  return (r * Geo<D>::CPR + (ch ^ swz_key<D, VT>(r))) * 16;
 }
 
 // Issues this wave's share of the direct-to-LDS loads of one tensor tile.
 // Rows at or past key_end are clamped to key_end-1 (finite data, masked later).
-template <int D, int WAVES>
+template <int D, int WAVES, bool VT>
 __device__ __forceinline__ void load_tile(const u16* base, int tile0, int key_end, char* lds_tile,
                                           int wave, int lane) {
   using G = Geo<D>;
@@ -102,7 +116,7 @@ __device__ __forceinline__ void load_tile(const u16* base, int tile0, int key_en
     const int instr = wave * PER + it;
     const int r = instr * G::RPI + lane / G::CPR;       // row inside the tile
     const int p = lane % G::CPR;                        // physical chunk in the row
-    const int ch = p ^ (r & (G::CPR - 1));              // logical chunk stored there
+    const int ch = p ^ swz_key<D, VT>(r);               // logical chunk stored there
     int key = tile0 + r;
     key = key < key_end ? key : key_end - 1;
     const u16* src = base + (size_t)key * D + ch * 8;
@@ -132,6 +146,9 @@ template <int D, int WAVES, int MODE, int NSTAGE>
 struct Stream {
   using G = Geo<D>;
   static constexpr bool PASS_B = MODE != kModeLse;
+  // P as a bf16 hi+lo pair in P.V: Y and X V0 form the residual R the solve
+  // works on, and plain bf16 P (2^-9 per term) moves D_after by up to ~3e-3
+  static constexpr bool SPLIT = true;
   static constexpr int TK = G::TK, NKT = G::NKT, NT = 2 * WAVES;
   static constexpr int LOADS = (G::INSTR / WAVES) * (PASS_B ? 2 : 1);  // per thread per tile
 
@@ -139,14 +156,15 @@ struct Stream {
   const u16* kbase;
   const u16* vbase;
   int u, key0, key_end, ntiles, win0, lane, wave, l16, g;
+  bool all_rows;             // m == mp: no padding rows to mask
   float (*colpart)[WAVES][TK];
   uint4* xg;                 // retained pass: [2][NT][2][64] fragment exchange
   const uint8_t* fixs;       // retained pass: fixed flags of this split (LDS)
 
   __device__ __forceinline__ void issue(int t, char* stage) {
     if (t < ntiles) {
-      load_tile<D, WAVES>(kbase, key0 + t * TK, key_end, stage, wave, lane);
-      if (PASS_B) load_tile<D, WAVES>(vbase, key0 + t * TK, key_end, stage + kTileBytes, wave, lane);
+      load_tile<D, WAVES, false>(kbase, key0 + t * TK, key_end, stage, wave, lane);
+      if (PASS_B) load_tile<D, WAVES, true>(vbase, key0 + t * TK, key_end, stage + kTileBytes, wave, lane);
     }
   }
 
@@ -229,6 +247,9 @@ struct Stream {
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt)
           st[kt][rt] = mfma_bf16(as_bf16x8(kv[ks][kt]), as_bf16x8(S.qb[rt][ks]), st[kt][rt]);
+    // An interior tile has every key valid and outside the window, and the
+    // block has no padding rows: nothing to mask.
+    const bool interior = all_rows && tile0 + TK <= key_end && tile0 + TK <= win0;
     bool ok[NKT][2][4];
 #pragma unroll
     for (int kt = 0; kt < NKT; ++kt)
@@ -237,44 +258,70 @@ struct Stream {
         const int key = tile0 + kt * 16 + 4 * g + i;
         const int kw = key - win0;   // < 0 outside the window
 #pragma unroll
-        for (int rt = 0; rt < 2; ++rt) ok[kt][rt][i] = S.rowok[rt] && key < key_end && kw <= S.rowwin[rt];
+        for (int rt = 0; rt < 2; ++rt)
+          ok[kt][rt][i] = interior || (S.rowok[rt] && key < key_end && kw <= S.rowwin[rt]);
       }
 
     if (!PASS_B) {
+      // running max of the raw dot products (the scale is positive), then
+      // 2^(dot * scale - max) with one fma per element
 #pragma unroll
       for (int rt = 0; rt < 2; ++rt) {
-        float tv[NKT][4];
-        float tmax = -INFINITY;
+        float smax = -INFINITY;
+        if (interior) {
 #pragma unroll
-        for (int kt = 0; kt < NKT; ++kt)
+          for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            tv[kt][i] = ok[kt][rt][i] ? st[kt][rt][i] * a.scale_log2 : -INFINITY;
-            tmax = fmaxf(tmax, tv[kt][i]);
-          }
-        if (tmax == -INFINITY) continue;
+            for (int i = 0; i < 4; ++i) smax = fmaxf(smax, st[kt][rt][i]);
+        } else {
+#pragma unroll
+          for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) smax = fmaxf(smax, ok[kt][rt][i] ? st[kt][rt][i] : -INFINITY);
+        }
+        if (smax == -INFINITY) continue;
+        const float tmax = smax * a.scale_log2;
         if (tmax > S.mrun[rt]) {
           if (S.mrun[rt] != -INFINITY) S.srun[rt] *= exp2((double)S.mrun[rt] - (double)tmax);
           S.mrun[rt] = tmax;
         }
+        const float nm = -S.mrun[rt];
         float acc = 0.f;
+        if (interior) {
 #pragma unroll
-        for (int kt = 0; kt < NKT; ++kt)
+          for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) acc += exp2f(tv[kt][i] - S.mrun[rt]);
+            for (int i = 0; i < 4; ++i) acc += fast_exp2(fmaf(st[kt][rt][i], a.scale_log2, nm));
+        } else {
+#pragma unroll
+          for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              acc += ok[kt][rt][i] ? fast_exp2(fmaf(st[kt][rt][i], a.scale_log2, nm)) : 0.f;
+        }
         S.srun[rt] += (double)acc;
       }
       return;
     }
 
     float pv[NKT][2][4];
+    if (interior) {
 #pragma unroll
-    for (int kt = 0; kt < NKT; ++kt)
+      for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
-      for (int rt = 0; rt < 2; ++rt)
+        for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-          pv[kt][rt][i] = ok[kt][rt][i] ? exp2f(fmaf(st[kt][rt][i], a.scale_log2, -S.lse[rt])) : 0.f;
+          for (int i = 0; i < 4; ++i)
+            pv[kt][rt][i] = fast_exp2(fmaf(st[kt][rt][i], a.scale_log2, -S.lse[rt]));
+    } else {
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            pv[kt][rt][i] = ok[kt][rt][i] ? fast_exp2(fmaf(st[kt][rt][i], a.scale_log2, -S.lse[rt])) : 0.f;
+    }
     if (MODE == kModeFull && a.colsum) {
 #pragma unroll
       for (int kt = 0; kt < NKT; ++kt)
@@ -294,7 +341,12 @@ struct Stream {
         float x8[8] = {pv[2 * kp][rt][0], pv[2 * kp][rt][1], pv[2 * kp][rt][2], pv[2 * kp][rt][3],
                        pv[2 * kp + 1][rt][0], pv[2 * kp + 1][rt][1], pv[2 * kp + 1][rt][2],
                        pv[2 * kp + 1][rt][3]};
-        split8(x8, ahi[rt], alo[rt]);
+        if (SPLIT) {
+          split8(x8, ahi[rt], alo[rt]);
+        } else {
+#pragma unroll
+          for (int q = 0; q < 8; ++q) ahi[rt][q] = (__bf16)x8[q];
+        }
       }
       // lane 4e+q of group g supplies key row 32kp + 4g + e (and +16), columns dt*16 + 4q..+3
       const int r0 = 32 * kp + 4 * g + e;
@@ -303,9 +355,9 @@ struct Stream {
       for (int dt = 0; dt < D / 16; ++dt) {
         const int col = dt * 16 + 4 * qq;
         v4i16 b0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (lds_v4i16*)(vt + swz<D>(r0, col >> 3) + (col & 7) * 2));
+            (lds_v4i16*)(vt + swz<D, true>(r0, col >> 3) + (col & 7) * 2));
         v4i16 b1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (lds_v4i16*)(vt + swz<D>(r0 + 16, col >> 3) + (col & 7) * 2));
+            (lds_v4i16*)(vt + swz<D, true>(r0 + 16, col >> 3) + (col & 7) * 2));
         b[dt] = __builtin_bit_cast(bf16x8, (v8i16){b0[0], b0[1], b0[2], b0[3],
                                                    b1[0], b1[1], b1[2], b1[3]});
       }
@@ -314,7 +366,7 @@ struct Stream {
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt) {
           S.y[rt][dt] = mfma_bf16(ahi[rt], b[dt], S.y[rt][dt]);
-          S.y[rt][dt] = mfma_bf16(alo[rt], b[dt], S.y[rt][dt]);
+          if (SPLIT) S.y[rt][dt] = mfma_bf16(alo[rt], b[dt], S.y[rt][dt]);
         }
       if (MODE == kModeRetained) gram_step(t, kp, pv, S);
     }
@@ -348,6 +400,7 @@ __global__ __launch_bounds__(WAVES * 64) void stream_kernel(StreamK a) {
   sm.kbase = a.k + (size_t)sm.u * a.nk * D;
   sm.vbase = a.v + (size_t)sm.u * a.nk * D;
   sm.win0 = a.nk - a.w;
+  sm.all_rows = a.m == a.mp;
   sm.colpart = colpart;
   sm.xg = dyn;
   sm.fixs = reinterpret_cast<const uint8_t*>(dyn + 2 * NT * 2 * 64);

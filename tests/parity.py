@@ -80,7 +80,7 @@ def check_unit(cfg, q, K, V, gpu, u, slot=None, opt=None, report=None):
     info["y_err"] = float(np.abs(gpu["y"][slot] - r["Y"]).max() / max(np.abs(r["Y"]).max(), 1e-30))
     if K.shape[1] > cfg.window:
         info["p_err"] = float(np.abs(gpu["pooled"][slot] - r["p"]).max() / r["p"].max())
-    assert info["lse_err"] < 1e-4 and info["y_err"] < 1e-3
+    assert info["lse_err"] < 1e-4 and info["y_err"] < 1e-3, info
     if report is not None:
         report.append(info)
     return info
