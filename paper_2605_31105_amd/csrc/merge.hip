@@ -273,22 +273,24 @@ __global__ __launch_bounds__(MP / 32 * 256) void solve_kernel(
 }
 
 // ---------------------------------------------------------------- update ----
-// v_out = V0 + X_G^T Z for 256 retained slots per block (fixed slots, and every
+// v_out = V0 + X_G^T Z for 512 retained slots per block (fixed slots, and every
 // slot of a unit whose system was singular, get V0).  X is recomputed from the
 // window queries, K0 and the retained-set log-sum-exp rather than stored:
 // S = Q K0^T on the MFMA leaves each lane holding eight rows (two groups of
 // four) of one key's column, which is exactly the A operand of X_G^T Z with
 // the rows as the contraction index; Z^T arrives as bf16 hi/lo from the solve.
 // Q and Z^T are staged in LDS once per block.
+constexpr int kUpdWaves = 8;          // waves per update block
+constexpr int kUpdSlots = 512;        // retained slots per update block
+
 template <int MP, int D>
-__global__ __launch_bounds__(256) void update_kernel(const u16* q, const u16* k0,
-                                                     const float* lse_log2, const uint8_t* fixed,
-                                                     const u16* zhi, const u16* zlo,
-                                                     const float* stats_ws, const u16* v0c,
-                                                     float* v_out, int m, int w, int c,
-                                                     int causal, float scale_log2) {
+__global__ __launch_bounds__(kUpdWaves * 64) void update_kernel(
+    const u16* q, const u16* k0, const float* lse_log2, const uint8_t* fixed, const u16* zhi,
+    const u16* zlo, const float* stats_ws, const u16* v0c, float* v_out, int m, int w, int c,
+    int causal, float scale_log2) {
   constexpr int QS = D + 8;    // LDS row stride (bf16) of Q rows
   constexpr int ZS = MP + 8;   // LDS row stride (bf16) of Z^T rows
+  constexpr int NTH = kUpdWaves * 64;
   extern __shared__ __attribute__((aligned(16))) u16 sm[];
   u16* qs = sm;                  // [MP][QS]
   u16* zh = qs + MP * QS;        // [D][ZS]
@@ -298,10 +300,11 @@ __global__ __launch_bounds__(256) void update_kernel(const u16* q, const u16* k0
   const bool singular = stats_ws[u * 4 + 3] != 0.f;
   const uint8_t* fu = fixed + (size_t)u * c;
   const int win0 = c - w;   // first window slot of the retained set
+  const int slot0 = blockIdx.x * kUpdSlots;
 
   if (!singular) {
     const u16* qu = q + (size_t)u * m * D;
-    for (int e = tid; e < MP * (D / 8); e += 256) {
+    for (int e = tid; e < MP * (D / 8); e += NTH) {
       const int r = e / (D / 8), ch = e % (D / 8);
       const uint4 v = r < m ? *reinterpret_cast<const uint4*>(qu + (size_t)r * D + ch * 8)
                             : make_uint4(0, 0, 0, 0);
@@ -309,7 +312,7 @@ __global__ __launch_bounds__(256) void update_kernel(const u16* q, const u16* k0
     }
     const u16* zhu = zhi + (size_t)u * D * MP;
     const u16* zlu = zlo + (size_t)u * D * MP;
-    for (int e = tid; e < D * (MP / 8); e += 256) {
+    for (int e = tid; e < D * (MP / 8); e += NTH) {
       const int r = e / (MP / 8), ch = e % (MP / 8);
       *reinterpret_cast<uint4*>(zh + r * ZS + ch * 8) =
           *reinterpret_cast<const uint4*>(zhu + (size_t)r * MP + ch * 8);
@@ -331,21 +334,28 @@ __global__ __launch_bounds__(256) void update_kernel(const u16* q, const u16* k0
       rowwin[rt][i] = causal ? row % w : 0x3fffffff;
     }
 
-  for (int kt = 0; kt < 4; ++kt) {
-    const int tbase = blockIdx.x * 256 + (kt * 4 + wave) * 16;   // this wave's 16 slots
-    if (tbase >= c) break;
-    const int t = tbase + l16;   // the slot whose column this lane holds
+  // this wave's 16-slot tiles: slot0 + 16 * (wave + kUpdWaves * j)
+  constexpr int TILES = kUpdSlots / 16 / kUpdWaves;
+  auto kload = [&](int tb, uint4 (&kb)[D / 32]) {
+    const int t = tb + l16;
+    const u16* kr = k0 + ((size_t)u * c + (t < c ? t : c - 1)) * D;
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) kb[ks] = *reinterpret_cast<const uint4*>(kr + ks * 32 + 8 * g);
+  };
+  uint4 kb[D / 32], kn[D / 32];
+  int tb = slot0 + 16 * wave;
+  if (!singular && tb < c) kload(tb, kn);
+  for (int j = 0; j < TILES; ++j, tb += 16 * kUpdWaves) {
+    if (tb >= c) break;
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) kb[ks] = kn[ks];
+    if (!singular && j + 1 < TILES && tb + 16 * kUpdWaves < c) kload(tb + 16 * kUpdWaves, kn);
+    const int t = tb + l16;   // the slot whose column this lane holds
     f32x4 acc[D / 16];
 #pragma unroll
     for (int dt = 0; dt < D / 16; ++dt) acc[dt] = zero4();
-    const bool tok = t < c;
-    const bool free_slot = tok && !fu[t];
+    const bool free_slot = t < c && !fu[t];
     if (!singular) {
-      // K0 rows as the B operand of S = Q K0^T: lane holds K0[t][32ks + 8g .. +8]
-      uint4 kb[D / 32];
-      const u16* kr = k0 + ((size_t)u * c + (tok ? t : c - 1)) * D;
-#pragma unroll
-      for (int ks = 0; ks < D / 32; ++ks) kb[ks] = *reinterpret_cast<const uint4*>(kr + ks * 32 + 8 * g);
       const int tw = t - win0;   // window index of slot t (< 0 outside the window)
 #pragma unroll
       for (int rp = 0; rp < MP / 32; ++rp) {
@@ -385,10 +395,10 @@ __global__ __launch_bounds__(256) void update_kernel(const u16* q, const u16* k0
         }
       }
     }
-    // lane holds dV[slot = tbase + 4g + i][dd = 16dt + l16]
+    // lane holds dV[slot = tb + 4g + i][dd = 16dt + l16]
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int ts = tbase + 4 * g + i;
+      const int ts = tb + 4 * g + i;
       if (ts >= c) continue;
       const bool upd = !singular && !fu[ts];
 #pragma unroll
@@ -427,7 +437,8 @@ hipError_t launch_update_t(const Plan& p, const void* q, const void* k0, const f
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   const float scale_log2 = (float)(1.4426950408889634 / __builtin_sqrt((double)D));
-  hipLaunchKernelGGL((update_kernel<MP, D>), dim3((p.c + 255) / 256, p.U), dim3(256), lds, s,
+  hipLaunchKernelGGL((update_kernel<MP, D>), dim3((p.c + kUpdSlots - 1) / kUpdSlots, p.U),
+                     dim3(kUpdWaves * 64), lds, s,
                      (const u16*)q, (const u16*)k0, lse_log2, fixed, zhi, zlo, stats_ws, v0c,
                      v_out, p.m, p.w, p.c, p.opt.causal_window ? 1 : 0, scale_log2);
   return hipGetLastError();
