@@ -186,7 +186,7 @@ __global__ __launch_bounds__(MP / 32 * 256) void solve_kernel(
       const float pk = rk[k];
       if (tid == 0 && !(pk > 0.f && isfinite(pk))) fail = 1;
       if (active && rb >= pb) {
-        const float f = rk[j] / pk;
+        const float f = rk[j] * __builtin_amdgcn_rcpf(pk);
         if (rb > pb) {
 #pragma unroll
           for (int ii = 0; ii < 32; ++ii) a[ii] -= rk[r0 + ii] * f;
@@ -207,7 +207,7 @@ __global__ __launch_bounds__(MP / 32 * 256) void solve_kernel(
       const int k = pb * 32 + kk;
       float* zb = zk[kk & 1];
       if (rb == pb && rhs) {
-        const float zv = a[kk] / ucol[k * US + k];
+        const float zv = a[kk] * __builtin_amdgcn_rcpf(ucol[k * US + k]);
         a[kk] = zv;
         zb[j] = zv;
       }

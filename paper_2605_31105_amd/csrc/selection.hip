@@ -132,9 +132,15 @@ constexpr int kSmallPer = 64;   // pooled scores per thread: prefixes up to 3276
 
 // Block-wide sum of one value per thread (kSmallThreads threads); `part` holds
 // 2 x 8 words and alternates by `parity` so consecutive calls need one barrier.
+// Within a wave: DPP sums over 16-lane rows, then the four row totals.
 __device__ __forceinline__ uint32_t block_sum_small(uint32_t v, uint32_t (*part)[8], int parity) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+  int x = (int)v;
+  x += __builtin_amdgcn_update_dpp(0, x, 0xB1, 0xF, 0xF, false);
+  x += __builtin_amdgcn_update_dpp(0, x, 0x4E, 0xF, 0xF, false);
+  x += __builtin_amdgcn_update_dpp(0, x, 0x141, 0xF, 0xF, false);
+  x += __builtin_amdgcn_update_dpp(0, x, 0x140, 0xF, 0xF, false);
+  v = (uint32_t)(__builtin_amdgcn_readlane(x, 0) + __builtin_amdgcn_readlane(x, 16) +
+                 __builtin_amdgcn_readlane(x, 32) + __builtin_amdgcn_readlane(x, 48));
   if ((threadIdx.x & 63) == 0) part[parity][threadIdx.x >> 6] = v;
   __syncthreads();
   uint32_t tot = 0;
@@ -149,7 +155,7 @@ __device__ __forceinline__ uint32_t block_sum_small(uint32_t v, uint32_t (*part)
 // patterns order like values): 31 block-wide counts of "score >= mid", no
 // histograms and no atomics.
 __global__ __launch_bounds__(kSmallThreads) void select_small_kernel(SelK a) {
-  __shared__ float sl[kSmallThreads * kSmallPer];
+  __shared__ float sl[kSmallThreads * kSmallPer + kSmallThreads * kSmallPer / 64];
   __shared__ uint32_t part[2][8];
   __shared__ uint32_t scan_scratch[16];
   constexpr int PER = kSmallPer;
@@ -164,21 +170,38 @@ __global__ __launch_bounds__(kSmallThreads) void select_small_kernel(SelK a) {
   // Positions past the prefix get key 0 (score 0.0): they rank after every
   // real position with an equal score, so they are never taken while real
   // positions are left.
-  // scores of the whole prefix into LDS (coalesced), then each thread pools
-  // its 64 consecutive positions, summing s[j-h..j+h] left to right
-  for (int t = tid; t < P; t += kSmallThreads) sl[t] = s[t];
+  // Scores of the whole prefix into LDS (coalesced), stored with one pad word
+  // per 64 entries so that the 64 lanes of a wave, each reading its own
+  // contiguous run, fall on distinct banks.  Each thread then takes its 64
+  // positions plus 8 on either side into registers and pools them, summing
+  // s[j-h..j+h] left to right.
+  for (int t = tid; t < P; t += kSmallThreads) sl[t + (t >> 6)] = s[t];
   __syncthreads();
   uint32_t key[PER];
+  {
+    float v[PER + 16];
 #pragma unroll
-  for (int q = 0; q < PER; ++q) {
-    const int j = j0 + q;
-    float acc = 0.f;
-    const int lo = j - a.h < 0 ? 0 : j - a.h;
-    const int hi = j + a.h > P - 1 ? P - 1 : j + a.h;
-    for (int t = lo; t <= hi; ++t) acc += sl[t];
-    key[q] = j < P ? __float_as_uint(acc) : 0u;
-    if (j < P) pg[j] = acc;
+    for (int q = 0; q < PER + 16; ++q) {
+      const int t = j0 - 8 + q;
+      v[q] = (t >= 0 && t < P) ? sl[t + (t >> 6)] : 0.f;
+    }
+    const int h = a.h;
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      const int j = j0 + q;
+      float acc = 0.f;
+#pragma unroll
+      for (int t = -8; t <= 8; ++t)   // offsets -h..h in increasing order
+        if (t >= -h && t <= h) acc += v[q + 8 + t];
+      key[q] = j < P ? __float_as_uint(acc) : 0u;
+    }
   }
+  // the pooled scores (an intermediate the caller may inspect), coalesced
+  __syncthreads();
+#pragma unroll
+  for (int q = 0; q < PER; ++q) sl[j0 + q + ((j0 + q) >> 6)] = __uint_as_float(key[q]);
+  __syncthreads();
+  for (int t = tid; t < P; t += kSmallThreads) pg[t] = sl[t + (t >> 6)];
 
   // count of keys >= x over the block
   int parity = 0;
