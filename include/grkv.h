@@ -104,7 +104,9 @@ typedef struct {
   void** stage_events;
 } grkv_outputs;
 
-/* Stages of one call, in launch order (indices into stage_events / 2). */
+/* Stages of one call, in launch order (indices into stage_events / 2).  A stage
+ * that a given call does not run (the fast bf16 path folds FULL_Y, RESID and
+ * GRAM into neighbouring stages) leaves its two events unrecorded. */
 enum {
   GRKV_STAGE_FULL_LSE = 0,     /* full-cache pass A: row max / sum-exp per split */
   GRKV_STAGE_FULL_LSE_COMBINE, /* -> log-sum-exp of every window row */
@@ -117,7 +119,7 @@ enum {
   GRKV_STAGE_RET_PROB,         /* retained-cache pass B: X and X V0 partials */
   GRKV_STAGE_RESID,            /* R = Y - X V0 */
   GRKV_STAGE_GRAM,             /* N partials */
-  GRKV_STAGE_SOLVE,            /* Cholesky, Z, stats */
+  GRKV_STAGE_SOLVE,            /* (Y, R, N combines,) Cholesky, Z, stats */
   GRKV_STAGE_UPDATE,           /* V* = V0 + X_G^T Z */
   GRKV_NUM_STAGES
 };

@@ -198,7 +198,9 @@ int grkv_compress(const void* q_obs, const void* K, const void* V, int64_t n, in
   GRKV_STAGE(GRKV_STAGE_FULL_LSE_COMBINE,
              launch_lse_combine(p, full.pmax, full.psum, p.S1, Dd(p.lse1), F(p.lse1_log2), s));
   GRKV_STAGE(GRKV_STAGE_FULL_PROB, pass_b(full));
-  GRKV_STAGE(GRKV_STAGE_FULL_Y, launch_combine_rows(p, F(p.ypart), p.S1, nullptr, F(p.y), s));
+  // (the fast value step combines the Y partials inside its solve)
+  if (!p.fast_merge)
+    GRKV_STAGE(GRKV_STAGE_FULL_Y, launch_combine_rows(p, F(p.ypart), p.S1, nullptr, F(p.y), s));
   // 2. pooled top-k retention and the fixed set; gather K0, V0
   uint8_t* fixed = (uint8_t*)(ws + p.fixed);
   GRKV_STAGE(GRKV_STAGE_SELECT, launch_select(p, F(p.colsum), F(p.pooled), out->idx, fixed, s));
@@ -221,14 +223,16 @@ int grkv_compress(const void* q_obs, const void* K, const void* V, int64_t n, in
   // the generic value step needs X itself, which only the generic pass writes
   GRKV_STAGE(GRKV_STAGE_RET_PROB,
              fast_merge ? launch_stream(p, ret, 2, s) : launch_prob_pass(p, ret, s));
-  GRKV_STAGE(GRKV_STAGE_RESID, launch_combine_rows(p, F(p.xvpart), p.S2, F(p.y), F(p.resid), s));
+  if (!fast_merge)
+    GRKV_STAGE(GRKV_STAGE_RESID,
+               launch_combine_rows(p, F(p.xvpart), p.S2, F(p.y), F(p.resid), s));
   // 4. value step: N, Cholesky solve for Z, V* = V0 + X_G^T Z
   if (!fast_merge) GRKV_STAGE(GRKV_STAGE_GRAM, launch_gram(p, F(p.x), fixed, F(p.npart), s));
   if (fast_merge) {
     GRKV_STAGE(GRKV_STAGE_SOLVE,
-               launch_solve(p, F(p.npart), F(p.y), F(p.resid), F(p.gram), F(p.z),
-                            (uint16_t*)(ws + p.zhi), (uint16_t*)(ws + p.zlo), F(p.stats_ws),
-                            out->stats, s));
+               launch_solve(p, F(p.ypart), F(p.xvpart), F(p.npart), F(p.y), F(p.resid),
+                            F(p.gram), F(p.z), (uint16_t*)(ws + p.zhi), (uint16_t*)(ws + p.zlo),
+                            F(p.stats_ws), out->stats, s));
     GRKV_STAGE(GRKV_STAGE_UPDATE,
                launch_update(p, q_obs, out->k_out, F(p.lse2_log2), fixed,
                              (const uint16_t*)(ws + p.zhi),

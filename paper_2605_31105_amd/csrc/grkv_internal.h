@@ -86,12 +86,13 @@ hipError_t launch_gather(const Plan& p, const void* K, const void* V,
 hipError_t launch_gram(const Plan& p, const float* x, const uint8_t* fixed,
                        float* npart, hipStream_t s);
 
-// Fast value step (bf16, mp <= 128): elimination solve, then
-// v_out = V0 + X_G^T Z written in one pass from the compact V0 copy.
+// Fast value step (bf16, mp <= 128): the solve combines the Y, X V0 and Gram
+// partials (writing y, resid and gram) and solves by blocked Cholesky; then
+// v_out = V0 + X_G^T Z is written in one pass from the compact V0 copy.
 bool merge_fast_supported(const Plan& p);
-hipError_t launch_solve(const Plan& p, const float* npart, const float* y,
-                        const float* resid, float* gram, float* z, uint16_t* zhi,
-                        uint16_t* zlo, float* stats_ws, float* stats_user,
+hipError_t launch_solve(const Plan& p, const float* ypart, const float* xvpart,
+                        const float* npart, float* y, float* resid, float* gram, float* z,
+                        uint16_t* zhi, uint16_t* zlo, float* stats_ws, float* stats_user,
                         hipStream_t s);
 // X is recomputed from q_obs, K0 (k_out) and the retained log-sum-exp.
 hipError_t launch_update(const Plan& p, const void* q, const void* k0,

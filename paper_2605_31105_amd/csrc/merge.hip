@@ -8,6 +8,8 @@
 // X_G is X with the fixed columns zeroed.  The fp32 operands of the two
 // products go through the bf16 MFMA as hi+lo pairs (three products per tile),
 // which keeps about 16 significant bits per term; accumulation is fp32.
+#include <type_traits>
+
 #include "grkv_device.h"
 #include "grkv_internal.h"
 
@@ -114,153 +116,305 @@ __global__ __launch_bounds__(WAVES * 64) void gram_kernel(const float* x, const 
 }
 
 // ----------------------------------------------------------------- solve ----
-// One block per unit solves N Z = R for the d right-hand sides by Gaussian
-// elimination without pivoting (N is symmetric positive definite for
-// lambda > 0) followed by back substitution, in fp32.
-// Thread (rb, j) holds rows 32rb..32rb+31 of column j of the augmented matrix
-// [N | R] in registers (j < MP: N, j >= MP: right-hand side j - MP).  The
-// elimination step for pivot k publishes row k in LDS; since the trailing
-// block stays symmetric, the multipliers of the rows below k are that row's
-// own entries, A[i][k] = A[k][i].  The finished rows of U are kept in LDS,
-// transposed, for the back substitution.
+// One block per unit.  The split partials are combined here, in a fixed order:
+// Y = sum of the full-cache partials, R = Y - (sum of the retained X V0
+// partials), N = (sum of the Gram partials) + lambda I (padding rows and
+// columns of N become identity rows, padding rows of R zero).  N Z = R is then
+// solved by a blocked Cholesky factorisation N = L L^T over 16-wide panels:
+//  * factor: for each panel p one wave factors the diagonal block and inverts
+//    its factor (row layout, one row per lane of a 16-lane DPP row), the panel
+//    below becomes L_ip = A_ip L_pp^-T and the trailing lower blocks take
+//    A_ij -= L_ip L_jp^T; the update of the next diagonal block runs first, on
+//    the wave that factors it, while the other waves finish the rest;
+//  * solve: each wave then owns 16 columns of R in registers and runs the
+//    forward (W_p = L_pp^-1 (R_p - sum L_pq W_q)) and backward
+//    (Z_p = L_pp^-T (W_p - sum L_qp^T Z_q)) substitutions without barriers.
+// Every product is an fp32 MFMA (16x16x4), so the solve stays in fp32.
+constexpr int kSolveWaves = 16;
+
+// Broadcast lane J of each 16-lane row to the whole row (DPP row_newbcast).
+template <int J>
+__device__ __forceinline__ float row_bcast(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x150 + J, 0xF, 0xF, true));
+}
+
+template <int J>
+__device__ __forceinline__ float row_bcast_rt(int j, float v) {
+  if constexpr (J < 16) {
+    if (j == J) return row_bcast<J>(v);
+    return row_bcast_rt<J + 1>(j, v);
+  } else {
+    return 0.f;
+  }
+}
+
+// Factor the 16x16 SPD block at `blk` (LDS, row stride AS) as L L^T and write
+// L^-1 (lower triangular, zero above) to `inv` (row stride 20).  Every 16-lane
+// row of the calling wave computes the same result; lane i holds row i.
+// Returns false when a pivot is not positive and finite.
+template <int AS>
+__device__ __forceinline__ bool factor_diag(const float* blk, float* inv, int lane) {
+  const int i = lane & 15;
+  float a[16];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const float4 v = *reinterpret_cast<const float4*>(blk + i * AS + 4 * q);
+    a[4 * q] = v.x; a[4 * q + 1] = v.y; a[4 * q + 2] = v.z; a[4 * q + 3] = v.w;
+  }
+  bool ok = true;
+  float invd[16];
+  // right-looking: column k is scaled, then the trailing lower part updated;
+  // lane i's entries right of its diagonal carry values never read back.
+#pragma unroll
+  for (int k = 0; k < 16; ++k) {
+    const float dk = row_bcast_rt<0>(k, a[k]);
+    ok = ok && dk > 0.f && dk < __builtin_huge_valf();
+    const float r = __builtin_amdgcn_rsqf(dk);   // 1 / L_kk
+    invd[k] = r;
+    a[k] = (i == k) ? dk * r : a[k] * r;
+#pragma unroll
+    for (int j = k + 1; j < 16; ++j) a[j] = fmaf(-a[k], row_bcast_rt<0>(j, a[k]), a[j]);
+  }
+  // L = D M with M unit lower triangular (M_ik = L_ik / L_ii); M^-1 by forward
+  // substitution over rows, then L^-1 = M^-1 D^-1 scales column j by 1 / L_jj.
+  float dii = 0.f;
+#pragma unroll
+  for (int k = 0; k < 16; ++k) dii = (i == k) ? invd[k] : dii;
+  float x[16];
+#pragma unroll
+  for (int j = 0; j < 16; ++j) x[j] = (j == i) ? 1.f : 0.f;
+#pragma unroll
+  for (int k = 0; k < 15; ++k) {
+    const float mik = (i > k) ? a[k] * dii : 0.f;   // M_ik for the rows below k
+#pragma unroll
+    for (int j = 0; j <= k; ++j) x[j] = fmaf(-mik, row_bcast_rt<0>(k, x[j]), x[j]);
+  }
+#pragma unroll
+  for (int j = 0; j < 16; ++j) x[j] *= invd[j];
+  if (lane < 16) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      *reinterpret_cast<float4*>(inv + i * 20 + 4 * q) =
+          make_float4(x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]);
+  }
+  return ok;
+}
+
 template <int MP, int D>
-__global__ __launch_bounds__(MP / 32 * 256) void solve_kernel(
-    const float* npart, int S3, const float* y, const float* resid, float* gram, float* z,
-    u16* zhi, u16* zlo, float* stats_ws, float* stats_user, int m, float lam) {
-  constexpr int RB = MP / 32;
-  constexpr int NC = MP + D;              // augmented columns (<= 256)
-  constexpr int US = MP + 4;              // Ucol row stride
-  __shared__ __attribute__((aligned(16))) float rowk[2][256];
-  __shared__ __attribute__((aligned(16))) float ucol[MP * US];   // ucol[k][i] = U[i][k]
-  __shared__ float zk[2][256];
+__global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
+    const float* ypart, int S1, const float* xvpart, int S2, const float* npart, int S3,
+    float* y, float* resid, float* gram, float* z, u16* zhi, u16* zlo, float* stats_ws,
+    float* stats_user, int m, float lam) {
+  constexpr int NP = MP / 16;   // panels
+  constexpr int NC = D / 16;    // 16-column tiles of the right-hand side
+  constexpr int AS = MP + 4;    // LDS row strides (floats); 16-byte aligned rows
+  constexpr int BS = D + 4;
+  constexpr int LS = 20;
+  constexpr int NTH = kSolveWaves * 64;
+  __shared__ __attribute__((aligned(16))) float A[MP * AS];
+  __shared__ __attribute__((aligned(16))) float B[MP * BS];
+  __shared__ __attribute__((aligned(16))) float Li[NP * 16 * LS];
+  __shared__ double red[3][kSolveWaves];
   __shared__ int fail;
-  __shared__ double red[3][RB * 4];
 
   const int u = blockIdx.x, tid = threadIdx.x;
-  const int rb = tid >> 8, j = tid & 255;
-  const bool active = j < NC;
-  const bool rhs = j >= MP && active;
-  const int r0 = rb * 32;
-  float a[32];
-
+  const int lane = tid & 63, wave = tid >> 6, l16 = lane & 15, g = lane >> 4;
   if (tid == 0) fail = 0;
-  // load: column j < MP is row j of the symmetric N; j >= MP is column j-MP of R
-  const float* np = npart + (size_t)u * S3 * MP * MP;
-  const float* ru = resid + (size_t)u * MP * D;
-  if (j < MP) {
+
+  // 1. combine the partials; every thread issues the loads of two elements
+  // before it sums them, which keeps more of them in flight
+  double sy = 0.0, sr = 0.0, sz = 0.0;
+  auto add4 = [](float4& a, const float4 b) { a.x += b.x; a.y += b.y; a.z += b.z; a.w += b.w; };
+  {
+    constexpr int E = MP * D / 4;
+    const float4* __restrict__ yp = reinterpret_cast<const float4*>(ypart) + (size_t)u * S1 * E;
+    const float4* __restrict__ xp = reinterpret_cast<const float4*>(xvpart) + (size_t)u * S2 * E;
+    float4* __restrict__ yo = reinterpret_cast<float4*>(y) + (size_t)u * E;
+    float4* __restrict__ ro = reinterpret_cast<float4*>(resid) + (size_t)u * E;
+    for (int e0 = tid; e0 < E; e0 += 2 * NTH) {
+      float4 yv[2], xv[2];
 #pragma unroll
-    for (int ii = 0; ii < 32; ++ii) a[ii] = 0.f;
-    for (int s = 0; s < S3; ++s) {
-      const float4* src = reinterpret_cast<const float4*>(np + (size_t)s * MP * MP + (size_t)j * MP + r0);
+      for (int h = 0; h < 2; ++h) yv[h] = xv[h] = make_float4(0.f, 0.f, 0.f, 0.f);
+      const int e1 = min(e0 + NTH, E - 1);   // the second element, clamped (stored only if < E)
+      for (int s = 0; s < S1; ++s) {
+        add4(yv[0], yp[(size_t)s * E + e0]);
+        add4(yv[1], yp[(size_t)s * E + e1]);
+      }
+      for (int s = 0; s < S2; ++s) {
+        add4(xv[0], xp[(size_t)s * E + e0]);
+        add4(xv[1], xp[(size_t)s * E + e1]);
+      }
 #pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        float4 v = src[q];
-        a[4 * q] += v.x; a[4 * q + 1] += v.y; a[4 * q + 2] += v.z; a[4 * q + 3] += v.w;
+      for (int h = 0; h < 2; ++h) {
+        const int e = e0 + h * NTH;
+        if (e >= E) break;
+        const int r = e / (D / 4), c4 = (e % (D / 4)) * 4;
+        float4 rv = make_float4(yv[h].x - xv[h].x, yv[h].y - xv[h].y, yv[h].z - xv[h].z,
+                                yv[h].w - xv[h].w);
+        float4 yy = yv[h];
+        if (r >= m) yy = rv = make_float4(0.f, 0.f, 0.f, 0.f);
+        yo[e] = yy;
+        ro[e] = rv;
+        *reinterpret_cast<float4*>(B + r * BS + c4) = rv;
+        sy += (double)yy.x * yy.x + (double)yy.y * yy.y + (double)yy.z * yy.z + (double)yy.w * yy.w;
+        sr += (double)rv.x * rv.x + (double)rv.y * rv.y + (double)rv.z * rv.z + (double)rv.w * rv.w;
       }
     }
-#pragma unroll
-    for (int ii = 0; ii < 32; ++ii)
-      if (r0 + ii == j) a[ii] += (j < m) ? lam : 1.f;
-    float* gu = gram + (size_t)u * MP * MP + (size_t)j * MP + r0;
-#pragma unroll
-    for (int ii = 0; ii < 32; ++ii) gu[ii] = a[ii];
-  } else if (rhs) {
-#pragma unroll
-    for (int ii = 0; ii < 32; ++ii) a[ii] = ru[(size_t)(r0 + ii) * D + (j - MP)];
-  } else {
-#pragma unroll
-    for (int ii = 0; ii < 32; ++ii) a[ii] = 0.f;
   }
-
-  // forward elimination
-  for (int pb = 0; pb < RB; ++pb) {
+  {
+    constexpr int E = MP * MP / 4;
+    const float4* __restrict__ np = reinterpret_cast<const float4*>(npart) + (size_t)u * S3 * E;
+    float4* __restrict__ go = reinterpret_cast<float4*>(gram) + (size_t)u * E;
+    for (int e = tid; e < E; e += NTH) {
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int s = 0; s < S3; ++s) add4(v, np[(size_t)s * E + e]);
+      const int r = e / (MP / 4), c4 = (e % (MP / 4)) * 4;
+      float vv[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-    for (int kk = 0; kk < 32; ++kk) {
-      const int k = pb * 32 + kk;
-      float* rk = rowk[kk & 1];
-      if (rb == pb && active) {
-        rk[j] = a[kk];
-        if (j < MP) ucol[j * US + k] = a[kk];   // U[k][j], stored transposed
+      for (int k = 0; k < 4; ++k) {
+        const int col = c4 + k;
+        if (r >= m || col >= m) vv[k] = 0.f;
+        if (r == col) vv[k] += r < m ? lam : 1.f;
       }
-      __syncthreads();
-      const float pk = rk[k];
-      if (tid == 0 && !(pk > 0.f && isfinite(pk))) fail = 1;
-      if (active && rb >= pb) {
-        const float f = rk[j] * __builtin_amdgcn_rcpf(pk);
-        if (rb > pb) {
-#pragma unroll
-          for (int ii = 0; ii < 32; ++ii) a[ii] -= rk[r0 + ii] * f;
-        } else {
-#pragma unroll
-          for (int ii = kk + 1; ii < 32; ++ii) a[ii] -= rk[r0 + ii] * f;
-        }
-      }
+      const float4 o = make_float4(vv[0], vv[1], vv[2], vv[3]);
+      go[e] = o;
+      *reinterpret_cast<float4*>(A + r * AS + c4) = o;
     }
   }
   __syncthreads();
+
+  // 2. factor N = L L^T in place (lower blocks), L_pp^-1 into Li
+  // lower-triangle tile t -> (ii, jj), jj <= ii < T
+  auto tri = [](int t, int& ii, int& jj) {
+    ii = 0;
+    while ((ii + 1) * (ii + 2) / 2 <= t) ++ii;
+    jj = t - ii * (ii + 1) / 2;
+  };
+  bool ok_local = true;
+  for (int p = 0; p < NP; ++p) {
+    const int p0 = p * 16;
+    if (p > 0) {
+      // trailing update from panel q = p - 1 over blocks (ib, jb), p <= jb <= ib;
+      // tile 0 is the diagonal block (p, p), taken by wave 0
+      const int q0 = p0 - 16, T = NP - p, TA = T * (T + 1) / 2;
+      for (int t = wave; t < (wave == 0 ? 1 : TA); t += kSolveWaves - 1) {
+        int ii, jj;
+        tri(t, ii, jj);
+        const int i0 = (p + ii) * 16, j0 = (p + jj) * 16;
+        const float4 af = *reinterpret_cast<const float4*>(A + (i0 + l16) * AS + q0 + 4 * g);
+        const float4 bf = *reinterpret_cast<const float4*>(A + (j0 + l16) * AS + q0 + 4 * g);
+        f32x4 acc;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[i] = A[(i0 + 4 * g + i) * AS + j0 + l16];
+        acc = mfma_f32(-af.x, bf.x, acc);
+        acc = mfma_f32(-af.y, bf.y, acc);
+        acc = mfma_f32(-af.z, bf.z, acc);
+        acc = mfma_f32(-af.w, bf.w, acc);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) A[(i0 + 4 * g + i) * AS + j0 + l16] = acc[i];
+      }
+    }
+    if (wave == 0) ok_local = factor_diag<AS>(A + p0 * AS + p0, Li + p * 16 * LS, lane) && ok_local;
+    __syncthreads();
+    // panel: L_ip = A_ip L_pp^-T for the blocks below the diagonal
+    for (int t = wave; t < NP - 1 - p; t += kSolveWaves) {
+      const int i0 = (p + 1 + t) * 16;
+      const float4 af = *reinterpret_cast<const float4*>(A + (i0 + l16) * AS + p0 + 4 * g);
+      const float4 bf = *reinterpret_cast<const float4*>(Li + (p * 16 + l16) * LS + 4 * g);
+      f32x4 acc = zero4();
+      acc = mfma_f32(af.x, bf.x, acc);
+      acc = mfma_f32(af.y, bf.y, acc);
+      acc = mfma_f32(af.z, bf.z, acc);
+      acc = mfma_f32(af.w, bf.w, acc);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) A[(i0 + 4 * g + i) * AS + p0 + l16] = acc[i];
+    }
+    __syncthreads();
+  }
+  if (wave == 0 && lane == 0 && !ok_local) fail = 1;
+  __syncthreads();
   const bool ok = fail == 0;
 
-  // back substitution: z[k] = w[k] / U[k][k], then w[i] -= U[i][k] z[k] for i < k
-  for (int pb = RB - 1; pb >= 0; --pb) {
+  // 3. forward and backward substitution, 16 right-hand-side columns per wave;
+  // tile rows 16t + 4g + i, column c0 + l16 live in r[t][i]
+  for (int cb = wave; cb < NC; cb += kSolveWaves) {
+    const int c0 = cb * 16;
+    f32x4 r[NP];
 #pragma unroll
-    for (int kk = 31; kk >= 0; --kk) {
-      const int k = pb * 32 + kk;
-      float* zb = zk[kk & 1];
-      if (rb == pb && rhs) {
-        const float zv = a[kk] * __builtin_amdgcn_rcpf(ucol[k * US + k]);
-        a[kk] = zv;
-        zb[j] = zv;
+    for (int t = 0; t < NP; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) r[t][i] = B[(16 * t + 4 * g + i) * BS + c0 + l16];
+    // forward: W_p = L_pp^-1 R_p, then R_i -= L_ip W_p for i > p
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      const float4 lf = *reinterpret_cast<const float4*>(Li + (p * 16 + l16) * LS + 4 * g);
+      f32x4 w = zero4();
+      w = mfma_f32(lf.x, r[p][0], w);
+      w = mfma_f32(lf.y, r[p][1], w);
+      w = mfma_f32(lf.z, r[p][2], w);
+      w = mfma_f32(lf.w, r[p][3], w);
+      r[p] = w;
+#pragma unroll
+      for (int t = p + 1; t < NP; ++t) {
+        const float4 af = *reinterpret_cast<const float4*>(A + (16 * t + l16) * AS + 16 * p + 4 * g);
+        r[t] = mfma_f32(-af.x, w[0], r[t]);
+        r[t] = mfma_f32(-af.y, w[1], r[t]);
+        r[t] = mfma_f32(-af.z, w[2], r[t]);
+        r[t] = mfma_f32(-af.w, w[3], r[t]);
       }
-      __syncthreads();
-      if (rhs && rb <= pb) {
-        const float zv = zb[j];
-        const float* uc = ucol + k * US + r0;
-        if (rb < pb) {
+    }
+    // backward: Z_p = L_pp^-T W_p, then W_i -= L_pi^T Z_p for i < p
 #pragma unroll
-          for (int ii = 0; ii < 32; ++ii) a[ii] -= uc[ii] * zv;
-        } else {
+    for (int p = NP - 1; p >= 0; --p) {
+      f32x4 zt = zero4();
 #pragma unroll
-          for (int ii = 0; ii < kk; ++ii) a[ii] -= uc[ii] * zv;
-        }
+      for (int kb = 0; kb < 4; ++kb)
+        zt = mfma_f32(Li[(p * 16 + 4 * g + kb) * LS + l16], r[p][kb], zt);
+      r[p] = zt;
+#pragma unroll
+      for (int t = 0; t < p; ++t) {
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb)
+          r[t] = mfma_f32(-A[(16 * p + 4 * g + kb) * AS + 16 * t + l16], zt[kb], r[t]);
       }
+    }
+    // Z^T out: row dd = c0 + l16, entries 16t + 4g .. +3
+    const int dd = c0 + l16;
+    float* zr = z + ((size_t)u * D + dd) * MP;
+    u16* hr = zhi + ((size_t)u * D + dd) * MP;
+    u16* lr = zlo + ((size_t)u * D + dd) * MP;
+#pragma unroll
+    for (int t = 0; t < NP; ++t) {
+      float zv[4];
+      u16 hv[4], lv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = 16 * t + 4 * g + i;
+        zv[i] = ok && row < m ? r[t][i] : 0.f;
+        const __bf16 h = (__bf16)zv[i];
+        hv[i] = __builtin_bit_cast(u16, h);
+        lv[i] = __builtin_bit_cast(u16, (__bf16)(zv[i] - (float)h));
+        sz += (double)zv[i] * zv[i];
+      }
+      *reinterpret_cast<float4*>(zr + 16 * t + 4 * g) = make_float4(zv[0], zv[1], zv[2], zv[3]);
+      *reinterpret_cast<uint2*>(hr + 16 * t + 4 * g) =
+          make_uint2(hv[0] | ((uint32_t)hv[1] << 16), hv[2] | ((uint32_t)hv[3] << 16));
+      *reinterpret_cast<uint2*>(lr + 16 * t + 4 * g) =
+          make_uint2(lv[0] | ((uint32_t)lv[1] << 16), lv[2] | ((uint32_t)lv[3] << 16));
     }
   }
 
-  // outputs: Z^T in fp32 and as bf16 hi/lo pairs (the update's MFMA operand)
-  double sz = 0.0;
-  if (rhs) {
-    const int dd = j - MP;
-    float* zr = z + ((size_t)u * D + dd) * MP + r0;
-    u16* hr = zhi + ((size_t)u * D + dd) * MP + r0;
-    u16* lr = zlo + ((size_t)u * D + dd) * MP + r0;
-#pragma unroll
-    for (int ii = 0; ii < 32; ++ii) {
-      const float zv = ok ? a[ii] : 0.f;
-      zr[ii] = zv;
-      const __bf16 h = (__bf16)zv;
-      hr[ii] = __builtin_bit_cast(u16, h);
-      lr[ii] = __builtin_bit_cast(u16, (__bf16)(zv - (float)h));
-      if (r0 + ii < m) sz += (double)zv * zv;
-    }
-  }
-  // ||Y||^2 and ||R||^2 over the m real rows
-  const float* yu = y + (size_t)u * MP * D;
-  double sy = 0.0, sr = 0.0;
-  for (int e = tid; e < m * D; e += blockDim.x) {
-    const double yv = yu[e], rv = ru[e];
-    sy += yv * yv;
-    sr += rv * rv;
-  }
+  // 4. stats: ||Y||^2, D before = ||R||^2 / ||Y||^2, D after = lambda^2 ||Z||^2 / ||Y||^2
   for (int off = 32; off > 0; off >>= 1) {
     sy += __shfl_xor(sy, off);
     sr += __shfl_xor(sr, off);
     sz += __shfl_xor(sz, off);
   }
-  if ((tid & 63) == 0) { red[0][tid >> 6] = sy; red[1][tid >> 6] = sr; red[2][tid >> 6] = sz; }
+  if (lane == 0) { red[0][wave] = sy; red[1][wave] = sr; red[2][wave] = sz; }
   __syncthreads();
   if (tid == 0) {
     double Y2 = 0, R2 = 0, Z2 = 0;
-    for (int k = 0; k < RB * 4; ++k) { Y2 += red[0][k]; R2 += red[1][k]; Z2 += red[2][k]; }
+    for (int k = 0; k < kSolveWaves; ++k) { Y2 += red[0][k]; R2 += red[1][k]; Z2 += red[2][k]; }
     const double dn = Y2 > 0 ? Y2 : 1.0;
     const double dbefore = R2 / dn;
     const double dafter = ok ? (double)lam * lam * Z2 / dn : dbefore;
@@ -273,34 +427,50 @@ __global__ __launch_bounds__(MP / 32 * 256) void solve_kernel(
 }
 
 // ---------------------------------------------------------------- update ----
-// v_out = V0 + X_G^T Z for 512 retained slots per block (fixed slots, and every
-// slot of a unit whose system was singular, get V0).  X is recomputed from the
-// window queries, K0 and the retained-set log-sum-exp rather than stored:
-// S = Q K0^T on the MFMA leaves each lane holding eight rows (two groups of
-// four) of one key's column, which is exactly the A operand of X_G^T Z with
-// the rows as the contraction index; Z^T arrives as bf16 hi/lo from the solve.
-// Q and Z^T are staged in LDS once per block.
-constexpr int kUpdWaves = 8;          // waves per update block
-constexpr int kUpdSlots = 512;        // retained slots per update block
+// v_out = V0 + X_G^T Z over a range of retained slots per block (fixed slots,
+// and every slot of a unit whose system was singular, get V0).  X is
+// recomputed from the window queries, K0 and the retained-set log-sum-exp
+// rather than stored: S = Q K0^T on the MFMA leaves each lane holding eight
+// rows (two groups of four) of one slot's column, which is exactly the A
+// operand of X_G^T Z with the rows as the contraction index.  Z^T arrives as
+// bf16 hi/lo from the solve; Q, Z^T, -LSE and the block's fixed flags are
+// staged in LDS once per block.  A wave works on two 16-slot tiles at a time,
+// so every Q and Z^T fragment read from LDS feeds two MFMAs; it loads the K0
+// rows of its next pair of tiles and the V0 rows of the current one before
+// computing.  The rows of Z^T are staged in the order (dd mod DT) * 16 + dd / DT
+// (DT = D / 16 output tiles), which hands each lane DT consecutive output
+// columns: V0 and v_out move in 16-byte pieces.
+constexpr int kUpdWaves = 8;        // waves per update block
+constexpr int kUpdMaxSlots = 4096;  // retained slots per update block at most
+
+template <int MP, int D>
+__host__ __device__ constexpr size_t update_lds_bytes(int spb) {
+  return ((size_t)MP * (D + 8) + 2 * (size_t)D * (MP + 8)) * sizeof(u16) + MP * sizeof(float) +
+         (size_t)spb;
+}
 
 template <int MP, int D>
 __global__ __launch_bounds__(kUpdWaves * 64) void update_kernel(
     const u16* q, const u16* k0, const float* lse_log2, const uint8_t* fixed, const u16* zhi,
     const u16* zlo, const float* stats_ws, const u16* v0c, float* v_out, int m, int w, int c,
-    int causal, float scale_log2) {
+    int spb, int causal, float scale_log2) {
   constexpr int QS = D + 8;    // LDS row stride (bf16) of Q rows
   constexpr int ZS = MP + 8;   // LDS row stride (bf16) of Z^T rows
+  constexpr int DT = D / 16;   // output tiles per slot row
   constexpr int NTH = kUpdWaves * 64;
+  constexpr float NEG_INF = -__builtin_huge_valf();
   extern __shared__ __attribute__((aligned(16))) u16 sm[];
-  u16* qs = sm;                  // [MP][QS]
-  u16* zh = qs + MP * QS;        // [D][ZS]
-  u16* zl = zh + D * ZS;         // [D][ZS]
+  u16* qs = sm;                                            // [MP][QS]
+  u16* zh = qs + MP * QS;                                  // [D][ZS]
+  u16* zl = zh + D * ZS;                                   // [D][ZS]
+  float* nls = reinterpret_cast<float*>(zl + D * ZS);      // [MP] -LSE (log2 domain)
+  uint8_t* fl = reinterpret_cast<uint8_t*>(nls + MP);      // [spb] fixed flags
   const int u = blockIdx.y, tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, l16 = lane & 15, g = lane >> 4;
   const bool singular = stats_ws[u * 4 + 3] != 0.f;
-  const uint8_t* fu = fixed + (size_t)u * c;
   const int win0 = c - w;   // first window slot of the retained set
-  const int slot0 = blockIdx.x * kUpdSlots;
+  const int s0 = blockIdx.x * spb;
+  const int s1 = min(c, s0 + spb);
 
   if (!singular) {
     const u16* qu = q + (size_t)u * m * D;
@@ -312,102 +482,159 @@ __global__ __launch_bounds__(kUpdWaves * 64) void update_kernel(
     }
     const u16* zhu = zhi + (size_t)u * D * MP;
     const u16* zlu = zlo + (size_t)u * D * MP;
+    // Z^T row dd goes to LDS row (dd mod DT) * 16 + dd / DT; within a row, Z
+    // row r = 32rp + 16h + 4g + i sits at 32rp + 8g + 4h + i, the order in
+    // which a lane of group g holds its eight X values (one 16-byte read)
     for (int e = tid; e < D * (MP / 8); e += NTH) {
-      const int r = e / (MP / 8), ch = e % (MP / 8);
-      *reinterpret_cast<uint4*>(zh + r * ZS + ch * 8) =
-          *reinterpret_cast<const uint4*>(zhu + (size_t)r * MP + ch * 8);
-      *reinterpret_cast<uint4*>(zl + r * ZS + ch * 8) =
-          *reinterpret_cast<const uint4*>(zlu + (size_t)r * MP + ch * 8);
+      const int dd = e / (MP / 8), r0 = 8 * (e % (MP / 8));
+      const int row = (dd % DT) * 16 + dd / DT;
+      const int rp = r0 >> 5, h = (r0 >> 4) & 1, g0 = (r0 >> 2) & 3;   // rows r0..r0+7: groups g0, g0+1
+      const int p0 = row * ZS + 32 * rp + 8 * g0 + 4 * h, p1 = p0 + 8;
+      const uint4 vh = *reinterpret_cast<const uint4*>(zhu + (size_t)dd * MP + r0);
+      const uint4 vl = *reinterpret_cast<const uint4*>(zlu + (size_t)dd * MP + r0);
+      *reinterpret_cast<uint2*>(zh + p0) = make_uint2(vh.x, vh.y);
+      *reinterpret_cast<uint2*>(zh + p1) = make_uint2(vh.z, vh.w);
+      *reinterpret_cast<uint2*>(zl + p0) = make_uint2(vl.x, vl.y);
+      *reinterpret_cast<uint2*>(zl + p1) = make_uint2(vl.z, vl.w);
     }
-    __syncthreads();
+    // padding rows get -inf, hence probability zero
+    for (int r = tid; r < MP; r += NTH) nls[r] = r < m ? -lse_log2[(size_t)u * MP + r] : NEG_INF;
   }
-  float lse[MP / 16][4];
-  bool rowok[MP / 16][4];
-  int rowwin[MP / 16][4];
-#pragma unroll
-  for (int rt = 0; rt < MP / 16; ++rt)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = rt * 16 + 4 * g + i;
-      lse[rt][i] = lse_log2[(size_t)u * MP + row];
-      rowok[rt][i] = row < m;
-      rowwin[rt][i] = causal ? row % w : 0x3fffffff;
-    }
+  for (int t = tid; t < s1 - s0; t += NTH) fl[t] = fixed[(size_t)u * c + s0 + t];
+  __syncthreads();
 
-  // this wave's 16-slot tiles: slot0 + 16 * (wave + kUpdWaves * j)
-  constexpr int TILES = kUpdSlots / 16 / kUpdWaves;
-  auto kload = [&](int tb, uint4 (&kb)[D / 32]) {
-    const int t = tb + l16;
-    const u16* kr = k0 + ((size_t)u * c + (t < c ? t : c - 1)) * D;
+  auto load_k = [&](int tb, uint4 (&kb)[2][D / 32]) {
 #pragma unroll
-    for (int ks = 0; ks < D / 32; ++ks) kb[ks] = *reinterpret_cast<const uint4*>(kr + ks * 32 + 8 * g);
+    for (int T = 0; T < 2; ++T) {
+      const int t = tb + 16 * T + l16;
+      const u16* kr = k0 + ((size_t)u * c + (t < s1 ? t : s1 - 1)) * D;
+#pragma unroll
+      for (int ks = 0; ks < D / 32; ++ks) kb[T][ks] = *reinterpret_cast<const uint4*>(kr + ks * 32 + 8 * g);
+    }
   };
-  uint4 kb[D / 32], kn[D / 32];
-  int tb = slot0 + 16 * wave;
-  if (!singular && tb < c) kload(tb, kn);
-  for (int j = 0; j < TILES; ++j, tb += 16 * kUpdWaves) {
-    if (tb >= c) break;
+  uint4 kb[2][D / 32];
+  int tb = s0 + 32 * wave;
+  if (!singular && tb < s1) load_k(tb, kb);
+  for (; tb < s1; tb += 32 * kUpdWaves) {
+    const int tnext = tb + 32 * kUpdWaves;
+    // V0 rows of this pair (slot tb + 16T + 4g + i, columns l16 * DT ..),
+    // loaded now so that they arrive during the products
+    uint32_t v0r[2][4][DT / 2];
 #pragma unroll
-    for (int ks = 0; ks < D / 32; ++ks) kb[ks] = kn[ks];
-    if (!singular && j + 1 < TILES && tb + 16 * kUpdWaves < c) kload(tb + 16 * kUpdWaves, kn);
-    const int t = tb + l16;   // the slot whose column this lane holds
-    f32x4 acc[D / 16];
+    for (int T = 0; T < 2; ++T)
 #pragma unroll
-    for (int dt = 0; dt < D / 16; ++dt) acc[dt] = zero4();
-    const bool free_slot = t < c && !fu[t];
+      for (int i = 0; i < 4; ++i) {
+        const int ts = min(tb + 16 * T + 4 * g + i, s1 - 1);
+        const u16* src = v0c + ((size_t)u * c + ts) * D + l16 * DT;
+        if constexpr (DT == 8) {
+          const uint4 r4 = *reinterpret_cast<const uint4*>(src);
+          v0r[T][i][0] = r4.x; v0r[T][i][1] = r4.y; v0r[T][i][2] = r4.z; v0r[T][i][3] = r4.w;
+        } else {
+          const uint2 r2 = *reinterpret_cast<const uint2*>(src);
+          v0r[T][i][0] = r2.x; v0r[T][i][1] = r2.y;
+        }
+      }
+    f32x4 acc[2][DT];
+#pragma unroll
+    for (int T = 0; T < 2; ++T)
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) acc[T][dt] = zero4();
     if (!singular) {
-      const int tw = t - win0;   // window index of slot t (< 0 outside the window)
+      uint4 kn[2][D / 32];
+      if (tnext < s1) load_k(tnext, kn);
+      float cm[2];   // 0 for a free slot, -inf for a fixed or missing one
+      int tw[2];     // window index of the slot (< 0 outside the window)
 #pragma unroll
-      for (int rp = 0; rp < MP / 32; ++rp) {
-        float x8[8];
+      for (int T = 0; T < 2; ++T) {
+        const int t = tb + 16 * T + l16;   // the slot whose column this lane holds
+        cm[T] = (t < s1 && !fl[t - s0]) ? 0.f : NEG_INF;
+        tw[T] = t - win0;
+      }
+      // X_G^T Z for this pair of tiles; WIN adds the causal rule of the window
+      // slots, which only the last tiles of the retained set contain
+      auto pair_product = [&](auto win_tag) {
+        constexpr bool WIN = decltype(win_tag)::value;
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int rt = 2 * rp + h;
-          f32x4 st = zero4();
+        for (int rp = 0; rp < MP / 32; ++rp) {
+          bf16x8 ah[2], al[2];
+          float x8[2][8];
 #pragma unroll
-          for (int ks = 0; ks < D / 32; ++ks) {
-            const bf16x8 qa = as_bf16x8(*reinterpret_cast<const uint4*>(qs + (rt * 16 + l16) * QS + ks * 32 + 8 * g));
-            st = mfma_bf16(qa, as_bf16x8(kb[ks]), st);
+          for (int h = 0; h < 2; ++h) {
+            const int rt = 2 * rp + h;
+            f32x4 st[2] = {zero4(), zero4()};
+#pragma unroll
+            for (int ks = 0; ks < D / 32; ++ks) {
+              const bf16x8 qa = as_bf16x8(*reinterpret_cast<const uint4*>(qs + (rt * 16 + l16) * QS + ks * 32 + 8 * g));
+              st[0] = mfma_bf16(qa, as_bf16x8(kb[0][ks]), st[0]);
+              st[1] = mfma_bf16(qa, as_bf16x8(kb[1][ks]), st[1]);
+            }
+            const float4 nv = *reinterpret_cast<const float4*>(nls + rt * 16 + 4 * g);
+            const float nl[4] = {nv.x, nv.y, nv.z, nv.w};
+            // st[T][i] = q_row . k_t for row = 16rt + 4g + i
+#pragma unroll
+            for (int T = 0; T < 2; ++T)
+#pragma unroll
+              for (int i = 0; i < 4; ++i) {
+                float arg = fmaf(st[T][i], scale_log2, nl[i]) + cm[T];
+                if constexpr (WIN) {
+                  if (tw[T] > (rt * 16 + 4 * g + i) % w) arg = NEG_INF;
+                }
+                x8[T][4 * h + i] = __builtin_amdgcn_exp2f(arg);
+              }
           }
-          // st[i] = q_row . k_t for row = 16rt + 4g + i
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const bool ok = free_slot && rowok[rt][i] && tw <= rowwin[rt][i];
-            x8[4 * h + i] = ok ? __builtin_amdgcn_exp2f(fmaf(st[i], scale_log2, -lse[rt][i])) : 0.f;
+          for (int T = 0; T < 2; ++T) split8(x8[T], ah[T], al[T]);
+          // the eight rows {32rp + 4g + i, 32rp + 16 + 4g + i} of a lane form
+          // its A operand; Z^T rows in the permuted order above, output
+          // column l16 * DT + dt
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) {
+            const int zo = (dt * 16 + l16) * ZS + 32 * rp + 8 * g;
+            const bf16x8 bh = as_bf16x8(*reinterpret_cast<const uint4*>(zh + zo));
+            const bf16x8 bl = as_bf16x8(*reinterpret_cast<const uint4*>(zl + zo));
+#pragma unroll
+            for (int T = 0; T < 2; ++T) {
+              acc[T][dt] = mfma_bf16(ah[T], bh, acc[T][dt]);
+              acc[T][dt] = mfma_bf16(ah[T], bl, acc[T][dt]);
+              acc[T][dt] = mfma_bf16(al[T], bh, acc[T][dt]);
+            }
           }
         }
-        bf16x8 ah, al;
-        split8(x8, ah, al);
-        // Z rows {32rp + 4g + i, 32rp + 16 + 4g + i}, column dd = 16dt + l16
+      };
+      if (causal && tb + 31 >= win0)   // wave-uniform
+        pair_product(std::true_type{});
+      else
+        pair_product(std::false_type{});
+      if (tnext < s1) {
 #pragma unroll
-        for (int dt = 0; dt < D / 16; ++dt) {
-          const u16* zr = zh + (dt * 16 + l16) * ZS + 32 * rp + 4 * g;
-          const u16* zr2 = zl + (dt * 16 + l16) * ZS + 32 * rp + 4 * g;
-          const uint2 h0 = *reinterpret_cast<const uint2*>(zr);
-          const uint2 h1 = *reinterpret_cast<const uint2*>(zr + 16);
-          const uint2 l0 = *reinterpret_cast<const uint2*>(zr2);
-          const uint2 l1 = *reinterpret_cast<const uint2*>(zr2 + 16);
-          const bf16x8 bh = as_bf16x8(make_uint4(h0.x, h0.y, h1.x, h1.y));
-          const bf16x8 bl = as_bf16x8(make_uint4(l0.x, l0.y, l1.x, l1.y));
-          acc[dt] = mfma_bf16(ah, bh, acc[dt]);
-          acc[dt] = mfma_bf16(ah, bl, acc[dt]);
-          acc[dt] = mfma_bf16(al, bh, acc[dt]);
+        for (int T = 0; T < 2; ++T)
+#pragma unroll
+          for (int ks = 0; ks < D / 32; ++ks) kb[T][ks] = kn[T][ks];
+      }
+    }
+    // lane holds dV[slot = tb + 16T + 4g + i][dd = l16 * DT + dt]
+#pragma unroll
+    for (int T = 0; T < 2; ++T)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int ts = tb + 16 * T + 4 * g + i;
+        if (ts >= s1) continue;
+        const bool upd = !singular && !fl[ts - s0];
+        float v[DT];
+#pragma unroll
+        for (int k = 0; k < DT / 2; ++k) {
+          v[2 * k] = __uint_as_float(v0r[T][i][k] << 16);
+          v[2 * k + 1] = __uint_as_float(v0r[T][i][k] & 0xffff0000u);
         }
-      }
-    }
-    // lane holds dV[slot = tb + 4g + i][dd = 16dt + l16]
+        if (upd) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int ts = tb + 4 * g + i;
-      if (ts >= c) continue;
-      const bool upd = !singular && !fu[ts];
+          for (int dt = 0; dt < DT; ++dt) v[dt] += acc[T][dt][i];
+        }
+        float* dst = v_out + ((size_t)u * c + ts) * D + l16 * DT;
 #pragma unroll
-      for (int dt = 0; dt < D / 16; ++dt) {
-        const size_t o = ((size_t)u * c + ts) * D + dt * 16 + l16;
-        const float v0 = bf16_to_f32(v0c[o]);
-        v_out[o] = upd ? v0 + acc[dt][i] : v0;
+        for (int k = 0; k < DT / 4; ++k)
+          *reinterpret_cast<float4*>(dst + 4 * k) = make_float4(v[4 * k], v[4 * k + 1], v[4 * k + 2], v[4 * k + 3]);
       }
-    }
   }
 }
 
@@ -420,11 +647,12 @@ hipError_t launch_gram_w(const Plan& p, const float* x, const uint8_t* fixed, fl
 }
 
 template <int MP, int D>
-hipError_t launch_solve_t(const Plan& p, const float* npart, const float* y, const float* resid,
-                          float* gram, float* z, u16* zhi, u16* zlo, float* stats_ws,
-                          float* stats_user, hipStream_t s) {
-  hipLaunchKernelGGL((solve_kernel<MP, D>), dim3(p.U), dim3(MP / 32 * 256), 0, s, npart, p.S3, y,
-                     resid, gram, z, zhi, zlo, stats_ws, stats_user, p.m, p.lam);
+hipError_t launch_solve_t(const Plan& p, const float* ypart, const float* xvpart,
+                          const float* npart, float* y, float* resid, float* gram, float* z,
+                          u16* zhi, u16* zlo, float* stats_ws, float* stats_user, hipStream_t s) {
+  hipLaunchKernelGGL((solve_kernel<MP, D>), dim3(p.U), dim3(kSolveWaves * 64), 0, s, ypart, p.S1,
+                     xvpart, p.S2, npart, p.S3, y, resid, gram, z, zhi, zlo, stats_ws, stats_user,
+                     p.m, p.lam);
   return hipGetLastError();
 }
 
@@ -432,15 +660,26 @@ template <int MP, int D>
 hipError_t launch_update_t(const Plan& p, const void* q, const void* k0, const float* lse_log2,
                            const uint8_t* fixed, const u16* zhi, const u16* zlo,
                            const float* stats_ws, const u16* v0c, float* v_out, hipStream_t s) {
-  const size_t lds = ((size_t)MP * (D + 8) + 2 * (size_t)D * (MP + 8)) * sizeof(u16);
+  // about one block per compute unit: split a unit's slots over several
+  // blocks only when there are fewer units than that
+  const int pair_rows = 32 * kUpdWaves;
+  int bpu = (256 + p.U - 1) / p.U;
+  const int most = (p.c + pair_rows - 1) / pair_rows;
+  if (bpu > most) bpu = most;
+  const int least = (p.c + kUpdMaxSlots - 1) / kUpdMaxSlots;
+  if (bpu < least) bpu = least;
+  if (bpu < 1) bpu = 1;
+  int spb = (p.c + bpu - 1) / bpu;
+  spb = (spb + 31) / 32 * 32;
+  bpu = (p.c + spb - 1) / spb;
+  const size_t lds = update_lds_bytes<MP, D>(spb);
   hipError_t e = hipFuncSetAttribute((const void*)update_kernel<MP, D>,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   const float scale_log2 = (float)(1.4426950408889634 / __builtin_sqrt((double)D));
-  hipLaunchKernelGGL((update_kernel<MP, D>), dim3((p.c + kUpdSlots - 1) / kUpdSlots, p.U),
-                     dim3(kUpdWaves * 64), lds, s,
+  hipLaunchKernelGGL((update_kernel<MP, D>), dim3(bpu, p.U), dim3(kUpdWaves * 64), lds, s,
                      (const u16*)q, (const u16*)k0, lse_log2, fixed, zhi, zlo, stats_ws, v0c,
-                     v_out, p.m, p.w, p.c, p.opt.causal_window ? 1 : 0, scale_log2);
+                     v_out, p.m, p.w, p.c, spb, p.opt.causal_window ? 1 : 0, scale_log2);
   return hipGetLastError();
 }
 
@@ -461,12 +700,13 @@ hipError_t launch_gram(const Plan& p, const float* x, const uint8_t* fixed, floa
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_solve(const Plan& p, const float* npart, const float* y, const float* resid,
-                        float* gram, float* z, u16* zhi, u16* zlo, float* stats_ws,
-                        float* stats_user, hipStream_t s) {
+hipError_t launch_solve(const Plan& p, const float* ypart, const float* xvpart, const float* npart,
+                        float* y, float* resid, float* gram, float* z, u16* zhi, u16* zlo,
+                        float* stats_ws, float* stats_user, hipStream_t s) {
 #define GRKV_SOLVE(MPV, DV)                                                                   \
   if (p.mp == MPV && p.d == DV)                                                               \
-    return launch_solve_t<MPV, DV>(p, npart, y, resid, gram, z, zhi, zlo, stats_ws, stats_user, s);
+    return launch_solve_t<MPV, DV>(p, ypart, xvpart, npart, y, resid, gram, z, zhi, zlo,        \
+                                   stats_ws, stats_user, s);
   GRKV_SOLVE(32, 64) GRKV_SOLVE(32, 128) GRKV_SOLVE(64, 64) GRKV_SOLVE(64, 128)
   GRKV_SOLVE(128, 64) GRKV_SOLVE(128, 128)
 #undef GRKV_SOLVE

@@ -223,7 +223,8 @@ struct Stream {
                                        State<D, MODE, NT>& S) {
     if (t >= ntiles) return;
     const int ahead = min(ntiles - 1 - t, NSTAGE - 2);
-    if (ahead >= 2) wait_vmcnt<2 * LOADS>();
+    if (NSTAGE > 4 && ahead >= 3) wait_vmcnt<(NSTAGE > 4 ? 3 : 0) * LOADS>();
+    else if (ahead >= 2) wait_vmcnt<2 * LOADS>();
     else if (ahead == 1) wait_vmcnt<LOADS>();
     else wait_vmcnt<0>();
     lds_barrier();
@@ -374,16 +375,21 @@ struct Stream {
 };
 
 template <int D, int WAVES, int MODE>
-__global__ __launch_bounds__(WAVES * 64) void stream_kernel(StreamK a) {
+__global__ __launch_bounds__(WAVES * 64)
+__attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : 1))) void stream_kernel(StreamK a) {
   using G = Geo<D>;
   constexpr bool PASS_B = MODE != kModeLse;
   constexpr int TK = G::TK, NT = 2 * WAVES;
-  constexpr int NSTAGE = PASS_B ? 3 : 4;
+  // ring depth: pass A 5 x 8 KB (four blocks per CU at 4 waves per SIMD);
+  // pass B 3 x 16 KB (a fourth stage measured slower)
+  constexpr int NSTAGE = MODE == kModeLse ? 5 : 3;
+  static_assert(NSTAGE == 3 || NSTAGE == 5, "ring depths with an unrolled loop below");
   constexpr int STAGE_BYTES = kTileBytes * (PASS_B ? 2 : 1);
   __shared__ __attribute__((aligned(16))) char stg0[STAGE_BYTES];
   __shared__ __attribute__((aligned(16))) char stg1[STAGE_BYTES];
   __shared__ __attribute__((aligned(16))) char stg2[STAGE_BYTES];
-  __shared__ __attribute__((aligned(16))) char stg3[PASS_B ? 16 : STAGE_BYTES];
+  __shared__ __attribute__((aligned(16))) char stg3[NSTAGE > 3 ? STAGE_BYTES : 16];
+  __shared__ __attribute__((aligned(16))) char stg4[NSTAGE > 4 ? STAGE_BYTES : 16];
   __shared__ float colpart[2][WAVES][TK];
   extern __shared__ __attribute__((aligned(16))) uint4 dyn[];   // retained pass only
 
@@ -439,17 +445,21 @@ __global__ __launch_bounds__(WAVES * 64) void stream_kernel(StreamK a) {
 
   sm.issue(0, stg0);
   sm.issue(1, stg1);
-  if (NSTAGE == 4) sm.issue(2, stg2);
+  if constexpr (NSTAGE == 5) {
+    sm.issue(2, stg2);
+    sm.issue(3, stg3);
+  }
   for (int t = 0; t < sm.ntiles; t += NSTAGE) {
-    if (NSTAGE == 3) {
+    if constexpr (NSTAGE == 3) {
       sm.step(t + 0, stg0, stg2, S);
       sm.step(t + 1, stg1, stg0, S);
       sm.step(t + 2, stg2, stg1, S);
     } else {
-      sm.step(t + 0, stg0, stg3, S);
+      sm.step(t + 0, stg0, stg4, S);
       sm.step(t + 1, stg1, stg0, S);
       sm.step(t + 2, stg2, stg1, S);
       sm.step(t + 3, stg3, stg2, S);
+      sm.step(t + 4, stg4, stg3, S);
     }
   }
 
