@@ -34,14 +34,24 @@ __device__ __forceinline__ float bf16_to_f32(u16 b) {
   return __uint_as_float(((uint32_t)b) << 16);
 }
 
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
 // Round-to-nearest-even split of 8 floats into bf16 hi and lo parts,
-// x ~= hi + lo with about 16 significant bits.
+// x ~= hi + lo with about 16 significant bits.  Pairs go through the packed
+// conversion (two values per instruction); hi back to fp32 is a shift or a
+// mask of the packed word.
 __device__ __forceinline__ void split8(const float* x, bf16x8& hi, bf16x8& lo) {
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    __bf16 h = (__bf16)x[i];
-    hi[i] = h;
-    lo[i] = (__bf16)(x[i] - (float)h);
+  for (int i = 0; i < 8; i += 2) {
+    const bf16x2 h = __builtin_convertvector((f32x2){x[i], x[i + 1]}, bf16x2);
+    const uint32_t hw = __builtin_bit_cast(uint32_t, h);
+    const float h0 = __uint_as_float(hw << 16), h1 = __uint_as_float(hw & 0xffff0000u);
+    const bf16x2 l = __builtin_convertvector((f32x2){x[i] - h0, x[i + 1] - h1}, bf16x2);
+    hi[i] = h[0];
+    hi[i + 1] = h[1];
+    lo[i] = l[0];
+    lo[i + 1] = l[1];
   }
 }
 

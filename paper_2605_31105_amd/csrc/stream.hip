@@ -17,10 +17,11 @@
 //    ds_read_b64_tr_b16: within a 16-lane group, lane 4e+q supplies the
 //    address of key row e, columns 4q..4q+3, and lane i receives column i of
 //    the four rows.
-//  * Pass A keeps a running max and sum per lane (its own keys of its row) and
-//    merges the four lanes of a row once at the end; pass B's column sums use
-//    DPP within 16-lane rows.  Neither touches the LDS for reductions inside
-//    the tile loop except one 32-float exchange per tile for column sums.
+//  * Pass A keeps a reference exponent and a sum per lane (its own keys of its
+//    row) and merges the four lanes of a row once at the end; pass B's column
+//    sums are one DPP reduce-scatter within 16-lane rows.  Neither touches the
+//    LDS for reductions inside the tile loop except one 32-float exchange per
+//    tile for column sums.
 //  * Window positions are the last w key slots of both key sets (the full
 //    cache, and the retained set whose last w entries are the window), so the
 //    causal rule needs no position array.
@@ -75,6 +76,49 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+// Sum of each of NV values (8 or 16) over the 16 lanes of a DPP row, as a
+// reduce-scatter: each step pairs lanes that differ in one bit b of l16 (and
+// agree on the bits of the earlier steps); a lane keeps the upper half of its
+// list when b is set, the lower half otherwise, and adds its partner's copy
+// of that half.  Pairings: bit 3 by row_mirror (l ^ 15), bit 2 by
+// row_half_mirror (l ^ 7), bit 1 by quad_perm [2,3,0,1] (l ^ 2), bit 0 by
+// quad_perm [1,0,3,2] (l ^ 1); over the four steps a lane collects all 16
+// lanes.  With NV = 8 the last step is a plain pair sum.  Returns the sum of
+// value *v, v = the kept index (8 b3 + 4 b2 + 2 b1 + b0 for NV = 16,
+// 4 b3 + 2 b2 + b1 for NV = 8).
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, true));
+}
+
+template <int L, int STEP>
+__device__ __forceinline__ void rs_step(float* c, int l16) {
+  constexpr int CTRL = STEP == 0 ? 0x140 : STEP == 1 ? 0x141 : STEP == 2 ? 0x4E : 0xB1;
+  const bool up = (l16 >> (3 - STEP)) & 1;
+#pragma unroll
+  for (int k = 0; k < L / 2; ++k) {
+    const float keep = up ? c[k + L / 2] : c[k];
+    const float send = up ? c[k] : c[k + L / 2];
+    c[k] = keep + dpp_f<CTRL>(send);
+  }
+}
+
+template <int NV>
+__device__ __forceinline__ float row_reduce_scatter(float (&c)[NV], int l16, int* v) {
+  static_assert(NV == 8 || NV == 16, "8 or 16 values");
+  rs_step<NV, 0>(c, l16);
+  rs_step<NV / 2, 1>(c, l16);
+  rs_step<NV / 4, 2>(c, l16);
+  if constexpr (NV == 16) {
+    rs_step<2, 3>(c, l16);
+    *v = l16;
+    return c[0];
+  } else {
+    *v = l16 >> 1;
+    return c[0] + dpp_f<0xB1>(c[0]);
+  }
+}
+
 // 2^x on the transcendental unit (v_exp_f32).  Results below 2^-126 flush to
 // zero, far below the precision any probability here is used at.
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
@@ -106,11 +150,26 @@ __device__ __forceinline__ int swz(int r, int ch) {
 
 // Issues this wave's share of the direct-to-LDS loads of one tensor tile.
 // Rows at or past key_end are clamped to key_end-1 (finite data, masked later).
+// A whole tile (the common case) is addressed as a uniform tile base plus a
+// per-lane byte offset that does not change from tile to tile, so the loads
+// take a scalar base and cost no vector instructions per tile.
 template <int D, int WAVES, bool VT>
 __device__ __forceinline__ void load_tile(const u16* base, int tile0, int key_end, char* lds_tile,
                                           int wave, int lane) {
   using G = Geo<D>;
   constexpr int PER = G::INSTR / WAVES;
+  if (tile0 + G::TK <= key_end) {
+    const char* tb = reinterpret_cast<const char*>(base + (size_t)tile0 * D);
+#pragma unroll
+    for (int it = 0; it < PER; ++it) {
+      const int instr = wave * PER + it;
+      const int r = instr * G::RPI + lane / G::CPR;
+      const int ch = (lane % G::CPR) ^ swz_key<D, VT>(r);
+      const uint32_t voff = (uint32_t)(r * D + ch * 8) * 2u;
+      __builtin_amdgcn_global_load_lds(tb + voff, (lds_void*)(lds_tile + instr * 1024), 16, 0, 0);
+    }
+    return;
+  }
 #pragma unroll
   for (int it = 0; it < PER; ++it) {
     const int instr = wave * PER + it;
@@ -136,8 +195,9 @@ struct State {
   int rowwin[2];
   bool rowok[2];
   float lse[2];
-  float mrun[2];   // pass A: per-lane running max of this lane's keys
-  double srun[2];  // pass A: per-lane running sum of 2^(t - mrun)
+  float mref[2];   // pass A: per-lane reference exponent (an integer, or -inf
+                   // before the lane's first visible key)
+  double srun[2];  // pass A: per-lane sum of 2^(t - mref) over this lane's keys
   f32x4 y[2][MODE != kModeLse ? D / 16 : 1];
   f32x4 n[2][MODE == kModeRetained ? NT : 1];   // Gram rows of this wave
 };
@@ -251,6 +311,14 @@ struct Stream {
     // An interior tile has every key valid and outside the window, and the
     // block has no padding rows: nothing to mask.
     const bool interior = all_rows && tile0 + TK <= key_end && tile0 + TK <= win0;
+    if (interior) body<true>(t, tile0, cur, st, S);
+    else body<false>(t, tile0, cur, st, S);
+  }
+
+  // The tile's work after the logits.  INTERIOR skips every mask.
+  template <bool INTERIOR>
+  __device__ __forceinline__ void body(int t, int tile0, const char* cur, const f32x4 (&st)[NKT][2],
+                                       State<D, MODE, NT>& S) {
     bool ok[NKT][2][4];
 #pragma unroll
     for (int kt = 0; kt < NKT; ++kt)
@@ -260,45 +328,49 @@ struct Stream {
         const int kw = key - win0;   // < 0 outside the window
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt)
-          ok[kt][rt][i] = interior || (S.rowok[rt] && key < key_end && kw <= S.rowwin[rt]);
+          ok[kt][rt][i] = INTERIOR || (S.rowok[rt] && key < key_end && kw <= S.rowwin[rt]);
       }
 
     if (!PASS_B) {
-      // running max of the raw dot products (the scale is positive), then
-      // 2^(dot * scale - max) with one fma per element
+      // Sum of 2^(t - ref) against a per-lane integer reference.  The
+      // reference is set from the first visible tile (ceil of its largest
+      // scaled logit) and moved up only when a tile's partial sum exceeds
+      // 2^64, so the tile maximum is taken only on those rare tiles, and a
+      // move rescales the running sum exactly (a power of two).  Terms below
+      // the float range (2^-126 under the reference) are at least 2^-125
+      // smaller than the sum and drop out.
 #pragma unroll
       for (int rt = 0; rt < 2; ++rt) {
-        float smax = -INFINITY;
-        if (interior) {
+        const float nref = -S.mref[rt];
+        float acc = 0.f;
 #pragma unroll
-          for (int kt = 0; kt < NKT; ++kt)
+        for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) smax = fmaxf(smax, st[kt][rt][i]);
-        } else {
+          for (int i = 0; i < 4; ++i) {
+            const float e = fast_exp2(fmaf(st[kt][rt][i], a.scale_log2, nref));
+            acc += ok[kt][rt][i] ? e : 0.f;
+          }
+        // also taken when the reference is still -inf and a key is visible
+        // (the sum is then +inf)
+        if (!(acc <= 0x1p64f)) {
+          float smax = -INFINITY;
 #pragma unroll
           for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
             for (int i = 0; i < 4; ++i) smax = fmaxf(smax, ok[kt][rt][i] ? st[kt][rt][i] : -INFINITY);
-        }
-        if (smax == -INFINITY) continue;
-        const float tmax = smax * a.scale_log2;
-        if (tmax > S.mrun[rt]) {
-          if (S.mrun[rt] != -INFINITY) S.srun[rt] *= exp2((double)S.mrun[rt] - (double)tmax);
-          S.mrun[rt] = tmax;
-        }
-        const float nm = -S.mrun[rt];
-        float acc = 0.f;
-        if (interior) {
+          acc = 0.f;
+          if (smax != -INFINITY) {
+            const float ref = ceilf(smax * a.scale_log2);
+            S.srun[rt] = S.mref[rt] == -INFINITY ? 0.0 : ldexp(S.srun[rt], (int)(S.mref[rt] - ref));
+            S.mref[rt] = ref;
 #pragma unroll
-          for (int kt = 0; kt < NKT; ++kt)
+            for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) acc += fast_exp2(fmaf(st[kt][rt][i], a.scale_log2, nm));
-        } else {
-#pragma unroll
-          for (int kt = 0; kt < NKT; ++kt)
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-              acc += ok[kt][rt][i] ? fast_exp2(fmaf(st[kt][rt][i], a.scale_log2, nm)) : 0.f;
+              for (int i = 0; i < 4; ++i) {
+                const float e = fast_exp2(fmaf(st[kt][rt][i], a.scale_log2, -ref));
+                acc += ok[kt][rt][i] ? e : 0.f;
+              }
+          }
         }
         S.srun[rt] += (double)acc;
       }
@@ -306,31 +378,28 @@ struct Stream {
     }
 
     float pv[NKT][2][4];
-    if (interior) {
 #pragma unroll
-      for (int kt = 0; kt < NKT; ++kt)
+    for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
-        for (int rt = 0; rt < 2; ++rt)
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            pv[kt][rt][i] = fast_exp2(fmaf(st[kt][rt][i], a.scale_log2, -S.lse[rt]));
-    } else {
-#pragma unroll
-      for (int kt = 0; kt < NKT; ++kt)
-#pragma unroll
-        for (int rt = 0; rt < 2; ++rt)
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            pv[kt][rt][i] = ok[kt][rt][i] ? fast_exp2(fmaf(st[kt][rt][i], a.scale_log2, -S.lse[rt])) : 0.f;
-    }
-    if (MODE == kModeFull && a.colsum) {
-#pragma unroll
-      for (int kt = 0; kt < NKT; ++kt)
+      for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float c = sum16_dpp(pv[kt][0][i] + pv[kt][1][i]);
-          if (l16 == 0) colpart[t & 1][wave][kt * 16 + 4 * g + i] = c;
+          const float e = fast_exp2(fmaf(st[kt][rt][i], a.scale_log2, -S.lse[rt]));
+          pv[kt][rt][i] = ok[kt][rt][i] ? e : 0.f;
         }
+    if (MODE == kModeFull && a.colsum) {
+      // column sums over this wave's 32 rows: the two row tiles first, then
+      // the 16 lanes of each DPP row (one reduce-scatter; lane l16 ends with
+      // key v = kt*4 + i of its group, v taken from the high bits of l16)
+      float cs[NKT * 4];
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) cs[kt * 4 + i] = pv[kt][0][i] + pv[kt][1][i];
+      int v;
+      const float c = row_reduce_scatter<NKT * 4>(cs, l16, &v);
+      if (NKT * 4 == 16 || (l16 & 1) == 0)
+        colpart[t & 1][wave][(v >> 2) * 16 + 4 * g + (v & 3)] = c;
     }
     const char* vt = cur + kTileBytes;
     const int e = l16 >> 2, qq = l16 & 3;
@@ -376,7 +445,7 @@ struct Stream {
 
 template <int D, int WAVES, int MODE>
 __global__ __launch_bounds__(WAVES * 64)
-__attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : 1))) void stream_kernel(StreamK a) {
+__attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : MODE == kModeFull ? 2 : 1))) void stream_kernel(StreamK a) {
   using G = Geo<D>;
   constexpr bool PASS_B = MODE != kModeLse;
   constexpr int TK = G::TK, NT = 2 * WAVES;
@@ -435,7 +504,7 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : 1))) void stream_kerne
       S.qb[rt][ks] = S.rowok[rt] ? *reinterpret_cast<const uint4*>(q + ks * 32 + 8 * g)
                                  : make_uint4(0, 0, 0, 0);
     S.lse[rt] = PASS_B ? a.lse_log2[(size_t)u * a.mp + row] : 0.f;
-    S.mrun[rt] = -INFINITY;
+    S.mref[rt] = -INFINITY;
     S.srun[rt] = 0.0;
 #pragma unroll
     for (int dt = 0; dt < (PASS_B ? D / 16 : 1); ++dt) S.y[rt][dt] = zero4();
@@ -491,11 +560,12 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : 1))) void stream_kerne
           }
     }
   } else {
-    // merge the four lanes of each row: M = max m_g, sum = sum_g s_g 2^(m_g - M)
+    // merge the four lanes of each row: M = max ref_g, sum = sum_g s_g 2^(ref_g - M)
+    // (integer exponents: exact)
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) {
-      float M = max_over_groups(S.mrun[rt]);
-      double part = (S.mrun[rt] == -INFINITY) ? 0.0 : S.srun[rt] * exp2((double)S.mrun[rt] - (double)M);
+      float M = max_over_groups(S.mref[rt]);
+      double part = (S.mref[rt] == -INFINITY) ? 0.0 : ldexp(S.srun[rt], (int)(S.mref[rt] - M));
       const double tot = sum_over_groups(part);
       const int row = wave * kRowsPerWave + rt * 16 + l16;
       if (g == 0) {
