@@ -93,7 +93,10 @@ int make_plan(const grkv_problem* prob, int64_t n, int32_t window, int32_t budge
   p->colsum = take(U * (P > 0 ? P : 1) * sizeof(float));
   p->pooled = take(U * (P > 0 ? P : 1) * sizeof(float));
   p->fixed = take(U * c);
-  p->v0c = take(U * c * d * esz);
+  // the compact V0 copy serves the generic retained passes only; the fast
+  // path reads V0 rows through idx
+  const bool fast_path = stream_supported(*p) && merge_fast_supported(*p);
+  p->v0c = take(fast_path ? 0 : U * c * d * esz);
   p->pmax2 = take(U * p->S2 * mp * sizeof(float));
   p->psum2 = take(U * p->S2 * mp * sizeof(double));
   p->lse2 = take(U * mp * sizeof(double));
@@ -205,8 +208,12 @@ int grkv_compress(const void* q_obs, const void* K, const void* V, int64_t n, in
   uint8_t* fixed = (uint8_t*)(ws + p.fixed);
   GRKV_STAGE(GRKV_STAGE_SELECT, launch_select(p, F(p.colsum), F(p.pooled), out->idx, fixed, s));
   const bool fast_merge = p.fast_merge;
-  GRKV_STAGE(GRKV_STAGE_GATHER, launch_gather(p, K, V, out->idx, out->k_out, ws + p.v0c,
-                                              fast_merge ? nullptr : out->v_out, s));
+  // fast path: the retained pass A reads the K rows through idx and copies
+  // them to k_out; V0 rows are read through idx where needed
+  const bool direct = fast && fast_merge;
+  if (!direct)
+    GRKV_STAGE(GRKV_STAGE_GATHER, launch_gather(p, K, V, out->idx, out->k_out, ws + p.v0c,
+                                                fast_merge ? nullptr : out->v_out, s));
   // 3. window attention over the retained cache: X and X V0, then R = Y - X V0
   AttnPass ret = {};
   ret.q = q_obs; ret.k = out->k_out; ret.v = ws + p.v0c; ret.kpos = out->idx; ret.nk = p.c;
@@ -217,7 +224,14 @@ int grkv_compress(const void* q_obs, const void* K, const void* V, int64_t n, in
   ret.xout = fast_merge ? nullptr : F(p.x);
   ret.split_p = true;
   ret.fixed = fixed; ret.npart = F(p.npart);
-  GRKV_STAGE(GRKV_STAGE_RET_LSE, pass_a(ret));
+  if (direct) {
+    AttnPass ra = ret;
+    ra.k = K; ra.gather_k = true; ra.src_rows = n; ra.kcopy = out->k_out;
+    GRKV_STAGE(GRKV_STAGE_RET_LSE, pass_a(ra));
+    ret.v = V; ret.gather_v = true; ret.src_rows = n;
+  } else {
+    GRKV_STAGE(GRKV_STAGE_RET_LSE, pass_a(ret));
+  }
   GRKV_STAGE(GRKV_STAGE_RET_LSE_COMBINE,
              launch_lse_combine(p, ret.pmax, ret.psum, p.S2, Dd(p.lse2), F(p.lse2_log2), s));
   // the generic value step needs X itself, which only the generic pass writes
@@ -237,7 +251,7 @@ int grkv_compress(const void* q_obs, const void* K, const void* V, int64_t n, in
                launch_update(p, q_obs, out->k_out, F(p.lse2_log2), fixed,
                              (const uint16_t*)(ws + p.zhi),
                              (const uint16_t*)(ws + p.zlo), F(p.stats_ws),
-                             (const uint16_t*)(ws + p.v0c), out->v_out, s));
+                             V, out->idx, out->v_out, s));
   } else {
     GRKV_STAGE(GRKV_STAGE_SOLVE, launch_cholesky_solve(p, F(p.npart), F(p.y), F(p.resid),
                                                        F(p.gram), F(p.z), F(p.stats_ws),

@@ -60,6 +60,12 @@ struct AttnPass {
   bool split_p;        // P.V with P as a bf16 hi+lo pair (else bf16 P)
   const uint8_t* fixed; // retained pass B (fast path): fixed flags [U][nk]
   float* npart;        // retained pass B (fast path): Gram partials [U][S][mp][mp]
+  // streaming passes over the retained set: read K and/or V rows through
+  // kpos from tensors of src_rows rows per unit (instead of [U][nk][d]), and
+  // optionally copy the K tiles to kcopy [U][nk][d]
+  bool gather_k, gather_v;
+  int64_t src_rows;
+  void* kcopy;
 };
 
 hipError_t launch_lse_pass(const Plan& p, const AttnPass& a, hipStream_t s);
@@ -94,12 +100,13 @@ hipError_t launch_solve(const Plan& p, const float* ypart, const float* xvpart,
                         const float* npart, float* y, float* resid, float* gram, float* z,
                         uint16_t* zhi, uint16_t* zlo, float* stats_ws, float* stats_user,
                         hipStream_t s);
-// X is recomputed from q_obs, K0 (k_out) and the retained log-sum-exp.
+// X is recomputed from q_obs, K0 (k_out) and the retained log-sum-exp; V0
+// rows are read from V [U][n][d] through idx.
 hipError_t launch_update(const Plan& p, const void* q, const void* k0,
                          const float* lse_log2, const uint8_t* fixed,
                          const uint16_t* zhi, const uint16_t* zlo,
-                         const float* stats_ws, const uint16_t* v0c, float* v_out,
-                         hipStream_t s);
+                         const float* stats_ws, const void* V, const int32_t* idx,
+                         float* v_out, hipStream_t s);
 
 // Generic value step (any dtype, mp up to 256): Cholesky in LDS; the update
 // adds X_G^T Z into v_out, which the gather filled with V0.

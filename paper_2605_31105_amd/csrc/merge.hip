@@ -446,14 +446,14 @@ constexpr int kUpdMaxSlots = 4096;  // retained slots per update block at most
 template <int MP, int D>
 __host__ __device__ constexpr size_t update_lds_bytes(int spb) {
   return ((size_t)MP * (D + 8) + 2 * (size_t)D * (MP + 8)) * sizeof(u16) + MP * sizeof(float) +
-         (size_t)spb;
+         (size_t)spb * sizeof(int32_t) + (size_t)spb;
 }
 
 template <int MP, int D>
 __global__ __launch_bounds__(kUpdWaves * 64) void update_kernel(
     const u16* q, const u16* k0, const float* lse_log2, const uint8_t* fixed, const u16* zhi,
-    const u16* zlo, const float* stats_ws, const u16* v0c, float* v_out, int m, int w, int c,
-    int spb, int causal, float scale_log2) {
+    const u16* zlo, const float* stats_ws, const u16* V, const int32_t* idx, int64_t n,
+    float* v_out, int m, int w, int c, int spb, int causal, float scale_log2) {
   constexpr int QS = D + 8;    // LDS row stride (bf16) of Q rows
   constexpr int ZS = MP + 8;   // LDS row stride (bf16) of Z^T rows
   constexpr int DT = D / 16;   // output tiles per slot row
@@ -464,7 +464,8 @@ __global__ __launch_bounds__(kUpdWaves * 64) void update_kernel(
   u16* zh = qs + MP * QS;                                  // [D][ZS]
   u16* zl = zh + D * ZS;                                   // [D][ZS]
   float* nls = reinterpret_cast<float*>(zl + D * ZS);      // [MP] -LSE (log2 domain)
-  uint8_t* fl = reinterpret_cast<uint8_t*>(nls + MP);      // [spb] fixed flags
+  int32_t* ps = reinterpret_cast<int32_t*>(nls + MP);      // [spb] source rows of the slots
+  uint8_t* fl = reinterpret_cast<uint8_t*>(ps + spb);      // [spb] fixed flags
   const int u = blockIdx.y, tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, l16 = lane & 15, g = lane >> 4;
   const bool singular = stats_ws[u * 4 + 3] != 0.f;
@@ -500,7 +501,11 @@ __global__ __launch_bounds__(kUpdWaves * 64) void update_kernel(
     // padding rows get -inf, hence probability zero
     for (int r = tid; r < MP; r += NTH) nls[r] = r < m ? -lse_log2[(size_t)u * MP + r] : NEG_INF;
   }
-  for (int t = tid; t < s1 - s0; t += NTH) fl[t] = fixed[(size_t)u * c + s0 + t];
+  for (int t = tid; t < s1 - s0; t += NTH) {
+    fl[t] = fixed[(size_t)u * c + s0 + t];
+    const int64_t r = idx[(size_t)u * c + s0 + t];
+    ps[t] = (int32_t)(r < 0 ? 0 : r >= n ? n - 1 : r);   // in range by construction
+  }
   __syncthreads();
 
   auto load_k = [&](int tb, uint4 (&kb)[2][D / 32]) {
@@ -525,7 +530,7 @@ __global__ __launch_bounds__(kUpdWaves * 64) void update_kernel(
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int ts = min(tb + 16 * T + 4 * g + i, s1 - 1);
-        const u16* src = v0c + ((size_t)u * c + ts) * D + l16 * DT;
+        const u16* src = V + ((size_t)u * n + ps[ts - s0]) * D + l16 * DT;
         if constexpr (DT == 8) {
           const uint4 r4 = *reinterpret_cast<const uint4*>(src);
           v0r[T][i][0] = r4.x; v0r[T][i][1] = r4.y; v0r[T][i][2] = r4.z; v0r[T][i][3] = r4.w;
@@ -659,7 +664,8 @@ hipError_t launch_solve_t(const Plan& p, const float* ypart, const float* xvpart
 template <int MP, int D>
 hipError_t launch_update_t(const Plan& p, const void* q, const void* k0, const float* lse_log2,
                            const uint8_t* fixed, const u16* zhi, const u16* zlo,
-                           const float* stats_ws, const u16* v0c, float* v_out, hipStream_t s) {
+                           const float* stats_ws, const u16* V, const int32_t* idx,
+                           float* v_out, hipStream_t s) {
   // about one block per compute unit: split a unit's slots over several
   // blocks only when there are fewer units than that
   const int pair_rows = 32 * kUpdWaves;
@@ -678,8 +684,8 @@ hipError_t launch_update_t(const Plan& p, const void* q, const void* k0, const f
   if (e != hipSuccess) return e;
   const float scale_log2 = (float)(1.4426950408889634 / __builtin_sqrt((double)D));
   hipLaunchKernelGGL((update_kernel<MP, D>), dim3(bpu, p.U), dim3(kUpdWaves * 64), lds, s,
-                     (const u16*)q, (const u16*)k0, lse_log2, fixed, zhi, zlo, stats_ws, v0c,
-                     v_out, p.m, p.w, p.c, spb, p.opt.causal_window ? 1 : 0, scale_log2);
+                     (const u16*)q, (const u16*)k0, lse_log2, fixed, zhi, zlo, stats_ws, V, idx,
+                     p.n, v_out, p.m, p.w, p.c, spb, p.opt.causal_window ? 1 : 0, scale_log2);
   return hipGetLastError();
 }
 
@@ -715,10 +721,12 @@ hipError_t launch_solve(const Plan& p, const float* ypart, const float* xvpart, 
 
 hipError_t launch_update(const Plan& p, const void* q, const void* k0, const float* lse_log2,
                          const uint8_t* fixed, const u16* zhi, const u16* zlo,
-                         const float* stats_ws, const u16* v0c, float* v_out, hipStream_t s) {
+                         const float* stats_ws, const void* V, const int32_t* idx, float* v_out,
+                         hipStream_t s) {
 #define GRKV_UPD(MPV, DV)                                                                     \
   if (p.mp == MPV && p.d == DV)                                                               \
-    return launch_update_t<MPV, DV>(p, q, k0, lse_log2, fixed, zhi, zlo, stats_ws, v0c, v_out, s);
+    return launch_update_t<MPV, DV>(p, q, k0, lse_log2, fixed, zhi, zlo, stats_ws,             \
+                                    (const u16*)V, idx, v_out, s);
   GRKV_UPD(32, 64) GRKV_UPD(32, 128) GRKV_UPD(64, 64) GRKV_UPD(64, 128)
   GRKV_UPD(128, 64) GRKV_UPD(128, 128)
 #undef GRKV_UPD

@@ -52,6 +52,12 @@ struct StreamK {
   int prefix;
   const uint8_t* fixed;   // retained pass: fixed flag per retained slot
   float* npart;           // retained pass: Gram partials [U][S][mp][mp]
+  // retained passes: rows of K (gather_k) and/or V (gather_v) are read
+  // through kpos [U][nk] from tensors of src_rows rows per unit
+  const int32_t* kpos;
+  int64_t src_rows;
+  int gather_k, gather_v;
+  u16* kcopy;             // if set, every K tile is also copied to [U][nk][D]
 };
 
 constexpr int kTileElems = 4096;   // elements of one tensor per tile
@@ -153,11 +159,27 @@ __device__ __forceinline__ int swz(int r, int ch) {
 // A whole tile (the common case) is addressed as a uniform tile base plus a
 // per-lane byte offset that does not change from tile to tile, so the loads
 // take a scalar base and cost no vector instructions per tile.
+// With `pos` (LDS, one source row per key slot of the block, starting at
+// slot key0) the rows are gathered: slot key reads source row pos[key - key0].
 template <int D, int WAVES, bool VT>
 __device__ __forceinline__ void load_tile(const u16* base, int tile0, int key_end, char* lds_tile,
-                                          int wave, int lane) {
+                                          int wave, int lane, const int32_t* pos = nullptr,
+                                          int key0 = 0) {
   using G = Geo<D>;
   constexpr int PER = G::INSTR / WAVES;
+  if (pos) {
+#pragma unroll
+    for (int it = 0; it < PER; ++it) {
+      const int instr = wave * PER + it;
+      const int r = instr * G::RPI + lane / G::CPR;
+      const int ch = (lane % G::CPR) ^ swz_key<D, VT>(r);
+      int key = tile0 + r;
+      key = key < key_end ? key : key_end - 1;
+      const u16* src = base + (size_t)pos[key - key0] * D + ch * 8;
+      __builtin_amdgcn_global_load_lds(src, (lds_void*)(lds_tile + instr * 1024), 16, 0, 0);
+    }
+    return;
+  }
   if (tile0 + G::TK <= key_end) {
     const char* tb = reinterpret_cast<const char*>(base + (size_t)tile0 * D);
 #pragma unroll
@@ -220,11 +242,27 @@ struct Stream {
   float (*colpart)[WAVES][TK];
   uint4* xg;                 // retained pass: [2][NT][2][64] fragment exchange
   const uint8_t* fixs;       // retained pass: fixed flags of this split (LDS)
+  const int32_t* posl;       // gathered rows: source row of each slot of this split (LDS)
 
   __device__ __forceinline__ void issue(int t, char* stage) {
     if (t < ntiles) {
-      load_tile<D, WAVES, false>(kbase, key0 + t * TK, key_end, stage, wave, lane);
-      if (PASS_B) load_tile<D, WAVES, true>(vbase, key0 + t * TK, key_end, stage + kTileBytes, wave, lane);
+      load_tile<D, WAVES, false>(kbase, key0 + t * TK, key_end, stage, wave, lane,
+                                 a.gather_k ? posl : nullptr, key0);
+      if (PASS_B)
+        load_tile<D, WAVES, true>(vbase, key0 + t * TK, key_end, stage + kTileBytes, wave, lane,
+                                  a.gather_v ? posl : nullptr, key0);
+    }
+  }
+
+  // Copy of the K tile in stage `cur` to kcopy (rows in key order).
+  __device__ __forceinline__ void copy_k(int t, const char* cur) {
+    const int tile0 = key0 + t * TK;
+    for (int c = threadIdx.x; c < TK * G::CPR; c += WAVES * 64) {
+      const int r = c / G::CPR, ch = c % G::CPR;
+      const int key = tile0 + r;
+      if (key < key_end)
+        *reinterpret_cast<uint4*>(a.kcopy + ((size_t)u * a.nk + key) * D + ch * 8) =
+            *reinterpret_cast<const uint4*>(cur + swz<D>(r, ch));
     }
   }
 
@@ -289,6 +327,7 @@ struct Stream {
     else wait_vmcnt<0>();
     lds_barrier();
     if (MODE == kModeFull && a.colsum && t > 0) flush_colsum(t - 1);
+    if (MODE != kModeFull && a.kcopy) copy_k(t, cur);
     issue(t + NSTAGE - 1, refill);
 
     const int tile0 = key0 + t * TK;
@@ -460,7 +499,7 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : MODE == kModeFull ? 2 
   __shared__ __attribute__((aligned(16))) char stg3[NSTAGE > 3 ? STAGE_BYTES : 16];
   __shared__ __attribute__((aligned(16))) char stg4[NSTAGE > 4 ? STAGE_BYTES : 16];
   __shared__ float colpart[2][WAVES][TK];
-  extern __shared__ __attribute__((aligned(16))) uint4 dyn[];   // retained pass only
+  extern __shared__ __attribute__((aligned(16))) uint4 dyn[];   // retained passes only
 
   Stream<D, WAVES, MODE, NSTAGE> sm{a};
   sm.u = blockIdx.y;
@@ -472,25 +511,39 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : MODE == kModeFull ? 2 
   sm.key0 = s * a.chunk;
   sm.key_end = min(sm.key0 + a.chunk, a.nk);
   sm.ntiles = sm.key_end > sm.key0 ? (sm.key_end - sm.key0 + TK - 1) / TK : 0;
-  sm.kbase = a.k + (size_t)sm.u * a.nk * D;
-  sm.vbase = a.v + (size_t)sm.u * a.nk * D;
+  sm.kbase = a.k + (size_t)sm.u * (a.gather_k ? a.src_rows : (int64_t)a.nk) * D;
+  sm.vbase = a.v + (size_t)sm.u * (a.gather_v ? a.src_rows : (int64_t)a.nk) * D;
   sm.win0 = a.nk - a.w;
   sm.all_rows = a.m == a.mp;
   sm.colpart = colpart;
   sm.xg = dyn;
   sm.fixs = reinterpret_cast<const uint8_t*>(dyn + 2 * NT * 2 * 64);
   const int u = sm.u, wave = sm.wave, l16 = sm.l16, g = sm.g;
+  // dynamic LDS: [retained pass B: fragment exchange, fixed flags] [positions]
+  const int nsl = sm.ntiles * TK;
+  const size_t pos_off = MODE == kModeRetained
+                             ? (size_t)2 * NT * 2 * 64 * sizeof(uint4) + (((size_t)nsl + 15) & ~(size_t)15)
+                             : 0;
+  sm.posl = reinterpret_cast<const int32_t*>(reinterpret_cast<char*>(dyn) + pos_off);
 
   if (MODE == kModeRetained) {
     // fixed flags of this split's slots (padded with "fixed" past the end)
     uint8_t* fl = reinterpret_cast<uint8_t*>(dyn + 2 * NT * 2 * 64);
-    const int nsl = sm.ntiles * TK;
     for (int i = threadIdx.x; i < nsl; i += WAVES * 64) {
       const int key = sm.key0 + i;
       fl[i] = key < sm.key_end ? a.fixed[(size_t)u * a.nk + key] : 1;
     }
-    __syncthreads();
   }
+  if (a.gather_k || a.gather_v) {
+    // source row of each slot, clamped into the source tensor
+    int32_t* pl = reinterpret_cast<int32_t*>(reinterpret_cast<char*>(dyn) + pos_off);
+    for (int i = threadIdx.x; i < nsl; i += WAVES * 64) {
+      const int key = min(sm.key0 + i, sm.key_end - 1);
+      const int64_t r = a.kpos[(size_t)u * a.nk + key];
+      pl[i] = (int32_t)(r < 0 ? 0 : r >= a.src_rows ? a.src_rows - 1 : r);
+    }
+  }
+  if (MODE == kModeRetained || a.gather_k || a.gather_v) __syncthreads();
 
   State<D, MODE, NT> S;
 #pragma unroll
@@ -587,11 +640,16 @@ hipError_t launch_stream_t(const Plan& p, const AttnPass& a, hipStream_t s) {
   k.pmax = a.pmax; k.psum = a.psum; k.lse_log2 = a.lse_log2;
   k.ypart = a.ypart; k.colsum = a.colsum; k.prefix = a.prefix;
   k.fixed = a.fixed; k.npart = a.npart;
+  k.kpos = a.kpos; k.src_rows = a.src_rows;
+  k.gather_k = a.gather_k ? 1 : 0; k.gather_v = a.gather_v ? 1 : 0;
+  k.kcopy = (u16*)a.kcopy;
+  if ((k.gather_k || k.gather_v) && (!a.kpos || a.src_rows < 1)) return hipErrorInvalidValue;
+  const int tk = kTileElems / D;
+  const size_t slots = (size_t)((a.chunk + tk - 1) / tk) * tk;
   size_t dyn = 0;
-  if (MODE == kModeRetained) {
-    const int tk = kTileElems / D;
-    const size_t slots = (size_t)((a.chunk + tk - 1) / tk) * tk;
-    dyn = (size_t)2 * (2 * WAVES) * 2 * 64 * sizeof(uint4) + ((slots + 15) & ~(size_t)15);
+  if (MODE == kModeRetained) dyn = (size_t)2 * (2 * WAVES) * 2 * 64 * sizeof(uint4) + ((slots + 15) & ~(size_t)15);
+  if (k.gather_k || k.gather_v) dyn += slots * sizeof(int32_t);
+  if (dyn) {
     hipError_t e = hipFuncSetAttribute((const void*)stream_kernel<D, WAVES, MODE>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
     if (e != hipSuccess) return e;
