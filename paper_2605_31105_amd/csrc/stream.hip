@@ -242,6 +242,9 @@ struct Stream {
   float (*colpart)[WAVES][TK];
   uint4* xg;                 // retained pass: [2][NT][2][64] fragment exchange
   const uint8_t* fixs;       // retained pass: fixed flags of this split (LDS)
+  // Row tile (16 rows) held as row tile rt of this wave: tiles w and NT-1-w,
+  // which pairs a short and a long row of the Gram matrix's lower triangle.
+  __device__ __forceinline__ int rtile(int rt) const { return rt == 0 ? wave : NT - 1 - wave; }
   const int32_t* posl;       // gathered rows: source row of each slot of this split (LDS)
 
   __device__ __forceinline__ void issue(int t, char* stage) {
@@ -280,8 +283,9 @@ struct Stream {
   }
 
   // Gram contribution of 32 keys (16-key tiles 2kp, 2kp+1): this wave's
-  // X_G fragments (hi/lo) go to LDS, then every wave multiplies its two row
-  // tiles by all NT row tiles.  X_G is P with fixed slots zeroed.
+  // X_G fragments (hi/lo) go to LDS, then every wave forms the lower-triangle
+  // blocks N[I][J], J <= I, of its two row tiles I (NT+1 blocks per wave, the
+  // same count for every wave).  X_G is P with fixed slots zeroed.
   __device__ __forceinline__ void gram_step(int t, int kp, const float (&pv)[NKT][2][4],
                                             State<D, MODE, NT>& S) {
     const int buf = (t * (NKT / 2) + kp) & 1;
@@ -299,20 +303,24 @@ struct Stream {
           x8[4 * h + i] = fixs[kl] ? 0.f : pv[2 * kp + h][rt][i];
         }
       split8(x8, fh[rt], fl[rt]);
-      xb[((2 * wave + rt) * 2 + 0) * 64 + lane] = __builtin_bit_cast(uint4, fh[rt]);
-      xb[((2 * wave + rt) * 2 + 1) * 64 + lane] = __builtin_bit_cast(uint4, fl[rt]);
+      xb[(rtile(rt) * 2 + 0) * 64 + lane] = __builtin_bit_cast(uint4, fh[rt]);
+      xb[(rtile(rt) * 2 + 1) * 64 + lane] = __builtin_bit_cast(uint4, fl[rt]);
     }
     lds_barrier();
+    const int I0 = rtile(0), I1 = rtile(1);   // I0 <= I1
 #pragma unroll
     for (int bt = 0; bt < NT; ++bt) {
+      if (bt > I1) break;   // wave-uniform
       const bf16x8 bh = __builtin_bit_cast(bf16x8, xb[(bt * 2 + 0) * 64 + lane]);
       const bf16x8 bl = __builtin_bit_cast(bf16x8, xb[(bt * 2 + 1) * 64 + lane]);
-#pragma unroll
-      for (int rt = 0; rt < 2; ++rt) {
-        S.n[rt][bt] = mfma_bf16(fh[rt], bh, S.n[rt][bt]);
-        S.n[rt][bt] = mfma_bf16(fh[rt], bl, S.n[rt][bt]);
-        S.n[rt][bt] = mfma_bf16(fl[rt], bh, S.n[rt][bt]);
+      if (bt <= I0) {
+        S.n[0][bt] = mfma_bf16(fh[0], bh, S.n[0][bt]);
+        S.n[0][bt] = mfma_bf16(fh[0], bl, S.n[0][bt]);
+        S.n[0][bt] = mfma_bf16(fl[0], bh, S.n[0][bt]);
       }
+      S.n[1][bt] = mfma_bf16(fh[1], bh, S.n[1][bt]);
+      S.n[1][bt] = mfma_bf16(fh[1], bl, S.n[1][bt]);
+      S.n[1][bt] = mfma_bf16(fl[1], bh, S.n[1][bt]);
     }
   }
 
@@ -505,7 +513,7 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : MODE == kModeFull ? 2 
   sm.u = blockIdx.y;
   const int s = blockIdx.x;
   sm.lane = threadIdx.x & 63;
-  sm.wave = threadIdx.x >> 6;
+  sm.wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
   sm.l16 = sm.lane & 15;
   sm.g = sm.lane >> 4;
   sm.key0 = s * a.chunk;
@@ -548,7 +556,7 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : MODE == kModeFull ? 2 
   State<D, MODE, NT> S;
 #pragma unroll
   for (int rt = 0; rt < 2; ++rt) {
-    const int row = wave * kRowsPerWave + rt * 16 + l16;
+    const int row = sm.rtile(rt) * 16 + l16;
     S.rowok[rt] = row < a.m;
     S.rowwin[rt] = a.causal ? row % a.w : 0x3fffffff;
     const u16* q = a.q + ((size_t)u * a.m + row) * D;
@@ -597,20 +605,25 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : MODE == kModeFull ? 2 
       for (int dt = 0; dt < D / 16; ++dt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int row = wave * kRowsPerWave + rt * 16 + 4 * g + i;
+          const int row = sm.rtile(rt) * 16 + 4 * g + i;
           yp[(size_t)row * D + dt * 16 + l16] = S.y[rt][dt][i];
         }
     if (MODE == kModeRetained) {
+      // lower blocks N[I][J] (J <= I) and their mirrors N[J][I]
       float* np = a.npart + ((size_t)u * a.S + s) * a.mp * a.mp;
 #pragma unroll
       for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
-        for (int bt = 0; bt < (MODE == kModeRetained ? NT : 1); ++bt)
+        for (int bt = 0; bt < (MODE == kModeRetained ? NT : 1); ++bt) {
+          const int I = sm.rtile(rt);
+          if (bt > I) continue;
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int row = wave * kRowsPerWave + rt * 16 + 4 * g + i;
-            np[(size_t)row * a.mp + bt * 16 + l16] = S.n[rt][bt][i];
-          }
+          for (int i = 0; i < 4; ++i)
+            np[(size_t)(I * 16 + 4 * g + i) * a.mp + bt * 16 + l16] = S.n[rt][bt][i];
+          if (bt < I)
+            *reinterpret_cast<float4*>(np + (size_t)(bt * 16 + l16) * a.mp + I * 16 + 4 * g) =
+                make_float4(S.n[rt][bt][0], S.n[rt][bt][1], S.n[rt][bt][2], S.n[rt][bt][3]);
+        }
     }
   } else {
     // merge the four lanes of each row: M = max ref_g, sum = sum_g s_g 2^(ref_g - M)
@@ -620,7 +633,7 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : MODE == kModeFull ? 2 
       float M = max_over_groups(S.mref[rt]);
       double part = (S.mref[rt] == -INFINITY) ? 0.0 : ldexp(S.srun[rt], (int)(S.mref[rt] - M));
       const double tot = sum_over_groups(part);
-      const int row = wave * kRowsPerWave + rt * 16 + l16;
+      const int row = sm.rtile(rt) * 16 + l16;
       if (g == 0) {
         const size_t o = ((size_t)u * a.S + s) * a.mp + row;
         a.pmax[o] = M;
