@@ -58,6 +58,10 @@ typedef enum { GRKV_BF16 = 0, GRKV_F32 = 1 } grkv_dtype;
 /* Per-unit status in stats[u][3]. */
 #define GRKV_UNIT_OK 0
 #define GRKV_UNIT_SINGULAR 1 /* non-positive Cholesky pivot: v_out holds V0 */
+#define GRKV_UNIT_RANGE 2    /* bf16 path: a window row's attention mass on the
+                                retained keys is below 2^-108 of its full-cache
+                                mass (outside the range the path resolves):
+                                v_out holds V0 */
 
 typedef struct {
   int32_t units;    /* U >= 1: number of (layer, KV head) slices */

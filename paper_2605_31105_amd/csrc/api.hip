@@ -105,6 +105,7 @@ int make_plan(const grkv_problem* prob, int64_t n, int32_t window, int32_t budge
   p->x = take(p->fast_merge ? 0 : U * mp * c * sizeof(float));   // generic path only
   p->resid = take(U * mp * d * sizeof(float));
   p->npart = take(U * p->S3 * mp * mp * sizeof(float));
+  p->mpart = take(fast_path ? U * p->S2 * mp * sizeof(float) : 0);
   p->gram = take(U * mp * mp * sizeof(float));
   p->z = take(U * d * mp * sizeof(float));
   p->zhi = take(U * d * mp * 2);
@@ -225,15 +226,17 @@ int grkv_compress(const void* q_obs, const void* K, const void* V, int64_t n, in
   ret.split_p = true;
   ret.fixed = fixed; ret.npart = F(p.npart);
   if (direct) {
-    AttnPass ra = ret;
-    ra.k = K; ra.gather_k = true; ra.src_rows = n; ra.kcopy = out->k_out;
-    GRKV_STAGE(GRKV_STAGE_RET_LSE, pass_a(ra));
+    // one pass over the retained set: K and V rows through idx (K tiles also
+    // copied to k_out), P against the full-cache LSE; the solve normalises by
+    // the retained row sums, so no retained log-sum-exp pass is needed
+    ret.k = K; ret.gather_k = true; ret.kcopy = out->k_out;
     ret.v = V; ret.gather_v = true; ret.src_rows = n;
+    ret.lse_log2 = F(p.lse1_log2); ret.lse_bias = kRetainedBias; ret.mpart = F(p.mpart);
   } else {
     GRKV_STAGE(GRKV_STAGE_RET_LSE, pass_a(ret));
+    GRKV_STAGE(GRKV_STAGE_RET_LSE_COMBINE,
+               launch_lse_combine(p, ret.pmax, ret.psum, p.S2, Dd(p.lse2), F(p.lse2_log2), s));
   }
-  GRKV_STAGE(GRKV_STAGE_RET_LSE_COMBINE,
-             launch_lse_combine(p, ret.pmax, ret.psum, p.S2, Dd(p.lse2), F(p.lse2_log2), s));
   // the generic value step needs X itself, which only the generic pass writes
   GRKV_STAGE(GRKV_STAGE_RET_PROB,
              fast_merge ? launch_stream(p, ret, 2, s) : launch_prob_pass(p, ret, s));
@@ -244,9 +247,11 @@ int grkv_compress(const void* q_obs, const void* K, const void* V, int64_t n, in
   if (!fast_merge) GRKV_STAGE(GRKV_STAGE_GRAM, launch_gram(p, F(p.x), fixed, F(p.npart), s));
   if (fast_merge) {
     GRKV_STAGE(GRKV_STAGE_SOLVE,
-               launch_solve(p, F(p.ypart), F(p.xvpart), F(p.npart), F(p.y), F(p.resid),
-                            F(p.gram), F(p.z), (uint16_t*)(ws + p.zhi), (uint16_t*)(ws + p.zlo),
-                            F(p.stats_ws), out->stats, s));
+               launch_solve(p, F(p.ypart), F(p.xvpart), F(p.npart),
+                            direct ? F(p.mpart) : nullptr, F(p.lse1_log2), kRetainedBias,
+                            F(p.lse2_log2), F(p.y), F(p.resid), F(p.gram), F(p.z),
+                            (uint16_t*)(ws + p.zhi), (uint16_t*)(ws + p.zlo), F(p.stats_ws),
+                            out->stats, s));
     GRKV_STAGE(GRKV_STAGE_UPDATE,
                launch_update(p, q_obs, out->k_out, F(p.lse2_log2), fixed,
                              (const uint16_t*)(ws + p.zhi),

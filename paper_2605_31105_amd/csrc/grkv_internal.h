@@ -13,6 +13,10 @@ namespace grkv {
 constexpr int kRowsPerWave = 32;   // each wave owns 32 stacked window rows
 constexpr int kKeyTile = 32;       // keys per streamed tile
 constexpr int kSelectThreads = 1024;
+// The fast retained pass forms P = 2^(t - LSE + kRetainedBias) against the
+// full-cache log-sum-exp: retained attention masses down to 2^-108 stay
+// well inside the float range (P <= 2^48, Gram entries <= 2^96).
+constexpr float kRetainedBias = 48.f;
 
 // Everything a call needs, derived on the host from the arguments.
 struct Plan {
@@ -32,7 +36,7 @@ struct Plan {
   bool fast_merge;
   // workspace offsets (bytes)
   size_t pmax1, psum1, lse1, lse1_log2, ypart, y, colsum, pooled, fixed, v0c;
-  size_t pmax2, psum2, lse2, lse2_log2, xvpart, x, resid, npart, gram, z, zhi, zlo, stats_ws;
+  size_t pmax2, psum2, lse2, lse2_log2, xvpart, x, resid, npart, mpart, gram, z, zhi, zlo, stats_ws;
   size_t total;
 };
 
@@ -66,6 +70,10 @@ struct AttnPass {
   bool gather_k, gather_v;
   int64_t src_rows;
   void* kcopy;
+  // retained pass B (fast path): P = 2^(t - (lse_log2 - lse_bias)) against
+  // the full-cache LSE, with its row sums in mpart [U][S][mp]
+  float lse_bias;
+  float* mpart;
 };
 
 hipError_t launch_lse_pass(const Plan& p, const AttnPass& a, hipStream_t s);
@@ -96,10 +104,14 @@ hipError_t launch_gram(const Plan& p, const float* x, const uint8_t* fixed,
 // partials (writing y, resid and gram) and solves by blocked Cholesky; then
 // v_out = V0 + X_G^T Z is written in one pass from the compact V0 copy.
 bool merge_fast_supported(const Plan& p);
+// mpart: row sums of the retained P partials [U][S2][mp] when P was formed
+// against the full-cache LSE lse1_log2 scaled by 2^lse_bias (X = P / row sum;
+// the retained LSE is written to lse2_log2), or null when X itself was used.
 hipError_t launch_solve(const Plan& p, const float* ypart, const float* xvpart,
-                        const float* npart, float* y, float* resid, float* gram, float* z,
-                        uint16_t* zhi, uint16_t* zlo, float* stats_ws, float* stats_user,
-                        hipStream_t s);
+                        const float* npart, const float* mpart, const float* lse1_log2,
+                        float lse_bias, float* lse2_log2, float* y, float* resid,
+                        float* gram, float* z, uint16_t* zhi, uint16_t* zlo,
+                        float* stats_ws, float* stats_user, hipStream_t s);
 // X is recomputed from q_obs, K0 (k_out) and the retained log-sum-exp; V0
 // rows are read from V [U][n][d] through idx.
 hipError_t launch_update(const Plan& p, const void* q, const void* k0,

@@ -203,6 +203,7 @@ __device__ __forceinline__ bool factor_diag(const float* blk, float* inv, int la
 template <int MP, int D>
 __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
     const float* ypart, int S1, const float* xvpart, int S2, const float* npart, int S3,
+    const float* mpart, const float* lse1_log2, float lse_bias, float* lse2_log2,
     float* y, float* resid, float* gram, float* z, u16* zhi, u16* zlo, float* stats_ws,
     float* stats_user, int m, float lam) {
   constexpr int NP = MP / 16;   // panels
@@ -215,11 +216,38 @@ __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
   __shared__ __attribute__((aligned(16))) float B[MP * BS];
   __shared__ __attribute__((aligned(16))) float Li[NP * 16 * LS];
   __shared__ double red[3][kSolveWaves];
-  __shared__ int fail;
+  __shared__ float inv_mass[MP];
+  __shared__ int fail, range_fail;
 
   const int u = blockIdx.x, tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, l16 = lane & 15, g = lane >> 4;
-  if (tid == 0) fail = 0;
+  if (tid == 0) fail = range_fail = 0;
+  __syncthreads();
+
+  // 0. retained masses: the retained pass forms P against the full-cache
+  // log-sum-exp (scaled by 2^lse_bias), so X = P / (row sum of P).  Its
+  // log-sum-exp (log2 domain) goes to lse2_log2 for the update.  A row whose
+  // retained mass is below 2^-60 after the scaling is outside the range this
+  // path resolves: the unit reports GRKV_UNIT_RANGE.
+  for (int r = tid; r < MP; r += kSolveWaves * 64) {
+    float inv = 1.f;
+    if (mpart) {
+      float ms = 0.f;
+      for (int s2 = 0; s2 < S2; ++s2) ms += mpart[((size_t)u * S2 + s2) * MP + r];
+      inv = 0.f;
+      if (r < m) {
+        if (ms >= 0x1p-60f && ms < __builtin_huge_valf()) {
+          inv = 1.f / ms;
+          lse2_log2[(size_t)u * MP + r] = lse1_log2[(size_t)u * MP + r] - lse_bias + __log2f(ms);
+        } else {
+          range_fail = 1;
+          lse2_log2[(size_t)u * MP + r] = 0.f;
+        }
+      }
+    }
+    inv_mass[r] = inv;
+  }
+  __syncthreads();
 
   // 1. combine the partials; every thread issues the loads of two elements
   // before it sums them, which keeps more of them in flight
@@ -249,8 +277,9 @@ __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
         const int e = e0 + h * NTH;
         if (e >= E) break;
         const int r = e / (D / 4), c4 = (e % (D / 4)) * 4;
-        float4 rv = make_float4(yv[h].x - xv[h].x, yv[h].y - xv[h].y, yv[h].z - xv[h].z,
-                                yv[h].w - xv[h].w);
+        const float im = inv_mass[r];
+        float4 rv = make_float4(yv[h].x - im * xv[h].x, yv[h].y - im * xv[h].y,
+                                yv[h].z - im * xv[h].z, yv[h].w - im * xv[h].w);
         float4 yy = yv[h];
         if (r >= m) yy = rv = make_float4(0.f, 0.f, 0.f, 0.f);
         yo[e] = yy;
@@ -273,6 +302,7 @@ __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
         const int col = c4 + k;
+        vv[k] *= inv_mass[r] * inv_mass[col];
         if (r >= m || col >= m) vv[k] = 0.f;
         if (r == col) vv[k] += r < m ? lam : 1.f;
       }
@@ -333,7 +363,7 @@ __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
   }
   if (wave == 0 && lane == 0 && !ok_local) fail = 1;
   __syncthreads();
-  const bool ok = fail == 0;
+  const bool ok = fail == 0 && range_fail == 0;
 
   // 3. forward and backward substitution, 16 right-hand-side columns per wave;
   // tile rows 16t + 4g + i, column c0 + l16 live in r[t][i]
@@ -418,7 +448,8 @@ __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
     const double dn = Y2 > 0 ? Y2 : 1.0;
     const double dbefore = R2 / dn;
     const double dafter = ok ? (double)lam * lam * Z2 / dn : dbefore;
-    const float st[4] = {(float)Y2, (float)dbefore, (float)dafter, ok ? 0.f : (float)GRKV_UNIT_SINGULAR};
+    const float st[4] = {(float)Y2, (float)dbefore, (float)dafter,
+                         range_fail ? (float)GRKV_UNIT_RANGE : ok ? 0.f : (float)GRKV_UNIT_SINGULAR};
     for (int k = 0; k < 4; ++k) {
       stats_ws[u * 4 + k] = st[k];
       if (stats_user) stats_user[u * 4 + k] = st[k];
@@ -653,11 +684,13 @@ hipError_t launch_gram_w(const Plan& p, const float* x, const uint8_t* fixed, fl
 
 template <int MP, int D>
 hipError_t launch_solve_t(const Plan& p, const float* ypart, const float* xvpart,
-                          const float* npart, float* y, float* resid, float* gram, float* z,
-                          u16* zhi, u16* zlo, float* stats_ws, float* stats_user, hipStream_t s) {
+                          const float* npart, const float* mpart, const float* lse1_log2,
+                          float lse_bias, float* lse2_log2, float* y, float* resid, float* gram,
+                          float* z, u16* zhi, u16* zlo, float* stats_ws, float* stats_user,
+                          hipStream_t s) {
   hipLaunchKernelGGL((solve_kernel<MP, D>), dim3(p.U), dim3(kSolveWaves * 64), 0, s, ypart, p.S1,
-                     xvpart, p.S2, npart, p.S3, y, resid, gram, z, zhi, zlo, stats_ws, stats_user,
-                     p.m, p.lam);
+                     xvpart, p.S2, npart, p.S3, mpart, lse1_log2, lse_bias, lse2_log2, y, resid,
+                     gram, z, zhi, zlo, stats_ws, stats_user, p.m, p.lam);
   return hipGetLastError();
 }
 
@@ -707,12 +740,14 @@ hipError_t launch_gram(const Plan& p, const float* x, const uint8_t* fixed, floa
 }
 
 hipError_t launch_solve(const Plan& p, const float* ypart, const float* xvpart, const float* npart,
-                        float* y, float* resid, float* gram, float* z, u16* zhi, u16* zlo,
-                        float* stats_ws, float* stats_user, hipStream_t s) {
+                        const float* mpart, const float* lse1_log2, float lse_bias,
+                        float* lse2_log2, float* y, float* resid, float* gram, float* z, u16* zhi,
+                        u16* zlo, float* stats_ws, float* stats_user, hipStream_t s) {
 #define GRKV_SOLVE(MPV, DV)                                                                   \
   if (p.mp == MPV && p.d == DV)                                                               \
-    return launch_solve_t<MPV, DV>(p, ypart, xvpart, npart, y, resid, gram, z, zhi, zlo,        \
-                                   stats_ws, stats_user, s);
+    return launch_solve_t<MPV, DV>(p, ypart, xvpart, npart, mpart, lse1_log2, lse_bias,         \
+                                   lse2_log2, y, resid, gram, z, zhi, zlo, stats_ws,            \
+                                   stats_user, s);
   GRKV_SOLVE(32, 64) GRKV_SOLVE(32, 128) GRKV_SOLVE(64, 64) GRKV_SOLVE(64, 128)
   GRKV_SOLVE(128, 64) GRKV_SOLVE(128, 128)
 #undef GRKV_SOLVE

@@ -52,6 +52,8 @@ struct StreamK {
   int prefix;
   const uint8_t* fixed;   // retained pass: fixed flag per retained slot
   float* npart;           // retained pass: Gram partials [U][S][mp][mp]
+  float* mpart;           // retained pass: row sums of P [U][S][mp]
+  float lse_bias;         // pass B: P = 2^(t - (lse_log2 - lse_bias))
   // retained passes: rows of K (gather_k) and/or V (gather_v) are read
   // through kpos [U][nk] from tensors of src_rows rows per unit
   const int32_t* kpos;
@@ -220,6 +222,7 @@ struct State {
   float mref[2];   // pass A: per-lane reference exponent (an integer, or -inf
                    // before the lane's first visible key)
   double srun[2];  // pass A: per-lane sum of 2^(t - mref) over this lane's keys
+  float msum[2];   // retained pass B: per-lane row sum of P over this lane's keys
   f32x4 y[2][MODE != kModeLse ? D / 16 : 1];
   f32x4 n[2][MODE == kModeRetained ? NT : 1];   // Gram rows of this wave
 };
@@ -448,6 +451,17 @@ struct Stream {
       if (NKT * 4 == 16 || (l16 & 1) == 0)
         colpart[t & 1][wave][(v >> 2) * 16 + 4 * g + (v & 3)] = c;
     }
+    if (MODE == kModeRetained && a.mpart) {
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt) {
+        float acc = 0.f;
+#pragma unroll
+        for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) acc += pv[kt][rt][i];
+        S.msum[rt] += acc;
+      }
+    }
     const char* vt = cur + kTileBytes;
     const int e = l16 >> 2, qq = l16 & 3;
 #pragma unroll
@@ -564,7 +578,8 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : MODE == kModeFull ? 2 
     for (int ks = 0; ks < D / 32; ++ks)
       S.qb[rt][ks] = S.rowok[rt] ? *reinterpret_cast<const uint4*>(q + ks * 32 + 8 * g)
                                  : make_uint4(0, 0, 0, 0);
-    S.lse[rt] = PASS_B ? a.lse_log2[(size_t)u * a.mp + row] : 0.f;
+    S.lse[rt] = PASS_B ? a.lse_log2[(size_t)u * a.mp + row] - a.lse_bias : 0.f;
+    S.msum[rt] = 0.f;
     S.mref[rt] = -INFINITY;
     S.srun[rt] = 0.0;
 #pragma unroll
@@ -609,6 +624,16 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : MODE == kModeFull ? 2 
           yp[(size_t)row * D + dt * 16 + l16] = S.y[rt][dt][i];
         }
     if (MODE == kModeRetained) {
+      if (a.mpart) {
+        // row sums: the four lane groups of a row hold disjoint keys
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt) {
+          float v = S.msum[rt];
+          v += __shfl_xor(v, 16);
+          v += __shfl_xor(v, 32);
+          if (g == 0) a.mpart[((size_t)u * a.S + s) * a.mp + sm.rtile(rt) * 16 + l16] = v;
+        }
+      }
       // lower blocks N[I][J] (J <= I) and their mirrors N[J][I]
       float* np = a.npart + ((size_t)u * a.S + s) * a.mp * a.mp;
 #pragma unroll
@@ -652,7 +677,7 @@ hipError_t launch_stream_t(const Plan& p, const AttnPass& a, hipStream_t s) {
   k.scale_log2 = (float)(1.4426950408889634 / __builtin_sqrt((double)D));
   k.pmax = a.pmax; k.psum = a.psum; k.lse_log2 = a.lse_log2;
   k.ypart = a.ypart; k.colsum = a.colsum; k.prefix = a.prefix;
-  k.fixed = a.fixed; k.npart = a.npart;
+  k.fixed = a.fixed; k.npart = a.npart; k.mpart = a.mpart; k.lse_bias = a.lse_bias;
   k.kpos = a.kpos; k.src_rows = a.src_rows;
   k.gather_k = a.gather_k ? 1 : 0; k.gather_v = a.gather_v ? 1 : 0;
   k.kcopy = (u16*)a.kcopy;
