@@ -127,20 +127,26 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(SelK a) {
   }
 }
 
-constexpr int kSmallThreads = 512;
-constexpr int kSmallPer = 64;   // pooled scores per thread: prefixes up to 32768
+constexpr int kSmallThreads = 1024;
+constexpr int kSmallPer = 32;          // pooled scores per thread: prefixes up to 32768
+constexpr uint32_t kCandCap = 4096;    // candidates finished by one wave (64 per lane)
 
-// Block-wide sum of one value per thread (kSmallThreads threads); `part` holds
-// 2 x 8 words and alternates by `parity` so consecutive calls need one barrier.
-// Within a wave: DPP sums over 16-lane rows, then the four row totals.
-__device__ __forceinline__ uint32_t block_sum_small(uint32_t v, uint32_t (*part)[8], int parity) {
+// Sum over the 64 lanes of a wave, in every lane (DPP within 16-lane rows,
+// then the four row totals).
+__device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
   int x = (int)v;
   x += __builtin_amdgcn_update_dpp(0, x, 0xB1, 0xF, 0xF, false);
   x += __builtin_amdgcn_update_dpp(0, x, 0x4E, 0xF, 0xF, false);
   x += __builtin_amdgcn_update_dpp(0, x, 0x141, 0xF, 0xF, false);
   x += __builtin_amdgcn_update_dpp(0, x, 0x140, 0xF, 0xF, false);
-  v = (uint32_t)(__builtin_amdgcn_readlane(x, 0) + __builtin_amdgcn_readlane(x, 16) +
-                 __builtin_amdgcn_readlane(x, 32) + __builtin_amdgcn_readlane(x, 48));
+  return (uint32_t)(__builtin_amdgcn_readlane(x, 0) + __builtin_amdgcn_readlane(x, 16) +
+                    __builtin_amdgcn_readlane(x, 32) + __builtin_amdgcn_readlane(x, 48));
+}
+
+// Block-wide sum of one value per thread; `part` holds 2 x 16 words and
+// alternates by `parity`, so consecutive calls need one barrier each.
+__device__ __forceinline__ uint32_t block_sum_small(uint32_t v, uint32_t (*part)[16], int parity) {
+  v = wave_sum(v);
   if ((threadIdx.x & 63) == 0) part[parity][threadIdx.x >> 6] = v;
   __syncthreads();
   uint32_t tot = 0;
@@ -149,17 +155,30 @@ __device__ __forceinline__ uint32_t block_sum_small(uint32_t v, uint32_t (*part)
   return tot;
 }
 
+// State of one k-th-largest search over the keys (fp32 bit patterns of
+// non-negative scores, which order like the values): lo <= T < hi with
+// clo = count(>= lo) >= k > count(>= hi) = chi.
+struct Bracket {
+  uint32_t lo, hi, clo, chi;
+};
+
 // Same selection for prefixes of at most 32768 tokens, with each thread
-// keeping 64 consecutive pooled scores in registers.  The k-th largest score
-// is found by bisection on the fp32 bit pattern (scores are >= 0, so bit
-// patterns order like values): 31 block-wide counts of "score >= mid", no
-// histograms and no atomics.
+// keeping 32 consecutive pooled scores in registers.  The (c-w)-th largest
+// score T0 is found by bisection on the bit patterns: block-wide counts of
+// "score >= mid" from the [min, max] bracket until at most kCandCap keys
+// remain inside it; those candidates go to LDS and radix rounds (256 bins of
+// the bit pattern's offset in the bracket) finish.  The floor(beta*c)-th
+// largest T1 lies among the keys >= T0 (about c-w of them), so it starts
+// from the candidates directly.
 __global__ __launch_bounds__(kSmallThreads) void select_small_kernel(SelK a) {
   __shared__ float sl[kSmallThreads * kSmallPer + kSmallThreads * kSmallPer / 64];
-  __shared__ uint32_t part[2][8];
+  __shared__ uint32_t part[2][16];
   __shared__ uint32_t scan_scratch[16];
+  __shared__ uint32_t sh[8];
+  __shared__ uint32_t hist[256];
   constexpr int PER = kSmallPer;
-  const int u = blockIdx.x, tid = threadIdx.x;
+  const int u = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int P = a.prefix;
   const float* s = a.colsum + (size_t)u * P;
   float* pg = a.pooled + (size_t)u * P;
@@ -167,17 +186,29 @@ __global__ __launch_bounds__(kSmallThreads) void select_small_kernel(SelK a) {
   uint8_t* fixed = a.fixed + (size_t)u * a.c;
   const int j0 = tid * PER;
 
-  // Positions past the prefix get key 0 (score 0.0): they rank after every
-  // real position with an equal score, so they are never taken while real
-  // positions are left.
-  // Scores of the whole prefix into LDS (coalesced), stored with one pad word
-  // per 64 entries so that the 64 lanes of a wave, each reading its own
-  // contiguous run, fall on distinct banks.  Each thread then takes its 64
-  // positions plus 8 on either side into registers and pools them, summing
-  // s[j-h..j+h] left to right.
-  for (int t = tid; t < P; t += kSmallThreads) sl[t + (t >> 6)] = s[t];
+  // Scores of the whole prefix into LDS (coalesced), one pad word per 64
+  // entries so that the lanes of a wave, each reading its own contiguous
+  // run, fall on distinct banks.  Each thread then pools its 32 positions
+  // (plus 8 on either side) in registers, summing s[j-h..j+h] left to right.
+  // Positions past the prefix get key 0: they rank after every real position
+  // with an equal score and are never taken while real positions are left.
+  {
+    // all PER loads of a thread in flight at once
+    float ld[PER];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int t = tid + k * kSmallThreads;
+      ld[k] = t < P ? s[t] : 0.f;
+    }
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int t = tid + k * kSmallThreads;
+      sl[t + (t >> 6)] = ld[k];
+    }
+  }
   __syncthreads();
   uint32_t key[PER];
+  uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
   {
     float v[PER + 16];
 #pragma unroll
@@ -194,6 +225,10 @@ __global__ __launch_bounds__(kSmallThreads) void select_small_kernel(SelK a) {
       for (int t = -8; t <= 8; ++t)   // offsets -h..h in increasing order
         if (t >= -h && t <= h) acc += v[q + 8 + t];
       key[q] = j < P ? __float_as_uint(acc) : 0u;
+      if (j < P) {
+        kmin = min(kmin, key[q]);
+        kmax = max(kmax, key[q]);
+      }
     }
   }
   // the pooled scores (an intermediate the caller may inspect), coalesced
@@ -203,38 +238,134 @@ __global__ __launch_bounds__(kSmallThreads) void select_small_kernel(SelK a) {
   __syncthreads();
   for (int t = tid; t < P; t += kSmallThreads) pg[t] = sl[t + (t >> 6)];
 
-  // count of keys >= x over the block
-  int parity = 0;
-  auto count_ge = [&](uint32_t x0, uint32_t x1, uint32_t* c0, uint32_t* c1) {
-    uint32_t n0 = 0, n1 = 0;
+  // key range of the real positions (block min and max)
+  {
+    uint32_t mn = kmin, mx = kmax;
 #pragma unroll
-    for (int q = 0; q < PER; ++q) {
-      n0 += key[q] >= x0;
-      n1 += key[q] >= x1;
+    for (int off = 32; off > 0; off >>= 1) {
+      mn = min(mn, (uint32_t)__shfl_xor((int)mn, off));
+      mx = max(mx, (uint32_t)__shfl_xor((int)mx, off));
     }
-    *c0 = block_sum_small(n0 | (n1 << 16), part, parity);
-    parity ^= 1;
-    *c1 = *c0 >> 16;
-    *c0 &= 0xFFFF;
-  };
-  // largest T with count(>= T) >= k, for k = s_sel (0) and n_top (1)
-  uint32_t lo0 = 0, hi0 = 0x7F800001u, lo1 = 0, hi1 = 0x7F800001u;
-  const uint32_t k0 = (uint32_t)a.s_sel, k1 = (uint32_t)a.n_top;
-#pragma unroll 1
-  for (int it = 0; it < 32; ++it) {
-    const bool go0 = k0 > 0 && hi0 - lo0 > 1, go1 = k1 > 0 && hi1 - lo1 > 1;
-    if (!go0 && !go1) break;   // uniform: every thread holds the same bounds
-    const uint32_t m0 = lo0 + (hi0 - lo0) / 2, m1 = lo1 + (hi1 - lo1) / 2;
-    uint32_t c0, c1;
-    count_ge(m0, m1, &c0, &c1);
-    if (go0) { if (c0 >= k0) lo0 = m0; else hi0 = m0; }
-    if (go1) { if (c1 >= k1) lo1 = m1; else hi1 = m1; }
+    if (lane == 0) {
+      part[0][wave] = mn;
+      part[1][wave] = mx;
+    }
+    __syncthreads();
+    kmin = 0xFFFFFFFFu;
+    kmax = 0u;
+#pragma unroll
+    for (int k = 0; k < kSmallThreads / 64; ++k) {
+      kmin = min(kmin, part[0][k]);
+      kmax = max(kmax, part[1][k]);
+    }
+    __syncthreads();   // part is reused below
   }
-  const uint32_t T0 = lo0, T1 = lo1;
-  uint32_t gt0, gt1;
-  count_ge(T0 + 1, T1 + 1, &gt0, &gt1);
+  kmax = min(kmax, 0x7F800000u);   // +inf at most (no NaN scores)
+  uint32_t* cand = reinterpret_cast<uint32_t*>(sl);   // [kCandCap], reuses the staging area
+  int parity = 0;
+
+  // k-th largest key from bracket b: block rounds while more than kCandCap
+  // keys lie in [lo, hi), then the candidates into LDS and radix rounds.
+  // Returns T with b.lo = T, b.hi = T + 1 (so b.chi = count(> T) and
+  // b.clo = count(>= T)).
+  auto kth = [&](uint32_t k, Bracket b) -> Bracket {
+#pragma unroll 1
+    for (int it = 0; it < 33 && b.hi - b.lo > 1 && b.clo - b.chi > kCandCap; ++it) {
+      const uint32_t mid = b.lo + (b.hi - b.lo) / 2;
+      uint32_t n = 0;
+#pragma unroll
+      for (int q = 0; q < PER; ++q) n += key[q] >= mid;
+      const uint32_t c = block_sum_small(n, part, parity);
+      parity ^= 1;
+      if (c >= k) { b.lo = mid; b.clo = c; }
+      else { b.hi = mid; b.chi = c; }
+    }
+    if (b.hi - b.lo <= 1) return b;
+    uint32_t n = 0;
+#pragma unroll
+    for (int q = 0; q < PER; ++q) n += key[q] >= b.lo && key[q] < b.hi;
+    uint32_t tot;
+    uint32_t o = block_exclusive_scan(n, scan_scratch, &tot);
+#pragma unroll
+    for (int q = 0; q < PER; ++q)
+      if (key[q] >= b.lo && key[q] < b.hi) {
+        if (o < kCandCap) cand[o] = key[q];
+        ++o;
+      }
+    __syncthreads();
+    // Radix rounds on the candidates: 256 bins of (x - lo) >> shift cover
+    // [lo, hi); the bin holding the k-th largest becomes the new bracket.  A
+    // 32-bit range takes at most four rounds.
+    const uint32_t L = min(b.clo - b.chi, kCandCap);
+#pragma unroll 1
+    for (int it = 0; it < 5 && b.hi - b.lo > 1; ++it) {
+      const uint32_t width = b.hi - b.lo;
+      const int bits = 32 - __builtin_clz(width - 1);   // width - 1 < 2^bits
+      const int shift = bits > 8 ? bits - 8 : 0;
+      if (tid < 256) hist[tid] = 0u;
+      __syncthreads();
+      for (uint32_t e = tid; e < L; e += kSmallThreads) {
+        const uint32_t x = cand[e];
+        if (x >= b.lo && x < b.hi) atomicAdd(&hist[(x - b.lo) >> shift], 1u);
+      }
+      __syncthreads();
+      if (wave == 0) {
+        // suffix sums over the bins: lane l holds bins 4l .. 4l+3
+        uint32_t h4[4], suf = 0;
+#pragma unroll
+        for (int i = 3; i >= 0; --i) {
+          h4[i] = hist[4 * lane + i];
+          suf += h4[i];
+        }
+        // inclusive suffix scan across lanes (lanes above l)
+        uint32_t incl = suf;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+          const uint32_t o = (uint32_t)__shfl_down((int)incl, off);
+          if (lane + off < 64) incl += o;
+        }
+        // count(>= start of bin 4l + i) = chi + (bins above) ; the largest bin
+        // whose count reaches k holds the k-th largest
+        uint32_t above = b.chi + incl - suf;   // keys in bins > 4l+3, plus those >= hi
+        int best = -1;
+        uint32_t bc = 0, bh = 0;
+#pragma unroll
+        for (int i = 3; i >= 0; --i) {
+          const uint32_t c = above + h4[i];
+          if (best < 0 && c >= k) { best = 4 * lane + i; bc = c; bh = above; }
+          above = c;
+        }
+        // the highest lane with a hit owns the answer
+        const uint64_t hit = __ballot(best >= 0);
+        const int owner = 63 - __builtin_clzll(hit);
+        if (lane == owner) {
+          const uint32_t nlo = b.lo + ((uint32_t)best << shift);
+          const uint64_t nhi = (uint64_t)b.lo + ((uint64_t)(best + 1) << shift);
+          sh[0] = nlo;
+          sh[1] = nhi < b.hi ? (uint32_t)nhi : b.hi;
+          sh[2] = bc;
+          sh[3] = bh;
+        }
+      }
+      __syncthreads();
+      b.lo = sh[0]; b.hi = sh[1]; b.clo = sh[2]; b.chi = sh[3];
+      __syncthreads();   // hist and sh are rewritten by the next round
+    }
+    return b;
+  };
+
+  const uint32_t k0 = (uint32_t)a.s_sel, k1 = (uint32_t)a.n_top;
   const bool any0 = k0 > 0, any1 = k1 > 0;
-  const uint32_t krem0 = k0 - gt0, krem1 = k1 - gt1;   // ties taken, lowest positions first
+  // count(>= kmin) = P (the padding keys, 0, count only when kmin is 0)
+  const uint32_t all = kmin > 0 ? (uint32_t)P : (uint32_t)(kSmallThreads * PER);
+  Bracket b0 = {kmin, kmax + 1, all, 0u};
+  if (any0) b0 = kth(k0, b0);
+  // the n_top-th largest is at least T0 (n_top <= s_sel)
+  Bracket b1 = any0 ? Bracket{b0.lo, kmax + 1, b0.clo, 0u} : Bracket{kmin, kmax + 1, all, 0u};
+  if (any1) b1 = kth(k1, b1);
+  const uint32_t T0 = b0.lo, T1 = b1.lo;
+  // ties taken, lowest positions first
+  const uint32_t krem0 = k0 - b0.chi, krem1 = k1 - b1.chi;
 
   uint32_t eq0 = 0, eq1 = 0;
 #pragma unroll
@@ -245,23 +376,9 @@ __global__ __launch_bounds__(kSmallThreads) void select_small_kernel(SelK a) {
   if (!any0) eq0 = 0;
   if (!any1) eq1 = 0;
   uint32_t tot;
-  const uint32_t eqb0 = block_exclusive_scan(eq0, scan_scratch, &tot);
-  const uint32_t eqb1 = block_exclusive_scan(eq1, scan_scratch, &tot);
-  uint32_t nsel = 0;
-  {
-    uint32_t e0 = eqb0;
-#pragma unroll
-    for (int q = 0; q < PER; ++q) {
-      const bool sel = key[q] > T0 || (key[q] == T0 && e0 < krem0);
-      e0 += key[q] == T0;
-      nsel += sel;
-    }
-    if (!any0) nsel = 0;
-  }
-  uint32_t off = block_exclusive_scan(nsel, scan_scratch, &tot);
-  // selection and top-beta membership as bit masks over this thread's positions,
-  // then the selected positions in increasing order
-  uint64_t selm = 0, topm = 0;
+  const uint32_t eqb = block_exclusive_scan(eq0 | (eq1 << 16), scan_scratch, &tot);
+  const uint32_t eqb0 = eqb & 0xFFFF, eqb1 = eqb >> 16;
+  uint32_t selm = 0, topm = 0;
   {
     uint32_t e0 = eqb0, e1 = eqb1;
 #pragma unroll
@@ -270,21 +387,23 @@ __global__ __launch_bounds__(kSmallThreads) void select_small_kernel(SelK a) {
       const bool top = key[q] > T1 || (key[q] == T1 && e1 < krem1);
       e0 += key[q] == T0;
       e1 += key[q] == T1;
-      selm |= (uint64_t)sel << q;
-      topm |= (uint64_t)top << q;
+      selm |= (uint32_t)sel << q;
+      topm |= (uint32_t)top << q;
     }
   }
   if (!any0) selm = 0;
   if (!any1) topm = 0;
+  uint32_t off = block_exclusive_scan(__builtin_popcount(selm), scan_scratch, &tot);
+  // the selected positions in increasing order
   while (selm) {
-    const int q = __builtin_ctzll(selm);
+    const int q = __builtin_ctz(selm);
     const int j = j0 + q;
     idx[off] = j;
     fixed[off] = (j < a.n_sink || ((topm >> q) & 1)) ? 1 : 0;
     ++off;
     selm &= selm - 1;
   }
-  for (int i = tid; i < a.w; i += blockDim.x) {
+  for (int i = tid; i < a.w; i += kSmallThreads) {
     const int64_t pos = a.n - a.w + i;
     idx[a.s_sel + i] = (int32_t)pos;
     fixed[a.s_sel + i] = (a.fix_window || pos < a.n_sink) ? 1 : 0;
