@@ -109,18 +109,21 @@ typedef struct {
 } grkv_outputs;
 
 /* Stages of one call, in launch order (indices into stage_events / 2).  A stage
- * that a given call does not run (the fast bf16 path folds FULL_Y, RESID and
- * GRAM into neighbouring stages) leaves its two events unrecorded. */
+ * that a given call does not run leaves its two events unrecorded: the bf16
+ * path (head_dim 64/128, G*w <= 128) folds FULL_Y, RESID and GRAM into
+ * neighbouring stages, reads the retained rows inside RET_PROB (no GATHER) and
+ * forms the retained softmax from the full-cache log-sum-exp (no RET_LSE). */
 enum {
-  GRKV_STAGE_FULL_LSE = 0,     /* full-cache pass A: row max / sum-exp per split */
+  GRKV_STAGE_FULL_LSE = 0,     /* full-cache pass A: reference / sum-exp per split */
   GRKV_STAGE_FULL_LSE_COMBINE, /* -> log-sum-exp of every window row */
   GRKV_STAGE_FULL_PROB,        /* full-cache pass B: P.V partials, SnapKV column sums */
   GRKV_STAGE_FULL_Y,           /* -> Y */
   GRKV_STAGE_SELECT,           /* pooling, top-k, fixed set */
-  GRKV_STAGE_GATHER,           /* K0 -> k_out, V0 -> v_out */
-  GRKV_STAGE_RET_LSE,          /* retained-cache pass A */
+  GRKV_STAGE_GATHER,           /* K0 -> k_out, V0 (generic path) */
+  GRKV_STAGE_RET_LSE,          /* retained-cache pass A (generic path) */
   GRKV_STAGE_RET_LSE_COMBINE,
-  GRKV_STAGE_RET_PROB,         /* retained-cache pass B: X and X V0 partials */
+  GRKV_STAGE_RET_PROB,         /* retained-cache pass B: X V0 (and on the bf16 path
+                                  K0 -> k_out, Gram and retained-mass partials) */
   GRKV_STAGE_RESID,            /* R = Y - X V0 */
   GRKV_STAGE_GRAM,             /* N partials */
   GRKV_STAGE_SOLVE,            /* (Y, R, N combines,) Cholesky, Z, stats */

@@ -1,7 +1,7 @@
 // Value step of the ridge merge in its Woodbury dual form (Eq. 8; Algorithm 1,
 // value step; App. D.1, fixed tokens App. D.3):
 //   N = X_G X_G^T + lambda I_m   (gram: partial sums over column splits)
-//   Z = N^-1 R                   (solve: elimination in registers and LDS)
+//   Z = N^-1 R                   (solve: blocked Cholesky on fp32 MFMA)
 //   V*_G = V0_G + X_G^T Z        (update: fixed columns keep V0)
 // On this fast path the Gram partials come from the retained-cache pass
 // (stream.hip); the gram kernel here serves the generic path.
