@@ -65,14 +65,23 @@ int make_plan(const grkv_problem* prob, int64_t n, int32_t window, int32_t budge
   p->lam = lambda;
   p->opt = o;
 
-  // Target about 1024 blocks per launch (four per CU) for the streaming passes.
-  int64_t target = 1024;
-  if (const char* e = getenv("GRKV_TARGET_BLOCKS")) target = atoll(e);   // tuning experiments
+  // Target about 1024 blocks per launch (four per CU) for the full-cache
+  // streaming passes, and about one block per CU for the bf16 retained pass
+  // (which holds one block per CU): fewer splits mean fewer partials for the
+  // solve to combine.
+  int64_t target = 1024, target_ret = 256;
+  if (const char* e = getenv("GRKV_TARGET_BLOCKS")) target = atoll(e);       // tuning experiments
+  if (const char* e = getenv("GRKV_TARGET_RET_BLOCKS")) target_ret = atoll(e);
   const int64_t want = ceil_div(target, p->U);
   split_range(n, want, 512, &p->S1, &p->chunk1);
-  split_range(budget, want, 128, &p->S2, &p->chunk2);
-  if (p->chunk2 > 8192) split_range(budget, ceil_div(budget, 8192), 128, &p->S2, &p->chunk2);
   p->fast_merge = merge_fast_supported(*p);
+  if (p->fast_merge) {
+    split_range(budget, ceil_div(target_ret, p->U), 128, &p->S2, &p->chunk2);
+    if (p->chunk2 > 4096) split_range(budget, ceil_div(budget, 4096), 128, &p->S2, &p->chunk2);
+  } else {
+    split_range(budget, want, 128, &p->S2, &p->chunk2);
+    if (p->chunk2 > 8192) split_range(budget, ceil_div(budget, 8192), 128, &p->S2, &p->chunk2);
+  }
   if (p->fast_merge) {
     p->S3 = p->S2;
     p->chunk3 = p->chunk2;

@@ -250,9 +250,29 @@ __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
   __syncthreads();
 
   // 1. combine the partials; every thread issues the loads of two elements
-  // before it sums them, which keeps more of them in flight
+  // and four splits at a time before it sums them (in split order), which
+  // keeps them in flight together
   double sy = 0.0, sr = 0.0, sz = 0.0;
   auto add4 = [](float4& a, const float4 b) { a.x += b.x; a.y += b.y; a.z += b.z; a.w += b.w; };
+  // acc[h] += sum over s < S of p[s * stride + e[h]], h = 0, 1, in order of s
+  auto sum_parts = [&](const float4* __restrict__ p, size_t stride, int S, const int (&e)[2],
+                       float4 (&acc)[2]) {
+    int s = 0;
+    for (; s + 4 <= S; s += 4) {
+      float4 v[4][2];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) v[i][h] = p[(size_t)(s + i) * stride + e[h]];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) add4(acc[h], v[i][h]);
+    }
+    for (; s < S; ++s)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) add4(acc[h], p[(size_t)s * stride + e[h]]);
+  };
   {
     constexpr int E = MP * D / 4;
     const float4* __restrict__ yp = reinterpret_cast<const float4*>(ypart) + (size_t)u * S1 * E;
@@ -264,14 +284,9 @@ __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
 #pragma unroll
       for (int h = 0; h < 2; ++h) yv[h] = xv[h] = make_float4(0.f, 0.f, 0.f, 0.f);
       const int e1 = min(e0 + NTH, E - 1);   // the second element, clamped (stored only if < E)
-      for (int s = 0; s < S1; ++s) {
-        add4(yv[0], yp[(size_t)s * E + e0]);
-        add4(yv[1], yp[(size_t)s * E + e1]);
-      }
-      for (int s = 0; s < S2; ++s) {
-        add4(xv[0], xp[(size_t)s * E + e0]);
-        add4(xv[1], xp[(size_t)s * E + e1]);
-      }
+      const int ee[2] = {e0, e1};
+      sum_parts(yp, E, S1, ee, yv);
+      sum_parts(xp, E, S2, ee, xv);
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const int e = e0 + h * NTH;
@@ -294,9 +309,15 @@ __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
     constexpr int E = MP * MP / 4;
     const float4* __restrict__ np = reinterpret_cast<const float4*>(npart) + (size_t)u * S3 * E;
     float4* __restrict__ go = reinterpret_cast<float4*>(gram) + (size_t)u * E;
-    for (int e = tid; e < E; e += NTH) {
-      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-      for (int s = 0; s < S3; ++s) add4(v, np[(size_t)s * E + e]);
+    for (int e2 = tid; e2 < E; e2 += 2 * NTH) {
+     float4 v2[2] = {make_float4(0.f, 0.f, 0.f, 0.f), make_float4(0.f, 0.f, 0.f, 0.f)};
+     const int ee[2] = {e2, min(e2 + NTH, E - 1)};
+     sum_parts(np, E, S3, ee, v2);
+#pragma unroll
+     for (int h = 0; h < 2; ++h) {
+      const int e = e2 + h * NTH;
+      if (e >= E) break;
+      const float4 v = v2[h];
       const int r = e / (MP / 4), c4 = (e % (MP / 4)) * 4;
       float vv[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
@@ -309,6 +330,7 @@ __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
       const float4 o = make_float4(vv[0], vv[1], vv[2], vv[3]);
       go[e] = o;
       *reinterpret_cast<float4*>(A + r * AS + c4) = o;
+     }
     }
   }
   __syncthreads();

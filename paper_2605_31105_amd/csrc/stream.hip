@@ -511,8 +511,9 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : MODE == kModeFull ? 2 
   constexpr bool PASS_B = MODE != kModeLse;
   constexpr int TK = G::TK, NT = 2 * WAVES;
   // ring depth: pass A 5 x 8 KB (four blocks per CU at 4 waves per SIMD);
-  // pass B 3 x 16 KB (a fourth stage measured slower)
-  constexpr int NSTAGE = MODE == kModeLse ? 5 : 3;
+  // pass B 3 x 16 KB (a fourth stage measured slower); retained pass 5 x 16 KB
+  // (the retained pass runs one block per CU, so its ring is deeper)
+  constexpr int NSTAGE = MODE == kModeFull ? 3 : 5;
   static_assert(NSTAGE == 3 || NSTAGE == 5, "ring depths with an unrolled loop below");
   constexpr int STAGE_BYTES = kTileBytes * (PASS_B ? 2 : 1);
   __shared__ __attribute__((aligned(16))) char stg0[STAGE_BYTES];
