@@ -102,6 +102,7 @@ int make_plan(const grkv_problem* prob, int64_t n, int32_t window, int32_t budge
   p->colsum = take(U * (P > 0 ? P : 1) * sizeof(float));
   p->pooled = take(U * (P > 0 ? P : 1) * sizeof(float));
   p->fixed = take(U * c);
+  p->redo = take(U * p->S1 * sizeof(int32_t));
   // the compact V0 copy serves the generic retained passes only; the fast
   // path reads V0 rows through idx
   const bool fast_path = stream_supported(*p) && merge_fast_supported(*p);
@@ -204,6 +205,7 @@ int grkv_compress(const void* q_obs, const void* K, const void* V, int64_t n, in
   full.lse = Dd(p.lse1); full.lse_log2 = F(p.lse1_log2);
   full.ypart = F(p.ypart); full.colsum = p.prefix > 0 ? F(p.colsum) : nullptr;
   full.prefix = p.prefix; full.xout = nullptr; full.split_p = true;
+  full.redo = (int*)(ws + p.redo);
   const bool fast = stream_supported(p);
   auto pass_a = [&](const AttnPass& a) { return fast ? launch_stream(p, a, 0, s) : launch_lse_pass(p, a, s); };
   auto pass_b = [&](const AttnPass& a) { return fast ? launch_stream(p, a, 1, s) : launch_prob_pass(p, a, s); };

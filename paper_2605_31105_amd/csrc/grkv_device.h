@@ -19,6 +19,14 @@ __device__ __forceinline__ f32x4 mfma_bf16(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+
+// The same tile shape with fp16 operands.
+__device__ __forceinline__ f32x4 mfma_f16(f16x8 a, f16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
+
 // 16x16 output tile, K = 4 fp32: lane l holds A[l%16][l/16], B[l/16][l%16].
 __device__ __forceinline__ f32x4 mfma_f32(float a, float b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
@@ -53,6 +61,25 @@ __device__ __forceinline__ void split8(const float* x, bf16x8& hi, bf16x8& lo) {
     lo[i] = l[0];
     lo[i + 1] = l[1];
   }
+}
+
+// Round-to-nearest-even conversion of 8 floats to fp16.
+__device__ __forceinline__ f16x8 to_f16x8(const float* x) {
+  f16x8 h;
+#pragma unroll
+  for (int i = 0; i < 8; i += 2) {
+    const f16x2 p = __builtin_convertvector((f32x2){x[i], x[i + 1]}, f16x2);
+    h[i] = p[0];
+    h[i + 1] = p[1];
+  }
+  return h;
+}
+
+// Two bf16 values (one 32-bit word) to two fp16 values, round to nearest even
+// (exact when the magnitudes lie in fp16's normal range).
+__device__ __forceinline__ uint32_t bf16x2_to_f16x2(uint32_t w) {
+  const f32x2 f = {__uint_as_float(w << 16), __uint_as_float(w & 0xffff0000u)};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, f16x2));
 }
 
 // Sum over the 16 lanes that share l/16 (lanes differing in bits 0..3).

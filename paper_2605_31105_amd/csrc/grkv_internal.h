@@ -35,7 +35,7 @@ struct Plan {
   int S3, chunk3;
   bool fast_merge;
   // workspace offsets (bytes)
-  size_t pmax1, psum1, lse1, lse1_log2, ypart, y, colsum, pooled, fixed, v0c;
+  size_t pmax1, psum1, lse1, lse1_log2, ypart, y, colsum, pooled, fixed, v0c, redo;
   size_t pmax2, psum2, lse2, lse2_log2, xvpart, x, resid, npart, mpart, gram, z, zhi, zlo, stats_ws;
   size_t total;
 };
@@ -74,6 +74,9 @@ struct AttnPass {
   // the full-cache LSE, with its row sums in mpart [U][S][mp]
   float lse_bias;
   float* mpart;
+  // full-cache pass B (bf16 streaming): per-split flags [U][S] of the fp16
+  // P.V pass; flagged splits are recomputed exactly
+  int* redo;
 };
 
 hipError_t launch_lse_pass(const Plan& p, const AttnPass& a, hipStream_t s);

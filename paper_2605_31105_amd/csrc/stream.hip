@@ -54,6 +54,7 @@ struct StreamK {
   float* npart;           // retained pass: Gram partials [U][S][mp][mp]
   float* mpart;           // retained pass: row sums of P [U][S][mp]
   float lse_bias;         // pass B: P = 2^(t - (lse_log2 - lse_bias))
+  int* redo;              // full-cache pass B: per-split flag [U][S] (see the modes)
   // retained passes: rows of K (gather_k) and/or V (gather_v) are read
   // through kpos [U][nk] from tensors of src_rows rows per unit
   const int32_t* kpos;
@@ -156,53 +157,62 @@ __device__ __forceinline__ int swz(int r, int ch) {
   return (r * Geo<D>::CPR + (ch ^ swz_key<D, VT>(r))) * 16;
 }
 
-// Issues this wave's share of the direct-to-LDS loads of one tensor tile.
-// Rows at or past key_end are clamped to key_end-1 (finite data, masked later).
-// A whole tile (the common case) is addressed as a uniform tile base plus a
-// per-lane byte offset that does not change from tile to tile, so the loads
-// take a scalar base and cost no vector instructions per tile.
-// With `pos` (LDS, one source row per key slot of the block, starting at
-// slot key0) the rows are gathered: slot key reads source row pos[key - key0].
+// Direct-to-LDS loads of one tensor tile; each wave issues its share, one
+// 16-byte chunk per lane and 1 KB of LDS per wave instruction.
+//
+// A whole tile (the common case) is one buffer load per instruction against a
+// buffer resource based at the block's first key: a per-lane 32-bit offset
+// that is the same for every tile (row and swizzled chunk inside the tile)
+// plus a scalar tile offset, so the loop spends no vector instructions or
+// 64-bit address registers on it.  The resource's byte range ends at key_end,
+// so nothing past the block's keys can be read.
 template <int D, int WAVES, bool VT>
-__device__ __forceinline__ void load_tile(const u16* base, int tile0, int key_end, char* lds_tile,
-                                          int wave, int lane, const int32_t* pos = nullptr,
-                                          int key0 = 0) {
+struct TileLoads {
+  using G = Geo<D>;
+  static constexpr int PER = G::INSTR / WAVES;
+  __amdgpu_buffer_rsrc_t res;
+  uint32_t off[PER];
+
+  __device__ __forceinline__ void init(const u16* base, int key0, int key_end, int wave, int lane) {
+    const int nbytes = (key_end > key0 ? key_end - key0 : 0) * D * 2;
+    res = __builtin_amdgcn_make_buffer_rsrc((void*)(base + (size_t)key0 * D), (short)0, nbytes,
+                                            0x00020000);
+#pragma unroll
+    for (int it = 0; it < PER; ++it) {
+      const int r = (wave * PER + it) * G::RPI + lane / G::CPR;
+      const int ch = (lane % G::CPR) ^ swz_key<D, VT>(r);
+      off[it] = (uint32_t)(r * D + ch * 8) * 2u;
+    }
+  }
+
+  // whole tile starting `tkey` keys after the block's first key
+  __device__ __forceinline__ void whole(int tkey, char* lds_tile, int wave) const {
+#pragma unroll
+    for (int it = 0; it < PER; ++it)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(res, (lds_void*)(lds_tile + (wave * PER + it) * 1024),
+                                               16, (int)off[it], tkey * D * 2, 0, 0);
+  }
+};
+
+// The last, partial tile of a block: rows at or past key_end are clamped to
+// key_end-1 (finite data, masked later).  With `pos` (LDS, one source row per
+// key slot of the block, starting at slot key0) the rows are gathered: slot
+// key reads source row pos[key - key0].
+template <int D, int WAVES, bool VT>
+__device__ __forceinline__ void load_tile_rows(const u16* base, int tile0, int key_end, char* lds_tile,
+                                               int wave, int lane, const int32_t* pos = nullptr,
+                                               int key0 = 0) {
   using G = Geo<D>;
   constexpr int PER = G::INSTR / WAVES;
-  if (pos) {
-#pragma unroll
-    for (int it = 0; it < PER; ++it) {
-      const int instr = wave * PER + it;
-      const int r = instr * G::RPI + lane / G::CPR;
-      const int ch = (lane % G::CPR) ^ swz_key<D, VT>(r);
-      int key = tile0 + r;
-      key = key < key_end ? key : key_end - 1;
-      const u16* src = base + (size_t)pos[key - key0] * D + ch * 8;
-      __builtin_amdgcn_global_load_lds(src, (lds_void*)(lds_tile + instr * 1024), 16, 0, 0);
-    }
-    return;
-  }
-  if (tile0 + G::TK <= key_end) {
-    const char* tb = reinterpret_cast<const char*>(base + (size_t)tile0 * D);
-#pragma unroll
-    for (int it = 0; it < PER; ++it) {
-      const int instr = wave * PER + it;
-      const int r = instr * G::RPI + lane / G::CPR;
-      const int ch = (lane % G::CPR) ^ swz_key<D, VT>(r);
-      const uint32_t voff = (uint32_t)(r * D + ch * 8) * 2u;
-      __builtin_amdgcn_global_load_lds(tb + voff, (lds_void*)(lds_tile + instr * 1024), 16, 0, 0);
-    }
-    return;
-  }
 #pragma unroll
   for (int it = 0; it < PER; ++it) {
     const int instr = wave * PER + it;
     const int r = instr * G::RPI + lane / G::CPR;       // row inside the tile
-    const int p = lane % G::CPR;                        // physical chunk in the row
-    const int ch = p ^ swz_key<D, VT>(r);               // logical chunk stored there
+    const int ch = (lane % G::CPR) ^ swz_key<D, VT>(r); // logical chunk stored there
     int key = tile0 + r;
     key = key < key_end ? key : key_end - 1;
-    const u16* src = base + (size_t)key * D + ch * 8;
+    const int64_t row = pos ? (int64_t)pos[key - key0] : (int64_t)key;
+    const u16* src = base + (size_t)row * D + ch * 8;
     __builtin_amdgcn_global_load_lds(src, (lds_void*)(lds_tile + instr * 1024), 16, 0, 0);
   }
 }
@@ -210,7 +220,20 @@ __device__ __forceinline__ void load_tile(const u16* base, int tile0, int key_en
 // Kernel modes: pass A (log-sum-exp partials), pass B over the full cache
 // (P.V partials and SnapKV column sums), pass B over the retained set (P.V
 // partials and the Gram matrix X_G X_G^T of the fixed-masked probabilities).
-enum { kModeLse = 0, kModeFull = 1, kModeRetained = 2 };
+//  * kModeFull: P.V in fp16 (fp16 P times the fp16-converted V tile); a split
+//    whose P.V comes out non-finite (a V element beyond the fp16 range) sets
+//    its redo flag;
+//  * kModeFullExact: P as a bf16 hi+lo pair times the bf16 V tile, run on the
+//    splits whose redo flag is set (the other blocks exit at once).
+enum { kModeLse = 0, kModeFull = 1, kModeRetained = 2, kModeFullExact = 3 };
+
+template <int MODE>
+constexpr bool is_full() { return MODE == kModeFull || MODE == kModeFullExact; }
+
+template <bool B>
+struct BoolTag {
+  static constexpr bool value = B;
+};
 
 // Per-block state of one (unit, split) stream.
 template <int D, int MODE, int NT>
@@ -250,13 +273,51 @@ struct Stream {
   __device__ __forceinline__ int rtile(int rt) const { return rt == 0 ? wave : NT - 1 - wave; }
   const int32_t* posl;       // gathered rows: source row of each slot of this split (LDS)
 
+  TileLoads<D, WAVES, false> kld;
+  TileLoads<D, WAVES, true> vld;
+  // Per-lane LDS byte offsets inside a tile, computed once: K operand chunk
+  // ks of key row l16 (key tile kt adds kt*16 rows), and the V transpose-read
+  // address of column block dt for key row 4g + l16/4 (key pair kp adds 32
+  // rows, the second half 16 rows).  The swizzle keys depend only on the row
+  // modulo 8 or 16, so those row steps are plain constant offsets.
+  uint32_t koff[D / 32];
+  uint32_t voff[D / 16];
+
+  __device__ __forceinline__ void init_offsets() {
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) koff[ks] = (uint32_t)swz<D>(l16, ks * 4 + g);
+    const int e = l16 >> 2, qq = l16 & 3;
+#pragma unroll
+    for (int dt = 0; dt < D / 16; ++dt) {
+      const int col = dt * 16 + 4 * qq;
+      voff[dt] = (uint32_t)(swz<D, true>(4 * g + e, col >> 3) + (col & 7) * 2);
+    }
+  }
+  __device__ __forceinline__ const uint4* kaddr(const char* cur, int kt, int ks) const {
+    const uint32_t o = koff[ks];
+    __builtin_assume(o < kTileBytes);
+    return reinterpret_cast<const uint4*>(cur + o + kt * 16 * D * 2);
+  }
+
   __device__ __forceinline__ void issue(int t, char* stage) {
-    if (t < ntiles) {
-      load_tile<D, WAVES, false>(kbase, key0 + t * TK, key_end, stage, wave, lane,
-                                 a.gather_k ? posl : nullptr, key0);
-      if (PASS_B)
-        load_tile<D, WAVES, true>(vbase, key0 + t * TK, key_end, stage + kTileBytes, wave, lane,
-                                  a.gather_v ? posl : nullptr, key0);
+    if (t >= ntiles) return;
+    const int tile0 = key0 + t * TK;
+    if constexpr (MODE == kModeRetained) {
+      // gathered rows (retained set read through its positions)
+      if (a.gather_k || a.gather_v || tile0 + TK > key_end) {
+        load_tile_rows<D, WAVES, false>(kbase, tile0, key_end, stage, wave, lane,
+                                        a.gather_k ? posl : nullptr, key0);
+        load_tile_rows<D, WAVES, true>(vbase, tile0, key_end, stage + kTileBytes, wave, lane,
+                                       a.gather_v ? posl : nullptr, key0);
+        return;
+      }
+    }
+    if (tile0 + TK <= key_end) {
+      kld.whole(t * TK, stage, wave);
+      if (PASS_B) vld.whole(t * TK, stage + kTileBytes, wave);
+    } else {
+      load_tile_rows<D, WAVES, false>(kbase, tile0, key_end, stage, wave, lane);
+      if (PASS_B) load_tile_rows<D, WAVES, true>(vbase, tile0, key_end, stage + kTileBytes, wave, lane);
     }
   }
 
@@ -327,8 +388,32 @@ struct Stream {
     }
   }
 
+  // Full-cache pass B with fp16 P.V: tile t is computed while this thread's
+  // share of tile t+1 (already complete) is converted to fp16; tiles t+2 and
+  // t+3 are in flight (a four-stage ring).  The barrier at the start of each
+  // step publishes the conversion made in the step before.
+  __device__ __forceinline__ void step_f16(int t, char* cur, char* nxt, char* refill,
+                                           State<D, MODE, NT>& S) {
+    static_assert(NSTAGE == 4, "four-stage ring");
+    if (t >= ntiles) return;
+    if (t + 2 < ntiles) wait_vmcnt<LOADS>();   // tile t+2 may stay in flight
+    else wait_vmcnt<0>();
+    lds_barrier();
+    if (a.colsum && t > 0) flush_colsum(t - 1);
+    issue(t + 3, refill);
+    if (t + 1 < ntiles) v_to_f16(nxt + kTileBytes);
+    // keep the scheduler from hoisting the tile's loads above the conversion
+    // (register pressure)
+    __builtin_amdgcn_sched_barrier(0);
+    const int tile0 = key0 + t * TK;
+    const bool interior = all_rows && tile0 + TK <= key_end && tile0 + TK <= win0;
+    if (interior) body_full<true, true>(t, tile0, cur, S);
+    else body_full<false, true>(t, tile0, cur, S);
+  }
+
   // One tile: wait for it, refill the stage freed last step, compute.
-  __device__ __forceinline__ void step(int t, const char* cur, char* refill,
+  template <bool F16>
+  __device__ __forceinline__ void step(int t, char* cur, char* refill,
                                        State<D, MODE, NT>& S) {
     if (t >= ntiles) return;
     const int ahead = min(ntiles - 1 - t, NSTAGE - 2);
@@ -337,18 +422,35 @@ struct Stream {
     else if (ahead == 1) wait_vmcnt<LOADS>();
     else wait_vmcnt<0>();
     lds_barrier();
-    if (MODE == kModeFull && a.colsum && t > 0) flush_colsum(t - 1);
-    if (MODE != kModeFull && a.kcopy) copy_k(t, cur);
+    if (is_full<MODE>() && a.colsum && t > 0) flush_colsum(t - 1);
+    if (MODE == kModeRetained && a.kcopy) copy_k(t, cur);
     issue(t + NSTAGE - 1, refill);
 
     const int tile0 = key0 + t * TK;
-    f32x4 st[NKT][2];
+    // An interior tile has every key valid and outside the window, and the
+    // block has no padding rows: nothing to mask.
+    const bool interior = all_rows && tile0 + TK <= key_end && tile0 + TK <= win0;
+    if constexpr (is_full<MODE>()) {
+      if (interior) body_full<true, F16>(t, tile0, cur, S);
+      else body_full<false, F16>(t, tile0, cur, S);
+    } else {
+      f32x4 st[NKT][2];
+      logits(cur, S, st);
+      if (interior) body<true>(t, tile0, cur, st, S);
+      else body<false>(t, tile0, cur, st, S);
+    }
+  }
+
+  // Logits of the tile in stage `cur` for this wave's two row tiles:
+  // st[kt][rt] = K[16 keys of kt] . Q[16 rows of rt]^T.
+  __device__ __forceinline__ void logits(const char* cur, const State<D, MODE, NT>& S,
+                                         f32x4 (&st)[NKT][2]) {
     uint4 kv[D / 32][NKT];
 #pragma unroll
     for (int ks = 0; ks < D / 32; ++ks)
 #pragma unroll
       for (int kt = 0; kt < NKT; ++kt)
-        kv[ks][kt] = *reinterpret_cast<const uint4*>(cur + swz<D>(kt * 16 + l16, ks * 4 + g));
+        kv[ks][kt] = *kaddr(cur, kt, ks);
 #pragma unroll
     for (int kt = 0; kt < NKT; ++kt) st[kt][0] = st[kt][1] = zero4();
 #pragma unroll
@@ -358,11 +460,118 @@ struct Stream {
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt)
           st[kt][rt] = mfma_bf16(as_bf16x8(kv[ks][kt]), as_bf16x8(S.qb[rt][ks]), st[kt][rt]);
-    // An interior tile has every key valid and outside the window, and the
-    // block has no padding rows: nothing to mask.
-    const bool interior = all_rows && tile0 + TK <= key_end && tile0 + TK <= win0;
-    if (interior) body<true>(t, tile0, cur, st, S);
-    else body<false>(t, tile0, cur, st, S);
+  }
+
+  // bf16 -> fp16 in place for this thread's share of the V tile at vt (the
+  // element order, and so the swizzle, is unchanged).  Exact for magnitudes in
+  // [2^-14, 65504]; smaller ones become fp16 subnormals (absolute error at
+  // most 2^-25), larger ones overflow to infinity, which the caller detects.
+  __device__ __forceinline__ void v_to_f16(char* vt) {
+    constexpr int CH = kTileBytes / 16, PER = CH / (WAVES * 64);
+    static_assert(PER * WAVES * 64 == CH, "whole chunks per thread");
+    uint4 x[PER];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) x[k] = *reinterpret_cast<const uint4*>(vt + (threadIdx.x + k * WAVES * 64) * 16);
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      x[k].x = bf16x2_to_f16x2(x[k].x);
+      x[k].y = bf16x2_to_f16x2(x[k].y);
+      x[k].z = bf16x2_to_f16x2(x[k].z);
+      x[k].w = bf16x2_to_f16x2(x[k].w);
+      *reinterpret_cast<uint4*>(vt + (threadIdx.x + k * WAVES * 64) * 16) = x[k];
+    }
+  }
+
+  // V operand fragment of keys 32kp + (4g + e, +16), columns dt*16 + 4q..+3
+  // (lane 4e + q of group g supplies the address), by the LDS transpose read.
+  __device__ __forceinline__ uint4 v_frag(const char* vt, int kp, int dt) const {
+    const uint32_t o = voff[dt];
+    __builtin_assume(o < kTileBytes);
+    const char* p0 = vt + o + kp * 32 * D * 2;
+    v4i16 b0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)p0);
+    v4i16 b1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(p0 + 16 * D * 2));
+    return __builtin_bit_cast(uint4, (v8i16){b0[0], b0[1], b0[2], b0[3], b1[0], b1[1], b1[2], b1[3]});
+  }
+
+  // Full-cache pass B on one tile, ordered by row tile so that the VALU work
+  // of one row tile (exponentials, operand packing) can run beside the MFMAs
+  // of the other.  F16: P.V as fp16 P times the fp16 V tile (one MFMA per
+  // fragment); otherwise P as a bf16 hi+lo pair times the bf16 V tile.
+  template <bool INTERIOR, bool F16>
+  __device__ __forceinline__ void body_full(int t, int tile0, const char* cur,
+                                            State<D, MODE, NT>& S) {
+    uint4 kv[D / 32][NKT];
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks)
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt)
+        kv[ks][kt] = *kaddr(cur, kt, ks);
+    f32x4 st[2][NKT];
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt) {
+        st[rt][kt] = zero4();
+#pragma unroll
+        for (int ks = 0; ks < D / 32; ++ks)
+          st[rt][kt] = mfma_bf16(as_bf16x8(kv[ks][kt]), as_bf16x8(S.qb[rt][ks]), st[rt][kt]);
+      }
+    // V operand fragments of the whole tile (shared by both row tiles), read
+    // once the K fragments are dead
+    const char* vt = cur + kTileBytes;
+    uint4 b[NKT / 2][D / 16];
+#pragma unroll
+    for (int kp = 0; kp < NKT / 2; ++kp)
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt) b[kp][dt] = v_frag(vt, kp, dt);
+    float pv[2][NKT][4];
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt) {
+#pragma unroll
+      for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float x = fast_exp2(fmaf(st[rt][kt][i], a.scale_log2, -S.lse[rt]));
+          if (INTERIOR) {
+            pv[rt][kt][i] = x;
+          } else {
+            const int key = tile0 + kt * 16 + 4 * g + i;
+            pv[rt][kt][i] = (S.rowok[rt] && key < key_end && key - win0 <= S.rowwin[rt]) ? x : 0.f;
+          }
+        }
+#pragma unroll
+      for (int kp = 0; kp < NKT / 2; ++kp) {
+        const float x8[8] = {pv[rt][2 * kp][0], pv[rt][2 * kp][1], pv[rt][2 * kp][2],
+                             pv[rt][2 * kp][3], pv[rt][2 * kp + 1][0], pv[rt][2 * kp + 1][1],
+                             pv[rt][2 * kp + 1][2], pv[rt][2 * kp + 1][3]};
+        if constexpr (F16) {
+          const f16x8 ph = to_f16x8(x8);
+#pragma unroll
+          for (int dt = 0; dt < D / 16; ++dt)
+            S.y[rt][dt] = mfma_f16(ph, __builtin_bit_cast(f16x8, b[kp][dt]), S.y[rt][dt]);
+        } else {
+          bf16x8 ahi, alo;
+          split8(x8, ahi, alo);
+#pragma unroll
+          for (int dt = 0; dt < D / 16; ++dt) {
+            S.y[rt][dt] = mfma_bf16(ahi, as_bf16x8(b[kp][dt]), S.y[rt][dt]);
+            S.y[rt][dt] = mfma_bf16(alo, as_bf16x8(b[kp][dt]), S.y[rt][dt]);
+          }
+        }
+      }
+    }
+    // column sums over this wave's 32 rows: the two row tiles first, then the
+    // 16 lanes of each DPP row (one reduce-scatter; lane l16 ends with key
+    // v = kt*4 + i of its group, v taken from the high bits of l16; with 8
+    // values both lanes of a pair hold the same sum and store it)
+    float cs[NKT * 4];
+#pragma unroll
+    for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) cs[kt * 4 + i] = pv[0][kt][i] + pv[1][kt][i];
+    int v;
+    const float c = row_reduce_scatter<NKT * 4>(cs, l16, &v);
+    colpart[t & 1][wave][(v >> 2) * 16 + 4 * g + (v & 3)] = c;
   }
 
   // The tile's work after the logits.  INTERIOR skips every mask.
@@ -437,20 +646,6 @@ struct Stream {
           const float e = fast_exp2(fmaf(st[kt][rt][i], a.scale_log2, -S.lse[rt]));
           pv[kt][rt][i] = ok[kt][rt][i] ? e : 0.f;
         }
-    if (MODE == kModeFull && a.colsum) {
-      // column sums over this wave's 32 rows: the two row tiles first, then
-      // the 16 lanes of each DPP row (one reduce-scatter; lane l16 ends with
-      // key v = kt*4 + i of its group, v taken from the high bits of l16)
-      float cs[NKT * 4];
-#pragma unroll
-      for (int kt = 0; kt < NKT; ++kt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) cs[kt * 4 + i] = pv[kt][0][i] + pv[kt][1][i];
-      int v;
-      const float c = row_reduce_scatter<NKT * 4>(cs, l16, &v);
-      if (NKT * 4 == 16 || (l16 & 1) == 0)
-        colpart[t & 1][wave][(v >> 2) * 16 + 4 * g + (v & 3)] = c;
-    }
     if (MODE == kModeRetained && a.mpart) {
 #pragma unroll
       for (int rt = 0; rt < 2; ++rt) {
@@ -463,7 +658,6 @@ struct Stream {
       }
     }
     const char* vt = cur + kTileBytes;
-    const int e = l16 >> 2, qq = l16 & 3;
 #pragma unroll
     for (int kp = 0; kp < NKT / 2; ++kp) {
       bf16x8 ahi[2], alo[2];
@@ -479,19 +673,9 @@ struct Stream {
           for (int q = 0; q < 8; ++q) ahi[rt][q] = (__bf16)x8[q];
         }
       }
-      // lane 4e+q of group g supplies key row 32kp + 4g + e (and +16), columns dt*16 + 4q..+3
-      const int r0 = 32 * kp + 4 * g + e;
       bf16x8 b[D / 16];
 #pragma unroll
-      for (int dt = 0; dt < D / 16; ++dt) {
-        const int col = dt * 16 + 4 * qq;
-        v4i16 b0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (lds_v4i16*)(vt + swz<D, true>(r0, col >> 3) + (col & 7) * 2));
-        v4i16 b1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-            (lds_v4i16*)(vt + swz<D, true>(r0 + 16, col >> 3) + (col & 7) * 2));
-        b[dt] = __builtin_bit_cast(bf16x8, (v8i16){b0[0], b0[1], b0[2], b0[3],
-                                                   b1[0], b1[1], b1[2], b1[3]});
-      }
+      for (int dt = 0; dt < D / 16; ++dt) b[dt] = as_bf16x8(v_frag(vt, kp, dt));
 #pragma unroll
       for (int dt = 0; dt < D / 16; ++dt)
 #pragma unroll
@@ -506,15 +690,15 @@ struct Stream {
 
 template <int D, int WAVES, int MODE>
 __global__ __launch_bounds__(WAVES * 64)
-__attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : MODE == kModeFull ? 2 : 1))) void stream_kernel(StreamK a) {
+__attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : is_full<MODE>() ? 2 : 1))) void stream_kernel(StreamK a) {
   using G = Geo<D>;
   constexpr bool PASS_B = MODE != kModeLse;
   constexpr int TK = G::TK, NT = 2 * WAVES;
   // ring depth: pass A 5 x 8 KB (four blocks per CU at 4 waves per SIMD);
-  // pass B 3 x 16 KB (a fourth stage measured slower); retained pass 5 x 16 KB
-  // (the retained pass runs one block per CU, so its ring is deeper)
-  constexpr int NSTAGE = MODE == kModeFull ? 3 : 5;
-  static_assert(NSTAGE == 3 || NSTAGE == 5, "ring depths with an unrolled loop below");
+  // pass B 4 x 16 KB (one stage holds the tile whose V is being converted);
+  // retained pass 5 x 16 KB (one block per CU, so its ring is deeper)
+  constexpr int NSTAGE = is_full<MODE>() ? 4 : 5;
+  static_assert(NSTAGE == 4 || NSTAGE == 5, "ring depths with an unrolled loop below");
   constexpr int STAGE_BYTES = kTileBytes * (PASS_B ? 2 : 1);
   __shared__ __attribute__((aligned(16))) char stg0[STAGE_BYTES];
   __shared__ __attribute__((aligned(16))) char stg1[STAGE_BYTES];
@@ -524,6 +708,7 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : MODE == kModeFull ? 2 
   __shared__ float colpart[2][WAVES][TK];
   extern __shared__ __attribute__((aligned(16))) uint4 dyn[];   // retained passes only
 
+  if (MODE == kModeFullExact && !a.redo[(size_t)blockIdx.y * a.S + blockIdx.x]) return;
   Stream<D, WAVES, MODE, NSTAGE> sm{a};
   sm.u = blockIdx.y;
   const int s = blockIdx.x;
@@ -538,6 +723,10 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : MODE == kModeFull ? 2 
   sm.vbase = a.v + (size_t)sm.u * (a.gather_v ? a.src_rows : (int64_t)a.nk) * D;
   sm.win0 = a.nk - a.w;
   sm.all_rows = a.m == a.mp;
+  sm.init_offsets();
+  // (the gathered retained pass does not use these)
+  sm.kld.init(sm.kbase, sm.key0, sm.key_end, sm.wave, sm.lane);
+  if (PASS_B) sm.vld.init(sm.vbase, sm.key0, sm.key_end, sm.wave, sm.lane);
   sm.colpart = colpart;
   sm.xg = dyn;
   sm.fixs = reinterpret_cast<const uint8_t*>(dyn + 2 * NT * 2 * 64);
@@ -589,31 +778,66 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : MODE == kModeFull ? 2 
     for (int bt = 0; bt < (MODE == kModeRetained ? NT : 1); ++bt) S.n[rt][bt] = zero4();
   }
 
-  sm.issue(0, stg0);
-  sm.issue(1, stg1);
-  if constexpr (NSTAGE == 5) {
+  auto run = [&](auto f16) {
+    constexpr bool F16 = decltype(f16)::value;
+    sm.issue(0, stg0);
+    sm.issue(1, stg1);
     sm.issue(2, stg2);
-    sm.issue(3, stg3);
-  }
-  for (int t = 0; t < sm.ntiles; t += NSTAGE) {
-    if constexpr (NSTAGE == 3) {
-      sm.step(t + 0, stg0, stg2, S);
-      sm.step(t + 1, stg1, stg0, S);
-      sm.step(t + 2, stg2, stg1, S);
+    if constexpr (NSTAGE == 5) sm.issue(3, stg3);
+    if constexpr (F16) {
+      // tile 0 converted before the loop (published by step 0's barrier)
+      if (sm.ntiles > 2) wait_vmcnt<2 * decltype(sm)::LOADS>();
+      else if (sm.ntiles > 1) wait_vmcnt<decltype(sm)::LOADS>();
+      else wait_vmcnt<0>();
+      lds_barrier();
+      if (sm.ntiles > 0) sm.v_to_f16(stg0 + kTileBytes);
+      for (int t = 0; t < sm.ntiles; t += 4) {
+        sm.step_f16(t + 0, stg0, stg1, stg3, S);
+        sm.step_f16(t + 1, stg1, stg2, stg0, S);
+        sm.step_f16(t + 2, stg2, stg3, stg1, S);
+        sm.step_f16(t + 3, stg3, stg0, stg2, S);
+      }
     } else {
-      sm.step(t + 0, stg0, stg4, S);
-      sm.step(t + 1, stg1, stg0, S);
-      sm.step(t + 2, stg2, stg1, S);
-      sm.step(t + 3, stg3, stg2, S);
-      sm.step(t + 4, stg4, stg3, S);
+      for (int t = 0; t < sm.ntiles; t += NSTAGE) {
+        if constexpr (NSTAGE == 4) {
+          sm.template step<F16>(t + 0, stg0, stg3, S);
+          sm.template step<F16>(t + 1, stg1, stg0, S);
+          sm.template step<F16>(t + 2, stg2, stg1, S);
+          sm.template step<F16>(t + 3, stg3, stg2, S);
+        } else {
+          sm.template step<F16>(t + 0, stg0, stg4, S);
+          sm.template step<F16>(t + 1, stg1, stg0, S);
+          sm.template step<F16>(t + 2, stg2, stg1, S);
+          sm.template step<F16>(t + 3, stg3, stg2, S);
+          sm.template step<F16>(t + 4, stg4, stg3, S);
+        }
+      }
     }
-  }
-
-  if (PASS_B) {
-    if (MODE == kModeFull && a.colsum && sm.ntiles > 0) {
+    if (is_full<MODE>() && a.colsum && sm.ntiles > 0) {
       lds_barrier();
       sm.flush_colsum(sm.ntiles - 1);
     }
+  };
+
+  if constexpr (MODE == kModeFull) {
+    run(BoolTag<true>{});
+    // A V element beyond the fp16 range (|v| > 65504) makes this split's P.V
+    // non-finite: flag the split for the exact pass.
+    bool bad = false;
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) bad |= !__builtin_isfinite(S.y[rt][dt][i]);
+    bad = __syncthreads_or(bad);
+    if (threadIdx.x == 0) a.redo[(size_t)u * a.S + s] = bad ? 1 : 0;
+    if (bad) return;
+  } else {
+    run(BoolTag<false>{});
+  }
+
+  if (PASS_B) {
     float* yp = a.ypart + ((size_t)u * a.S + s) * a.mp * D;
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt)
@@ -679,6 +903,7 @@ hipError_t launch_stream_t(const Plan& p, const AttnPass& a, hipStream_t s) {
   k.pmax = a.pmax; k.psum = a.psum; k.lse_log2 = a.lse_log2;
   k.ypart = a.ypart; k.colsum = a.colsum; k.prefix = a.prefix;
   k.fixed = a.fixed; k.npart = a.npart; k.mpart = a.mpart; k.lse_bias = a.lse_bias;
+  k.redo = a.redo;
   k.kpos = a.kpos; k.src_rows = a.src_rows;
   k.gather_k = a.gather_k ? 1 : 0; k.gather_v = a.gather_v ? 1 : 0;
   k.kcopy = (u16*)a.kcopy;
@@ -714,7 +939,13 @@ hipError_t launch_stream_w(const Plan& p, const AttnPass& a, hipStream_t s) {
 template <int D>
 hipError_t launch_stream_d(const Plan& p, const AttnPass& a, int mode, hipStream_t s) {
   if (mode == kModeLse) return launch_stream_w<D, kModeLse>(p, a, s);
-  if (mode == kModeFull) return launch_stream_w<D, kModeFull>(p, a, s);
+  if (mode == kModeFull) {
+    // fp16 pass, then the exact pass on the splits it flagged
+    if (!a.redo) return hipErrorInvalidValue;
+    hipError_t e = launch_stream_w<D, kModeFull>(p, a, s);
+    if (e != hipSuccess) return e;
+    return launch_stream_w<D, kModeFullExact>(p, a, s);
+  }
   return launch_stream_w<D, kModeRetained>(p, a, s);
 }
 

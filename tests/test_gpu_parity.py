@@ -151,3 +151,25 @@ def test_deterministic_bitwise():
     b = run_gpu(cfg, q, K, V)
     for k in ("idx", "k_out", "v_out", "stats", "lse", "y", "pooled"):
         assert np.array_equal(a[k], b[k]), k
+
+
+@pytest.mark.parametrize("label,scale", [("v-beyond-fp16", 2.0 ** 17), ("v-small", 2.0 ** -10)],
+                         ids=["v-beyond-fp16", "v-small"])
+def test_value_range(label, scale):
+    # values beyond the fp16 range in a few rows (first split, interior and a
+    # window row) must still match, as must a cache whose values are all small
+    cfg = W.config(2, layers=1, kv_heads=2, n=4096, budget=384)
+    q, K, V = _batch(cfg)
+    v = W.decode(V, cfg.dtype)
+    if scale > 1:
+        v[:, [5, 700, cfg.n - 3]] *= scale
+    else:
+        v *= scale
+    V = W.f32_to_bf16_bits(v.astype(np.float32))
+    print("case", label, flush=True)
+    gpu = run_gpu(cfg, q, K, V)
+    rep = []
+    for u in range(cfg.units):
+        check_unit(cfg, q, K, V, gpu, u, report=rep)
+    for r in rep:
+        print(r, flush=True)
