@@ -64,6 +64,7 @@ struct StreamK {
 };
 
 constexpr int kTileElems = 4096;   // elements of one tensor per tile
+constexpr int kRetMaxSlots = 4096;  // retained pass: key slots per block (the plan's split bound)
 constexpr int kTileBytes = kTileElems * 2;
 
 // s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
@@ -160,23 +161,20 @@ __device__ __forceinline__ int swz(int r, int ch) {
 // Direct-to-LDS loads of one tensor tile; each wave issues its share, one
 // 16-byte chunk per lane and 1 KB of LDS per wave instruction.
 //
-// A whole tile (the common case) is one buffer load per instruction against a
-// buffer resource based at the block's first key: a per-lane 32-bit offset
-// that is the same for every tile (row and swizzled chunk inside the tile)
-// plus a scalar tile offset, so the loop spends no vector instructions or
-// 64-bit address registers on it.  The resource's byte range ends at key_end,
-// so nothing past the block's keys can be read.
+// A whole tile (the common case) is addressed as the block's first key plus
+// a per-lane 32-bit offset that is the same for every tile (row and swizzled
+// chunk inside the tile) plus a uniform tile offset.  (The global form of the
+// LDS-destination load is used: the compiler tracks which LDS array it
+// writes, so reads of the other ring stages need not wait for it.)
 template <int D, int WAVES, bool VT>
 struct TileLoads {
   using G = Geo<D>;
   static constexpr int PER = G::INSTR / WAVES;
-  __amdgpu_buffer_rsrc_t res;
+  const char* base;
   uint32_t off[PER];
 
-  __device__ __forceinline__ void init(const u16* base, int key0, int key_end, int wave, int lane) {
-    const int nbytes = (key_end > key0 ? key_end - key0 : 0) * D * 2;
-    res = __builtin_amdgcn_make_buffer_rsrc((void*)(base + (size_t)key0 * D), (short)0, nbytes,
-                                            0x00020000);
+  __device__ __forceinline__ void init(const u16* b, int key0, int wave, int lane) {
+    base = reinterpret_cast<const char*>(b + (size_t)key0 * D);
 #pragma unroll
     for (int it = 0; it < PER; ++it) {
       const int r = (wave * PER + it) * G::RPI + lane / G::CPR;
@@ -187,10 +185,11 @@ struct TileLoads {
 
   // whole tile starting `tkey` keys after the block's first key
   __device__ __forceinline__ void whole(int tkey, char* lds_tile, int wave) const {
+    const char* tb = base + (size_t)tkey * D * 2;
 #pragma unroll
     for (int it = 0; it < PER; ++it)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(res, (lds_void*)(lds_tile + (wave * PER + it) * 1024),
-                                               16, (int)off[it], tkey * D * 2, 0, 0);
+      __builtin_amdgcn_global_load_lds(tb + off[it], (lds_void*)(lds_tile + (wave * PER + it) * 1024),
+                                       16, 0, 0);
   }
 };
 
@@ -266,12 +265,16 @@ struct Stream {
   int u, key0, key_end, ntiles, win0, lane, wave, l16, g;
   bool all_rows;             // m == mp: no padding rows to mask
   float (*colpart)[WAVES][TK];
-  uint4* xg;                 // retained pass: [2][NT][2][64] fragment exchange
+  uint4* xg;                 // retained pass: [NT][2][64] fragment exchange
   const uint8_t* fixs;       // retained pass: fixed flags of this split (LDS)
   // Row tile (16 rows) held as row tile rt of this wave: tiles w and NT-1-w,
   // which pairs a short and a long row of the Gram matrix's lower triangle.
   __device__ __forceinline__ int rtile(int rt) const { return rt == 0 ? wave : NT - 1 - wave; }
   const int32_t* posl;       // gathered rows: source row of each slot of this split (LDS)
+  // retained pass: first fragment of this wave's row tile rt in an exchange
+  // buffer (a non-negative uniform value the compiler treats as opaque, so the
+  // store addresses stay plain offsets into the exchange array)
+  int xrow[2];
 
   TileLoads<D, WAVES, false> kld;
   TileLoads<D, WAVES, true> vld;
@@ -347,13 +350,16 @@ struct Stream {
   }
 
   // Gram contribution of 32 keys (16-key tiles 2kp, 2kp+1): this wave's
-  // X_G fragments (hi/lo) go to LDS, then every wave forms the lower-triangle
-  // blocks N[I][J], J <= I, of its two row tiles I (NT+1 blocks per wave, the
-  // same count for every wave).  X_G is P with fixed slots zeroed.
+  // X_G fragments (hi/lo) go to LDS, then every wave forms the blocks N[I][J]
+  // of its two row tiles I (the lower triangle, J <= I, is written out).  X_G
+  // is P with fixed slots zeroed.
   __device__ __forceinline__ void gram_step(int t, int kp, const float (&pv)[NKT][2][4],
                                             State<D, MODE, NT>& S) {
-    const int buf = (t * (NKT / 2) + kp) & 1;
-    uint4* xb = xg + buf * NT * 2 * 64;
+    // One exchange buffer: the step barrier between tiles, and this barrier
+    // between the key pairs of one tile (64-key tiles), separate every wave's
+    // reads of it from the next writes.
+    if (kp > 0) lds_barrier();
+    uint4* xb = xg;
     const int tl = t * TK;   // key offset of this tile inside the split
     bf16x8 fh[2], fl[2];
 #pragma unroll
@@ -367,25 +373,28 @@ struct Stream {
           x8[4 * h + i] = fixs[kl] ? 0.f : pv[2 * kp + h][rt][i];
         }
       split8(x8, fh[rt], fl[rt]);
-      xb[(rtile(rt) * 2 + 0) * 64 + lane] = __builtin_bit_cast(uint4, fh[rt]);
-      xb[(rtile(rt) * 2 + 1) * 64 + lane] = __builtin_bit_cast(uint4, fl[rt]);
+      xb[xrow[rt] + lane] = __builtin_bit_cast(uint4, fh[rt]);
+      xb[xrow[rt] + 64 + lane] = __builtin_bit_cast(uint4, fl[rt]);
     }
     lds_barrier();
-    const int I0 = rtile(0), I1 = rtile(1);   // I0 <= I1
+    // All column blocks of both row tiles, straight-line: one batch of
+    // fragment reads and one wait (the blocks above the diagonal are computed
+    // and not written out; the MFMA pipe has room for them, and a branch per
+    // block would expose an LDS round trip each).
+    uint4 bh[NT], bl[NT];
 #pragma unroll
     for (int bt = 0; bt < NT; ++bt) {
-      if (bt > I1) break;   // wave-uniform
-      const bf16x8 bh = __builtin_bit_cast(bf16x8, xb[(bt * 2 + 0) * 64 + lane]);
-      const bf16x8 bl = __builtin_bit_cast(bf16x8, xb[(bt * 2 + 1) * 64 + lane]);
-      if (bt <= I0) {
-        S.n[0][bt] = mfma_bf16(fh[0], bh, S.n[0][bt]);
-        S.n[0][bt] = mfma_bf16(fh[0], bl, S.n[0][bt]);
-        S.n[0][bt] = mfma_bf16(fl[0], bh, S.n[0][bt]);
-      }
-      S.n[1][bt] = mfma_bf16(fh[1], bh, S.n[1][bt]);
-      S.n[1][bt] = mfma_bf16(fh[1], bl, S.n[1][bt]);
-      S.n[1][bt] = mfma_bf16(fl[1], bh, S.n[1][bt]);
+      bh[bt] = xb[(bt * 2 + 0) * 64 + lane];
+      bl[bt] = xb[(bt * 2 + 1) * 64 + lane];
     }
+#pragma unroll
+    for (int bt = 0; bt < NT; ++bt)
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt) {
+        S.n[rt][bt] = mfma_bf16(fh[rt], as_bf16x8(bh[bt]), S.n[rt][bt]);
+        S.n[rt][bt] = mfma_bf16(fh[rt], as_bf16x8(bl[bt]), S.n[rt][bt]);
+        S.n[rt][bt] = mfma_bf16(fl[rt], as_bf16x8(bh[bt]), S.n[rt][bt]);
+      }
   }
 
   // Full-cache pass B with fp16 P.V: tile t is computed while this thread's
@@ -395,12 +404,14 @@ struct Stream {
   __device__ __forceinline__ void step_f16(int t, char* cur, char* nxt, char* refill,
                                            State<D, MODE, NT>& S) {
     static_assert(NSTAGE == 4, "four-stage ring");
-    if (t >= ntiles) return;
-    if (t + 2 < ntiles) wait_vmcnt<LOADS>();   // tile t+2 may stay in flight
-    else wait_vmcnt<0>();
+    // Every step issues one tile (past the end, the last tile again, into the
+    // stage freed last step), so exactly the loads of tile t+2 may still be in
+    // flight here: the wait is the same constant in every step, which keeps
+    // the compiler's count of outstanding LDS loads exact.
+    wait_vmcnt<LOADS>();
     lds_barrier();
     if (a.colsum && t > 0) flush_colsum(t - 1);
-    issue(t + 3, refill);
+    issue(min(t + 3, ntiles - 1), refill);
     if (t + 1 < ntiles) v_to_f16(nxt + kTileBytes);
     // keep the scheduler from hoisting the tile's loads above the conversion
     // (register pressure)
@@ -571,7 +582,7 @@ struct Stream {
       for (int i = 0; i < 4; ++i) cs[kt * 4 + i] = pv[0][kt][i] + pv[1][kt][i];
     int v;
     const float c = row_reduce_scatter<NKT * 4>(cs, l16, &v);
-    colpart[t & 1][wave][(v >> 2) * 16 + 4 * g + (v & 3)] = c;
+    if (NKT * 4 == 16 || (l16 & 1) == 0) colpart[t & 1][wave][(v >> 2) * 16 + 4 * g + (v & 3)] = c;
   }
 
   // The tile's work after the logits.  INTERIOR skips every mask.
@@ -697,8 +708,8 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : is_full<MODE>() ? 2 : 
   // ring depth: pass A 5 x 8 KB (four blocks per CU at 4 waves per SIMD);
   // pass B 4 x 16 KB (one stage holds the tile whose V is being converted);
   // retained pass 5 x 16 KB (one block per CU, so its ring is deeper)
-  constexpr int NSTAGE = is_full<MODE>() ? 4 : 5;
-  static_assert(NSTAGE == 4 || NSTAGE == 5, "ring depths with an unrolled loop below");
+  constexpr int NSTAGE = MODE == kModeFull ? 4 : MODE == kModeFullExact ? 3 : 5;
+  static_assert(NSTAGE >= 3 && NSTAGE <= 5, "ring depths with an unrolled loop below");
   constexpr int STAGE_BYTES = kTileBytes * (PASS_B ? 2 : 1);
   __shared__ __attribute__((aligned(16))) char stg0[STAGE_BYTES];
   __shared__ __attribute__((aligned(16))) char stg1[STAGE_BYTES];
@@ -706,7 +717,13 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : is_full<MODE>() ? 2 : 
   __shared__ __attribute__((aligned(16))) char stg3[NSTAGE > 3 ? STAGE_BYTES : 16];
   __shared__ __attribute__((aligned(16))) char stg4[NSTAGE > 4 ? STAGE_BYTES : 16];
   __shared__ float colpart[2][WAVES][TK];
-  extern __shared__ __attribute__((aligned(16))) uint4 dyn[];   // retained passes only
+  // retained pass only: X_G fragment exchange [NT][2][64], fixed flags and
+  // source rows of the split's slots (static arrays, so the compiler can tell
+  // them apart from the ring stages the tile loads are filling)
+  constexpr bool RET = MODE == kModeRetained;
+  __shared__ __attribute__((aligned(16))) uint4 xgs[RET ? NT * 2 * 64 : 1];
+  __shared__ uint8_t fixl[RET ? kRetMaxSlots : 1];
+  __shared__ int32_t posl[RET ? kRetMaxSlots : 1];
 
   if (MODE == kModeFullExact && !a.redo[(size_t)blockIdx.y * a.S + blockIdx.x]) return;
   Stream<D, WAVES, MODE, NSTAGE> sm{a};
@@ -725,37 +742,37 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : is_full<MODE>() ? 2 : 
   sm.all_rows = a.m == a.mp;
   sm.init_offsets();
   // (the gathered retained pass does not use these)
-  sm.kld.init(sm.kbase, sm.key0, sm.key_end, sm.wave, sm.lane);
-  if (PASS_B) sm.vld.init(sm.vbase, sm.key0, sm.key_end, sm.wave, sm.lane);
+  sm.kld.init(sm.kbase, sm.key0, sm.wave, sm.lane);
+  if (PASS_B) sm.vld.init(sm.vbase, sm.key0, sm.wave, sm.lane);
   sm.colpart = colpart;
-  sm.xg = dyn;
-  sm.fixs = reinterpret_cast<const uint8_t*>(dyn + 2 * NT * 2 * 64);
+  sm.xg = xgs;
+#pragma unroll
+  for (int rt = 0; rt < 2; ++rt) {
+    int x = sm.rtile(rt) * 2 * 64;
+    asm("" : "+s"(x));
+    sm.xrow[rt] = x;
+  }
+  sm.fixs = fixl;
+  sm.posl = posl;
   const int u = sm.u, wave = sm.wave, l16 = sm.l16, g = sm.g;
-  // dynamic LDS: [retained pass B: fragment exchange, fixed flags] [positions]
-  const int nsl = sm.ntiles * TK;
-  const size_t pos_off = MODE == kModeRetained
-                             ? (size_t)2 * NT * 2 * 64 * sizeof(uint4) + (((size_t)nsl + 15) & ~(size_t)15)
-                             : 0;
-  sm.posl = reinterpret_cast<const int32_t*>(reinterpret_cast<char*>(dyn) + pos_off);
+  const int nsl = sm.ntiles * TK;   // <= kRetMaxSlots in the retained pass (host check)
 
-  if (MODE == kModeRetained) {
+  if (RET) {
     // fixed flags of this split's slots (padded with "fixed" past the end)
-    uint8_t* fl = reinterpret_cast<uint8_t*>(dyn + 2 * NT * 2 * 64);
     for (int i = threadIdx.x; i < nsl; i += WAVES * 64) {
       const int key = sm.key0 + i;
-      fl[i] = key < sm.key_end ? a.fixed[(size_t)u * a.nk + key] : 1;
+      fixl[i] = key < sm.key_end ? a.fixed[(size_t)u * a.nk + key] : 1;
+    }
+    if (a.gather_k || a.gather_v) {
+      // source row of each slot, clamped into the source tensor
+      for (int i = threadIdx.x; i < nsl; i += WAVES * 64) {
+        const int key = min(sm.key0 + i, sm.key_end - 1);
+        const int64_t r = a.kpos[(size_t)u * a.nk + key];
+        posl[i] = (int32_t)(r < 0 ? 0 : r >= a.src_rows ? a.src_rows - 1 : r);
+      }
     }
   }
-  if (a.gather_k || a.gather_v) {
-    // source row of each slot, clamped into the source tensor
-    int32_t* pl = reinterpret_cast<int32_t*>(reinterpret_cast<char*>(dyn) + pos_off);
-    for (int i = threadIdx.x; i < nsl; i += WAVES * 64) {
-      const int key = min(sm.key0 + i, sm.key_end - 1);
-      const int64_t r = a.kpos[(size_t)u * a.nk + key];
-      pl[i] = (int32_t)(r < 0 ? 0 : r >= a.src_rows ? a.src_rows - 1 : r);
-    }
-  }
-  if (MODE == kModeRetained || a.gather_k || a.gather_v) __syncthreads();
+  if (RET) __syncthreads();
 
   State<D, MODE, NT> S;
 #pragma unroll
@@ -780,26 +797,44 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : is_full<MODE>() ? 2 : 
 
   auto run = [&](auto f16) {
     constexpr bool F16 = decltype(f16)::value;
-    sm.issue(0, stg0);
-    sm.issue(1, stg1);
-    sm.issue(2, stg2);
-    if constexpr (NSTAGE == 5) sm.issue(3, stg3);
     if constexpr (F16) {
-      // tile 0 converted before the loop (published by step 0's barrier)
-      if (sm.ntiles > 2) wait_vmcnt<2 * decltype(sm)::LOADS>();
-      else if (sm.ntiles > 1) wait_vmcnt<decltype(sm)::LOADS>();
-      else wait_vmcnt<0>();
-      lds_barrier();
-      if (sm.ntiles > 0) sm.v_to_f16(stg0 + kTileBytes);
-      for (int t = 0; t < sm.ntiles; t += 4) {
+      // tiles 0..2 (clamped to the last tile) in flight; tile 0 converted
+      // before the loop (published by step 0's barrier)
+      const int last = sm.ntiles - 1;
+      if (last >= 0) {
+        sm.issue(0, stg0);
+        sm.issue(min(1, last), stg1);
+        sm.issue(min(2, last), stg2);
+        wait_vmcnt<2 * decltype(sm)::LOADS>();
+        lds_barrier();
+        sm.v_to_f16(stg0 + kTileBytes);
+      }
+      // whole groups of four steps as straight-line code (every step names
+      // its stages at compile time), then the remaining zero to three steps
+      int t = 0;
+      for (; t + 4 <= sm.ntiles; t += 4) {
         sm.step_f16(t + 0, stg0, stg1, stg3, S);
         sm.step_f16(t + 1, stg1, stg2, stg0, S);
         sm.step_f16(t + 2, stg2, stg3, stg1, S);
         sm.step_f16(t + 3, stg3, stg0, stg2, S);
       }
+      if (t < sm.ntiles) sm.step_f16(t, stg0, stg1, stg3, S);
+      if (t + 1 < sm.ntiles) sm.step_f16(t + 1, stg1, stg2, stg0, S);
+      if (t + 2 < sm.ntiles) sm.step_f16(t + 2, stg2, stg3, stg1, S);
+      // the clamped loads past the end must land before the block's LDS is
+      // released
+      wait_vmcnt<0>();
     } else {
+      sm.issue(0, stg0);
+      sm.issue(1, stg1);
+      if constexpr (NSTAGE >= 4) sm.issue(2, stg2);
+      if constexpr (NSTAGE == 5) sm.issue(3, stg3);
       for (int t = 0; t < sm.ntiles; t += NSTAGE) {
-        if constexpr (NSTAGE == 4) {
+        if constexpr (NSTAGE == 3) {
+          sm.template step<F16>(t + 0, stg0, stg2, S);
+          sm.template step<F16>(t + 1, stg1, stg0, S);
+          sm.template step<F16>(t + 2, stg2, stg1, S);
+        } else if constexpr (NSTAGE == 4) {
           sm.template step<F16>(t + 0, stg0, stg3, S);
           sm.template step<F16>(t + 1, stg1, stg0, S);
           sm.template step<F16>(t + 2, stg2, stg1, S);
@@ -908,17 +943,13 @@ hipError_t launch_stream_t(const Plan& p, const AttnPass& a, hipStream_t s) {
   k.gather_k = a.gather_k ? 1 : 0; k.gather_v = a.gather_v ? 1 : 0;
   k.kcopy = (u16*)a.kcopy;
   if ((k.gather_k || k.gather_v) && (!a.kpos || a.src_rows < 1)) return hipErrorInvalidValue;
-  const int tk = kTileElems / D;
-  const size_t slots = (size_t)((a.chunk + tk - 1) / tk) * tk;
-  size_t dyn = 0;
-  if (MODE == kModeRetained) dyn = (size_t)2 * (2 * WAVES) * 2 * 64 * sizeof(uint4) + ((slots + 15) & ~(size_t)15);
-  if (k.gather_k || k.gather_v) dyn += slots * sizeof(int32_t);
-  if (dyn) {
-    hipError_t e = hipFuncSetAttribute((const void*)stream_kernel<D, WAVES, MODE>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
-    if (e != hipSuccess) return e;
+  if (MODE == kModeRetained) {
+    const int tk = kTileElems / D;
+    if ((size_t)((a.chunk + tk - 1) / tk) * tk > (size_t)kRetMaxSlots) return hipErrorInvalidValue;
+  } else if (k.gather_k || k.gather_v) {
+    return hipErrorInvalidValue;   // only the retained pass reads rows through positions
   }
-  hipLaunchKernelGGL((stream_kernel<D, WAVES, MODE>), dim3(a.S, p.U), dim3(WAVES * 64), dyn, s, k);
+  hipLaunchKernelGGL((stream_kernel<D, WAVES, MODE>), dim3(a.S, p.U), dim3(WAVES * 64), 0, s, k);
   return hipGetLastError();
 }
 
