@@ -265,7 +265,8 @@ struct Stream {
   int u, key0, key_end, ntiles, win0, lane, wave, l16, g;
   bool all_rows;             // m == mp: no padding rows to mask
   float (*colpart)[WAVES][TK];
-  uint4* xg;                 // retained pass: [NT][2][64] fragment exchange
+  uint4* xg;                 // retained pass: fragment exchange of row tiles 0..NT/2-1 [NT/2][2][64]
+  uint4* xg2;                // and of row tiles NT-1..NT/2 (row tile NT-1-j at j)
   const uint8_t* fixs;       // retained pass: fixed flags of this split (LDS)
   // Row tile (16 rows) held as row tile rt of this wave: tiles w and NT-1-w,
   // which pairs a short and a long row of the Gram matrix's lower triangle.
@@ -373,8 +374,11 @@ struct Stream {
           x8[4 * h + i] = fixs[kl] ? 0.f : pv[2 * kp + h][rt][i];
         }
       split8(x8, fh[rt], fl[rt]);
-      xb[xrow[rt] + lane] = __builtin_bit_cast(uint4, fh[rt]);
-      xb[xrow[rt] + 64 + lane] = __builtin_bit_cast(uint4, fl[rt]);
+      // row tile rtile(rt) lives in half rt of the exchange: rtile(0) = wave
+      // in the first half, rtile(1) = NT-1-wave in the second
+      uint4* xh = rt == 0 ? xg : xg2;
+      xh[xrow[rt] + lane] = __builtin_bit_cast(uint4, fh[rt]);
+      xh[xrow[rt] + 64 + lane] = __builtin_bit_cast(uint4, fl[rt]);
     }
     lds_barrier();
     // All column blocks of both row tiles, straight-line: one batch of
@@ -384,8 +388,10 @@ struct Stream {
     uint4 bh[NT], bl[NT];
 #pragma unroll
     for (int bt = 0; bt < NT; ++bt) {
-      bh[bt] = xb[(bt * 2 + 0) * 64 + lane];
-      bl[bt] = xb[(bt * 2 + 1) * 64 + lane];
+      const uint4* xh = bt < NT / 2 ? xg : xg2;
+      const int b2 = bt < NT / 2 ? bt : NT - 1 - bt;
+      bh[bt] = xh[(b2 * 2 + 0) * 64 + lane];
+      bl[bt] = xh[(b2 * 2 + 1) * 64 + lane];
     }
 #pragma unroll
     for (int bt = 0; bt < NT; ++bt)
@@ -435,7 +441,11 @@ struct Stream {
     lds_barrier();
     if (is_full<MODE>() && a.colsum && t > 0) flush_colsum(t - 1);
     if (MODE == kModeRetained && a.kcopy) copy_k(t, cur);
-    issue(t + NSTAGE - 1, refill);
+    // The retained pass refills at the end of the step: its Gram exchange
+    // has one LDS access that the compiler makes wait for every tile load in
+    // flight, and a load issued at the start of the same step would still be
+    // in flight there.
+    if (MODE != kModeRetained) issue(t + NSTAGE - 1, refill);
 
     const int tile0 = key0 + t * TK;
     // An interior tile has every key valid and outside the window, and the
@@ -447,8 +457,18 @@ struct Stream {
     } else {
       f32x4 st[NKT][2];
       logits(cur, S, st);
-      if (interior) body<true>(t, tile0, cur, st, S);
-      else body<false>(t, tile0, cur, st, S);
+      float pv[NKT][2][4];
+      if (interior) body<true>(t, tile0, cur, st, pv, S);
+      else body<false>(t, tile0, cur, st, pv, S);
+      // once, after the branch: the exchange stores of a Gram step in both
+      // branches would be merged into one store that has lost the record of
+      // which LDS array it writes, and that store would wait for every tile
+      // load in flight
+      if constexpr (MODE == kModeRetained) {
+#pragma unroll
+        for (int kp = 0; kp < NKT / 2; ++kp) gram_step(t, kp, pv, S);
+        issue(t + NSTAGE - 1, refill);
+      }
     }
   }
 
@@ -588,7 +608,7 @@ struct Stream {
   // The tile's work after the logits.  INTERIOR skips every mask.
   template <bool INTERIOR>
   __device__ __forceinline__ void body(int t, int tile0, const char* cur, const f32x4 (&st)[NKT][2],
-                                       State<D, MODE, NT>& S) {
+                                       float (&pv)[NKT][2][4], State<D, MODE, NT>& S) {
     bool ok[NKT][2][4];
 #pragma unroll
     for (int kt = 0; kt < NKT; ++kt)
@@ -647,7 +667,6 @@ struct Stream {
       return;
     }
 
-    float pv[NKT][2][4];
 #pragma unroll
     for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
@@ -694,7 +713,6 @@ struct Stream {
           S.y[rt][dt] = mfma_bf16(ahi[rt], b[dt], S.y[rt][dt]);
           if (SPLIT) S.y[rt][dt] = mfma_bf16(alo[rt], b[dt], S.y[rt][dt]);
         }
-      if (MODE == kModeRetained) gram_step(t, kp, pv, S);
     }
   }
 };
@@ -721,7 +739,8 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : is_full<MODE>() ? 2 : 
   // source rows of the split's slots (static arrays, so the compiler can tell
   // them apart from the ring stages the tile loads are filling)
   constexpr bool RET = MODE == kModeRetained;
-  __shared__ __attribute__((aligned(16))) uint4 xgs[RET ? NT * 2 * 64 : 1];
+  __shared__ __attribute__((aligned(16))) uint4 xgs[RET ? NT / 2 * 2 * 64 : 1];
+  __shared__ __attribute__((aligned(16))) uint4 xgs2[RET ? NT / 2 * 2 * 64 : 1];
   __shared__ uint8_t fixl[RET ? kRetMaxSlots : 1];
   __shared__ int32_t posl[RET ? kRetMaxSlots : 1];
 
@@ -746,9 +765,10 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : is_full<MODE>() ? 2 : 
   if (PASS_B) sm.vld.init(sm.vbase, sm.key0, sm.wave, sm.lane);
   sm.colpart = colpart;
   sm.xg = xgs;
+  sm.xg2 = xgs2;
 #pragma unroll
   for (int rt = 0; rt < 2; ++rt) {
-    int x = sm.rtile(rt) * 2 * 64;
+    int x = sm.wave * 2 * 64;   // rtile(0) = wave; rtile(1) = NT-1-wave sits at index wave of xg2
     asm("" : "+s"(x));
     sm.xrow[rt] = x;
   }
