@@ -234,19 +234,26 @@ struct BoolTag {
   static constexpr bool value = B;
 };
 
+// Row tiles (16 rows) per wave: two in the full-cache passes, one in the
+// retained pass (which runs twice the waves, so that its Gram and X V0
+// accumulators fit two waves per SIMD).
+template <int MODE>
+constexpr int row_tiles() { return MODE == kModeRetained ? 1 : 2; }
+
 // Per-block state of one (unit, split) stream.
 template <int D, int MODE, int NT>
 struct State {
-  uint4 qb[2][D / 32];
-  int rowwin[2];
-  bool rowok[2];
-  float lse[2];
-  float mref[2];   // pass A: per-lane reference exponent (an integer, or -inf
-                   // before the lane's first visible key)
-  double srun[2];  // pass A: per-lane sum of 2^(t - mref) over this lane's keys
-  float msum[2];   // retained pass B: per-lane row sum of P over this lane's keys
-  f32x4 y[2][MODE != kModeLse ? D / 16 : 1];
-  f32x4 n[2][MODE == kModeRetained ? NT : 1];   // Gram rows of this wave
+  static constexpr int RT = row_tiles<MODE>();
+  uint4 qb[RT][D / 32];
+  int rowwin[RT];
+  bool rowok[RT];
+  float lse[RT];
+  float mref[RT];   // pass A: per-lane reference exponent (an integer, or -inf
+                    // before the lane's first visible key)
+  double srun[RT];  // pass A: per-lane sum of 2^(t - mref) over this lane's keys
+  float msum[RT];   // retained pass B: per-lane row sum of P over this lane's keys
+  f32x4 y[RT][MODE != kModeLse ? D / 16 : 1];
+  f32x4 n[RT][MODE == kModeRetained ? NT : 1];   // Gram rows of this wave
 };
 
 template <int D, int WAVES, int MODE, int NSTAGE>
@@ -256,7 +263,8 @@ struct Stream {
   // P as a bf16 hi+lo pair in P.V: Y and X V0 form the residual R the solve
   // works on, and plain bf16 P (2^-9 per term) moves D_after by up to ~3e-3
   static constexpr bool SPLIT = true;
-  static constexpr int TK = G::TK, NKT = G::NKT, NT = 2 * WAVES;
+  static constexpr int RT = row_tiles<MODE>();
+  static constexpr int TK = G::TK, NKT = G::NKT, NT = RT * WAVES;
   static constexpr int LOADS = (G::INSTR / WAVES) * (PASS_B ? 2 : 1);  // per thread per tile
 
   const StreamK& a;
@@ -265,17 +273,18 @@ struct Stream {
   int u, key0, key_end, ntiles, win0, lane, wave, l16, g;
   bool all_rows;             // m == mp: no padding rows to mask
   float (*colpart)[WAVES][TK];
-  uint4* xg;                 // retained pass: fragment exchange of row tiles 0..NT/2-1 [NT/2][2][64]
-  uint4* xg2;                // and of row tiles NT-1..NT/2 (row tile NT-1-j at j)
+  uint4* xg;                 // retained pass: fragment exchange [NT][2][64]
   const uint8_t* fixs;       // retained pass: fixed flags of this split (LDS)
   // Row tile (16 rows) held as row tile rt of this wave: tiles w and NT-1-w,
   // which pairs a short and a long row of the Gram matrix's lower triangle.
-  __device__ __forceinline__ int rtile(int rt) const { return rt == 0 ? wave : NT - 1 - wave; }
+  __device__ __forceinline__ int rtile(int rt) const {
+    return RT == 1 ? wave : rt == 0 ? wave : NT - 1 - wave;
+  }
   const int32_t* posl;       // gathered rows: source row of each slot of this split (LDS)
-  // retained pass: first fragment of this wave's row tile rt in an exchange
-  // buffer (a non-negative uniform value the compiler treats as opaque, so the
-  // store addresses stay plain offsets into the exchange array)
-  int xrow[2];
+  // retained pass: first fragment of this wave's row tile in the exchange
+  // (a non-negative uniform value the compiler treats as opaque, so the store
+  // addresses stay plain offsets into the exchange array)
+  int xrow;
 
   TileLoads<D, WAVES, false> kld;
   TileLoads<D, WAVES, true> vld;
@@ -352,55 +361,51 @@ struct Stream {
 
   // Gram contribution of 32 keys (16-key tiles 2kp, 2kp+1): this wave's
   // X_G fragments (hi/lo) go to LDS, then every wave forms the blocks N[I][J]
-  // of its two row tiles I (the lower triangle, J <= I, is written out).  X_G
-  // is P with fixed slots zeroed.
-  __device__ __forceinline__ void gram_step(int t, int kp, const float (&pv)[NKT][2][4],
+  // of its row tile I against all row tiles J (the lower triangle, J <= I, is
+  // written out).  X_G is P with fixed slots zeroed.
+  __device__ __forceinline__ void gram_step(int t, int kp, const float (&pv)[NKT][RT][4],
                                             State<D, MODE, NT>& S) {
+    static_assert(RT == 1, "the retained pass holds one row tile per wave");
     // One exchange buffer: the step barrier between tiles, and this barrier
     // between the key pairs of one tile (64-key tiles), separate every wave's
     // reads of it from the next writes.
     if (kp > 0) lds_barrier();
-    uint4* xb = xg;
     const int tl = t * TK;   // key offset of this tile inside the split
-    bf16x8 fh[2], fl[2];
-#pragma unroll
-    for (int rt = 0; rt < 2; ++rt) {
+    bf16x8 fh, fl;
+    {
       float x8[8];
 #pragma unroll
       for (int h = 0; h < 2; ++h)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int kl = tl + (2 * kp + h) * 16 + 4 * g + i;   // slot offset in the split
-          x8[4 * h + i] = fixs[kl] ? 0.f : pv[2 * kp + h][rt][i];
+          x8[4 * h + i] = fixs[kl] ? 0.f : pv[2 * kp + h][0][i];
         }
-      split8(x8, fh[rt], fl[rt]);
-      // row tile rtile(rt) lives in half rt of the exchange: rtile(0) = wave
-      // in the first half, rtile(1) = NT-1-wave in the second
-      uint4* xh = rt == 0 ? xg : xg2;
-      xh[xrow[rt] + lane] = __builtin_bit_cast(uint4, fh[rt]);
-      xh[xrow[rt] + 64 + lane] = __builtin_bit_cast(uint4, fl[rt]);
+      split8(x8, fh, fl);
+      xg[xrow + lane] = __builtin_bit_cast(uint4, fh);
+      xg[xrow + 64 + lane] = __builtin_bit_cast(uint4, fl);
     }
     lds_barrier();
-    // All column blocks of both row tiles, straight-line: one batch of
-    // fragment reads and one wait (the blocks above the diagonal are computed
-    // and not written out; the MFMA pipe has room for them, and a branch per
-    // block would expose an LDS round trip each).
-    uint4 bh[NT], bl[NT];
+    // All column blocks, straight-line, in two batches of fragment reads (the
+    // blocks above the diagonal are computed and not written out; the MFMA
+    // pipe has room for them, and a branch per block would expose an LDS
+    // round trip each).
+    constexpr int HB = NT > 4 ? NT / 2 : NT;
 #pragma unroll
-    for (int bt = 0; bt < NT; ++bt) {
-      const uint4* xh = bt < NT / 2 ? xg : xg2;
-      const int b2 = bt < NT / 2 ? bt : NT - 1 - bt;
-      bh[bt] = xh[(b2 * 2 + 0) * 64 + lane];
-      bl[bt] = xh[(b2 * 2 + 1) * 64 + lane];
-    }
+    for (int b0 = 0; b0 < NT; b0 += HB) {
+      uint4 bh[HB], bl[HB];
 #pragma unroll
-    for (int bt = 0; bt < NT; ++bt)
-#pragma unroll
-      for (int rt = 0; rt < 2; ++rt) {
-        S.n[rt][bt] = mfma_bf16(fh[rt], as_bf16x8(bh[bt]), S.n[rt][bt]);
-        S.n[rt][bt] = mfma_bf16(fh[rt], as_bf16x8(bl[bt]), S.n[rt][bt]);
-        S.n[rt][bt] = mfma_bf16(fl[rt], as_bf16x8(bh[bt]), S.n[rt][bt]);
+      for (int j = 0; j < HB; ++j) {
+        bh[j] = xg[((b0 + j) * 2 + 0) * 64 + lane];
+        bl[j] = xg[((b0 + j) * 2 + 1) * 64 + lane];
       }
+#pragma unroll
+      for (int j = 0; j < HB; ++j) {
+        S.n[0][b0 + j] = mfma_bf16(fh, as_bf16x8(bh[j]), S.n[0][b0 + j]);
+        S.n[0][b0 + j] = mfma_bf16(fh, as_bf16x8(bl[j]), S.n[0][b0 + j]);
+        S.n[0][b0 + j] = mfma_bf16(fl, as_bf16x8(bh[j]), S.n[0][b0 + j]);
+      }
+    }
   }
 
   // Full-cache pass B with fp16 P.V: tile t is computed while this thread's
@@ -455,9 +460,9 @@ struct Stream {
       if (interior) body_full<true, F16>(t, tile0, cur, S);
       else body_full<false, F16>(t, tile0, cur, S);
     } else {
-      f32x4 st[NKT][2];
+      f32x4 st[NKT][RT];
       logits(cur, S, st);
-      float pv[NKT][2][4];
+      float pv[NKT][RT][4];
       if (interior) body<true>(t, tile0, cur, st, pv, S);
       else body<false>(t, tile0, cur, st, pv, S);
       // once, after the branch: the exchange stores of a Gram step in both
@@ -475,7 +480,7 @@ struct Stream {
   // Logits of the tile in stage `cur` for this wave's two row tiles:
   // st[kt][rt] = K[16 keys of kt] . Q[16 rows of rt]^T.
   __device__ __forceinline__ void logits(const char* cur, const State<D, MODE, NT>& S,
-                                         f32x4 (&st)[NKT][2]) {
+                                         f32x4 (&st)[NKT][RT]) {
     uint4 kv[D / 32][NKT];
 #pragma unroll
     for (int ks = 0; ks < D / 32; ++ks)
@@ -483,13 +488,15 @@ struct Stream {
       for (int kt = 0; kt < NKT; ++kt)
         kv[ks][kt] = *kaddr(cur, kt, ks);
 #pragma unroll
-    for (int kt = 0; kt < NKT; ++kt) st[kt][0] = st[kt][1] = zero4();
+    for (int kt = 0; kt < NKT; ++kt)
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) st[kt][rt] = zero4();
 #pragma unroll
     for (int ks = 0; ks < D / 32; ++ks)
 #pragma unroll
       for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
-        for (int rt = 0; rt < 2; ++rt)
+        for (int rt = 0; rt < RT; ++rt)
           st[kt][rt] = mfma_bf16(as_bf16x8(kv[ks][kt]), as_bf16x8(S.qb[rt][ks]), st[kt][rt]);
   }
 
@@ -607,9 +614,9 @@ struct Stream {
 
   // The tile's work after the logits.  INTERIOR skips every mask.
   template <bool INTERIOR>
-  __device__ __forceinline__ void body(int t, int tile0, const char* cur, const f32x4 (&st)[NKT][2],
-                                       float (&pv)[NKT][2][4], State<D, MODE, NT>& S) {
-    bool ok[NKT][2][4];
+  __device__ __forceinline__ void body(int t, int tile0, const char* cur, const f32x4 (&st)[NKT][RT],
+                                       float (&pv)[NKT][RT][4], State<D, MODE, NT>& S) {
+    bool ok[NKT][RT][4];
 #pragma unroll
     for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
@@ -617,7 +624,7 @@ struct Stream {
         const int key = tile0 + kt * 16 + 4 * g + i;
         const int kw = key - win0;   // < 0 outside the window
 #pragma unroll
-        for (int rt = 0; rt < 2; ++rt)
+        for (int rt = 0; rt < RT; ++rt)
           ok[kt][rt][i] = INTERIOR || (S.rowok[rt] && key < key_end && kw <= S.rowwin[rt]);
       }
 
@@ -630,7 +637,7 @@ struct Stream {
       // the float range (2^-126 under the reference) are at least 2^-125
       // smaller than the sum and drop out.
 #pragma unroll
-      for (int rt = 0; rt < 2; ++rt) {
+      for (int rt = 0; rt < RT; ++rt) {
         const float nref = -S.mref[rt];
         float acc = 0.f;
 #pragma unroll
@@ -670,7 +677,7 @@ struct Stream {
 #pragma unroll
     for (int kt = 0; kt < NKT; ++kt)
 #pragma unroll
-      for (int rt = 0; rt < 2; ++rt)
+      for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const float e = fast_exp2(fmaf(st[kt][rt][i], a.scale_log2, -S.lse[rt]));
@@ -678,7 +685,7 @@ struct Stream {
         }
     if (MODE == kModeRetained && a.mpart) {
 #pragma unroll
-      for (int rt = 0; rt < 2; ++rt) {
+      for (int rt = 0; rt < RT; ++rt) {
         float acc = 0.f;
 #pragma unroll
         for (int kt = 0; kt < NKT; ++kt)
@@ -690,9 +697,9 @@ struct Stream {
     const char* vt = cur + kTileBytes;
 #pragma unroll
     for (int kp = 0; kp < NKT / 2; ++kp) {
-      bf16x8 ahi[2], alo[2];
+      bf16x8 ahi[RT], alo[RT];
 #pragma unroll
-      for (int rt = 0; rt < 2; ++rt) {
+      for (int rt = 0; rt < RT; ++rt) {
         float x8[8] = {pv[2 * kp][rt][0], pv[2 * kp][rt][1], pv[2 * kp][rt][2], pv[2 * kp][rt][3],
                        pv[2 * kp + 1][rt][0], pv[2 * kp + 1][rt][1], pv[2 * kp + 1][rt][2],
                        pv[2 * kp + 1][rt][3]};
@@ -709,7 +716,7 @@ struct Stream {
 #pragma unroll
       for (int dt = 0; dt < D / 16; ++dt)
 #pragma unroll
-        for (int rt = 0; rt < 2; ++rt) {
+        for (int rt = 0; rt < RT; ++rt) {
           S.y[rt][dt] = mfma_bf16(ahi[rt], b[dt], S.y[rt][dt]);
           if (SPLIT) S.y[rt][dt] = mfma_bf16(alo[rt], b[dt], S.y[rt][dt]);
         }
@@ -719,13 +726,15 @@ struct Stream {
 
 template <int D, int WAVES, int MODE>
 __global__ __launch_bounds__(WAVES * 64)
-__attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : is_full<MODE>() ? 2 : 1))) void stream_kernel(StreamK a) {
+__attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : 2))) void stream_kernel(StreamK a) {
   using G = Geo<D>;
   constexpr bool PASS_B = MODE != kModeLse;
-  constexpr int TK = G::TK, NT = 2 * WAVES;
+  constexpr int RT = row_tiles<MODE>();
+  constexpr int TK = G::TK, NT = RT * WAVES;
   // ring depth: pass A 5 x 8 KB (four blocks per CU at 4 waves per SIMD);
   // pass B 4 x 16 KB (one stage holds the tile whose V is being converted);
-  // retained pass 5 x 16 KB (one block per CU, so its ring is deeper)
+  // retained pass 5 x 16 KB (one block of twice the waves per CU, so its
+  // ring is deeper)
   constexpr int NSTAGE = MODE == kModeFull ? 4 : MODE == kModeFullExact ? 3 : 5;
   static_assert(NSTAGE >= 3 && NSTAGE <= 5, "ring depths with an unrolled loop below");
   constexpr int STAGE_BYTES = kTileBytes * (PASS_B ? 2 : 1);
@@ -739,8 +748,7 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : is_full<MODE>() ? 2 : 
   // source rows of the split's slots (static arrays, so the compiler can tell
   // them apart from the ring stages the tile loads are filling)
   constexpr bool RET = MODE == kModeRetained;
-  __shared__ __attribute__((aligned(16))) uint4 xgs[RET ? NT / 2 * 2 * 64 : 1];
-  __shared__ __attribute__((aligned(16))) uint4 xgs2[RET ? NT / 2 * 2 * 64 : 1];
+  __shared__ __attribute__((aligned(16))) uint4 xgs[RET ? NT * 2 * 64 : 1];
   __shared__ uint8_t fixl[RET ? kRetMaxSlots : 1];
   __shared__ int32_t posl[RET ? kRetMaxSlots : 1];
 
@@ -765,12 +773,10 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : is_full<MODE>() ? 2 : 
   if (PASS_B) sm.vld.init(sm.vbase, sm.key0, sm.wave, sm.lane);
   sm.colpart = colpart;
   sm.xg = xgs;
-  sm.xg2 = xgs2;
-#pragma unroll
-  for (int rt = 0; rt < 2; ++rt) {
-    int x = sm.wave * 2 * 64;   // rtile(0) = wave; rtile(1) = NT-1-wave sits at index wave of xg2
+  {
+    int x = sm.rtile(0) * 2 * 64;
     asm("" : "+s"(x));
-    sm.xrow[rt] = x;
+    sm.xrow = x;
   }
   sm.fixs = fixl;
   sm.posl = posl;
@@ -796,7 +802,7 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : is_full<MODE>() ? 2 : 
 
   State<D, MODE, NT> S;
 #pragma unroll
-  for (int rt = 0; rt < 2; ++rt) {
+  for (int rt = 0; rt < RT; ++rt) {
     const int row = sm.rtile(rt) * 16 + l16;
     S.rowok[rt] = row < a.m;
     S.rowwin[rt] = a.causal ? row % a.w : 0x3fffffff;
@@ -880,7 +886,7 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : is_full<MODE>() ? 2 : 
     // non-finite: flag the split for the exact pass.
     bool bad = false;
 #pragma unroll
-    for (int rt = 0; rt < 2; ++rt)
+    for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
       for (int dt = 0; dt < D / 16; ++dt)
 #pragma unroll
@@ -895,7 +901,7 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : is_full<MODE>() ? 2 : 
   if (PASS_B) {
     float* yp = a.ypart + ((size_t)u * a.S + s) * a.mp * D;
 #pragma unroll
-    for (int rt = 0; rt < 2; ++rt)
+    for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
       for (int dt = 0; dt < D / 16; ++dt)
 #pragma unroll
@@ -907,7 +913,7 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : is_full<MODE>() ? 2 : 
       if (a.mpart) {
         // row sums: the four lane groups of a row hold disjoint keys
 #pragma unroll
-        for (int rt = 0; rt < 2; ++rt) {
+        for (int rt = 0; rt < RT; ++rt) {
           float v = S.msum[rt];
           v += __shfl_xor(v, 16);
           v += __shfl_xor(v, 32);
@@ -917,7 +923,7 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : is_full<MODE>() ? 2 : 
       // lower blocks N[I][J] (J <= I) and their mirrors N[J][I]
       float* np = a.npart + ((size_t)u * a.S + s) * a.mp * a.mp;
 #pragma unroll
-      for (int rt = 0; rt < 2; ++rt)
+      for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
         for (int bt = 0; bt < (MODE == kModeRetained ? NT : 1); ++bt) {
           const int I = sm.rtile(rt);
@@ -934,7 +940,7 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : is_full<MODE>() ? 2 : 
     // merge the four lanes of each row: M = max ref_g, sum = sum_g s_g 2^(ref_g - M)
     // (integer exponents: exact)
 #pragma unroll
-    for (int rt = 0; rt < 2; ++rt) {
+    for (int rt = 0; rt < RT; ++rt) {
       float M = max_over_groups(S.mref[rt]);
       double part = (S.mref[rt] == -INFINITY) ? 0.0 : ldexp(S.srun[rt], (int)(S.mref[rt] - M));
       const double tot = sum_over_groups(part);
@@ -975,14 +981,16 @@ hipError_t launch_stream_t(const Plan& p, const AttnPass& a, hipStream_t s) {
 
 template <int D, int MODE>
 hipError_t launch_stream_w(const Plan& p, const AttnPass& a, hipStream_t s) {
-  switch (p.waves) {
-    case 1: return launch_stream_t<D, 1, MODE>(p, a, s);
+  // one wave per row tile in the retained pass, one per two elsewhere
+  const int waves = p.mp / (16 * row_tiles<MODE>());
+  switch (waves) {
+    case 1:
+      // (the retained pass has at least two row tiles)
+      if constexpr (MODE != kModeRetained) return launch_stream_t<D, 1, MODE>(p, a, s);
+      break;
     case 2: return launch_stream_t<D, 2, MODE>(p, a, s);
     case 4: return launch_stream_t<D, 4, MODE>(p, a, s);
-    case 8:
-      // the retained pass accumulates the Gram matrix in registers: m <= 128 only
-      if constexpr (MODE != kModeRetained) return launch_stream_t<D, 8, MODE>(p, a, s);
-      break;
+    case 8: return launch_stream_t<D, 8, MODE>(p, a, s);
   }
   return hipErrorInvalidValue;
 }
