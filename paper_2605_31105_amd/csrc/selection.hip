@@ -26,7 +26,93 @@ struct SelK {
   int64_t n;
 };
 
+// Band of candidates around a threshold, as refine_boundary below describes
+// (that is the form for keys held in registers); here each thread scans the
+// contiguous positions [j0, j1) of the pooled scores in memory.  With
+// big == false the band's positions (ascending) and take flags are in `bt`
+// and `boff` is where this thread's band entries start.
+constexpr uint32_t kBandUlps = 16;
+constexpr uint32_t kBandCap = 1024;
+
+struct BandRule {
+  uint32_t T, lo, hi, krem;   // krem: ties at T taken when the band is too big
+  bool big;
+  uint32_t boff;
+  const uint32_t* take;
+};
+
+__device__ BandRule band_rule(const float* p, uint32_t T, uint32_t k, const float* s, int j0,
+                              int j1, int P, int h, char* work, uint32_t* scan_scratch) {
+  BandRule r;
+  r.T = T;
+  r.lo = T > kBandUlps ? T - kBandUlps : 0u;
+  r.hi = T < 0x7F800000u - kBandUlps ? T + kBandUlps : 0x7F800000u;
+  uint32_t nabove = 0, nband = 0, ngt = 0, neq = 0;
+  for (int j = j0; j < j1; ++j) {
+    const uint32_t key = __float_as_uint(p[j]);
+    nabove += key > r.hi;
+    nband += key >= r.lo && key <= r.hi;
+    ngt += key > T;
+    neq += key == T;
+  }
+  uint32_t tot_above, tot_band, tot_gt, tot_eq;
+  block_exclusive_scan(nabove, scan_scratch, &tot_above);
+  r.boff = block_exclusive_scan(nband, scan_scratch, &tot_band);
+  block_exclusive_scan(ngt, scan_scratch, &tot_gt);
+  r.krem = block_exclusive_scan(neq, scan_scratch, &tot_eq);   // this thread's first tie index
+  r.krem = (k - tot_gt) > r.krem ? (k - tot_gt) - r.krem : 0u;  // ties this thread may take
+  r.big = tot_band > kBandCap;
+  double* v64 = reinterpret_cast<double*>(work);
+  int32_t* bpos = reinterpret_cast<int32_t*>(v64 + kBandCap);
+  uint32_t* btake = reinterpret_cast<uint32_t*>(bpos + kBandCap);
+  r.take = btake;
+  if (r.big) return r;
+  const uint32_t need = k - tot_above;
+  {
+    uint32_t o = r.boff;
+    for (int j = j0; j < j1; ++j) {
+      const uint32_t key = __float_as_uint(p[j]);
+      if (key >= r.lo && key <= r.hi) bpos[o++] = j;
+    }
+  }
+  __syncthreads();
+  for (uint32_t e = threadIdx.x; e < tot_band; e += blockDim.x) {
+    const int j = bpos[e];
+    const int t0 = j - h < 0 ? 0 : j - h, t1 = j + h > P - 1 ? P - 1 : j + h;
+    double acc = 0.0;
+    for (int t = t0; t <= t1; ++t) acc += (double)s[t];   // left to right
+    v64[e] = acc;
+  }
+  __syncthreads();
+  for (uint32_t e = threadIdx.x; e < tot_band; e += blockDim.x) {
+    const double v = v64[e];
+    const int j = bpos[e];
+    uint32_t rank = 0;
+    for (uint32_t f = 0; f < tot_band; ++f) {
+      const double w = v64[f];
+      rank += w > v || (w == v && bpos[f] < j);
+    }
+    btake[e] = rank < need;
+  }
+  __syncthreads();
+  return r;
+}
+
+// Whether position key is taken under rule r; `e` counts this thread's band
+// entries (or, for a big band, its ties at T) seen so far.
+__device__ __forceinline__ bool band_take(const BandRule& r, uint32_t key, uint32_t& e) {
+  if (r.big) {
+    const bool t = key > r.T || (key == r.T && e < r.krem);
+    e += key == r.T;
+    return t;
+  }
+  if (key > r.hi) return true;
+  if (key >= r.lo) return r.take[r.boff + e++] != 0;
+  return false;
+}
+
 __global__ __launch_bounds__(kSelectThreads) void select_kernel(SelK a) {
+  __shared__ __attribute__((aligned(16))) char band_work[2][kBandCap * 16];
   __shared__ uint32_t hist[2][256];
   __shared__ uint32_t sh_state[4];
   __shared__ uint32_t scan_scratch[16];
@@ -85,34 +171,25 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(SelK a) {
 
   const int per = (P + blockDim.x - 1) / blockDim.x;
   const int j0 = min(P, tid * per), j1 = min(P, j0 + per);
-  uint32_t eq0 = 0, eq1 = 0;
-  for (int j = j0; j < j1; ++j) {
-    uint32_t key = __float_as_uint(p[j]);
-    eq0 += (any0 && key == T0);
-    eq1 += (any1 && key == T1);
-  }
-  uint32_t tot;
-  uint32_t eqb0 = block_exclusive_scan(eq0, scan_scratch, &tot);
-  uint32_t eqb1 = block_exclusive_scan(eq1, scan_scratch, &tot);
+  BandRule r0 = {}, r1 = {};
+  if (any0) r0 = band_rule(p, T0, (uint32_t)a.s_sel, s, j0, j1, P, a.h, band_work[0], scan_scratch);
+  if (any1) r1 = band_rule(p, T1, (uint32_t)a.n_top, s, j0, j1, P, a.h, band_work[1], scan_scratch);
   uint32_t nsel = 0;
   {
-    uint32_t e0 = eqb0;
+    uint32_t e0 = 0;
     for (int j = j0; j < j1; ++j) {
-      uint32_t key = __float_as_uint(p[j]);
-      bool sel = any0 && (key > T0 || (key == T0 && e0 < krem[0]));
-      e0 += (any0 && key == T0);
-      nsel += sel;
+      const uint32_t key = __float_as_uint(p[j]);
+      nsel += any0 && band_take(r0, key, e0);
     }
   }
+  uint32_t tot;
   uint32_t off = block_exclusive_scan(nsel, scan_scratch, &tot);
   {
-    uint32_t e0 = eqb0, e1 = eqb1;
+    uint32_t e0 = 0, e1 = 0;
     for (int j = j0; j < j1; ++j) {
-      uint32_t key = __float_as_uint(p[j]);
-      bool sel = any0 && (key > T0 || (key == T0 && e0 < krem[0]));
-      bool top = any1 && (key > T1 || (key == T1 && e1 < krem[1]));
-      e0 += (any0 && key == T0);
-      e1 += (any1 && key == T1);
+      const uint32_t key = __float_as_uint(p[j]);
+      const bool sel = any0 && band_take(r0, key, e0);
+      const bool top = any1 && band_take(r1, key, e1);
       if (sel) {
         idx[off] = j;
         fixed[off] = (j < a.n_sink || top) ? 1 : 0;
@@ -161,6 +238,98 @@ __device__ __forceinline__ uint32_t block_sum_small(uint32_t v, uint32_t (*part)
 struct Bracket {
   uint32_t lo, hi, clo, chi;
 };
+
+// The positions taken at a threshold T, the k-th largest fp32 pooled score,
+// as a mask over the PER keys of this thread (key q <-> position j0 + q).
+//
+// The fp32 pooled sums round away differences that decide the order: two
+// overlapping windows share all but their edge terms, and when a large score
+// sits in both, their fp32 sums are equal while the edge terms differ.  So
+// the candidates whose fp32 sum lies within kBandUlps units in the last place
+// of T are ranked again by their sum recomputed in fp64 from the fp32 column
+// sums (in which the shared terms cancel exactly), then by position; the
+// keys above the band are taken, and the band fills the remaining places.
+// A band of more than kBandCap keys (scores equal over long runs) keeps the
+// fp32 order with ties to the lower position.  `work` is LDS of at least
+// kBandCap * (8 + 4 + 4) bytes.
+template <int PER>
+__device__ uint32_t refine_boundary(const uint32_t (&key)[PER], uint32_t T, uint32_t k,
+                                    const float* s, int j0, int P, int h, float* work,
+                                    uint32_t (*part)[16], uint32_t* scan_scratch, uint32_t* sh) {
+  const uint32_t lo = T > kBandUlps ? T - kBandUlps : 0u;
+  const uint32_t hi = T < 0x7F800000u - kBandUlps ? T + kBandUlps : 0x7F800000u;
+  uint32_t nabove = 0, nband = 0;
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    nabove += key[q] > hi;
+    nband += key[q] >= lo && key[q] <= hi;
+  }
+  // both counts in one scan (each total is at most PER * blockDim <= 32768)
+  uint32_t tot;
+  const uint32_t boff = block_exclusive_scan(nabove | (nband << 16), scan_scratch, &tot) >> 16;
+  const uint32_t tot_above = tot & 0xFFFFu, tot_band = tot >> 16;
+  const uint32_t need = k - tot_above;   // 1 <= need <= tot_band
+  uint32_t m = 0;
+  if (tot_band > kBandCap) {
+    // fp32 order, ties (key == T) to the lower position
+    uint32_t gt = 0, eq = 0;
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      gt += key[q] > T;
+      eq += key[q] == T;
+    }
+    uint32_t t2;
+    uint32_t e = block_exclusive_scan(gt | (eq << 16), scan_scratch, &t2) >> 16;
+    const uint32_t krem = k - (t2 & 0xFFFFu);
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      const bool take = key[q] > T || (key[q] == T && e < krem);
+      e += key[q] == T;
+      m |= (uint32_t)take << q;
+    }
+    return m;
+  }
+  double* v64 = reinterpret_cast<double*>(work);                       // [kBandCap]
+  int32_t* bpos = reinterpret_cast<int32_t*>(v64 + kBandCap);          // [kBandCap]
+  uint32_t* btake = reinterpret_cast<uint32_t*>(bpos + kBandCap);      // [kBandCap]
+  {
+    uint32_t o = boff;
+#pragma unroll
+    for (int q = 0; q < PER; ++q)
+      if (key[q] >= lo && key[q] <= hi) bpos[o++] = j0 + q;
+  }
+  __syncthreads();
+  for (uint32_t e = threadIdx.x; e < tot_band; e += blockDim.x) {
+    const int j = bpos[e];
+    const int t0 = j - h < 0 ? 0 : j - h, t1 = j + h > P - 1 ? P - 1 : j + h;
+    double acc = 0.0;
+    for (int t = t0; t <= t1; ++t) acc += (double)s[t];   // left to right
+    v64[e] = acc;
+  }
+  __syncthreads();
+  for (uint32_t e = threadIdx.x; e < tot_band; e += blockDim.x) {
+    const double v = v64[e];
+    const int j = bpos[e];
+    uint32_t rank = 0;
+    for (uint32_t f = 0; f < tot_band; ++f) {
+      const double w = v64[f];
+      rank += w > v || (w == v && bpos[f] < j);
+    }
+    btake[e] = rank < need;
+  }
+  __syncthreads();
+  {
+    uint32_t o = boff;
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      bool take = key[q] > hi;
+      if (key[q] >= lo && key[q] <= hi) take = btake[o++] != 0;
+      m |= (uint32_t)take << q;
+    }
+  }
+  __syncthreads();   // work is reused by the next call
+  return m;
+}
 
 // Same selection for prefixes of at most 32768 tokens, with each thread
 // keeping 32 consecutive pooled scores in registers.  The (c-w)-th largest
@@ -364,35 +533,9 @@ __global__ __launch_bounds__(kSmallThreads) void select_small_kernel(SelK a) {
   Bracket b1 = any0 ? Bracket{b0.lo, kmax + 1, b0.clo, 0u} : Bracket{kmin, kmax + 1, all, 0u};
   if (any1) b1 = kth(k1, b1);
   const uint32_t T0 = b0.lo, T1 = b1.lo;
-  // ties taken, lowest positions first
-  const uint32_t krem0 = k0 - b0.chi, krem1 = k1 - b1.chi;
-
-  uint32_t eq0 = 0, eq1 = 0;
-#pragma unroll
-  for (int q = 0; q < PER; ++q) {
-    eq0 += key[q] == T0;
-    eq1 += key[q] == T1;
-  }
-  if (!any0) eq0 = 0;
-  if (!any1) eq1 = 0;
+  uint32_t selm = any0 ? refine_boundary(key, T0, k0, s, j0, P, a.h, sl, part, scan_scratch, sh) : 0u;
+  uint32_t topm = any1 ? refine_boundary(key, T1, k1, s, j0, P, a.h, sl, part, scan_scratch, sh) : 0u;
   uint32_t tot;
-  const uint32_t eqb = block_exclusive_scan(eq0 | (eq1 << 16), scan_scratch, &tot);
-  const uint32_t eqb0 = eqb & 0xFFFF, eqb1 = eqb >> 16;
-  uint32_t selm = 0, topm = 0;
-  {
-    uint32_t e0 = eqb0, e1 = eqb1;
-#pragma unroll
-    for (int q = 0; q < PER; ++q) {
-      const bool sel = key[q] > T0 || (key[q] == T0 && e0 < krem0);
-      const bool top = key[q] > T1 || (key[q] == T1 && e1 < krem1);
-      e0 += key[q] == T0;
-      e1 += key[q] == T1;
-      selm |= (uint32_t)sel << q;
-      topm |= (uint32_t)top << q;
-    }
-  }
-  if (!any0) selm = 0;
-  if (!any1) topm = 0;
   uint32_t off = block_exclusive_scan(__builtin_popcount(selm), scan_scratch, &tot);
   // the selected positions in increasing order
   while (selm) {

@@ -72,6 +72,38 @@ def test_config4_full_32_layers_sampled():
     assert np.all(gpu["stats"][:, 2] < gpu["stats"][:, 1])
 
 
+def _oracle_selection(cfg, q, K, u):
+    """Retained positions and fixed flags of unit u by the oracle's selection
+    steps alone (scores, pooling, order), without the merge."""
+    qd, Kd = W.decode(q[u], cfg.dtype), W.decode(K[u], cfg.dtype)
+    Q = O.stack_queries(qd)
+    pos = O.query_positions(cfg.group, cfg.window, cfg.n)
+    A, _ = O.softmax_rows(O.window_logits(Q, Kd, pos, True))
+    p = O.pool_box(O.selection_scores(A, cfg.n - cfg.window), cfg.pool_kernel)
+    order = O.selection_order(p)
+    idx = O.retained_index(order, cfg.n, cfg.window, cfg.budget)
+    return idx, O.fixed_mask(idx, order, cfg.n, cfg.window, cfg.budget, O.Options())
+
+
+def test_config4_all_units_retained_set():
+    # every unit of the benchmark's workload: retained positions and fixed
+    # flags exactly as the oracle selects them (unit 242 holds a pooled-window
+    # near-tie 1.3e-12 apart that only the fp64 boundary ranking resolves)
+    cfg = W.config(4)
+    print("case config4 all units, selection", flush=True)
+    q, K, V = _batch(cfg)
+    gpu = run_gpu(cfg, q, K, V)
+    bad = []
+    for u in range(cfg.units):
+        idx, fixed = _oracle_selection(cfg, q, K, u)
+        if not (np.array_equal(gpu["idx"][u], idx) and
+                np.array_equal(gpu["fixed"][u].astype(bool), fixed)):
+            bad.append(u)
+        if u % 64 == 63:
+            print("units checked", u + 1, "mismatches", bad, flush=True)
+    assert not bad, "units whose retained set or fixed set differs: %s" % bad
+
+
 def test_config5_long_context_sampled():
     cfg = W.config(5)
     units = list(range(8))           # 8 of the 32 units (one layer), full length
