@@ -210,8 +210,10 @@ int grkv_compress(const void* q_obs, const void* K, const void* V, int64_t n, in
   auto pass_a = [&](const AttnPass& a) { return fast ? launch_stream(p, a, 0, s) : launch_lse_pass(p, a, s); };
   auto pass_b = [&](const AttnPass& a) { return fast ? launch_stream(p, a, 1, s) : launch_prob_pass(p, a, s); };
   GRKV_STAGE(GRKV_STAGE_FULL_LSE, pass_a(full));
-  GRKV_STAGE(GRKV_STAGE_FULL_LSE_COMBINE,
-             launch_lse_combine(p, full.pmax, full.psum, p.S1, Dd(p.lse1), F(p.lse1_log2), s));
+  // (the bf16 streaming pass B combines the split partials itself)
+  if (!fast)
+    GRKV_STAGE(GRKV_STAGE_FULL_LSE_COMBINE,
+               launch_lse_combine(p, full.pmax, full.psum, p.S1, Dd(p.lse1), F(p.lse1_log2), s));
   GRKV_STAGE(GRKV_STAGE_FULL_PROB, pass_b(full));
   // (the fast value step combines the Y partials inside its solve)
   if (!p.fast_merge)

@@ -47,6 +47,11 @@ struct StreamK {
   float* pmax;
   double* psum;
   const float* lse_log2;
+  // full-cache pass B: the log-sum-exp is combined here from pass A's split
+  // partials (pmax, psum); blocks of split 0 write it to lse_out (natural,
+  // fp64) and lse_log2_out (log2 domain, fp32) for the later kernels
+  double* lse_out;
+  float* lse_log2_out;
   float* ypart;
   float* colsum;
   int prefix;
@@ -811,7 +816,30 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : 2))) void stream_kerne
     for (int ks = 0; ks < D / 32; ++ks)
       S.qb[rt][ks] = S.rowok[rt] ? *reinterpret_cast<const uint4*>(q + ks * 32 + 8 * g)
                                  : make_uint4(0, 0, 0, 0);
-    S.lse[rt] = PASS_B ? a.lse_log2[(size_t)u * a.mp + row] - a.lse_bias : 0.f;
+    if constexpr (is_full<MODE>()) {
+      // fixed-order combine of pass A's split partials: M = max of the
+      // integer reference exponents, sum = sum_s psum_s 2^(ref_s - M) (exact
+      // powers of two), LSE (log2) = M + log2(sum)
+      float M = -INFINITY;
+      for (int sp = 0; sp < a.S; ++sp) M = fmaxf(M, a.pmax[((size_t)u * a.S + sp) * a.mp + row]);
+      double l2 = 0.0;
+      if (M != -INFINITY) {
+        double sum = 0.0;
+        for (int sp = 0; sp < a.S; ++sp) {
+          const size_t o = ((size_t)u * a.S + sp) * a.mp + row;
+          const float ms = a.pmax[o];
+          if (ms != -INFINITY) sum += a.psum[o] * exp2((double)ms - (double)M);
+        }
+        l2 = (double)M + log2(sum);
+      }
+      S.lse[rt] = (float)l2;
+      if (s == 0 && g == 0) {
+        a.lse_out[(size_t)u * a.mp + row] = M != -INFINITY ? l2 * 0.69314718055994530942 : -INFINITY;
+        a.lse_log2_out[(size_t)u * a.mp + row] = (float)l2;
+      }
+    } else {
+      S.lse[rt] = PASS_B ? a.lse_log2[(size_t)u * a.mp + row] - a.lse_bias : 0.f;
+    }
     S.msum[rt] = 0.f;
     S.mref[rt] = -INFINITY;
     S.srun[rt] = 0.0;
@@ -962,6 +990,7 @@ hipError_t launch_stream_t(const Plan& p, const AttnPass& a, hipStream_t s) {
   k.nk = a.nk; k.S = a.S; k.chunk = a.chunk;
   k.scale_log2 = (float)(1.4426950408889634 / __builtin_sqrt((double)D));
   k.pmax = a.pmax; k.psum = a.psum; k.lse_log2 = a.lse_log2;
+  k.lse_out = const_cast<double*>(a.lse); k.lse_log2_out = const_cast<float*>(a.lse_log2);
   k.ypart = a.ypart; k.colsum = a.colsum; k.prefix = a.prefix;
   k.fixed = a.fixed; k.npart = a.npart; k.mpart = a.mpart; k.lse_bias = a.lse_bias;
   k.redo = a.redo;
