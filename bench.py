@@ -11,9 +11,11 @@ lambda 1e-2, bfloat16, synthetic seeded inputs resident in HBM.
 Prints one JSON line: heads/s (value), ms per step and per layer, the
 roofline of the dominant kernel (its duration measured with HIP events around
 its launches inside the timed steps), and the float64 oracle's CPU throughput
-on a bounded sample of the same workload.
+on a bounded sample of the same workload.  Besides: the same workload as one
+call per layer (`per_layer_calls`, not `value`) and the device copy bandwidth
+(`copy_gbs`, the practical ceiling for streaming).
 
-  python bench.py [--steps K] [--warmup W] [--config 4] [--no-cpu-baseline]
+  python bench.py [--steps K] [--warmup W] [--config 4] [--no-cpu-baseline] [--no-per-layer]
 """
 from __future__ import annotations
 
@@ -40,6 +42,8 @@ def parse():
     ap.add_argument("--config", type=int, default=4)
     ap.add_argument("--budget", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-per-layer", dest="per_layer", action="store_false",
+                    help="skip the one-call-per-layer measurement")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a 1 GiB device copy (for counter calibration)")
@@ -196,6 +200,49 @@ def main():
         if t.get("source_hash") == source_hash(t.get("sources", [])):
             traffic = t.get("bytes_per_launch")
 
+    # the same workload as one call per layer (the kv_heads units of a layer
+    # per call, back to back on one stream): the pattern of a prefill that
+    # compresses each layer as it finishes
+    per_layer = None
+    if args.per_layer and cfg.layers > 1:
+        upl = cfg.kv_heads
+        calls = []
+        for l in range(cfg.layers):
+            sl = slice(l * upl, (l + 1) * upl)
+            a = (qd[sl], Kd[sl], Vd[sl])
+            calls.append((a, G.compress(*a, w, c, cfg.pool_kernel, cfg.lam)))
+        def layer_step():
+            for a, r in calls:
+                G.compress(*a, w, c, cfg.pool_kernel, cfg.lam, workspace=r.workspace, out=r)
+        for _ in range(args.warmup):
+            layer_step()
+        torch.cuda.synchronize()
+        p0, p1 = hip.event(), hip.event()
+        hip.lib.hipEventRecord(p0, ctypes.c_void_p(stream.cuda_stream))
+        for _ in range(args.steps):
+            layer_step()
+        hip.lib.hipEventRecord(p1, ctypes.c_void_p(stream.cuda_stream))
+        torch.cuda.synchronize()
+        ms_pl = hip.elapsed_ms(p0, p1) / args.steps
+        per_layer = {"units_per_call": upl, "calls_per_step": cfg.layers,
+                     "ms_per_step": ms_pl, "ms_per_layer": ms_pl / cfg.layers,
+                     "heads_per_s": U / (ms_pl / 1e3)}
+
+    # device copy bandwidth on this GPU (read + write of 1 GiB), the practical
+    # ceiling for streaming kernels
+    x = torch.empty(2 ** 28, dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    y.copy_(x)
+    torch.cuda.synchronize()
+    c0, c1 = hip.event(), hip.event()
+    hip.lib.hipEventRecord(c0, ctypes.c_void_p(stream.cuda_stream))
+    for _ in range(5):
+        y.copy_(x)
+    hip.lib.hipEventRecord(c1, ctypes.c_void_p(stream.cuda_stream))
+    torch.cuda.synchronize()
+    copy_gbs = 5 * 2 * 2 ** 30 / (hip.elapsed_ms(c0, c1) / 1e3) / 1e9
+    del x, y
+
     cpu = None
     if not args.no_cpu_baseline:
         print("bench: timing the oracle on the host", file=sys.stderr, flush=True)
@@ -221,9 +268,12 @@ def main():
                    "budget": c, "pool_kernel": cfg.pool_kernel, "lambda": cfg.lam,
                    "units": U},
         "path_hbm_frac": (U * path_bytes / (ms_step / 1e3) / 1e9) / HBM_PEAK_GBS,
+        "copy_gbs": copy_gbs,
+        "per_layer_calls": per_layer,
         "stage_ms": stage_ms,
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "frac_of_copy": achieved / copy_gbs,
                      "traffic": traffic},
         "cpu_baseline": cpu,
     }
