@@ -128,6 +128,7 @@ enum {
   GRKV_STAGE_GRAM,             /* N partials */
   GRKV_STAGE_SOLVE,            /* (Y, R, N combines,) Cholesky, Z, stats */
   GRKV_STAGE_UPDATE,           /* V* = V0 + X_G^T Z */
+  GRKV_STAGE_KEY,              /* key step (grkv_compress_kv only): CG, K* */
   GRKV_NUM_STAGES
 };
 
@@ -152,6 +153,56 @@ int grkv_compress(const void* q_obs, const void* K, const void* V, int64_t n,
                   int32_t window, int32_t budget, int32_t pool_kernel,
                   float lambda, void* stream, const grkv_problem* prob,
                   const grkv_options* opt, const grkv_outputs* out);
+
+/* Key step of GRKV (Sec. 3.3 "Key step" and "Linearized dual solution",
+ * Eq. 9-10; Algorithm 1, key step; App. D.2 and D.3), run by grkv_compress_kv
+ * after the value step with the merged values V* held fixed and the keys at K0
+ * (one alternating step, S = 1, the paper's default).  With f(K) =
+ * softmax(Q K^T / sqrt(d)) V* over the retained keys, E = Y - f(K0) and J_G the
+ * derivative of f with respect to the free keys, the free keys move to
+ *   K*_G = K0_G + unvec(J_G^T alpha),
+ *   alpha = (J_G J_G^T + lambda_k I_{md})^-1 vec(E),
+ * which minimises ||E - J_G dK||^2 + lambda_k ||dK||^2; fixed keys keep K0.
+ * The md x md system is solved matrix-free by conjugate gradients from
+ * alpha = 0.  NULL options select {lambda_k = lambda, max_iter = 64,
+ * tol = 1e-5f} (the paper uses lambda_k = lambda_v and does not state its CG
+ * settings). */
+typedef struct {
+  float lambda_k;   /* ridge coefficient of the keys, >= 0 and finite */
+  int32_t max_iter; /* conjugate-gradient iterations at most, 0 .. 4096 */
+  float tol;        /* stop once ||r|| <= tol ||E|| (recursive residual), >= 0 */
+} grkv_key_options;
+
+/* Per-unit key-step outcome in cg_info[u][2]. */
+#define GRKV_KEY_CONVERGED 1 /* the residual reached tol */
+#define GRKV_KEY_MAX_ITER 2  /* max_iter iterations ran first */
+#define GRKV_KEY_SKIPPED 3   /* the unit's value step reported a non-zero
+                                status (stats[u][3]): K* = K0 */
+#define GRKV_KEY_BREAKDOWN 4 /* a CG step found p^T A p <= 0 (possible only
+                                for lambda_k = 0); the last iterate is kept */
+
+/* grkv_compress followed by the key step.  All arguments as for
+ * grkv_compress; in addition
+ *   kopt     key-step options, or NULL for the defaults above
+ *   k_star   float [U][c][d]   merged keys K*, device memory (required);
+ *                              k_out still receives K0
+ *   cg_info  float [U][4]      {CG iterations, final ||r|| / ||E||,
+ *                              GRKV_KEY_* outcome, ||E||_F}, or NULL
+ * out->workspace_bytes must be at least grkv_workspace_bytes_kv().
+ * Errors: those of grkv_compress; GRKV_ERR_INVALID for a null k_star or bad
+ * kopt; GRKV_ERR_UNSUPPORTED unless dtype is bf16 and G*w <= 128. */
+int grkv_compress_kv(const void* q_obs, const void* K, const void* V, int64_t n,
+                     int32_t window, int32_t budget, int32_t pool_kernel,
+                     float lambda, void* stream, const grkv_problem* prob,
+                     const grkv_options* opt, const grkv_outputs* out,
+                     const grkv_key_options* kopt, float* k_star, float* cg_info);
+
+/* Workspace bytes grkv_compress_kv needs; 0 if invalid or unsupported. */
+size_t grkv_workspace_bytes_kv(const grkv_problem* prob, int64_t n,
+                               int32_t window, int32_t budget);
+
+/* The default key options for a value ridge coefficient lambda. */
+void grkv_default_key_options(grkv_key_options* kopt, float lambda);
 
 /* Workspace bytes grkv_compress needs for this shape; 0 if the shape is
  * invalid or unsupported. */

@@ -16,16 +16,19 @@ __all__ = [
     "GRKV_OK", "GRKV_ERR_INVALID", "GRKV_ERR_WORKSPACE", "GRKV_ERR_UNSUPPORTED",
     "GRKV_ERR_HIP", "GrkvError", "lib", "lib_path", "Problem", "Options", "Outputs",
     "Layout", "workspace_bytes", "workspace_layout", "compress", "Result",
-    "intermediates", "EXPORTED_SYMBOLS",
+    "intermediates", "EXPORTED_SYMBOLS", "KeyOptions", "workspace_bytes_kv", "compress_kv",
+    "KEY_CONVERGED", "KEY_MAX_ITER", "KEY_SKIPPED", "KEY_BREAKDOWN",
 ]
 
 GRKV_OK, GRKV_ERR_INVALID, GRKV_ERR_WORKSPACE, GRKV_ERR_UNSUPPORTED, GRKV_ERR_HIP = 0, -1, -2, -3, -4
 GRKV_BF16, GRKV_F32 = 0, 1
 STAGES = ("full_lse", "full_lse_combine", "full_prob", "full_y", "select", "gather",
-          "ret_lse", "ret_lse_combine", "ret_prob", "resid", "gram", "solve", "update")
+          "ret_lse", "ret_lse_combine", "ret_prob", "resid", "gram", "solve", "update", "key")
 NUM_STAGES = len(STAGES)
 EXPORTED_SYMBOLS = ("grkv_compress", "grkv_workspace_bytes", "grkv_workspace_layout",
-                    "grkv_default_options", "grkv_status_string")
+                    "grkv_default_options", "grkv_status_string", "grkv_compress_kv",
+                    "grkv_workspace_bytes_kv", "grkv_default_key_options")
+KEY_CONVERGED, KEY_MAX_ITER, KEY_SKIPPED, KEY_BREAKDOWN = 1, 2, 3, 4
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 
@@ -57,6 +60,10 @@ class Outputs(ctypes.Structure):
                 ("stage_events", ctypes.POINTER(ctypes.c_void_p))]
 
 
+class KeyOptions(ctypes.Structure):
+    _fields_ = [("lambda_k", ctypes.c_float), ("max_iter", ctypes.c_int32), ("tol", ctypes.c_float)]
+
+
 class Layout(ctypes.Structure):
     _fields_ = [(f, ctypes.c_size_t) for f in
                 ("lse", "y", "score", "pooled", "fixed", "resid", "gram", "z", "total")]
@@ -86,6 +93,17 @@ def lib() -> ctypes.CDLL:
                                             ctypes.c_int32, P(Layout)]
         L.grkv_default_options.restype = None
         L.grkv_default_options.argtypes = [P(Options)]
+        L.grkv_compress_kv.restype = ctypes.c_int
+        L.grkv_compress_kv.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                       ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                       ctypes.c_int32, ctypes.c_float, ctypes.c_void_p,
+                                       P(Problem), P(Options), P(Outputs), P(KeyOptions),
+                                       ctypes.c_void_p, ctypes.c_void_p]
+        L.grkv_workspace_bytes_kv.restype = ctypes.c_size_t
+        L.grkv_workspace_bytes_kv.argtypes = [P(Problem), ctypes.c_int64, ctypes.c_int32,
+                                              ctypes.c_int32]
+        L.grkv_default_key_options.restype = None
+        L.grkv_default_key_options.argtypes = [P(KeyOptions), ctypes.c_float]
         L.grkv_status_string.restype = ctypes.c_char_p
         L.grkv_status_string.argtypes = [ctypes.c_int]
         _LIB = L
@@ -113,6 +131,11 @@ def workspace_layout(units, group, head_dim, dtype, n, window, budget) -> Layout
     return lay
 
 
+def workspace_bytes_kv(units, group, head_dim, dtype, n, window, budget) -> int:
+    prob = Problem(units, group, head_dim, dtype)
+    return int(lib().grkv_workspace_bytes_kv(ctypes.byref(prob), n, window, budget))
+
+
 @dataclass
 class Result:
     idx: "object"        # int32 [U, c]
@@ -123,19 +146,8 @@ class Result:
     shape: tuple         # (U, G, d, dtype, n, window, budget)
 
 
-def compress(q_obs, K, V, window: int, budget: int, pool_kernel: int, lam: float, *,
-             n_sink: int = 4, beta: float = 0.10, fix_window: bool = True,
-             causal_window: bool = True, stream=None, workspace=None, out=None,
-             stage_events=None) -> Result:
-    """GRKV compression of U units on the GPU.
-
-    q_obs [U, G, w, d], K and V [U, n, d]: contiguous CUDA tensors of one dtype
-    (bfloat16 or float32).  Returns the retained indices, K0, the merged V*,
-    per-unit stats {||Y||^2, D_before, D_after, status} and the workspace.
-    ``workspace`` (uint8, >= workspace_bytes) and ``out`` (a Result whose
-    tensors are reused) avoid allocations in timed loops.  ``stage_events`` is
-    an optional ctypes array of 2 * NUM_STAGES event handles (see grkv.h).
-    """
+def _prepare(q_obs, K, V, window, budget, need_fn, n_sink, beta, fix_window, causal_window,
+             stream, workspace, out, stage_events):
     import torch
 
     if not (q_obs.is_cuda and K.is_cuda and V.is_cuda):
@@ -151,7 +163,7 @@ def compress(q_obs, K, V, window: int, budget: int, pool_kernel: int, lam: float
     n = K.shape[1]
     dt = GRKV_BF16 if K.dtype == torch.bfloat16 else GRKV_F32
     dev = K.device
-    need = workspace_bytes(U, G, d, dt, n, window, budget)
+    need = need_fn(U, G, d, dt, n, window, budget)
     if need == 0:
         # let the library report the precise error
         need = 256
@@ -173,11 +185,61 @@ def compress(q_obs, K, V, window: int, budget: int, pool_kernel: int, lam: float
     if stream is None:
         stream = torch.cuda.current_stream(dev)
     handle = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+    return out, prob, opt, outs, handle, n
+
+
+def compress(q_obs, K, V, window: int, budget: int, pool_kernel: int, lam: float, *,
+             n_sink: int = 4, beta: float = 0.10, fix_window: bool = True,
+             causal_window: bool = True, stream=None, workspace=None, out=None,
+             stage_events=None) -> Result:
+    """GRKV compression of U units on the GPU.
+
+    q_obs [U, G, w, d], K and V [U, n, d]: contiguous CUDA tensors of one dtype
+    (bfloat16 or float32).  Returns the retained indices, K0, the merged V*,
+    per-unit stats {||Y||^2, D_before, D_after, status} and the workspace.
+    ``workspace`` (uint8, >= workspace_bytes) and ``out`` (a Result whose
+    tensors are reused) avoid allocations in timed loops.  ``stage_events`` is
+    an optional ctypes array of 2 * NUM_STAGES event handles (see grkv.h).
+    """
+    out, prob, opt, outs, handle, n = _prepare(
+        q_obs, K, V, window, budget, workspace_bytes, n_sink, beta, fix_window, causal_window,
+        stream, workspace, out, stage_events)
     st = lib().grkv_compress(q_obs.data_ptr(), K.data_ptr(), V.data_ptr(), n, window, budget,
                              pool_kernel, float(lam), ctypes.c_void_p(handle),
                              ctypes.byref(prob), ctypes.byref(opt), ctypes.byref(outs))
     _check(st)
     return out
+
+
+def compress_kv(q_obs, K, V, window: int, budget: int, pool_kernel: int, lam: float, *,
+                lambda_k=None, max_iter: int = 64, tol: float = 1e-5, n_sink: int = 4,
+                beta: float = 0.10, fix_window: bool = True, causal_window: bool = True,
+                stream=None, workspace=None, out=None, k_star=None, cg_info=None,
+                stage_events=None):
+    """``compress`` followed by the key step (bfloat16 inputs, G*w <= 128).
+
+    Returns ``(result, k_star, cg_info)``: k_star float32 [U, c, d] holds the
+    merged keys K*, cg_info float32 [U, 4] holds {CG iterations, final
+    relative residual, KEY_* outcome, ||E||}.  ``lambda_k`` defaults to
+    ``lam``."""
+    import torch
+
+    out, prob, opt, outs, handle, n = _prepare(
+        q_obs, K, V, window, budget, workspace_bytes_kv, n_sink, beta, fix_window,
+        causal_window, stream, workspace, out, stage_events)
+    U, d = q_obs.shape[0], q_obs.shape[3]
+    if k_star is None:
+        k_star = torch.empty((U, budget, d), dtype=torch.float32, device=K.device)
+    if cg_info is None:
+        cg_info = torch.empty((U, 4), dtype=torch.float32, device=K.device)
+    kopt = KeyOptions(float(lam if lambda_k is None else lambda_k), int(max_iter), float(tol))
+    st = lib().grkv_compress_kv(q_obs.data_ptr(), K.data_ptr(), V.data_ptr(), n, window, budget,
+                                pool_kernel, float(lam), ctypes.c_void_p(handle),
+                                ctypes.byref(prob), ctypes.byref(opt), ctypes.byref(outs),
+                                ctypes.byref(kopt), ctypes.c_void_p(k_star.data_ptr()),
+                                ctypes.c_void_p(cg_info.data_ptr()))
+    _check(st)
+    return out, k_star, cg_info
 
 
 def intermediates(res: Result) -> dict:

@@ -125,6 +125,24 @@ int make_plan(const grkv_problem* prob, int64_t n, int32_t window, int32_t budge
   return GRKV_OK;
 }
 
+// Workspace of the key step, after the compress workspace.  The key passes
+// hold one block per compute unit (all m rows, a split of the retained keys).
+static void make_key_plan(const Plan& p, KeyPlan* kp) {
+  split_range(p.c, ceil_div(256, p.U), 64, &kp->S4, &kp->chunk4);
+  const size_t U = p.U, mp = p.mp, d = p.d;
+  size_t off = p.total;
+  auto take = [&](size_t bytes) { size_t o2 = off; off = align256(off + bytes); return o2; };
+  kp->Fm = take(U * mp * d * sizeof(float));
+  kp->alpha = take(U * mp * d * sizeof(float));
+  kp->r = take(U * mp * d * sizeof(float));
+  kp->p = take(U * mp * d * sizeof(float));
+  kp->W = take(U * mp * mp * sizeof(float));
+  kp->opart = take(U * kp->S4 * mp * d * sizeof(float));
+  kp->hpart = take(U * kp->S4 * mp * sizeof(float));
+  kp->cg = take(U * 4 * sizeof(double));
+  kp->total = off;
+}
+
 }  // namespace grkv
 
 using namespace grkv;
@@ -174,18 +192,22 @@ int grkv_workspace_layout(const grkv_problem* prob, int64_t n, int32_t window, i
   return GRKV_OK;
 }
 
-int grkv_compress(const void* q_obs, const void* K, const void* V, int64_t n, int32_t window,
-                  int32_t budget, int32_t pool_kernel, float lambda, void* stream,
-                  const grkv_problem* prob, const grkv_options* opt, const grkv_outputs* out) {
+}  // extern "C"
+
+namespace {
+
+// Pointer checks shared by the entry points.
+int check_pointers(const void* q_obs, const void* K, const void* V, const grkv_problem* prob,
+                   const grkv_outputs* out) {
   if (!q_obs || !K || !V || !prob || !out) return GRKV_ERR_INVALID;
   if (!out->idx || !out->k_out || !out->v_out || !out->workspace) return GRKV_ERR_INVALID;
-  Plan p;
-  int st = make_plan(prob, n, window, budget, pool_kernel, lambda, opt, &p);
-  if (st != GRKV_OK) return st;
-  if (out->workspace_bytes < p.total) return GRKV_ERR_WORKSPACE;
   if (((uintptr_t)out->workspace & 255) != 0) return GRKV_ERR_INVALID;
+  return GRKV_OK;
+}
 
-  hipStream_t s = (hipStream_t)stream;
+// The launch sequence of one call (arguments already checked).
+int run_compress(const Plan& p, const void* q_obs, const void* K, const void* V, int64_t n,
+                 hipStream_t s, const grkv_outputs* out) {
   char* ws = (char*)out->workspace;
   auto F = [&](size_t o) { return (float*)(ws + o); };
   auto Dd = [&](size_t o) { return (double*)(ws + o); };
@@ -279,6 +301,98 @@ int grkv_compress(const void* q_obs, const void* K, const void* V, int64_t n, in
   }
 #undef GRKV_STAGE
 #undef GRKV_TRY
+  return GRKV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int grkv_compress(const void* q_obs, const void* K, const void* V, int64_t n, int32_t window,
+                  int32_t budget, int32_t pool_kernel, float lambda, void* stream,
+                  const grkv_problem* prob, const grkv_options* opt, const grkv_outputs* out) {
+  int st = check_pointers(q_obs, K, V, prob, out);
+  if (st != GRKV_OK) return st;
+  Plan p;
+  st = make_plan(prob, n, window, budget, pool_kernel, lambda, opt, &p);
+  if (st != GRKV_OK) return st;
+  if (out->workspace_bytes < p.total) return GRKV_ERR_WORKSPACE;
+  return run_compress(p, q_obs, K, V, n, (hipStream_t)stream, out);
+}
+
+void grkv_default_key_options(grkv_key_options* kopt, float lambda) {
+  if (!kopt) return;
+  kopt->lambda_k = lambda;
+  kopt->max_iter = 64;
+  kopt->tol = 1e-5f;
+}
+
+size_t grkv_workspace_bytes_kv(const grkv_problem* prob, int64_t n, int32_t window,
+                               int32_t budget) {
+  Plan p;
+  if (make_plan(prob, n, window, budget, 1, 0.f, nullptr, &p) != GRKV_OK) return 0;
+  if (!key_supported(p)) return 0;
+  KeyPlan kp;
+  make_key_plan(p, &kp);
+  return kp.total;
+}
+
+int grkv_compress_kv(const void* q_obs, const void* K, const void* V, int64_t n, int32_t window,
+                     int32_t budget, int32_t pool_kernel, float lambda, void* stream,
+                     const grkv_problem* prob, const grkv_options* opt, const grkv_outputs* out,
+                     const grkv_key_options* kopt, float* k_star, float* cg_info) {
+  int st = check_pointers(q_obs, K, V, prob, out);
+  if (st != GRKV_OK) return st;
+  if (!k_star) return GRKV_ERR_INVALID;
+  grkv_key_options ko;
+  grkv_default_key_options(&ko, lambda);
+  if (kopt) ko = *kopt;
+  if (!(ko.lambda_k >= 0.f) || !isfinite(ko.lambda_k)) return GRKV_ERR_INVALID;
+  if (ko.max_iter < 0 || ko.max_iter > 4096 || !(ko.tol >= 0.f) || !isfinite(ko.tol))
+    return GRKV_ERR_INVALID;
+  Plan p;
+  st = make_plan(prob, n, window, budget, pool_kernel, lambda, opt, &p);
+  if (st != GRKV_OK) return st;
+  if (!key_supported(p)) return GRKV_ERR_UNSUPPORTED;
+  KeyPlan kp;
+  make_key_plan(p, &kp);
+  if (out->workspace_bytes < kp.total) return GRKV_ERR_WORKSPACE;
+  hipStream_t s = (hipStream_t)stream;
+  st = run_compress(p, q_obs, K, V, n, s, out);
+  if (st != GRKV_OK) return st;
+
+  char* ws = (char*)out->workspace;
+  auto F = [&](size_t o) { return (float*)(ws + o); };
+  KeyArgs a = {};
+  a.q = (const uint16_t*)q_obs;
+  a.k0 = (const uint16_t*)out->k_out;
+  a.vs = out->v_out;
+  a.lse2 = F(p.lse2_log2);
+  a.fixed = (const uint8_t*)(ws + p.fixed);
+  a.idx = out->idx;
+  a.y = F(p.y);
+  a.zt = F(p.z);
+  a.stats_ws = F(p.stats_ws);
+  a.Fm = F(kp.Fm);
+  a.alpha = F(kp.alpha);
+  a.r = F(kp.r);
+  a.p = F(kp.p);
+  a.W = F(kp.W);
+  a.opart = F(kp.opart);
+  a.hpart = F(kp.hpart);
+  a.cg = (double*)(ws + kp.cg);
+  a.kstar = k_star;
+  a.cg_info = cg_info;
+  a.lam_k = ko.lambda_k;
+  a.tol = ko.tol;
+  a.max_iter = ko.max_iter;
+  void** ev = out->stage_events;
+  const bool timed = ev && ev[2 * GRKV_STAGE_KEY] && ev[2 * GRKV_STAGE_KEY + 1];
+  if (timed && hipEventRecord((hipEvent_t)ev[2 * GRKV_STAGE_KEY], s) != hipSuccess)
+    return GRKV_ERR_HIP;
+  if (launch_key(p, kp, a, s) != hipSuccess) return GRKV_ERR_HIP;
+  if (timed && hipEventRecord((hipEvent_t)ev[2 * GRKV_STAGE_KEY + 1], s) != hipSuccess)
+    return GRKV_ERR_HIP;
   return GRKV_OK;
 }
 

@@ -134,4 +134,36 @@ hipError_t launch_update_add(const Plan& p, const float* x, const uint8_t* fixed
                              const float* z, const float* stats_ws, float* v_out,
                              hipStream_t s);
 
+// Key step (bf16 path, mp <= 128): conjugate gradients on the dual system of
+// the linearized key ridge problem, then K* = K0 + J_G^T alpha.  Per-unit CG
+// state values (cg[u][3], reported in cg_info[u][2] as the GRKV_KEY_* codes).
+enum { kKeyRunning = 0, kKeyConverged = 1, kKeyMaxIter = 2, kKeySkipped = 3, kKeyBreakdown = 4 };
+
+struct KeyPlan {
+  int S4, chunk4;   // splits of the retained keys per unit for the key passes
+  size_t Fm, alpha, r, p, W, opart, hpart, cg;   // offsets after Plan::total
+  size_t total;
+};
+
+struct KeyArgs {
+  const uint16_t* q;        // [U][m][d] window queries
+  const uint16_t* k0;       // [U][c][d] retained keys K0
+  const float* vs;          // [U][c][d] merged values V*
+  const float* lse2;        // [U][mp] retained log-sum-exp (log2 domain)
+  const uint8_t* fixed;     // [U][c]
+  const int32_t* idx;       // [U][c] retained positions
+  const float* y;           // [U][mp][d] Y
+  const float* zt;          // [U][d][mp] Z^T of the value step
+  const float* stats_ws;    // [U][4] value-step stats (status in [3])
+  float *Fm, *alpha, *r, *p, *W, *opart, *hpart;
+  double* cg;               // [U][4] {r.r, r0.r0, iterations, state}
+  float* kstar;             // [U][c][d] out
+  float* cg_info;           // [U][4] out or null
+  float lam_k, tol;
+  int max_iter;
+};
+
+bool key_supported(const Plan& p);
+hipError_t launch_key(const Plan& p, const KeyPlan& kp, const KeyArgs& a, hipStream_t s);
+
 }  // namespace grkv

@@ -1,0 +1,567 @@
+// Key step of GRKV on the bf16 path: the local linearized dual ridge update of
+// the free retained keys (Sec. 3.3 "Key step" and "Linearized dual solution",
+// Eq. 9-10; Algorithm 1, key step; App. D.2 and D.3), run after the value step
+// with the merged values V* held fixed and K_cur = K0 (one alternating step).
+//
+// With X = softmax(Q K0^T / sqrt(d)) (the retained-set attention of the value
+// step), F = X V* = f(K0) and W = Q Q^T / d, the operator of the dual system
+// is applied matrix-free:
+//   J_G^T a : D = X o (a V*^T - rowdot(F, a) 1^T) with the fixed columns zeroed,
+//             dK_j = sum_r D_rj q_r / sqrt(d);
+//   J_G dK  : H = X o (W D) (the logit change is Q dK^T / sqrt(d) = W D),
+//             J_G dK = H V* - diag(H 1) F;
+// so (J_G J_G^T + lambda_k I) a needs no stored Jacobian.  The right-hand side
+// is E = Y - f(K0), which after the value step equals lambda_v Z in closed
+// form (Y - X V* = lambda_v Z), so F = Y - lambda_v Z as well.  The system is
+// solved by conjugate gradients from a = 0 (App. D.2); K* = K0 + J_G^T a.
+//
+// Kernels: key_init (one block per unit: F, E, W, CG state), key_pass (the
+// operator, or the final J_G^T a, over the retained keys in splits), key_cg
+// (one block per unit: combines the split partials, one CG update).  The
+// host enqueues max_iter pairs of key_pass + key_cg; a unit that has converged
+// makes both return at once.
+//
+// key_pass: a block holds all m rows of one unit and a split of its retained
+// keys, one wave per 16 rows.  Keys come in tiles of 32: K0 rows (bf16) and V*
+// rows split into bf16 hi + lo parts are staged in LDS, V* also transposed.  A
+// wave computes, for its 16 rows, S = Q K^T and B = a V*^T on the MFMA (the
+// result holds each lane's key column), D = X o (B - s), and writes D to LDS
+// transposed; then A^T = D^T W and S^T = K Q^T give H^T = X^T o A^T with each
+// lane holding one row, which is the operand layout of out^T += V*^T H^T.
+// Products of fp32 values use three bf16 MFMAs (hi*hi + hi*lo + lo*hi).
+#include <math.h>
+
+#include "grkv_device.h"
+#include "grkv_internal.h"
+
+namespace grkv {
+namespace {
+
+constexpr int kKT = 32;   // retained keys per tile
+
+// Position, inside a block of 32, of the index a lane holds as element j of an
+// MFMA operand when the operand comes from an MFMA result: elements
+// {4g + i} and {16 + 4g + i} (i < 4) of group g become 8g + i and 8g + 4 + i,
+// so the eight values of a lane sit next to each other.
+__device__ __forceinline__ int kperm(int x) {
+  const int b = x & ~31, o = x & 31;
+  return b + ((o & 15) >> 2) * 8 + (o >> 4) * 4 + (o & 3);
+}
+
+__device__ __forceinline__ double block_sum(double v, double* red) {
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  __syncthreads();
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  double t = 0;
+  for (int k = 0; k < nw; ++k) t += red[k];
+  return t;
+}
+
+// ------------------------------------------------------------------ init ----
+template <int MP, int D>
+__global__ __launch_bounds__(256) void key_init_kernel(
+    const u16* __restrict__ q, const float* __restrict__ y, const float* __restrict__ zt,
+    const float* __restrict__ stats_ws, float lam_v, int m, float* __restrict__ Fm,
+    float* __restrict__ alpha, float* __restrict__ r, float* __restrict__ p,
+    float* __restrict__ W, double* __restrict__ cg) {
+  __shared__ double red[4];
+  const int u = blockIdx.x, tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6, l16 = lane & 15, g = lane >> 4;
+  const bool skip = stats_ws[u * 4 + 3] != 0.f;
+  double ee = 0;
+  for (int e = tid; e < MP * D; e += 256) {
+    const int row = e / D, col = e % D;
+    const size_t o = (size_t)u * MP * D + e;
+    const float E = (!skip && row < m) ? lam_v * zt[((size_t)u * D + col) * MP + row] : 0.f;
+    Fm[o] = row < m ? y[o] - E : 0.f;
+    alpha[o] = 0.f;
+    r[o] = E;
+    p[o] = E;
+    ee += (double)E * E;
+  }
+  // W = Q Q^T / d (bf16 products are exact; fp32 sums)
+  const u16* qu = q + (size_t)u * m * D;
+  for (int t = wave; t < (MP / 16) * (MP / 16); t += 4) {
+    const int ta = t / (MP / 16), tb = t % (MP / 16);
+    const int ra = ta * 16 + l16, rb = tb * 16 + l16;
+    f32x4 acc = zero4();
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) {
+      const uint4 a = ra < m ? *reinterpret_cast<const uint4*>(qu + (size_t)ra * D + ks * 32 + 8 * g)
+                             : make_uint4(0, 0, 0, 0);
+      const uint4 b = rb < m ? *reinterpret_cast<const uint4*>(qu + (size_t)rb * D + ks * 32 + 8 * g)
+                             : make_uint4(0, 0, 0, 0);
+      acc = mfma_bf16(as_bf16x8(a), as_bf16x8(b), acc);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      W[((size_t)u * MP + ta * 16 + 4 * g + i) * MP + tb * 16 + l16] = acc[i] * (1.f / D);
+  }
+  ee = block_sum(ee, red);
+  if (tid == 0) {
+    cg[u * 4 + 0] = ee;
+    cg[u * 4 + 1] = ee;
+    cg[u * 4 + 2] = 0;
+    cg[u * 4 + 3] = skip ? kKeySkipped : ee == 0 ? kKeyConverged : kKeyRunning;
+  }
+}
+
+// ------------------------------------------------------------------ pass ----
+template <int MP, int D>
+struct KeyLds {
+  static constexpr int KS = D + 8;     // row stride (bf16) of K and V rows
+  static constexpr int TS = kKT + 8;   // row stride of V^T rows
+  static constexpr int DS = MP + 8;    // row stride of D^T rows
+  static constexpr int QS = MP + 8;    // row stride of Q^T rows
+  static constexpr int k = 0;
+  static constexpr int vh = k + kKT * KS;
+  static constexpr int vl = vh + kKT * KS;
+  static constexpr int th = vl + kKT * KS;
+  static constexpr int tl = th + D * TS;
+  static constexpr int dh = tl + D * TS;
+  static constexpr int dl = dh + kKT * DS;
+  static constexpr int qt = dl + kKT * DS;
+  static constexpr int end = qt;             // the operator pass
+  static constexpr int end_final = qt + D * QS;
+  static constexpr size_t bytes(bool final_pass) {
+    return (size_t)(final_pass ? end_final : end) * sizeof(u16) + kKT * (sizeof(int) + 1);
+  }
+};
+
+// FINAL = false: partial sums of H V* (opart) and H 1 (hpart) over this
+// block's keys for the direction in pv.  FINAL = true: K* = K0 + J_G^T pv for
+// this block's keys.
+template <int MP, int D, bool FINAL>
+__global__ __launch_bounds__(MP / 16 * 64) void key_pass_kernel(
+    const u16* __restrict__ q, const u16* __restrict__ k0, const float* __restrict__ vs,
+    const float* __restrict__ lse2, const uint8_t* __restrict__ fixed,
+    const int32_t* __restrict__ idx, const float* __restrict__ Fm, const float* __restrict__ W,
+    const float* __restrict__ pv, const double* __restrict__ cg, float* __restrict__ opart,
+    float* __restrict__ hpart, float* __restrict__ kstar, float* __restrict__ cg_info, int m,
+    int w, int64_t n, int c, int S, int chunk, int causal, float scale_log2, float inv_sqrt_d) {
+  constexpr int NW = MP / 16, NTH = NW * 64;
+  constexpr int KCH = kKT * D / 8;            // 16-byte chunks of a K tile
+  constexpr int KPT = (KCH + NTH - 1) / NTH;
+  constexpr int VPR = kKT / 4 * D;            // (4-key group, column) pairs of a V tile
+  constexpr int VPT = VPR / NTH;
+  static_assert(VPR % NTH == 0, "V tile pairs must divide over the block");
+  constexpr float NEG_INF = -__builtin_huge_valf();
+  using L = KeyLds<MP, D>;
+  extern __shared__ __attribute__((aligned(16))) u16 sm[];
+  int* kp_s = reinterpret_cast<int*>(sm + (FINAL ? L::end_final : L::end));
+  uint8_t* fx_s = reinterpret_cast<uint8_t*>(kp_s + kKT);
+
+  const int u = blockIdx.y, s = blockIdx.x, tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6, l16 = lane & 15, g = lane >> 4;
+  const int state = (int)cg[u * 4 + 3];
+  const int j0 = s * chunk, j1 = min(c, j0 + chunk);
+  if (FINAL && s == 0 && tid == 0 && cg_info) {
+    const double rr = cg[u * 4 + 0], rr0 = cg[u * 4 + 1];
+    cg_info[u * 4 + 0] = (float)cg[u * 4 + 2];
+    cg_info[u * 4 + 1] = rr0 > 0 ? (float)sqrt(rr / rr0) : 0.f;
+    cg_info[u * 4 + 2] = (float)(state == kKeyRunning ? kKeyMaxIter : state);
+    cg_info[u * 4 + 3] = (float)sqrt(rr0);
+  }
+  if (!FINAL && state != kKeyRunning) return;
+  if (FINAL && state == kKeySkipped) {
+    for (int e = tid; e < (j1 - j0) * D; e += NTH) {
+      const size_t o = ((size_t)u * c + j0) * D + e;
+      kstar[o] = bf16_to_f32(k0[o]);
+    }
+    return;
+  }
+
+  // per-wave constants: Q rows, the direction's rows (bf16 hi/lo), s = rowdot(F, dir)
+  const int row = 16 * wave + l16;
+  const u16* qu = q + (size_t)u * m * D;
+  uint4 qa[D / 32];
+#pragma unroll
+  for (int ks = 0; ks < D / 32; ++ks)
+    qa[ks] = row < m ? *reinterpret_cast<const uint4*>(qu + (size_t)row * D + ks * 32 + 8 * g)
+                     : make_uint4(0, 0, 0, 0);
+  bf16x8 pah[D / 32], pal[D / 32];
+  float sdot = 0.f;
+  {
+    const float* pr = pv + ((size_t)u * MP + row) * D;
+    const float* fr = Fm + ((size_t)u * MP + row) * D;
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) {
+      const float4 a0 = *reinterpret_cast<const float4*>(pr + ks * 32 + 8 * g);
+      const float4 a1 = *reinterpret_cast<const float4*>(pr + ks * 32 + 8 * g + 4);
+      const float4 f0 = *reinterpret_cast<const float4*>(fr + ks * 32 + 8 * g);
+      const float4 f1 = *reinterpret_cast<const float4*>(fr + ks * 32 + 8 * g + 4);
+      const float x[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+      sdot += a0.x * f0.x + a0.y * f0.y + a0.z * f0.z + a0.w * f0.w;
+      sdot += a1.x * f1.x + a1.y * f1.y + a1.z * f1.z + a1.w * f1.w;
+      split8(x, pah[ks], pal[ks]);
+    }
+  }
+  sdot += __shfl_xor(sdot, 16);
+  sdot += __shfl_xor(sdot, 32);
+  // an MFMA result gives a lane rows 16w + 4g + i
+  float s4[4], nl4[4];
+  int rp4[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r4 = 16 * wave + 4 * g + i;
+    s4[i] = __shfl(sdot, 4 * g + i);
+    nl4[i] = r4 < m ? -lse2[(size_t)u * MP + r4] : NEG_INF;
+    rp4[i] = r4 < m ? (int)(n - w + r4 % w) : -1;
+  }
+  const float nl_row = row < m ? -lse2[(size_t)u * MP + row] : NEG_INF;
+  const int rp_row = row < m ? (int)(n - w + row % w) : -1;
+
+  bf16x8 wah[MP / 32], wal[MP / 32];
+  if constexpr (!FINAL) {
+    // W row of this lane at the columns 32kb + {4g + i, 16 + 4g + i}
+    const float* wr = W + ((size_t)u * MP + row) * MP;
+#pragma unroll
+    for (int kb = 0; kb < MP / 32; ++kb) {
+      const float4 a = *reinterpret_cast<const float4*>(wr + 32 * kb + 4 * g);
+      const float4 b = *reinterpret_cast<const float4*>(wr + 32 * kb + 16 + 4 * g);
+      const float x[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+      split8(x, wah[kb], wal[kb]);
+    }
+  } else {
+    // Q^T in LDS, rows permuted by kperm: QT[dd][kperm(r)] = Q[r][dd]
+    for (int e = tid; e < MP * D; e += NTH) {
+      const int r = e / D, dd = e % D;
+      sm[L::qt + dd * L::QS + kperm(r)] = r < m ? qu[(size_t)r * D + dd] : (u16)0;
+    }
+  }
+
+  // register-staged tile loads
+  const u16* ku = k0 + (size_t)u * c * D;
+  const float* vu = vs + (size_t)u * c * D;
+  uint4 kreg[KPT];
+  float vreg[VPT][4];
+  int kpreg = 0, fxreg = 1;
+  auto load_tile = [&](int t0) {
+#pragma unroll
+    for (int k = 0; k < KPT; ++k) {
+      const int e = tid + k * NTH;
+      const int key = e / (D / 8), ch = e % (D / 8);
+      kreg[k] = (e < KCH && t0 + key < j1)
+                    ? *reinterpret_cast<const uint4*>(ku + (size_t)(t0 + key) * D + ch * 8)
+                    : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int k = 0; k < VPT; ++k) {
+      const int e = tid + k * NTH;
+      const int kq = e / D, dd = e % D;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int key = t0 + 4 * kq + i;
+        vreg[k][i] = key < j1 ? vu[(size_t)key * D + dd] : 0.f;
+      }
+    }
+    if (tid < kKT) {
+      const int key = t0 + tid;
+      kpreg = key < j1 ? idx[(size_t)u * c + key] : 0x7fffffff;
+      fxreg = key < j1 ? fixed[(size_t)u * c + key] : 1;
+    }
+  };
+  auto store_tile = [&]() {
+#pragma unroll
+    for (int k = 0; k < KPT; ++k) {
+      const int e = tid + k * NTH;
+      if (e < KCH) {
+        const int key = e / (D / 8), ch = e % (D / 8);
+        *reinterpret_cast<uint4*>(sm + L::k + key * L::KS + ch * 8) = kreg[k];
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < VPT; ++k) {
+      const int e = tid + k * NTH;
+      const int kq = e / D, dd = e % D;
+      u16 h[4], l[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const __bf16 hb = (__bf16)vreg[k][i];
+        h[i] = __builtin_bit_cast(u16, hb);
+        l[i] = __builtin_bit_cast(u16, (__bf16)(vreg[k][i] - (float)hb));
+        sm[L::vh + (4 * kq + i) * L::KS + dd] = h[i];
+        sm[L::vl + (4 * kq + i) * L::KS + dd] = l[i];
+      }
+      const int tp = dd * L::TS + kperm(4 * kq);
+      *reinterpret_cast<uint2*>(sm + L::th + tp) =
+          make_uint2(h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16));
+      *reinterpret_cast<uint2*>(sm + L::tl + tp) =
+          make_uint2(l[0] | ((uint32_t)l[1] << 16), l[2] | ((uint32_t)l[3] << 16));
+    }
+    if (tid < kKT) {
+      kp_s[tid] = kpreg;
+      fx_s[tid] = (uint8_t)fxreg;
+    }
+  };
+
+  f32x4 oacc[D / 16];
+#pragma unroll
+  for (int dt = 0; dt < D / 16; ++dt) oacc[dt] = zero4();
+  float hs = 0.f;
+
+  if (j0 < j1) load_tile(j0);
+  for (int t0 = j0; t0 < j1; t0 += kKT) {
+    __syncthreads();   // the previous tile is no longer read
+    store_tile();
+    __syncthreads();
+    if (t0 + kKT < j1) load_tile(t0 + kKT);
+
+    // S = Q K^T, B = dir V^T, D = X o (B - s) for this wave's rows -> D^T in LDS
+#pragma unroll
+    for (int kt = 0; kt < kKT / 16; ++kt) {
+      const int key = 16 * kt + l16;
+      f32x4 sacc = zero4(), bacc = zero4();
+#pragma unroll
+      for (int ks = 0; ks < D / 32; ++ks) {
+        const int o = key * L::KS + ks * 32 + 8 * g;
+        const bf16x8 kk = as_bf16x8(*reinterpret_cast<const uint4*>(sm + L::k + o));
+        const bf16x8 vh = as_bf16x8(*reinterpret_cast<const uint4*>(sm + L::vh + o));
+        const bf16x8 vl = as_bf16x8(*reinterpret_cast<const uint4*>(sm + L::vl + o));
+        sacc = mfma_bf16(as_bf16x8(qa[ks]), kk, sacc);
+        bacc = mfma_bf16(pah[ks], vh, bacc);
+        bacc = mfma_bf16(pah[ks], vl, bacc);
+        bacc = mfma_bf16(pal[ks], vh, bacc);
+      }
+      const int kpos = kp_s[key];
+      const bool live = t0 + key < j1;
+      const bool free_key = live && fx_s[key] == 0;
+      u16 dh[4], dl[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const bool vis = live && (!causal || kpos <= rp4[i]);
+        const float x = vis ? __builtin_amdgcn_exp2f(fmaf(sacc[i], scale_log2, nl4[i])) : 0.f;
+        const float dv = free_key ? x * (bacc[i] - s4[i]) : 0.f;
+        const __bf16 hb = (__bf16)dv;
+        dh[i] = __builtin_bit_cast(u16, hb);
+        dl[i] = __builtin_bit_cast(u16, (__bf16)(dv - (float)hb));
+      }
+      const int dp = key * L::DS + 32 * (wave >> 1) + 8 * g + 4 * (wave & 1);
+      *reinterpret_cast<uint2*>(sm + L::dh + dp) =
+          make_uint2(dh[0] | ((uint32_t)dh[1] << 16), dh[2] | ((uint32_t)dh[3] << 16));
+      *reinterpret_cast<uint2*>(sm + L::dl + dp) =
+          make_uint2(dl[0] | ((uint32_t)dl[1] << 16), dl[2] | ((uint32_t)dl[3] << 16));
+    }
+    __syncthreads();   // D^T of all rows is in LDS
+
+    if constexpr (FINAL) {
+      // dK [keys x d] = D^T Q / sqrt(d); K* = K0 + dK (fixed keys: dK = 0)
+      for (int tl = wave; tl < (kKT / 16) * (D / 16); tl += NW) {
+        const int kt = tl / (D / 16), dt = tl % (D / 16);
+        f32x4 acc = zero4();
+#pragma unroll
+        for (int kb = 0; kb < MP / 32; ++kb) {
+          const int ao = (16 * kt + l16) * L::DS + 32 * kb + 8 * g;
+          const bf16x8 ah = as_bf16x8(*reinterpret_cast<const uint4*>(sm + L::dh + ao));
+          const bf16x8 al = as_bf16x8(*reinterpret_cast<const uint4*>(sm + L::dl + ao));
+          const bf16x8 b = as_bf16x8(*reinterpret_cast<const uint4*>(
+              sm + L::qt + (16 * dt + l16) * L::QS + 32 * kb + 8 * g));
+          acc = mfma_bf16(ah, b, acc);
+          acc = mfma_bf16(al, b, acc);
+        }
+        const int dd = 16 * dt + l16;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int key = 16 * kt + 4 * g + i;
+          if (t0 + key < j1)
+            kstar[((size_t)u * c + t0 + key) * D + dd] =
+                bf16_to_f32(sm[L::k + key * L::KS + dd]) + acc[i] * inv_sqrt_d;
+        }
+      }
+    } else {
+      // A^T = D^T W and S^T = K Q^T: lane holds [key 16kt + 4g + i][row]
+      float h8[8];
+#pragma unroll
+      for (int kt = 0; kt < kKT / 16; ++kt) {
+        f32x4 aacc = zero4(), stacc = zero4();
+#pragma unroll
+        for (int kb = 0; kb < MP / 32; ++kb) {
+          const int ao = (16 * kt + l16) * L::DS + 32 * kb + 8 * g;
+          const bf16x8 dh = as_bf16x8(*reinterpret_cast<const uint4*>(sm + L::dh + ao));
+          const bf16x8 dl = as_bf16x8(*reinterpret_cast<const uint4*>(sm + L::dl + ao));
+          aacc = mfma_bf16(dh, wah[kb], aacc);
+          aacc = mfma_bf16(dh, wal[kb], aacc);
+          aacc = mfma_bf16(dl, wah[kb], aacc);
+        }
+#pragma unroll
+        for (int ks = 0; ks < D / 32; ++ks) {
+          const bf16x8 kk = as_bf16x8(*reinterpret_cast<const uint4*>(
+              sm + L::k + (16 * kt + l16) * L::KS + ks * 32 + 8 * g));
+          stacc = mfma_bf16(kk, as_bf16x8(qa[ks]), stacc);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int key = 16 * kt + 4 * g + i;
+          const bool vis = t0 + key < j1 && (!causal || kp_s[key] <= rp_row);
+          const float x = vis ? __builtin_amdgcn_exp2f(fmaf(stacc[i], scale_log2, nl_row)) : 0.f;
+          const float h = x * aacc[i];
+          h8[4 * kt + i] = h;
+          hs += h;
+        }
+      }
+      // out^T [d x rows] += V*^T H^T over the tile's 32 keys
+      bf16x8 hh, hl;
+      split8(h8, hh, hl);
+#pragma unroll
+      for (int dt = 0; dt < D / 16; ++dt) {
+        const int vo = (16 * dt + l16) * L::TS + 8 * g;
+        const bf16x8 th = as_bf16x8(*reinterpret_cast<const uint4*>(sm + L::th + vo));
+        const bf16x8 tl = as_bf16x8(*reinterpret_cast<const uint4*>(sm + L::tl + vo));
+        oacc[dt] = mfma_bf16(th, hh, oacc[dt]);
+        oacc[dt] = mfma_bf16(th, hl, oacc[dt]);
+        oacc[dt] = mfma_bf16(tl, hh, oacc[dt]);
+      }
+    }
+  }
+
+  if constexpr (!FINAL) {
+    // lane holds out[row][16dt + 4g + i]
+    float* op = opart + (((size_t)u * S + s) * MP + row) * D;
+#pragma unroll
+    for (int dt = 0; dt < D / 16; ++dt)
+      *reinterpret_cast<float4*>(op + 16 * dt + 4 * g) =
+          make_float4(oacc[dt][0], oacc[dt][1], oacc[dt][2], oacc[dt][3]);
+    hs += __shfl_xor(hs, 16);
+    hs += __shfl_xor(hs, 32);
+    if (g == 0) hpart[((size_t)u * S + s) * MP + row] = hs;
+  }
+}
+
+// -------------------------------------------------------------------- cg ----
+// One conjugate-gradient update per unit: Ap = sum_s opart - (sum_s hpart) o F
+// + lambda_k p; alpha += a p; r -= a Ap; p = r + beta p.
+template <int MP, int D>
+__global__ __launch_bounds__(1024) void key_cg_kernel(
+    const float* __restrict__ opart, const float* __restrict__ hpart, int S,
+    const float* __restrict__ Fm, float* __restrict__ alpha, float* __restrict__ r,
+    float* __restrict__ p, double* __restrict__ cg, float lam_k, float tol, int max_iter) {
+  constexpr int NTH = 1024, E = MP * D, PER = (E + NTH - 1) / NTH;
+  __shared__ float hsum[MP];
+  __shared__ double red[16];
+  const int u = blockIdx.x, tid = threadIdx.x;
+  if ((int)cg[u * 4 + 3] != kKeyRunning) return;
+  for (int i = tid; i < MP; i += NTH) {
+    float h = 0.f;
+    for (int k = 0; k < S; ++k) h += hpart[((size_t)u * S + k) * MP + i];
+    hsum[i] = h;
+  }
+  __syncthreads();
+  const size_t base = (size_t)u * E;
+  float ap[PER], pp[PER];
+  double pap = 0;
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int e = tid + k * NTH;
+    ap[k] = pp[k] = 0.f;
+    if (e < E) {
+      float v = 0.f;
+      for (int sp = 0; sp < S; ++sp) v += opart[((size_t)u * S + sp) * E + e];
+      const float pe = p[base + e];
+      v = v - hsum[e / D] * Fm[base + e] + lam_k * pe;
+      ap[k] = v;
+      pp[k] = pe;
+      pap += (double)pe * v;
+    }
+  }
+  pap = block_sum(pap, red);
+  const double rr = cg[u * 4 + 0], rr0 = cg[u * 4 + 1];
+  const int it = (int)cg[u * 4 + 2] + 1;
+  if (!(pap > 0)) {
+    if (tid == 0) cg[u * 4 + 3] = kKeyBreakdown;
+    return;
+  }
+  const float a = (float)(rr / pap);
+  float rv[PER];
+  double rn = 0;
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int e = tid + k * NTH;
+    rv[k] = 0.f;
+    if (e < E) {
+      alpha[base + e] += a * pp[k];
+      rv[k] = r[base + e] - a * ap[k];
+      r[base + e] = rv[k];
+      rn += (double)rv[k] * rv[k];
+    }
+  }
+  rn = block_sum(rn, red);
+  int st = kKeyRunning;
+  if (sqrt(rn) <= (double)tol * sqrt(rr0)) st = kKeyConverged;
+  else if (it >= max_iter) st = kKeyMaxIter;
+  if (st == kKeyRunning) {
+    const float beta = (float)(rn / rr);
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int e = tid + k * NTH;
+      if (e < E) p[base + e] = rv[k] + beta * pp[k];
+    }
+  }
+  if (tid == 0) {
+    cg[u * 4 + 0] = rn;
+    cg[u * 4 + 2] = it;
+    cg[u * 4 + 3] = st;
+  }
+}
+
+template <int MP, int D>
+hipError_t launch_key_t(const Plan& p, const KeyPlan& kp, const KeyArgs& a, hipStream_t s) {
+  using L = KeyLds<MP, D>;
+  const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
+  const float inv_sqrt_d = (float)(1.0 / sqrt((double)D));
+  hipLaunchKernelGGL((key_init_kernel<MP, D>), dim3(p.U), dim3(256), 0, s, a.q, a.y, a.zt,
+                     a.stats_ws, p.lam, p.m, a.Fm, a.alpha, a.r, a.p, a.W, a.cg);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const size_t lds_op = L::bytes(false), lds_fin = L::bytes(true);
+  e = hipFuncSetAttribute((const void*)key_pass_kernel<MP, D, false>,
+                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_op);
+  if (e != hipSuccess) return e;
+  e = hipFuncSetAttribute((const void*)key_pass_kernel<MP, D, true>,
+                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_fin);
+  if (e != hipSuccess) return e;
+  const dim3 grid(kp.S4, p.U), block(MP / 16 * 64);
+  const int causal = p.opt.causal_window ? 1 : 0;
+  for (int it = 0; it < a.max_iter; ++it) {
+    hipLaunchKernelGGL((key_pass_kernel<MP, D, false>), grid, block, lds_op, s, a.q, a.k0, a.vs,
+                       a.lse2, a.fixed, a.idx, a.Fm, a.W, a.p, a.cg, a.opart, a.hpart, nullptr,
+                       nullptr, p.m, p.w, p.n, p.c, kp.S4, kp.chunk4, causal, scale_log2,
+                       inv_sqrt_d);
+    hipLaunchKernelGGL((key_cg_kernel<MP, D>), dim3(p.U), dim3(1024), 0, s, a.opart, a.hpart,
+                       kp.S4, a.Fm, a.alpha, a.r, a.p, a.cg, a.lam_k, a.tol, a.max_iter);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL((key_pass_kernel<MP, D, true>), grid, block, lds_fin, s, a.q, a.k0, a.vs,
+                     a.lse2, a.fixed, a.idx, a.Fm, nullptr, a.alpha, a.cg, nullptr, nullptr,
+                     a.kstar, a.cg_info, p.m, p.w, p.n, p.c, kp.S4, kp.chunk4, causal,
+                     scale_log2, inv_sqrt_d);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+bool key_supported(const Plan& p) {
+  return stream_supported(p) && merge_fast_supported(p) && p.mp <= 128 &&
+         (p.d == 64 || p.d == 128);
+}
+
+hipError_t launch_key(const Plan& p, const KeyPlan& kp, const KeyArgs& a, hipStream_t s) {
+  if (p.d == 128) {
+    switch (p.mp) {
+      case 32: return launch_key_t<32, 128>(p, kp, a, s);
+      case 64: return launch_key_t<64, 128>(p, kp, a, s);
+      case 128: return launch_key_t<128, 128>(p, kp, a, s);
+    }
+  } else {
+    switch (p.mp) {
+      case 32: return launch_key_t<32, 64>(p, kp, a, s);
+      case 64: return launch_key_t<64, 64>(p, kp, a, s);
+      case 128: return launch_key_t<128, 64>(p, kp, a, s);
+    }
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace grkv

@@ -1,0 +1,195 @@
+"""GPU parity of the key step (grkv_compress_kv) against the float64 oracle.
+
+The oracle solves the dual key system to convergence; the GPU runs conjugate
+gradients in fp32 to a relative residual of 1e-5, so the bar is on the key
+update: max|K*_gpu - K*_oracle| <= 2e-3 max|K*_oracle - K0| per unit, with
+fixed keys bit-exact at K0.  Where the exact update is below 1% of the keys
+(budget = n, where the value step leaves no residual) the same 2e-3 applies
+relative to max|K*_oracle| instead.  The
+oracle takes the GPU's retained set (whose parity is tested on its own), so
+this file tests the key step alone.
+"""
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import grkv_key_oracle as KO
+from tests.parity import to_device
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+K_TOL = 2e-3
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _run(cfg, q, K, V, **kw):
+    import paper_2605_31105_amd as G
+    qd, Kd, Vd = (to_device(a, cfg.dtype) for a in (q, K, V))
+    res, kstar, info = G.compress_kv(qd, Kd, Vd, cfg.window, cfg.budget, cfg.pool_kernel,
+                                     cfg.lam, **kw)
+    torch.cuda.synchronize()
+    k0 = res.k_out.cpu().view(torch.int16).numpy().view(np.uint16)
+    return dict(idx=res.idx.cpu().numpy().astype(np.int64), k0=k0,
+                v_out=res.v_out.cpu().numpy(), stats=res.stats.cpu().numpy(),
+                kstar=kstar.cpu().numpy(), info=info.cpu().numpy())
+
+
+def _check(cfg, q, K, V, gpu, u, lam_k=None, report=None):
+    qd, Kd, Vd = (W.decode(a[u], cfg.dtype) for a in (q, K, V))
+    lam_k = cfg.lam if lam_k is None else lam_k
+    r = KO.grkv_unit(qd, Kd, Vd, cfg.window, cfg.budget, cfg.pool_kernel, cfg.lam, lam_k,
+                     idx=gpu["idx"][u])
+    K0 = W.bf16_bits_to_f32(gpu["k0"][u]).astype(np.float64)
+    ks = gpu["kstar"][u].astype(np.float64)
+    F = r["fixed"]
+    # fixed keys stay at K0 exactly
+    assert np.array_equal(ks[F], K0[F]), "unit %d: a fixed key moved" % u
+    dk = np.abs(r["Kstar"] - K0).max()
+    diff = np.abs(ks - r["Kstar"]).max()
+    kmax = np.abs(r["Kstar"]).max()
+    # the bar is on the update where the update is a visible part of the keys;
+    # where the exact update is (close to) zero, e.g. budget = n (R = 0), on
+    # the keys themselves (the merged-value gate applied to K*)
+    err = diff / dk if dk >= 1e-2 * kmax else diff / kmax
+    info = dict(unit=u, key_err=float(err), max_dk=float(dk), cg_iters=int(gpu["info"][u, 0]),
+                cg_rel=float(gpu["info"][u, 1]), state=int(gpu["info"][u, 2]),
+                oracle_iters=r["key"]["iterations"])
+    if report is not None:
+        report.append(info)
+    assert err <= K_TOL, info
+    return info
+
+
+def _full(cfg, label, units=None, **kw):
+    print("case", label, cfg, kw, flush=True)
+    q, K, V = W.make_batch(cfg)
+    gpu = _run(cfg, q, K, V, **kw)
+    rep = []
+    for u in (range(cfg.units) if units is None else units):
+        _check(cfg, q, K, V, gpu, u, lam_k=kw.get("lambda_k"), report=rep)
+    for r in rep:
+        print(r, flush=True)
+    return gpu
+
+
+def test_key_small_bf16_m32_d64():
+    gpu = _full(W.config(1, dtype="bf16"), "config1-bf16")
+    assert np.all(gpu["info"][:, 2] == 1)
+
+
+def test_key_config2_llama_layer_8k():
+    gpu = _full(W.config(2), "config2")
+    assert np.all(gpu["info"][:, 2] == 1)
+    assert np.all(gpu["info"][:, 1] <= 1e-5)
+
+
+def test_key_m64_d128():
+    _full(W.config(2, group=2, n=4096, budget=256), "config2-g2")
+
+
+def test_key_m128_d64():
+    _full(W.config(1, dtype="bf16", group=8, budget=256), "config1-bf16-g8")
+
+
+def test_key_config3_sampled():
+    _full(W.config(3), "config3", units=(0, 5))
+
+
+def test_key_config4_sampled():
+    # the 32-layer workload in one call; three units checked against the oracle
+    gpu = _full(W.config(4), "config4", units=(0, 128, 255))
+    assert np.all(np.isin(gpu["info"][:, 2], (1, 2)))
+
+
+@pytest.mark.parametrize("label,kw", [
+    ("lambda_k-0.1", dict(lambda_k=0.1)),
+    ("lambda_k-1e-3", dict(lambda_k=1e-3, max_iter=200)),
+    ("no-causal", dict(causal_window=False)),
+    ("beta-0", dict(beta=0.0, n_sink=0)),
+], ids=["lambda_k-0.1", "lambda_k-1e-3", "no-causal", "beta-0"])
+def test_key_options(label, kw):
+    cfg = W.config(2)
+    print("case", label, kw, flush=True)
+    q, K, V = W.make_batch(cfg, units=range(2))
+    cfg2 = W.config(2, layers=1, kv_heads=2)
+    gpu = _run(cfg2, q, K, V, **kw)
+    opt_kw = {k: v for k, v in kw.items() if k in ("causal_window", "beta", "n_sink")}
+    from oracle import grkv_oracle as O
+    opt = O.Options(**opt_kw) if opt_kw else None
+    for u in range(2):
+        qd, Kd, Vd = (W.decode(a[u], cfg.dtype) for a in (q, K, V))
+        lam_k = kw.get("lambda_k", cfg.lam)
+        r = KO.grkv_unit(qd, Kd, Vd, cfg.window, cfg.budget, cfg.pool_kernel, cfg.lam, lam_k,
+                         opt=opt, idx=gpu["idx"][u])
+        K0 = W.bf16_bits_to_f32(gpu["k0"][u]).astype(np.float64)
+        dk = np.abs(r["Kstar"] - K0).max()
+        assert dk >= 1e-2 * np.abs(r["Kstar"]).max()
+        err = np.abs(gpu["kstar"][u] - r["Kstar"]).max() / dk
+        print(label, u, err, gpu["info"][u], flush=True)
+        assert err <= K_TOL
+
+
+def test_key_iteration_limits():
+    cfg = W.config(2, layers=1, kv_heads=2)
+    q, K, V = W.make_batch(W.config(2), units=range(2))
+    # no iterations: alpha = 0, K* = K0 exactly
+    gpu = _run(cfg, q, K, V, max_iter=0)
+    K0 = W.bf16_bits_to_f32(gpu["k0"]).astype(np.float32)
+    assert np.array_equal(gpu["kstar"], K0)
+    assert np.all(gpu["info"][:, 0] == 0) and np.all(gpu["info"][:, 2] == 2)
+    # tol = 0 stops at max_iter
+    gpu = _run(cfg, q, K, V, max_iter=5, tol=0.0)
+    assert np.all(gpu["info"][:, 0] == 5) and np.all(gpu["info"][:, 2] == 2)
+    # a huge lambda_k keeps the keys
+    gpu = _run(cfg, q, K, V, lambda_k=1e9)
+    assert np.abs(gpu["kstar"] - K0).max() < 1e-6
+
+
+def test_key_value_outputs_match_compress():
+    # grkv_compress_kv returns the same value-step outputs as grkv_compress
+    import paper_2605_31105_amd as G
+    cfg = W.config(2)
+    q, K, V = W.make_batch(cfg)
+    qd, Kd, Vd = (to_device(a, cfg.dtype) for a in (q, K, V))
+    a = G.compress(qd, Kd, Vd, cfg.window, cfg.budget, cfg.pool_kernel, cfg.lam)
+    b, _, _ = G.compress_kv(qd, Kd, Vd, cfg.window, cfg.budget, cfg.pool_kernel, cfg.lam)
+    torch.cuda.synchronize()
+    assert torch.equal(a.idx, b.idx) and torch.equal(a.k_out, b.k_out)
+    assert torch.equal(a.v_out, b.v_out) and torch.equal(a.stats, b.stats)
+
+
+def test_key_deterministic():
+    cfg = W.config(2)
+    q, K, V = W.make_batch(cfg)
+    g1 = _run(cfg, q, K, V)
+    g2 = _run(cfg, q, K, V)
+    assert np.array_equal(g1["kstar"], g2["kstar"])
+
+
+KEY_EDGE = [
+    ("ragged-n", dict(n=1000, budget=200)),
+    ("m-96", dict(group=3)),
+    ("window-1", dict(window=1, budget=64)),
+    ("budget-eq-window", dict(budget=32)),
+    ("budget-eq-n", dict(n=640, budget=640)),
+    ("head-dim-64", dict(head_dim=64)),
+]
+
+
+@pytest.mark.parametrize("label,over", KEY_EDGE, ids=[e[0] for e in KEY_EDGE])
+def test_key_edge_shapes(label, over):
+    base = dict(layers=1, kv_heads=2, n=2048, budget=256)
+    base.update(over)
+    cfg = W.config(2, **base)
+    gpu = _full(cfg, label)
+    if label == "budget-eq-window":
+        # every retained token is a fixed window token: nothing moves
+        K0 = W.bf16_bits_to_f32(gpu["k0"]).astype(np.float32)
+        assert np.array_equal(gpu["kstar"], K0)
