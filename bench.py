@@ -13,9 +13,12 @@ roofline of the dominant kernel (its duration measured with HIP events around
 its launches inside the timed steps), and the float64 oracle's CPU throughput
 on a bounded sample of the same workload.  Besides: the same workload as one
 call per layer (`per_layer_calls`, not `value`) and the device copy bandwidth
-(`copy_gbs`, the practical ceiling for streaming).
+(`copy_gbs`, the practical ceiling for streaming), and the key step of GRKV
+run after the value step (`key_step`: grkv_compress_kv on the same workload,
+its CG iterations and the time of one CG iteration against the MFMA peak).
 
   python bench.py [--steps K] [--warmup W] [--config 4] [--no-cpu-baseline] [--no-per-layer]
+                  [--no-key-step]
 """
 from __future__ import annotations
 
@@ -44,6 +47,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-per-layer", dest="per_layer", action="store_false",
                     help="skip the one-call-per-layer measurement")
+    ap.add_argument("--no-key-step", dest="key_step", action="store_false",
+                    help="skip the key-step measurement (grkv_compress_kv)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a 1 GiB device copy (for counter calibration)")
@@ -110,6 +115,68 @@ def cpu_baseline(cfg, q, K, V, seconds):
     return {"value": done / el, "unit": "heads/s", "cores": int(threads), "kind": "oracle",
             "sample": "%d of %d units (whole units, float64 numpy oracle), %.1f s"
                       % (done, cfg.units, el)}
+
+
+def key_step(args, cfg, G, hip, stream, qd, Kd, Vd):
+    """The key step after the value step (grkv_compress_kv) on the same
+    workload: time per call and of its key stage (default CG settings), CG
+    iterations per unit, and the time of one CG iteration (one operator pass
+    plus one CG update), from the difference of two runs with a fixed
+    iteration count.  Algorithmic flops of one operator application per unit:
+    a V*^T and (X o W D) V* (2mcd each) and W D (2m^2 c)."""
+    import numpy as np
+    import torch
+
+    U, w, c, d, m = cfg.units, cfg.window, cfg.budget, cfg.head_dim, cfg.group * cfg.window
+    if G.workspace_bytes_kv(U, cfg.group, d, 0 if cfg.dtype == "bf16" else 1, cfg.n, w, c) == 0:
+        return None
+    print("bench: key step", file=sys.stderr, flush=True)
+    res, kstar, info = G.compress_kv(qd, Kd, Vd, w, c, cfg.pool_kernel, cfg.lam)
+    ks = G.STAGES.index("key")
+
+    def run(reps, **kw):
+        evs = []
+        for _ in range(reps):
+            arr = (ctypes.c_void_p * (2 * G.NUM_STAGES))()
+            a, b = hip.event(), hip.event()
+            arr[2 * ks], arr[2 * ks + 1] = a.value, b.value
+            evs.append((arr, a, b))
+        c0, c1 = hip.event(), hip.event()
+        hip.lib.hipEventRecord(c0, ctypes.c_void_p(stream.cuda_stream))
+        for arr, _, _ in evs:
+            G.compress_kv(qd, Kd, Vd, w, c, cfg.pool_kernel, cfg.lam, workspace=res.workspace,
+                          out=res, k_star=kstar, cg_info=info, stage_events=arr, **kw)
+        hip.lib.hipEventRecord(c1, ctypes.c_void_p(stream.cuda_stream))
+        torch.cuda.synchronize()
+        return (float(np.mean([hip.elapsed_ms(a, b) for _, a, b in evs])),
+                hip.elapsed_ms(c0, c1) / reps)
+
+    for _ in range(args.warmup):
+        run(1)
+    reps = max(1, min(args.steps, 5))
+    key_ms, call_ms = run(reps)
+    it = info[:, 0].cpu().numpy()
+    state = info[:, 2].cpu().numpy()
+    n1, n2 = 4, 20
+    t1, _ = run(reps, max_iter=n1, tol=0.0)
+    t2, _ = run(reps, max_iter=n2, tol=0.0)
+    it_ms = (t2 - t1) / (n2 - n1)
+    flops = U * (4.0 * m * c * d + 2.0 * m * m * c)
+    tflops = flops / (it_ms / 1e3) / 1e12
+    return {
+        "ms_per_call": call_ms,
+        "key_stage_ms": key_ms,
+        "heads_per_s": U / (call_ms / 1e3),
+        "cg_iterations_mean": float(it.mean()),
+        "cg_iterations_max": int(it.max()),
+        "units_converged": int((state == G.KEY_CONVERGED).sum()),
+        "cg_tol": 1e-5,
+        "iteration_ms": it_ms,
+        "roofline": {"bound": "mfma", "kernel": "key_pass + key_cg (one CG iteration)",
+                     "achieved": tflops, "peak": 2500.0, "unit": "TFLOP/s",
+                     "frac": tflops / 2500.0, "traffic": None,
+                     "note": "fp32-accurate products as three bf16 MFMAs each"},
+    }
 
 
 def main():
@@ -243,6 +310,8 @@ def main():
     copy_gbs = 5 * 2 * 2 ** 30 / (hip.elapsed_ms(c0, c1) / 1e3) / 1e9
     del x, y
 
+    key = key_step(args, cfg, G, hip, stream, qd, Kd, Vd) if args.key_step else None
+
     cpu = None
     if not args.no_cpu_baseline:
         print("bench: timing the oracle on the host", file=sys.stderr, flush=True)
@@ -275,6 +344,7 @@ def main():
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "frac_of_copy": achieved / copy_gbs,
                      "traffic": traffic},
+        "key_step": key,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

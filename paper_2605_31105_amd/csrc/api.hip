@@ -125,10 +125,13 @@ int make_plan(const grkv_problem* prob, int64_t n, int32_t window, int32_t budge
   return GRKV_OK;
 }
 
-// Workspace of the key step, after the compress workspace.  The key passes
-// hold one block per compute unit (all m rows, a split of the retained keys).
+// Workspace of the key step, after the compress workspace.  A key-pass block
+// holds all m rows of a unit and a split of its retained keys.
 static void make_key_plan(const Plan& p, KeyPlan* kp) {
-  split_range(p.c, ceil_div(256, p.U), 64, &kp->S4, &kp->chunk4);
+  // splits of at least 128 keys, about 2048 blocks in all: a unit's CG
+  // iteration then spans several compute units, which keeps the iterations
+  // short once only a few units are still converging
+  split_range(p.c, ceil_div(2048, p.U), 128, &kp->S4, &kp->chunk4);
   const size_t U = p.U, mp = p.mp, d = p.d;
   size_t off = p.total;
   auto take = [&](size_t bytes) { size_t o2 = off; off = align256(off + bytes); return o2; };
@@ -136,6 +139,7 @@ static void make_key_plan(const Plan& p, KeyPlan* kp) {
   kp->alpha = take(U * mp * d * sizeof(float));
   kp->r = take(U * mp * d * sizeof(float));
   kp->p = take(U * mp * d * sizeof(float));
+  kp->sdot = take(U * mp * sizeof(float));
   kp->W = take(U * mp * mp * sizeof(float));
   kp->opart = take(U * kp->S4 * mp * d * sizeof(float));
   kp->hpart = take(U * kp->S4 * mp * sizeof(float));
@@ -377,6 +381,7 @@ int grkv_compress_kv(const void* q_obs, const void* K, const void* V, int64_t n,
   a.alpha = F(kp.alpha);
   a.r = F(kp.r);
   a.p = F(kp.p);
+  a.sdot = F(kp.sdot);
   a.W = F(kp.W);
   a.opart = F(kp.opart);
   a.hpart = F(kp.hpart);

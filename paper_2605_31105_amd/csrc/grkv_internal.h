@@ -141,7 +141,7 @@ enum { kKeyRunning = 0, kKeyConverged = 1, kKeyMaxIter = 2, kKeySkipped = 3, kKe
 
 struct KeyPlan {
   int S4, chunk4;   // splits of the retained keys per unit for the key passes
-  size_t Fm, alpha, r, p, W, opart, hpart, cg;   // offsets after Plan::total
+  size_t Fm, alpha, r, p, sdot, W, opart, hpart, cg;   // offsets after Plan::total
   size_t total;
 };
 
@@ -156,6 +156,7 @@ struct KeyArgs {
   const float* zt;          // [U][d][mp] Z^T of the value step
   const float* stats_ws;    // [U][4] value-step stats (status in [3])
   float *Fm, *alpha, *r, *p, *W, *opart, *hpart;
+  float* sdot;              // [U][mp] rowdot(F, p) of the current direction
   double* cg;               // [U][4] {r.r, r0.r0, iterations, state}
   float* kstar;             // [U][c][d] out
   float* cg_info;           // [U][4] out or null

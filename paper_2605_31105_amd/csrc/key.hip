@@ -65,7 +65,7 @@ __global__ __launch_bounds__(256) void key_init_kernel(
     const u16* __restrict__ q, const float* __restrict__ y, const float* __restrict__ zt,
     const float* __restrict__ stats_ws, float lam_v, int m, float* __restrict__ Fm,
     float* __restrict__ alpha, float* __restrict__ r, float* __restrict__ p,
-    float* __restrict__ W, double* __restrict__ cg) {
+    float* __restrict__ sdot, float* __restrict__ W, double* __restrict__ cg) {
   __shared__ double red[4];
   const int u = blockIdx.x, tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, l16 = lane & 15, g = lane >> 4;
@@ -80,6 +80,17 @@ __global__ __launch_bounds__(256) void key_init_kernel(
     r[o] = E;
     p[o] = E;
     ee += (double)E * E;
+  }
+  // s = rowdot(F, p) for the first direction p = E, one thread per row
+  for (int row = tid; row < MP; row += 256) {
+    float acc = 0.f;
+    if (!skip && row < m)
+      for (int col = 0; col < D; ++col) {
+        const size_t o = (size_t)u * MP * D + (size_t)row * D + col;
+        const float E = lam_v * zt[((size_t)u * D + col) * MP + row];
+        acc += (y[o] - E) * E;
+      }
+    sdot[(size_t)u * MP + row] = acc;
   }
   // W = Q Q^T / d (bf16 products are exact; fp32 sums)
   const u16* qu = q + (size_t)u * m * D;
@@ -138,7 +149,8 @@ __global__ __launch_bounds__(MP / 16 * 64) void key_pass_kernel(
     const u16* __restrict__ q, const u16* __restrict__ k0, const float* __restrict__ vs,
     const float* __restrict__ lse2, const uint8_t* __restrict__ fixed,
     const int32_t* __restrict__ idx, const float* __restrict__ Fm, const float* __restrict__ W,
-    const float* __restrict__ pv, const double* __restrict__ cg, float* __restrict__ opart,
+    const float* __restrict__ pv, const float* __restrict__ sdot_in,
+    const double* __restrict__ cg, float* __restrict__ opart,
     float* __restrict__ hpart, float* __restrict__ kstar, float* __restrict__ cg_info, int m,
     int w, int64_t n, int c, int S, int chunk, int causal, float scale_log2, float inv_sqrt_d) {
   constexpr int NW = MP / 16, NTH = NW * 64;
@@ -190,23 +202,30 @@ __global__ __launch_bounds__(MP / 16 * 64) void key_pass_kernel(
     for (int ks = 0; ks < D / 32; ++ks) {
       const float4 a0 = *reinterpret_cast<const float4*>(pr + ks * 32 + 8 * g);
       const float4 a1 = *reinterpret_cast<const float4*>(pr + ks * 32 + 8 * g + 4);
-      const float4 f0 = *reinterpret_cast<const float4*>(fr + ks * 32 + 8 * g);
-      const float4 f1 = *reinterpret_cast<const float4*>(fr + ks * 32 + 8 * g + 4);
       const float x[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
-      sdot += a0.x * f0.x + a0.y * f0.y + a0.z * f0.z + a0.w * f0.w;
-      sdot += a1.x * f1.x + a1.y * f1.y + a1.z * f1.z + a1.w * f1.w;
+      if constexpr (FINAL) {
+        const float4 f0 = *reinterpret_cast<const float4*>(fr + ks * 32 + 8 * g);
+        const float4 f1 = *reinterpret_cast<const float4*>(fr + ks * 32 + 8 * g + 4);
+        sdot += a0.x * f0.x + a0.y * f0.y + a0.z * f0.z + a0.w * f0.w;
+        sdot += a1.x * f1.x + a1.y * f1.y + a1.z * f1.z + a1.w * f1.w;
+      }
       split8(x, pah[ks], pal[ks]);
     }
   }
-  sdot += __shfl_xor(sdot, 16);
-  sdot += __shfl_xor(sdot, 32);
+  if constexpr (FINAL) {
+    sdot += __shfl_xor(sdot, 16);
+    sdot += __shfl_xor(sdot, 32);
+  }
   // an MFMA result gives a lane rows 16w + 4g + i
   float s4[4], nl4[4];
   int rp4[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int r4 = 16 * wave + 4 * g + i;
-    s4[i] = __shfl(sdot, 4 * g + i);
+    if constexpr (FINAL)
+      s4[i] = __shfl(sdot, 4 * g + i);
+    else
+      s4[i] = sdot_in[(size_t)u * MP + r4];
     nl4[i] = r4 < m ? -lse2[(size_t)u * MP + r4] : NEG_INF;
     rp4[i] = r4 < m ? (int)(n - w + r4 % w) : -1;
   }
@@ -431,13 +450,19 @@ __global__ __launch_bounds__(MP / 16 * 64) void key_pass_kernel(
 
 // -------------------------------------------------------------------- cg ----
 // One conjugate-gradient update per unit: Ap = sum_s opart - (sum_s hpart) o F
-// + lambda_k p; alpha += a p; r -= a Ap; p = r + beta p.
+// + lambda_k p; alpha += a p; r -= a Ap; p = r + beta p; and the row dots
+// s = rowdot(F, p) of the new direction for the next operator pass.
+__device__ __forceinline__ float dot4(float4 a, float4 b) {
+  return a.x * b.x + a.y * b.y + a.z * b.z + a.w * b.w;
+}
+
 template <int MP, int D>
 __global__ __launch_bounds__(1024) void key_cg_kernel(
     const float* __restrict__ opart, const float* __restrict__ hpart, int S,
     const float* __restrict__ Fm, float* __restrict__ alpha, float* __restrict__ r,
-    float* __restrict__ p, double* __restrict__ cg, float lam_k, float tol, int max_iter) {
-  constexpr int NTH = 1024, E = MP * D, PER = (E + NTH - 1) / NTH;
+    float* __restrict__ p, float* __restrict__ sdot, double* __restrict__ cg, float lam_k,
+    float tol, int max_iter) {
+  constexpr int NTH = 1024, E4 = MP * D / 4, PER = (E4 + NTH - 1) / NTH, RW = D / 4;
   __shared__ float hsum[MP];
   __shared__ double red[16];
   const int u = blockIdx.x, tid = threadIdx.x;
@@ -448,21 +473,35 @@ __global__ __launch_bounds__(1024) void key_cg_kernel(
     hsum[i] = h;
   }
   __syncthreads();
-  const size_t base = (size_t)u * E;
-  float ap[PER], pp[PER];
+  const size_t base = (size_t)u * E4;
+  const float4* __restrict__ op4 = reinterpret_cast<const float4*>(opart) + (size_t)u * S * E4;
+  const float4* __restrict__ F4 = reinterpret_cast<const float4*>(Fm) + base;
+  float4* __restrict__ a4 = reinterpret_cast<float4*>(alpha) + base;
+  float4* __restrict__ r4 = reinterpret_cast<float4*>(r) + base;
+  float4* __restrict__ p4 = reinterpret_cast<float4*>(p) + base;
+  const float4 z4 = make_float4(0.f, 0.f, 0.f, 0.f);
+  float4 ap[PER], pp[PER], fv[PER];
   double pap = 0;
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
     const int e = tid + k * NTH;
-    ap[k] = pp[k] = 0.f;
-    if (e < E) {
-      float v = 0.f;
-      for (int sp = 0; sp < S; ++sp) v += opart[((size_t)u * S + sp) * E + e];
-      const float pe = p[base + e];
-      v = v - hsum[e / D] * Fm[base + e] + lam_k * pe;
+    ap[k] = pp[k] = fv[k] = z4;
+    if (e < E4) {
+      float4 v = z4;
+      for (int sp = 0; sp < S; ++sp) {
+        const float4 o = op4[(size_t)sp * E4 + e];
+        v.x += o.x; v.y += o.y; v.z += o.z; v.w += o.w;
+      }
+      const float4 pe = p4[e], f = F4[e];
+      const float h = hsum[e / RW];
+      v.x += lam_k * pe.x - h * f.x;
+      v.y += lam_k * pe.y - h * f.y;
+      v.z += lam_k * pe.z - h * f.z;
+      v.w += lam_k * pe.w - h * f.w;
       ap[k] = v;
       pp[k] = pe;
-      pap += (double)pe * v;
+      fv[k] = f;
+      pap += (double)dot4(pe, v);
     }
   }
   pap = block_sum(pap, red);
@@ -473,17 +512,20 @@ __global__ __launch_bounds__(1024) void key_cg_kernel(
     return;
   }
   const float a = (float)(rr / pap);
-  float rv[PER];
+  float4 rv[PER];
   double rn = 0;
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
     const int e = tid + k * NTH;
-    rv[k] = 0.f;
-    if (e < E) {
-      alpha[base + e] += a * pp[k];
-      rv[k] = r[base + e] - a * ap[k];
-      r[base + e] = rv[k];
-      rn += (double)rv[k] * rv[k];
+    rv[k] = z4;
+    if (e < E4) {
+      float4 al = a4[e], re = r4[e];
+      al.x += a * pp[k].x; al.y += a * pp[k].y; al.z += a * pp[k].z; al.w += a * pp[k].w;
+      re.x -= a * ap[k].x; re.y -= a * ap[k].y; re.z -= a * ap[k].z; re.w -= a * ap[k].w;
+      a4[e] = al;
+      r4[e] = re;
+      rv[k] = re;
+      rn += (double)dot4(re, re);
     }
   }
   rn = block_sum(rn, red);
@@ -495,7 +537,17 @@ __global__ __launch_bounds__(1024) void key_cg_kernel(
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
       const int e = tid + k * NTH;
-      if (e < E) p[base + e] = rv[k] + beta * pp[k];
+      float4 pn = z4;
+      if (e < E4) {
+        pn = make_float4(rv[k].x + beta * pp[k].x, rv[k].y + beta * pp[k].y,
+                         rv[k].z + beta * pp[k].z, rv[k].w + beta * pp[k].w);
+        p4[e] = pn;
+      }
+      // row dot over the RW consecutive threads of a row (whole rows only)
+      float sd = dot4(fv[k], pn);
+#pragma unroll
+      for (int off = 1; off < RW; off <<= 1) sd += __shfl_xor(sd, off);
+      if (e < E4 && (e % RW) == 0) sdot[(size_t)u * MP + e / RW] = sd;
     }
   }
   if (tid == 0) {
@@ -511,7 +563,7 @@ hipError_t launch_key_t(const Plan& p, const KeyPlan& kp, const KeyArgs& a, hipS
   const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
   const float inv_sqrt_d = (float)(1.0 / sqrt((double)D));
   hipLaunchKernelGGL((key_init_kernel<MP, D>), dim3(p.U), dim3(256), 0, s, a.q, a.y, a.zt,
-                     a.stats_ws, p.lam, p.m, a.Fm, a.alpha, a.r, a.p, a.W, a.cg);
+                     a.stats_ws, p.lam, p.m, a.Fm, a.alpha, a.r, a.p, a.sdot, a.W, a.cg);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const size_t lds_op = L::bytes(false), lds_fin = L::bytes(true);
@@ -525,16 +577,18 @@ hipError_t launch_key_t(const Plan& p, const KeyPlan& kp, const KeyArgs& a, hipS
   const int causal = p.opt.causal_window ? 1 : 0;
   for (int it = 0; it < a.max_iter; ++it) {
     hipLaunchKernelGGL((key_pass_kernel<MP, D, false>), grid, block, lds_op, s, a.q, a.k0, a.vs,
-                       a.lse2, a.fixed, a.idx, a.Fm, a.W, a.p, a.cg, a.opart, a.hpart, nullptr,
+                       a.lse2, a.fixed, a.idx, a.Fm, a.W, a.p, a.sdot, a.cg, a.opart, a.hpart,
+                       nullptr,
                        nullptr, p.m, p.w, p.n, p.c, kp.S4, kp.chunk4, causal, scale_log2,
                        inv_sqrt_d);
     hipLaunchKernelGGL((key_cg_kernel<MP, D>), dim3(p.U), dim3(1024), 0, s, a.opart, a.hpart,
-                       kp.S4, a.Fm, a.alpha, a.r, a.p, a.cg, a.lam_k, a.tol, a.max_iter);
+                       kp.S4, a.Fm, a.alpha, a.r, a.p, a.sdot, a.cg, a.lam_k, a.tol, a.max_iter);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   hipLaunchKernelGGL((key_pass_kernel<MP, D, true>), grid, block, lds_fin, s, a.q, a.k0, a.vs,
-                     a.lse2, a.fixed, a.idx, a.Fm, nullptr, a.alpha, a.cg, nullptr, nullptr,
+                     a.lse2, a.fixed, a.idx, a.Fm, nullptr, a.alpha, nullptr, a.cg, nullptr,
+                     nullptr,
                      a.kstar, a.cg_info, p.m, p.w, p.n, p.c, kp.S4, kp.chunk4, causal,
                      scale_log2, inv_sqrt_d);
   return hipGetLastError();

@@ -3,7 +3,7 @@
 The oracle solves the dual key system to convergence; the GPU runs conjugate
 gradients in fp32 to a relative residual of 1e-5, so the bar is on the key
 update: max|K*_gpu - K*_oracle| <= 2e-3 max|K*_oracle - K0| per unit, with
-fixed keys bit-exact at K0.  Where the exact update is below 1% of the keys
+fixed keys bit-exact at K0.  Where the exact update is below 0.1% of the keys
 (budget = n, where the value step leaves no residual) the same 2e-3 applies
 relative to max|K*_oracle| instead.  The
 oracle takes the GPU's retained set (whose parity is tested on its own), so
@@ -41,11 +41,11 @@ def _run(cfg, q, K, V, **kw):
                 kstar=kstar.cpu().numpy(), info=info.cpu().numpy())
 
 
-def _check(cfg, q, K, V, gpu, u, lam_k=None, report=None):
+def _check(cfg, q, K, V, gpu, u, lam_k=None, report=None, opt=None):
     qd, Kd, Vd = (W.decode(a[u], cfg.dtype) for a in (q, K, V))
     lam_k = cfg.lam if lam_k is None else lam_k
     r = KO.grkv_unit(qd, Kd, Vd, cfg.window, cfg.budget, cfg.pool_kernel, cfg.lam, lam_k,
-                     idx=gpu["idx"][u])
+                     opt=opt, idx=gpu["idx"][u])
     K0 = W.bf16_bits_to_f32(gpu["k0"][u]).astype(np.float64)
     ks = gpu["kstar"][u].astype(np.float64)
     F = r["fixed"]
@@ -54,10 +54,10 @@ def _check(cfg, q, K, V, gpu, u, lam_k=None, report=None):
     dk = np.abs(r["Kstar"] - K0).max()
     diff = np.abs(ks - r["Kstar"]).max()
     kmax = np.abs(r["Kstar"]).max()
-    # the bar is on the update where the update is a visible part of the keys;
-    # where the exact update is (close to) zero, e.g. budget = n (R = 0), on
-    # the keys themselves (the merged-value gate applied to K*)
-    err = diff / dk if dk >= 1e-2 * kmax else diff / kmax
+    # the bar is on the update; where the exact update is (close to) zero,
+    # e.g. budget = n (R = 0), on the keys themselves (the merged-value gate
+    # applied to K*)
+    err = diff / dk if dk >= 1e-3 * kmax else diff / kmax
     info = dict(unit=u, key_err=float(err), max_dk=float(dk), cg_iters=int(gpu["info"][u, 0]),
                 cg_rel=float(gpu["info"][u, 1]), state=int(gpu["info"][u, 2]),
                 oracle_iters=r["key"]["iterations"])
@@ -124,16 +124,9 @@ def test_key_options(label, kw):
     from oracle import grkv_oracle as O
     opt = O.Options(**opt_kw) if opt_kw else None
     for u in range(2):
-        qd, Kd, Vd = (W.decode(a[u], cfg.dtype) for a in (q, K, V))
-        lam_k = kw.get("lambda_k", cfg.lam)
-        r = KO.grkv_unit(qd, Kd, Vd, cfg.window, cfg.budget, cfg.pool_kernel, cfg.lam, lam_k,
-                         opt=opt, idx=gpu["idx"][u])
-        K0 = W.bf16_bits_to_f32(gpu["k0"][u]).astype(np.float64)
-        dk = np.abs(r["Kstar"] - K0).max()
-        assert dk >= 1e-2 * np.abs(r["Kstar"]).max()
-        err = np.abs(gpu["kstar"][u] - r["Kstar"]).max() / dk
-        print(label, u, err, gpu["info"][u], flush=True)
-        assert err <= K_TOL
+        info = _check(cfg2, q, K, V, gpu, u, lam_k=kw.get("lambda_k"), opt=opt)
+        print(label, info, flush=True)
+        assert info["max_dk"] > 0
 
 
 def test_key_iteration_limits():
