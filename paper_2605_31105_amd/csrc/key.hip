@@ -26,9 +26,11 @@
 // rows split into bf16 hi + lo parts are staged in LDS, V* also transposed.  A
 // wave computes, for its 16 rows, S = Q K^T and B = a V*^T on the MFMA (the
 // result holds each lane's key column), D = X o (B - s), and writes D to LDS
-// transposed; then A^T = D^T W and S^T = K Q^T give H^T = X^T o A^T with each
-// lane holding one row, which is the operand layout of out^T += V*^T H^T.
-// Products of fp32 values use three bf16 MFMAs (hi*hi + hi*lo + lo*hi).
+// transposed for the other waves; then A = W D (W rows in registers, D from
+// LDS) arrives in the same layout as X, so H = X o A needs no second product.
+// H goes through a small per-wave LDS area into the operand layout of
+// out^T += V*^T H^T.  Products of fp32 values use three bf16 MFMAs
+// (hi*hi + hi*lo + lo*hi).
 #include <math.h>
 
 #include "grkv_device.h"
@@ -37,7 +39,7 @@
 namespace grkv {
 namespace {
 
-constexpr int kKT = 32;   // retained keys per tile
+constexpr int kKT = 32;   // retained keys per tile (the key orders below assume 32)
 
 // Position, inside a block of 32, of the index a lane holds as element j of an
 // MFMA operand when the operand comes from an MFMA result: elements
@@ -46,6 +48,20 @@ constexpr int kKT = 32;   // retained keys per tile
 __device__ __forceinline__ int kperm(int x) {
   const int b = x & ~31, o = x & 31;
   return b + ((o & 15) >> 2) * 8 + (o >> 4) * 4 + (o & 3);
+}
+
+// Order of the 32 keys of a tile in the transposed V* rows and in a wave's H
+// rows: key k sits at 2 (k mod 16) + k / 16, so a lane's two keys {k, k + 16}
+// are adjacent, and the eight positions 8g .. 8g + 7 a lane reads as an MFMA
+// operand hold keys {4g + j/2 (+16 for odd j)} in both.
+__device__ __forceinline__ int tpos(int key) { return 2 * (key & 15) + (key >> 4); }
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b, uint32_t* lo) {
+  const bf16x2 h = __builtin_convertvector((f32x2){a, b}, bf16x2);
+  const uint32_t hw = __builtin_bit_cast(uint32_t, h);
+  const float a0 = __uint_as_float(hw << 16), b0 = __uint_as_float(hw & 0xffff0000u);
+  *lo = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){a - a0, b - b0}, bf16x2));
+  return hw;
 }
 
 __device__ __forceinline__ double block_sum(double v, double* red) {
@@ -133,7 +149,10 @@ struct KeyLds {
   static constexpr int tl = th + D * TS;
   static constexpr int dh = tl + D * TS;
   static constexpr int dl = dh + kKT * DS;
-  static constexpr int qt = dl + kKT * DS;
+  static constexpr int HS = kKT + 8;    // row stride of a wave's H rows
+  static constexpr int hh = dl + kKT * DS;  // [NW][16][HS] H hi, then lo
+  static constexpr int hl = hh + MP * HS;
+  static constexpr int qt = hl + MP * HS;
   static constexpr int end = qt;             // the operator pass
   static constexpr int end_final = qt + D * QS;
   static constexpr size_t bytes(bool final_pass) {
@@ -156,9 +175,11 @@ __global__ __launch_bounds__(MP / 16 * 64) void key_pass_kernel(
   constexpr int NW = MP / 16, NTH = NW * 64;
   constexpr int KCH = kKT * D / 8;            // 16-byte chunks of a K tile
   constexpr int KPT = (KCH + NTH - 1) / NTH;
-  constexpr int VPR = kKT / 4 * D;            // (4-key group, column) pairs of a V tile
-  constexpr int VPT = VPR / NTH;
-  static_assert(VPR % NTH == 0, "V tile pairs must divide over the block");
+  // V staging unit: keys {k, k + 16} x four columns, so that both the row-major
+  // copy (8-byte pieces) and the transposed copy (4-byte pieces) are written
+  // without 2-byte stores
+  constexpr int VUN = 16 * (D / 4);
+  constexpr int VPT = (VUN + NTH - 1) / NTH;
   constexpr float NEG_INF = -__builtin_huge_valf();
   using L = KeyLds<MP, D>;
   extern __shared__ __attribute__((aligned(16))) u16 sm[];
@@ -229,8 +250,6 @@ __global__ __launch_bounds__(MP / 16 * 64) void key_pass_kernel(
     nl4[i] = r4 < m ? -lse2[(size_t)u * MP + r4] : NEG_INF;
     rp4[i] = r4 < m ? (int)(n - w + r4 % w) : -1;
   }
-  const float nl_row = row < m ? -lse2[(size_t)u * MP + row] : NEG_INF;
-  const int rp_row = row < m ? (int)(n - w + row % w) : -1;
 
   bf16x8 wah[MP / 32], wal[MP / 32];
   if constexpr (!FINAL) {
@@ -245,9 +264,17 @@ __global__ __launch_bounds__(MP / 16 * 64) void key_pass_kernel(
     }
   } else {
     // Q^T in LDS, rows permuted by kperm: QT[dd][kperm(r)] = Q[r][dd]
-    for (int e = tid; e < MP * D; e += NTH) {
-      const int r = e / D, dd = e % D;
-      sm[L::qt + dd * L::QS + kperm(r)] = r < m ? qu[(size_t)r * D + dd] : (u16)0;
+    for (int e = tid; e < MP * (D / 8); e += NTH) {
+      const int r = e % MP, ch = e / MP;   // neighbouring lanes: neighbouring rows
+      const uint4 v = r < m ? *reinterpret_cast<const uint4*>(qu + (size_t)r * D + ch * 8)
+                            : make_uint4(0, 0, 0, 0);
+      const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+      u16* dst = sm + L::qt + (ch * 8) * L::QS + kperm(r);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        dst[(2 * k) * L::QS] = (u16)(wv[k] & 0xffffu);
+        dst[(2 * k + 1) * L::QS] = (u16)(wv[k] >> 16);
+      }
     }
   }
 
@@ -255,31 +282,34 @@ __global__ __launch_bounds__(MP / 16 * 64) void key_pass_kernel(
   const u16* ku = k0 + (size_t)u * c * D;
   const float* vu = vs + (size_t)u * c * D;
   uint4 kreg[KPT];
-  float vreg[VPT][4];
+  float4 vreg[VPT][2];
   int kpreg = 0, fxreg = 1;
+  // loads clamp the key into the split and zero what lies beyond it
   auto load_tile = [&](int t0) {
 #pragma unroll
     for (int k = 0; k < KPT; ++k) {
-      const int e = tid + k * NTH;
+      const int e = min(tid + k * NTH, KCH - 1);
       const int key = e / (D / 8), ch = e % (D / 8);
-      kreg[k] = (e < KCH && t0 + key < j1)
-                    ? *reinterpret_cast<const uint4*>(ku + (size_t)(t0 + key) * D + ch * 8)
-                    : make_uint4(0, 0, 0, 0);
+      const uint4 v = *reinterpret_cast<const uint4*>(ku + (size_t)min(t0 + key, j1 - 1) * D + ch * 8);
+      kreg[k] = t0 + key < j1 ? v : make_uint4(0, 0, 0, 0);
     }
 #pragma unroll
     for (int k = 0; k < VPT; ++k) {
-      const int e = tid + k * NTH;
-      const int kq = e / D, dd = e % D;
+      const int e = min(tid + k * NTH, VUN - 1);
+      const int kp = e % 16, dq = e / 16;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int key = t0 + 4 * kq + i;
-        vreg[k][i] = key < j1 ? vu[(size_t)key * D + dd] : 0.f;
+      for (int h = 0; h < 2; ++h) {
+        const int key = t0 + kp + 16 * h;
+        const float4 v = *reinterpret_cast<const float4*>(vu + (size_t)min(key, j1 - 1) * D + 4 * dq);
+        vreg[k][h] = key < j1 ? v : make_float4(0.f, 0.f, 0.f, 0.f);
       }
     }
     if (tid < kKT) {
-      const int key = t0 + tid;
-      kpreg = key < j1 ? idx[(size_t)u * c + key] : 0x7fffffff;
-      fxreg = key < j1 ? fixed[(size_t)u * c + key] : 1;
+      const int key = t0 + tid, kc = min(key, j1 - 1);
+      const int pv_ = idx[(size_t)u * c + kc];
+      const int fv_ = fixed[(size_t)u * c + kc];
+      kpreg = key < j1 ? pv_ : 0x7fffffff;
+      fxreg = key < j1 ? fv_ : 1;
     }
   };
   auto store_tile = [&]() {
@@ -294,21 +324,28 @@ __global__ __launch_bounds__(MP / 16 * 64) void key_pass_kernel(
 #pragma unroll
     for (int k = 0; k < VPT; ++k) {
       const int e = tid + k * NTH;
-      const int kq = e / D, dd = e % D;
-      u16 h[4], l[4];
+      if (e < VUN) {
+        const int kp = e % 16, dq = e / 16;
+        uint32_t hi[2][2], lo[2][2];   // [key kp + 16h][column pair]
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const __bf16 hb = (__bf16)vreg[k][i];
-        h[i] = __builtin_bit_cast(u16, hb);
-        l[i] = __builtin_bit_cast(u16, (__bf16)(vreg[k][i] - (float)hb));
-        sm[L::vh + (4 * kq + i) * L::KS + dd] = h[i];
-        sm[L::vl + (4 * kq + i) * L::KS + dd] = l[i];
+        for (int h = 0; h < 2; ++h) {
+          hi[h][0] = pack_bf16x2(vreg[k][h].x, vreg[k][h].y, &lo[h][0]);
+          hi[h][1] = pack_bf16x2(vreg[k][h].z, vreg[k][h].w, &lo[h][1]);
+          const int ro = (kp + 16 * h) * L::KS + 4 * dq;
+          *reinterpret_cast<uint2*>(sm + L::vh + ro) = make_uint2(hi[h][0], hi[h][1]);
+          *reinterpret_cast<uint2*>(sm + L::vl + ro) = make_uint2(lo[h][0], lo[h][1]);
+        }
+        // transposed: column 4dq + c holds (key kp, key kp + 16) at 2kp
+#pragma unroll
+        for (int cc = 0; cc < 4; ++cc) {
+          const int sh = (cc & 1) * 16;
+          const uint32_t th_ = ((hi[0][cc >> 1] >> sh) & 0xffffu) | (((hi[1][cc >> 1] >> sh) & 0xffffu) << 16);
+          const uint32_t tl_ = ((lo[0][cc >> 1] >> sh) & 0xffffu) | (((lo[1][cc >> 1] >> sh) & 0xffffu) << 16);
+          const int to = (4 * dq + cc) * L::TS + 2 * kp;
+          *reinterpret_cast<uint32_t*>(sm + L::th + to) = th_;
+          *reinterpret_cast<uint32_t*>(sm + L::tl + to) = tl_;
+        }
       }
-      const int tp = dd * L::TS + kperm(4 * kq);
-      *reinterpret_cast<uint2*>(sm + L::th + tp) =
-          make_uint2(h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16));
-      *reinterpret_cast<uint2*>(sm + L::tl + tp) =
-          make_uint2(l[0] | ((uint32_t)l[1] << 16), l[2] | ((uint32_t)l[3] << 16));
     }
     if (tid < kKT) {
       kp_s[tid] = kpreg;
@@ -319,7 +356,7 @@ __global__ __launch_bounds__(MP / 16 * 64) void key_pass_kernel(
   f32x4 oacc[D / 16];
 #pragma unroll
   for (int dt = 0; dt < D / 16; ++dt) oacc[dt] = zero4();
-  float hs = 0.f;
+  float hs4[4] = {0.f, 0.f, 0.f, 0.f};   // row sums of H, rows 16w + 4g + i
 
   if (j0 < j1) load_tile(j0);
   for (int t0 = j0; t0 < j1; t0 += kKT) {
@@ -329,6 +366,7 @@ __global__ __launch_bounds__(MP / 16 * 64) void key_pass_kernel(
     if (t0 + kKT < j1) load_tile(t0 + kKT);
 
     // S = Q K^T, B = dir V^T, D = X o (B - s) for this wave's rows -> D^T in LDS
+    float xk[kKT / 16][4];   // X[16w + 4g + i][key 16kt + l16]
 #pragma unroll
     for (int kt = 0; kt < kKT / 16; ++kt) {
       const int key = 16 * kt + l16;
@@ -347,21 +385,20 @@ __global__ __launch_bounds__(MP / 16 * 64) void key_pass_kernel(
       const int kpos = kp_s[key];
       const bool live = t0 + key < j1;
       const bool free_key = live && fx_s[key] == 0;
-      u16 dh[4], dl[4];
+      float dv[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const bool vis = live && (!causal || kpos <= rp4[i]);
         const float x = vis ? __builtin_amdgcn_exp2f(fmaf(sacc[i], scale_log2, nl4[i])) : 0.f;
-        const float dv = free_key ? x * (bacc[i] - s4[i]) : 0.f;
-        const __bf16 hb = (__bf16)dv;
-        dh[i] = __builtin_bit_cast(u16, hb);
-        dl[i] = __builtin_bit_cast(u16, (__bf16)(dv - (float)hb));
+        xk[kt][i] = x;
+        dv[i] = free_key ? x * (bacc[i] - s4[i]) : 0.f;
       }
+      uint32_t dl0, dl1;
+      const uint32_t dh0 = pack_bf16x2(dv[0], dv[1], &dl0);
+      const uint32_t dh1 = pack_bf16x2(dv[2], dv[3], &dl1);
       const int dp = key * L::DS + 32 * (wave >> 1) + 8 * g + 4 * (wave & 1);
-      *reinterpret_cast<uint2*>(sm + L::dh + dp) =
-          make_uint2(dh[0] | ((uint32_t)dh[1] << 16), dh[2] | ((uint32_t)dh[3] << 16));
-      *reinterpret_cast<uint2*>(sm + L::dl + dp) =
-          make_uint2(dl[0] | ((uint32_t)dl[1] << 16), dl[2] | ((uint32_t)dl[3] << 16));
+      *reinterpret_cast<uint2*>(sm + L::dh + dp) = make_uint2(dh0, dh1);
+      *reinterpret_cast<uint2*>(sm + L::dl + dp) = make_uint2(dl0, dl1);
     }
     __syncthreads();   // D^T of all rows is in LDS
 
@@ -390,39 +427,41 @@ __global__ __launch_bounds__(MP / 16 * 64) void key_pass_kernel(
         }
       }
     } else {
-      // A^T = D^T W and S^T = K Q^T: lane holds [key 16kt + 4g + i][row]
-      float h8[8];
+      // A = W D for this wave's rows, H = X o A: lane holds [row 16w + 4g + i][key]
+      const int hb = wave * 16 * L::HS;
+      float hv[kKT / 16][4];
 #pragma unroll
       for (int kt = 0; kt < kKT / 16; ++kt) {
-        f32x4 aacc = zero4(), stacc = zero4();
+        f32x4 aacc = zero4();
 #pragma unroll
         for (int kb = 0; kb < MP / 32; ++kb) {
           const int ao = (16 * kt + l16) * L::DS + 32 * kb + 8 * g;
           const bf16x8 dh = as_bf16x8(*reinterpret_cast<const uint4*>(sm + L::dh + ao));
           const bf16x8 dl = as_bf16x8(*reinterpret_cast<const uint4*>(sm + L::dl + ao));
-          aacc = mfma_bf16(dh, wah[kb], aacc);
-          aacc = mfma_bf16(dh, wal[kb], aacc);
-          aacc = mfma_bf16(dl, wah[kb], aacc);
-        }
-#pragma unroll
-        for (int ks = 0; ks < D / 32; ++ks) {
-          const bf16x8 kk = as_bf16x8(*reinterpret_cast<const uint4*>(
-              sm + L::k + (16 * kt + l16) * L::KS + ks * 32 + 8 * g));
-          stacc = mfma_bf16(kk, as_bf16x8(qa[ks]), stacc);
+          aacc = mfma_bf16(wah[kb], dh, aacc);
+          aacc = mfma_bf16(wal[kb], dh, aacc);
+          aacc = mfma_bf16(wah[kb], dl, aacc);
         }
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int key = 16 * kt + 4 * g + i;
-          const bool vis = t0 + key < j1 && (!causal || kp_s[key] <= rp_row);
-          const float x = vis ? __builtin_amdgcn_exp2f(fmaf(stacc[i], scale_log2, nl_row)) : 0.f;
-          const float h = x * aacc[i];
-          h8[4 * kt + i] = h;
-          hs += h;
+          hv[kt][i] = xk[kt][i] * aacc[i];
+          hs4[i] += hv[kt][i];
         }
       }
-      // out^T [d x rows] += V*^T H^T over the tile's 32 keys
-      bf16x8 hh, hl;
-      split8(h8, hh, hl);
+      // the lane's keys l16 and 16 + l16 are adjacent in the H rows
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        uint32_t lo;
+        const uint32_t hi = pack_bf16x2(hv[0][i], hv[1][i], &lo);
+        const int o = hb + (4 * g + i) * L::HS + 2 * l16;
+        *reinterpret_cast<uint32_t*>(sm + L::hh + o) = hi;
+        *reinterpret_cast<uint32_t*>(sm + L::hl + o) = lo;
+      }
+      // out^T [d x rows] += V*^T H^T over the tile's 32 keys (the H rows were
+      // written by this wave alone, and its LDS accesses complete in order)
+      const int ho = hb + l16 * L::HS + 8 * g;
+      const bf16x8 hh = as_bf16x8(*reinterpret_cast<const uint4*>(sm + L::hh + ho));
+      const bf16x8 hl = as_bf16x8(*reinterpret_cast<const uint4*>(sm + L::hl + ho));
 #pragma unroll
       for (int dt = 0; dt < D / 16; ++dt) {
         const int vo = (16 * dt + l16) * L::TS + 8 * g;
@@ -442,9 +481,11 @@ __global__ __launch_bounds__(MP / 16 * 64) void key_pass_kernel(
     for (int dt = 0; dt < D / 16; ++dt)
       *reinterpret_cast<float4*>(op + 16 * dt + 4 * g) =
           make_float4(oacc[dt][0], oacc[dt][1], oacc[dt][2], oacc[dt][3]);
-    hs += __shfl_xor(hs, 16);
-    hs += __shfl_xor(hs, 32);
-    if (g == 0) hpart[((size_t)u * S + s) * MP + row] = hs;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float h = sum16(hs4[i]);
+      if (l16 == 0) hpart[((size_t)u * S + s) * MP + 16 * wave + 4 * g + i] = h;
+    }
   }
 }
 
