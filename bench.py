@@ -117,7 +117,28 @@ def cpu_baseline(cfg, q, K, V, seconds):
                       % (done, cfg.units, el)}
 
 
-def key_step(args, cfg, G, hip, stream, qd, Kd, Vd):
+def cpu_baseline_key(cfg, q, K, V, seconds):
+    """The oracle's value step followed by its key step (float64 CG to 1e-12),
+    on a bounded sample of whole units."""
+    import workloads as W
+    from oracle import grkv_key_oracle as KO
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = 1
+    done, t0 = 0, time.perf_counter()
+    while done < cfg.units and (done < 2 or time.perf_counter() - t0 < seconds):
+        qd, Kd_, Vd_ = (W.decode(a[done], cfg.dtype) for a in (q, K, V))
+        KO.grkv_unit(qd, Kd_, Vd_, cfg.window, cfg.budget, cfg.pool_kernel, cfg.lam, cfg.lam)
+        done += 1
+    el = time.perf_counter() - t0
+    return {"value": done / el, "unit": "heads/s", "cores": int(threads), "kind": "oracle",
+            "sample": "%d of %d units (whole units: value and key step, float64 numpy oracle), %.1f s"
+                      % (done, cfg.units, el)}
+
+
+def key_step(args, cfg, G, hip, stream, qd, Kd, Vd, host=None):
     """The key step after the value step (grkv_compress_kv) on the same
     workload: time per call and of its key stage (default CG settings), CG
     iterations per unit, and the time of one CG iteration (one operator pass
@@ -163,6 +184,10 @@ def key_step(args, cfg, G, hip, stream, qd, Kd, Vd):
     it_ms = (t2 - t1) / (n2 - n1)
     flops = U * (4.0 * m * c * d + 2.0 * m * m * c)
     tflops = flops / (it_ms / 1e3) / 1e12
+    cpu = None
+    if host is not None:
+        print("bench: timing the key-step oracle on the host", file=sys.stderr, flush=True)
+        cpu = cpu_baseline_key(cfg, *host, min(args.cpu_seconds, 10.0))
     return {
         "ms_per_call": call_ms,
         "key_stage_ms": key_ms,
@@ -176,6 +201,7 @@ def key_step(args, cfg, G, hip, stream, qd, Kd, Vd):
                      "achieved": tflops, "peak": 2500.0, "unit": "TFLOP/s",
                      "frac": tflops / 2500.0, "traffic": None,
                      "note": "fp32-accurate products as three bf16 MFMAs each"},
+        "cpu_baseline": cpu,
     }
 
 
@@ -310,7 +336,9 @@ def main():
     copy_gbs = 5 * 2 * 2 ** 30 / (hip.elapsed_ms(c0, c1) / 1e3) / 1e9
     del x, y
 
-    key = key_step(args, cfg, G, hip, stream, qd, Kd, Vd) if args.key_step else None
+    key = (key_step(args, cfg, G, hip, stream, qd, Kd, Vd,
+                    host=None if args.no_cpu_baseline else (q, K, V))
+           if args.key_step else None)
 
     cpu = None
     if not args.no_cpu_baseline:
