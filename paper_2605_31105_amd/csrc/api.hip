@@ -128,10 +128,12 @@ int make_plan(const grkv_problem* prob, int64_t n, int32_t window, int32_t budge
 // Workspace of the key step, after the compress workspace.  A key-pass block
 // holds all m rows of a unit and a split of its retained keys.
 static void make_key_plan(const Plan& p, KeyPlan* kp) {
-  // splits of at least 128 keys, about 2048 blocks in all: a unit's CG
-  // iteration then spans several compute units, which keeps the iterations
-  // short once only a few units are still converging
-  split_range(p.c, ceil_div(2048, p.U), 128, &kp->S4, &kp->chunk4);
+  // about 256 blocks (one per compute unit) while every unit is iterating;
+  // about 2048 later, when a unit's iteration spanning several compute units
+  // keeps it short once only a few units are still converging
+  split_range(p.c, ceil_div(256, p.U), 64, &kp->S_full, &kp->chunk_full);
+  split_range(p.c, ceil_div(2048, p.U), 64, &kp->S4, &kp->chunk4);
+  const int Smax = kp->S4 > kp->S_full ? kp->S4 : kp->S_full;
   const size_t U = p.U, mp = p.mp, d = p.d;
   size_t off = p.total;
   auto take = [&](size_t bytes) { size_t o2 = off; off = align256(off + bytes); return o2; };
@@ -141,8 +143,8 @@ static void make_key_plan(const Plan& p, KeyPlan* kp) {
   kp->p = take(U * mp * d * sizeof(float));
   kp->sdot = take(U * mp * sizeof(float));
   kp->W = take(U * mp * mp * sizeof(float));
-  kp->opart = take(U * kp->S4 * mp * d * sizeof(float));
-  kp->hpart = take(U * kp->S4 * mp * sizeof(float));
+  kp->opart = take(U * Smax * mp * d * sizeof(float));
+  kp->hpart = take(U * Smax * mp * sizeof(float));
   kp->cg = take(U * 4 * sizeof(double));
   kp->total = off;
 }

@@ -140,7 +140,8 @@ hipError_t launch_update_add(const Plan& p, const float* x, const uint8_t* fixed
 enum { kKeyRunning = 0, kKeyConverged = 1, kKeyMaxIter = 2, kKeySkipped = 3, kKeyBreakdown = 4 };
 
 struct KeyPlan {
-  int S4, chunk4;   // splits of the retained keys per unit for the key passes
+  int S4, chunk4;           // splits of the retained keys per unit, later CG iterations
+  int S_full, chunk_full;   // the same for the first iterations and the final pass
   size_t Fm, alpha, r, p, sdot, W, opart, hpart, cg;   // offsets after Plan::total
   size_t total;
 };

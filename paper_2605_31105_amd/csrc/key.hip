@@ -40,6 +40,7 @@ namespace grkv {
 namespace {
 
 constexpr int kKT = 32;   // retained keys per tile (the key orders below assume 32)
+constexpr int kKeyEarlyIters = 10;  // CG iterations run with the fewest splits
 
 // Position, inside a block of 32, of the index a lane holds as element j of an
 // MFMA operand when the operand comes from an MFMA result: elements
@@ -206,78 +207,6 @@ __global__ __launch_bounds__(MP / 16 * 64) void key_pass_kernel(
     return;
   }
 
-  // per-wave constants: Q rows, the direction's rows (bf16 hi/lo), s = rowdot(F, dir)
-  const int row = 16 * wave + l16;
-  const u16* qu = q + (size_t)u * m * D;
-  uint4 qa[D / 32];
-#pragma unroll
-  for (int ks = 0; ks < D / 32; ++ks)
-    qa[ks] = row < m ? *reinterpret_cast<const uint4*>(qu + (size_t)row * D + ks * 32 + 8 * g)
-                     : make_uint4(0, 0, 0, 0);
-  bf16x8 pah[D / 32], pal[D / 32];
-  float sdot = 0.f;
-  {
-    const float* pr = pv + ((size_t)u * MP + row) * D;
-    const float* fr = Fm + ((size_t)u * MP + row) * D;
-#pragma unroll
-    for (int ks = 0; ks < D / 32; ++ks) {
-      const float4 a0 = *reinterpret_cast<const float4*>(pr + ks * 32 + 8 * g);
-      const float4 a1 = *reinterpret_cast<const float4*>(pr + ks * 32 + 8 * g + 4);
-      const float x[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
-      if constexpr (FINAL) {
-        const float4 f0 = *reinterpret_cast<const float4*>(fr + ks * 32 + 8 * g);
-        const float4 f1 = *reinterpret_cast<const float4*>(fr + ks * 32 + 8 * g + 4);
-        sdot += a0.x * f0.x + a0.y * f0.y + a0.z * f0.z + a0.w * f0.w;
-        sdot += a1.x * f1.x + a1.y * f1.y + a1.z * f1.z + a1.w * f1.w;
-      }
-      split8(x, pah[ks], pal[ks]);
-    }
-  }
-  if constexpr (FINAL) {
-    sdot += __shfl_xor(sdot, 16);
-    sdot += __shfl_xor(sdot, 32);
-  }
-  // an MFMA result gives a lane rows 16w + 4g + i
-  float s4[4], nl4[4];
-  int rp4[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int r4 = 16 * wave + 4 * g + i;
-    if constexpr (FINAL)
-      s4[i] = __shfl(sdot, 4 * g + i);
-    else
-      s4[i] = sdot_in[(size_t)u * MP + r4];
-    nl4[i] = r4 < m ? -lse2[(size_t)u * MP + r4] : NEG_INF;
-    rp4[i] = r4 < m ? (int)(n - w + r4 % w) : -1;
-  }
-
-  bf16x8 wah[MP / 32], wal[MP / 32];
-  if constexpr (!FINAL) {
-    // W row of this lane at the columns 32kb + {4g + i, 16 + 4g + i}
-    const float* wr = W + ((size_t)u * MP + row) * MP;
-#pragma unroll
-    for (int kb = 0; kb < MP / 32; ++kb) {
-      const float4 a = *reinterpret_cast<const float4*>(wr + 32 * kb + 4 * g);
-      const float4 b = *reinterpret_cast<const float4*>(wr + 32 * kb + 16 + 4 * g);
-      const float x[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-      split8(x, wah[kb], wal[kb]);
-    }
-  } else {
-    // Q^T in LDS, rows permuted by kperm: QT[dd][kperm(r)] = Q[r][dd]
-    for (int e = tid; e < MP * (D / 8); e += NTH) {
-      const int r = e % MP, ch = e / MP;   // neighbouring lanes: neighbouring rows
-      const uint4 v = r < m ? *reinterpret_cast<const uint4*>(qu + (size_t)r * D + ch * 8)
-                            : make_uint4(0, 0, 0, 0);
-      const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
-      u16* dst = sm + L::qt + (ch * 8) * L::QS + kperm(r);
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        dst[(2 * k) * L::QS] = (u16)(wv[k] & 0xffffu);
-        dst[(2 * k + 1) * L::QS] = (u16)(wv[k] >> 16);
-      }
-    }
-  }
-
   // register-staged tile loads
   const u16* ku = k0 + (size_t)u * c * D;
   const float* vu = vs + (size_t)u * c * D;
@@ -352,13 +281,86 @@ __global__ __launch_bounds__(MP / 16 * 64) void key_pass_kernel(
       fx_s[tid] = (uint8_t)fxreg;
     }
   };
+  // the first tile's loads go out before the per-block constants
+  if (j0 < j1) load_tile(j0);
+
+  // per-wave constants: Q rows, the direction's rows (bf16 hi/lo), s = rowdot(F, dir)
+  const int row = 16 * wave + l16;
+  const u16* qu = q + (size_t)u * m * D;
+  uint4 qa[D / 32];
+#pragma unroll
+  for (int ks = 0; ks < D / 32; ++ks)
+    qa[ks] = row < m ? *reinterpret_cast<const uint4*>(qu + (size_t)row * D + ks * 32 + 8 * g)
+                     : make_uint4(0, 0, 0, 0);
+  bf16x8 pah[D / 32], pal[D / 32];
+  float sdot = 0.f;
+  {
+    const float* pr = pv + ((size_t)u * MP + row) * D;
+    const float* fr = Fm + ((size_t)u * MP + row) * D;
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) {
+      const float4 a0 = *reinterpret_cast<const float4*>(pr + ks * 32 + 8 * g);
+      const float4 a1 = *reinterpret_cast<const float4*>(pr + ks * 32 + 8 * g + 4);
+      const float x[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+      if constexpr (FINAL) {
+        const float4 f0 = *reinterpret_cast<const float4*>(fr + ks * 32 + 8 * g);
+        const float4 f1 = *reinterpret_cast<const float4*>(fr + ks * 32 + 8 * g + 4);
+        sdot += a0.x * f0.x + a0.y * f0.y + a0.z * f0.z + a0.w * f0.w;
+        sdot += a1.x * f1.x + a1.y * f1.y + a1.z * f1.z + a1.w * f1.w;
+      }
+      split8(x, pah[ks], pal[ks]);
+    }
+  }
+  if constexpr (FINAL) {
+    sdot += __shfl_xor(sdot, 16);
+    sdot += __shfl_xor(sdot, 32);
+  }
+  // an MFMA result gives a lane rows 16w + 4g + i
+  float s4[4], nl4[4];
+  int rp4[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r4 = 16 * wave + 4 * g + i;
+    if constexpr (FINAL)
+      s4[i] = __shfl(sdot, 4 * g + i);
+    else
+      s4[i] = sdot_in[(size_t)u * MP + r4];
+    nl4[i] = r4 < m ? -lse2[(size_t)u * MP + r4] : NEG_INF;
+    rp4[i] = r4 < m ? (int)(n - w + r4 % w) : -1;
+  }
+
+  bf16x8 wah[MP / 32], wal[MP / 32];
+  if constexpr (!FINAL) {
+    // W row of this lane at the columns 32kb + {4g + i, 16 + 4g + i}
+    const float* wr = W + ((size_t)u * MP + row) * MP;
+#pragma unroll
+    for (int kb = 0; kb < MP / 32; ++kb) {
+      const float4 a = *reinterpret_cast<const float4*>(wr + 32 * kb + 4 * g);
+      const float4 b = *reinterpret_cast<const float4*>(wr + 32 * kb + 16 + 4 * g);
+      const float x[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+      split8(x, wah[kb], wal[kb]);
+    }
+  } else {
+    // Q^T in LDS, rows permuted by kperm: QT[dd][kperm(r)] = Q[r][dd]
+    for (int e = tid; e < MP * (D / 8); e += NTH) {
+      const int r = e % MP, ch = e / MP;   // neighbouring lanes: neighbouring rows
+      const uint4 v = r < m ? *reinterpret_cast<const uint4*>(qu + (size_t)r * D + ch * 8)
+                            : make_uint4(0, 0, 0, 0);
+      const uint32_t wv[4] = {v.x, v.y, v.z, v.w};
+      u16* dst = sm + L::qt + (ch * 8) * L::QS + kperm(r);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        dst[(2 * k) * L::QS] = (u16)(wv[k] & 0xffffu);
+        dst[(2 * k + 1) * L::QS] = (u16)(wv[k] >> 16);
+      }
+    }
+  }
 
   f32x4 oacc[D / 16];
 #pragma unroll
   for (int dt = 0; dt < D / 16; ++dt) oacc[dt] = zero4();
   float hs4[4] = {0.f, 0.f, 0.f, 0.f};   // row sums of H, rows 16w + 4g + i
 
-  if (j0 < j1) load_tile(j0);
   for (int t0 = j0; t0 < j1; t0 += kKT) {
     __syncthreads();   // the previous tile is no longer read
     store_tile();
@@ -614,24 +616,27 @@ hipError_t launch_key_t(const Plan& p, const KeyPlan& kp, const KeyArgs& a, hipS
   e = hipFuncSetAttribute((const void*)key_pass_kernel<MP, D, true>,
                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_fin);
   if (e != hipSuccess) return e;
-  const dim3 grid(kp.S4, p.U), block(MP / 16 * 64);
+  const dim3 block(MP / 16 * 64);
   const int causal = p.opt.causal_window ? 1 : 0;
   for (int it = 0; it < a.max_iter; ++it) {
-    hipLaunchKernelGGL((key_pass_kernel<MP, D, false>), grid, block, lds_op, s, a.q, a.k0, a.vs,
-                       a.lse2, a.fixed, a.idx, a.Fm, a.W, a.p, a.sdot, a.cg, a.opart, a.hpart,
-                       nullptr,
-                       nullptr, p.m, p.w, p.n, p.c, kp.S4, kp.chunk4, causal, scale_log2,
-                       inv_sqrt_d);
+    // the first iterations, while every unit is still running, with the
+    // fewest blocks a full GPU needs; later ones with more splits per unit,
+    // which shortens an iteration once few units remain
+    const bool early = it < kKeyEarlyIters;
+    const int S = early ? kp.S_full : kp.S4, chunk = early ? kp.chunk_full : kp.chunk4;
+    hipLaunchKernelGGL((key_pass_kernel<MP, D, false>), dim3(S, p.U), block, lds_op, s, a.q,
+                       a.k0, a.vs, a.lse2, a.fixed, a.idx, a.Fm, a.W, a.p, a.sdot, a.cg,
+                       a.opart, a.hpart, nullptr, nullptr, p.m, p.w, p.n, p.c, S, chunk, causal,
+                       scale_log2, inv_sqrt_d);
     hipLaunchKernelGGL((key_cg_kernel<MP, D>), dim3(p.U), dim3(1024), 0, s, a.opart, a.hpart,
-                       kp.S4, a.Fm, a.alpha, a.r, a.p, a.sdot, a.cg, a.lam_k, a.tol, a.max_iter);
+                       S, a.Fm, a.alpha, a.r, a.p, a.sdot, a.cg, a.lam_k, a.tol, a.max_iter);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL((key_pass_kernel<MP, D, true>), grid, block, lds_fin, s, a.q, a.k0, a.vs,
-                     a.lse2, a.fixed, a.idx, a.Fm, nullptr, a.alpha, nullptr, a.cg, nullptr,
-                     nullptr,
-                     a.kstar, a.cg_info, p.m, p.w, p.n, p.c, kp.S4, kp.chunk4, causal,
-                     scale_log2, inv_sqrt_d);
+  hipLaunchKernelGGL((key_pass_kernel<MP, D, true>), dim3(kp.S_full, p.U), block, lds_fin, s,
+                     a.q, a.k0, a.vs, a.lse2, a.fixed, a.idx, a.Fm, nullptr, a.alpha, nullptr,
+                     a.cg, nullptr, nullptr, a.kstar, a.cg_info, p.m, p.w, p.n, p.c, kp.S_full,
+                     kp.chunk_full, causal, scale_log2, inv_sqrt_d);
   return hipGetLastError();
 }
 
