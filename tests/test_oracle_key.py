@@ -193,3 +193,55 @@ def test_workload_unit_value_step_residual_feeds_the_key_step():
     assert r["key"]["rel_residual"] <= 1e-12
     assert np.array_equal(r["Kstar"][r["fixed"]], r["K0"][r["fixed"]])
     assert np.abs(r["Kstar"] - r["K0"]).max() > 0
+
+
+# ------------------------------------------------------ alternating steps ----
+
+def _unit(cfg_id=1, **over):
+    cfg = W.config(cfg_id, **over)
+    q, K, V, _ = W.make_unit(cfg, 0, 1)
+    return cfg, tuple(W.decode(a, cfg.dtype) for a in (q, K, V))
+
+
+def test_one_alternating_step_is_the_value_and_key_step():
+    cfg, (qd, Kd, Vd) = _unit()
+    a = KO.grkv_alternating(qd, Kd, Vd, cfg.window, cfg.budget, cfg.pool_kernel, cfg.lam,
+                            cfg.lam, steps=1)
+    b = KO.grkv_unit(qd, Kd, Vd, cfg.window, cfg.budget, cfg.pool_kernel, cfg.lam, cfg.lam)
+    assert a["steps_run"] == 1
+    np.testing.assert_allclose(a["Kstar"], b["Kstar"], atol=1e-12)
+    np.testing.assert_allclose(a["Vstar"], b["Vstar"], atol=1e-12)
+
+
+def test_second_step_linearizes_at_the_moved_keys():
+    # step 2 must use G = K^(1) - K0: its right-hand side is E + J_G G, and its
+    # key update solves the local ridge problem around K^(1) (KKT of Eq. 9-10
+    # with the g term), checked against the explicit-Jacobian primal
+    cfg, (qd, Kd, Vd) = _unit(n=256, budget=48)
+    lam = 5e-2
+    a = KO.grkv_alternating(qd, Kd, Vd, cfg.window, cfg.budget, cfg.pool_kernel, lam, lam,
+                            steps=2, stop=0.0)
+    assert a["steps_run"] == 2
+    h1, h2 = a["history"]
+    K1, V2 = h1["Kstar"], h2["Vstar"]
+    prim = KO.key_primal(a["Q"], a["K0"], K1, V2, a["Y"], a["idx"], a["pos"], a["fixed"], lam)
+    np.testing.assert_allclose(h2["Kstar"], prim, atol=1e-9)
+    # the second value step is the ridge solution for X at K^(1), anchored at V0
+    X1 = KO.attention_output(a["Q"], K1, V2, a["idx"], a["pos"], True)[1]
+    G = np.flatnonzero(~a["fixed"])
+    A = np.vstack([X1[:, G], np.sqrt(lam) * np.eye(G.size)])
+    b = np.vstack([a["Y"] - X1 @ a["V0"], np.zeros((G.size, a["Y"].shape[1]))])
+    dVG = np.linalg.lstsq(A, b, rcond=None)[0]
+    np.testing.assert_allclose(V2[G] - a["V0"][G], dVG, atol=1e-9)
+    assert np.array_equal(V2[a["fixed"]], a["V0"][a["fixed"]])
+
+
+def test_stop_rule_when_keys_cannot_move():
+    # lambda_k -> infinity keeps K = K0, so the second value step repeats the
+    # first and the iterates stop changing: the loop ends after step 2
+    cfg, (qd, Kd, Vd) = _unit()
+    a = KO.grkv_alternating(qd, Kd, Vd, cfg.window, cfg.budget, cfg.pool_kernel, cfg.lam,
+                            1e14, steps=5)
+    assert a["steps_run"] == 2
+    assert a["history"][1]["delta_v"] <= 1e-9 and a["history"][1]["delta_k"] <= 1e-9
+    assert np.abs(a["Kstar"] - a["K0"]).max() < 1e-10
