@@ -165,12 +165,19 @@ int grkv_compress(const void* q_obs, const void* K, const void* V, int64_t n,
  * which minimises ||E - J_G dK||^2 + lambda_k ||dK||^2; fixed keys keep K0.
  * The md x md system is solved matrix-free by conjugate gradients from
  * alpha = 0.  NULL options select {lambda_k = lambda, max_iter = 64,
- * tol = 1e-5f} (the paper uses lambda_k = lambda_v and does not state its CG
- * settings). */
+ * tol = 1e-5f, steps = 1} (the paper uses lambda_k = lambda_v and does not
+ * state its CG settings). */
 typedef struct {
   float lambda_k;   /* ridge coefficient of the keys, >= 0 and finite */
   int32_t max_iter; /* conjugate-gradient iterations at most, 0 .. 4096 */
-  float tol;        /* stop once ||r|| <= tol ||E|| (recursive residual), >= 0 */
+  float tol;        /* stop once ||r|| <= tol ||rhs|| (recursive residual), >= 0 */
+  int32_t steps;    /* alternating value/key steps S, 1 .. 16 (Algorithm 1; the
+                       paper's default and best setting is 1).  Step t > 1 takes
+                       the value step at the current keys K^(t) (X from K^(t),
+                       the update still anchored at V0) and the key step
+                       linearized at K^(t), whose right-hand side gains
+                       J_G (K^(t) - K0).  All S steps run (the paper's early
+                       stop at a change <= 1e-9 is below fp32 resolution). */
 } grkv_key_options;
 
 /* Per-unit key-step outcome in cg_info[u][2]. */
@@ -181,14 +188,17 @@ typedef struct {
 #define GRKV_KEY_BREAKDOWN 4 /* a CG step found p^T A p <= 0 (possible only
                                 for lambda_k = 0); the last iterate is kept */
 
-/* grkv_compress followed by the key step.  All arguments as for
- * grkv_compress; in addition
+/* grkv_compress followed by the key step (and, for steps > 1, further
+ * alternating value and key steps).  All arguments as for grkv_compress; in
+ * addition
  *   kopt     key-step options, or NULL for the defaults above
  *   k_star   float [U][c][d]   merged keys K*, device memory (required);
  *                              k_out still receives K0
- *   cg_info  float [U][4]      {CG iterations, final ||r|| / ||E||,
- *                              GRKV_KEY_* outcome, ||E||_F}, or NULL
- * out->workspace_bytes must be at least grkv_workspace_bytes_kv().
+ *   cg_info  float [U][4]      of the last key step: {CG iterations, final
+ *                              ||r|| / ||rhs||, GRKV_KEY_* outcome, ||rhs||_F},
+ *                              or NULL
+ * v_out and stats hold the last value step.  out->workspace_bytes must be at
+ * least grkv_workspace_bytes_kv() for the same number of steps.
  * Errors: those of grkv_compress; GRKV_ERR_INVALID for a null k_star or bad
  * kopt; GRKV_ERR_UNSUPPORTED unless dtype is bf16 and G*w <= 128. */
 int grkv_compress_kv(const void* q_obs, const void* K, const void* V, int64_t n,
@@ -197,9 +207,10 @@ int grkv_compress_kv(const void* q_obs, const void* K, const void* V, int64_t n,
                      const grkv_options* opt, const grkv_outputs* out,
                      const grkv_key_options* kopt, float* k_star, float* cg_info);
 
-/* Workspace bytes grkv_compress_kv needs; 0 if invalid or unsupported. */
+/* Workspace bytes grkv_compress_kv needs for `steps` alternating steps; 0 if
+ * invalid or unsupported. */
 size_t grkv_workspace_bytes_kv(const grkv_problem* prob, int64_t n,
-                               int32_t window, int32_t budget);
+                               int32_t window, int32_t budget, int32_t steps);
 
 /* The default key options for a value ridge coefficient lambda. */
 void grkv_default_key_options(grkv_key_options* kopt, float lambda);

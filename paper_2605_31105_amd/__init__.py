@@ -61,7 +61,8 @@ class Outputs(ctypes.Structure):
 
 
 class KeyOptions(ctypes.Structure):
-    _fields_ = [("lambda_k", ctypes.c_float), ("max_iter", ctypes.c_int32), ("tol", ctypes.c_float)]
+    _fields_ = [("lambda_k", ctypes.c_float), ("max_iter", ctypes.c_int32), ("tol", ctypes.c_float),
+                ("steps", ctypes.c_int32)]
 
 
 class Layout(ctypes.Structure):
@@ -101,7 +102,7 @@ def lib() -> ctypes.CDLL:
                                        ctypes.c_void_p, ctypes.c_void_p]
         L.grkv_workspace_bytes_kv.restype = ctypes.c_size_t
         L.grkv_workspace_bytes_kv.argtypes = [P(Problem), ctypes.c_int64, ctypes.c_int32,
-                                              ctypes.c_int32]
+                                              ctypes.c_int32, ctypes.c_int32]
         L.grkv_default_key_options.restype = None
         L.grkv_default_key_options.argtypes = [P(KeyOptions), ctypes.c_float]
         L.grkv_status_string.restype = ctypes.c_char_p
@@ -131,9 +132,9 @@ def workspace_layout(units, group, head_dim, dtype, n, window, budget) -> Layout
     return lay
 
 
-def workspace_bytes_kv(units, group, head_dim, dtype, n, window, budget) -> int:
+def workspace_bytes_kv(units, group, head_dim, dtype, n, window, budget, steps=1) -> int:
     prob = Problem(units, group, head_dim, dtype)
-    return int(lib().grkv_workspace_bytes_kv(ctypes.byref(prob), n, window, budget))
+    return int(lib().grkv_workspace_bytes_kv(ctypes.byref(prob), n, window, budget, steps))
 
 
 @dataclass
@@ -212,27 +213,31 @@ def compress(q_obs, K, V, window: int, budget: int, pool_kernel: int, lam: float
 
 
 def compress_kv(q_obs, K, V, window: int, budget: int, pool_kernel: int, lam: float, *,
-                lambda_k=None, max_iter: int = 64, tol: float = 1e-5, n_sink: int = 4,
+                lambda_k=None, max_iter: int = 64, tol: float = 1e-5, steps: int = 1,
+                n_sink: int = 4,
                 beta: float = 0.10, fix_window: bool = True, causal_window: bool = True,
                 stream=None, workspace=None, out=None, k_star=None, cg_info=None,
                 stage_events=None):
-    """``compress`` followed by the key step (bfloat16 inputs, G*w <= 128).
+    """``compress`` followed by the key step (bfloat16 inputs, G*w <= 128), and
+    for ``steps`` > 1 further alternating value and key steps.
 
     Returns ``(result, k_star, cg_info)``: k_star float32 [U, c, d] holds the
     merged keys K*, cg_info float32 [U, 4] holds {CG iterations, final
-    relative residual, KEY_* outcome, ||E||}.  ``lambda_k`` defaults to
-    ``lam``."""
+    relative residual, KEY_* outcome, ||rhs||} of the last key step.
+    ``lambda_k`` defaults to ``lam``."""
     import torch
 
     out, prob, opt, outs, handle, n = _prepare(
-        q_obs, K, V, window, budget, workspace_bytes_kv, n_sink, beta, fix_window,
+        q_obs, K, V, window, budget,
+        lambda *a: workspace_bytes_kv(*a, steps=steps), n_sink, beta, fix_window,
         causal_window, stream, workspace, out, stage_events)
     U, d = q_obs.shape[0], q_obs.shape[3]
     if k_star is None:
         k_star = torch.empty((U, budget, d), dtype=torch.float32, device=K.device)
     if cg_info is None:
         cg_info = torch.empty((U, 4), dtype=torch.float32, device=K.device)
-    kopt = KeyOptions(float(lam if lambda_k is None else lambda_k), int(max_iter), float(tol))
+    kopt = KeyOptions(float(lam if lambda_k is None else lambda_k), int(max_iter), float(tol),
+                      int(steps))
     st = lib().grkv_compress_kv(q_obs.data_ptr(), K.data_ptr(), V.data_ptr(), n, window, budget,
                                 pool_kernel, float(lam), ctypes.c_void_p(handle),
                                 ctypes.byref(prob), ctypes.byref(opt), ctypes.byref(outs),

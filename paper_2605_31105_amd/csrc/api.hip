@@ -127,7 +127,7 @@ int make_plan(const grkv_problem* prob, int64_t n, int32_t window, int32_t budge
 
 // Workspace of the key step, after the compress workspace.  A key-pass block
 // holds all m rows of a unit and a split of its retained keys.
-static void make_key_plan(const Plan& p, KeyPlan* kp) {
+static void make_key_plan(const Plan& p, int steps, KeyPlan* kp) {
   // about 256 blocks (one per compute unit) while every unit is iterating;
   // about 2048 later, when a unit's iteration spanning several compute units
   // keeps it short once only a few units are still converging
@@ -146,6 +146,12 @@ static void make_key_plan(const Plan& p, KeyPlan* kp) {
   kp->opart = take(U * Smax * mp * d * sizeof(float));
   kp->hpart = take(U * Smax * mp * sizeof(float));
   kp->cg = take(U * 4 * sizeof(double));
+  const size_t later = steps > 1 ? 1 : 0;
+  kp->q32 = take(later * U * p.m * d * sizeof(float));
+  kp->v0f = take(later * U * p.c * d * sizeof(float));
+  kp->v0c = take(later * U * p.c * d * sizeof(uint16_t));
+  kp->x = take(later * U * mp * p.c * sizeof(float));
+  kp->kcur = take(later * U * p.c * d * sizeof(float));
   kp->total = off;
 }
 
@@ -331,15 +337,17 @@ void grkv_default_key_options(grkv_key_options* kopt, float lambda) {
   kopt->lambda_k = lambda;
   kopt->max_iter = 64;
   kopt->tol = 1e-5f;
+  kopt->steps = 1;
 }
 
 size_t grkv_workspace_bytes_kv(const grkv_problem* prob, int64_t n, int32_t window,
-                               int32_t budget) {
+                               int32_t budget, int32_t steps) {
   Plan p;
+  if (steps < 1 || steps > 16) return 0;
   if (make_plan(prob, n, window, budget, 1, 0.f, nullptr, &p) != GRKV_OK) return 0;
   if (!key_supported(p)) return 0;
   KeyPlan kp;
-  make_key_plan(p, &kp);
+  make_key_plan(p, steps, &kp);
   return kp.total;
 }
 
@@ -356,12 +364,13 @@ int grkv_compress_kv(const void* q_obs, const void* K, const void* V, int64_t n,
   if (!(ko.lambda_k >= 0.f) || !isfinite(ko.lambda_k)) return GRKV_ERR_INVALID;
   if (ko.max_iter < 0 || ko.max_iter > 4096 || !(ko.tol >= 0.f) || !isfinite(ko.tol))
     return GRKV_ERR_INVALID;
+  if (ko.steps < 1 || ko.steps > 16) return GRKV_ERR_INVALID;
   Plan p;
   st = make_plan(prob, n, window, budget, pool_kernel, lambda, opt, &p);
   if (st != GRKV_OK) return st;
   if (!key_supported(p)) return GRKV_ERR_UNSUPPORTED;
   KeyPlan kp;
-  make_key_plan(p, &kp);
+  make_key_plan(p, ko.steps, &kp);
   if (out->workspace_bytes < kp.total) return GRKV_ERR_WORKSPACE;
   hipStream_t s = (hipStream_t)stream;
   st = run_compress(p, q_obs, K, V, n, s, out);
@@ -398,6 +407,47 @@ int grkv_compress_kv(const void* q_obs, const void* K, const void* V, int64_t n,
   if (timed && hipEventRecord((hipEvent_t)ev[2 * GRKV_STAGE_KEY], s) != hipSuccess)
     return GRKV_ERR_HIP;
   if (launch_key(p, kp, a, s) != hipSuccess) return GRKV_ERR_HIP;
+
+  // Later alternating steps (Algorithm 1, S > 1): the value step at the
+  // current fp32 keys K^(t) (still anchored at V0) on the generic fp32
+  // kernels, then the key step linearized at K^(t).
+  if (ko.steps > 1) {
+    Plan p32 = p;
+    p32.dtype = GRKV_F32;
+    float* q32 = F(kp.q32);
+    float* v0f = F(kp.v0f);
+    float* kcur = F(kp.kcur);
+    float* x = F(kp.x);
+    const size_t vbytes = (size_t)p.U * p.c * p.d * sizeof(float);
+    if (launch_to_f32((const uint16_t*)q_obs, q32, (size_t)p.U * p.m * p.d, s) != hipSuccess)
+      return GRKV_ERR_HIP;
+    if (launch_gather(p, K, V, out->idx, out->k_out, ws + kp.v0c, v0f, s) != hipSuccess)
+      return GRKV_ERR_HIP;
+    a.kcur = kcur;
+    for (int t = 1; t < ko.steps; ++t) {
+      if (hipMemcpyAsync(kcur, k_star, vbytes, hipMemcpyDeviceToDevice, s) != hipSuccess)
+        return GRKV_ERR_HIP;
+      AttnPass r = {};
+      r.q = q32; r.k = kcur; r.v = v0f; r.kpos = out->idx; r.nk = p.c;
+      r.S = p.S2; r.chunk = p.chunk2;
+      r.pmax = F(p.pmax2); r.psum = (double*)(ws + p.psum2);
+      r.lse = (double*)(ws + p.lse2); r.lse_log2 = F(p.lse2_log2);
+      r.ypart = F(p.xvpart); r.colsum = nullptr; r.prefix = 0; r.xout = x; r.split_p = true;
+      uint8_t* fixed = (uint8_t*)(ws + p.fixed);
+      if (launch_lse_pass(p32, r, s) != hipSuccess ||
+          launch_lse_combine(p32, r.pmax, r.psum, p.S2, (double*)(ws + p.lse2), F(p.lse2_log2),
+                             s) != hipSuccess ||
+          launch_prob_pass(p32, r, s) != hipSuccess ||
+          launch_combine_rows(p32, F(p.xvpart), p.S2, F(p.y), F(p.resid), s) != hipSuccess ||
+          launch_gram(p32, x, fixed, F(p.npart), s) != hipSuccess ||
+          launch_cholesky_solve(p32, F(p.npart), F(p.y), F(p.resid), F(p.gram), F(p.z),
+                                F(p.stats_ws), out->stats, s) != hipSuccess ||
+          hipMemcpyAsync(out->v_out, v0f, vbytes, hipMemcpyDeviceToDevice, s) != hipSuccess ||
+          launch_update_add(p32, x, fixed, F(p.z), F(p.stats_ws), out->v_out, s) != hipSuccess)
+        return GRKV_ERR_HIP;
+      if (launch_key(p, kp, a, s) != hipSuccess) return GRKV_ERR_HIP;
+    }
+  }
   if (timed && hipEventRecord((hipEvent_t)ev[2 * GRKV_STAGE_KEY + 1], s) != hipSuccess)
     return GRKV_ERR_HIP;
   return GRKV_OK;

@@ -143,12 +143,16 @@ struct KeyPlan {
   int S4, chunk4;           // splits of the retained keys per unit, later CG iterations
   int S_full, chunk_full;   // the same for the first iterations and the final pass
   size_t Fm, alpha, r, p, sdot, W, opart, hpart, cg;   // offsets after Plan::total
+  // later alternating steps (steps > 1): fp32 copies of Q and V0, the compact
+  // bf16 V0, X [U][mp][c] of the fp32 value step, the current keys
+  size_t q32, v0f, v0c, x, kcur;
   size_t total;
 };
 
 struct KeyArgs {
   const uint16_t* q;        // [U][m][d] window queries
   const uint16_t* k0;       // [U][c][d] retained keys K0
+  const float* kcur;        // [U][c][d] current keys (fp32) at a later alternating step, or null (K0)
   const float* vs;          // [U][c][d] merged values V*
   const float* lse2;        // [U][mp] retained log-sum-exp (log2 domain)
   const uint8_t* fixed;     // [U][c]
@@ -167,5 +171,6 @@ struct KeyArgs {
 
 bool key_supported(const Plan& p);
 hipError_t launch_key(const Plan& p, const KeyPlan& kp, const KeyArgs& a, hipStream_t s);
+hipError_t launch_to_f32(const uint16_t* src, float* dst, size_t n, hipStream_t s);
 
 }  // namespace grkv

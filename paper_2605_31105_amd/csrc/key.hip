@@ -65,6 +65,10 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b, uint32_t* lo) 
   return hw;
 }
 
+__device__ __forceinline__ float dot4(float4 a, float4 b) {
+  return a.x * b.x + a.y * b.y + a.z * b.z + a.w * b.w;
+}
+
 __device__ __forceinline__ double block_sum(double v, double* red) {
   for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
@@ -137,54 +141,64 @@ __global__ __launch_bounds__(256) void key_init_kernel(
 }
 
 // ------------------------------------------------------------------ pass ----
-template <int MP, int D>
+enum { kOp = 0, kFinal = 1, kJvp = 2 };   // key_pass modes
+
+// LDS regions (bf16 elements).  KF: the current keys are fp32 (later
+// alternating steps) and are held as bf16 hi + lo; JVP: the tile of
+// G = K_cur - K0 (hi + lo) replaces D^T.
+template <int MP, int D, int KM, bool KF>
 struct KeyLds {
-  static constexpr int KS = D + 8;     // row stride (bf16) of K and V rows
+  static constexpr int KS = D + 8;     // row stride (bf16) of K, G and V rows
   static constexpr int TS = kKT + 8;   // row stride of V^T rows
   static constexpr int DS = MP + 8;    // row stride of D^T rows
   static constexpr int QS = MP + 8;    // row stride of Q^T rows
-  static constexpr int k = 0;
-  static constexpr int vh = k + kKT * KS;
+  static constexpr int HS = kKT + 8;   // row stride of a wave's H rows
+  static constexpr int k = 0;                                   // K (hi)
+  static constexpr int kl = k + kKT * KS;                       // K lo
+  static constexpr int vh = kl + (KF ? kKT * KS : 0);
   static constexpr int vl = vh + kKT * KS;
   static constexpr int th = vl + kKT * KS;
   static constexpr int tl = th + D * TS;
-  static constexpr int dh = tl + D * TS;
-  static constexpr int dl = dh + kKT * DS;
-  static constexpr int HS = kKT + 8;    // row stride of a wave's H rows
-  static constexpr int hh = dl + kKT * DS;  // [NW][16][HS] H hi, then lo
-  static constexpr int hl = hh + MP * HS;
-  static constexpr int qt = hl + MP * HS;
-  static constexpr int end = qt;             // the operator pass
-  static constexpr int end_final = qt + D * QS;
-  static constexpr size_t bytes(bool final_pass) {
-    return (size_t)(final_pass ? end_final : end) * sizeof(u16) + kKT * (sizeof(int) + 1);
-  }
+  static constexpr int dh = tl + D * TS;                        // D^T hi / G hi
+  static constexpr int dl = dh + kKT * (KM == kJvp ? KS : DS);  // D^T lo / G lo
+  static constexpr int hh = dl + kKT * (KM == kJvp ? KS : DS);  // [NW][16][HS] H hi, then lo
+  static constexpr int hl = hh + (KM == kFinal ? 0 : MP * HS);
+  static constexpr int qt = hl + (KM == kFinal ? 0 : MP * HS);
+  static constexpr int end = qt + (KM == kFinal ? D * QS : 0);
+  static constexpr size_t bytes() { return (size_t)end * sizeof(u16) + kKT * (sizeof(int) + 1); }
 };
 
-// FINAL = false: partial sums of H V* (opart) and H 1 (hpart) over this
-// block's keys for the direction in pv.  FINAL = true: K* = K0 + J_G^T pv for
-// this block's keys.
-template <int MP, int D, bool FINAL>
+// One pass over a split of the retained keys of unit blockIdx.y, with X from
+// the current keys (K0 in bf16, or fp32 K_cur when KF) and the retained LSE.
+//   kOp:    partial sums of H V* (opart) and H 1 (hpart) for the direction p,
+//           H = X o (W D), D = X o (p V*^T - rowdot(F, p)) with fixed columns 0;
+//   kJvp:   the same partials for H = X o (Q G^T / sqrt(d)), G = K_cur - K0
+//           (the J_G G term of the right-hand side at later steps);
+//   kFinal: K* = K0 + J_G^T alpha for the split's keys.
+template <int MP, int D, int KM, bool KF>
 __global__ __launch_bounds__(MP / 16 * 64) void key_pass_kernel(
-    const u16* __restrict__ q, const u16* __restrict__ k0, const float* __restrict__ vs,
-    const float* __restrict__ lse2, const uint8_t* __restrict__ fixed,
-    const int32_t* __restrict__ idx, const float* __restrict__ Fm, const float* __restrict__ W,
-    const float* __restrict__ pv, const float* __restrict__ sdot_in,
-    const double* __restrict__ cg, float* __restrict__ opart,
+    const u16* __restrict__ q, const u16* __restrict__ k0, const float* __restrict__ kcur,
+    const float* __restrict__ vs, const float* __restrict__ lse2,
+    const uint8_t* __restrict__ fixed, const int32_t* __restrict__ idx,
+    const float* __restrict__ Fm, const float* __restrict__ W, const float* __restrict__ pv,
+    const float* __restrict__ sdot_in, const double* __restrict__ cg, float* __restrict__ opart,
     float* __restrict__ hpart, float* __restrict__ kstar, float* __restrict__ cg_info, int m,
     int w, int64_t n, int c, int S, int chunk, int causal, float scale_log2, float inv_sqrt_d) {
+  constexpr bool FINAL = KM == kFinal, JVP = KM == kJvp;
   constexpr int NW = MP / 16, NTH = NW * 64;
-  constexpr int KCH = kKT * D / 8;            // 16-byte chunks of a K tile
+  constexpr int KCH = kKT * D / 8;            // 16-byte chunks of a bf16 K tile
   constexpr int KPT = (KCH + NTH - 1) / NTH;
+  constexpr int KCH4 = kKT * D / 4;           // 4-element pieces of an fp32 K tile
+  constexpr int KPT4 = (KCH4 + NTH - 1) / NTH;
   // V staging unit: keys {k, k + 16} x four columns, so that both the row-major
   // copy (8-byte pieces) and the transposed copy (4-byte pieces) are written
   // without 2-byte stores
   constexpr int VUN = 16 * (D / 4);
   constexpr int VPT = (VUN + NTH - 1) / NTH;
   constexpr float NEG_INF = -__builtin_huge_valf();
-  using L = KeyLds<MP, D>;
+  using L = KeyLds<MP, D, KM, KF>;
   extern __shared__ __attribute__((aligned(16))) u16 sm[];
-  int* kp_s = reinterpret_cast<int*>(sm + (FINAL ? L::end_final : L::end));
+  int* kp_s = reinterpret_cast<int*>(sm + L::end);
   uint8_t* fx_s = reinterpret_cast<uint8_t*>(kp_s + kKT);
 
   const int u = blockIdx.y, s = blockIdx.x, tid = threadIdx.x;
@@ -209,18 +223,36 @@ __global__ __launch_bounds__(MP / 16 * 64) void key_pass_kernel(
 
   // register-staged tile loads
   const u16* ku = k0 + (size_t)u * c * D;
+  const float* kf = KF ? kcur + (size_t)u * c * D : nullptr;
   const float* vu = vs + (size_t)u * c * D;
-  uint4 kreg[KPT];
+  uint4 kreg[KF ? 1 : KPT];
+  float4 kfreg[KF ? KPT4 : 1];
+  uint2 k0reg[JVP ? KPT4 : 1];
   float4 vreg[VPT][2];
   int kpreg = 0, fxreg = 1;
   // loads clamp the key into the split and zero what lies beyond it
   auto load_tile = [&](int t0) {
+    if constexpr (KF) {
 #pragma unroll
-    for (int k = 0; k < KPT; ++k) {
-      const int e = min(tid + k * NTH, KCH - 1);
-      const int key = e / (D / 8), ch = e % (D / 8);
-      const uint4 v = *reinterpret_cast<const uint4*>(ku + (size_t)min(t0 + key, j1 - 1) * D + ch * 8);
-      kreg[k] = t0 + key < j1 ? v : make_uint4(0, 0, 0, 0);
+      for (int k = 0; k < KPT4; ++k) {
+        const int e = min(tid + k * NTH, KCH4 - 1);
+        const int key = e / (D / 4), ch = e % (D / 4);
+        const size_t o = (size_t)min(t0 + key, j1 - 1) * D + ch * 4;
+        const float4 v = *reinterpret_cast<const float4*>(kf + o);
+        kfreg[k] = t0 + key < j1 ? v : make_float4(0.f, 0.f, 0.f, 0.f);
+        if constexpr (JVP) {
+          const uint2 b = *reinterpret_cast<const uint2*>(ku + o);
+          k0reg[k] = t0 + key < j1 ? b : make_uint2(0, 0);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < KPT; ++k) {
+        const int e = min(tid + k * NTH, KCH - 1);
+        const int key = e / (D / 8), ch = e % (D / 8);
+        const uint4 v = *reinterpret_cast<const uint4*>(ku + (size_t)min(t0 + key, j1 - 1) * D + ch * 8);
+        kreg[k] = t0 + key < j1 ? v : make_uint4(0, 0, 0, 0);
+      }
     }
 #pragma unroll
     for (int k = 0; k < VPT; ++k) {
@@ -242,12 +274,38 @@ __global__ __launch_bounds__(MP / 16 * 64) void key_pass_kernel(
     }
   };
   auto store_tile = [&]() {
+    if constexpr (KF) {
 #pragma unroll
-    for (int k = 0; k < KPT; ++k) {
-      const int e = tid + k * NTH;
-      if (e < KCH) {
-        const int key = e / (D / 8), ch = e % (D / 8);
-        *reinterpret_cast<uint4*>(sm + L::k + key * L::KS + ch * 8) = kreg[k];
+      for (int k = 0; k < KPT4; ++k) {
+        const int e = tid + k * NTH;
+        if (e < KCH4) {
+          const int key = e / (D / 4), ch = e % (D / 4);
+          const int o = key * L::KS + ch * 4;
+          const float4 v = kfreg[k];
+          uint32_t l0, l1;
+          const uint32_t h0 = pack_bf16x2(v.x, v.y, &l0), h1 = pack_bf16x2(v.z, v.w, &l1);
+          *reinterpret_cast<uint2*>(sm + L::k + o) = make_uint2(h0, h1);
+          *reinterpret_cast<uint2*>(sm + L::kl + o) = make_uint2(l0, l1);
+          if constexpr (JVP) {
+            // G = K_cur - K0 (zero for fixed keys, which never move)
+            const uint2 b = k0reg[k];
+            const float gx = v.x - __uint_as_float(b.x << 16), gy = v.y - __uint_as_float(b.x & 0xffff0000u);
+            const float gz = v.z - __uint_as_float(b.y << 16), gw = v.w - __uint_as_float(b.y & 0xffff0000u);
+            uint32_t gl0, gl1;
+            const uint32_t gh0 = pack_bf16x2(gx, gy, &gl0), gh1 = pack_bf16x2(gz, gw, &gl1);
+            *reinterpret_cast<uint2*>(sm + L::dh + o) = make_uint2(gh0, gh1);
+            *reinterpret_cast<uint2*>(sm + L::dl + o) = make_uint2(gl0, gl1);
+          }
+        }
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < KPT; ++k) {
+        const int e = tid + k * NTH;
+        if (e < KCH) {
+          const int key = e / (D / 8), ch = e % (D / 8);
+          *reinterpret_cast<uint4*>(sm + L::k + key * L::KS + ch * 8) = kreg[k];
+        }
       }
     }
 #pragma unroll
@@ -292,9 +350,9 @@ __global__ __launch_bounds__(MP / 16 * 64) void key_pass_kernel(
   for (int ks = 0; ks < D / 32; ++ks)
     qa[ks] = row < m ? *reinterpret_cast<const uint4*>(qu + (size_t)row * D + ks * 32 + 8 * g)
                      : make_uint4(0, 0, 0, 0);
-  bf16x8 pah[D / 32], pal[D / 32];
+  bf16x8 pah[JVP ? 1 : D / 32], pal[JVP ? 1 : D / 32];
   float sdot = 0.f;
-  {
+  if constexpr (!JVP) {
     const float* pr = pv + ((size_t)u * MP + row) * D;
     const float* fr = Fm + ((size_t)u * MP + row) * D;
 #pragma unroll
@@ -323,14 +381,16 @@ __global__ __launch_bounds__(MP / 16 * 64) void key_pass_kernel(
     const int r4 = 16 * wave + 4 * g + i;
     if constexpr (FINAL)
       s4[i] = __shfl(sdot, 4 * g + i);
-    else
+    else if constexpr (!JVP)
       s4[i] = sdot_in[(size_t)u * MP + r4];
+    else
+      s4[i] = 0.f;
     nl4[i] = r4 < m ? -lse2[(size_t)u * MP + r4] : NEG_INF;
     rp4[i] = r4 < m ? (int)(n - w + r4 % w) : -1;
   }
 
-  bf16x8 wah[MP / 32], wal[MP / 32];
-  if constexpr (!FINAL) {
+  bf16x8 wah[KM == kOp ? MP / 32 : 1], wal[KM == kOp ? MP / 32 : 1];
+  if constexpr (KM == kOp) {
     // W row of this lane at the columns 32kb + {4g + i, 16 + 4g + i}
     const float* wr = W + ((size_t)u * MP + row) * MP;
 #pragma unroll
@@ -340,7 +400,8 @@ __global__ __launch_bounds__(MP / 16 * 64) void key_pass_kernel(
       const float x[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
       split8(x, wah[kb], wal[kb]);
     }
-  } else {
+  }
+  if constexpr (FINAL) {
     // Q^T in LDS, rows permuted by kperm: QT[dd][kperm(r)] = Q[r][dd]
     for (int e = tid; e < MP * (D / 8); e += NTH) {
       const int r = e % MP, ch = e / MP;   // neighbouring lanes: neighbouring rows
@@ -367,7 +428,7 @@ __global__ __launch_bounds__(MP / 16 * 64) void key_pass_kernel(
     __syncthreads();
     if (t0 + kKT < j1) load_tile(t0 + kKT);
 
-    // S = Q K^T, B = dir V^T, D = X o (B - s) for this wave's rows -> D^T in LDS
+    // S = Q K^T (and for kOp / kFinal B = dir V^T, D = X o (B - s) -> D^T in LDS)
     float xk[kKT / 16][4];   // X[16w + 4g + i][key 16kt + l16]
 #pragma unroll
     for (int kt = 0; kt < kKT / 16; ++kt) {
@@ -377,12 +438,18 @@ __global__ __launch_bounds__(MP / 16 * 64) void key_pass_kernel(
       for (int ks = 0; ks < D / 32; ++ks) {
         const int o = key * L::KS + ks * 32 + 8 * g;
         const bf16x8 kk = as_bf16x8(*reinterpret_cast<const uint4*>(sm + L::k + o));
-        const bf16x8 vh = as_bf16x8(*reinterpret_cast<const uint4*>(sm + L::vh + o));
-        const bf16x8 vl = as_bf16x8(*reinterpret_cast<const uint4*>(sm + L::vl + o));
         sacc = mfma_bf16(as_bf16x8(qa[ks]), kk, sacc);
-        bacc = mfma_bf16(pah[ks], vh, bacc);
-        bacc = mfma_bf16(pah[ks], vl, bacc);
-        bacc = mfma_bf16(pal[ks], vh, bacc);
+        if constexpr (KF) {
+          const bf16x8 kl = as_bf16x8(*reinterpret_cast<const uint4*>(sm + L::kl + o));
+          sacc = mfma_bf16(as_bf16x8(qa[ks]), kl, sacc);
+        }
+        if constexpr (!JVP) {
+          const bf16x8 vh = as_bf16x8(*reinterpret_cast<const uint4*>(sm + L::vh + o));
+          const bf16x8 vl = as_bf16x8(*reinterpret_cast<const uint4*>(sm + L::vl + o));
+          bacc = mfma_bf16(pah[ks], vh, bacc);
+          bacc = mfma_bf16(pah[ks], vl, bacc);
+          bacc = mfma_bf16(pal[ks], vh, bacc);
+        }
       }
       const int kpos = kp_s[key];
       const bool live = t0 + key < j1;
@@ -395,14 +462,16 @@ __global__ __launch_bounds__(MP / 16 * 64) void key_pass_kernel(
         xk[kt][i] = x;
         dv[i] = free_key ? x * (bacc[i] - s4[i]) : 0.f;
       }
-      uint32_t dl0, dl1;
-      const uint32_t dh0 = pack_bf16x2(dv[0], dv[1], &dl0);
-      const uint32_t dh1 = pack_bf16x2(dv[2], dv[3], &dl1);
-      const int dp = key * L::DS + 32 * (wave >> 1) + 8 * g + 4 * (wave & 1);
-      *reinterpret_cast<uint2*>(sm + L::dh + dp) = make_uint2(dh0, dh1);
-      *reinterpret_cast<uint2*>(sm + L::dl + dp) = make_uint2(dl0, dl1);
+      if constexpr (!JVP) {
+        uint32_t dl0, dl1;
+        const uint32_t dh0 = pack_bf16x2(dv[0], dv[1], &dl0);
+        const uint32_t dh1 = pack_bf16x2(dv[2], dv[3], &dl1);
+        const int dp = key * L::DS + 32 * (wave >> 1) + 8 * g + 4 * (wave & 1);
+        *reinterpret_cast<uint2*>(sm + L::dh + dp) = make_uint2(dh0, dh1);
+        *reinterpret_cast<uint2*>(sm + L::dl + dp) = make_uint2(dl0, dl1);
+      }
     }
-    __syncthreads();   // D^T of all rows is in LDS
+    if constexpr (!JVP) __syncthreads();   // D^T of all rows is in LDS
 
     if constexpr (FINAL) {
       // dK [keys x d] = D^T Q / sqrt(d); K* = K0 + dK (fixed keys: dK = 0)
@@ -423,26 +492,42 @@ __global__ __launch_bounds__(MP / 16 * 64) void key_pass_kernel(
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int key = 16 * kt + 4 * g + i;
-          if (t0 + key < j1)
-            kstar[((size_t)u * c + t0 + key) * D + dd] =
-                bf16_to_f32(sm[L::k + key * L::KS + dd]) + acc[i] * inv_sqrt_d;
+          if (t0 + key < j1) {
+            const size_t o = ((size_t)u * c + t0 + key) * D + dd;
+            const float base = KF ? bf16_to_f32(k0[o]) : bf16_to_f32(sm[L::k + key * L::KS + dd]);
+            kstar[o] = base + acc[i] * inv_sqrt_d;
+          }
         }
       }
     } else {
-      // A = W D for this wave's rows, H = X o A: lane holds [row 16w + 4g + i][key]
+      // A = W D (kOp) or A = Q G^T / sqrt(d) (kJvp) for this wave's rows, and
+      // H = X o A: lane holds [row 16w + 4g + i][key]
       const int hb = wave * 16 * L::HS;
       float hv[kKT / 16][4];
 #pragma unroll
       for (int kt = 0; kt < kKT / 16; ++kt) {
         f32x4 aacc = zero4();
+        if constexpr (JVP) {
 #pragma unroll
-        for (int kb = 0; kb < MP / 32; ++kb) {
-          const int ao = (16 * kt + l16) * L::DS + 32 * kb + 8 * g;
-          const bf16x8 dh = as_bf16x8(*reinterpret_cast<const uint4*>(sm + L::dh + ao));
-          const bf16x8 dl = as_bf16x8(*reinterpret_cast<const uint4*>(sm + L::dl + ao));
-          aacc = mfma_bf16(wah[kb], dh, aacc);
-          aacc = mfma_bf16(wal[kb], dh, aacc);
-          aacc = mfma_bf16(wah[kb], dl, aacc);
+          for (int ks = 0; ks < D / 32; ++ks) {
+            const int o = (16 * kt + l16) * L::KS + ks * 32 + 8 * g;
+            const bf16x8 gh = as_bf16x8(*reinterpret_cast<const uint4*>(sm + L::dh + o));
+            const bf16x8 gl = as_bf16x8(*reinterpret_cast<const uint4*>(sm + L::dl + o));
+            aacc = mfma_bf16(as_bf16x8(qa[ks]), gh, aacc);
+            aacc = mfma_bf16(as_bf16x8(qa[ks]), gl, aacc);
+          }
+#pragma unroll
+          for (int i = 0; i < 4; ++i) aacc[i] *= inv_sqrt_d;
+        } else {
+#pragma unroll
+          for (int kb = 0; kb < MP / 32; ++kb) {
+            const int ao = (16 * kt + l16) * L::DS + 32 * kb + 8 * g;
+            const bf16x8 dh = as_bf16x8(*reinterpret_cast<const uint4*>(sm + L::dh + ao));
+            const bf16x8 dl = as_bf16x8(*reinterpret_cast<const uint4*>(sm + L::dl + ao));
+            aacc = mfma_bf16(wah[kb], dh, aacc);
+            aacc = mfma_bf16(wal[kb], dh, aacc);
+            aacc = mfma_bf16(wah[kb], dl, aacc);
+          }
         }
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -491,13 +576,67 @@ __global__ __launch_bounds__(MP / 16 * 64) void key_pass_kernel(
   }
 }
 
+// Right-hand side at a later alternating step: r = E + J_G G from the kJvp
+// partials (J_G G = sum_s opart - (sum_s hpart) o F), then p = r, alpha = 0
+// and the CG state.  key_init has already set F, E (in r) and the skip state.
+template <int MP, int D>
+__global__ __launch_bounds__(1024) void key_rhs_kernel(
+    const float* __restrict__ opart, const float* __restrict__ hpart, int S,
+    const float* __restrict__ Fm, float* __restrict__ r, float* __restrict__ p,
+    float* __restrict__ sdot, double* __restrict__ cg) {
+  constexpr int NTH = 1024, E4 = MP * D / 4, PER = (E4 + NTH - 1) / NTH, RW = D / 4;
+  __shared__ float hsum[MP];
+  __shared__ double red[16];
+  const int u = blockIdx.x, tid = threadIdx.x;
+  if ((int)cg[u * 4 + 3] == kKeySkipped) return;
+  for (int i = tid; i < MP; i += NTH) {
+    float h = 0.f;
+    for (int k = 0; k < S; ++k) h += hpart[((size_t)u * S + k) * MP + i];
+    hsum[i] = h;
+  }
+  __syncthreads();
+  const size_t base = (size_t)u * E4;
+  const float4* __restrict__ op4 = reinterpret_cast<const float4*>(opart) + (size_t)u * S * E4;
+  const float4* __restrict__ F4 = reinterpret_cast<const float4*>(Fm) + base;
+  float4* __restrict__ r4 = reinterpret_cast<float4*>(r) + base;
+  float4* __restrict__ p4 = reinterpret_cast<float4*>(p) + base;
+  double rr = 0;
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    const int e = tid + k * NTH;
+    float4 re = make_float4(0.f, 0.f, 0.f, 0.f), f = re;
+    if (e < E4) {
+      float4 v = r4[e];
+      for (int sp = 0; sp < S; ++sp) {
+        const float4 o = op4[(size_t)sp * E4 + e];
+        v.x += o.x; v.y += o.y; v.z += o.z; v.w += o.w;
+      }
+      f = F4[e];
+      const float h = hsum[e / RW];
+      re = make_float4(v.x - h * f.x, v.y - h * f.y, v.z - h * f.z, v.w - h * f.w);
+      r4[e] = re;
+      p4[e] = re;
+      rr += (double)dot4(re, re);
+    }
+    // row dot over the RW consecutive threads of a row (whole rows only)
+    float sd = dot4(f, re);
+#pragma unroll
+    for (int off = 1; off < RW; off <<= 1) sd += __shfl_xor(sd, off);
+    if (e < E4 && (e % RW) == 0) sdot[(size_t)u * MP + e / RW] = sd;
+  }
+  rr = block_sum(rr, red);
+  if (tid == 0) {
+    cg[u * 4 + 0] = rr;
+    cg[u * 4 + 1] = rr;
+    cg[u * 4 + 2] = 0;
+    cg[u * 4 + 3] = rr == 0 ? kKeyConverged : kKeyRunning;
+  }
+}
+
 // -------------------------------------------------------------------- cg ----
 // One conjugate-gradient update per unit: Ap = sum_s opart - (sum_s hpart) o F
 // + lambda_k p; alpha += a p; r -= a Ap; p = r + beta p; and the row dots
 // s = rowdot(F, p) of the new direction for the next operator pass.
-__device__ __forceinline__ float dot4(float4 a, float4 b) {
-  return a.x * b.x + a.y * b.y + a.z * b.z + a.w * b.w;
-}
 
 template <int MP, int D>
 __global__ __launch_bounds__(1024) void key_cg_kernel(
@@ -600,47 +739,73 @@ __global__ __launch_bounds__(1024) void key_cg_kernel(
   }
 }
 
-template <int MP, int D>
-hipError_t launch_key_t(const Plan& p, const KeyPlan& kp, const KeyArgs& a, hipStream_t s) {
-  using L = KeyLds<MP, D>;
+template <int MP, int D, int KM, bool KF>
+hipError_t launch_pass(const Plan& p, const KeyArgs& a, int S, int chunk, const float* dir,
+                       hipStream_t s) {
+  using L = KeyLds<MP, D, KM, KF>;
+  const size_t lds = L::bytes();
+  hipError_t e = hipFuncSetAttribute((const void*)key_pass_kernel<MP, D, KM, KF>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
   const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
   const float inv_sqrt_d = (float)(1.0 / sqrt((double)D));
+  hipLaunchKernelGGL((key_pass_kernel<MP, D, KM, KF>), dim3(S, p.U), dim3(MP / 16 * 64), lds, s,
+                     a.q, a.k0, a.kcur, a.vs, a.lse2, a.fixed, a.idx, a.Fm, a.W, dir, a.sdot,
+                     a.cg, a.opart, a.hpart, a.kstar, a.cg_info, p.m, p.w, p.n, p.c, S, chunk,
+                     p.opt.causal_window ? 1 : 0, scale_log2, inv_sqrt_d);
+  return hipGetLastError();
+}
+
+template <int MP, int D, bool KF>
+hipError_t launch_key_t(const Plan& p, const KeyPlan& kp, const KeyArgs& a, hipStream_t s) {
   hipLaunchKernelGGL((key_init_kernel<MP, D>), dim3(p.U), dim3(256), 0, s, a.q, a.y, a.zt,
                      a.stats_ws, p.lam, p.m, a.Fm, a.alpha, a.r, a.p, a.sdot, a.W, a.cg);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const size_t lds_op = L::bytes(false), lds_fin = L::bytes(true);
-  e = hipFuncSetAttribute((const void*)key_pass_kernel<MP, D, false>,
-                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_op);
-  if (e != hipSuccess) return e;
-  e = hipFuncSetAttribute((const void*)key_pass_kernel<MP, D, true>,
-                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_fin);
-  if (e != hipSuccess) return e;
-  const dim3 block(MP / 16 * 64);
-  const int causal = p.opt.causal_window ? 1 : 0;
+  if constexpr (KF) {
+    // a later alternating step: the right-hand side gains J_G (K_cur - K0)
+    e = launch_pass<MP, D, kJvp, KF>(p, a, kp.S_full, kp.chunk_full, nullptr, s);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((key_rhs_kernel<MP, D>), dim3(p.U), dim3(1024), 0, s, a.opart, a.hpart,
+                       kp.S_full, a.Fm, a.r, a.p, a.sdot, a.cg);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   for (int it = 0; it < a.max_iter; ++it) {
     // the first iterations, while every unit is still running, with the
     // fewest blocks a full GPU needs; later ones with more splits per unit,
     // which shortens an iteration once few units remain
     const bool early = it < kKeyEarlyIters;
     const int S = early ? kp.S_full : kp.S4, chunk = early ? kp.chunk_full : kp.chunk4;
-    hipLaunchKernelGGL((key_pass_kernel<MP, D, false>), dim3(S, p.U), block, lds_op, s, a.q,
-                       a.k0, a.vs, a.lse2, a.fixed, a.idx, a.Fm, a.W, a.p, a.sdot, a.cg,
-                       a.opart, a.hpart, nullptr, nullptr, p.m, p.w, p.n, p.c, S, chunk, causal,
-                       scale_log2, inv_sqrt_d);
+    e = launch_pass<MP, D, kOp, KF>(p, a, S, chunk, a.p, s);
+    if (e != hipSuccess) return e;
     hipLaunchKernelGGL((key_cg_kernel<MP, D>), dim3(p.U), dim3(1024), 0, s, a.opart, a.hpart,
                        S, a.Fm, a.alpha, a.r, a.p, a.sdot, a.cg, a.lam_k, a.tol, a.max_iter);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL((key_pass_kernel<MP, D, true>), dim3(kp.S_full, p.U), block, lds_fin, s,
-                     a.q, a.k0, a.vs, a.lse2, a.fixed, a.idx, a.Fm, nullptr, a.alpha, nullptr,
-                     a.cg, nullptr, nullptr, a.kstar, a.cg_info, p.m, p.w, p.n, p.c, kp.S_full,
-                     kp.chunk_full, causal, scale_log2, inv_sqrt_d);
-  return hipGetLastError();
+  return launch_pass<MP, D, kFinal, KF>(p, a, kp.S_full, kp.chunk_full, a.alpha, s);
+}
+
+template <int MP, int D>
+hipError_t launch_key_kf(const Plan& p, const KeyPlan& kp, const KeyArgs& a, hipStream_t s) {
+  return a.kcur ? launch_key_t<MP, D, true>(p, kp, a, s) : launch_key_t<MP, D, false>(p, kp, a, s);
+}
+
+__global__ void to_f32_kernel(const u16* __restrict__ src, float* __restrict__ dst, size_t n) {
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n;
+       i += (size_t)gridDim.x * blockDim.x)
+    dst[i] = bf16_to_f32(src[i]);
 }
 
 }  // namespace
+
+hipError_t launch_to_f32(const uint16_t* src, float* dst, size_t n, hipStream_t s) {
+  const size_t blocks = (n + 255) / 256;
+  hipLaunchKernelGGL(to_f32_kernel, dim3((unsigned)(blocks < 65535 ? blocks : 65535)), dim3(256),
+                     0, s, src, dst, n);
+  return hipGetLastError();
+}
 
 bool key_supported(const Plan& p) {
   return stream_supported(p) && merge_fast_supported(p) && p.mp <= 128 &&
@@ -650,15 +815,15 @@ bool key_supported(const Plan& p) {
 hipError_t launch_key(const Plan& p, const KeyPlan& kp, const KeyArgs& a, hipStream_t s) {
   if (p.d == 128) {
     switch (p.mp) {
-      case 32: return launch_key_t<32, 128>(p, kp, a, s);
-      case 64: return launch_key_t<64, 128>(p, kp, a, s);
-      case 128: return launch_key_t<128, 128>(p, kp, a, s);
+      case 32: return launch_key_kf<32, 128>(p, kp, a, s);
+      case 64: return launch_key_kf<64, 128>(p, kp, a, s);
+      case 128: return launch_key_kf<128, 128>(p, kp, a, s);
     }
   } else {
     switch (p.mp) {
-      case 32: return launch_key_t<32, 64>(p, kp, a, s);
-      case 64: return launch_key_t<64, 64>(p, kp, a, s);
-      case 128: return launch_key_t<128, 64>(p, kp, a, s);
+      case 32: return launch_key_kf<32, 64>(p, kp, a, s);
+      case 64: return launch_key_kf<64, 64>(p, kp, a, s);
+      case 128: return launch_key_kf<128, 64>(p, kp, a, s);
     }
   }
   return hipErrorInvalidValue;

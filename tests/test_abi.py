@@ -102,10 +102,10 @@ def test_binding_refuses_host_tensors():
 
 
 def _call_kv(L, U=2, Gq=4, d=128, dt=0, n=8192, w=32, c=512, k=7, lam=1e-2, kopt=None,
-             ws_bytes=None, null_kstar=False):
+             ws_bytes=None, null_kstar=False, steps_ws=1):
     prob = G.Problem(U, Gq, d, dt)
     fake = ctypes.c_void_p(4096)   # never dereferenced: validation fails first
-    need = L.grkv_workspace_bytes_kv(ctypes.byref(prob), n, w, c)
+    need = L.grkv_workspace_bytes_kv(ctypes.byref(prob), n, w, c, steps_ws)
     outs = G.Outputs(4096, 4096, 4096, 0, 4096, (need if ws_bytes is None else ws_bytes))
     return L.grkv_compress_kv(fake, fake, fake, n, w, c, k, lam, None, ctypes.byref(prob), None,
                               ctypes.byref(outs), ctypes.byref(kopt) if kopt else None,
@@ -114,11 +114,14 @@ def _call_kv(L, U=2, Gq=4, d=128, dt=0, n=8192, w=32, c=512, k=7, lam=1e-2, kopt
 
 @pytest.mark.parametrize("kw,code", [
     (dict(null_kstar=True), G.GRKV_ERR_INVALID),
-    (dict(kopt=G.KeyOptions(-1.0, 10, 1e-5)), G.GRKV_ERR_INVALID),
-    (dict(kopt=G.KeyOptions(math.nan, 10, 1e-5)), G.GRKV_ERR_INVALID),
-    (dict(kopt=G.KeyOptions(1e-2, -1, 1e-5)), G.GRKV_ERR_INVALID),
-    (dict(kopt=G.KeyOptions(1e-2, 5000, 1e-5)), G.GRKV_ERR_INVALID),
-    (dict(kopt=G.KeyOptions(1e-2, 10, -1.0)), G.GRKV_ERR_INVALID),
+    (dict(kopt=G.KeyOptions(-1.0, 10, 1e-5, 1)), G.GRKV_ERR_INVALID),
+    (dict(kopt=G.KeyOptions(math.nan, 10, 1e-5, 1)), G.GRKV_ERR_INVALID),
+    (dict(kopt=G.KeyOptions(1e-2, -1, 1e-5, 1)), G.GRKV_ERR_INVALID),
+    (dict(kopt=G.KeyOptions(1e-2, 5000, 1e-5, 1)), G.GRKV_ERR_INVALID),
+    (dict(kopt=G.KeyOptions(1e-2, 10, -1.0, 1)), G.GRKV_ERR_INVALID),
+    (dict(kopt=G.KeyOptions(1e-2, 10, 1e-5, 0)), G.GRKV_ERR_INVALID),
+    (dict(kopt=G.KeyOptions(1e-2, 10, 1e-5, 17)), G.GRKV_ERR_INVALID),
+    (dict(kopt=G.KeyOptions(1e-2, 10, 1e-5, 2), ws_bytes=None, steps_ws=1), G.GRKV_ERR_WORKSPACE),
     (dict(c=16), G.GRKV_ERR_INVALID),
     (dict(dt=1), G.GRKV_ERR_UNSUPPORTED),
     (dict(Gq=8, w=32), G.GRKV_ERR_UNSUPPORTED),
@@ -131,9 +134,11 @@ def test_key_step_invalid_arguments_rejected_before_launch(L, kw, code):
 def test_key_step_workspace_and_defaults(L):
     base = G.workspace_bytes(8, 4, 128, 0, 8192, 32, 512)
     kv = G.workspace_bytes_kv(8, 4, 128, 0, 8192, 32, 512)
+    assert G.workspace_bytes_kv(8, 4, 128, 0, 8192, 32, 512, steps=2) > kv
+    assert G.workspace_bytes_kv(8, 4, 128, 0, 8192, 32, 512, steps=0) == 0
     assert kv > base
     assert G.workspace_bytes_kv(8, 4, 128, 1, 8192, 32, 512) == 0     # fp32: no key step
     assert G.workspace_bytes_kv(8, 8, 128, 0, 8192, 32, 512) == 0     # m = 256
     ko = G.KeyOptions()
     L.grkv_default_key_options(ctypes.byref(ko), ctypes.c_float(0.25))
-    assert (ko.lambda_k, ko.max_iter) == (0.25, 64) and abs(ko.tol - 1e-5) < 1e-12
+    assert (ko.lambda_k, ko.max_iter, ko.steps) == (0.25, 64, 1) and abs(ko.tol - 1e-5) < 1e-12

@@ -186,3 +186,63 @@ def test_key_edge_shapes(label, over):
         # every retained token is a fixed window token: nothing moves
         K0 = W.bf16_bits_to_f32(gpu["k0"]).astype(np.float32)
         assert np.array_equal(gpu["kstar"], K0)
+
+
+def _alt_check(cfg, q, K, V, gpu, u, steps, lam_k=None, report=None):
+    qd, Kd, Vd = (W.decode(a[u], cfg.dtype) for a in (q, K, V))
+    lam_k = cfg.lam if lam_k is None else lam_k
+    r = KO.grkv_alternating(qd, Kd, Vd, cfg.window, cfg.budget, cfg.pool_kernel, cfg.lam, lam_k,
+                            steps=steps, idx=gpu["idx"][u], stop=0.0)
+    K0 = W.bf16_bits_to_f32(gpu["k0"][u]).astype(np.float64)
+    F = r["fixed"]
+    assert np.array_equal(gpu["kstar"][u][F].astype(np.float64), K0[F])
+    dk = np.abs(r["Kstar"] - K0).max()
+    kerr = np.abs(gpu["kstar"][u] - r["Kstar"]).max() / dk
+    verr = np.abs(gpu["v_out"][u] - r["Vstar"]).max() / np.abs(r["Vstar"]).max()
+    info = dict(unit=u, steps=steps, key_err=float(kerr), v_err=float(verr), max_dk=float(dk),
+                cg_iters=int(gpu["info"][u, 0]), state=int(gpu["info"][u, 2]))
+    if report is not None:
+        report.append(info)
+    assert kerr <= K_TOL and verr <= K_TOL, info
+    return info
+
+
+@pytest.mark.parametrize("steps", [2, 3])
+def test_key_alternating_steps_config2(steps):
+    # Algorithm 1 with S > 1: the value step at the moved keys, the key step
+    # with the J_G (K - K0) term, against the oracle's loop (no early stop)
+    cfg = W.config(2)
+    print("case alternating", steps, flush=True)
+    q, K, V = W.make_batch(cfg)
+    gpu = _run(cfg, q, K, V, steps=steps)
+    rep = []
+    for u in range(cfg.units):
+        _alt_check(cfg, q, K, V, gpu, u, steps, report=rep)
+    for r in rep:
+        print(r, flush=True)
+
+
+@pytest.mark.parametrize("label,over", [("m-32-d-64", dict(cfg=1, dtype="bf16")),
+                                        ("m-96", dict(cfg=2, group=3, layers=1, kv_heads=2,
+                                                      n=2048, budget=256))],
+                         ids=["m-32-d-64", "m-96"])
+def test_key_alternating_shapes(label, over):
+    over = dict(over)
+    cfg = W.config(over.pop("cfg"), **over)
+    print("case alternating", label, flush=True)
+    q, K, V = W.make_batch(cfg)
+    gpu = _run(cfg, q, K, V, steps=2)
+    for u in range(cfg.units):
+        print(_alt_check(cfg, q, K, V, gpu, u, 2), flush=True)
+
+
+def test_key_alternating_fixed_keys_repeat_the_value_step():
+    # with lambda_k huge the keys stay at K0, so every later value step
+    # repeats the first: S = 3 gives the S = 1 values
+    cfg = W.config(2, layers=1, kv_heads=2)
+    q, K, V = W.make_batch(W.config(2), units=range(2))
+    g1 = _run(cfg, q, K, V, lambda_k=1e9)
+    g3 = _run(cfg, q, K, V, lambda_k=1e9, steps=3)
+    K0 = W.bf16_bits_to_f32(g3["k0"]).astype(np.float32)
+    assert np.abs(g3["kstar"] - K0).max() < 1e-6
+    assert np.abs(g3["v_out"] - g1["v_out"]).max() <= 1e-4 * np.abs(g1["v_out"]).max()
