@@ -15,10 +15,12 @@ on a bounded sample of the same workload.  Besides: the same workload as one
 call per layer (`per_layer_calls`, not `value`) and the device copy bandwidth
 (`copy_gbs`, the practical ceiling for streaming), and the key step of GRKV
 run after the value step (`key_step`: grkv_compress_kv on the same workload,
-its CG iterations and the time of one CG iteration against the MFMA peak).
+its CG iterations and the time of one CG iteration against the MFMA peak), and
+the carrier-concentration diagnostic (`carrier`: the key-cosine matcher and
+the load metrics, against the MFMA peak).
 
   python bench.py [--steps K] [--warmup W] [--config 4] [--no-cpu-baseline] [--no-per-layer]
-                  [--no-key-step]
+                  [--no-key-step] [--no-carrier]
 """
 from __future__ import annotations
 
@@ -49,6 +51,8 @@ def parse():
                     help="skip the one-call-per-layer measurement")
     ap.add_argument("--no-key-step", dest="key_step", action="store_false",
                     help="skip the key-step measurement (grkv_compress_kv)")
+    ap.add_argument("--no-carrier", dest="carrier", action="store_false",
+                    help="skip the carrier-concentration measurement")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a 1 GiB device copy (for counter calibration)")
@@ -136,6 +140,60 @@ def cpu_baseline_key(cfg, q, K, V, seconds):
     return {"value": done / el, "unit": "heads/s", "cores": int(threads), "kind": "oracle",
             "sample": "%d of %d units (whole units: value and key step, float64 numpy oracle), %.1f s"
                       % (done, cfg.units, el)}
+
+
+def carrier(args, cfg, G, hip, stream, Kd, res, host=None):
+    """The carrier-concentration diagnostic on the same workload: the key-cosine
+    matcher over every cache position against the retained keys of the
+    compress call, then the per-unit load metrics.  Algorithmic flops per unit:
+    2 (n - c) c d (the similarities of the evicted tokens)."""
+    import numpy as np
+    import torch
+
+    U, n, c, d = cfg.units, cfg.n, cfg.budget, cfg.head_dim
+    if cfg.dtype != "bf16":
+        return None
+    print("bench: carrier diagnostics", file=sys.stderr, flush=True)
+    a, cnt, met, lc = G.carrier_stats(Kd, res.idx, cfg.group, res.stats)
+    torch.cuda.synchronize()
+    reps = max(1, min(args.steps, 5))
+    c0, c1 = hip.event(), hip.event()
+    hip.lib.hipEventRecord(c0, ctypes.c_void_p(stream.cuda_stream))
+    for _ in range(reps):
+        G.carrier_stats(Kd, res.idx, cfg.group, res.stats, assign=a, counts=cnt, metrics=met,
+                        l_common=lc)
+    hip.lib.hipEventRecord(c1, ctypes.c_void_p(stream.cuda_stream))
+    torch.cuda.synchronize()
+    ms = hip.elapsed_ms(c0, c1) / reps
+    flops = U * 2.0 * (n - c) * c * d
+    tflops = flops / (ms / 1e3) / 1e12
+    m = met.cpu().numpy().astype(np.float64)
+    summary = {k: float(np.nanmean(m[:, i])) for i, k in enumerate(G.CARRIER_METRICS)}
+    summary["b_over_c"] = summary["b"] / c
+    summary["b_eff_over_c"] = summary["b_eff"] / c
+    cpu = None
+    if host is not None:
+        import workloads as W
+        from oracle import grkv_carrier_oracle as CO
+        idx = res.idx.cpu().numpy().astype(np.int64)
+        done, t0 = 0, time.perf_counter()
+        while done < U and (done < 1 or time.perf_counter() - t0 < min(args.cpu_seconds, 10.0)):
+            CO.carrier_metrics(CO.carrier_assignment(W.decode(host[done], cfg.dtype), idx[done]),
+                               idx[done])
+            done += 1
+        el = time.perf_counter() - t0
+        cpu = {"value": done / el, "unit": "heads/s", "cores": 16, "kind": "oracle",
+               "sample": "%d of %d units (float64 numpy oracle), %.1f s" % (done, U, el)}
+    return {
+        "ms_per_call": ms,
+        "heads_per_s": U / (ms / 1e3),
+        "l_common": float(lc.cpu()[0]),
+        "macro_metrics": summary,
+        "roofline": {"bound": "mfma", "kernel": "match_kernel + stats_kernel",
+                     "achieved": tflops, "peak": 2500.0, "unit": "TFLOP/s",
+                     "frac": tflops / 2500.0, "traffic": None},
+        "cpu_baseline": cpu,
+    }
 
 
 def key_step(args, cfg, G, hip, stream, qd, Kd, Vd, host=None):
@@ -354,6 +412,8 @@ def main():
     key = (key_step(args, cfg, G, hip, stream, qd, Kd, Vd,
                     host=None if args.no_cpu_baseline else (q, K, V))
            if args.key_step else None)
+    car = (carrier(args, cfg, G, hip, stream, Kd, out, host=None if args.no_cpu_baseline else K)
+           if args.carrier else None)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -388,6 +448,7 @@ def main():
                      "frac_of_copy": achieved / copy_gbs,
                      "traffic": traffic},
         "key_step": key,
+        "carrier": car,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

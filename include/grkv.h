@@ -215,6 +215,40 @@ size_t grkv_workspace_bytes_kv(const grkv_problem* prob, int64_t n,
 /* The default key options for a value ridge coefficient lambda. */
 void grkv_default_key_options(grkv_key_options* kopt, float lambda);
 
+/* Carrier concentration of a local merge rule (App. B, "Quantitative Carrier
+ * Concentration"; Sec. 1): the diagnostic the paper uses to show that, after
+ * span-based eviction, a key-similarity matcher (as in D2O/KVMerger) loads a
+ * few span-boundary tokens with most of the evicted tokens.  Every evicted
+ * token j is assigned to the retained slot i with the highest key cosine
+ * similarity cos(k_j, k_idx[i]) over all retained tokens (equal values go to
+ * the lower slot; a zero key has cosine 0 with all), and with a_i the number of
+ * tokens assigned to slot i:
+ *   K        dtype [U][n][d]  the full cache keys (bf16 only)
+ *   idx      int32 [U][c]     ascending retained positions (grkv_compress)
+ *   stats    float [U][4]     the stats of a grkv_compress call, or NULL
+ *   assign   int32 [U][n]     out: slot of each evicted position, -1 for the
+ *                             retained positions (required)
+ *   counts   int32 [U][c]     out: a_i, or NULL
+ *   metrics  float [U][8]     out: {b = #(a_i > 0), b_eff = (sum a)^2 / sum a^2,
+ *                             A_max = max a / mean a, Gini of the a_i (mean
+ *                             absolute difference over all pairs / twice the
+ *                             mean), boundary fraction (first and last slots
+ *                             of each run of consecutive positions, over c),
+ *                             boundary share of the assignments, enrichment
+ *                             (share / fraction), boundary / interior mean
+ *                             load (NaN without both kinds; the load figures
+ *                             are NaN when nothing is evicted)}
+ *   l_common float [1]        out (needs stats): the discrepancy summed over the
+ *                             units, sum D_after ||Y||^2 / sum ||Y||^2 (the
+ *                             paper's L_common over these units), or NULL
+ * Errors: GRKV_ERR_INVALID for null required pointers, units or group < 1, an
+ * unknown dtype, budget outside [1, n]; GRKV_ERR_UNSUPPORTED for fp32 keys, d
+ * not 64/128 or budget > 8192; GRKV_ERR_HIP for a failed launch.  Allocates
+ * nothing; asynchronous on stream. */
+int grkv_carrier_stats(const void* K, int64_t n, int32_t budget, const grkv_problem* prob,
+                       const int32_t* idx, const float* stats, void* stream, int32_t* assign,
+                       int32_t* counts, float* metrics, float* l_common);
+
 /* Workspace bytes grkv_compress needs for this shape; 0 if the shape is
  * invalid or unsupported. */
 size_t grkv_workspace_bytes(const grkv_problem* prob, int64_t n,

@@ -17,7 +17,8 @@ __all__ = [
     "GRKV_ERR_HIP", "GrkvError", "lib", "lib_path", "Problem", "Options", "Outputs",
     "Layout", "workspace_bytes", "workspace_layout", "compress", "Result",
     "intermediates", "EXPORTED_SYMBOLS", "KeyOptions", "workspace_bytes_kv", "compress_kv",
-    "KEY_CONVERGED", "KEY_MAX_ITER", "KEY_SKIPPED", "KEY_BREAKDOWN",
+    "KEY_CONVERGED", "KEY_MAX_ITER", "KEY_SKIPPED", "KEY_BREAKDOWN", "carrier_stats",
+    "CARRIER_METRICS",
 ]
 
 GRKV_OK, GRKV_ERR_INVALID, GRKV_ERR_WORKSPACE, GRKV_ERR_UNSUPPORTED, GRKV_ERR_HIP = 0, -1, -2, -3, -4
@@ -27,8 +28,10 @@ STAGES = ("full_lse", "full_lse_combine", "full_prob", "full_y", "select", "gath
 NUM_STAGES = len(STAGES)
 EXPORTED_SYMBOLS = ("grkv_compress", "grkv_workspace_bytes", "grkv_workspace_layout",
                     "grkv_default_options", "grkv_status_string", "grkv_compress_kv",
-                    "grkv_workspace_bytes_kv", "grkv_default_key_options")
+                    "grkv_workspace_bytes_kv", "grkv_default_key_options", "grkv_carrier_stats")
 KEY_CONVERGED, KEY_MAX_ITER, KEY_SKIPPED, KEY_BREAKDOWN = 1, 2, 3, 4
+CARRIER_METRICS = ("b", "b_eff", "a_max", "gini", "boundary_fraction", "boundary_share",
+                   "enrichment", "boundary_interior_load")
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 
@@ -105,6 +108,11 @@ def lib() -> ctypes.CDLL:
                                               ctypes.c_int32, ctypes.c_int32]
         L.grkv_default_key_options.restype = None
         L.grkv_default_key_options.argtypes = [P(KeyOptions), ctypes.c_float]
+        L.grkv_carrier_stats.restype = ctypes.c_int
+        L.grkv_carrier_stats.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32,
+                                         P(Problem), ctypes.c_void_p, ctypes.c_void_p,
+                                         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                         ctypes.c_void_p, ctypes.c_void_p]
         L.grkv_status_string.restype = ctypes.c_char_p
         L.grkv_status_string.argtypes = [ctypes.c_int]
         _LIB = L
@@ -245,6 +253,43 @@ def compress_kv(q_obs, K, V, window: int, budget: int, pool_kernel: int, lam: fl
                                 ctypes.c_void_p(cg_info.data_ptr()))
     _check(st)
     return out, k_star, cg_info
+
+
+def carrier_stats(K, idx, group: int, stats=None, *, stream=None, assign=None, counts=None,
+                  metrics=None, l_common=None):
+    """Key-cosine carrier assignment and its load metrics (see grkv.h).
+
+    K [U, n, d] bfloat16 device tensor, idx [U, c] int32 (from ``compress``),
+    stats [U, 4] optional (gives L_common).  Returns ``(assign [U, n] int32,
+    counts [U, c] int32, metrics [U, 8] float32, l_common [1] float32 or None)``;
+    the metric columns are named in CARRIER_METRICS."""
+    import torch
+
+    if not (K.is_cuda and idx.is_cuda) or not K.is_contiguous() or not idx.is_contiguous():
+        raise ValueError("K and idx must be contiguous device tensors")
+    U, n, d = K.shape
+    c = idx.shape[1]
+    dt = GRKV_BF16 if K.dtype == torch.bfloat16 else GRKV_F32
+    dev = K.device
+    if assign is None:
+        assign = torch.empty((U, n), dtype=torch.int32, device=dev)
+    if counts is None:
+        counts = torch.empty((U, c), dtype=torch.int32, device=dev)
+    if metrics is None:
+        metrics = torch.empty((U, 8), dtype=torch.float32, device=dev)
+    if stats is not None and l_common is None:
+        l_common = torch.empty(1, dtype=torch.float32, device=dev)
+    if stream is None:
+        stream = torch.cuda.current_stream(dev)
+    handle = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+    prob = Problem(U, group, d, dt)
+    ptr = lambda t: None if t is None else ctypes.c_void_p(t.data_ptr())
+    st = lib().grkv_carrier_stats(K.data_ptr(), n, c, ctypes.byref(prob), idx.data_ptr(),
+                                  ptr(stats), ctypes.c_void_p(handle), assign.data_ptr(),
+                                  ptr(counts), metrics.data_ptr(),
+                                  ptr(l_common) if stats is not None else None)
+    _check(st)
+    return assign, counts, metrics, (l_common if stats is not None else None)
 
 
 def intermediates(res: Result) -> dict:

@@ -453,4 +453,18 @@ int grkv_compress_kv(const void* q_obs, const void* K, const void* V, int64_t n,
   return GRKV_OK;
 }
 
+int grkv_carrier_stats(const void* K, int64_t n, int32_t budget, const grkv_problem* prob,
+                       const int32_t* idx, const float* stats, void* stream, int32_t* assign,
+                       int32_t* counts, float* metrics, float* l_common) {
+  if (!K || !prob || !idx || !assign || !metrics) return GRKV_ERR_INVALID;
+  if (prob->units < 1 || prob->group < 1) return GRKV_ERR_INVALID;
+  if (prob->dtype != GRKV_BF16 && prob->dtype != GRKV_F32) return GRKV_ERR_INVALID;
+  if (budget < 1 || (int64_t)budget > n || n > (int64_t(1) << 30)) return GRKV_ERR_INVALID;
+  if (!carrier_supported(prob->dtype, prob->head_dim, budget)) return GRKV_ERR_UNSUPPORTED;
+  if (launch_carrier(K, idx, prob->units, n, budget, prob->head_dim, stats, assign, counts,
+                     metrics, l_common, (hipStream_t)stream) != hipSuccess)
+    return GRKV_ERR_HIP;
+  return GRKV_OK;
+}
+
 }  // extern "C"

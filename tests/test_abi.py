@@ -142,3 +142,22 @@ def test_key_step_workspace_and_defaults(L):
     ko = G.KeyOptions()
     L.grkv_default_key_options(ctypes.byref(ko), ctypes.c_float(0.25))
     assert (ko.lambda_k, ko.max_iter, ko.steps) == (0.25, 64, 1) and abs(ko.tol - 1e-5) < 1e-12
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(nullk=True), G.GRKV_ERR_INVALID),
+    (dict(c=0), G.GRKV_ERR_INVALID),
+    (dict(c=9000, n=8192), G.GRKV_ERR_INVALID),
+    (dict(dt=1), G.GRKV_ERR_UNSUPPORTED),
+    (dict(d=96), G.GRKV_ERR_UNSUPPORTED),
+    (dict(c=8193, n=20000), G.GRKV_ERR_UNSUPPORTED),
+    (dict(U=0), G.GRKV_ERR_INVALID),
+])
+def test_carrier_stats_invalid_arguments_rejected_before_launch(L, kw, code):
+    a = dict(U=2, Gq=4, d=128, dt=0, n=8192, c=512, nullk=False)
+    a.update(kw)
+    prob = G.Problem(a["U"], a["Gq"], a["d"], a["dt"])
+    fake = ctypes.c_void_p(4096)   # never dereferenced: validation fails first
+    st = L.grkv_carrier_stats(None if a["nullk"] else fake, a["n"], a["c"], ctypes.byref(prob),
+                              fake, None, None, fake, None, fake, None)
+    assert st == code
