@@ -215,6 +215,49 @@ size_t grkv_workspace_bytes_kv(const grkv_problem* prob, int64_t n,
 /* The default key options for a value ridge coefficient lambda. */
 void grkv_default_key_options(grkv_key_options* kopt, float lambda);
 
+/* Per-unit (ragged) budgets: the back-ends the paper pairs GRKV with (Sec. 4,
+ * compatibility) differ in how much of the cache each unit keeps (PyramidKV
+ * per layer, Ada-KV per head); the merge is unchanged.  grkv_compress_ragged
+ * compresses unit u exactly as grkv_compress would with budget budgets[u]
+ * (w <= budgets[u] <= n; the fixed set uses floor(beta * budgets[u])).
+ *   budgets  int32 [U], HOST memory
+ *   out      packed outputs: idx int32 [sum c_u], k_out dtype [sum c_u][d],
+ *            v_out float [sum c_u][d], unit u starting at slot
+ *            off_u = budgets[0] + ... + budgets[u-1]; stats [U][4] as before;
+ *            out->stage_events is ignored
+ * Consecutive units with equal budgets run as one batch, so a budget per
+ * layer costs one batched call per layer.  The workspace is
+ * grkv_workspace_bytes_ragged(); errors as for grkv_compress. */
+int grkv_compress_ragged(const void* q_obs, const void* K, const void* V, int64_t n,
+                         int32_t window, const int32_t* budgets, int32_t pool_kernel,
+                         float lambda, void* stream, const grkv_problem* prob,
+                         const grkv_options* opt, const grkv_outputs* out);
+
+size_t grkv_workspace_bytes_ragged(const grkv_problem* prob, int64_t n, int32_t window,
+                                   const int32_t* budgets);
+
+/* Pyramid schedule (PyramidKV: lower layers keep more of the cache, higher
+ * layers less): budgets fall linearly from (2 - ratio) * mean_budget at layer
+ * 0 to ratio * mean_budget at the top layer, rounded to nearest, clipped to
+ * [window, n], with the rounding remainder given to the lowest layers so that
+ * the layers' mean stays mean_budget where the clip allows.  Every head of a
+ * layer gets the layer's budget; units are layer-major (u = layer * kv_heads
+ * + head).  budgets: int32 [layers * kv_heads], HOST memory.  ratio in [0, 1];
+ * errors: GRKV_ERR_INVALID. */
+int grkv_pyramid_budgets(int32_t layers, int32_t kv_heads, int32_t mean_budget, int32_t window,
+                         int64_t n, float ratio, int32_t* budgets);
+
+/* Adaptive per-head budgets (Ada-KV: heads that need long-range context keep
+ * more): inside each layer the kv_heads heads share kv_heads * (budget - w)
+ * selected tokens, taken as the highest pooled scores over all its heads (ties
+ * to the lower head, then the lower position); head h gets w plus the number
+ * of its tokens taken.  pooled: float [U][n - w] device memory, the pooled
+ * scores of a grkv_compress call (grkv_workspace_layout().pooled); budgets:
+ * int32 [U] device memory, written asynchronously on stream.  kv_heads <= 128.
+ * Errors: GRKV_ERR_INVALID, GRKV_ERR_UNSUPPORTED, GRKV_ERR_HIP. */
+int grkv_adaptive_budgets(const float* pooled, int32_t layers, int32_t kv_heads, int64_t n,
+                          int32_t window, int32_t budget, void* stream, int32_t* budgets);
+
 /* Carrier concentration of a local merge rule (App. B, "Quantitative Carrier
  * Concentration"; Sec. 1): the diagnostic the paper uses to show that, after
  * span-based eviction, a key-similarity matcher (as in D2O/KVMerger) loads a

@@ -18,7 +18,7 @@ __all__ = [
     "Layout", "workspace_bytes", "workspace_layout", "compress", "Result",
     "intermediates", "EXPORTED_SYMBOLS", "KeyOptions", "workspace_bytes_kv", "compress_kv",
     "KEY_CONVERGED", "KEY_MAX_ITER", "KEY_SKIPPED", "KEY_BREAKDOWN", "carrier_stats",
-    "CARRIER_METRICS",
+    "CARRIER_METRICS", "compress_ragged", "pyramid_budgets", "adaptive_budgets",
 ]
 
 GRKV_OK, GRKV_ERR_INVALID, GRKV_ERR_WORKSPACE, GRKV_ERR_UNSUPPORTED, GRKV_ERR_HIP = 0, -1, -2, -3, -4
@@ -28,7 +28,9 @@ STAGES = ("full_lse", "full_lse_combine", "full_prob", "full_y", "select", "gath
 NUM_STAGES = len(STAGES)
 EXPORTED_SYMBOLS = ("grkv_compress", "grkv_workspace_bytes", "grkv_workspace_layout",
                     "grkv_default_options", "grkv_status_string", "grkv_compress_kv",
-                    "grkv_workspace_bytes_kv", "grkv_default_key_options", "grkv_carrier_stats")
+                    "grkv_workspace_bytes_kv", "grkv_default_key_options", "grkv_carrier_stats",
+                    "grkv_compress_ragged", "grkv_workspace_bytes_ragged", "grkv_pyramid_budgets",
+                    "grkv_adaptive_budgets")
 KEY_CONVERGED, KEY_MAX_ITER, KEY_SKIPPED, KEY_BREAKDOWN = 1, 2, 3, 4
 CARRIER_METRICS = ("b", "b_eff", "a_max", "gini", "boundary_fraction", "boundary_share",
                    "enrichment", "boundary_interior_load")
@@ -113,6 +115,22 @@ def lib() -> ctypes.CDLL:
                                          P(Problem), ctypes.c_void_p, ctypes.c_void_p,
                                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                          ctypes.c_void_p, ctypes.c_void_p]
+        L.grkv_compress_ragged.restype = ctypes.c_int
+        L.grkv_compress_ragged.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                           ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p,
+                                           ctypes.c_int32, ctypes.c_float, ctypes.c_void_p,
+                                           P(Problem), P(Options), P(Outputs)]
+        L.grkv_workspace_bytes_ragged.restype = ctypes.c_size_t
+        L.grkv_workspace_bytes_ragged.argtypes = [P(Problem), ctypes.c_int64, ctypes.c_int32,
+                                                  ctypes.c_void_p]
+        L.grkv_pyramid_budgets.restype = ctypes.c_int
+        L.grkv_pyramid_budgets.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+                                           ctypes.c_int32, ctypes.c_int64, ctypes.c_float,
+                                           ctypes.c_void_p]
+        L.grkv_adaptive_budgets.restype = ctypes.c_int
+        L.grkv_adaptive_budgets.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                                            ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                            ctypes.c_void_p, ctypes.c_void_p]
         L.grkv_status_string.restype = ctypes.c_char_p
         L.grkv_status_string.argtypes = [ctypes.c_int]
         _LIB = L
@@ -290,6 +308,79 @@ def carrier_stats(K, idx, group: int, stats=None, *, stream=None, assign=None, c
                                   ptr(l_common) if stats is not None else None)
     _check(st)
     return assign, counts, metrics, (l_common if stats is not None else None)
+
+
+def pyramid_budgets(layers: int, kv_heads: int, mean_budget: int, window: int, n: int,
+                    ratio: float = 0.5):
+    """Per-unit budgets (numpy int32 [layers * kv_heads]) of the pyramid schedule."""
+    import numpy as np
+    out = np.empty(layers * kv_heads, dtype=np.int32)
+    _check(lib().grkv_pyramid_budgets(layers, kv_heads, mean_budget, window, n, float(ratio),
+                                      out.ctypes.data_as(ctypes.c_void_p)))
+    return out
+
+
+def adaptive_budgets(pooled, layers: int, kv_heads: int, budget: int, window: int, *,
+                     stream=None, out=None):
+    """Per-unit budgets (int32 device tensor [U]) from the pooled scores [U, n - w]
+    of a ``compress`` call (see ``intermediates``)."""
+    import torch
+
+    if not pooled.is_cuda or pooled.dtype != torch.float32 or not pooled.is_contiguous():
+        raise ValueError("pooled must be a contiguous float32 device tensor")
+    U, P = pooled.shape
+    n = P + window
+    if out is None:
+        out = torch.empty(U, dtype=torch.int32, device=pooled.device)
+    if stream is None:
+        stream = torch.cuda.current_stream(pooled.device)
+    handle = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+    _check(lib().grkv_adaptive_budgets(ctypes.c_void_p(pooled.data_ptr()), layers, kv_heads, n,
+                                       window, budget, ctypes.c_void_p(handle),
+                                       ctypes.c_void_p(out.data_ptr())))
+    return out
+
+
+def compress_ragged(q_obs, K, V, window: int, budgets, pool_kernel: int, lam: float, *,
+                    n_sink: int = 4, beta: float = 0.10, fix_window: bool = True,
+                    causal_window: bool = True, stream=None, workspace=None):
+    """Every unit compressed with its own budget (``budgets``: host sequence of U
+    ints).  Returns ``(idx, k_out, v_out, stats, offsets)`` with the packed
+    layout of grkv.h (unit u at slots offsets[u] .. offsets[u] + budgets[u])."""
+    import numpy as np
+    import torch
+
+    if not (q_obs.is_cuda and K.is_cuda and V.is_cuda):
+        raise ValueError("q_obs, K and V must be device tensors")
+    U, G, w, d = q_obs.shape
+    n = K.shape[1]
+    b = np.ascontiguousarray(np.asarray(budgets, dtype=np.int32))
+    if b.shape != (U,) or w != window:
+        raise ValueError("budgets must hold one budget per unit")
+    dt = GRKV_BF16 if K.dtype == torch.bfloat16 else GRKV_F32
+    prob = Problem(U, G, d, dt)
+    need = int(lib().grkv_workspace_bytes_ragged(ctypes.byref(prob), n, window,
+                                                 b.ctypes.data_as(ctypes.c_void_p)))
+    dev = K.device
+    if workspace is None or workspace.numel() < max(need, 256):
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+    tot = int(b.sum())
+    idx = torch.empty(tot, dtype=torch.int32, device=dev)
+    k_out = torch.empty((tot, d), dtype=K.dtype, device=dev)
+    v_out = torch.empty((tot, d), dtype=torch.float32, device=dev)
+    stats = torch.empty((U, 4), dtype=torch.float32, device=dev)
+    opt = Options(n_sink, beta, 1 if fix_window else 0, 1 if causal_window else 0)
+    outs = Outputs(idx.data_ptr(), k_out.data_ptr(), v_out.data_ptr(), stats.data_ptr(),
+                   workspace.data_ptr(), workspace.numel(), None)
+    if stream is None:
+        stream = torch.cuda.current_stream(dev)
+    handle = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+    _check(lib().grkv_compress_ragged(q_obs.data_ptr(), K.data_ptr(), V.data_ptr(), n, window,
+                                      b.ctypes.data_as(ctypes.c_void_p), pool_kernel, float(lam),
+                                      ctypes.c_void_p(handle), ctypes.byref(prob),
+                                      ctypes.byref(opt), ctypes.byref(outs)))
+    offsets = np.concatenate([[0], np.cumsum(b)[:-1]]).astype(np.int64)
+    return idx, k_out, v_out, stats, offsets
 
 
 def intermediates(res: Result) -> dict:

@@ -453,6 +453,123 @@ int grkv_compress_kv(const void* q_obs, const void* K, const void* V, int64_t n,
   return GRKV_OK;
 }
 
+int grkv_pyramid_budgets(int32_t layers, int32_t kv_heads, int32_t mean_budget, int32_t window,
+                         int64_t n, float ratio, int32_t* budgets) {
+  if (layers < 1 || kv_heads < 1 || !budgets || window < 1 || mean_budget < window ||
+      (int64_t)mean_budget > n || !(ratio >= 0.f && ratio <= 1.f))
+    return GRKV_ERR_INVALID;
+  const int L = layers;
+  int64_t* per = (int64_t*)malloc(sizeof(int64_t) * L);   // host scratch of the schedule
+  if (!per) return GRKV_ERR_INVALID;
+  if (L == 1) {
+    per[0] = mean_budget;
+  } else {
+    const double top = (double)ratio * mean_budget, bot = (2.0 - (double)ratio) * mean_budget;
+    int64_t sum = 0;
+    for (int l = 0; l < L; ++l) {
+      const double raw = bot + (top - bot) * (double)l / (double)(L - 1);
+      int64_t b = (int64_t)floor(raw + 0.5);
+      b = b < window ? window : b > n ? n : b;
+      per[l] = b;
+      sum += b;
+    }
+    // rounding remainder to the lowest layers, one token each, within [w, n]
+    int64_t diff = (int64_t)L * mean_budget - sum;
+    for (int i = 0; diff != 0 && i < 4 * L; ++i) {
+      const int j = i % L;
+      const int64_t step = diff > 0 ? 1 : -1;
+      if (per[j] + step >= window && per[j] + step <= n) {
+        per[j] += step;
+        diff -= step;
+      }
+    }
+  }
+  for (int l = 0; l < L; ++l)
+    for (int h = 0; h < kv_heads; ++h) budgets[(size_t)l * kv_heads + h] = (int32_t)per[l];
+  free(per);
+  return GRKV_OK;
+}
+
+int grkv_adaptive_budgets(const float* pooled, int32_t layers, int32_t kv_heads, int64_t n,
+                          int32_t window, int32_t budget, void* stream, int32_t* budgets) {
+  if (!pooled || !budgets || layers < 1 || kv_heads < 1 || window < 1 || budget < window ||
+      (int64_t)budget > n)
+    return GRKV_ERR_INVALID;
+  if (kv_heads > 128) return GRKV_ERR_UNSUPPORTED;
+  const int64_t P = n - window;
+  if (P < 1 || (int64_t)kv_heads * P > (int64_t(1) << 31)) return GRKV_ERR_UNSUPPORTED;
+  const int64_t kk = (int64_t)kv_heads * (budget - window);
+  if (launch_adaptive_budgets(pooled, layers, kv_heads, (int)P, kk, window, budgets,
+                              (hipStream_t)stream) != hipSuccess)
+    return GRKV_ERR_HIP;
+  return GRKV_OK;
+}
+
+// Runs of consecutive units with one budget; the plan of each run.
+static int ragged_runs(const grkv_problem* prob, int64_t n, int32_t window,
+                       const int32_t* budgets, int32_t pool_kernel, float lambda,
+                       const grkv_options* opt, size_t* ws_max) {
+  if (!prob || !budgets || prob->units < 1) return GRKV_ERR_INVALID;
+  size_t mx = 0;
+  for (int u0 = 0; u0 < prob->units;) {
+    int u1 = u0 + 1;
+    while (u1 < prob->units && budgets[u1] == budgets[u0]) ++u1;
+    grkv_problem pr = *prob;
+    pr.units = u1 - u0;
+    Plan p;
+    const int st = make_plan(&pr, n, window, budgets[u0], pool_kernel, lambda, opt, &p);
+    if (st != GRKV_OK) return st;
+    mx = p.total > mx ? p.total : mx;
+    u0 = u1;
+  }
+  *ws_max = mx;
+  return GRKV_OK;
+}
+
+size_t grkv_workspace_bytes_ragged(const grkv_problem* prob, int64_t n, int32_t window,
+                                   const int32_t* budgets) {
+  size_t mx = 0;
+  if (ragged_runs(prob, n, window, budgets, 1, 0.f, nullptr, &mx) != GRKV_OK) return 0;
+  return mx;
+}
+
+int grkv_compress_ragged(const void* q_obs, const void* K, const void* V, int64_t n,
+                         int32_t window, const int32_t* budgets, int32_t pool_kernel,
+                         float lambda, void* stream, const grkv_problem* prob,
+                         const grkv_options* opt, const grkv_outputs* out) {
+  int st = check_pointers(q_obs, K, V, prob, out);
+  if (st != GRKV_OK) return st;
+  size_t need = 0;
+  st = ragged_runs(prob, n, window, budgets, pool_kernel, lambda, opt, &need);
+  if (st != GRKV_OK) return st;
+  if (out->workspace_bytes < need) return GRKV_ERR_WORKSPACE;
+  const size_t esz = prob->dtype == GRKV_BF16 ? 2 : 4;
+  const size_t m = (size_t)prob->group * window, d = prob->head_dim;
+  size_t off = 0;   // packed slot offset of unit u0
+  for (int u0 = 0; u0 < prob->units;) {
+    int u1 = u0 + 1;
+    while (u1 < prob->units && budgets[u1] == budgets[u0]) ++u1;
+    grkv_problem pr = *prob;
+    pr.units = u1 - u0;
+    Plan p;
+    st = make_plan(&pr, n, window, budgets[u0], pool_kernel, lambda, opt, &p);
+    if (st != GRKV_OK) return st;
+    grkv_outputs o = *out;
+    o.idx = out->idx + off;
+    o.k_out = (char*)out->k_out + off * d * esz;
+    o.v_out = out->v_out + off * d;
+    o.stats = out->stats ? out->stats + (size_t)4 * u0 : nullptr;
+    o.stage_events = nullptr;
+    st = run_compress(p, (const char*)q_obs + (size_t)u0 * m * d * esz,
+                      (const char*)K + (size_t)u0 * n * d * esz,
+                      (const char*)V + (size_t)u0 * n * d * esz, n, (hipStream_t)stream, &o);
+    if (st != GRKV_OK) return st;
+    off += (size_t)(u1 - u0) * budgets[u0];
+    u0 = u1;
+  }
+  return GRKV_OK;
+}
+
 int grkv_carrier_stats(const void* K, int64_t n, int32_t budget, const grkv_problem* prob,
                        const int32_t* idx, const float* stats, void* stream, int32_t* assign,
                        int32_t* counts, float* metrics, float* l_common) {

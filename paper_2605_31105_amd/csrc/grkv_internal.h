@@ -173,6 +173,10 @@ bool key_supported(const Plan& p);
 hipError_t launch_key(const Plan& p, const KeyPlan& kp, const KeyArgs& a, hipStream_t s);
 hipError_t launch_to_f32(const uint16_t* src, float* dst, size_t n, hipStream_t s);
 
+// Adaptive per-head budgets: one block per layer of H adjacent units.
+hipError_t launch_adaptive_budgets(const float* pooled, int layers, int H, int P, int64_t kk,
+                                   int w, int32_t* budgets, hipStream_t s);
+
 // Carrier-concentration diagnostics (bf16 keys, d 64/128, c <= 8192).
 bool carrier_supported(int dtype, int d, int c);
 hipError_t launch_carrier(const void* K, const int32_t* idx, int U, int64_t n, int c, int d,

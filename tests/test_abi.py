@@ -5,6 +5,7 @@ import math
 import os
 import re
 
+import numpy as np
 import pytest
 
 import paper_2605_31105_amd as G
@@ -161,3 +162,29 @@ def test_carrier_stats_invalid_arguments_rejected_before_launch(L, kw, code):
     st = L.grkv_carrier_stats(None if a["nullk"] else fake, a["n"], a["c"], ctypes.byref(prob),
                               fake, None, None, fake, None, fake, None)
     assert st == code
+
+
+@pytest.mark.parametrize("args", [(32, 8, 2048, 32, 32768, 0.5), (4, 2, 256, 32, 2048, 0.5),
+                                  (4, 1, 40, 32, 100, 0.1), (1, 4, 500, 16, 1000, 0.5),
+                                  (7, 3, 300, 8, 5000, 0.3)])
+def test_pyramid_budgets_match_the_oracle(L, args):
+    # a host function: no GPU needed
+    from oracle import grkv_frontend_oracle as FO
+    got = G.pyramid_budgets(*args)
+    want = FO.pyramid_budgets(*args[:5], ratio=args[5])
+    assert np.array_equal(got, want)
+
+
+def test_front_end_arguments_rejected(L):
+    out = (ctypes.c_int32 * 8)()
+    assert L.grkv_pyramid_budgets(0, 8, 100, 8, 1000, ctypes.c_float(0.5), out) == G.GRKV_ERR_INVALID
+    assert L.grkv_pyramid_budgets(2, 4, 4, 8, 1000, ctypes.c_float(0.5), out) == G.GRKV_ERR_INVALID
+    assert L.grkv_pyramid_budgets(2, 4, 100, 8, 1000, ctypes.c_float(1.5), out) == G.GRKV_ERR_INVALID
+    fake = ctypes.c_void_p(4096)
+    assert L.grkv_adaptive_budgets(fake, 1, 8, 1000, 8, 4, None, fake) == G.GRKV_ERR_INVALID
+    assert L.grkv_adaptive_budgets(fake, 1, 200, 1000, 8, 100, None, fake) == G.GRKV_ERR_UNSUPPORTED
+    prob = G.Problem(2, 4, 128, 0)
+    b = (ctypes.c_int32 * 2)(64, 16)   # second budget below the window
+    assert L.grkv_workspace_bytes_ragged(ctypes.byref(prob), 2048, 32, b) == 0
+    b = (ctypes.c_int32 * 2)(64, 128)
+    assert L.grkv_workspace_bytes_ragged(ctypes.byref(prob), 2048, 32, b) > 0
