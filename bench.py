@@ -51,6 +51,8 @@ def parse():
                     help="skip the one-call-per-layer measurement")
     ap.add_argument("--no-key-step", dest="key_step", action="store_false",
                     help="skip the key-step measurement (grkv_compress_kv)")
+    ap.add_argument("--no-front-ends", dest="front_ends", action="store_false",
+                    help="skip the ragged-budget front-end timings")
     ap.add_argument("--no-carrier", dest="carrier", action="store_false",
                     help="skip the carrier-concentration measurement")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -194,6 +196,47 @@ def carrier(args, cfg, G, hip, stream, Kd, res, host=None):
                      "frac": tflops / 2500.0, "traffic": None},
         "cpu_baseline": cpu,
     }
+
+
+def front_ends(args, cfg, G, hip, stream, qd, Kd, Vd, res):
+    """The budget front-ends on the same workload: ragged compression with the
+    pyramid schedule (mean budget c, top layer c / 2, bottom 3c / 2) and with
+    the adaptive per-head allocation computed on the GPU from the pooled scores
+    of the uniform call (the allocation kernel timed on its own)."""
+    import torch
+
+    U, w, c = cfg.units, cfg.window, cfg.budget
+    print("bench: budget front-ends", file=sys.stderr, flush=True)
+    reps = max(1, min(args.steps, 5))
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        a, b = hip.event(), hip.event()
+        hip.lib.hipEventRecord(a, ctypes.c_void_p(stream.cuda_stream))
+        for _ in range(reps):
+            fn()
+        hip.lib.hipEventRecord(b, ctypes.c_void_p(stream.cuda_stream))
+        torch.cuda.synchronize()
+        return hip.elapsed_ms(a, b) / reps
+
+    pooled = G.intermediates(res)["pooled"].contiguous().clone()
+    budgets = G.adaptive_budgets(pooled, cfg.layers, cfg.kv_heads, c, w)
+    ms_alloc = timed(lambda: G.adaptive_budgets(pooled, cfg.layers, cfg.kv_heads, c, w,
+                                                out=budgets))
+    out = {"adaptive_allocation_ms": ms_alloc}
+    for name, b in (("pyramid", G.pyramid_budgets(cfg.layers, cfg.kv_heads, c, w, cfg.n)),
+                    ("adaptive", budgets.cpu().numpy())):
+        dt = G.GRKV_BF16 if cfg.dtype == "bf16" else G.GRKV_F32
+        ws = torch.empty(max(256, G.workspace_bytes_ragged(U, cfg.group, cfg.head_dim, dt, cfg.n,
+                                                           w, b)), dtype=torch.uint8, device="cuda")
+        r = G.compress_ragged(qd, Kd, Vd, w, b, cfg.pool_kernel, cfg.lam, workspace=ws)
+        ms = timed(lambda: G.compress_ragged(qd, Kd, Vd, w, b, cfg.pool_kernel, cfg.lam,
+                                             workspace=ws, out=r))
+        out[name] = {"ms_per_call": ms, "heads_per_s": U / (ms / 1e3),
+                     "distinct_budgets": int(len(set(b.tolist()))),
+                     "budget_min": int(b.min()), "budget_max": int(b.max())}
+    return out
 
 
 def key_step(args, cfg, G, hip, stream, qd, Kd, Vd, host=None):
@@ -415,6 +458,8 @@ def main():
     car = (carrier(args, cfg, G, hip, stream, Kd, out, host=None if args.no_cpu_baseline else K)
            if args.carrier else None)
 
+    fe = front_ends(args, cfg, G, hip, stream, qd, Kd, Vd, out) if args.front_ends else None
+
     cpu = None
     if not args.no_cpu_baseline:
         print("bench: timing the oracle on the host", file=sys.stderr, flush=True)
@@ -449,6 +494,7 @@ def main():
                      "traffic": traffic},
         "key_step": key,
         "carrier": car,
+        "front_ends": fe,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

@@ -19,6 +19,7 @@ __all__ = [
     "intermediates", "EXPORTED_SYMBOLS", "KeyOptions", "workspace_bytes_kv", "compress_kv",
     "KEY_CONVERGED", "KEY_MAX_ITER", "KEY_SKIPPED", "KEY_BREAKDOWN", "carrier_stats",
     "CARRIER_METRICS", "compress_ragged", "pyramid_budgets", "adaptive_budgets",
+    "workspace_bytes_ragged",
 ]
 
 GRKV_OK, GRKV_ERR_INVALID, GRKV_ERR_WORKSPACE, GRKV_ERR_UNSUPPORTED, GRKV_ERR_HIP = 0, -1, -2, -3, -4
@@ -161,6 +162,14 @@ def workspace_layout(units, group, head_dim, dtype, n, window, budget) -> Layout
 def workspace_bytes_kv(units, group, head_dim, dtype, n, window, budget, steps=1) -> int:
     prob = Problem(units, group, head_dim, dtype)
     return int(lib().grkv_workspace_bytes_kv(ctypes.byref(prob), n, window, budget, steps))
+
+
+def workspace_bytes_ragged(units, group, head_dim, dtype, n, window, budgets) -> int:
+    import numpy as np
+    prob = Problem(units, group, head_dim, dtype)
+    b = np.ascontiguousarray(np.asarray(budgets, dtype=np.int32))
+    return int(lib().grkv_workspace_bytes_ragged(ctypes.byref(prob), n, window,
+                                                 b.ctypes.data_as(ctypes.c_void_p)))
 
 
 @dataclass
@@ -343,10 +352,12 @@ def adaptive_budgets(pooled, layers: int, kv_heads: int, budget: int, window: in
 
 def compress_ragged(q_obs, K, V, window: int, budgets, pool_kernel: int, lam: float, *,
                     n_sink: int = 4, beta: float = 0.10, fix_window: bool = True,
-                    causal_window: bool = True, stream=None, workspace=None):
+                    causal_window: bool = True, stream=None, workspace=None, out=None):
     """Every unit compressed with its own budget (``budgets``: host sequence of U
     ints).  Returns ``(idx, k_out, v_out, stats, offsets)`` with the packed
-    layout of grkv.h (unit u at slots offsets[u] .. offsets[u] + budgets[u])."""
+    layout of grkv.h (unit u at slots offsets[u] .. offsets[u] + budgets[u]).
+    ``out``: the first four of a previous call's results with the same budgets,
+    reused as the outputs."""
     import numpy as np
     import torch
 
@@ -365,10 +376,15 @@ def compress_ragged(q_obs, K, V, window: int, budgets, pool_kernel: int, lam: fl
     if workspace is None or workspace.numel() < max(need, 256):
         workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
     tot = int(b.sum())
-    idx = torch.empty(tot, dtype=torch.int32, device=dev)
-    k_out = torch.empty((tot, d), dtype=K.dtype, device=dev)
-    v_out = torch.empty((tot, d), dtype=torch.float32, device=dev)
-    stats = torch.empty((U, 4), dtype=torch.float32, device=dev)
+    if out is not None:
+        idx, k_out, v_out, stats = out[:4]
+        if idx.numel() != tot or k_out.shape != (tot, d) or stats.shape != (U, 4):
+            raise ValueError("out does not match the budgets")
+    else:
+        idx = torch.empty(tot, dtype=torch.int32, device=dev)
+        k_out = torch.empty((tot, d), dtype=K.dtype, device=dev)
+        v_out = torch.empty((tot, d), dtype=torch.float32, device=dev)
+        stats = torch.empty((U, 4), dtype=torch.float32, device=dev)
     opt = Options(n_sink, beta, 1 if fix_window else 0, 1 if causal_window else 0)
     outs = Outputs(idx.data_ptr(), k_out.data_ptr(), v_out.data_ptr(), stats.data_ptr(),
                    workspace.data_ptr(), workspace.numel(), None)

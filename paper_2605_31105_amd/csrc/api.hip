@@ -5,6 +5,8 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <vector>
+
 #include "grkv_internal.h"
 
 namespace grkv {
@@ -25,6 +27,8 @@ static void split_range(int64_t len, int64_t want, int64_t min_len, int* S, int*
   *chunk = (int)ch;
   *S = (int)(len > 0 ? ceil_div(len, ch) : 1);
 }
+
+static void layout_plan(Plan* p, size_t slots, size_t splits2, size_t splits3, size_t tab);
 
 int make_plan(const grkv_problem* prob, int64_t n, int32_t window, int32_t budget,
               int32_t pool_kernel, float lambda, const grkv_options* opt, Plan* p) {
@@ -89,7 +93,15 @@ int make_plan(const grkv_problem* prob, int64_t n, int32_t window, int32_t budge
     split_range(budget, ceil_div(256, p->U), 256, &p->S3, &p->chunk3);
   }
 
-  const size_t U = p->U, mp = p->mp, d = p->d, c = budget, P = p->prefix;
+  layout_plan(p, (size_t)p->U * budget, (size_t)p->U * p->S2, (size_t)p->U * p->S3, 0);
+  return GRKV_OK;
+}
+
+// Workspace offsets: `slots` retained slots and `splits2` / `splits3`
+// retained-pass and Gram partial blocks over all units, then `tab` bytes of
+// ragged tables.
+static void layout_plan(Plan* p, size_t slots, size_t splits2, size_t splits3, size_t tab) {
+  const size_t U = p->U, mp = p->mp, d = p->d, P = p->prefix;
   const size_t esz = p->dtype == GRKV_BF16 ? 2 : 4;
   size_t off = 0;
   auto take = [&](size_t bytes) { size_t o2 = off; off = align256(off + bytes); return o2; };
@@ -101,28 +113,28 @@ int make_plan(const grkv_problem* prob, int64_t n, int32_t window, int32_t budge
   p->y = take(U * mp * d * sizeof(float));
   p->colsum = take(U * (P > 0 ? P : 1) * sizeof(float));
   p->pooled = take(U * (P > 0 ? P : 1) * sizeof(float));
-  p->fixed = take(U * c);
+  p->fixed = take(slots);
   p->redo = take(U * p->S1 * sizeof(int32_t));
   // the compact V0 copy serves the generic retained passes only; the fast
   // path reads V0 rows through idx
   const bool fast_path = stream_supported(*p) && merge_fast_supported(*p);
-  p->v0c = take(fast_path ? 0 : U * c * d * esz);
-  p->pmax2 = take(U * p->S2 * mp * sizeof(float));
-  p->psum2 = take(U * p->S2 * mp * sizeof(double));
+  p->v0c = take(fast_path ? 0 : slots * d * esz);
+  p->pmax2 = take(splits2 * mp * sizeof(float));
+  p->psum2 = take(splits2 * mp * sizeof(double));
   p->lse2 = take(U * mp * sizeof(double));
   p->lse2_log2 = take(U * mp * sizeof(float));
-  p->xvpart = take(U * p->S2 * mp * d * sizeof(float));
-  p->x = take(p->fast_merge ? 0 : U * mp * c * sizeof(float));   // generic path only
+  p->xvpart = take(splits2 * mp * d * sizeof(float));
+  p->x = take(p->fast_merge ? 0 : mp * slots * sizeof(float));   // generic path only
   p->resid = take(U * mp * d * sizeof(float));
-  p->npart = take(U * p->S3 * mp * mp * sizeof(float));
-  p->mpart = take(fast_path ? U * p->S2 * mp * sizeof(float) : 0);
+  p->npart = take(splits3 * mp * mp * sizeof(float));
+  p->mpart = take(fast_path ? splits2 * mp * sizeof(float) : 0);
   p->gram = take(U * mp * mp * sizeof(float));
   p->z = take(U * d * mp * sizeof(float));
   p->zhi = take(U * d * mp * 2);
   p->zlo = take(U * d * mp * 2);
   p->stats_ws = take(U * 4 * sizeof(float));
+  p->rag_tab = take(tab);
   p->total = off;
-  return GRKV_OK;
 }
 
 // Workspace of the key step, after the compress workspace.  A key-pass block
@@ -505,7 +517,68 @@ int grkv_adaptive_budgets(const float* pooled, int32_t layers, int32_t kv_heads,
   return GRKV_OK;
 }
 
-// Runs of consecutive units with one budget; the plan of each run.
+// Native ragged plan (bf16 fast path): the budget-independent passes as for
+// one budget; the retained pass in splits of one length over each unit's own
+// budget, the update in blocks of one slot count, both as flat grids whose
+// blocks find their unit in device tables.  `tab` receives the tables
+// (RagUnit [U], the unit of every retained-pass block, the unit of every
+// update block) for the caller to copy into the workspace.  *native is false
+// when the shape takes the generic path (one call per run of equal budgets).
+static int make_ragged_plan(const grkv_problem* prob, int64_t n, int32_t window,
+                            const int32_t* budgets, int32_t pool_kernel, float lambda,
+                            const grkv_options* opt, Plan* p, std::vector<int32_t>* tab,
+                            bool* native) {
+  *native = false;
+  if (!prob || !budgets || prob->units < 1) return GRKV_ERR_INVALID;
+  const int U = prob->units;
+  int64_t sum = 0;
+  int cmax = 0;
+  for (int u = 0; u < U; ++u) {
+    if (budgets[u] < window || (int64_t)budgets[u] > n || window < 1) return GRKV_ERR_INVALID;
+    sum += budgets[u];
+    cmax = budgets[u] > cmax ? budgets[u] : cmax;
+  }
+  if (sum > INT32_MAX) return GRKV_ERR_UNSUPPORTED;   // packed slot offsets are int32
+  int cmean = (int)((sum + U / 2) / U);
+  if (cmean < window) cmean = window;
+  if (cmean > n) cmean = (int)n;
+  const int st = make_plan(prob, n, window, cmean, pool_kernel, lambda, opt, p);
+  if (st != GRKV_OK) return st;
+  if (!(stream_supported(*p) && p->fast_merge)) return GRKV_OK;
+  const int chunk = p->chunk2, spb = update_slots_per_block(*p, cmean);
+  std::vector<int32_t> split_unit, upd_unit;
+  tab->assign((size_t)8 * U, 0);
+  int64_t off = 0;
+  for (int u = 0; u < U; ++u) {
+    const int c = budgets[u];
+    RagUnit r;
+    r.off = (int32_t)off;
+    r.c = c;
+    r.s0 = (int32_t)split_unit.size();
+    r.ns = (c + chunk - 1) / chunk;
+    const int64_t top = (int64_t)floor((double)p->opt.beta * (double)c);
+    r.ntop = (int32_t)(top < c - window ? top : c - window);
+    r.ub0 = (int32_t)upd_unit.size();
+    r.nub = (c + spb - 1) / spb;
+    r.pad = 0;
+    split_unit.insert(split_unit.end(), r.ns, u);
+    upd_unit.insert(upd_unit.end(), r.nub, u);
+    memcpy(tab->data() + (size_t)8 * u, &r, sizeof(r));
+    off += c;
+  }
+  p->rag_splits = (int)split_unit.size();
+  p->rag_upd_blocks = (int)upd_unit.size();
+  p->upd_spb = spb;
+  tab->insert(tab->end(), split_unit.begin(), split_unit.end());
+  tab->insert(tab->end(), upd_unit.begin(), upd_unit.end());
+  p->c = cmax;
+  p->s_sel = cmax - window;
+  layout_plan(p, (size_t)sum, split_unit.size(), split_unit.size(), tab->size() * sizeof(int32_t));
+  *native = true;
+  return GRKV_OK;
+}
+
+// Runs of consecutive units with one budget (generic path); the largest plan.
 static int ragged_runs(const grkv_problem* prob, int64_t n, int32_t window,
                        const int32_t* budgets, int32_t pool_kernel, float lambda,
                        const grkv_options* opt, size_t* ws_max) {
@@ -528,6 +601,12 @@ static int ragged_runs(const grkv_problem* prob, int64_t n, int32_t window,
 
 size_t grkv_workspace_bytes_ragged(const grkv_problem* prob, int64_t n, int32_t window,
                                    const int32_t* budgets) {
+  Plan p;
+  std::vector<int32_t> tab;
+  bool native = false;
+  if (make_ragged_plan(prob, n, window, budgets, 1, 0.f, nullptr, &p, &tab, &native) != GRKV_OK)
+    return 0;
+  if (native) return p.total;
   size_t mx = 0;
   if (ragged_runs(prob, n, window, budgets, 1, 0.f, nullptr, &mx) != GRKV_OK) return 0;
   return mx;
@@ -539,6 +618,25 @@ int grkv_compress_ragged(const void* q_obs, const void* K, const void* V, int64_
                          const grkv_options* opt, const grkv_outputs* out) {
   int st = check_pointers(q_obs, K, V, prob, out);
   if (st != GRKV_OK) return st;
+  Plan rp;
+  std::vector<int32_t> tab;
+  bool native = false;
+  st = make_ragged_plan(prob, n, window, budgets, pool_kernel, lambda, opt, &rp, &tab, &native);
+  if (st != GRKV_OK) return st;
+  if (native) {
+    // one launch per stage over every unit; the tables go into the workspace
+    // first (a pageable-memory copy: the host array is consumed on return)
+    if (out->workspace_bytes < rp.total) return GRKV_ERR_WORKSPACE;
+    char* ws = (char*)out->workspace;
+    int32_t* dt = (int32_t*)(ws + rp.rag_tab);
+    if (hipMemcpyAsync(dt, tab.data(), tab.size() * sizeof(int32_t), hipMemcpyHostToDevice,
+                       (hipStream_t)stream) != hipSuccess)
+      return GRKV_ERR_HIP;
+    rp.rag = (const RagUnit*)dt;
+    rp.rag_split_unit = dt + (size_t)8 * rp.U;
+    rp.rag_upd_unit = rp.rag_split_unit + rp.rag_splits;
+    return run_compress(rp, q_obs, K, V, n, (hipStream_t)stream, out);
+  }
   size_t need = 0;
   st = ragged_runs(prob, n, window, budgets, pool_kernel, lambda, opt, &need);
   if (st != GRKV_OK) return st;

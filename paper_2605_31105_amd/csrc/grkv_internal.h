@@ -18,6 +18,15 @@ constexpr int kSelectThreads = 1024;
 // well inside the float range (P <= 2^48, Gram entries <= 2^96).
 constexpr float kRetainedBias = 48.f;
 
+// Ragged budgets: one entry per unit, in device memory.  The packed outputs
+// hold unit u's c slots from slot `off`; its retained-pass splits are the
+// flat blocks s0 .. s0 + ns - 1 (their partials are indexed by the flat block
+// number), its update blocks ub0 .. ub0 + nub - 1; ntop is the size of its
+// score-ranked fixed subset, min(floor(beta c), c - w).
+struct RagUnit {
+  int32_t off, c, s0, ns, ntop, ub0, nub, pad;
+};
+
 // Everything a call needs, derived on the host from the arguments.
 struct Plan {
   // shape
@@ -34,9 +43,17 @@ struct Plan {
   // on the fast value-step path, where that pass produces the Gram partials)
   int S3, chunk3;
   bool fast_merge;
+  // ragged budgets (bf16 fast path): device tables, null for one budget.
+  // p.c is then the largest budget, chunk2 the uniform split length of the
+  // retained pass and upd_spb the slots per update block.
+  const RagUnit* rag;
+  const int32_t* rag_split_unit;   // [rag_splits] unit of each retained-pass block
+  const int32_t* rag_upd_unit;     // [rag_upd_blocks] unit of each update block
+  int rag_splits, rag_upd_blocks, upd_spb;
   // workspace offsets (bytes)
   size_t pmax1, psum1, lse1, lse1_log2, ypart, y, colsum, pooled, fixed, v0c, redo;
   size_t pmax2, psum2, lse2, lse2_log2, xvpart, x, resid, npart, mpart, gram, z, zhi, zlo, stats_ws;
+  size_t rag_tab;   // ragged tables: RagUnit [U], then the two block-to-unit maps
   size_t total;
 };
 
@@ -117,6 +134,8 @@ hipError_t launch_solve(const Plan& p, const float* ypart, const float* xvpart,
                         float* stats_ws, float* stats_user, hipStream_t s);
 // X is recomputed from q_obs, K0 (k_out) and the retained log-sum-exp; V0
 // rows are read from V [U][n][d] through idx.
+// Slots per update block for budget c (blocks per unit = ceil(c / spb)).
+int update_slots_per_block(const Plan& p, int c);
 hipError_t launch_update(const Plan& p, const void* q, const void* k0,
                          const float* lse_log2, const uint8_t* fixed,
                          const uint16_t* zhi, const uint16_t* zlo,

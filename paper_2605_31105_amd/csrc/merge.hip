@@ -205,7 +205,7 @@ __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
     const float* ypart, int S1, const float* xvpart, int S2, const float* npart, int S3,
     const float* mpart, const float* lse1_log2, float lse_bias, float* lse2_log2,
     float* y, float* resid, float* gram, float* z, u16* zhi, u16* zlo, float* stats_ws,
-    float* stats_user, int m, float lam) {
+    float* stats_user, int m, float lam, const RagUnit* rag) {
   constexpr int NP = MP / 16;   // panels
   constexpr int NC = D / 16;    // 16-column tiles of the right-hand side
   constexpr int AS = MP + 4;    // LDS row strides (floats); 16-byte aligned rows
@@ -221,6 +221,14 @@ __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
 
   const int u = blockIdx.x, tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, l16 = lane & 15, g = lane >> 4;
+  // this unit's retained-pass partials: splits sp0 .. sp0 + S2 - 1 (with
+  // ragged budgets a unit's own split count, indexed by flat block)
+  size_t sp0 = (size_t)u * S2, sp3 = (size_t)u * S3;
+  if (rag) {
+    const RagUnit ru = rag[u];
+    sp0 = sp3 = (size_t)ru.s0;
+    S2 = S3 = ru.ns;
+  }
   if (tid == 0) fail = range_fail = 0;
   __syncthreads();
 
@@ -233,7 +241,7 @@ __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
     float inv = 1.f;
     if (mpart) {
       float ms = 0.f;
-      for (int s2 = 0; s2 < S2; ++s2) ms += mpart[((size_t)u * S2 + s2) * MP + r];
+      for (int s2 = 0; s2 < S2; ++s2) ms += mpart[(sp0 + s2) * MP + r];
       inv = 0.f;
       if (r < m) {
         if (ms >= 0x1p-60f && ms < __builtin_huge_valf()) {
@@ -276,7 +284,7 @@ __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
   {
     constexpr int E = MP * D / 4;
     const float4* __restrict__ yp = reinterpret_cast<const float4*>(ypart) + (size_t)u * S1 * E;
-    const float4* __restrict__ xp = reinterpret_cast<const float4*>(xvpart) + (size_t)u * S2 * E;
+    const float4* __restrict__ xp = reinterpret_cast<const float4*>(xvpart) + sp0 * E;
     float4* __restrict__ yo = reinterpret_cast<float4*>(y) + (size_t)u * E;
     float4* __restrict__ ro = reinterpret_cast<float4*>(resid) + (size_t)u * E;
     for (int e0 = tid; e0 < E; e0 += 2 * NTH) {
@@ -307,7 +315,7 @@ __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
   }
   {
     constexpr int E = MP * MP / 4;
-    const float4* __restrict__ np = reinterpret_cast<const float4*>(npart) + (size_t)u * S3 * E;
+    const float4* __restrict__ np = reinterpret_cast<const float4*>(npart) + sp3 * E;
     float4* __restrict__ go = reinterpret_cast<float4*>(gram) + (size_t)u * E;
     for (int e2 = tid; e2 < E; e2 += 2 * NTH) {
      float4 v2[2] = {make_float4(0.f, 0.f, 0.f, 0.f), make_float4(0.f, 0.f, 0.f, 0.f)};
@@ -506,7 +514,8 @@ template <int MP, int D>
 __global__ __launch_bounds__(kUpdWaves * 64) void update_kernel(
     const u16* q, const u16* k0, const float* lse_log2, const uint8_t* fixed, const u16* zhi,
     const u16* zlo, const float* stats_ws, const u16* V, const int32_t* idx, int64_t n,
-    float* v_out, int m, int w, int c, int spb, int causal, float scale_log2) {
+    float* v_out, int m, int w, int c, int spb, int causal, float scale_log2, const RagUnit* rag,
+    const int32_t* upd_unit) {
   constexpr int QS = D + 8;    // LDS row stride (bf16) of Q rows
   constexpr int ZS = MP + 8;   // LDS row stride (bf16) of Z^T rows
   constexpr int DT = D / 16;   // output tiles per slot row
@@ -519,11 +528,22 @@ __global__ __launch_bounds__(kUpdWaves * 64) void update_kernel(
   float* nls = reinterpret_cast<float*>(zl + D * ZS);      // [MP] -LSE (log2 domain)
   int32_t* ps = reinterpret_cast<int32_t*>(nls + MP);      // [spb] source rows of the slots
   uint8_t* fl = reinterpret_cast<uint8_t*>(ps + spb);      // [spb] fixed flags
-  const int u = blockIdx.y, tid = threadIdx.x;
+  // unit, block within the unit and first slot (ragged budgets: a flat grid
+  // of update blocks, each unit's slots packed from its own offset)
+  int u = blockIdx.y, blk = blockIdx.x;
+  size_t slot0 = (size_t)blockIdx.y * c;
+  if (rag) {
+    u = upd_unit[blockIdx.x];
+    const RagUnit ru = rag[u];
+    blk = blockIdx.x - ru.ub0;
+    c = ru.c;
+    slot0 = (size_t)ru.off;
+  }
+  const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, l16 = lane & 15, g = lane >> 4;
   const bool singular = stats_ws[u * 4 + 3] != 0.f;
   const int win0 = c - w;   // first window slot of the retained set
-  const int s0 = blockIdx.x * spb;
+  const int s0 = blk * spb;
   const int s1 = min(c, s0 + spb);
 
   if (!singular) {
@@ -555,8 +575,8 @@ __global__ __launch_bounds__(kUpdWaves * 64) void update_kernel(
     for (int r = tid; r < MP; r += NTH) nls[r] = r < m ? -lse_log2[(size_t)u * MP + r] : NEG_INF;
   }
   for (int t = tid; t < s1 - s0; t += NTH) {
-    fl[t] = fixed[(size_t)u * c + s0 + t];
-    const int64_t r = idx[(size_t)u * c + s0 + t];
+    fl[t] = fixed[slot0 + s0 + t];
+    const int64_t r = idx[slot0 + s0 + t];
     ps[t] = (int32_t)(r < 0 ? 0 : r >= n ? n - 1 : r);   // in range by construction
   }
   __syncthreads();
@@ -565,7 +585,7 @@ __global__ __launch_bounds__(kUpdWaves * 64) void update_kernel(
 #pragma unroll
     for (int T = 0; T < 2; ++T) {
       const int t = tb + 16 * T + l16;
-      const u16* kr = k0 + ((size_t)u * c + (t < s1 ? t : s1 - 1)) * D;
+      const u16* kr = k0 + (slot0 + (t < s1 ? t : s1 - 1)) * D;
 #pragma unroll
       for (int ks = 0; ks < D / 32; ++ks) kb[T][ks] = *reinterpret_cast<const uint4*>(kr + ks * 32 + 8 * g);
     }
@@ -688,7 +708,7 @@ __global__ __launch_bounds__(kUpdWaves * 64) void update_kernel(
 #pragma unroll
           for (int dt = 0; dt < DT; ++dt) v[dt] += acc[T][dt][i];
         }
-        float* dst = v_out + ((size_t)u * c + ts) * D + l16 * DT;
+        float* dst = v_out + (slot0 + ts) * D + l16 * DT;
 #pragma unroll
         for (int k = 0; k < DT / 4; ++k)
           *reinterpret_cast<float4*>(dst + 4 * k) = make_float4(v[4 * k], v[4 * k + 1], v[4 * k + 2], v[4 * k + 3]);
@@ -712,7 +732,7 @@ hipError_t launch_solve_t(const Plan& p, const float* ypart, const float* xvpart
                           hipStream_t s) {
   hipLaunchKernelGGL((solve_kernel<MP, D>), dim3(p.U), dim3(kSolveWaves * 64), 0, s, ypart, p.S1,
                      xvpart, p.S2, npart, p.S3, mpart, lse1_log2, lse_bias, lse2_log2, y, resid,
-                     gram, z, zhi, zlo, stats_ws, stats_user, p.m, p.lam);
+                     gram, z, zhi, zlo, stats_ws, stats_user, p.m, p.lam, p.rag);
   return hipGetLastError();
 }
 
@@ -721,30 +741,38 @@ hipError_t launch_update_t(const Plan& p, const void* q, const void* k0, const f
                            const uint8_t* fixed, const u16* zhi, const u16* zlo,
                            const float* stats_ws, const u16* V, const int32_t* idx,
                            float* v_out, hipStream_t s) {
-  // about one block per compute unit: split a unit's slots over several
-  // blocks only when there are fewer units than that
-  const int pair_rows = 32 * kUpdWaves;
-  int bpu = (256 + p.U - 1) / p.U;
-  const int most = (p.c + pair_rows - 1) / pair_rows;
-  if (bpu > most) bpu = most;
-  const int least = (p.c + kUpdMaxSlots - 1) / kUpdMaxSlots;
-  if (bpu < least) bpu = least;
-  if (bpu < 1) bpu = 1;
-  int spb = (p.c + bpu - 1) / bpu;
-  spb = (spb + 31) / 32 * 32;
-  bpu = (p.c + spb - 1) / spb;
+  int spb = p.rag ? p.upd_spb : update_slots_per_block(p, p.c);
+  if (spb < 32 || spb > kUpdMaxSlots || (p.rag && (!p.rag_upd_unit || p.rag_upd_blocks < 1)))
+    return hipErrorInvalidValue;
+  const int bpu = (p.c + spb - 1) / spb;
   const size_t lds = update_lds_bytes<MP, D>(spb);
   hipError_t e = hipFuncSetAttribute((const void*)update_kernel<MP, D>,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   const float scale_log2 = (float)(1.4426950408889634 / __builtin_sqrt((double)D));
-  hipLaunchKernelGGL((update_kernel<MP, D>), dim3(bpu, p.U), dim3(kUpdWaves * 64), lds, s,
+  const dim3 grid = p.rag ? dim3(p.rag_upd_blocks, 1) : dim3(bpu, p.U);
+  hipLaunchKernelGGL((update_kernel<MP, D>), grid, dim3(kUpdWaves * 64), lds, s,
                      (const u16*)q, (const u16*)k0, lse_log2, fixed, zhi, zlo, stats_ws, V, idx,
-                     p.n, v_out, p.m, p.w, p.c, spb, p.opt.causal_window ? 1 : 0, scale_log2);
+                     p.n, v_out, p.m, p.w, p.c, spb, p.opt.causal_window ? 1 : 0, scale_log2,
+                     p.rag, p.rag_upd_unit);
   return hipGetLastError();
 }
 
 }  // namespace
+
+int update_slots_per_block(const Plan& p, int c) {
+  // about one block per compute unit: split a unit's slots over several
+  // blocks only when there are fewer units than that
+  const int pair_rows = 32 * kUpdWaves;
+  int bpu = (256 + p.U - 1) / p.U;
+  const int most = (c + pair_rows - 1) / pair_rows;
+  if (bpu > most) bpu = most;
+  const int least = (c + kUpdMaxSlots - 1) / kUpdMaxSlots;
+  if (bpu < least) bpu = least;
+  if (bpu < 1) bpu = 1;
+  int spb = (c + bpu - 1) / bpu;
+  return (spb + 31) / 32 * 32;
+}
 
 bool merge_fast_supported(const Plan& p) {
   return p.dtype == GRKV_BF16 && p.mp <= 128 && (p.d == 64 || p.d == 128);

@@ -24,7 +24,24 @@ struct SelK {
   uint8_t* fixed;
   int prefix, c, w, h, s_sel, n_top, n_sink, fix_window;
   int64_t n;
+  const RagUnit* rag;   // ragged budgets, or null (every unit keeps c)
 };
+
+// Budget, selection count, fixed-subset count and first output slot of unit u.
+struct UnitSel {
+  int c, s_sel, n_top;
+  size_t base;
+};
+__device__ __forceinline__ UnitSel unit_sel(const SelK& a, int u) {
+  UnitSel r;
+  if (a.rag) {
+    const RagUnit ru = a.rag[u];
+    r.c = ru.c; r.s_sel = ru.c - a.w; r.n_top = ru.ntop; r.base = (size_t)ru.off;
+  } else {
+    r.c = a.c; r.s_sel = a.s_sel; r.n_top = a.n_top; r.base = (size_t)u * a.c;
+  }
+  return r;
+}
 
 // Band of candidates around a threshold, as refine_boundary below describes
 // (that is the form for keys held in registers); here each thread scans the
@@ -121,8 +138,9 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(SelK a) {
   const int P = a.prefix;
   const float* s = a.colsum + (size_t)u * P;
   float* p = a.pooled + (size_t)u * P;
-  int32_t* idx = a.idx + (size_t)u * a.c;
-  uint8_t* fixed = a.fixed + (size_t)u * a.c;
+  const UnitSel us = unit_sel(a, u);
+  int32_t* idx = a.idx + us.base;
+  uint8_t* fixed = a.fixed + us.base;
 
   for (int j = tid; j < P; j += blockDim.x) {
     int lo = j - a.h < 0 ? 0 : j - a.h;
@@ -134,7 +152,7 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(SelK a) {
   __syncthreads();
 
   // radix select of the k-th largest for k = s_sel (target 0) and n_top (1)
-  uint32_t prefix[2] = {0u, 0u}, krem[2] = {(uint32_t)a.s_sel, (uint32_t)a.n_top};
+  uint32_t prefix[2] = {0u, 0u}, krem[2] = {(uint32_t)us.s_sel, (uint32_t)us.n_top};
   uint32_t mask = 0u;
   for (int shift = 24; shift >= 0; shift -= 8) {
     for (int b = tid; b < 512; b += blockDim.x) (&hist[0][0])[b] = 0u;
@@ -167,13 +185,13 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(SelK a) {
   // prefix[t] = bits of the k-th largest score; krem[t] = how many scores
   // equal to it are taken (lowest positions first); all larger ones are taken.
   const uint32_t T0 = prefix[0], T1 = prefix[1];
-  const bool any0 = a.s_sel > 0, any1 = a.n_top > 0;
+  const bool any0 = us.s_sel > 0, any1 = us.n_top > 0;
 
   const int per = (P + blockDim.x - 1) / blockDim.x;
   const int j0 = min(P, tid * per), j1 = min(P, j0 + per);
   BandRule r0 = {}, r1 = {};
-  if (any0) r0 = band_rule(p, T0, (uint32_t)a.s_sel, s, j0, j1, P, a.h, band_work[0], scan_scratch);
-  if (any1) r1 = band_rule(p, T1, (uint32_t)a.n_top, s, j0, j1, P, a.h, band_work[1], scan_scratch);
+  if (any0) r0 = band_rule(p, T0, (uint32_t)us.s_sel, s, j0, j1, P, a.h, band_work[0], scan_scratch);
+  if (any1) r1 = band_rule(p, T1, (uint32_t)us.n_top, s, j0, j1, P, a.h, band_work[1], scan_scratch);
   uint32_t nsel = 0;
   {
     uint32_t e0 = 0;
@@ -199,8 +217,8 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(SelK a) {
   }
   for (int i = tid; i < a.w; i += blockDim.x) {
     int64_t pos = a.n - a.w + i;
-    idx[a.s_sel + i] = (int32_t)pos;
-    fixed[a.s_sel + i] = (a.fix_window || pos < a.n_sink) ? 1 : 0;
+    idx[us.s_sel + i] = (int32_t)pos;
+    fixed[us.s_sel + i] = (a.fix_window || pos < a.n_sink) ? 1 : 0;
   }
 }
 
@@ -351,8 +369,9 @@ __global__ __launch_bounds__(kSmallThreads) void select_small_kernel(SelK a) {
   const int P = a.prefix;
   const float* s = a.colsum + (size_t)u * P;
   float* pg = a.pooled + (size_t)u * P;
-  int32_t* idx = a.idx + (size_t)u * a.c;
-  uint8_t* fixed = a.fixed + (size_t)u * a.c;
+  const UnitSel us = unit_sel(a, u);
+  int32_t* idx = a.idx + us.base;
+  uint8_t* fixed = a.fixed + us.base;
   const int j0 = tid * PER;
 
   // Scores of the whole prefix into LDS (coalesced), one pad word per 64
@@ -523,7 +542,7 @@ __global__ __launch_bounds__(kSmallThreads) void select_small_kernel(SelK a) {
     return b;
   };
 
-  const uint32_t k0 = (uint32_t)a.s_sel, k1 = (uint32_t)a.n_top;
+  const uint32_t k0 = (uint32_t)us.s_sel, k1 = (uint32_t)us.n_top;
   const bool any0 = k0 > 0, any1 = k1 > 0;
   // count(>= kmin) = P (the padding keys, 0, count only when kmin is 0)
   const uint32_t all = kmin > 0 ? (uint32_t)P : (uint32_t)(kSmallThreads * PER);
@@ -548,8 +567,8 @@ __global__ __launch_bounds__(kSmallThreads) void select_small_kernel(SelK a) {
   }
   for (int i = tid; i < a.w; i += kSmallThreads) {
     const int64_t pos = a.n - a.w + i;
-    idx[a.s_sel + i] = (int32_t)pos;
-    fixed[a.s_sel + i] = (a.fix_window || pos < a.n_sink) ? 1 : 0;
+    idx[us.s_sel + i] = (int32_t)pos;
+    fixed[us.s_sel + i] = (a.fix_window || pos < a.n_sink) ? 1 : 0;
   }
 }
 
@@ -591,6 +610,7 @@ hipError_t launch_select(const Plan& p, const float* colsum, float* pooled, int3
   a.prefix = p.prefix; a.c = p.c; a.w = p.w; a.h = (p.k_pool - 1) / 2;
   a.s_sel = p.s_sel; a.n_top = p.n_top_fixed; a.n_sink = p.opt.n_sink;
   a.fix_window = p.opt.fix_window ? 1 : 0; a.n = p.n;
+  a.rag = p.rag;
   if (p.prefix <= kSmallThreads * kSmallPer && p.k_pool <= 17)
     hipLaunchKernelGGL(select_small_kernel, dim3(p.U), dim3(kSmallThreads), 0, s, a);
   else

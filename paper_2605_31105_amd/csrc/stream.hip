@@ -66,6 +66,12 @@ struct StreamK {
   int64_t src_rows;
   int gather_k, gather_v;
   u16* kcopy;             // if set, every K tile is also copied to [U][nk][D]
+  // retained pass with ragged budgets (gathered rows only): a flat grid of
+  // splits; block f belongs to unit split_unit[f], whose entry in rag gives
+  // its slot count and first slot (the per-unit arrays kpos, fixed and kcopy
+  // are packed), and its partials are indexed by f
+  const RagUnit* rag;
+  const int32_t* split_unit;
 };
 
 constexpr int kTileElems = 4096;   // elements of one tensor per tile
@@ -276,6 +282,7 @@ struct Stream {
   const u16* kbase;
   const u16* vbase;
   int u, key0, key_end, ntiles, win0, lane, wave, l16, g;
+  size_t slot0;              // first slot of this unit in the per-slot arrays
   bool all_rows;             // m == mp: no padding rows to mask
   float (*colpart)[WAVES][TK];
   uint4* xg;                 // retained pass: fragment exchange [NT][2][64]
@@ -346,7 +353,7 @@ struct Stream {
       const int r = c / G::CPR, ch = c % G::CPR;
       const int key = tile0 + r;
       if (key < key_end)
-        *reinterpret_cast<uint4*>(a.kcopy + ((size_t)u * a.nk + key) * D + ch * 8) =
+        *reinterpret_cast<uint4*>(a.kcopy + (slot0 + key) * D + ch * 8) =
             *reinterpret_cast<const uint4*>(cur + swz<D>(r, ch));
     }
   }
@@ -759,18 +766,30 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : 2))) void stream_kerne
 
   if (MODE == kModeFullExact && !a.redo[(size_t)blockIdx.y * a.S + blockIdx.x]) return;
   Stream<D, WAVES, MODE, NSTAGE> sm{a};
+  // unit, split, key count and partial index of this block
+  int s = blockIdx.x, nk = a.nk;
+  size_t pidx = (size_t)blockIdx.y * a.S + blockIdx.x;
   sm.u = blockIdx.y;
-  const int s = blockIdx.x;
+  sm.slot0 = (size_t)blockIdx.y * a.nk;
+  if (RET && a.rag) {
+    const int f = blockIdx.x;
+    sm.u = a.split_unit[f];
+    const RagUnit ru = a.rag[sm.u];
+    s = f - ru.s0;
+    nk = ru.c;
+    sm.slot0 = (size_t)ru.off;
+    pidx = (size_t)f;
+  }
   sm.lane = threadIdx.x & 63;
   sm.wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
   sm.l16 = sm.lane & 15;
   sm.g = sm.lane >> 4;
   sm.key0 = s * a.chunk;
-  sm.key_end = min(sm.key0 + a.chunk, a.nk);
+  sm.key_end = min(sm.key0 + a.chunk, nk);
   sm.ntiles = sm.key_end > sm.key0 ? (sm.key_end - sm.key0 + TK - 1) / TK : 0;
-  sm.kbase = a.k + (size_t)sm.u * (a.gather_k ? a.src_rows : (int64_t)a.nk) * D;
-  sm.vbase = a.v + (size_t)sm.u * (a.gather_v ? a.src_rows : (int64_t)a.nk) * D;
-  sm.win0 = a.nk - a.w;
+  sm.kbase = a.k + (size_t)sm.u * (a.gather_k ? a.src_rows : (int64_t)nk) * D;
+  sm.vbase = a.v + (size_t)sm.u * (a.gather_v ? a.src_rows : (int64_t)nk) * D;
+  sm.win0 = nk - a.w;
   sm.all_rows = a.m == a.mp;
   sm.init_offsets();
   // (the gathered retained pass does not use these)
@@ -792,13 +811,13 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : 2))) void stream_kerne
     // fixed flags of this split's slots (padded with "fixed" past the end)
     for (int i = threadIdx.x; i < nsl; i += WAVES * 64) {
       const int key = sm.key0 + i;
-      fixl[i] = key < sm.key_end ? a.fixed[(size_t)u * a.nk + key] : 1;
+      fixl[i] = key < sm.key_end ? a.fixed[sm.slot0 + key] : 1;
     }
     if (a.gather_k || a.gather_v) {
       // source row of each slot, clamped into the source tensor
       for (int i = threadIdx.x; i < nsl; i += WAVES * 64) {
         const int key = min(sm.key0 + i, sm.key_end - 1);
-        const int64_t r = a.kpos[(size_t)u * a.nk + key];
+        const int64_t r = a.kpos[sm.slot0 + key];
         posl[i] = (int32_t)(r < 0 ? 0 : r >= a.src_rows ? a.src_rows - 1 : r);
       }
     }
@@ -920,14 +939,14 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : 2))) void stream_kerne
 #pragma unroll
         for (int i = 0; i < 4; ++i) bad |= !__builtin_isfinite(S.y[rt][dt][i]);
     bad = __syncthreads_or(bad);
-    if (threadIdx.x == 0) a.redo[(size_t)u * a.S + s] = bad ? 1 : 0;
+    if (threadIdx.x == 0) a.redo[pidx] = bad ? 1 : 0;
     if (bad) return;
   } else {
     run(BoolTag<false>{});
   }
 
   if (PASS_B) {
-    float* yp = a.ypart + ((size_t)u * a.S + s) * a.mp * D;
+    float* yp = a.ypart + pidx * a.mp * D;
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
@@ -945,11 +964,11 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : 2))) void stream_kerne
           float v = S.msum[rt];
           v += __shfl_xor(v, 16);
           v += __shfl_xor(v, 32);
-          if (g == 0) a.mpart[((size_t)u * a.S + s) * a.mp + sm.rtile(rt) * 16 + l16] = v;
+          if (g == 0) a.mpart[pidx * a.mp + sm.rtile(rt) * 16 + l16] = v;
         }
       }
       // lower blocks N[I][J] (J <= I) and their mirrors N[J][I]
-      float* np = a.npart + ((size_t)u * a.S + s) * a.mp * a.mp;
+      float* np = a.npart + pidx * a.mp * a.mp;
 #pragma unroll
       for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
@@ -974,7 +993,7 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : 2))) void stream_kerne
       const double tot = sum_over_groups(part);
       const int row = sm.rtile(rt) * 16 + l16;
       if (g == 0) {
-        const size_t o = ((size_t)u * a.S + s) * a.mp + row;
+        const size_t o = pidx * a.mp + row;
         a.pmax[o] = M;
         a.psum[o] = M == -INFINITY ? 0.0 : tot;
       }
@@ -997,14 +1016,21 @@ hipError_t launch_stream_t(const Plan& p, const AttnPass& a, hipStream_t s) {
   k.kpos = a.kpos; k.src_rows = a.src_rows;
   k.gather_k = a.gather_k ? 1 : 0; k.gather_v = a.gather_v ? 1 : 0;
   k.kcopy = (u16*)a.kcopy;
+  k.rag = MODE == kModeRetained ? p.rag : nullptr;
+  k.split_unit = p.rag_split_unit;
   if ((k.gather_k || k.gather_v) && (!a.kpos || a.src_rows < 1)) return hipErrorInvalidValue;
+  // ragged budgets: gathered rows only (the per-unit source tensors are the
+  // full caches, never a [U][nk][d] array of one budget)
+  if (k.rag && (!k.gather_k || !k.gather_v || !k.split_unit || p.rag_splits < 1))
+    return hipErrorInvalidValue;
   if (MODE == kModeRetained) {
     const int tk = kTileElems / D;
     if ((size_t)((a.chunk + tk - 1) / tk) * tk > (size_t)kRetMaxSlots) return hipErrorInvalidValue;
   } else if (k.gather_k || k.gather_v) {
     return hipErrorInvalidValue;   // only the retained pass reads rows through positions
   }
-  hipLaunchKernelGGL((stream_kernel<D, WAVES, MODE>), dim3(a.S, p.U), dim3(WAVES * 64), 0, s, k);
+  const dim3 grid = k.rag ? dim3(p.rag_splits, 1) : dim3(a.S, p.U);
+  hipLaunchKernelGGL((stream_kernel<D, WAVES, MODE>), grid, dim3(WAVES * 64), 0, s, k);
   return hipGetLastError();
 }
 
