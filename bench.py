@@ -198,7 +198,7 @@ def carrier(args, cfg, G, hip, stream, Kd, res, host=None):
     }
 
 
-def front_ends(args, cfg, G, hip, stream, qd, Kd, Vd, res):
+def front_ends(args, cfg, G, hip, stream, qd, Kd, Vd, res, host=None):
     """The budget front-ends on the same workload: ragged compression with the
     pyramid schedule (mean budget c, top layer c / 2, bottom 3c / 2) and with
     the adaptive per-head allocation computed on the GPU from the pooled scores
@@ -220,11 +220,20 @@ def front_ends(args, cfg, G, hip, stream, qd, Kd, Vd, res):
         torch.cuda.synchronize()
         return hip.elapsed_ms(a, b) / reps
 
+    import numpy as np
+
     pooled = G.intermediates(res)["pooled"].contiguous().clone()
     budgets = G.adaptive_budgets(pooled, cfg.layers, cfg.kv_heads, c, w)
     ms_alloc = timed(lambda: G.adaptive_budgets(pooled, cfg.layers, cfg.kv_heads, c, w,
                                                 out=budgets))
-    out = {"adaptive_allocation_ms": ms_alloc}
+    # the allocation reads every pooled score once (algorithmic bytes)
+    alloc_gbs = pooled.numel() * 4 / (ms_alloc / 1e3) / 1e9
+    out = {"adaptive_allocation": {
+        "ms_per_call": ms_alloc, "kernel": "adaptive_kernel",
+        "roofline": {"bound": "hbm", "achieved": alloc_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": alloc_gbs / HBM_PEAK_GBS, "traffic": None}}}
+    full_prob = G.STAGES.index("full_prob")
+    esz = 2 if cfg.dtype == "bf16" else 4
     for name, b in (("pyramid", G.pyramid_budgets(cfg.layers, cfg.kv_heads, c, w, cfg.n)),
                     ("adaptive", budgets.cpu().numpy())):
         dt = G.GRKV_BF16 if cfg.dtype == "bf16" else G.GRKV_F32
@@ -233,9 +242,39 @@ def front_ends(args, cfg, G, hip, stream, qd, Kd, Vd, res):
         r = G.compress_ragged(qd, Kd, Vd, w, b, cfg.pool_kernel, cfg.lam, workspace=ws)
         ms = timed(lambda: G.compress_ragged(qd, Kd, Vd, w, b, cfg.pool_kernel, cfg.lam,
                                              workspace=ws, out=r))
+        # the dominant stage (full-cache pass B), timed with events on the stream
+        evs = (ctypes.c_void_p * (2 * G.NUM_STAGES))()
+        e0, e1 = hip.event(), hip.event()
+        evs[2 * full_prob], evs[2 * full_prob + 1] = e0.value, e1.value
+        fp = []
+        for _ in range(reps):
+            G.compress_ragged(qd, Kd, Vd, w, b, cfg.pool_kernel, cfg.lam, workspace=ws, out=r,
+                              stage_events=evs)
+            torch.cuda.synchronize()
+            fp.append(hip.elapsed_ms(e0, e1))
+        fp_ms = float(np.mean(fp))
+        gbs = U * (2 * cfg.n * cfg.head_dim * esz + cfg.group * w * cfg.head_dim * esz) / \
+            (fp_ms / 1e3) / 1e9
         out[name] = {"ms_per_call": ms, "heads_per_s": U / (ms / 1e3),
                      "distinct_budgets": int(len(set(b.tolist()))),
-                     "budget_min": int(b.min()), "budget_max": int(b.max())}
+                     "budget_min": int(b.min()), "budget_max": int(b.max()),
+                     "roofline": {"bound": "hbm", "kernel": "full_prob", "achieved": gbs,
+                                  "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                  "frac": gbs / HBM_PEAK_GBS, "traffic": None}}
+    if host is not None:
+        # the oracle's allocation (float64 joint top-k per layer) on a few layers
+        from oracle import grkv_frontend_oracle as FO
+        pl = pooled.cpu().numpy().astype(np.float64)
+        H = cfg.kv_heads
+        done, t0 = 0, time.perf_counter()
+        while done < cfg.layers and (done < 1 or time.perf_counter() - t0 < 5.0):
+            FO.adaptive_budgets(pl[done * H:(done + 1) * H], 1, H, c, w)
+            done += 1
+        el = time.perf_counter() - t0
+        out["adaptive_allocation"]["cpu_baseline"] = {
+            "value": done / el, "unit": "layers/s", "cores": 1, "kind": "oracle",
+            "sample": "%d of %d layers (float64 numpy lexsort), %.1f s" % (done, cfg.layers, el)}
+        out["adaptive_allocation"]["layers_per_s"] = cfg.layers / (ms_alloc / 1e3)
     return out
 
 
@@ -458,7 +497,8 @@ def main():
     car = (carrier(args, cfg, G, hip, stream, Kd, out, host=None if args.no_cpu_baseline else K)
            if args.carrier else None)
 
-    fe = front_ends(args, cfg, G, hip, stream, qd, Kd, Vd, out) if args.front_ends else None
+    fe = (front_ends(args, cfg, G, hip, stream, qd, Kd, Vd, out,
+                     host=None if args.no_cpu_baseline else True) if args.front_ends else None)
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -223,11 +223,15 @@ void grkv_default_key_options(grkv_key_options* kopt, float lambda);
  *   budgets  int32 [U], HOST memory
  *   out      packed outputs: idx int32 [sum c_u], k_out dtype [sum c_u][d],
  *            v_out float [sum c_u][d], unit u starting at slot
- *            off_u = budgets[0] + ... + budgets[u-1]; stats [U][4] as before;
- *            out->stage_events is ignored
- * Consecutive units with equal budgets run as one batch, so a budget per
- * layer costs one batched call per layer.  The workspace is
- * grkv_workspace_bytes_ragged(); errors as for grkv_compress. */
+ *            off_u = budgets[0] + ... + budgets[u-1]; stats [U][4] as before
+ * On the bf16 path (d 64/128, group * window <= 128) every stage is one launch
+ * over all units: a per-unit table (slot offset, budget, splits) is copied
+ * into the workspace from host memory on `stream` first (the host array may
+ * be reused once the call returns), and out->stage_events is honoured as for
+ * grkv_compress.  Other shapes run consecutive units of equal budget as one
+ * grkv_compress batch each (out->stage_events ignored).  The workspace is
+ * grkv_workspace_bytes_ragged(); errors as for grkv_compress, and
+ * GRKV_ERR_UNSUPPORTED when the budgets sum past 2^31 - 1. */
 int grkv_compress_ragged(const void* q_obs, const void* K, const void* V, int64_t n,
                          int32_t window, const int32_t* budgets, int32_t pool_kernel,
                          float lambda, void* stream, const grkv_problem* prob,
@@ -254,6 +258,8 @@ int grkv_pyramid_budgets(int32_t layers, int32_t kv_heads, int32_t mean_budget, 
  * of its tokens taken.  pooled: float [U][n - w] device memory, the pooled
  * scores of a grkv_compress call (grkv_workspace_layout().pooled); budgets:
  * int32 [U] device memory, written asynchronously on stream.  kv_heads <= 128.
+ * The scores must be finite and non-negative (pooled attention masses are);
+ * one block per layer selects by radix over their bit patterns.
  * Errors: GRKV_ERR_INVALID, GRKV_ERR_UNSUPPORTED, GRKV_ERR_HIP. */
 int grkv_adaptive_budgets(const float* pooled, int32_t layers, int32_t kv_heads, int64_t n,
                           int32_t window, int32_t budget, void* stream, int32_t* budgets);

@@ -352,12 +352,14 @@ def adaptive_budgets(pooled, layers: int, kv_heads: int, budget: int, window: in
 
 def compress_ragged(q_obs, K, V, window: int, budgets, pool_kernel: int, lam: float, *,
                     n_sink: int = 4, beta: float = 0.10, fix_window: bool = True,
-                    causal_window: bool = True, stream=None, workspace=None, out=None):
+                    causal_window: bool = True, stream=None, workspace=None, out=None,
+                    stage_events=None):
     """Every unit compressed with its own budget (``budgets``: host sequence of U
     ints).  Returns ``(idx, k_out, v_out, stats, offsets)`` with the packed
     layout of grkv.h (unit u at slots offsets[u] .. offsets[u] + budgets[u]).
     ``out``: the first four of a previous call's results with the same budgets,
-    reused as the outputs."""
+    reused as the outputs.  ``stage_events``: as for ``compress`` (recorded on
+    the bf16 path, where one launch per stage serves every unit)."""
     import numpy as np
     import torch
 
@@ -387,7 +389,7 @@ def compress_ragged(q_obs, K, V, window: int, budgets, pool_kernel: int, lam: fl
         stats = torch.empty((U, 4), dtype=torch.float32, device=dev)
     opt = Options(n_sink, beta, 1 if fix_window else 0, 1 if causal_window else 0)
     outs = Outputs(idx.data_ptr(), k_out.data_ptr(), v_out.data_ptr(), stats.data_ptr(),
-                   workspace.data_ptr(), workspace.numel(), None)
+                   workspace.data_ptr(), workspace.numel(), stage_events)
     if stream is None:
         stream = torch.cuda.current_stream(dev)
     handle = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)

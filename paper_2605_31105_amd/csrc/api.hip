@@ -5,6 +5,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <algorithm>
 #include <vector>
 
 #include "grkv_internal.h"
@@ -521,8 +522,9 @@ int grkv_adaptive_budgets(const float* pooled, int32_t layers, int32_t kv_heads,
 // one budget; the retained pass in splits of one length over each unit's own
 // budget, the update in blocks of one slot count, both as flat grids whose
 // blocks find their unit in device tables.  `tab` receives the tables
-// (RagUnit [U], the unit of every retained-pass block, the unit of every
-// update block) for the caller to copy into the workspace.  *native is false
+// (RagUnit [U], the unit of every retained-pass split, the unit of every
+// update block, then the two launch orders) for the caller to copy into the
+// workspace.  *native is false
 // when the shape takes the generic path (one call per run of equal budgets).
 static int make_ragged_plan(const grkv_problem* prob, int64_t n, int32_t window,
                             const int32_t* budgets, int32_t pool_kernel, float lambda,
@@ -569,8 +571,27 @@ static int make_ragged_plan(const grkv_problem* prob, int64_t n, int32_t window,
   p->rag_splits = (int)split_unit.size();
   p->rag_upd_blocks = (int)upd_unit.size();
   p->upd_spb = spb;
+  // launch orders: splits (update blocks) by decreasing slot count, ties in
+  // split order (a stable sort)
+  auto order = [&](const std::vector<int32_t>& unit_of, int len, int first_of_unit) {
+    std::vector<int32_t> o(unit_of.size()), size(unit_of.size());
+    for (size_t f = 0; f < unit_of.size(); ++f) {
+      const RagUnit* r = reinterpret_cast<const RagUnit*>(tab->data()) + unit_of[f];
+      const int first = first_of_unit == 0 ? r->s0 : r->ub0;
+      const int k = (int)f - first;
+      const int rest = r->c - k * len;
+      size[f] = rest < len ? rest : len;
+      o[f] = (int32_t)f;
+    }
+    std::stable_sort(o.begin(), o.end(), [&](int32_t a, int32_t b) { return size[a] > size[b]; });
+    return o;
+  };
+  const std::vector<int32_t> split_order = order(split_unit, chunk, 0);
+  const std::vector<int32_t> upd_order = order(upd_unit, spb, 1);
   tab->insert(tab->end(), split_unit.begin(), split_unit.end());
   tab->insert(tab->end(), upd_unit.begin(), upd_unit.end());
+  tab->insert(tab->end(), split_order.begin(), split_order.end());
+  tab->insert(tab->end(), upd_order.begin(), upd_order.end());
   p->c = cmax;
   p->s_sel = cmax - window;
   layout_plan(p, (size_t)sum, split_unit.size(), split_unit.size(), tab->size() * sizeof(int32_t));
@@ -635,6 +656,8 @@ int grkv_compress_ragged(const void* q_obs, const void* K, const void* V, int64_
     rp.rag = (const RagUnit*)dt;
     rp.rag_split_unit = dt + (size_t)8 * rp.U;
     rp.rag_upd_unit = rp.rag_split_unit + rp.rag_splits;
+    rp.rag_split_order = rp.rag_upd_unit + rp.rag_upd_blocks;
+    rp.rag_upd_order = rp.rag_split_order + rp.rag_splits;
     return run_compress(rp, q_obs, K, V, n, (hipStream_t)stream, out);
   }
   size_t need = 0;

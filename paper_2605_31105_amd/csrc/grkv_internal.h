@@ -46,9 +46,13 @@ struct Plan {
   // ragged budgets (bf16 fast path): device tables, null for one budget.
   // p.c is then the largest budget, chunk2 the uniform split length of the
   // retained pass and upd_spb the slots per update block.
+  // Blocks are launched largest first (split f = *_order[blockIdx.x]), so
+  // that the short remainder splits fill the compute units that finish early.
   const RagUnit* rag;
-  const int32_t* rag_split_unit;   // [rag_splits] unit of each retained-pass block
+  const int32_t* rag_split_unit;   // [rag_splits] unit of each retained-pass split
   const int32_t* rag_upd_unit;     // [rag_upd_blocks] unit of each update block
+  const int32_t* rag_split_order;  // [rag_splits] split run by each retained-pass block
+  const int32_t* rag_upd_order;    // [rag_upd_blocks] update block run by each block
   int rag_splits, rag_upd_blocks, upd_spb;
   // workspace offsets (bytes)
   size_t pmax1, psum1, lse1, lse1_log2, ypart, y, colsum, pooled, fixed, v0c, redo;

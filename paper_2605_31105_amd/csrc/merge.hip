@@ -515,7 +515,7 @@ __global__ __launch_bounds__(kUpdWaves * 64) void update_kernel(
     const u16* q, const u16* k0, const float* lse_log2, const uint8_t* fixed, const u16* zhi,
     const u16* zlo, const float* stats_ws, const u16* V, const int32_t* idx, int64_t n,
     float* v_out, int m, int w, int c, int spb, int causal, float scale_log2, const RagUnit* rag,
-    const int32_t* upd_unit) {
+    const int32_t* upd_unit, const int32_t* upd_order) {
   constexpr int QS = D + 8;    // LDS row stride (bf16) of Q rows
   constexpr int ZS = MP + 8;   // LDS row stride (bf16) of Z^T rows
   constexpr int DT = D / 16;   // output tiles per slot row
@@ -533,9 +533,10 @@ __global__ __launch_bounds__(kUpdWaves * 64) void update_kernel(
   int u = blockIdx.y, blk = blockIdx.x;
   size_t slot0 = (size_t)blockIdx.y * c;
   if (rag) {
-    u = upd_unit[blockIdx.x];
+    const int f = upd_order[blockIdx.x];
+    u = upd_unit[f];
     const RagUnit ru = rag[u];
-    blk = blockIdx.x - ru.ub0;
+    blk = f - ru.ub0;
     c = ru.c;
     slot0 = (size_t)ru.off;
   }
@@ -742,7 +743,8 @@ hipError_t launch_update_t(const Plan& p, const void* q, const void* k0, const f
                            const float* stats_ws, const u16* V, const int32_t* idx,
                            float* v_out, hipStream_t s) {
   int spb = p.rag ? p.upd_spb : update_slots_per_block(p, p.c);
-  if (spb < 32 || spb > kUpdMaxSlots || (p.rag && (!p.rag_upd_unit || p.rag_upd_blocks < 1)))
+  if (spb < 32 || spb > kUpdMaxSlots ||
+      (p.rag && (!p.rag_upd_unit || !p.rag_upd_order || p.rag_upd_blocks < 1)))
     return hipErrorInvalidValue;
   const int bpu = (p.c + spb - 1) / spb;
   const size_t lds = update_lds_bytes<MP, D>(spb);
@@ -754,7 +756,7 @@ hipError_t launch_update_t(const Plan& p, const void* q, const void* k0, const f
   hipLaunchKernelGGL((update_kernel<MP, D>), grid, dim3(kUpdWaves * 64), lds, s,
                      (const u16*)q, (const u16*)k0, lse_log2, fixed, zhi, zlo, stats_ws, V, idx,
                      p.n, v_out, p.m, p.w, p.c, spb, p.opt.causal_window ? 1 : 0, scale_log2,
-                     p.rag, p.rag_upd_unit);
+                     p.rag, p.rag_upd_unit, p.rag_upd_order);
   return hipGetLastError();
 }
 

@@ -72,6 +72,7 @@ struct StreamK {
   // are packed), and its partials are indexed by f
   const RagUnit* rag;
   const int32_t* split_unit;
+  const int32_t* split_order;   // flat split run by each block (largest first)
 };
 
 constexpr int kTileElems = 4096;   // elements of one tensor per tile
@@ -772,7 +773,7 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : 2))) void stream_kerne
   sm.u = blockIdx.y;
   sm.slot0 = (size_t)blockIdx.y * a.nk;
   if (RET && a.rag) {
-    const int f = blockIdx.x;
+    const int f = a.split_order[blockIdx.x];
     sm.u = a.split_unit[f];
     const RagUnit ru = a.rag[sm.u];
     s = f - ru.s0;
@@ -1018,10 +1019,12 @@ hipError_t launch_stream_t(const Plan& p, const AttnPass& a, hipStream_t s) {
   k.kcopy = (u16*)a.kcopy;
   k.rag = MODE == kModeRetained ? p.rag : nullptr;
   k.split_unit = p.rag_split_unit;
+  k.split_order = p.rag_split_order;
   if ((k.gather_k || k.gather_v) && (!a.kpos || a.src_rows < 1)) return hipErrorInvalidValue;
   // ragged budgets: gathered rows only (the per-unit source tensors are the
   // full caches, never a [U][nk][d] array of one budget)
-  if (k.rag && (!k.gather_k || !k.gather_v || !k.split_unit || p.rag_splits < 1))
+  if (k.rag && (!k.gather_k || !k.gather_v || !k.split_unit || !k.split_order ||
+                p.rag_splits < 1))
     return hipErrorInvalidValue;
   if (MODE == kModeRetained) {
     const int tk = kTileElems / D;

@@ -44,24 +44,35 @@ def test_adaptive_budgets(cfg_id):
     assert np.all(got.reshape(cfg.layers, cfg.kv_heads).sum(axis=1) == cfg.kv_heads * cfg.budget)
 
 
-def _ragged_check(cfg, q, K, V, budgets, **opts):
+def _ragged_check(cfg, q, K, V, budgets, units=None, **opts):
+    """Every unit (or the sampled ``units``) against the oracle with its own
+    budget; every unit's retained set checked for the properties that hold at
+    any size."""
     import paper_2605_31105_amd as G
     qd, Kd, Vd = (to_device(a, cfg.dtype) for a in (q, K, V))
     idx, k_out, v_out, stats, off = G.compress_ragged(qd, Kd, Vd, cfg.window, budgets,
                                                       cfg.pool_kernel, cfg.lam, **opts)
     torch.cuda.synchronize()
     idx, v_out, stats = idx.cpu().numpy(), v_out.cpu().numpy(), stats.cpu().numpy()
-    kb = k_out.cpu().view(torch.int16).numpy().view(np.uint16)
+    kc = k_out.cpu()
+    kb = kc.view(torch.int16).numpy().view(np.uint16) if cfg.dtype == "bf16" else kc.numpy()
     oo = {k: v for k, v in opts.items() if k in ("n_sink", "beta", "fix_window", "causal_window")}
     opt = O.Options(**oo) if oo else None
+    assert np.array_equal(off, FO.packed_offsets(budgets))
     for u, b in enumerate(budgets):
-        s = slice(int(off[u]), int(off[u]) + int(b))
-        r = O.compress_unit(*(W.decode(a[u], cfg.dtype) for a in (q, K, V)), cfg.window, int(b),
+        ids = idx[int(off[u]):int(off[u]) + int(b)]
+        assert np.all(np.diff(ids) > 0)
+        assert np.array_equal(ids[-cfg.window:], np.arange(cfg.n - cfg.window, cfg.n))
+    assert np.all(stats[:, 3] == 0)
+    for u in (range(len(budgets)) if units is None else units):
+        b = int(budgets[u])
+        s = slice(int(off[u]), int(off[u]) + b)
+        r = O.compress_unit(*(W.decode(a[u], cfg.dtype) for a in (q, K, V)), cfg.window, b,
                             cfg.pool_kernel, cfg.lam, opt)
         assert np.array_equal(idx[s], r["idx"]), "unit %d: retained set" % u
         assert np.array_equal(kb[s], K[u][r["idx"]])
         verr = np.abs(v_out[s] - r["Vstar"]).max() / np.abs(r["Vstar"]).max()
-        print(dict(unit=u, budget=int(b), v_err=float(verr), d=float(stats[u, 2]),
+        print(dict(unit=u, budget=b, v_err=float(verr), d=float(stats[u, 2]),
                    d_oracle=float(r["D_after"])), flush=True)
         assert verr <= V_TOL and stats[u, 3] == r["status"]
         if r["D_after"] > 1e-12:
@@ -108,3 +119,30 @@ def test_ragged_uniform_equals_compress():
     torch.cuda.synchronize()
     assert torch.equal(a.idx.reshape(-1), idx) and torch.equal(a.k_out.reshape(-1, cfg.head_dim), k_out)
     assert torch.equal(a.v_out.reshape(-1, cfg.head_dim), v_out) and torch.equal(a.stats, stats)
+
+
+def test_ragged_full_workload_pyramid_and_adaptive_sampled():
+    # the 32-layer n=32k workload in one ragged call per front-end, sampled
+    # units against the oracle (the adaptive sample holds the smallest and
+    # the largest budget)
+    import paper_2605_31105_amd as G
+    cfg = W.config(4)
+    q, K, V = W.make_batch(cfg)
+    b = G.pyramid_budgets(cfg.layers, cfg.kv_heads, cfg.budget, cfg.window, cfg.n)
+    _ragged_check(cfg, q, K, V, b, units=(0, 37, 128, 255))
+    qd, Kd, Vd = (to_device(a, cfg.dtype) for a in (q, K, V))
+    b = G.adaptive_budgets(_pooled(cfg, qd, Kd, Vd), cfg.layers, cfg.kv_heads, cfg.budget,
+                           cfg.window).cpu().numpy()
+    del qd, Kd, Vd
+    _ragged_check(cfg, q, K, V, b, units=(int(np.argmin(b)), int(np.argmax(b)), 101, 200))
+
+
+@pytest.mark.parametrize("label,cfg_id,over,budgets", [
+    ("fp32", 1, {}, [16, 300]),
+    ("bf16-m256", 2, dict(layers=1, kv_heads=2, n=2048, window=64, budget=512), [512, 300]),
+], ids=["fp32", "bf16-m256"])
+def test_ragged_generic_path(label, cfg_id, over, budgets):
+    # shapes outside the bf16 fast path run one call per run of equal budgets
+    cfg = W.config(cfg_id, **over)
+    q, K, V = W.make_batch(cfg)
+    _ragged_check(cfg, q, K, V, budgets)
