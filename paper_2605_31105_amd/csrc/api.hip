@@ -257,13 +257,17 @@ int run_compress(const Plan& p, const void* q_obs, const void* K, const void* V,
   auto pass_a = [&](const AttnPass& a) { return fast ? launch_stream(p, a, 0, s) : launch_lse_pass(p, a, s); };
   auto pass_b = [&](const AttnPass& a) { return fast ? launch_stream(p, a, 1, s) : launch_prob_pass(p, a, s); };
   GRKV_STAGE(GRKV_STAGE_FULL_LSE, pass_a(full));
-  // (the bf16 streaming pass B combines the split partials itself)
-  if (!fast)
+  // (the bf16 streaming pass B combines the split partials itself, unless a
+  // unit has so many splits that a kernel of its own does it faster)
+  const bool pre = fast && p.fast_merge && p.S1 >= kPrecombineSplits;
+  full.lse_ready = pre;
+  if (!fast || pre)
     GRKV_STAGE(GRKV_STAGE_FULL_LSE_COMBINE,
                launch_lse_combine(p, full.pmax, full.psum, p.S1, Dd(p.lse1), F(p.lse1_log2), s));
   GRKV_STAGE(GRKV_STAGE_FULL_PROB, pass_b(full));
-  // (the fast value step combines the Y partials inside its solve)
-  if (!p.fast_merge)
+  // (the fast value step combines the Y partials inside its solve, again
+  // unless there are many)
+  if (!p.fast_merge || pre)
     GRKV_STAGE(GRKV_STAGE_FULL_Y, launch_combine_rows(p, F(p.ypart), p.S1, nullptr, F(p.y), s));
   // 2. pooled top-k retention and the fixed set; gather K0, V0
   uint8_t* fixed = (uint8_t*)(ws + p.fixed);
@@ -307,7 +311,7 @@ int run_compress(const Plan& p, const void* q_obs, const void* K, const void* V,
   if (!fast_merge) GRKV_STAGE(GRKV_STAGE_GRAM, launch_gram(p, F(p.x), fixed, F(p.npart), s));
   if (fast_merge) {
     GRKV_STAGE(GRKV_STAGE_SOLVE,
-               launch_solve(p, F(p.ypart), F(p.xvpart), F(p.npart),
+               launch_solve(p, pre ? F(p.y) : F(p.ypart), pre ? 1 : p.S1, F(p.xvpart), F(p.npart),
                             direct ? F(p.mpart) : nullptr, F(p.lse1_log2), kRetainedBias,
                             F(p.lse2_log2), F(p.y), F(p.resid), F(p.gram), F(p.z),
                             (uint16_t*)(ws + p.zhi), (uint16_t*)(ws + p.zlo), F(p.stats_ws),

@@ -397,23 +397,43 @@ __global__ __launch_bounds__(WAVES * 64) void prob_pass_kernel(PassK a) {
       }
 }
 
+// The partials of a row are loaded kBatch at a time (all in flight), then
+// reduced in split order, so the result does not depend on the batching.
+constexpr int kCombineBatch = 16;
+
 __global__ void lse_combine_kernel(const float* pmax, const double* psum, int S, int mp,
                                    int total, double* lse, float* lse_log2) {
   int id = blockIdx.x * blockDim.x + threadIdx.x;
   if (id >= total) return;
   int u = id / mp, row = id % mp;
+  const size_t base = (size_t)u * S * mp + row;
   float M = -INFINITY;
-  for (int s = 0; s < S; ++s) M = fmaxf(M, pmax[((size_t)u * S + s) * mp + row]);
+  for (int s0 = 0; s0 < S; s0 += kCombineBatch) {
+    float ms[kCombineBatch];
+#pragma unroll
+    for (int k = 0; k < kCombineBatch; ++k)
+      ms[k] = s0 + k < S ? pmax[base + (size_t)(s0 + k) * mp] : -INFINITY;
+#pragma unroll
+    for (int k = 0; k < kCombineBatch; ++k) M = fmaxf(M, ms[k]);
+  }
   if (M == -INFINITY) {  // padding row: no visible key
     lse[id] = -INFINITY;
     lse_log2[id] = 0.f;
     return;
   }
   double sum = 0.0;
-  for (int s = 0; s < S; ++s) {
-    size_t o = ((size_t)u * S + s) * mp + row;
-    float ms = pmax[o];
-    if (ms != -INFINITY) sum += psum[o] * exp2((double)ms - (double)M);
+  for (int s0 = 0; s0 < S; s0 += kCombineBatch) {
+    float ms[kCombineBatch];
+    double ps[kCombineBatch];
+#pragma unroll
+    for (int k = 0; k < kCombineBatch; ++k) {
+      const bool in = s0 + k < S;
+      ms[k] = in ? pmax[base + (size_t)(s0 + k) * mp] : -INFINITY;
+      ps[k] = in ? psum[base + (size_t)(s0 + k) * mp] : 0.0;
+    }
+#pragma unroll
+    for (int k = 0; k < kCombineBatch; ++k)
+      if (ms[k] != -INFINITY) sum += ps[k] * exp2((double)ms[k] - (double)M);
   }
   double l2 = (double)M + log2(sum);
   lse[id] = l2 * 0.69314718055994530942;
@@ -425,8 +445,16 @@ __global__ void combine_rows_kernel(const float* part, int S, size_t per_unit, s
   size_t id = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (id >= total) return;
   size_t u = id / per_unit, e = id % per_unit;
+  const float* p0 = part + u * S * per_unit + e;
   float acc = 0.f;
-  for (int s = 0; s < S; ++s) acc += part[(u * S + s) * per_unit + e];
+  for (int s0 = 0; s0 < S; s0 += kCombineBatch) {
+    float v[kCombineBatch];
+#pragma unroll
+    for (int k = 0; k < kCombineBatch; ++k) v[k] = s0 + k < S ? p0[(size_t)(s0 + k) * per_unit] : 0.f;
+#pragma unroll
+    for (int k = 0; k < kCombineBatch; ++k)
+      if (s0 + k < S) acc += v[k];
+  }
   out[id] = base ? base[id] - acc : acc;
 }
 

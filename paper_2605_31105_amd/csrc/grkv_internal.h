@@ -17,6 +17,10 @@ constexpr int kSelectThreads = 1024;
 // full-cache log-sum-exp: retained attention masses down to 2^-108 stay
 // well inside the float range (P <= 2^48, Gram entries <= 2^96).
 constexpr float kRetainedBias = 48.f;
+// From this many full-cache splits per unit (small calls), pass A's partials
+// and the Y partials are combined by their own kernels over all rows at once
+// instead of serially inside every pass-B block and every solve block.
+constexpr int kPrecombineSplits = 16;
 
 // Ragged budgets: one entry per unit, in device memory.  The packed outputs
 // hold unit u's c slots from slot `off`; its retained-pass splits are the
@@ -83,6 +87,8 @@ struct AttnPass {
   int prefix;          // only keys < prefix get a column sum
   float* xout;         // pass B out [U][mp][nk] probabilities, or null (generic path)
   bool split_p;        // P.V with P as a bf16 hi+lo pair (else bf16 P)
+  bool lse_ready;      // full-cache pass B (bf16 streaming): lse / lse_log2 already
+                       // combined from pass A's partials (else combined per block)
   const uint8_t* fixed; // retained pass B (fast path): fixed flags [U][nk]
   float* npart;        // retained pass B (fast path): Gram partials [U][S][mp][mp]
   // streaming passes over the retained set: read K and/or V rows through
@@ -131,7 +137,8 @@ bool merge_fast_supported(const Plan& p);
 // mpart: row sums of the retained P partials [U][S2][mp] when P was formed
 // against the full-cache LSE lse1_log2 scaled by 2^lse_bias (X = P / row sum;
 // the retained LSE is written to lse2_log2), or null when X itself was used.
-hipError_t launch_solve(const Plan& p, const float* ypart, const float* xvpart,
+// ypart holds S1 partials per unit (p.S1, or 1 when Y was combined already).
+hipError_t launch_solve(const Plan& p, const float* ypart, int S1, const float* xvpart,
                         const float* npart, const float* mpart, const float* lse1_log2,
                         float lse_bias, float* lse2_log2, float* y, float* resid,
                         float* gram, float* z, uint16_t* zhi, uint16_t* zlo,

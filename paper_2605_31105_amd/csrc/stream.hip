@@ -52,6 +52,7 @@ struct StreamK {
   // fp64) and lse_log2_out (log2 domain, fp32) for the later kernels
   double* lse_out;
   float* lse_log2_out;
+  int lse_ready;          // full-cache pass B: read the combined LSE from lse_log2_out
   float* ypart;
   float* colsum;
   int prefix;
@@ -836,7 +837,9 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : 2))) void stream_kerne
     for (int ks = 0; ks < D / 32; ++ks)
       S.qb[rt][ks] = S.rowok[rt] ? *reinterpret_cast<const uint4*>(q + ks * 32 + 8 * g)
                                  : make_uint4(0, 0, 0, 0);
-    if constexpr (is_full<MODE>()) {
+    if (is_full<MODE>() && a.lse_ready) {
+      S.lse[rt] = a.lse_log2_out[(size_t)u * a.mp + row];
+    } else if constexpr (is_full<MODE>()) {
       // fixed-order combine of pass A's split partials: M = max of the
       // integer reference exponents, sum = sum_s psum_s 2^(ref_s - M) (exact
       // powers of two), LSE (log2) = M + log2(sum)
@@ -1011,6 +1014,7 @@ hipError_t launch_stream_t(const Plan& p, const AttnPass& a, hipStream_t s) {
   k.scale_log2 = (float)(1.4426950408889634 / __builtin_sqrt((double)D));
   k.pmax = a.pmax; k.psum = a.psum; k.lse_log2 = a.lse_log2;
   k.lse_out = const_cast<double*>(a.lse); k.lse_log2_out = const_cast<float*>(a.lse_log2);
+  k.lse_ready = a.lse_ready ? 1 : 0;
   k.ypart = a.ypart; k.colsum = a.colsum; k.prefix = a.prefix;
   k.fixed = a.fixed; k.npart = a.npart; k.mpart = a.mpart; k.lse_bias = a.lse_bias;
   k.redo = a.redo;
