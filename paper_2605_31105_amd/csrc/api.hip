@@ -129,6 +129,10 @@ static void layout_plan(Plan* p, size_t slots, size_t splits2, size_t splits3, s
   p->resid = take(U * mp * d * sizeof(float));
   p->npart = take(splits3 * mp * mp * sizeof(float));
   p->mpart = take(fast_path ? splits2 * mp * sizeof(float) : 0);
+  const size_t comb = fast_path && p->S2 >= kPrecombineRetSplits ? U : 0;
+  p->xvcomb = take(comb * mp * d * sizeof(float));
+  p->ncomb = take(comb * mp * mp * sizeof(float));
+  p->mcomb = take(comb * mp * sizeof(float));
   p->gram = take(U * mp * mp * sizeof(float));
   p->z = take(U * d * mp * sizeof(float));
   p->zhi = take(U * d * mp * 2);
@@ -310,9 +314,19 @@ int run_compress(const Plan& p, const void* q_obs, const void* K, const void* V,
   // 4. value step: N, Cholesky solve for Z, V* = V0 + X_G^T Z
   if (!fast_merge) GRKV_STAGE(GRKV_STAGE_GRAM, launch_gram(p, F(p.x), fixed, F(p.npart), s));
   if (fast_merge) {
+    // many retained splits per unit (small uniform calls): their partials are
+    // summed by one launch over all units first
+    const bool pre2 = direct && !p.rag && p.S2 >= kPrecombineRetSplits;
+    if (pre2) {
+      const float* part[3] = {F(p.xvpart), F(p.npart), F(p.mpart)};
+      float* const outs[3] = {F(p.xvcomb), F(p.ncomb), F(p.mcomb)};
+      const size_t per[3] = {(size_t)p.mp * p.d, (size_t)p.mp * p.mp, (size_t)p.mp};
+      GRKV_STAGE(GRKV_STAGE_RESID, launch_combine_parts(p.U, p.S2, part, outs, per, s));
+    }
     GRKV_STAGE(GRKV_STAGE_SOLVE,
-               launch_solve(p, pre ? F(p.y) : F(p.ypart), pre ? 1 : p.S1, F(p.xvpart), F(p.npart),
-                            direct ? F(p.mpart) : nullptr, F(p.lse1_log2), kRetainedBias,
+               launch_solve(p, pre ? F(p.y) : F(p.ypart), pre ? 1 : p.S1, pre2 ? 1 : p.S2,
+                            pre2 ? F(p.xvcomb) : F(p.xvpart), pre2 ? F(p.ncomb) : F(p.npart),
+                            direct ? (pre2 ? F(p.mcomb) : F(p.mpart)) : nullptr, F(p.lse1_log2), kRetainedBias,
                             F(p.lse2_log2), F(p.y), F(p.resid), F(p.gram), F(p.z),
                             (uint16_t*)(ws + p.zhi), (uint16_t*)(ws + p.zlo), F(p.stats_ws),
                             out->stats, s));

@@ -458,6 +458,36 @@ __global__ void combine_rows_kernel(const float* part, int S, size_t per_unit, s
   out[id] = base ? base[id] - acc : acc;
 }
 
+// Up to three partial arrays summed over S splits in one launch: segment i
+// covers U * per_unit[i] consecutive ids.
+struct CombineSeg {
+  const float* part[3];
+  float* out[3];
+  size_t per_unit[3];
+};
+
+__global__ void combine_segments_kernel(CombineSeg g, int S, int U, size_t total) {
+  size_t id = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (id >= total) return;
+  int i = 0;
+  while (i < 2 && id >= (size_t)U * g.per_unit[i]) {
+    id -= (size_t)U * g.per_unit[i];
+    ++i;
+  }
+  const size_t pu = g.per_unit[i], u = id / pu, e = id % pu;
+  const float* p0 = g.part[i] + u * S * pu + e;
+  float acc = 0.f;
+  for (int s0 = 0; s0 < S; s0 += kCombineBatch) {
+    float v[kCombineBatch];
+#pragma unroll
+    for (int k = 0; k < kCombineBatch; ++k) v[k] = s0 + k < S ? p0[(size_t)(s0 + k) * pu] : 0.f;
+#pragma unroll
+    for (int k = 0; k < kCombineBatch; ++k)
+      if (s0 + k < S) acc += v[k];
+  }
+  g.out[i][id] = acc;
+}
+
 template <bool BF, int D, int WAVES>
 hipError_t launch_pass(const Plan& p, const AttnPass& a, hipStream_t s, bool pass_b) {
   PassK k;
@@ -524,6 +554,21 @@ hipError_t launch_combine_rows(const Plan& p, const float* part, int S, const fl
   size_t per_unit = (size_t)p.mp * p.d, total = per_unit * p.U;
   hipLaunchKernelGGL(combine_rows_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s,
                      part, S, per_unit, total, base, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_combine_parts(int U, int S, const float* const part[3], float* const out[3],
+                                const size_t per_unit[3], hipStream_t s) {
+  CombineSeg g;
+  size_t total = 0;
+  for (int i = 0; i < 3; ++i) {
+    g.part[i] = part[i];
+    g.out[i] = out[i];
+    g.per_unit[i] = per_unit[i];
+    total += (size_t)U * per_unit[i];
+  }
+  hipLaunchKernelGGL(combine_segments_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s,
+                     g, S, U, total);
   return hipGetLastError();
 }
 

@@ -21,6 +21,9 @@ constexpr float kRetainedBias = 48.f;
 // and the Y partials are combined by their own kernels over all rows at once
 // instead of serially inside every pass-B block and every solve block.
 constexpr int kPrecombineSplits = 16;
+// The same for the retained-pass partials (X V0, Gram, row masses) from this
+// many retained splits per unit.
+constexpr int kPrecombineRetSplits = 8;
 
 // Ragged budgets: one entry per unit, in device memory.  The packed outputs
 // hold unit u's c slots from slot `off`; its retained-pass splits are the
@@ -61,6 +64,8 @@ struct Plan {
   // workspace offsets (bytes)
   size_t pmax1, psum1, lse1, lse1_log2, ypart, y, colsum, pooled, fixed, v0c, redo;
   size_t pmax2, psum2, lse2, lse2_log2, xvpart, x, resid, npart, mpart, gram, z, zhi, zlo, stats_ws;
+  // retained-pass partials summed over the splits (small calls only)
+  size_t xvcomb, ncomb, mcomb;
   size_t rag_tab;   // ragged tables: RagUnit [U], then the two block-to-unit maps
   size_t total;
 };
@@ -111,6 +116,10 @@ hipError_t launch_lse_combine(const Plan& p, const float* pmax,
                               const double* psum, int S, double* lse,
                               float* lse_log2, hipStream_t s);
 hipError_t launch_prob_pass(const Plan& p, const AttnPass& a, hipStream_t s);
+// out[i][u][e] = sum_s part[i][u][s][e], e < per_unit[i], for the three arrays i
+// (a per_unit of 0 leaves that array out); one launch.
+hipError_t launch_combine_parts(int U, int S, const float* const part[3], float* const out[3],
+                                const size_t per_unit[3], hipStream_t s);
 // out[u][r][c] = (base ? base[u][r][c] : 0) +/- sum_s part[u][s][r][c]
 hipError_t launch_combine_rows(const Plan& p, const float* part, int S,
                                const float* base, float* out, hipStream_t s);
@@ -137,8 +146,9 @@ bool merge_fast_supported(const Plan& p);
 // mpart: row sums of the retained P partials [U][S2][mp] when P was formed
 // against the full-cache LSE lse1_log2 scaled by 2^lse_bias (X = P / row sum;
 // the retained LSE is written to lse2_log2), or null when X itself was used.
-// ypart holds S1 partials per unit (p.S1, or 1 when Y was combined already).
-hipError_t launch_solve(const Plan& p, const float* ypart, int S1, const float* xvpart,
+// ypart holds S1 partials per unit (p.S1, or 1 when Y was combined already);
+// xvpart, npart and mpart S2 (p.S2, or 1), unless p.rag gives each unit's own.
+hipError_t launch_solve(const Plan& p, const float* ypart, int S1, int S2, const float* xvpart,
                         const float* npart, const float* mpart, const float* lse1_log2,
                         float lse_bias, float* lse2_log2, float* y, float* resid,
                         float* gram, float* z, uint16_t* zhi, uint16_t* zlo,

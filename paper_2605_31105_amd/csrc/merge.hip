@@ -726,13 +726,13 @@ hipError_t launch_gram_w(const Plan& p, const float* x, const uint8_t* fixed, fl
 }
 
 template <int MP, int D>
-hipError_t launch_solve_t(const Plan& p, const float* ypart, int S1, const float* xvpart,
+hipError_t launch_solve_t(const Plan& p, const float* ypart, int S1, int S2, const float* xvpart,
                           const float* npart, const float* mpart, const float* lse1_log2,
                           float lse_bias, float* lse2_log2, float* y, float* resid, float* gram,
                           float* z, u16* zhi, u16* zlo, float* stats_ws, float* stats_user,
                           hipStream_t s) {
   hipLaunchKernelGGL((solve_kernel<MP, D>), dim3(p.U), dim3(kSolveWaves * 64), 0, s, ypart, S1,
-                     xvpart, p.S2, npart, p.S3, mpart, lse1_log2, lse_bias, lse2_log2, y, resid,
+                     xvpart, S2, npart, S2, mpart, lse1_log2, lse_bias, lse2_log2, y, resid,
                      gram, z, zhi, zlo, stats_ws, stats_user, p.m, p.lam, p.rag);
   return hipGetLastError();
 }
@@ -791,14 +791,14 @@ hipError_t launch_gram(const Plan& p, const float* x, const uint8_t* fixed, floa
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_solve(const Plan& p, const float* ypart, int S1, const float* xvpart,
+hipError_t launch_solve(const Plan& p, const float* ypart, int S1, int S2, const float* xvpart,
                         const float* npart,
                         const float* mpart, const float* lse1_log2, float lse_bias,
                         float* lse2_log2, float* y, float* resid, float* gram, float* z, u16* zhi,
                         u16* zlo, float* stats_ws, float* stats_user, hipStream_t s) {
 #define GRKV_SOLVE(MPV, DV)                                                                   \
   if (p.mp == MPV && p.d == DV)                                                               \
-    return launch_solve_t<MPV, DV>(p, ypart, S1, xvpart, npart, mpart, lse1_log2, lse_bias,     \
+    return launch_solve_t<MPV, DV>(p, ypart, S1, S2, xvpart, npart, mpart, lse1_log2, lse_bias, \
                                    lse2_log2, y, resid, gram, z, zhi, zlo, stats_ws,            \
                                    stats_user, s);
   GRKV_SOLVE(32, 64) GRKV_SOLVE(32, 128) GRKV_SOLVE(64, 64) GRKV_SOLVE(64, 128)
