@@ -18,7 +18,7 @@ namespace {
 
 constexpr int kAdaThreads = 1024;
 constexpr int kAdaMaxHeads = 128;
-constexpr int kAdaUnroll = 8;     // independent loads in flight per thread
+constexpr int kAdaUnroll = 32;    // independent loads in flight per thread
 constexpr int kAdaBins = 2048;    // widest digit (11 bits)
 
 // The scores of one layer, kAdaUnroll coalesced loads per thread at a time;
