@@ -593,9 +593,9 @@ __global__ __launch_bounds__(kUpdWaves * 64) void update_kernel(
   };
   uint4 kb[2][D / 32];
   int tb = s0 + 32 * wave;
-  if (!singular && tb < s1) load_k(tb, kb);
   for (; tb < s1; tb += 32 * kUpdWaves) {
-    const int tnext = tb + 32 * kUpdWaves;
+    // this pair's K0 rows (the other waves of the block hide their latency)
+    if (!singular) load_k(tb, kb);
     // V0 rows of this pair (slot tb + 16T + 4g + i, columns l16 * DT ..),
     // loaded now so that they arrive during the products
     uint32_t v0r[2][4][DT / 2];
@@ -619,8 +619,6 @@ __global__ __launch_bounds__(kUpdWaves * 64) void update_kernel(
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) acc[T][dt] = zero4();
     if (!singular) {
-      uint4 kn[2][D / 32];
-      if (tnext < s1) load_k(tnext, kn);
       float cm[2];   // 0 for a free slot, -inf for a fixed or missing one
       int tw[2];     // window index of the slot (< 0 outside the window)
 #pragma unroll
@@ -684,12 +682,6 @@ __global__ __launch_bounds__(kUpdWaves * 64) void update_kernel(
         pair_product(std::true_type{});
       else
         pair_product(std::false_type{});
-      if (tnext < s1) {
-#pragma unroll
-        for (int T = 0; T < 2; ++T)
-#pragma unroll
-          for (int ks = 0; ks < D / 32; ++ks) kb[T][ks] = kn[T][ks];
-      }
     }
     // lane holds dV[slot = tb + 16T + 4g + i][dd = l16 * DT + dt]
 #pragma unroll
