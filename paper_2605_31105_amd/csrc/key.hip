@@ -40,7 +40,7 @@ namespace grkv {
 namespace {
 
 constexpr int kKT = 32;   // retained keys per tile (the key orders below assume 32)
-constexpr int kKeyEarlyIters = 10;  // CG iterations run with the fewest splits
+constexpr int kKeyEarlyIters = 13;  // CG iterations run with the fewest splits
 
 // Position, inside a block of 32, of the index a lane holds as element j of an
 // MFMA operand when the operand comes from an MFMA result: elements
