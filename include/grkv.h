@@ -227,7 +227,8 @@ void grkv_default_key_options(grkv_key_options* kopt, float lambda);
  * On the bf16 path (d 64/128, group * window <= 128) every stage is one launch
  * over all units: a per-unit table (slot offset, budget, splits) is copied
  * into the workspace from host memory on `stream` first (the host array may
- * be reused once the call returns), and out->stage_events is honoured as for
+ * be reused once the call returns; a copy from pageable memory, so the call
+ * is not for HIP graph capture), and out->stage_events is honoured as for
  * grkv_compress.  Other shapes run consecutive units of equal budget as one
  * grkv_compress batch each (out->stage_events ignored).  The workspace is
  * grkv_workspace_bytes_ragged(); errors as for grkv_compress, and
