@@ -363,9 +363,9 @@ def key_step(args, cfg, G, hip, stream, qd, Kd, Vd, host=None):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(units shard across GPUs with no communication; see the design notes)",
-              file=sys.stderr)
+        print("bench.py measures one GPU only: the library has no multi-GPU path (units are "
+              "independent, so a multi-GPU run would give each GPU its own units with no "
+              "communication)", file=sys.stderr)
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()
