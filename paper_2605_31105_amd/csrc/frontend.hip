@@ -20,6 +20,10 @@ constexpr int kAdaThreads = 1024;
 constexpr int kAdaMaxHeads = 128;
 constexpr int kAdaUnroll = 32;    // independent loads in flight per thread
 constexpr int kAdaBins = 2048;    // widest digit (11 bits)
+// Each bin is kept in kAdaCopies copies (chosen by lane), so that lanes of a
+// wave landing in one crowded bin (scores share few exponents) add to
+// different words; the scan sums the copies.
+constexpr int kAdaCopies = 16;
 
 // The scores of one layer, kAdaUnroll coalesced loads per thread at a time;
 // past the end the key is 0xFFFFFFFF, which no radix prefix of a finite
@@ -47,7 +51,7 @@ __device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
 __global__ __launch_bounds__(kAdaThreads) void adaptive_kernel(const float* __restrict__ pooled,
                                                                int H, int P, int64_t kk, int w,
                                                                int32_t* __restrict__ budgets) {
-  __shared__ uint32_t hist[kAdaBins];
+  __shared__ uint32_t hist[kAdaBins * kAdaCopies];
   __shared__ uint32_t scratch[kAdaThreads / 64];
   __shared__ uint32_t gt[kAdaMaxHeads], eq[kAdaMaxHeads];
   __shared__ uint32_t pick[2];
@@ -66,11 +70,12 @@ __global__ __launch_bounds__(kAdaThreads) void adaptive_kernel(const float* __re
 #pragma unroll
     for (int lev = 0; lev < 3; ++lev) {
       const int shift = kShift[lev], nb = 1 << kBits[lev], top = shift + kBits[lev];
-      for (int b = tid; b < nb; b += kAdaThreads) hist[b] = 0;
+      for (int b = tid; b < nb * kAdaCopies; b += kAdaThreads) hist[b] = 0;
       __syncthreads();
       const uint32_t want = prefix >> top;
+      const int copy = lane & (kAdaCopies - 1);
       for_keys(key, N, [&](uint32_t x) {
-        if ((x >> top) == want) atomicAdd(&hist[(x >> shift) & (nb - 1)], 1u);
+        if ((x >> top) == want) atomicAdd(&hist[((x >> shift) & (nb - 1)) * kAdaCopies + copy], 1u);
       });
       // (no pick when the scores break the non-negative precondition: T = 0)
       if (tid == 0) pick[0] = pick[1] = 0u;
@@ -81,9 +86,15 @@ __global__ __launch_bounds__(kAdaThreads) void adaptive_kernel(const float* __re
       const int per = nb / kAdaThreads > 0 ? nb / kAdaThreads : 1;   // 2 or 1 bins
       uint32_t v[2] = {0u, 0u};
       const int b0 = nb - 1 - per * tid;
+      auto bin = [&](int b) {
+        uint32_t t = 0;
+#pragma unroll
+        for (int k = 0; k < kAdaCopies; ++k) t += hist[b * kAdaCopies + k];
+        return t;
+      };
       if (b0 >= 0) {
-        v[0] = hist[b0];
-        if (per == 2) v[1] = hist[b0 - 1];
+        v[0] = bin(b0);
+        if (per == 2) v[1] = bin(b0 - 1);
       }
       uint32_t tot;
       const uint32_t before = block_exclusive_scan(v[0] + v[1], scratch, &tot);
