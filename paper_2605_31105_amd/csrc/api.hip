@@ -1,6 +1,8 @@
-// Host side of the C ABI: argument checks, the workspace plan and the launch
-// sequence of one grkv_compress call.  Everything is enqueued on the caller's
-// stream without a host synchronisation.
+// Host side of the C ABI: argument checks, the workspace plans and the launch
+// sequences of grkv_compress, the key step (grkv_compress_kv), ragged budgets
+// and the budget rules, and the carrier diagnostics.  Everything is enqueued
+// on the caller's stream; the only host-to-device transfer is the ragged
+// call's copy of its per-unit table.
 #include <math.h>
 #include <stdlib.h>
 #include <string.h>

@@ -11,7 +11,10 @@
 //  * A tile is 4096 elements per tensor (32 keys of d=128, 64 keys of d=64),
 //    row-major with the 16-byte chunks of row r XOR-swizzled by r, which keeps
 //    the MFMA operand reads of K free of bank conflicts.
-//  * P.V uses P as a bf16 hi+lo pair (two MFMAs, about 16 bits of P).
+//  * Pass B's P.V takes fp16 P times the V tile converted to fp16 in LDS (one
+//    MFMA); a split whose V leaves the fp16 range is flagged and recomputed
+//    by the exact mode with P as a bf16 hi+lo pair (two MFMAs, about 16 bits
+//    of P), which the retained pass also uses.
 //  * The P.V B-operand (four consecutive keys of one d column per lane) is
 //    read from the row-major V tile with the LDS transpose read
 //    ds_read_b64_tr_b16: within a 16-lane group, lane 4e+q supplies the
@@ -25,6 +28,11 @@
 //  * Window positions are the last w key slots of both key sets (the full
 //    cache, and the retained set whose last w entries are the window), so the
 //    causal rule needs no position array.
+//  * Pass B combines pass A's split partials into the log-sum-exp in its
+//    prologue, or reads it combined already (calls with many splits per unit).
+//  * With ragged budgets the retained pass runs as one flat grid: a per-unit
+//    table gives each block its unit, split and first slot, and its partials
+//    are indexed by the flat split.
 #include "grkv_device.h"
 #include "grkv_internal.h"
 
