@@ -88,29 +88,38 @@ __global__ __launch_bounds__(256) void key_init_kernel(
     float* __restrict__ alpha, float* __restrict__ r, float* __restrict__ p,
     float* __restrict__ sdot, float* __restrict__ W, double* __restrict__ cg) {
   __shared__ double red[4];
+  // E = lam_v Z and F = Y - E of this unit, rows padded by one float
+  constexpr int ES = D + 1;
+  __shared__ float Es[MP * ES], Fs[MP * ES];
   const int u = blockIdx.x, tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, l16 = lane & 15, g = lane >> 4;
   const bool skip = stats_ws[u * 4 + 3] != 0.f;
+  // Z^T is [d][mp]: read along its rows (coalesced), store transposed
+  for (int e = tid; e < MP * D; e += 256) {
+    const int col = e / MP, row = e % MP;
+    Es[row * ES + col] = (!skip && row < m) ? lam_v * zt[(size_t)u * D * MP + e] : 0.f;
+  }
+  __syncthreads();
   double ee = 0;
   for (int e = tid; e < MP * D; e += 256) {
     const int row = e / D, col = e % D;
     const size_t o = (size_t)u * MP * D + e;
-    const float E = (!skip && row < m) ? lam_v * zt[((size_t)u * D + col) * MP + row] : 0.f;
-    Fm[o] = row < m ? y[o] - E : 0.f;
+    const float E = Es[row * ES + col];
+    const float F = row < m ? y[o] - E : 0.f;
+    Fs[row * ES + col] = F;
+    Fm[o] = F;
     alpha[o] = 0.f;
     r[o] = E;
     p[o] = E;
     ee += (double)E * E;
   }
-  // s = rowdot(F, p) for the first direction p = E, one thread per row
+  __syncthreads();
+  // s = rowdot(F, p) for the first direction p = E, summed over the columns
+  // in order (one thread per row, from LDS)
   for (int row = tid; row < MP; row += 256) {
     float acc = 0.f;
     if (!skip && row < m)
-      for (int col = 0; col < D; ++col) {
-        const size_t o = (size_t)u * MP * D + (size_t)row * D + col;
-        const float E = lam_v * zt[((size_t)u * D + col) * MP + row];
-        acc += (y[o] - E) * E;
-      }
+      for (int col = 0; col < D; ++col) acc += Fs[row * ES + col] * Es[row * ES + col];
     sdot[(size_t)u * MP + row] = acc;
   }
   // W = Q Q^T / d (bf16 products are exact; fp32 sums)
