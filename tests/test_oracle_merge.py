@@ -188,3 +188,46 @@ def test_end_to_end_tiny_config_properties():
     span_rate = len(span_tok & set(idx[0].tolist())) / len(span_tok)
     base_rate = (cfg.budget - cfg.window) / (cfg.n - cfg.window)
     assert span_rate > 3 * base_rate
+
+
+@pytest.mark.parametrize("seed,lam", [(0, 1e-2), (1, 0.3), (11, 2.0)])
+def test_discrepancy_closed_forms(seed, lam):
+    # Eq. 4 normalised by the target energy.  Before the merge the residual is
+    # R = Y - X V0, so D_before = ||R||^2 / ||Y||^2.  After it, Y - X V* = lam Z
+    # (App. D.1: X_G X_G^T Z = R - lam Z), so D_after = lam^2 ||Z||^2 / ||Y||^2.
+    X, Y, V0, F = _problem(seed)
+    dV, Z, R, _ = O.merge_dual(X, Y, V0, F, lam)
+    y2 = float(np.sum(Y ** 2))
+    np.testing.assert_allclose(O.discrepancy(Y, X, V0), np.sum(R ** 2) / y2, rtol=1e-12)
+    np.testing.assert_allclose(O.discrepancy(Y, X, V0 + dV), lam ** 2 * np.sum(Z ** 2) / y2,
+                               rtol=1e-9)
+
+
+def test_discrepancy_hand_values():
+    # worked by hand: Y = [3, 4] has ||Y||^2 = 25
+    Y = np.array([[3.0, 4.0]])
+    X = np.array([[1.0]])
+    assert O.discrepancy(Y, X, np.array([[0.0, 0.0]])) == 1.0          # 25 / 25
+    assert O.discrepancy(Y, X, np.array([[3.0, 0.0]])) == 16.0 / 25.0  # (0^2 + 4^2) / 25
+    assert O.discrepancy(Y, X, Y) == 0.0
+    # two rows, two retained slots: X V = [[1.5, 0], [0, 2]] against Y = [[1, 0], [0, 1]]
+    Y2 = np.eye(2)
+    X2 = np.array([[0.5, 0.5], [0.0, 1.0]])
+    V2 = np.array([[1.0, -2.0], [2.0, 2.0]])
+    # X2 V2 = [[1.5, 0.0], [2.0, 2.0]]; residual [[-0.5, 0], [-2, -1]] -> 0.25 + 4 + 1 = 5.25
+    assert O.discrepancy(Y2, X2, V2) == 5.25 / 2.0
+
+
+def test_discrepancy_single_row_merge_by_hand():
+    # the m = 1 case of test_single_row_closed_form, carried through to D:
+    # D_before = r^2 / y^2 and D_after = (lam z)^2 / y^2 with z = r / (sum_G x^2 + lam)
+    x = np.array([[0.5, 0.2, 0.3]])
+    V0 = np.array([[1.0], [2.0], [-1.0]])
+    Y = np.array([[0.7]])
+    F = np.array([False, True, False])
+    lam = 0.1
+    dV, Z, R, _ = O.merge_dual(x, Y, V0, F, lam)
+    r = 0.7 - 0.6
+    z = r / (0.25 + 0.09 + lam)
+    np.testing.assert_allclose(O.discrepancy(Y, x, V0), r * r / 0.49, rtol=1e-12)
+    np.testing.assert_allclose(O.discrepancy(Y, x, V0 + dV), (lam * z) ** 2 / 0.49, rtol=1e-12)
