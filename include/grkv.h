@@ -58,10 +58,11 @@ typedef enum { GRKV_BF16 = 0, GRKV_F32 = 1 } grkv_dtype;
 /* Per-unit status in stats[u][3]. */
 #define GRKV_UNIT_OK 0
 #define GRKV_UNIT_SINGULAR 1 /* non-positive Cholesky pivot: v_out holds V0 */
-#define GRKV_UNIT_RANGE 2    /* bf16 path: a window row's attention mass on the
+#define GRKV_UNIT_RANGE 2    /* internal: a window row's attention mass on the
                                 retained keys is below 2^-108 of its full-cache
-                                mass (outside the range the path resolves):
-                                v_out holds V0 */
+                                mass.  The bf16 path then redoes that unit's
+                                value step against the retained set's own row
+                                maxima, so a call never returns this code */
 
 typedef struct {
   int32_t units;    /* U >= 1: number of (layer, KV head) slices */
@@ -154,7 +155,7 @@ int grkv_compress(const void* q_obs, const void* K, const void* V, int64_t n,
                   float lambda, void* stream, const grkv_problem* prob,
                   const grkv_options* opt, const grkv_outputs* out);
 
-/* Key step of GRKV (Sec. 3.3 "Key step" and "Linearized dual solution",
+/* Key step of GRKV (Sec. 3.4 "Key step" and "Linearized dual solution",
  * Eq. 9-10; Algorithm 1, key step; App. D.2 and D.3), run by grkv_compress_kv
  * after the value step with the merged values V* held fixed and the keys at K0
  * (one alternating step, S = 1, the paper's default).  With f(K) =

@@ -5,7 +5,7 @@ TEST INFRASTRUCTURE ONLY, like ``grkv_oracle``: imported by the test suite,
 the smoke check and the benchmark's CPU-baseline leg, never by the product
 path, and sharing no code with the HIP path.
 
-The key step (Sec. 3.3 "Key step" and "Linearized dual solution", Eq. 9-10;
+The key step (Sec. 3.4 "Key step" and "Linearized dual solution", Eq. 9-10;
 Algorithm 1, key step; App. D.2 "Local Dual Key Update"; App. D.3 for fixed
 tokens), with the values V fixed at the value step's result:
 

@@ -1,5 +1,5 @@
 // Key step of GRKV on the bf16 path: the local linearized dual ridge update of
-// the free retained keys (Sec. 3.3 "Key step" and "Linearized dual solution",
+// the free retained keys (Sec. 3.4 "Key step" and "Linearized dual solution",
 // Eq. 9-10; Algorithm 1, key step; App. D.2 and D.3), run after the value step
 // with the merged values V* held fixed and K_cur = K0 (one alternating step).
 //

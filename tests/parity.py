@@ -70,7 +70,15 @@ def check_unit(cfg, q, K, V, gpu, u, slot=None, opt=None, report=None):
     d_eval = abs(O.discrepancy(r["Y"], r["X"], gpu["v_out"][slot].astype(np.float64))
                  - r["D_after"]) / max(r["D_after"], 1e-30)
     d_before = abs(st[1] - r["D_before"]) / max(r["D_before"], 1e-30)
-    info.update(d_rep=float(d_rep), d_eval=float(d_eval), d_before=float(d_before))
+    y2_err = abs(st[0] - r["y2"]) / max(r["y2"], 1e-30)
+    info.update(d_rep=float(d_rep), d_eval=float(d_eval), d_before=float(d_before),
+                y2_err=float(y2_err))
+    # stats[0] = ||Y||^2 and stats[1] = D_before (Eq. 4 at V0), same relative bar as D_after
+    assert y2_err <= D_TOL, "unit %d: ||Y||^2 rel err %.3e" % (u, y2_err)
+    if r["D_before"] > 1e-12:
+        assert d_before <= D_TOL, "unit %d: D_before rel err %.3e" % (u, d_before)
+    else:
+        assert st[1] <= 1e-6, "unit %d: D_before %.3e where the oracle has %.3e" % (u, st[1], r["D_before"])
     if r["D_after"] > 1e-12:
         assert d_rep <= D_TOL and d_eval <= D_TOL, "unit %d: D errs %.3e %.3e" % (u, d_rep, d_eval)
     else:

@@ -1,4 +1,4 @@
-"""Pins for the oracle's key step (Sec. 3.3 key step, Eq. 9-10; Algorithm 1, key
+"""Pins for the oracle's key step (Sec. 3.4 key step, Eq. 9-10; Algorithm 1, key
 step; App. D.2 local dual key update; App. D.3 fixed tokens).
 
 The key step linearizes f(K) = softmax(Q K^T / sqrt(d)) V around the current
