@@ -155,6 +155,25 @@ int grkv_compress(const void* q_obs, const void* K, const void* V, int64_t n,
                   float lambda, void* stream, const grkv_problem* prob,
                   const grkv_options* opt, const grkv_outputs* out);
 
+/* grkv_compress for callers that cannot allocate device memory (code under
+ * stream capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * same computation, kernels and arguments, but the workspace is a device array
+ * of GRKV_NOALLOC_SCRATCH_BYTES held by the library on every device it runs on
+ * (until the process ends); out->workspace and out->workspace_bytes are not
+ * read.  The call runs on the current device (stream must belong to it) and
+ * calls no allocating routine.  The first call on a device looks up the
+ * array's address there.  Every call on one device shares that array: calls
+ * that overlap on one device (several streams or host threads) race on it.
+ * Nothing in it needs to start at zero.  Errors: those of grkv_compress;
+ * GRKV_ERR_WORKSPACE when grkv_workspace_bytes() for the shape exceeds
+ * GRKV_NOALLOC_SCRATCH_BYTES (64 MiB holds, for example, a one-layer call of
+ * 8 KV heads, n = 32768, w = 32, budget 2048, d = 128: 54.5 MiB). */
+#define GRKV_NOALLOC_SCRATCH_BYTES (64ull << 20)
+int grkv_compress_noalloc(const void* q_obs, const void* K, const void* V, int64_t n,
+                          int32_t window, int32_t budget, int32_t pool_kernel,
+                          float lambda, void* stream, const grkv_problem* prob,
+                          const grkv_options* opt, const grkv_outputs* out);
+
 /* Key step of GRKV (Sec. 3.4 "Key step" and "Linearized dual solution",
  * Eq. 9-10; Algorithm 1, key step; App. D.2 and D.3), run by grkv_compress_kv
  * after the value step with the merged values V* held fixed and the keys at K0

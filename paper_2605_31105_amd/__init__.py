@@ -19,7 +19,7 @@ __all__ = [
     "intermediates", "EXPORTED_SYMBOLS", "KeyOptions", "workspace_bytes_kv", "compress_kv",
     "KEY_CONVERGED", "KEY_MAX_ITER", "KEY_SKIPPED", "KEY_BREAKDOWN", "carrier_stats",
     "CARRIER_METRICS", "compress_ragged", "pyramid_budgets", "adaptive_budgets",
-    "workspace_bytes_ragged",
+    "workspace_bytes_ragged", "compress_noalloc", "NOALLOC_SCRATCH_BYTES",
 ]
 
 GRKV_OK, GRKV_ERR_INVALID, GRKV_ERR_WORKSPACE, GRKV_ERR_UNSUPPORTED, GRKV_ERR_HIP = 0, -1, -2, -3, -4
@@ -31,7 +31,8 @@ EXPORTED_SYMBOLS = ("grkv_compress", "grkv_workspace_bytes", "grkv_workspace_lay
                     "grkv_default_options", "grkv_status_string", "grkv_compress_kv",
                     "grkv_workspace_bytes_kv", "grkv_default_key_options", "grkv_carrier_stats",
                     "grkv_compress_ragged", "grkv_workspace_bytes_ragged", "grkv_pyramid_budgets",
-                    "grkv_adaptive_budgets")
+                    "grkv_adaptive_budgets", "grkv_compress_noalloc")
+NOALLOC_SCRATCH_BYTES = 64 << 20
 KEY_CONVERGED, KEY_MAX_ITER, KEY_SKIPPED, KEY_BREAKDOWN = 1, 2, 3, 4
 CARRIER_METRICS = ("b", "b_eff", "a_max", "gini", "boundary_fraction", "boundary_share",
                    "enrichment", "boundary_interior_load")
@@ -93,6 +94,8 @@ def lib() -> ctypes.CDLL:
                                     ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
                                     ctypes.c_int32, ctypes.c_float, ctypes.c_void_p,
                                     P(Problem), P(Options), P(Outputs)]
+        L.grkv_compress_noalloc.restype = ctypes.c_int
+        L.grkv_compress_noalloc.argtypes = L.grkv_compress.argtypes
         L.grkv_workspace_bytes.restype = ctypes.c_size_t
         L.grkv_workspace_bytes.argtypes = [P(Problem), ctypes.c_int64, ctypes.c_int32, ctypes.c_int32]
         L.grkv_workspace_layout.restype = ctypes.c_int
@@ -244,6 +247,50 @@ def compress(q_obs, K, V, window: int, budget: int, pool_kernel: int, lam: float
                              pool_kernel, float(lam), ctypes.c_void_p(handle),
                              ctypes.byref(prob), ctypes.byref(opt), ctypes.byref(outs))
     _check(st)
+    return out
+
+
+def compress_noalloc(q_obs, K, V, window: int, budget: int, pool_kernel: int, lam: float, *,
+                     out: Result, n_sink: int = 4, beta: float = 0.10, fix_window: bool = True,
+                     causal_window: bool = True, stream=None) -> Result:
+    """``compress`` through the entry point that allocates nothing: the
+    library's own per-device scratch array (NOALLOC_SCRATCH_BYTES) serves as the
+    workspace.  ``out`` (a Result with idx, k_out, v_out and stats of the
+    right shapes) is required, so this call allocates no device memory either.
+    Calls that overlap on one device race on the shared scratch array."""
+    import torch
+
+    if not (q_obs.is_cuda and K.is_cuda and V.is_cuda):
+        raise ValueError("q_obs, K and V must be device tensors")
+    if not (q_obs.dtype == K.dtype == V.dtype) or K.dtype not in (torch.bfloat16, torch.float32):
+        raise ValueError("q_obs, K, V must share dtype bfloat16 or float32")
+    if not (q_obs.is_contiguous() and K.is_contiguous() and V.is_contiguous()):
+        raise ValueError("inputs must be contiguous")
+    U, G, w, d = q_obs.shape
+    if w != window or K.shape[0] != U or K.shape[2] != d or V.shape != K.shape:
+        raise ValueError("shape mismatch: q_obs %s K %s V %s window %d"
+                         % (tuple(q_obs.shape), tuple(K.shape), tuple(V.shape), window))
+    n = K.shape[1]
+    if (tuple(out.idx.shape) != (U, budget) or tuple(out.k_out.shape) != (U, budget, d)
+            or tuple(out.v_out.shape) != (U, budget, d) or tuple(out.stats.shape) != (U, 4)
+            or out.k_out.dtype != K.dtype or out.v_out.dtype != torch.float32
+            or out.idx.dtype != torch.int32 or out.stats.dtype != torch.float32):
+        raise ValueError("out tensors do not match the call's shapes")
+    dt = GRKV_BF16 if K.dtype == torch.bfloat16 else GRKV_F32
+    prob = Problem(U, G, d, dt)
+    opt = Options(n_sink, beta, 1 if fix_window else 0, 1 if causal_window else 0)
+    outs = Outputs(out.idx.data_ptr(), out.k_out.data_ptr(), out.v_out.data_ptr(),
+                   out.stats.data_ptr(), None, 0, None)
+    if stream is None:
+        stream = torch.cuda.current_stream(K.device)
+    handle = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+    with torch.cuda.device(K.device):
+        st = lib().grkv_compress_noalloc(q_obs.data_ptr(), K.data_ptr(), V.data_ptr(), n, window,
+                                         budget, pool_kernel, float(lam), ctypes.c_void_p(handle),
+                                         ctypes.byref(prob), ctypes.byref(opt), ctypes.byref(outs))
+    _check(st)
+    out.workspace = None
+    out.shape = (U, G, d, dt, n, window, budget)
     return out
 
 

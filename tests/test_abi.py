@@ -188,3 +188,35 @@ def test_front_end_arguments_rejected(L):
     assert L.grkv_workspace_bytes_ragged(ctypes.byref(prob), 2048, 32, b) == 0
     b = (ctypes.c_int32 * 2)(64, 128)
     assert L.grkv_workspace_bytes_ragged(ctypes.byref(prob), 2048, 32, b) > 0
+
+
+def _call_noalloc(L, U=2, Gq=4, d=128, dt=0, n=8192, w=32, c=512, k=7, lam=1e-2, opt=None,
+                  nullq=False):
+    prob = G.Problem(U, Gq, d, dt)
+    fake = ctypes.c_void_p(4096)   # never dereferenced: validation fails first
+    outs = G.Outputs(4096, 4096, 4096, 0, None, 0)
+    return L.grkv_compress_noalloc(None if nullq else fake, fake, fake, n, w, c, k, lam, None,
+                                   ctypes.byref(prob), ctypes.byref(opt) if opt else None,
+                                   ctypes.byref(outs))
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(nullq=True), G.GRKV_ERR_INVALID),
+    (dict(U=0), G.GRKV_ERR_INVALID),
+    (dict(c=16), G.GRKV_ERR_INVALID),
+    (dict(k=4), G.GRKV_ERR_INVALID),
+    (dict(lam=math.nan), G.GRKV_ERR_INVALID),
+    (dict(opt=G.Options(4, 1.5, 1, 1)), G.GRKV_ERR_INVALID),
+    (dict(d=96), G.GRKV_ERR_UNSUPPORTED),
+    # 256 units of the 32k Llama-shaped workload need ~243 MiB > the 64 MiB array
+    (dict(U=256, n=32768, c=2048), G.GRKV_ERR_WORKSPACE),
+    (dict(U=8, n=131072, w=64, c=4096), G.GRKV_ERR_WORKSPACE),
+])
+def test_noalloc_rejects_before_touching_the_device(L, kw, code):
+    assert _call_noalloc(L, **kw) == code
+
+
+def test_noalloc_scratch_holds_a_one_layer_32k_call(L):
+    prob = G.Problem(8, 4, 128, G.GRKV_BF16)
+    need = L.grkv_workspace_bytes(ctypes.byref(prob), 32768, 32, 2048)
+    assert 0 < need <= G.NOALLOC_SCRATCH_BYTES
