@@ -55,6 +55,8 @@ def parse():
                     help="skip the ragged-budget front-end timings")
     ap.add_argument("--no-carrier", dest="carrier", action="store_false",
                     help="skip the carrier-concentration measurement")
+    ap.add_argument("--no-configs", dest="configs", action="store_false",
+                    help="skip the one-layer 32k and 4-layer 128k workloads")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a 1 GiB device copy (for counter calibration)")
@@ -101,26 +103,51 @@ def copy_calibration():
     print(json.dumps({"copy_calibration_bytes": 2 ** 30, "launches": 5}), flush=True)
 
 
-def cpu_baseline(cfg, q, K, V, seconds):
-    """The oracle as it stands, on a bounded sample of whole units."""
-    import numpy as np
-    import workloads as W
-    from oracle import grkv_oracle as O
+def blas_threads():
+    """Threads the oracle's numpy linear algebra runs on (its matmuls are the
+    only multi-threaded part of it)."""
     try:
         from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        return int(max([i.get("num_threads", 1) for i in threadpool_info()] or [1]))
     except Exception:
-        threads = 1
+        return 1
+
+
+def host_info():
+    """The host the oracle is timed on: usable cores and the CPU model."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"host_cores": len(os.sched_getaffinity(0)), "cpu_model": model}
+
+
+def oracle_record(done, total, el, what, unit="heads/s", per=1.0):
+    rec = {"value": per * done / el, "unit": unit, "cores": blas_threads(), "kind": "oracle",
+           "sample": "%d of %d %s, %.1f s" % (done, total, what, el),
+           "label": "plain fp64 reference, not an optimized CPU implementation"}
+    rec.update(host_info())
+    return rec
+
+
+def cpu_baseline(cfg, q, K, V, seconds, units=None):
+    """The oracle as it stands, on a bounded sample of whole units."""
+    import workloads as W
+    from oracle import grkv_oracle as O
+    units = list(range(cfg.units)) if units is None else list(units)
     done, t0 = 0, time.perf_counter()
-    while done < cfg.units and (done < 2 or time.perf_counter() - t0 < seconds):
-        u = done
+    while done < len(units) and (done < 2 or time.perf_counter() - t0 < seconds):
+        u = units[done]
         qd, Kd, Vd = (W.decode(a[u], cfg.dtype) for a in (q, K, V))
         O.compress_unit(qd, Kd, Vd, cfg.window, cfg.budget, cfg.pool_kernel, cfg.lam)
         done += 1
     el = time.perf_counter() - t0
-    return {"value": done / el, "unit": "heads/s", "cores": int(threads), "kind": "oracle",
-            "sample": "%d of %d units (whole units, float64 numpy oracle), %.1f s"
-                      % (done, cfg.units, el)}
+    return oracle_record(done, cfg.units, el, "units (whole units, float64 numpy oracle)")
 
 
 def cpu_baseline_key(cfg, q, K, V, seconds):
@@ -128,20 +155,14 @@ def cpu_baseline_key(cfg, q, K, V, seconds):
     on a bounded sample of whole units."""
     import workloads as W
     from oracle import grkv_key_oracle as KO
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        threads = 1
     done, t0 = 0, time.perf_counter()
     while done < cfg.units and (done < 2 or time.perf_counter() - t0 < seconds):
         qd, Kd_, Vd_ = (W.decode(a[done], cfg.dtype) for a in (q, K, V))
         KO.grkv_unit(qd, Kd_, Vd_, cfg.window, cfg.budget, cfg.pool_kernel, cfg.lam, cfg.lam)
         done += 1
     el = time.perf_counter() - t0
-    return {"value": done / el, "unit": "heads/s", "cores": int(threads), "kind": "oracle",
-            "sample": "%d of %d units (whole units: value and key step, float64 numpy oracle), %.1f s"
-                      % (done, cfg.units, el)}
+    return oracle_record(done, cfg.units, el,
+                         "units (whole units: value and key step, float64 numpy oracle)")
 
 
 def carrier(args, cfg, G, hip, stream, Kd, res, host=None):
@@ -184,8 +205,7 @@ def carrier(args, cfg, G, hip, stream, Kd, res, host=None):
                                idx[done])
             done += 1
         el = time.perf_counter() - t0
-        cpu = {"value": done / el, "unit": "heads/s", "cores": 16, "kind": "oracle",
-               "sample": "%d of %d units (float64 numpy oracle), %.1f s" % (done, U, el)}
+        cpu = oracle_record(done, U, el, "units (float64 numpy oracle)")
     return {
         "ms_per_call": ms,
         "heads_per_s": U / (ms / 1e3),
@@ -271,9 +291,10 @@ def front_ends(args, cfg, G, hip, stream, qd, Kd, Vd, res, host=None):
             FO.adaptive_budgets(pl[done * H:(done + 1) * H], 1, H, c, w)
             done += 1
         el = time.perf_counter() - t0
-        out["adaptive_allocation"]["cpu_baseline"] = {
-            "value": done / el, "unit": "layers/s", "cores": 1, "kind": "oracle",
-            "sample": "%d of %d layers (float64 numpy lexsort), %.1f s" % (done, cfg.layers, el)}
+        rec = oracle_record(done, cfg.layers, el, "layers (float64 numpy lexsort)",
+                            unit="layers/s")
+        rec["cores"] = 1   # a sort: numpy runs it on one thread
+        out["adaptive_allocation"]["cpu_baseline"] = rec
         out["adaptive_allocation"]["layers_per_s"] = cfg.layers / (ms_alloc / 1e3)
     return out
 
@@ -360,6 +381,75 @@ def key_step(args, cfg, G, hip, stream, qd, Kd, Vd, host=None):
     }
 
 
+def path_bytes_per_unit(cfg):
+    """Algorithmic bytes of one unit: read K, V and q_obs once, write idx,
+    k_out (input dtype) and v_out (fp32) once."""
+    esz = 2 if cfg.dtype == "bf16" else 4
+    n, d, c, m = cfg.n, cfg.head_dim, cfg.budget, cfg.group * cfg.window
+    return 2 * n * d * esz + m * d * esz + c * 4 + c * d * esz + c * d * 4
+
+
+def other_configs(args, G, hip, stream, want_cpu):
+    """The other workloads of the benchmark spec, each timed as one call over all
+    of its units (the same measurement as the headline, at their sizes): the
+    one-layer 32k cache at budgets 1024 and 2048, and the 4-layer 128k cache
+    (window 64, so m = 256 stacked rows), with the oracle timed on a bounded
+    sample of each."""
+    import numpy as np
+    import torch
+    import workloads as W
+
+    out = {}
+    full_prob = G.STAGES.index("full_prob")
+    for key, cfg in (("llama3-8b-layer-n32k-c1024", W.config(3, budget=1024)),
+                     ("llama3-8b-layer-n32k-c2048", W.config(3, budget=2048)),
+                     ("llama3-8b-4layer-n128k", W.config(5))):
+        print("bench: %s (%d units, n=%d, c=%d)" % (key, cfg.units, cfg.n, cfg.budget),
+              file=sys.stderr, flush=True)
+        q, K, V = W.make_batch(cfg)
+        qd, Kd, Vd = (torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
+                      for a in (q, K, V))
+        w, c = cfg.window, cfg.budget
+        res = G.compress(qd, Kd, Vd, w, c, cfg.pool_kernel, cfg.lam)
+        for _ in range(args.warmup):
+            G.compress(qd, Kd, Vd, w, c, cfg.pool_kernel, cfg.lam, workspace=res.workspace, out=res)
+        torch.cuda.synchronize()
+        reps = max(3, min(args.steps, 10))
+        evs = []
+        for _ in range(reps):
+            arr = (ctypes.c_void_p * (2 * G.NUM_STAGES))()
+            a, b = hip.event(), hip.event()
+            arr[2 * full_prob], arr[2 * full_prob + 1] = a.value, b.value
+            evs.append((arr, a, b))
+        c0, c1 = hip.event(), hip.event()
+        hip.lib.hipEventRecord(c0, ctypes.c_void_p(stream.cuda_stream))
+        for arr, _, _ in evs:
+            G.compress(qd, Kd, Vd, w, c, cfg.pool_kernel, cfg.lam, workspace=res.workspace,
+                       out=res, stage_events=arr)
+        hip.lib.hipEventRecord(c1, ctypes.c_void_p(stream.cuda_stream))
+        torch.cuda.synchronize()
+        ms = hip.elapsed_ms(c0, c1) / reps
+        fp_ms = float(np.mean([hip.elapsed_ms(a, b) for _, a, b in evs]))
+        esz = 2
+        fp_bytes = cfg.units * (2 * cfg.n * cfg.head_dim * esz + cfg.group * w * cfg.head_dim * esz)
+        path = cfg.units * path_bytes_per_unit(cfg)
+        rec = {"units": cfg.units, "n": cfg.n, "window": w, "budget": c, "m": cfg.group * w,
+               "ms_per_call": ms, "ms_per_layer": ms / cfg.layers,
+               "heads_per_s": cfg.units / (ms / 1e3),
+               "roofline": {"bound": "hbm", "kernel": "full_prob",
+                            "achieved": fp_bytes / (fp_ms / 1e3) / 1e9, "peak": HBM_PEAK_GBS,
+                            "unit": "GB/s",
+                            "frac": fp_bytes / (fp_ms / 1e3) / 1e9 / HBM_PEAK_GBS,
+                            "path_frac": path / (ms / 1e3) / 1e9 / HBM_PEAK_GBS,
+                            "traffic": None}}
+        if want_cpu:
+            rec["cpu_baseline"] = cpu_baseline(cfg, q, K, V, min(args.cpu_seconds, 6.0))
+        out[key] = rec
+        del res, qd, Kd, Vd, q, K, V
+        torch.cuda.empty_cache()
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -436,7 +526,7 @@ def main():
     esz = 2 if cfg.dtype == "bf16" else 4
     kv_bytes = 2 * n * d * esz
     q_bytes = m * d * esz
-    path_bytes = kv_bytes + q_bytes + c * 4 + c * d * esz + c * d * 4
+    path_bytes = path_bytes_per_unit(cfg)
     alg = {"full_prob": U * (kv_bytes + q_bytes), "full_lse": U * (n * d * esz + q_bytes)}
     dom = max(stage_ms, key=stage_ms.get)
     achieved = alg[dom] / (stage_ms[dom] / 1e3) / 1e9
@@ -505,6 +595,12 @@ def main():
         print("bench: timing the oracle on the host", file=sys.stderr, flush=True)
         cpu = cpu_baseline(cfg, q, K, V, args.cpu_seconds)
 
+    path_gbs = U * path_bytes / (ms_step / 1e3) / 1e9
+    others = None
+    if args.configs and args.config == 4:
+        del q, K, V
+        others = other_configs(args, G, hip, stream, not args.no_cpu_baseline)
+
     line = {
         "metric": METRIC,
         "value": heads_s,
@@ -524,17 +620,21 @@ def main():
                    "query_heads": cfg.kv_heads * Gq, "head_dim": d, "n": n, "window": w,
                    "budget": c, "pool_kernel": cfg.pool_kernel, "lambda": cfg.lam,
                    "units": U},
-        "path_hbm_frac": (U * path_bytes / (ms_step / 1e3) / 1e9) / HBM_PEAK_GBS,
+        "path_hbm_frac": path_gbs / HBM_PEAK_GBS,
         "copy_gbs": copy_gbs,
         "per_layer_calls": per_layer,
         "stage_ms": stage_ms,
         "roofline": {"bound": "hbm", "kernel": dom, "achieved": achieved,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "frac_of_copy": achieved / copy_gbs,
-                     "traffic": traffic},
+                     "traffic": traffic,
+                     # the whole call: every unit's algorithmic bytes over the step time
+                     "path_achieved": path_gbs, "path_frac": path_gbs / HBM_PEAK_GBS,
+                     "path_bytes_per_unit": path_bytes},
         "key_step": key,
         "carrier": car,
         "front_ends": fe,
+        "configs": others,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

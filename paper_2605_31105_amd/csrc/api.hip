@@ -347,9 +347,16 @@ int run_compress(const Plan& p, const void* q_obs, const void* K, const void* V,
                              (const uint16_t*)(ws + p.zlo), F(p.stats_ws),
                              V, out->idx, out->v_out, s));
   } else {
-    GRKV_STAGE(GRKV_STAGE_SOLVE, launch_cholesky_solve(p, F(p.npart), F(p.y), F(p.resid),
-                                                       F(p.gram), F(p.z), F(p.stats_ws),
-                                                       out->stats, s));
+    // 256 stacked rows: blocked MFMA factorisation (block-packed in LDS);
+    // otherwise the column-by-column one
+    if (solve_big_supported(p))
+      GRKV_STAGE(GRKV_STAGE_SOLVE, launch_solve_big(p, F(p.npart), F(p.y), F(p.resid),
+                                                    F(p.gram), F(p.z), F(p.stats_ws),
+                                                    out->stats, s));
+    else
+      GRKV_STAGE(GRKV_STAGE_SOLVE, launch_cholesky_solve(p, F(p.npart), F(p.y), F(p.resid),
+                                                         F(p.gram), F(p.z), F(p.stats_ws),
+                                                         out->stats, s));
     GRKV_STAGE(GRKV_STAGE_UPDATE,
                launch_update_add(p, F(p.x), fixed, F(p.z), F(p.stats_ws), out->v_out, s));
   }

@@ -179,6 +179,12 @@ hipError_t launch_cholesky_solve(const Plan& p, const float* npart,
                                  const float* y, const float* resid,
                                  float* gram, float* z, float* stats_ws,
                                  float* stats_user, hipStream_t s);
+// The same solve for mp = 256 (G * w in (128, 256]) with d 64 or 128: blocked
+// MFMA factorisation of N held block-packed in LDS, one 8-wave block per unit.
+bool solve_big_supported(const Plan& p);
+hipError_t launch_solve_big(const Plan& p, const float* npart, const float* y,
+                            const float* resid, float* gram, float* z, float* stats_ws,
+                            float* stats_user, hipStream_t s);
 hipError_t launch_update_add(const Plan& p, const float* x, const uint8_t* fixed,
                              const float* z, const float* stats_ws, float* v_out,
                              hipStream_t s);
