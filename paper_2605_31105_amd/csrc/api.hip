@@ -284,7 +284,7 @@ int run_compress(const Plan& p, const void* q_obs, const void* K, const void* V,
   const bool direct = fast && fast_merge;
   if (!direct)
     GRKV_STAGE(GRKV_STAGE_GATHER, launch_gather(p, K, V, out->idx, out->k_out, ws + p.v0c,
-                                                fast_merge ? nullptr : out->v_out, s));
+                                                nullptr, s));
   // 3. window attention over the retained cache: X and X V0, then R = Y - X V0
   AttnPass ret = {};
   ret.q = q_obs; ret.k = out->k_out; ret.v = ws + p.v0c; ret.kpos = out->idx; ret.nk = p.c;
@@ -358,7 +358,8 @@ int run_compress(const Plan& p, const void* q_obs, const void* K, const void* V,
                                                          F(p.gram), F(p.z), F(p.stats_ws),
                                                          out->stats, s));
     GRKV_STAGE(GRKV_STAGE_UPDATE,
-               launch_update_add(p, F(p.x), fixed, F(p.z), F(p.stats_ws), out->v_out, s));
+               launch_update_gen(p, F(p.x), fixed, F(p.z), F(p.stats_ws), ws + p.v0c,
+                                 out->v_out, s));
   }
 #undef GRKV_STAGE
 #undef GRKV_TRY

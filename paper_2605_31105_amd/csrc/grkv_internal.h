@@ -185,6 +185,12 @@ bool solve_big_supported(const Plan& p);
 hipError_t launch_solve_big(const Plan& p, const float* npart, const float* y,
                             const float* resid, float* gram, float* z, float* stats_ws,
                             float* stats_user, hipStream_t s);
+// v_out = V0 + X_G^T Z over every retained slot from the stored X [U][mp][c],
+// Z^T and the compact V0 copy v0c (input dtype), for the generic value step
+// (any dtype, mp up to 256, d 64/128); fixed slots and singular units get V0.
+hipError_t launch_update_gen(const Plan& p, const float* x, const uint8_t* fixed, const float* z,
+                             const float* stats_ws, const void* v0c, float* v_out,
+                             hipStream_t s);
 hipError_t launch_update_add(const Plan& p, const float* x, const uint8_t* fixed,
                              const float* z, const float* stats_ws, float* v_out,
                              hipStream_t s);

@@ -1,8 +1,11 @@
 // Generic value-step kernels for shapes outside the fast path (float32
-// inputs, or m > 128 rows): Cholesky of N in LDS (packed lower triangle, the
-// right-hand sides in LDS when they fit and in the z buffer otherwise), then
-// V* = V0 + X_G^T Z added into v_out, which the gather filled with V0.
-// Same arithmetic contract as merge.hip; slower, latency-bound per unit.
+// inputs, or m > 128 rows), which store X: Cholesky of N in LDS (packed lower
+// triangle, the right-hand sides in LDS when they fit and in the z buffer
+// otherwise; 256 rows have a blocked solve of their own), then
+// V* = V0 + X_G^T Z over every retained slot from X, Z^T and the compact V0
+// copy.  update_add_kernel adds X_G^T Z into a v_out that already holds V0
+// (the later alternating steps of the key-step entry point).  Same arithmetic
+// contract as merge.hip.
 #include "grkv_device.h"
 #include "grkv_internal.h"
 
@@ -174,7 +177,148 @@ __global__ __launch_bounds__(256) void update_add_kernel(const float* x, const u
   }
 }
 
+// v_out = V0 + X_G^T Z for 256 retained slots per block (fixed slots, and
+// every slot of a unit whose system was singular, get V0), from the stored X
+// [mp][c] and Z^T.  Z^T goes to LDS once per block as bf16 hi/lo pairs, its
+// row dd at (dd mod DT) * 16 + dd / DT (DT = D / 16 output tiles), which hands
+// each lane DT consecutive output columns: V0 and v_out move in 16-byte
+// pieces.  Each wave takes 32 slots (two 16-slot tiles); a lane reads the X
+// values of its slot straight from global memory (8 rows of one column per
+// MFMA step: across the 16 lanes of a row, 64 contiguous bytes), masked by the
+// slot's fixed flag and split into bf16 hi/lo.  Products are three bf16 MFMAs
+// (hi hi, hi lo, lo hi) with fp32 accumulation.
+constexpr int kUpdGenWaves = 8;
+constexpr int kUpdGenSlots = 32 * kUpdGenWaves;
+
+template <typename T, int MP, int D>
+__global__ __launch_bounds__(kUpdGenWaves * 64) void update_gen_kernel(
+    const float* x, const uint8_t* fixed, const float* z, const float* stats_ws, const T* v0c,
+    float* v_out, int m, int c) {
+  constexpr int DT = D / 16;
+  constexpr int ZS = MP + 8;   // LDS row stride (bf16) of Z^T rows
+  constexpr int NTH = kUpdGenWaves * 64;
+  __shared__ __attribute__((aligned(16))) u16 zh[D * ZS];
+  __shared__ __attribute__((aligned(16))) u16 zl[D * ZS];
+  const int u = blockIdx.y, t0 = blockIdx.x * kUpdGenSlots;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l16 = lane & 15, g = lane >> 4;
+  const bool singular = stats_ws[u * 4 + 3] != 0.f;   // block-uniform
+  const uint8_t* fu = fixed + (size_t)u * c;
+
+  if (!singular) {
+    const float* zu = z + (size_t)u * D * MP;
+    for (int e = tid; e < D * (MP / 4); e += NTH) {
+      const int dd = e / (MP / 4), r0 = 4 * (e % (MP / 4));
+      const float4 v = *reinterpret_cast<const float4*>(zu + (size_t)dd * MP + r0);
+      const float vv[4] = {v.x, v.y, v.z, v.w};
+      u16 hh[4], ll[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const __bf16 h = (__bf16)vv[i];
+        hh[i] = __builtin_bit_cast(u16, h);
+        ll[i] = __builtin_bit_cast(u16, (__bf16)(vv[i] - (float)h));
+      }
+      const int row = (dd % DT) * 16 + dd / DT;
+      *reinterpret_cast<uint2*>(zh + row * ZS + r0) =
+          make_uint2(hh[0] | ((uint32_t)hh[1] << 16), hh[2] | ((uint32_t)hh[3] << 16));
+      *reinterpret_cast<uint2*>(zl + row * ZS + r0) =
+          make_uint2(ll[0] | ((uint32_t)ll[1] << 16), ll[2] | ((uint32_t)ll[3] << 16));
+    }
+  }
+  __syncthreads();
+
+  const int tb = t0 + 32 * wave;   // this wave's first slot
+  f32x4 acc[2][DT];
+#pragma unroll
+  for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) acc[tt][dt] = zero4();
+  if (!singular && tb < c) {
+    const float* xu = x + (size_t)u * MP * c;
+    float keep[2];   // 1 for a free slot inside the retained set, else 0
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt) {
+      const int t = tb + 16 * tt + l16;
+      keep[tt] = (t < c && !fu[t]) ? 1.f : 0.f;
+    }
+#pragma unroll 1
+    for (int r0 = 0; r0 < MP; r0 += 32) {
+      bf16x8 ah[2], al[2];
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt) {
+        const int t = min(tb + 16 * tt + l16, c - 1);
+        float xv[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int r = r0 + 8 * g + e;
+          xv[e] = r < m ? keep[tt] * xu[(size_t)r * c + t] : 0.f;
+        }
+        split8(xv, ah[tt], al[tt]);
+      }
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const int zo = (dt * 16 + l16) * ZS + r0 + 8 * g;
+        const bf16x8 bh = as_bf16x8(*reinterpret_cast<const uint4*>(zh + zo));
+        const bf16x8 bl = as_bf16x8(*reinterpret_cast<const uint4*>(zl + zo));
+#pragma unroll
+        for (int tt = 0; tt < 2; ++tt) {
+          acc[tt][dt] = mfma_bf16(ah[tt], bh, acc[tt][dt]);
+          acc[tt][dt] = mfma_bf16(ah[tt], bl, acc[tt][dt]);
+          acc[tt][dt] = mfma_bf16(al[tt], bh, acc[tt][dt]);
+        }
+      }
+    }
+  }
+  // lane holds dV[slot = tb + 16tt + 4g + i][dd = l16 * DT + dt]; V0 from the
+  // compact copy, every slot of the block written
+#pragma unroll
+  for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int t = tb + 16 * tt + 4 * g + i;
+      if (t >= c) continue;
+      const bool upd = !singular && !fu[t];
+      const T* src = v0c + ((size_t)u * c + t) * D + l16 * DT;
+      float v[DT];
+#pragma unroll
+      for (int k = 0; k < DT; ++k) {
+        if constexpr (sizeof(T) == 2) v[k] = bf16_to_f32(src[k]);
+        else v[k] = (float)src[k];
+      }
+      if (upd) {
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) v[dt] += acc[tt][dt][i];
+      }
+      float* dst = v_out + ((size_t)u * c + t) * D + l16 * DT;
+#pragma unroll
+      for (int k = 0; k < DT / 4; ++k)
+        *reinterpret_cast<float4*>(dst + 4 * k) = make_float4(v[4 * k], v[4 * k + 1], v[4 * k + 2], v[4 * k + 3]);
+    }
+}
+
+template <typename T, int MP, int D>
+hipError_t launch_update_gen_t(const Plan& p, const float* x, const uint8_t* fixed, const float* z,
+                               const float* stats_ws, const void* v0c, float* v_out,
+                               hipStream_t s) {
+  const dim3 grid((p.c + kUpdGenSlots - 1) / kUpdGenSlots, p.U);
+  hipLaunchKernelGGL((update_gen_kernel<T, MP, D>), grid, dim3(kUpdGenWaves * 64), 0, s, x, fixed,
+                     z, stats_ws, (const T*)v0c, v_out, p.m, p.c);
+  return hipGetLastError();
+}
+
 }  // namespace
+
+hipError_t launch_update_gen(const Plan& p, const float* x, const uint8_t* fixed, const float* z,
+                             const float* stats_ws, const void* v0c, float* v_out, hipStream_t s) {
+#define GRKV_UG(MPV, DV)                                                                      \
+  if (p.mp == MPV && p.d == DV)                                                               \
+    return p.dtype == GRKV_BF16                                                               \
+               ? launch_update_gen_t<u16, MPV, DV>(p, x, fixed, z, stats_ws, v0c, v_out, s)   \
+               : launch_update_gen_t<float, MPV, DV>(p, x, fixed, z, stats_ws, v0c, v_out, s);
+  GRKV_UG(32, 64) GRKV_UG(32, 128) GRKV_UG(64, 64) GRKV_UG(64, 128) GRKV_UG(128, 64)
+  GRKV_UG(128, 128) GRKV_UG(256, 64) GRKV_UG(256, 128)
+#undef GRKV_UG
+  return hipErrorInvalidValue;
+}
 
 static size_t chol_lds_bytes(int mp, int D, bool* w_in_lds) {
   size_t tri_f = ((size_t)mp * (mp + 1) / 2 + 3) & ~(size_t)3;

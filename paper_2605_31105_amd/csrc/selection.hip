@@ -43,98 +43,254 @@ __device__ __forceinline__ UnitSel unit_sel(const SelK& a, int u) {
   return r;
 }
 
-// Band of candidates around a threshold, as refine_boundary below describes
-// (that is the form for keys held in registers); here each thread scans the
-// contiguous positions [j0, j1) of the pooled scores in memory.  With
-// big == false the band's positions (ascending) and take flags are in `bt`
-// and `boff` is where this thread's band entries start.
 constexpr uint32_t kBandUlps = 16;
 constexpr uint32_t kBandCap = 1024;
 
-struct BandRule {
-  uint32_t T, lo, hi, krem;   // krem: ties at T taken when the band is too big
-  bool big;
-  uint32_t boff;
-  const uint32_t* take;
-};
+// ---------------------------------------------------------------------------
+// Selection for prefixes too long for registers (or pools too wide for the
+// register kernel), one 1024-thread block per unit, the pooled scores held in
+// global memory (a unit's 512 KB at n = 128k stays in the L2 cache).  Every
+// sweep over them is block-strided (position j = j0 + q * 1024, coalesced)
+// with 16 loads in flight per thread; nothing depends on a thread owning a
+// contiguous run of positions:
+//  1. pooling, through LDS in rounds of positions;
+//  2. both thresholds at once (the (c-w)-th largest pooled score T0 and the
+//     floor(beta*c)-th largest T1): each round splits each bracket at 15
+//     pivots and counts every key against them in one sweep (no histogram
+//     atomics: the scores crowd into a few exponent bins), until at most
+//     kLargeCand keys remain inside; those go to LDS and 8-bit radix rounds
+//     on their offsets finish;
+//  3. the boundary band of each threshold (keys within kBandUlps units in the
+//     last place of it) is collected in any order and ranked by the pooled
+//     sum recomputed in fp64 from the fp32 column sums, then by position (as
+//     the register kernel's refine_boundary does); a band of more than
+//     kBandCap keys keeps the fp32 order with ties to the lower positions;
+//  4. per segment of 131072 positions: the taken positions are marked in an
+//     LDS bitmap (keys above the band, band entries taken, ties taken), and
+//     one block scan over the bitmap words writes them in ascending order.
+constexpr uint32_t kLargeCand = 4096;
+constexpr int kWays = 16;
+constexpr int kLoadBatch = 16;
+constexpr int kSegBits = 131072;                   // positions per bitmap segment
+constexpr int kSegWords = kSegBits / 32;
+constexpr int kWordsPerThread = kSegWords / kSelectThreads;
 
-__device__ BandRule band_rule(const float* p, uint32_t T, uint32_t k, const float* s, int j0,
-                              int j1, int P, int h, char* work, uint32_t* scan_scratch) {
-  BandRule r;
-  r.T = T;
-  r.lo = T > kBandUlps ? T - kBandUlps : 0u;
-  r.hi = T < 0x7F800000u - kBandUlps ? T + kBandUlps : 0x7F800000u;
-  uint32_t nabove = 0, nband = 0, ngt = 0, neq = 0;
-  for (int j = j0; j < j1; ++j) {
-    const uint32_t key = __float_as_uint(p[j]);
-    nabove += key > r.hi;
-    nband += key >= r.lo && key <= r.hi;
-    ngt += key > T;
-    neq += key == T;
+// keys of positions j0 + q * kSelectThreads (a block-strided sweep); keys past
+// the end read as 0
+__device__ __forceinline__ void load_strided(const float* p, int j0, int P, uint32_t (&k)[kLoadBatch]) {
+#pragma unroll
+  for (int q = 0; q < kLoadBatch; ++q) {
+    const int j = j0 + q * kSelectThreads;
+    k[q] = j < P ? __float_as_uint(p[j]) : 0u;
   }
-  uint32_t tot_above, tot_band, tot_gt, tot_eq;
-  block_exclusive_scan(nabove, scan_scratch, &tot_above);
-  r.boff = block_exclusive_scan(nband, scan_scratch, &tot_band);
-  block_exclusive_scan(ngt, scan_scratch, &tot_gt);
-  r.krem = block_exclusive_scan(neq, scan_scratch, &tot_eq);   // this thread's first tie index
-  r.krem = (k - tot_gt) > r.krem ? (k - tot_gt) - r.krem : 0u;  // ties this thread may take
-  r.big = tot_band > kBandCap;
-  double* v64 = reinterpret_cast<double*>(work);
-  int32_t* bpos = reinterpret_cast<int32_t*>(v64 + kBandCap);
-  uint32_t* btake = reinterpret_cast<uint32_t*>(bpos + kBandCap);
-  r.take = btake;
-  if (r.big) return r;
-  const uint32_t need = k - tot_above;
-  {
-    uint32_t o = r.boff;
-    for (int j = j0; j < j1; ++j) {
-      const uint32_t key = __float_as_uint(p[j]);
-      if (key >= r.lo && key <= r.hi) bpos[o++] = j;
-    }
-  }
-  __syncthreads();
-  for (uint32_t e = threadIdx.x; e < tot_band; e += blockDim.x) {
-    const int j = bpos[e];
-    const int t0 = j - h < 0 ? 0 : j - h, t1 = j + h > P - 1 ? P - 1 : j + h;
-    double acc = 0.0;
-    for (int t = t0; t <= t1; ++t) acc += (double)s[t];   // left to right
-    v64[e] = acc;
-  }
-  __syncthreads();
-  for (uint32_t e = threadIdx.x; e < tot_band; e += blockDim.x) {
-    const double v = v64[e];
-    const int j = bpos[e];
-    uint32_t rank = 0;
-    for (uint32_t f = 0; f < tot_band; ++f) {
-      const double w = v64[f];
-      rank += w > v || (w == v && bpos[f] < j);
-    }
-    btake[e] = rank < need;
-  }
-  __syncthreads();
-  return r;
 }
 
-// Whether position key is taken under rule r; `e` counts this thread's band
-// entries (or, for a big band, its ties at T) seen so far.
-__device__ __forceinline__ bool band_take(const BandRule& r, uint32_t key, uint32_t& e) {
-  if (r.big) {
-    const bool t = key > r.T || (key == r.T && e < r.krem);
-    e += key == r.T;
-    return t;
+// Two k-th largest searches sharing their sweeps.
+struct KthWork {
+  uint32_t part[kSelectThreads / 64][2 * kWays];
+  uint32_t tot[2 * kWays];
+  uint32_t hist[256];
+  uint32_t sh[4];
+  uint32_t ncand[2];
+  uint32_t cand[2][kLargeCand];
+};
+
+struct Search {
+  uint32_t k, lo, hi, clo, chi;   // lo <= T < hi, clo = count(>= lo) >= k > count(>= hi) = chi
+  bool on;
+  __device__ __forceinline__ bool wide() const { return on && hi - lo > 1 && clo - chi > kLargeCand; }
+};
+
+__device__ __forceinline__ uint32_t wave_sum_u(uint32_t v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += (uint32_t)__shfl_xor((int)v, off);
+  return v;
+}
+
+// Radix rounds over the candidates of one search (8-bit offsets in the bracket).
+__device__ void radix_finish(Search& b, const uint32_t* cand, uint32_t L, KthWork& wk) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+#pragma unroll 1
+  for (int it = 0; it < 5 && b.hi - b.lo > 1; ++it) {
+    const uint32_t width = b.hi - b.lo;
+    const int bits = 32 - __builtin_clz(width - 1);   // width - 1 < 2^bits
+    const int shift = bits > 8 ? bits - 8 : 0;
+    if (tid < 256) wk.hist[tid] = 0u;
+    __syncthreads();
+    for (uint32_t e = tid; e < L; e += kSelectThreads) {
+      const uint32_t x = cand[e];
+      if (x >= b.lo && x < b.hi) atomicAdd(&wk.hist[(x - b.lo) >> shift], 1u);
+    }
+    __syncthreads();
+    if (wave == 0) {
+      // lane l holds bins 4l .. 4l+3; counts of keys at or above each bin
+      uint32_t h4[4], suf = 0;
+#pragma unroll
+      for (int i = 3; i >= 0; --i) {
+        h4[i] = wk.hist[4 * lane + i];
+        suf += h4[i];
+      }
+      uint32_t incl = suf;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t t = (uint32_t)__shfl_down((int)incl, off);
+        if (lane + off < 64) incl += t;
+      }
+      uint32_t above = b.chi + incl - suf;
+      int best = -1;
+      uint32_t bc = 0, bh = 0;
+#pragma unroll
+      for (int i = 3; i >= 0; --i) {
+        const uint32_t c = above + h4[i];
+        if (best < 0 && c >= b.k) { best = 4 * lane + i; bc = c; bh = above; }
+        above = c;
+      }
+      const uint64_t hit = __ballot(best >= 0);
+      const int owner = 63 - __builtin_clzll(hit);
+      if (lane == owner) {
+        const uint32_t nl = b.lo + ((uint32_t)best << shift);
+        const uint64_t nh = (uint64_t)b.lo + ((uint64_t)(best + 1) << shift);
+        wk.sh[0] = nl;
+        wk.sh[1] = nh < b.hi ? (uint32_t)nh : b.hi;
+        wk.sh[2] = bc;
+        wk.sh[3] = bh;
+      }
+    }
+    __syncthreads();
+    b.lo = __builtin_amdgcn_readfirstlane(wk.sh[0]);
+    b.hi = __builtin_amdgcn_readfirstlane(wk.sh[1]);
+    b.clo = __builtin_amdgcn_readfirstlane(wk.sh[2]);
+    b.chi = __builtin_amdgcn_readfirstlane(wk.sh[3]);
+    __syncthreads();
   }
-  if (key > r.hi) return true;
-  if (key >= r.lo) return r.take[r.boff + e++] != 0;
-  return false;
+}
+
+// The k-th largest keys of both searches (each found exactly: T = lo).
+__device__ void kth_pair(const float* p, int P, Search (&b)[2], KthWork& wk) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  constexpr int NW = kSelectThreads / 64;
+#pragma unroll 1
+  while (b[0].wide() || b[1].wide()) {
+    uint32_t piv[2][kWays - 1], cnt[2][kWays - 1];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const uint32_t width = b[t].hi - b[t].lo;
+      const uint32_t step = width / kWays + (width % kWays ? 1u : 0u);   // >= 1
+#pragma unroll
+      for (int w = 0; w < kWays - 1; ++w) {
+        const uint64_t pv = (uint64_t)b[t].lo + (uint64_t)(w + 1) * step;
+        piv[t][w] = pv < b[t].hi ? (uint32_t)pv : b[t].hi;
+        cnt[t][w] = 0u;
+      }
+    }
+    for (int j0 = tid; j0 < P; j0 += kLoadBatch * kSelectThreads) {
+      uint32_t kk[kLoadBatch];
+      load_strided(p, j0, P, kk);
+#pragma unroll
+      for (int q = 0; q < kLoadBatch; ++q) {
+        const bool in = j0 + q * kSelectThreads < P;
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int w = 0; w < kWays - 1; ++w) cnt[t][w] += in && kk[q] >= piv[t][w];
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int w = 0; w < kWays - 1; ++w) {
+        const uint32_t v = wave_sum_u(cnt[t][w]);
+        if (lane == 0) wk.part[wave][t * kWays + w] = v;
+      }
+    __syncthreads();
+    if (tid < 2 * kWays) {
+      uint32_t t = 0;
+      for (int q = 0; q < NW; ++q) t += wk.part[q][tid];
+      wk.tot[tid] = t;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      if (!b[t].wide()) continue;
+      // the largest pivot whose count still reaches k bounds T from below
+      // (pivot counts do not increase with w); no pivot reaching k means
+      // T < piv[0]
+      uint32_t nlo = b[t].lo, nclo = b[t].clo, nhi = piv[t][0], nchi = wk.tot[t * kWays];
+#pragma unroll
+      for (int w = 0; w < kWays - 1; ++w) {
+        const uint32_t cw = wk.tot[t * kWays + w];
+        if (cw >= b[t].k) {
+          nlo = piv[t][w];
+          nclo = cw;
+          if (w + 1 < kWays - 1) {
+            nhi = piv[t][w + 1];
+            nchi = wk.tot[t * kWays + w + 1];
+          } else {
+            nhi = b[t].hi;
+            nchi = b[t].chi;
+          }
+        }
+      }
+      b[t].lo = __builtin_amdgcn_readfirstlane(nlo);
+      b[t].clo = __builtin_amdgcn_readfirstlane(nclo);
+      b[t].hi = __builtin_amdgcn_readfirstlane(nhi);
+      b[t].chi = __builtin_amdgcn_readfirstlane(nchi);
+    }
+    __syncthreads();   // part and tot are rewritten next round
+  }
+  // candidates of both brackets into LDS (in any order: only values matter)
+  if (tid < 2) wk.ncand[tid] = 0u;
+  __syncthreads();
+  const bool need0 = b[0].on && b[0].hi - b[0].lo > 1, need1 = b[1].on && b[1].hi - b[1].lo > 1;
+  if (need0 || need1) {
+    for (int j0 = tid; j0 < P; j0 += kLoadBatch * kSelectThreads) {
+      uint32_t kk[kLoadBatch];
+      load_strided(p, j0, P, kk);
+#pragma unroll
+      for (int q = 0; q < kLoadBatch; ++q) {
+        if (j0 + q * kSelectThreads >= P) continue;
+        if (need0 && kk[q] >= b[0].lo && kk[q] < b[0].hi) {
+          const uint32_t o = atomicAdd(&wk.ncand[0], 1u);
+          if (o < kLargeCand) wk.cand[0][o] = kk[q];
+        }
+        if (need1 && kk[q] >= b[1].lo && kk[q] < b[1].hi) {
+          const uint32_t o = atomicAdd(&wk.ncand[1], 1u);
+          if (o < kLargeCand) wk.cand[1][o] = kk[q];
+        }
+      }
+    }
+  }
+  __syncthreads();
+  if (need0) radix_finish(b[0], wk.cand[0], min(wk.ncand[0], kLargeCand), wk);
+  if (need1) radix_finish(b[1], wk.cand[1], min(wk.ncand[1], kLargeCand), wk);
+}
+
+// Boundary band of one threshold: its entries (unordered), their fp64 pooled
+// sums and take flags.
+struct BandSet {
+  uint32_t n;                 // keys inside [lo, hi] (may exceed kBandCap: "big")
+  uint32_t nabove, ngt;       // count(> hi), count(> T)
+  int32_t pos[kBandCap];
+  double v64[kBandCap];
+  uint32_t take[kBandCap];
+};
+
+__device__ __forceinline__ uint32_t band_lo(uint32_t T) { return T > kBandUlps ? T - kBandUlps : 0u; }
+__device__ __forceinline__ uint32_t band_hi(uint32_t T) {
+  return T < 0x7F800000u - kBandUlps ? T + kBandUlps : 0x7F800000u;
 }
 
 __global__ __launch_bounds__(kSelectThreads) void select_kernel(SelK a) {
-  __shared__ __attribute__((aligned(16))) char band_work[2][kBandCap * 16];
-  __shared__ uint32_t hist[2][256];
-  __shared__ uint32_t sh_state[4];
+  __shared__ BandSet band[2];
+  __shared__ KthWork wk;
+  __shared__ uint32_t bits[3][kSegWords];   // taken (T0), taken (T1), ties at T (big band)
   __shared__ uint32_t scan_scratch[16];
+  __shared__ uint32_t mm[2][kSelectThreads / 64];
+  __shared__ uint32_t cnt_sh[4];
+  float* stage = reinterpret_cast<float*>(&bits[0][0]);   // pooling staging (48 KB)
+  constexpr int kStageFloats = 3 * kSegWords;
 
-  const int u = blockIdx.x, tid = threadIdx.x;
+  const int u = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int P = a.prefix;
   const float* s = a.colsum + (size_t)u * P;
   float* p = a.pooled + (size_t)u * P;
@@ -142,78 +298,225 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(SelK a) {
   int32_t* idx = a.idx + us.base;
   uint8_t* fixed = a.fixed + us.base;
 
-  for (int j = tid; j < P; j += blockDim.x) {
-    int lo = j - a.h < 0 ? 0 : j - a.h;
-    int hi = j + a.h > P - 1 ? P - 1 : j + a.h;
-    float acc = 0.f;
-    for (int t = lo; t <= hi; ++t) acc += s[t];
-    p[j] = acc;
+  // 1. pooling, summed left to right; through LDS in rounds of CH outputs when
+  // the window fits beside them, straight from global memory otherwise
+  uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
+  const int h = a.h;
+  const int CH = kStageFloats - 2 * h >= 2048 ? min(16384, kStageFloats - 2 * h) : 0;
+  if (CH > 0) {
+    for (int base = 0; base < P; base += CH) {
+      __syncthreads();
+      for (int t0 = tid; t0 < CH + 2 * h; t0 += kLoadBatch * kSelectThreads) {
+        float v[kLoadBatch];
+#pragma unroll
+        for (int q = 0; q < kLoadBatch; ++q) {
+          const int t = t0 + q * kSelectThreads, j = base - h + t;
+          v[q] = (t < CH + 2 * h && j >= 0 && j < P) ? s[j] : 0.f;
+        }
+#pragma unroll
+        for (int q = 0; q < kLoadBatch; ++q) {
+          const int t = t0 + q * kSelectThreads;
+          if (t < CH + 2 * h) stage[t] = v[q];
+        }
+      }
+      __syncthreads();
+      for (int q = tid; q < CH && base + q < P; q += kSelectThreads) {
+        float acc = 0.f;
+        for (int t = 0; t <= 2 * h; ++t) acc += stage[q + t];
+        const uint32_t key = __float_as_uint(acc);
+        p[base + q] = acc;
+        kmin = min(kmin, key);
+        kmax = max(kmax, key);
+      }
+    }
+  } else {
+    for (int j = tid; j < P; j += kSelectThreads) {
+      const int lo = j - h < 0 ? 0 : j - h;
+      const int hi = j + h > P - 1 ? P - 1 : j + h;
+      float acc = 0.f;
+      for (int t = lo; t <= hi; ++t) acc += s[t];
+      p[j] = acc;
+      kmin = min(kmin, __float_as_uint(acc));
+      kmax = max(kmax, __float_as_uint(acc));
+    }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    kmin = min(kmin, (uint32_t)__shfl_xor((int)kmin, off));
+    kmax = max(kmax, (uint32_t)__shfl_xor((int)kmax, off));
+  }
+  if (lane == 0) { mm[0][wave] = kmin; mm[1][wave] = kmax; }
+  __syncthreads();   // also: every pooled score is written before the sweeps read them
+  kmin = 0xFFFFFFFFu;
+  kmax = 0u;
+#pragma unroll
+  for (int q = 0; q < kSelectThreads / 64; ++q) {
+    kmin = min(kmin, mm[0][q]);
+    kmax = max(kmax, mm[1][q]);
+  }
+  kmax = min(kmax, 0x7F800000u);   // +inf at most (no NaN scores)
+
+  // 2. T0 = the (c-w)-th largest, T1 = the floor(beta*c)-th largest
+  const bool any[2] = {us.s_sel > 0, us.n_top > 0};
+  Search b[2];
+  b[0] = {(uint32_t)us.s_sel, kmin, kmax + 1, (uint32_t)P, 0u, any[0]};
+  b[1] = {(uint32_t)us.n_top, kmin, kmax + 1, (uint32_t)P, 0u, any[1]};
+  kth_pair(p, P, b, wk);
+  const uint32_t T[2] = {b[0].lo, b[1].lo};
+  const uint32_t lo[2] = {band_lo(T[0]), band_lo(T[1])}, hi[2] = {band_hi(T[0]), band_hi(T[1])};
+  const uint32_t kk_[2] = {(uint32_t)us.s_sel, (uint32_t)us.n_top};
+
+  // 3. the boundary bands: entries (unordered), counts above the band and above T
+  if (tid < 2) { band[tid].n = 0u; cnt_sh[2 * tid] = 0u; cnt_sh[2 * tid + 1] = 0u; }
+  __syncthreads();
+  {
+    uint32_t nab[2] = {0u, 0u}, ngt[2] = {0u, 0u};
+    for (int j0 = tid; j0 < P; j0 += kLoadBatch * kSelectThreads) {
+      uint32_t kk[kLoadBatch];
+      load_strided(p, j0, P, kk);
+#pragma unroll
+      for (int q = 0; q < kLoadBatch; ++q) {
+        const int j = j0 + q * kSelectThreads;
+        if (j >= P) continue;
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          if (!any[t]) continue;
+          nab[t] += kk[q] > hi[t];
+          ngt[t] += kk[q] > T[t];
+          if (kk[q] >= lo[t] && kk[q] <= hi[t]) {
+            const uint32_t o = atomicAdd(&band[t].n, 1u);
+            if (o < kBandCap) band[t].pos[o] = j;
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const uint32_t x = wave_sum_u(nab[t]), y = wave_sum_u(ngt[t]);
+      if (lane == 0) { atomicAdd(&cnt_sh[2 * t], x); atomicAdd(&cnt_sh[2 * t + 1], y); }
+    }
+  }
+  __syncthreads();
+  bool big[2];
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    band[t].nabove = cnt_sh[2 * t];   // (same value from every thread)
+    band[t].ngt = cnt_sh[2 * t + 1];
+    big[t] = band[t].n > kBandCap;
+  }
+  __syncthreads();
+  // fp64 pooled sums of the band entries (left to right), then their ranks by
+  // (sum descending, position ascending): the first k - nabove are taken
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    if (!any[t] || big[t]) continue;
+    for (uint32_t e = tid; e < band[t].n; e += kSelectThreads) {
+      const int j = band[t].pos[e];
+      const int t0 = j - h < 0 ? 0 : j - h, t1 = j + h > P - 1 ? P - 1 : j + h;
+      double acc = 0.0;
+      for (int x = t0; x <= t1; ++x) acc += (double)s[x];
+      band[t].v64[e] = acc;
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    if (!any[t] || big[t]) continue;
+    const uint32_t nb = band[t].n, need = kk_[t] - band[t].nabove;
+    for (uint32_t e = tid; e < nb; e += kSelectThreads) {
+      const double v = band[t].v64[e];
+      const int j = band[t].pos[e];
+      uint32_t rank = 0;
+      for (uint32_t f = 0; f < nb; ++f) {
+        const double w = band[t].v64[f];
+        rank += w > v || (w == v && band[t].pos[f] < j);
+      }
+      band[t].take[e] = rank < need;
+    }
   }
   __syncthreads();
 
-  // radix select of the k-th largest for k = s_sel (target 0) and n_top (1)
-  uint32_t prefix[2] = {0u, 0u}, krem[2] = {(uint32_t)us.s_sel, (uint32_t)us.n_top};
-  uint32_t mask = 0u;
-  for (int shift = 24; shift >= 0; shift -= 8) {
-    for (int b = tid; b < 512; b += blockDim.x) (&hist[0][0])[b] = 0u;
+  // 4. per segment: mark the taken positions, then write them in order
+  uint32_t out_before = 0, eq_before[2] = {0u, 0u};
+  for (int seg0 = 0; seg0 < P; seg0 += kSegBits) {
+    const int seg1 = min(P, seg0 + kSegBits);
     __syncthreads();
-    for (int j = tid; j < P; j += blockDim.x) {
-      uint32_t key = __float_as_uint(p[j]);
+    for (int wd = tid; wd < 3 * kSegWords; wd += kSelectThreads) (&bits[0][0])[wd] = 0u;
+    __syncthreads();
+    for (int t = 0; t < 2; ++t) {
+      if (!any[t]) continue;
+      // keys above the band (or, for a big band, above T; ties marked apart)
+      for (int j0 = seg0 + tid; j0 < seg1; j0 += kLoadBatch * kSelectThreads) {
+        uint32_t kk[kLoadBatch];
+        load_strided(p, j0, seg1, kk);
 #pragma unroll
-      for (int t = 0; t < 2; ++t)
-        if (krem[t] > 0 && (key & mask) == prefix[t]) atomicAdd(&hist[t][(key >> shift) & 255u], 1u);
-    }
-    __syncthreads();
-    if (tid < 2 && krem[tid] > 0) {
-      uint32_t cum = 0;
-      int digit = 0;
-      for (int b = 255; b >= 0; --b) {
-        uint32_t hcount = hist[tid][b];
-        if (cum + hcount >= krem[tid]) { digit = b; break; }
-        cum += hcount;
+        for (int q = 0; q < kLoadBatch; ++q) {
+          const int j = j0 + q * kSelectThreads;
+          if (j >= seg1) continue;
+          const int bi = j - seg0;
+          if (big[t] ? kk[q] > T[t] : kk[q] > hi[t]) atomicOr(&bits[t][bi >> 5], 1u << (bi & 31));
+          if (big[t] && kk[q] == T[t]) atomicOr(&bits[2][bi >> 5], 1u << (bi & 31));
+        }
       }
-      sh_state[2 * tid] = prefix[tid] | ((uint32_t)digit << shift);
-      sh_state[2 * tid + 1] = krem[tid] - cum;
-    }
-    __syncthreads();
+      if (!big[t]) {
+        for (uint32_t e = tid; e < band[t].n; e += kSelectThreads) {
+          const int j = band[t].pos[e];
+          if (band[t].take[e] && j >= seg0 && j < seg1)
+            atomicOr(&bits[t][(j - seg0) >> 5], 1u << ((j - seg0) & 31));
+        }
+        continue;
+      }
+      // big band: ties at T go to the lowest positions, k - count(> T) of them
+      __syncthreads();
+      const uint32_t krem = kk_[t] - band[t].ngt;
+      uint32_t wv[kWordsPerThread], c = 0;
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
-      if (krem[t] > 0) { prefix[t] = sh_state[2 * t]; krem[t] = sh_state[2 * t + 1]; }
-    mask |= 255u << shift;
-    __syncthreads();
-  }
-  // prefix[t] = bits of the k-th largest score; krem[t] = how many scores
-  // equal to it are taken (lowest positions first); all larger ones are taken.
-  const uint32_t T0 = prefix[0], T1 = prefix[1];
-  const bool any0 = us.s_sel > 0, any1 = us.n_top > 0;
-
-  const int per = (P + blockDim.x - 1) / blockDim.x;
-  const int j0 = min(P, tid * per), j1 = min(P, j0 + per);
-  BandRule r0 = {}, r1 = {};
-  if (any0) r0 = band_rule(p, T0, (uint32_t)us.s_sel, s, j0, j1, P, a.h, band_work[0], scan_scratch);
-  if (any1) r1 = band_rule(p, T1, (uint32_t)us.n_top, s, j0, j1, P, a.h, band_work[1], scan_scratch);
-  uint32_t nsel = 0;
-  {
-    uint32_t e0 = 0;
-    for (int j = j0; j < j1; ++j) {
-      const uint32_t key = __float_as_uint(p[j]);
-      nsel += any0 && band_take(r0, key, e0);
+      for (int i = 0; i < kWordsPerThread; ++i) {
+        wv[i] = bits[2][tid * kWordsPerThread + i];
+        c += __builtin_popcount(wv[i]);
+      }
+      uint32_t tot;
+      uint32_t r = eq_before[t] + block_exclusive_scan(c, scan_scratch, &tot);
+#pragma unroll
+      for (int i = 0; i < kWordsPerThread; ++i) {
+        uint32_t wbits = wv[i], take = 0u;
+        while (wbits) {
+          const int bpos = __builtin_ctz(wbits);
+          if (r < krem) take |= 1u << bpos;
+          ++r;
+          wbits &= wbits - 1;
+        }
+        if (take) atomicOr(&bits[t][tid * kWordsPerThread + i], take);
+      }
+      eq_before[t] += tot;
+      __syncthreads();
+      for (int wd = tid; wd < kSegWords; wd += kSelectThreads) bits[2][wd] = 0u;
+      __syncthreads();   // cleared before the next threshold marks its ties
     }
-  }
-  uint32_t tot;
-  uint32_t off = block_exclusive_scan(nsel, scan_scratch, &tot);
-  {
-    uint32_t e0 = 0, e1 = 0;
-    for (int j = j0; j < j1; ++j) {
-      const uint32_t key = __float_as_uint(p[j]);
-      const bool sel = any0 && band_take(r0, key, e0);
-      const bool top = any1 && band_take(r1, key, e1);
-      if (sel) {
+    __syncthreads();
+    // the taken positions of this segment, ascending, with their fixed flags
+    uint32_t wv[kWordsPerThread], c = 0;
+#pragma unroll
+    for (int i = 0; i < kWordsPerThread; ++i) {
+      wv[i] = bits[0][tid * kWordsPerThread + i];
+      c += __builtin_popcount(wv[i]);
+    }
+    uint32_t tot;
+    uint32_t off = out_before + block_exclusive_scan(c, scan_scratch, &tot);
+#pragma unroll
+    for (int i = 0; i < kWordsPerThread; ++i) {
+      const uint32_t topw = bits[1][tid * kWordsPerThread + i];
+      uint32_t wbits = wv[i];
+      while (wbits) {
+        const int bpos = __builtin_ctz(wbits);
+        const int j = seg0 + (tid * kWordsPerThread + i) * 32 + bpos;
         idx[off] = j;
-        fixed[off] = (j < a.n_sink || top) ? 1 : 0;
+        fixed[off] = (j < a.n_sink || ((topw >> bpos) & 1u)) ? 1 : 0;
         ++off;
+        wbits &= wbits - 1;
       }
     }
+    out_before += tot;
   }
   for (int i = tid; i < a.w; i += blockDim.x) {
     int64_t pos = a.n - a.w + i;

@@ -85,6 +85,14 @@ struct StreamK {
 };
 
 constexpr int kTileElems = 4096;   // elements of one tensor per tile
+// The full-cache pass B forms P scaled by 2^kFullPBias (P <= 1, so the scaled
+// value stays below 2^15 and inside fp16's range): probabilities down to
+// 2^-29 stay normal fp16 numbers in the fp16 P.V, where unscaled ones below
+// 2^-14 would become subnormals whose rounding, the same for every equal
+// term of a flat long-context row, biases Y.  Y and the column sums are
+// scaled back by the exact power of two.
+constexpr float kFullPBias = 15.f;
+constexpr float kFullPUnscale = 0x1p-15f;
 constexpr int kRetMaxSlots = 4096;  // retained pass: key slots per block (the plan's split bound)
 constexpr int kTileBytes = kTileElems * 2;
 
@@ -376,7 +384,7 @@ struct Stream {
         float c = 0.f;
 #pragma unroll
         for (int wv = 0; wv < WAVES; ++wv) c += colpart[t & 1][wv][threadIdx.x];
-        a.colsum[(size_t)u * a.prefix + key] = c;
+        a.colsum[(size_t)u * a.prefix + key] = c * kFullPUnscale;
       }
     }
   }
@@ -846,7 +854,7 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : 2))) void stream_kerne
       S.qb[rt][ks] = S.rowok[rt] ? *reinterpret_cast<const uint4*>(q + ks * 32 + 8 * g)
                                  : make_uint4(0, 0, 0, 0);
     if (is_full<MODE>() && a.lse_ready) {
-      S.lse[rt] = a.lse_log2_out[(size_t)u * a.mp + row];
+      S.lse[rt] = a.lse_log2_out[(size_t)u * a.mp + row] - kFullPBias;
     } else if constexpr (is_full<MODE>()) {
       // fixed-order combine of pass A's split partials: M = max of the
       // integer reference exponents, sum = sum_s psum_s 2^(ref_s - M) (exact
@@ -863,7 +871,7 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : 2))) void stream_kerne
         }
         l2 = (double)M + log2(sum);
       }
-      S.lse[rt] = (float)l2;
+      S.lse[rt] = (float)l2 - kFullPBias;
       if (s == 0 && g == 0) {
         a.lse_out[(size_t)u * a.mp + row] = M != -INFINITY ? l2 * 0.69314718055994530942 : -INFINITY;
         a.lse_log2_out[(size_t)u * a.mp + row] = (float)l2;
@@ -966,7 +974,8 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : 2))) void stream_kerne
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int row = sm.rtile(rt) * 16 + 4 * g + i;
-          yp[(size_t)row * D + dt * 16 + l16] = S.y[rt][dt][i];
+          yp[(size_t)row * D + dt * 16 + l16] =
+              is_full<MODE>() ? S.y[rt][dt][i] * kFullPUnscale : S.y[rt][dt][i];
         }
     if (MODE == kModeRetained) {
       if (a.mpart) {

@@ -148,6 +148,12 @@ EDGE = [
     ("m-96", dict(group=3)),
     ("lambda-large", dict(lam=1e6)),
     ("lambda-0", dict(lam=0.0, group=1, window=8, budget=128)),
+    # the selection kernel for long prefixes or wide pools (scores in global
+    # memory): a prefix past 32768, a pool of 33, a pool wider than its
+    # LDS staging (summed straight from global memory)
+    ("prefix-40k", dict(n=40000, budget=1024)),
+    ("pool-33", dict(pool_kernel=33)),
+    ("pool-8001", dict(n=10000, budget=512, pool_kernel=8001)),
 ]
 
 
@@ -183,6 +189,23 @@ def test_zero_query_ties_lower_index():
     # all logits 0: the interior pooled scores tie exactly; the lowest
     # interior positions must be kept
     cfg = W.config(2, layers=1, kv_heads=2, n=1024, budget=160)
+    q, K, V = _batch(cfg)
+    q[:] = 0
+    gpu = run_gpu(cfg, q, K, V)
+    h = (cfg.pool_kernel - 1) // 2
+    want = np.concatenate([np.arange(h, h + cfg.budget - cfg.window),
+                           np.arange(cfg.n - cfg.window, cfg.n)])
+    for u in range(cfg.units):
+        assert np.array_equal(gpu["idx"][u], want)
+        check_unit(cfg, q, K, V, gpu, u)
+
+
+def test_zero_query_ties_lower_index_long_prefix():
+    # the same exact ties over a prefix past 32768 positions, where the
+    # selection keeps the pooled scores in global memory: the band of equal
+    # scores is far wider than the fp64 re-ranking takes, so the fp32 order
+    # with ties to the lowest positions decides (both thresholds)
+    cfg = W.config(2, layers=1, kv_heads=2, n=40000, budget=160)
     q, K, V = _batch(cfg)
     q[:] = 0
     gpu = run_gpu(cfg, q, K, V)
