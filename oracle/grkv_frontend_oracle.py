@@ -25,11 +25,20 @@ these methods in one sentence each:
   taken as the highest pooled SnapKV scores over all heads of the layer
   (ties to the lower head, then the lower position); head h keeps w plus the
   number of its tokens taken;
-* token-based (H2O-style) scoring is the pooled score with pool width 1.
+* token-based H2O: a prefix token's score is the attention it receives,
+  accumulated over every prompt position (Sec. 2: heavy hitters by
+  accumulated attention scores).  Reading: every query head of the KV head's
+  group and every prompt position i (the window included) contribute their
+  causal attention row softmax(q_i K^T / sqrt(d)) over keys 0..i; the score of
+  prefix token j is the sum of those rows' entries at j.  The retained set is
+  the top c - w prefix tokens by that score with no pooling (pool width 1)
+  plus the w most recent tokens, and the merge is GRKV's value step on the
+  window queries, as for any front-end.
 
 Parity status: pinned by ``tests/test_oracle_frontend.py`` (uniform budgets
 reduce to the batched oracle, brute-force joint top-k, closed forms of the
-schedule).
+schedule; the accumulated attention by brute force, its zero-query closed
+form in harmonic numbers, row normalisation and a dominant key).
 """
 from __future__ import annotations
 
@@ -37,7 +46,8 @@ import numpy as np
 
 from . import grkv_oracle as V
 
-__all__ = ["pyramid_budgets", "adaptive_budgets", "compress_ragged", "packed_offsets"]
+__all__ = ["pyramid_budgets", "adaptive_budgets", "compress_ragged", "packed_offsets",
+           "h2o_scores", "compress_h2o"]
 
 
 def pyramid_budgets(layers: int, kv_heads: int, mean_budget: int, window: int, n: int,
@@ -96,3 +106,31 @@ def compress_ragged(q_obs, K, Vv, budgets, window, pool_kernel, lam, opt=None, u
     units = range(U) if units is None else units
     return [V.compress_unit(q_obs[u], K[u], Vv[u], window, int(budgets[u]), pool_kernel, lam, opt)
             for u in units]
+
+
+def h2o_scores(q_all, K, window, all_columns=False):
+    """Accumulated attention (H2O's heavy-hitter score) of one unit.
+
+    q_all [G, n, d]: the queries of every prompt position for the G query
+    heads of the KV head; K [n, d].  Row (g, i) is the causal attention of
+    position i, softmax over keys 0..i of q_{g,i} . k_j / sqrt(d); the score
+    of token j is the sum over all rows of their entries at j.  Returns the
+    prefix scores [n - w] (all n columns with ``all_columns``)."""
+    q_all = np.asarray(q_all, dtype=np.float64)
+    G, n, d = q_all.shape
+    Kd = np.asarray(K, dtype=np.float64)
+    j = np.arange(n)
+    s = np.zeros(n, dtype=np.float64)
+    for g in range(G):
+        L = (q_all[g] @ Kd.T) / np.sqrt(d)
+        L = np.where(j[None, :] <= j[:, None], L, -np.inf)   # row i sees keys 0..i
+        A, _ = V.softmax_rows(L)
+        s += A.sum(axis=0)
+    return s if all_columns else s[: n - window]
+
+
+def compress_h2o(q_all, q_obs, K, Vv, window, budget, lam, opt=None):
+    """H2O retention (accumulated-attention scores, no pooling) followed by
+    GRKV's value step on the window queries q_obs [G, w, d]."""
+    s = h2o_scores(q_all, K, window)
+    return V.compress_unit(q_obs, K, Vv, window, budget, 1, lam, opt=opt, scores=s)

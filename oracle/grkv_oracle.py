@@ -224,13 +224,16 @@ def discrepancy(Y, X, V):
 # ------------------------------------------------------------- driver -------
 
 def compress_unit(q_obs, K, V, window, budget, pool_kernel, lam, opt=None,
-                  with_primal=False, idx=None):
+                  with_primal=False, idx=None, scores=None):
     """All steps for one unit on float64 inputs.
 
     q_obs [G, w, d], K [n, d], V [n, d] as exact float64 values.  When ``idx``
     is given the selection is skipped and that retained set is used (it must be
-    ascending and end with the window).  Returns a dict with every
-    intermediate, so tests can pin each step on its own."""
+    ascending and end with the window).  When ``scores`` [n - w] is given, the
+    selection ranks those per-token scores (pooled with the same box) instead
+    of the window attention's column sums: the form a token-based eviction
+    method such as H2O (Sec. 2) plugs in; the merge is unchanged.  Returns a
+    dict with every intermediate, so tests can pin each step on its own."""
     opt = opt or Options()
     G, w, d = q_obs.shape
     n = K.shape[0]
@@ -241,7 +244,8 @@ def compress_unit(q_obs, K, V, window, budget, pool_kernel, lam, opt=None,
     A, lse = softmax_rows(L)
     Y = A @ V
     prefix = n - w
-    s = selection_scores(A, prefix)
+    s = selection_scores(A, prefix) if scores is None else np.asarray(scores, dtype=np.float64)
+    assert s.shape == (prefix,)
     p = pool_box(s, pool_kernel)
     order = selection_order(p)
     if idx is None:
