@@ -285,6 +285,44 @@ int grkv_pyramid_budgets(int32_t layers, int32_t kv_heads, int32_t mean_budget, 
 int grkv_adaptive_budgets(const float* pooled, int32_t layers, int32_t kv_heads, int64_t n,
                           int32_t window, int32_t budget, void* stream, int32_t* budgets);
 
+/* Token scores of H2O (Sec. 2: heavy-hitter tokens kept by accumulated
+ * attention scores; Sec. 4.3, compatibility), the token-based eviction
+ * back-end GRKV is paired with.  For unit u the score of prefix token j < n - w
+ * is the attention it receives summed over every prompt position i >= j of
+ * every query head g of the unit's group, each row being the causal softmax of
+ * q_{g,i} . k / sqrt(d) over keys 0..i:
+ *   s_j = sum_g sum_{i >= j} exp(q_{g,i} . k_j / sqrt(d) - LSE_{g,i}).
+ *   q_all    dtype [U][G][n][d]  the queries of every prompt position (post-RoPE)
+ *   K        dtype [U][n][d]
+ *   scores   float [U][n - w]    out (device memory)
+ *   workspace                    >= grkv_h2o_workspace_bytes(), 256-byte aligned
+ * bf16 only, head_dim 64 or 128, group 1, 2, 4 or 8.  The cost is that of a
+ * prefill attention without P.V (two passes of O(n^2 d) MFMA work per head).
+ * Errors: GRKV_ERR_INVALID (null pointers, window outside [1, n], bad sizes),
+ * GRKV_ERR_UNSUPPORTED, GRKV_ERR_WORKSPACE, GRKV_ERR_HIP.  Asynchronous on
+ * stream; allocates nothing. */
+int grkv_h2o_scores(const void* q_all, const void* K, int64_t n, int32_t window, void* stream,
+                    const grkv_problem* prob, float* scores, void* workspace,
+                    size_t workspace_bytes);
+
+/* Workspace bytes of grkv_h2o_scores (the row log-sum-exps, U * G * n floats);
+ * 0 if the shape is invalid or unsupported. */
+size_t grkv_h2o_workspace_bytes(const grkv_problem* prob, int64_t n);
+
+/* grkv_compress with the selection driven by caller-supplied per-token scores
+ * instead of the window attention's column sums: the form a token-based
+ * eviction front-end such as H2O (scores from grkv_h2o_scores, pool_kernel 1)
+ * takes.  scores: float [U][n - w] device memory, finite and non-negative
+ * (attention masses are), pooled with pool_kernel exactly as the column sums
+ * would be; the top floor(beta * c) fixed subset follows the same order.  The
+ * window attention, Y and the value step are those of grkv_compress.  All
+ * other arguments, outputs, workspace and errors as for grkv_compress
+ * (GRKV_ERR_INVALID also for a null scores when n > window). */
+int grkv_compress_scored(const void* q_obs, const void* K, const void* V, int64_t n,
+                         int32_t window, int32_t budget, int32_t pool_kernel, float lambda,
+                         void* stream, const grkv_problem* prob, const grkv_options* opt,
+                         const float* scores, const grkv_outputs* out);
+
 /* Carrier concentration of a local merge rule (App. B, "Quantitative Carrier
  * Concentration"; Sec. 1): the diagnostic the paper uses to show that, after
  * span-based eviction, a key-similarity matcher (as in D2O/KVMerger) loads a

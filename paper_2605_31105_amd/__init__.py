@@ -19,7 +19,8 @@ __all__ = [
     "intermediates", "EXPORTED_SYMBOLS", "KeyOptions", "workspace_bytes_kv", "compress_kv",
     "KEY_CONVERGED", "KEY_MAX_ITER", "KEY_SKIPPED", "KEY_BREAKDOWN", "carrier_stats",
     "CARRIER_METRICS", "compress_ragged", "pyramid_budgets", "adaptive_budgets",
-    "workspace_bytes_ragged", "compress_noalloc", "NOALLOC_SCRATCH_BYTES",
+    "workspace_bytes_ragged", "compress_noalloc", "NOALLOC_SCRATCH_BYTES", "h2o_scores",
+    "compress_scored", "h2o_workspace_bytes",
 ]
 
 GRKV_OK, GRKV_ERR_INVALID, GRKV_ERR_WORKSPACE, GRKV_ERR_UNSUPPORTED, GRKV_ERR_HIP = 0, -1, -2, -3, -4
@@ -31,7 +32,8 @@ EXPORTED_SYMBOLS = ("grkv_compress", "grkv_workspace_bytes", "grkv_workspace_lay
                     "grkv_default_options", "grkv_status_string", "grkv_compress_kv",
                     "grkv_workspace_bytes_kv", "grkv_default_key_options", "grkv_carrier_stats",
                     "grkv_compress_ragged", "grkv_workspace_bytes_ragged", "grkv_pyramid_budgets",
-                    "grkv_adaptive_budgets", "grkv_compress_noalloc")
+                    "grkv_adaptive_budgets", "grkv_compress_noalloc", "grkv_h2o_scores",
+                    "grkv_h2o_workspace_bytes", "grkv_compress_scored")
 NOALLOC_SCRATCH_BYTES = 64 << 20
 KEY_CONVERGED, KEY_MAX_ITER, KEY_SKIPPED, KEY_BREAKDOWN = 1, 2, 3, 4
 CARRIER_METRICS = ("b", "b_eff", "a_max", "gini", "boundary_fraction", "boundary_share",
@@ -96,6 +98,17 @@ def lib() -> ctypes.CDLL:
                                     P(Problem), P(Options), P(Outputs)]
         L.grkv_compress_noalloc.restype = ctypes.c_int
         L.grkv_compress_noalloc.argtypes = L.grkv_compress.argtypes
+        L.grkv_compress_scored.restype = ctypes.c_int
+        L.grkv_compress_scored.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                           ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                           ctypes.c_int32, ctypes.c_float, ctypes.c_void_p,
+                                           P(Problem), P(Options), ctypes.c_void_p, P(Outputs)]
+        L.grkv_h2o_scores.restype = ctypes.c_int
+        L.grkv_h2o_scores.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                      ctypes.c_int32, ctypes.c_void_p, P(Problem), ctypes.c_void_p,
+                                      ctypes.c_void_p, ctypes.c_size_t]
+        L.grkv_h2o_workspace_bytes.restype = ctypes.c_size_t
+        L.grkv_h2o_workspace_bytes.argtypes = [P(Problem), ctypes.c_int64]
         L.grkv_workspace_bytes.restype = ctypes.c_size_t
         L.grkv_workspace_bytes.argtypes = [P(Problem), ctypes.c_int64, ctypes.c_int32, ctypes.c_int32]
         L.grkv_workspace_layout.restype = ctypes.c_int
@@ -291,6 +304,66 @@ def compress_noalloc(q_obs, K, V, window: int, budget: int, pool_kernel: int, la
     _check(st)
     out.workspace = None
     out.shape = (U, G, d, dt, n, window, budget)
+    return out
+
+
+def h2o_workspace_bytes(units, group, head_dim, dtype, n) -> int:
+    prob = Problem(units, group, head_dim, dtype)
+    return int(lib().grkv_h2o_workspace_bytes(ctypes.byref(prob), n))
+
+
+def h2o_scores(q_all, K, window: int, *, stream=None, workspace=None, out=None):
+    """H2O accumulated-attention scores of every prefix token (grkv_h2o_scores).
+
+    q_all [U, G, n, d] (the queries of every prompt position) and K [U, n, d]:
+    contiguous bfloat16 device tensors.  Returns float32 scores [U, n - window]."""
+    import torch
+
+    if not (q_all.is_cuda and K.is_cuda) or not (q_all.is_contiguous() and K.is_contiguous()):
+        raise ValueError("q_all and K must be contiguous device tensors")
+    if q_all.dtype != torch.bfloat16 or K.dtype != torch.bfloat16:
+        raise ValueError("q_all and K must be bfloat16")
+    U, Gq, n, d = q_all.shape
+    if tuple(K.shape) != (U, n, d):
+        raise ValueError("shape mismatch: q_all %s K %s" % (tuple(q_all.shape), tuple(K.shape)))
+    need = max(256, h2o_workspace_bytes(U, Gq, d, GRKV_BF16, n))
+    if workspace is None or workspace.numel() < need:
+        workspace = torch.empty(need, dtype=torch.uint8, device=K.device)
+    if out is None:
+        out = torch.empty((U, max(n - window, 0)), dtype=torch.float32, device=K.device)
+    prob = Problem(U, Gq, d, GRKV_BF16)
+    if stream is None:
+        stream = torch.cuda.current_stream(K.device)
+    handle = stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+    _check(lib().grkv_h2o_scores(q_all.data_ptr(), K.data_ptr(), n, window,
+                                 ctypes.c_void_p(handle), ctypes.byref(prob),
+                                 out.data_ptr() if out.numel() else None, workspace.data_ptr(),
+                                 workspace.numel()))
+    return out
+
+
+def compress_scored(q_obs, K, V, window: int, budget: int, pool_kernel: int, lam: float,
+                    scores, *, n_sink: int = 4, beta: float = 0.10, fix_window: bool = True,
+                    causal_window: bool = True, stream=None, workspace=None, out=None,
+                    stage_events=None) -> Result:
+    """``compress`` with the selection ranking caller-supplied per-token scores
+    (float32 [U, n - window], finite and non-negative) pooled with pool_kernel,
+    instead of the window attention's column sums (grkv_compress_scored)."""
+    import torch
+
+    out, prob, opt, outs, handle, n = _prepare(
+        q_obs, K, V, window, budget, workspace_bytes, n_sink, beta, fix_window, causal_window,
+        stream, workspace, out, stage_events)
+    if not (scores.is_cuda and scores.dtype == torch.float32 and scores.is_contiguous()):
+        raise ValueError("scores must be a contiguous float32 device tensor")
+    if tuple(scores.shape) != (K.shape[0], n - window):
+        raise ValueError("scores must be [U, n - window]")
+    st = lib().grkv_compress_scored(q_obs.data_ptr(), K.data_ptr(), V.data_ptr(), n, window,
+                                    budget, pool_kernel, float(lam), ctypes.c_void_p(handle),
+                                    ctypes.byref(prob), ctypes.byref(opt),
+                                    scores.data_ptr() if scores.numel() else None,
+                                    ctypes.byref(outs))
+    _check(st)
     return out
 
 

@@ -238,7 +238,7 @@ int check_pointers(const void* q_obs, const void* K, const void* V, const grkv_p
 
 // The launch sequence of one call (arguments already checked).
 int run_compress(const Plan& p, const void* q_obs, const void* K, const void* V, int64_t n,
-                 hipStream_t s, const grkv_outputs* out) {
+                 hipStream_t s, const grkv_outputs* out, const float* ext_scores = nullptr) {
   char* ws = (char*)out->workspace;
   auto F = [&](size_t o) { return (float*)(ws + o); };
   auto Dd = [&](size_t o) { return (double*)(ws + o); };
@@ -256,7 +256,8 @@ int run_compress(const Plan& p, const void* q_obs, const void* K, const void* V,
   full.S = p.S1; full.chunk = p.chunk1;
   full.pmax = F(p.pmax1); full.psum = Dd(p.psum1);
   full.lse = Dd(p.lse1); full.lse_log2 = F(p.lse1_log2);
-  full.ypart = F(p.ypart); full.colsum = p.prefix > 0 ? F(p.colsum) : nullptr;
+  // (with caller-supplied selection scores the window's column sums are not formed)
+  full.ypart = F(p.ypart); full.colsum = p.prefix > 0 && !ext_scores ? F(p.colsum) : nullptr;
   full.prefix = p.prefix; full.xout = nullptr; full.split_p = true;
   full.redo = (int*)(ws + p.redo);
   const bool fast = stream_supported(p);
@@ -277,7 +278,8 @@ int run_compress(const Plan& p, const void* q_obs, const void* K, const void* V,
     GRKV_STAGE(GRKV_STAGE_FULL_Y, launch_combine_rows(p, F(p.ypart), p.S1, nullptr, F(p.y), s));
   // 2. pooled top-k retention and the fixed set; gather K0, V0
   uint8_t* fixed = (uint8_t*)(ws + p.fixed);
-  GRKV_STAGE(GRKV_STAGE_SELECT, launch_select(p, F(p.colsum), F(p.pooled), out->idx, fixed, s));
+  GRKV_STAGE(GRKV_STAGE_SELECT, launch_select(p, ext_scores ? ext_scores : F(p.colsum), F(p.pooled),
+                                              out->idx, fixed, s));
   const bool fast_merge = p.fast_merge;
   // fast path: the retained pass A reads the K rows through idx and copies
   // them to k_out; V0 rows are read through idx where needed
@@ -380,6 +382,42 @@ int grkv_compress(const void* q_obs, const void* K, const void* V, int64_t n, in
   if (st != GRKV_OK) return st;
   if (out->workspace_bytes < p.total) return GRKV_ERR_WORKSPACE;
   return run_compress(p, q_obs, K, V, n, (hipStream_t)stream, out);
+}
+
+int grkv_compress_scored(const void* q_obs, const void* K, const void* V, int64_t n,
+                         int32_t window, int32_t budget, int32_t pool_kernel, float lambda,
+                         void* stream, const grkv_problem* prob, const grkv_options* opt,
+                         const float* scores, const grkv_outputs* out) {
+  int st = check_pointers(q_obs, K, V, prob, out);
+  if (st != GRKV_OK) return st;
+  if (!scores && n > window) return GRKV_ERR_INVALID;
+  Plan p;
+  st = make_plan(prob, n, window, budget, pool_kernel, lambda, opt, &p);
+  if (st != GRKV_OK) return st;
+  if (out->workspace_bytes < p.total) return GRKV_ERR_WORKSPACE;
+  return run_compress(p, q_obs, K, V, n, (hipStream_t)stream, out, scores);
+}
+
+size_t grkv_h2o_workspace_bytes(const grkv_problem* prob, int64_t n) {
+  if (!prob || prob->units < 1 || prob->group < 1 || n < 1 || n > (int64_t(1) << 30)) return 0;
+  if (!h2o_supported(prob->dtype, prob->head_dim, prob->group)) return 0;
+  return (size_t)prob->units * prob->group * (size_t)n * sizeof(float);
+}
+
+int grkv_h2o_scores(const void* q_all, const void* K, int64_t n, int32_t window, void* stream,
+                    const grkv_problem* prob, float* scores, void* workspace,
+                    size_t workspace_bytes) {
+  if (!q_all || !K || !prob || !workspace || (!scores && n > window)) return GRKV_ERR_INVALID;
+  if (prob->units < 1 || prob->group < 1) return GRKV_ERR_INVALID;
+  if (prob->dtype != GRKV_BF16 && prob->dtype != GRKV_F32) return GRKV_ERR_INVALID;
+  if (window < 1 || (int64_t)window > n || n > (int64_t(1) << 30)) return GRKV_ERR_INVALID;
+  if (((uintptr_t)workspace & 255) != 0) return GRKV_ERR_INVALID;
+  if (!h2o_supported(prob->dtype, prob->head_dim, prob->group)) return GRKV_ERR_UNSUPPORTED;
+  if (workspace_bytes < grkv_h2o_workspace_bytes(prob, n)) return GRKV_ERR_WORKSPACE;
+  if (launch_h2o(q_all, K, prob->units, prob->group, prob->head_dim, n, (int)(n - window),
+                 (float*)workspace, scores, (hipStream_t)stream) != hipSuccess)
+    return GRKV_ERR_HIP;
+  return GRKV_OK;
 }
 
 void grkv_default_key_options(grkv_key_options* kopt, float lambda) {

@@ -234,6 +234,13 @@ bool key_supported(const Plan& p);
 hipError_t launch_key(const Plan& p, const KeyPlan& kp, const KeyArgs& a, hipStream_t s);
 hipError_t launch_to_f32(const uint16_t* src, float* dst, size_t n, hipStream_t s);
 
+// H2O accumulated-attention scores (bf16, d 64/128, G in {1, 2, 4, 8}): row
+// log-sum-exps of every prompt position into lse2 [U][G][n], then the prefix
+// column sums into scores [U][P].
+bool h2o_supported(int dtype, int d, int G);
+hipError_t launch_h2o(const void* q_all, const void* K, int U, int G, int d, int64_t n, int P,
+                      float* lse2, float* scores, hipStream_t s);
+
 // Adaptive per-head budgets: one block per layer of H adjacent units.
 hipError_t launch_adaptive_budgets(const float* pooled, int layers, int H, int P, int64_t kk,
                                    int w, int32_t* budgets, hipStream_t s);

@@ -37,17 +37,18 @@ def run_gpu(cfg, q, K, V, **opts):
     return out
 
 
-def oracle_unit(cfg, q, K, V, u, opt=None, idx=None):
+def oracle_unit(cfg, q, K, V, u, opt=None, idx=None, scores=None):
     qd, Kd, Vd = (W.decode(a[u], cfg.dtype) for a in (q, K, V))
     return O.compress_unit(qd, Kd, Vd, cfg.window, cfg.budget, cfg.pool_kernel, cfg.lam,
-                           opt=opt, idx=idx)
+                           opt=opt, idx=idx, scores=scores)
 
 
-def check_unit(cfg, q, K, V, gpu, u, slot=None, opt=None, report=None):
+def check_unit(cfg, q, K, V, gpu, u, slot=None, opt=None, report=None, scores=None):
     """Compare GPU outputs of unit ``u`` (row ``slot`` of the GPU batch) with
-    the oracle.  Returns a dict of error figures; asserts the parity bar."""
+    the oracle (selection from ``scores`` when given).  Returns a dict of error
+    figures; asserts the parity bar."""
     slot = u if slot is None else slot
-    r = oracle_unit(cfg, q, K, V, u, opt=opt)
+    r = oracle_unit(cfg, q, K, V, u, opt=opt, scores=scores)
     idx_g = gpu["idx"][slot].astype(np.int64)
     diff = np.setdiff1d(r["idx"], idx_g).size
     info = {"unit": u, "idx_mismatch": int(diff)}

@@ -30,7 +30,7 @@ from concurrent.futures import ThreadPoolExecutor
 import numpy as np
 
 __all__ = [
-    "Config", "CONFIGS", "config", "make_unit", "make_batch",
+    "Config", "CONFIGS", "config", "make_unit", "make_batch", "make_prompt_queries",
     "f32_to_bf16_bits", "bf16_bits_to_f32", "decode",
 ]
 
@@ -180,3 +180,31 @@ def make_batch(cfg: Config, units=None, *, n: int | None = None, threads: int | 
         with ThreadPoolExecutor(threads) as ex:
             list(ex.map(fill, enumerate(ids)))
     return q, K, V
+
+
+def make_prompt_queries(cfg: Config, q_obs: np.ndarray, K: np.ndarray, units=None, *,
+                        n: int | None = None) -> np.ndarray:
+    """Queries of every prompt position, for front-ends that score tokens by
+    the attention of all prompt queries (accumulated attention).
+
+    Returns ``q_all [U, G, n, d]`` in storage form whose last w positions are
+    the window queries ``q_obs`` of the same units, and whose earlier positions
+    follow the window's recipe (``0.5*eps + 1.5*mu`` with ``mu`` the mean of the
+    unit's salient-span keys, recomputed from the same seed) with noise drawn
+    from ``SeedSequence([cfg, layer, head, 1])``."""
+    ids = list(range(cfg.units)) if units is None else [int(u) for u in units]
+    n_tok = cfg.n if n is None else n
+    U, G, w, d = q_obs.shape
+    dt = np.uint16 if cfg.dtype == "bf16" else np.float32
+    q_all = np.empty((U, G, n_tok, d), dtype=dt)
+    for slot, uid in enumerate(ids):
+        layer, head = uid // cfg.kv_heads, uid % cfg.kv_heads
+        _, _, _, spans = make_unit(cfg, layer, head, n=n)
+        rows = np.concatenate([np.arange(s0, s0 + l) for s0, l in spans])
+        mu = decode(K[slot][rows], cfg.dtype).mean(axis=0)
+        rng = np.random.default_rng(np.random.SeedSequence([cfg.cfg_id, layer, head, 1]))
+        eps = rng.standard_normal((G, n_tok - w, d))
+        q64 = 0.5 * eps + 1.5 * mu[None, None, :]
+        q_all[slot, :, : n_tok - w] = _store(q64.astype(np.float32), cfg.dtype)
+        q_all[slot, :, n_tok - w:] = q_obs[slot]
+    return q_all
