@@ -55,6 +55,8 @@ def parse():
                     help="skip the ragged-budget front-end timings")
     ap.add_argument("--no-carrier", dest="carrier", action="store_false",
                     help="skip the carrier-concentration measurement")
+    ap.add_argument("--no-h2o", dest="h2o", action="store_false",
+                    help="skip the H2O front-end (accumulated-attention scores)")
     ap.add_argument("--no-configs", dest="configs", action="store_false",
                     help="skip the one-layer 32k and 4-layer 128k workloads")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -381,6 +383,72 @@ def key_step(args, cfg, G, hip, stream, qd, Kd, Vd, host=None):
     }
 
 
+def h2o(args, G, hip, stream, want_cpu):
+    """The H2O front-end on one layer of the 32-layer workload (8 KV heads,
+    n = 32768): the accumulated-attention scores of every prefix token over all
+    prompt queries (grkv_h2o_scores), then compression from those scores with
+    no pooling (grkv_compress_scored).  Algorithmic flops of the scores: the
+    causal Q K^T of both passes, 2 * G * n(n+1)/2 * d * 2 per unit."""
+    import numpy as np
+    import torch
+    import workloads as W
+
+    cfg = W.config(4, layers=1)
+    print("bench: H2O front-end (%d units, n=%d)" % (cfg.units, cfg.n), file=sys.stderr, flush=True)
+    q, K, V = W.make_batch(cfg)
+    q_all = W.make_prompt_queries(cfg, q, K)
+    dev = lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
+    qd, Kd, Vd, qa = dev(q), dev(K), dev(V), dev(q_all)
+    w, c, n, d, Gq, U = cfg.window, cfg.budget, cfg.n, cfg.head_dim, cfg.group, cfg.units
+    ws = torch.empty(G.h2o_workspace_bytes(U, Gq, d, G.GRKV_BF16, n), dtype=torch.uint8, device="cuda")
+    s = G.h2o_scores(qa, Kd, w, workspace=ws)
+    res = G.compress_scored(qd, Kd, Vd, w, c, 1, cfg.lam, s)
+    torch.cuda.synchronize()
+
+    def timed(fn, reps):
+        a, b = hip.event(), hip.event()
+        hip.lib.hipEventRecord(a, ctypes.c_void_p(stream.cuda_stream))
+        for _ in range(reps):
+            fn()
+        hip.lib.hipEventRecord(b, ctypes.c_void_p(stream.cuda_stream))
+        torch.cuda.synchronize()
+        return hip.elapsed_ms(a, b) / reps
+
+    ms_scores = timed(lambda: G.h2o_scores(qa, Kd, w, workspace=ws, out=s), 3)
+    ms_comp = timed(lambda: G.compress_scored(qd, Kd, Vd, w, c, 1, cfg.lam, s,
+                                              workspace=res.workspace, out=res), 5)
+    flops = U * 2 * Gq * (n * (n + 1) / 2) * d * 2
+    tflops = flops / (ms_scores / 1e3) / 1e12
+    out = {"workload": "llama3-8b-layer-n32k (layer 0 of the 32-layer workload)", "units": U,
+           "ms_scores": ms_scores, "ms_compress_scored": ms_comp,
+           "heads_per_s": U / ((ms_scores + ms_comp) / 1e3),
+           "roofline": {"bound": "mfma", "kernel": "h2o_lse + h2o_colsum", "achieved": tflops,
+                        "peak": 2500.0, "unit": "TFLOP/s", "frac": tflops / 2500.0,
+                        "traffic": None}}
+    if want_cpu:
+        # the oracle forms each head's n x n attention: timed on the same
+        # recipe at n = 4096 (one unit), the scores and the compression
+        from oracle import grkv_frontend_oracle as FO
+        cs = W.config(4, layers=1, n=4096, budget=256)
+        q2, K2, V2 = W.make_batch(cs, units=[0])
+        qa2 = W.make_prompt_queries(cs, q2, K2, units=[0])
+        t0 = time.perf_counter()
+        done = 0
+        while done < 1 or time.perf_counter() - t0 < 3.0:
+            FO.compress_h2o(W.decode(qa2[0], cs.dtype), W.decode(q2[0], cs.dtype),
+                            W.decode(K2[0], cs.dtype), W.decode(V2[0], cs.dtype), cs.window,
+                            cs.budget, cs.lam)
+            done += 1
+        el = time.perf_counter() - t0
+        rec = oracle_record(done, done, el, "runs of one unit at n = 4096 (H2O scores and "
+                                            "compression, float64 numpy oracle; the oracle "
+                                            "forms n x n attention, so not at n = 32768)")
+        out["cpu_baseline"] = rec
+    del qd, Kd, Vd, qa, res, s, ws
+    torch.cuda.empty_cache()
+    return out
+
+
 def path_bytes_per_unit(cfg):
     """Algorithmic bytes of one unit: read K, V and q_obs once, write idx,
     k_out (input dtype) and v_out (fp32) once."""
@@ -596,6 +664,9 @@ def main():
         cpu = cpu_baseline(cfg, q, K, V, args.cpu_seconds)
 
     path_gbs = U * path_bytes / (ms_step / 1e3) / 1e9
+    h2o_rec = None
+    if args.h2o and args.config == 4:
+        h2o_rec = h2o(args, G, hip, stream, not args.no_cpu_baseline)
     others = None
     if args.configs and args.config == 4:
         del q, K, V
@@ -635,6 +706,7 @@ def main():
         "carrier": car,
         "front_ends": fe,
         "configs": others,
+        "h2o": h2o_rec,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
