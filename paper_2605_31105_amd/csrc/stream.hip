@@ -377,13 +377,16 @@ struct Stream {
   }
 
   __device__ __forceinline__ void flush_colsum(int t) {
-    // column sums of tile t (every wave wrote its part before the last barrier)
-    if (threadIdx.x < TK) {
-      const int key = key0 + t * TK + threadIdx.x;
+    // column sums of tile t (every wave wrote its part before the last
+    // barrier), by the first TK lanes of wave 0 (a wave-uniform test: no
+    // per-step use of the thread index, which would otherwise be held in a
+    // register for the whole loop)
+    if (wave == 0 && lane < TK) {
+      const int key = key0 + t * TK + lane;
       if (key < key_end && key < a.prefix) {
         float c = 0.f;
 #pragma unroll
-        for (int wv = 0; wv < WAVES; ++wv) c += colpart[t & 1][wv][threadIdx.x];
+        for (int wv = 0; wv < WAVES; ++wv) c += colpart[t & 1][wv][lane];
         a.colsum[(size_t)u * a.prefix + key] = c * kFullPUnscale;
       }
     }
