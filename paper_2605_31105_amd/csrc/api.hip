@@ -171,6 +171,9 @@ static void make_key_plan(const Plan& p, int steps, KeyPlan* kp) {
   kp->v0c = take(later * U * p.c * d * sizeof(uint16_t));
   kp->x = take(later * U * mp * p.c * sizeof(float));
   kp->kcur = take(later * U * p.c * d * sizeof(float));
+  kp->ring = key_ring_supported(p);
+  kp->vsplit = take(kp->ring ? 2 * U * p.c * d * sizeof(uint16_t) : 0);
+  kp->fixbits = take(kp->ring ? U * key_fixbits_words(p) * sizeof(uint32_t) : 0);
   kp->total = off;
 }
 
@@ -470,6 +473,11 @@ int grkv_compress_kv(const void* q_obs, const void* K, const void* V, int64_t n,
   a.q = (const uint16_t*)q_obs;
   a.k0 = (const uint16_t*)out->k_out;
   a.vs = out->v_out;
+  if (kp.ring) {
+    a.vh = (uint16_t*)(ws + kp.vsplit);
+    a.vl = a.vh + (size_t)p.U * p.c * p.d;
+    a.fixbits = (uint32_t*)(ws + kp.fixbits);
+  }
   a.lse2 = F(p.lse2_log2);
   a.fixed = (const uint8_t*)(ws + p.fixed);
   a.idx = out->idx;

@@ -63,6 +63,16 @@ __device__ __forceinline__ void split8(const float* x, bf16x8& hi, bf16x8& lo) {
   }
 }
 
+// The same split for two floats: returns the packed hi pair (a in the low
+// half) and stores the packed lo pair.
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b, uint32_t* lo) {
+  const bf16x2 h = __builtin_convertvector((f32x2){a, b}, bf16x2);
+  const uint32_t hw = __builtin_bit_cast(uint32_t, h);
+  const float a0 = __uint_as_float(hw << 16), b0 = __uint_as_float(hw & 0xffff0000u);
+  *lo = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){a - a0, b - b0}, bf16x2));
+  return hw;
+}
+
 // Round-to-nearest-even conversion of 8 floats to fp16.
 __device__ __forceinline__ f16x8 to_f16x8(const float* x) {
   f16x8 h;
@@ -80,6 +90,37 @@ __device__ __forceinline__ f16x8 to_f16x8(const float* x) {
 __device__ __forceinline__ uint32_t bf16x2_to_f16x2(uint32_t w) {
   const f32x2 f = {__uint_as_float(w << 16), __uint_as_float(w & 0xffff0000u)};
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, f16x2));
+}
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef short v8i16 __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+
+// LDS transpose read of 4 x 16-bit values: within a 16-lane group, lane
+// 4e + q supplies the address of row e, elements 4q..4q+3 (8 bytes), and
+// lane i receives element i of the four rows (rows 0..3 in order).
+__device__ __forceinline__ v4i16 ds_read_tr16(const void* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)p);
+}
+
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
+// vmcnt in bits 3:0 and 15:14, expcnt 6:4 and lgkmcnt 11:8 left at maximum).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// Workgroup barrier for the tile ring.  It waits for this wave's own LDS
+// reads and writes and synchronises the waves; it does not wait for the
+// vector-memory counter, so tile loads already in flight stay in flight (a
+// fence-based barrier counts the LDS writes of those loads as pending local
+// stores and would drain them).  The memory clobber keeps the compiler from
+// moving LDS accesses across it.  Completion of the tile about to be read is
+// established before the barrier by an explicit s_waitcnt on vmcnt.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
 // Sum over the 16 lanes that share l/16 (lanes differing in bits 0..3).

@@ -207,6 +207,10 @@ struct KeyPlan {
   // later alternating steps (steps > 1): fp32 copies of Q and V0, the compact
   // bf16 V0, X [U][mp][c] of the fp32 value step, the current keys
   size_t q32, v0f, v0c, x, kcur;
+  // the ring kernel's pass (key_ring.hip) applies: V* as bf16 hi and lo
+  // tensors [U][c][d] each, the fixed flags as bits [U][ceil(c / 32)]
+  bool ring;
+  size_t vsplit, fixbits;
   size_t total;
 };
 
@@ -215,6 +219,9 @@ struct KeyArgs {
   const uint16_t* k0;       // [U][c][d] retained keys K0
   const float* kcur;        // [U][c][d] current keys (fp32) at a later alternating step, or null (K0)
   const float* vs;          // [U][c][d] merged values V*
+  uint16_t* vh;             // [U][c][d] V* hi and lo (bf16), or null: the
+  uint16_t* vl;             // ring kernel's pass is not used
+  uint32_t* fixbits;        // [U][ceil(c / 32)] fixed flags as bits (ring kernel)
   const float* lse2;        // [U][mp] retained log-sum-exp (log2 domain)
   const uint8_t* fixed;     // [U][c]
   const int32_t* idx;       // [U][c] retained positions
@@ -232,6 +239,15 @@ struct KeyArgs {
 
 bool key_supported(const Plan& p);
 hipError_t launch_key(const Plan& p, const KeyPlan& kp, const KeyArgs& a, hipStream_t s);
+// Key-pass ring kernel (mp = 128, d = 128, bf16, first alternating step):
+// V* split into bf16 hi/lo and the fixed flags packed into bits once per key
+// step (key_prep), then the operator (final = false, direction dir) or final
+// (dir = alpha) pass over S splits.
+bool key_ring_supported(const Plan& p);
+size_t key_fixbits_words(const Plan& p);
+hipError_t launch_key_prep(const Plan& p, const KeyArgs& a, hipStream_t s);
+hipError_t launch_key_ring(const Plan& p, const KeyArgs& a, bool final, int S, int chunk,
+                           const float* dir, hipStream_t s);
 hipError_t launch_to_f32(const uint16_t* src, float* dst, size_t n, hipStream_t s);
 
 // H2O accumulated-attention scores (bf16, d 64/128, G in {1, 2, 4, 8}): row

@@ -57,14 +57,6 @@ __device__ __forceinline__ int kperm(int x) {
 // operand hold keys {4g + j/2 (+16 for odd j)} in both.
 __device__ __forceinline__ int tpos(int key) { return 2 * (key & 15) + (key >> 4); }
 
-__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b, uint32_t* lo) {
-  const bf16x2 h = __builtin_convertvector((f32x2){a, b}, bf16x2);
-  const uint32_t hw = __builtin_bit_cast(uint32_t, h);
-  const float a0 = __uint_as_float(hw << 16), b0 = __uint_as_float(hw & 0xffff0000u);
-  *lo = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){a - a0, b - b0}, bf16x2));
-  return hw;
-}
-
 __device__ __forceinline__ float dot4(float4 a, float4 b) {
   return a.x * b.x + a.y * b.y + a.z * b.z + a.w * b.w;
 }
@@ -771,6 +763,22 @@ hipError_t launch_key_t(const Plan& p, const KeyPlan& kp, const KeyArgs& a, hipS
                      a.stats_ws, p.lam, p.m, a.Fm, a.alpha, a.r, a.p, a.sdot, a.W, a.cg);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (!KF && a.vh) {
+    // the ring kernel's passes (key_ring.hip) on V* split once into hi/lo
+    e = launch_key_prep(p, a, s);
+    if (e != hipSuccess) return e;
+    for (int it = 0; it < a.max_iter; ++it) {
+      const bool early = it < kKeyEarlyIters;
+      const int S = early ? kp.S_full : kp.S4, chunk = early ? kp.chunk_full : kp.chunk4;
+      e = launch_key_ring(p, a, false, S, chunk, a.p, s);
+      if (e != hipSuccess) return e;
+      hipLaunchKernelGGL((key_cg_kernel<MP, D>), dim3(p.U), dim3(1024), 0, s, a.opart, a.hpart,
+                         S, a.Fm, a.alpha, a.r, a.p, a.sdot, a.cg, a.lam_k, a.tol, a.max_iter);
+      e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
+    return launch_key_ring(p, a, true, kp.S_full, kp.chunk_full, a.alpha, s);
+  }
   if constexpr (KF) {
     // a later alternating step: the right-hand side gains J_G (K_cur - K0)
     e = launch_pass<MP, D, kJvp, KF>(p, a, kp.S_full, kp.chunk_full, nullptr, s);

@@ -39,10 +39,6 @@
 namespace grkv {
 namespace {
 
-typedef short v4i16 __attribute__((ext_vector_type(4)));
-typedef short v8i16 __attribute__((ext_vector_type(8)));
-typedef __attribute__((address_space(3))) void lds_void;
-typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 
 struct StreamK {
   const u16* q;
@@ -95,25 +91,6 @@ constexpr float kFullPBias = 15.f;
 constexpr float kFullPUnscale = 0x1p-15f;
 constexpr int kRetMaxSlots = 4096;  // retained pass: key slots per block (the plan's split bound)
 constexpr int kTileBytes = kTileElems * 2;
-
-// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
-// vmcnt in bits 3:0 and 15:14, expcnt 6:4 and lgkmcnt 11:8 left at maximum).
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
-}
-
-// Workgroup barrier for the tile ring.  It waits for this wave's own LDS
-// reads and writes and synchronises the waves; it does not wait for the
-// vector-memory counter, so tile loads already in flight stay in flight (a
-// fence-based barrier counts the LDS writes of those loads as pending local
-// stores and would drain them).  The memory clobber keeps the compiler from
-// moving LDS accesses across it.  Completion of the tile about to be read is
-// established before the barrier by an explicit s_waitcnt on vmcnt.
-__device__ __forceinline__ void lds_barrier() {
-  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-}
 
 // Sum of each of NV values (8 or 16) over the 16 lanes of a DPP row, as a
 // reduce-scatter: each step pairs lanes that differ in one bit b of l16 (and
