@@ -173,7 +173,7 @@ static void make_key_plan(const Plan& p, int steps, KeyPlan* kp) {
   kp->kcur = take(later * U * p.c * d * sizeof(float));
   kp->ring = key_ring_supported(p);
   kp->vsplit = take(kp->ring ? 2 * U * p.c * d * sizeof(uint16_t) : 0);
-  kp->fixbits = take(kp->ring ? U * key_fixbits_words(p) * sizeof(uint32_t) : 0);
+  kp->xs = take(kp->ring ? key_x_bytes(p) : 0);
   kp->total = off;
 }
 
@@ -476,7 +476,7 @@ int grkv_compress_kv(const void* q_obs, const void* K, const void* V, int64_t n,
   if (kp.ring) {
     a.vh = (uint16_t*)(ws + kp.vsplit);
     a.vl = a.vh + (size_t)p.U * p.c * p.d;
-    a.fixbits = (uint32_t*)(ws + kp.fixbits);
+    a.xs = F(kp.xs);
   }
   a.lse2 = F(p.lse2_log2);
   a.fixed = (const uint8_t*)(ws + p.fixed);

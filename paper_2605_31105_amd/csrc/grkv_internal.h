@@ -208,9 +208,9 @@ struct KeyPlan {
   // bf16 V0, X [U][mp][c] of the fp32 value step, the current keys
   size_t q32, v0f, v0c, x, kcur;
   // the ring kernel's pass (key_ring.hip) applies: V* as bf16 hi and lo
-  // tensors [U][c][d] each, the fixed flags as bits [U][ceil(c / 32)]
+  // tensors [U][c][d] each, the X^T tiles [U][ceil(c / 32)][4096] (fp32)
   bool ring;
-  size_t vsplit, fixbits;
+  size_t vsplit, xs;
   size_t total;
 };
 
@@ -221,7 +221,7 @@ struct KeyArgs {
   const float* vs;          // [U][c][d] merged values V*
   uint16_t* vh;             // [U][c][d] V* hi and lo (bf16), or null: the
   uint16_t* vl;             // ring kernel's pass is not used
-  uint32_t* fixbits;        // [U][ceil(c / 32)] fixed flags as bits (ring kernel)
+  float* xs;                // [U][ceil(c / 32)][4096] X^T tiles (ring kernel)
   const float* lse2;        // [U][mp] retained log-sum-exp (log2 domain)
   const uint8_t* fixed;     // [U][c]
   const int32_t* idx;       // [U][c] retained positions
@@ -240,11 +240,11 @@ struct KeyArgs {
 bool key_supported(const Plan& p);
 hipError_t launch_key(const Plan& p, const KeyPlan& kp, const KeyArgs& a, hipStream_t s);
 // Key-pass ring kernel (mp = 128, d = 128, bf16, first alternating step):
-// V* split into bf16 hi/lo and the fixed flags packed into bits once per key
-// step (key_prep), then the operator (final = false, direction dir) or final
-// (dir = alpha) pass over S splits.
+// V* split into bf16 hi/lo and the retained-set softmax X written as tiles
+// once per key step (key_prep), then the operator (final = false, direction
+// dir) or final (dir = alpha) pass over S splits.
 bool key_ring_supported(const Plan& p);
-size_t key_fixbits_words(const Plan& p);
+size_t key_x_bytes(const Plan& p);
 hipError_t launch_key_prep(const Plan& p, const KeyArgs& a, hipStream_t s);
 hipError_t launch_key_ring(const Plan& p, const KeyArgs& a, bool final, int S, int chunk,
                            const float* dir, hipStream_t s);

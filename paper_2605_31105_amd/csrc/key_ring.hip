@@ -3,28 +3,29 @@
 // the kOp and kFinal passes of the first alternating step (K_cur = K0), with
 // the contract of key_pass in key.hip.
 //
-//  * Products are taken transposed, keys x rows: S^T = K Q^T and
-//    B^T = V* p^T (K and V* tiles as the A operand, Q and the direction p as
-//    B).  X^T, D^T and A^T = D^T W (W = Q Q^T / d is symmetric) then share one
-//    layout, and H^T = X^T o A^T is already the B operand of
-//    out^T += V*^T H^T once the keys of an operand are ordered
-//    {4g .. 4g+3, 16+4g .. 16+4g+3} (g = lane / 16).
+//  * Products are taken transposed, keys x rows: B^T = V* p^T (the V* tile as
+//    the A operand, the direction p as B).  X^T, D^T and A^T = D^T W
+//    (W = Q Q^T / d is symmetric) then share one layout, and H^T = X^T o A^T
+//    is already the B operand of out^T += V*^T H^T once the keys of an
+//    operand are ordered {4g .. 4g+3, 16+4g .. 16+4g+3} (g = lane / 16).
+//  * X (the retained-set softmax weights at K0 against the retained LSE, zero
+//    at invisible and fixed slots) does not change over the conjugate-gradient
+//    iterations: key_x writes it once per key step, tile by tile in the lane
+//    order the passes read it in, and the passes stream it instead of K0.
+//    V* is split once per key step into bf16 hi and lo tensors (key_prep).
 //  * One block per (unit, split) of 8 waves in two roles, one of each per
 //    SIMD.  Producer waves 0-3 (rows 32w .. 32w+31) run phase A of a tile:
-//    S^T, B^T, X^T and D^T; consumer waves 4-7 (the same rows) run phase B of
-//    the tile before: A^T = D^T W, H^T, out^T.  Each role holds only its own
-//    operands in registers (Q and p, or W and the output), and the MFMAs of
-//    one role run beside the exponentials and operand packing of the other.
-//  * V* is split once per key step into bf16 hi and lo tensors (key_prep), so
-//    a tile is three bf16 tensors (K0, V* hi, V* lo) that go from HBM straight
-//    into a four-stage LDS ring (global_load_lds, no register staging); two
-//    tiles stay in flight while two are read.  V*^T operands come from the
-//    row-major V* tiles by the LDS transpose read.
-//  * D (row-major, hi and lo) and X^T (in the producer lanes' own order) are
-//    handed over through double-buffered LDS; one barrier per interval
-//    publishes them, the next ring stage and the stage that is refilled.
-//  * The fixed flags of a tile are one 32-bit word (built by key_prep), read
-//    by a scalar load.
+//    B^T and D^T = X^T o (B^T - s); consumer waves 4-7 (the same rows) run
+//    phase B of the tile before: A^T = D^T W, H^T, out^T.  Each role holds
+//    only its own operands in registers (p, or W and the output), and the
+//    MFMAs of one role run beside the operand packing of the other.
+//  * A tile (X^T fp32, V* hi, V* lo) goes from HBM straight into a four-stage
+//    LDS ring (direct loads, no register staging); two tiles stay in flight
+//    while two are read.  V*^T operands come from the row-major V* tiles by
+//    the LDS transpose read.
+//  * D (row-major, hi and lo) is handed to the consumers through a
+//    double-buffered LDS tile; one barrier per interval publishes it, the next
+//    ring stage and the stage that is refilled.
 //  * Products of fp32 values use three bf16 MFMAs (hi*hi + hi*lo + lo*hi),
 //    as in key.hip.
 #include <math.h>
@@ -41,10 +42,10 @@ constexpr int kRW = 8;                            // waves: 4 producers, 4 consu
 constexpr int kRTh = kRW * 64;
 constexpr int kRTK = 32;                          // keys per tile
 constexpr int kRTB = kRTK * kRD * 2;              // one bf16 tensor tile (8 KB)
-constexpr int kRStage = 3 * kRTB;                 // K0, V* hi, V* lo
+constexpr int kRXB = kRMP * kRTK * 4;             // X^T of a tile (fp32, 16 KB)
+constexpr int kRStage = kRXB + 2 * kRTB;          // X^T, V* hi, V* lo
 constexpr int kRDB = kRMP * kRTK * 2;             // one D tile, hi or lo (8 KB)
-constexpr int kRXB = 4 * 16 * 64 * 4;             // X^T of a tile, 16 floats per producer lane
-constexpr int kRLoads = 3 * (kRTB / 1024) / kRW;  // tile loads per wave per tile (3)
+constexpr int kRLoads = kRStage / 1024 / kRW;     // tile loads per wave per tile (4)
 
 // 16-byte chunk permutations inside a 256-byte tile row (key row r).  K rows
 // are read 16 rows x one chunk (r mod 16 keeps those on distinct banks); V*
@@ -60,6 +61,7 @@ __device__ __forceinline__ int dswz(int R) { return ((R >> 2) & 3) << 1; }
 struct RingArgs {
   const u16* q;        // [U][m][d]
   const u16* k0;       // [U][c][d]
+  const float* xs;     // [U][ceil(c / 32)][4096] X^T tiles (key_x)
   const u16* vh;       // [U][c][d] V* hi
   const u16* vl;       // [U][c][d] V* lo
   const float* lse2;   // [U][mp]
@@ -72,7 +74,7 @@ struct RingArgs {
   float* hpart;        // [U][S][mp]
   float* kstar;        // [U][c][d]
   float* cg_info;      // [U][4] or null
-  int m, w, c, nw, S, chunk, causal;
+  int m, w, c, ntc, S, chunk, causal;   // ntc = ceil(c / 32)
   float scale_log2, inv_sqrt_d;
 };
 
@@ -98,19 +100,14 @@ __device__ __forceinline__ void dma16(const void* base, uint32_t voff, uint32_t 
                : "memory", "m0");
 }
 
-// fixbits [U][nw]: bit j of word t set when slot 32t + j is fixed (a separate
-// read-only argument, so that its wave-uniform reads are scalar loads).
 template <bool FINAL>
-__global__ __launch_bounds__(kRTh) void key_ring_kernel(RingArgs a,
-                                                        const uint32_t* __restrict__ fixbits) {
+__global__ __launch_bounds__(kRTh) void key_ring_kernel(RingArgs a) {
   __shared__ __attribute__((aligned(16))) char stg0[kRStage];
   __shared__ __attribute__((aligned(16))) char stg1[kRStage];
   __shared__ __attribute__((aligned(16))) char stg2[kRStage];
   __shared__ __attribute__((aligned(16))) char stg3[kRStage];
   __shared__ __attribute__((aligned(16))) char dbuf0[2 * kRDB];   // D hi, then D lo
   __shared__ __attribute__((aligned(16))) char dbuf1[2 * kRDB];
-  __shared__ __attribute__((aligned(16))) char xbuf0[kRXB];
-  __shared__ __attribute__((aligned(16))) char xbuf1[kRXB];
 
   const int u = blockIdx.y, s = blockIdx.x, tid = threadIdx.x;
   const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -147,44 +144,42 @@ __global__ __launch_bounds__(kRTh) void key_ring_kernel(RingArgs a,
   const int e = l16 >> 2, qq = l16 & 3;
   const int last = ntiles - 1;
 
-  // tile t of the split into a stage (K0, V* hi, V* lo: 24 wave loads of
-  // 1 KB, three per wave), rows past the split's end clamped to its last key
-  // (finite data, masked below)
-  // tile t of the split into a stage (K0, V* hi, V* lo: 24 wave loads of
-  // 1 KB, three per wave): a uniform base (the tile's first row) plus each
-  // lane's byte offset (its row and chunk); rows past the split's end are
-  // clamped to its last key (finite data, masked below)
+  // tile t of the split into a stage (X^T, V* hi, V* lo: 32 wave loads of
+  // 1 KB, four per wave): a uniform base (the tile's start) plus each lane's
+  // byte offset; V* rows past the split's end are clamped to its last key
+  // (finite data; X is zero there)
+  const int tg0 = j0 / kRTK;   // first tile of the split (splits are whole tiles)
   auto issue = [&](int t, char* stage) {
     const int tile0 = j0 + t * kRTK;
 #pragma unroll
     for (int it = 0; it < kRLoads; ++it) {
-      const int instr = wave * kRLoads + it;      // 0..23
-      const int tensor = instr >> 3, part = instr & 7;
-      const int r = part * 4 + (lane >> 4), pos = lane & 15;
-      const u16* base = (tensor == 0 ? a.k0 : tensor == 1 ? a.vh : a.vl) + ((size_t)u * c + tile0) * kRD;
-      const int rr = min(tile0 + r, j1 - 1) - tile0;
-      const uint32_t vo = (uint32_t)((rr * kRD + (pos ^ (tensor == 0 ? kswz(r) : vswz(r))) * 8) * 2);
-      dma16(base, vo, lds_off(stage) + tensor * kRTB + part * 1024);
+      const int instr = wave * kRLoads + it;      // 0..31
+      if (instr < kRXB / 1024) {
+        const float* base = a.xs + ((size_t)u * a.ntc + tg0 + t) * (kRXB / 4);
+        dma16(base, (uint32_t)(instr * 1024 + lane * 16), lds_off(stage) + instr * 1024);
+      } else {
+        const int vi = instr - kRXB / 1024, tensor = vi >> 3, part = vi & 7;
+        const int r = part * 4 + (lane >> 4), pos = lane & 15;
+        const u16* base = (tensor == 0 ? a.vh : a.vl) + ((size_t)u * c + tile0) * kRD;
+        const int rr = min(tile0 + r, j1 - 1) - tile0;
+        const uint32_t vo = (uint32_t)((rr * kRD + (pos ^ vswz(r)) * 8) * 2);
+        dma16(base, vo, lds_off(stage) + kRXB + tensor * kRTB + part * 1024);
+      }
     }
   };
 
   if (producer) {
     // ---------------------------------------------------------------- phase A
-    uint4 qb[2][kRD / 32];
     bf16x8 ph[2][kRD / 32], pl[2][kRD / 32];
-    float sd[2], nl[2];
-    int vlim[2];
+    float sd[2];
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) {
       const int row = row0 + 16 * rt + l16;
-      const bool ok = row < a.m;
-      const u16* qr = a.q + ((size_t)u * a.m + row) * kRD;
       const float* pr = a.dir + ((size_t)u * kRMP + row) * kRD;
       const float* fr = a.Fm + ((size_t)u * kRMP + row) * kRD;
       float acc = 0.f;
 #pragma unroll
       for (int ks = 0; ks < kRD / 32; ++ks) {
-        qb[rt][ks] = ok ? *reinterpret_cast<const uint4*>(qr + ks * 32 + 8 * g) : make_uint4(0, 0, 0, 0);
         const float4 x0 = *reinterpret_cast<const float4*>(pr + ks * 32 + 8 * g);
         const float4 x1 = *reinterpret_cast<const float4*>(pr + ks * 32 + 8 * g + 4);
         const float x[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
@@ -203,17 +198,11 @@ __global__ __launch_bounds__(kRTh) void key_ring_kernel(RingArgs a,
       } else {
         sd[rt] = a.sdot[(size_t)u * kRMP + row];
       }
-      nl[rt] = ok ? -a.lse2[(size_t)u * kRMP + row] : -__builtin_huge_valf();
-      // one past the last slot the row sees: the split's end, or its own
-      // window position (the window is the last w retained slots)
-      vlim[rt] = a.causal ? min(j1, c - a.w + row % a.w + 1) : j1;
     }
-    uint32_t kofs[kRD / 32], vofs[kRD / 32];   // operand chunk 4ks + g of key row l16
+    uint32_t vofs[kRD / 32];   // operand chunk 4ks + g of key row l16
 #pragma unroll
-    for (int ks = 0; ks < kRD / 32; ++ks) {
-      kofs[ks] = (uint32_t)(l16 * 256 + 16 * ((4 * ks + g) ^ kswz(l16)));
-      vofs[ks] = (uint32_t)(kRTB + l16 * 256 + 16 * ((4 * ks + g) ^ vswz(l16)));
-    }
+    for (int ks = 0; ks < kRD / 32; ++ks)
+      vofs[ks] = (uint32_t)(kRXB + l16 * 256 + 16 * ((4 * ks + g) ^ vswz(l16)));
     // D row writes: row row0 + l16 (+16 per row tile), keys 16kt + 4g .. +3
     uint32_t dwo[2];
 #pragma unroll
@@ -221,29 +210,23 @@ __global__ __launch_bounds__(kRTh) void key_ring_kernel(RingArgs a,
       const int R = row0 + l16;
       dwo[kt] = (uint32_t)(R * 64 + 8 * ((4 * kt + g) ^ dswz(R)));
     }
-    const uint32_t xwo = (uint32_t)(rw * 4096 + lane * 16);
-    const uint32_t* fb = fixbits + (size_t)u * a.nw + j0 / kRTK;
+    const uint32_t xo = (uint32_t)(rw * 4096 + lane * 16);   // this lane's X^T slots
 
-    // Phase A of tile t from stage sa: S^T and B^T (lane holds
-    // [key 16kt + 4g + i][row 16rt + l16]), X^T = softmax weights against the
-    // retained LSE, D^T = X^T o (B^T - s) with the fixed keys' columns zero;
-    // D rows and X^T to LDS.
-    auto phase_a = [&](int t, uint32_t fx, const char* sa, char* dw, char* xw) {
+    // Phase A of a tile from stage sa: B^T - s (lane holds
+    // [key 16kt + 4g + i][row 16rt + l16]) and D^T = X^T o (B^T - s); D rows
+    // to LDS.
+    auto phase_a = [&](const char* sa, char* dw) {
       // B^T accumulates from -s, so that it ends as B^T - s
-      f32x4 st[2][2], bt[2][2];
+      f32x4 bt[2][2];
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-        for (int rt = 0; rt < 2; ++rt) {
-          st[kt][rt] = zero4();
-          bt[kt][rt] = f32x4{-sd[rt], -sd[rt], -sd[rt], -sd[rt]};
-        }
+        for (int rt = 0; rt < 2; ++rt) bt[kt][rt] = f32x4{-sd[rt], -sd[rt], -sd[rt], -sd[rt]};
       // steps (ks, kt), the operands of the next step read before the MFMAs
       // of this one
-      uint4 kf[2], vhf[2], vlf[2];
+      uint4 vhf[2], vlf[2];
       auto rd = [&](int step, int b) {
         const int ks = step >> 1, kt = step & 1;
-        kf[b] = *reinterpret_cast<const uint4*>(sa + kofs[ks] + kt * 4096);
         vhf[b] = *reinterpret_cast<const uint4*>(sa + vofs[ks] + kt * 4096);
         vlf[b] = *reinterpret_cast<const uint4*>(sa + kRTB + vofs[ks] + kt * 4096);
       };
@@ -255,51 +238,25 @@ __global__ __launch_bounds__(kRTh) void key_ring_kernel(RingArgs a,
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt) {
-          st[kt][rt] = mfma_bf16(as_bf16x8(kf[b]), as_bf16x8(qb[rt][ks]), st[kt][rt]);
           bt[kt][rt] = mfma_bf16(as_bf16x8(vhf[b]), ph[rt][ks], bt[kt][rt]);
           bt[kt][rt] = mfma_bf16(as_bf16x8(vlf[b]), ph[rt][ks], bt[kt][rt]);
           bt[kt][rt] = mfma_bf16(as_bf16x8(vhf[b]), pl[rt][ks], bt[kt][rt]);
         }
         __builtin_amdgcn_sched_barrier(0);
       }
-      const int tile0 = j0 + t * kRTK;
-      float xk[2][2][4];
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-        const int kb0 = 16 * kt + 4 * g;              // the lane's first key in the tile
-        const uint32_t fr4 = (fx >> kb0) & 0xfu;      // fixed flags of its four keys
-        float dv[2][4];
-#pragma unroll
-        for (int rt = 0; rt < 2; ++rt) {
-          // keys i < nvis of the four are live and visible to the row; X is
-          // zero at the others and at fixed keys (whose D^T and H^T rows
-          // vanish either way)
-          const int nvis = vlim[rt] - tile0 - kb0;
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const bool keep = i < nvis && ((fr4 >> i) & 1u) == 0;
-            const float x =
-                keep ? __builtin_amdgcn_exp2f(fmaf(st[kt][rt][i], a.scale_log2, nl[rt])) : 0.f;
-            xk[kt][rt][i] = x;
-            dv[rt][i] = x * bt[kt][rt][i];
-          }
-        }
-#pragma unroll
-        for (int rt = 0; rt < 2; ++rt) {
-          uint32_t l0, l1;
-          const uint32_t h0 = pack_bf16x2(dv[rt][0], dv[rt][1], &l0);
-          const uint32_t h1 = pack_bf16x2(dv[rt][2], dv[rt][3], &l1);
-          *reinterpret_cast<uint2*>(dw + rt * 1024 + dwo[kt]) = make_uint2(h0, h1);
-          *reinterpret_cast<uint2*>(dw + kRDB + rt * 1024 + dwo[kt]) = make_uint2(l0, l1);
-        }
-      }
-      // X^T: 16 floats per lane, slot (2kt + rt) of 4, each a 1 KB row of lanes
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt) {
-          *reinterpret_cast<f32x4*>(xw + xwo + (2 * kt + rt) * 1024) =
-              f32x4{xk[kt][rt][0], xk[kt][rt][1], xk[kt][rt][2], xk[kt][rt][3]};
+          const f32x4 x = *reinterpret_cast<const f32x4*>(sa + xo + (2 * kt + rt) * 1024);
+          float dv[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) dv[i] = x[i] * bt[kt][rt][i];
+          uint32_t l0, l1;
+          const uint32_t h0 = pack_bf16x2(dv[0], dv[1], &l0);
+          const uint32_t h1 = pack_bf16x2(dv[2], dv[3], &l1);
+          *reinterpret_cast<uint2*>(dw + rt * 1024 + dwo[kt]) = make_uint2(h0, h1);
+          *reinterpret_cast<uint2*>(dw + kRDB + rt * 1024 + dwo[kt]) = make_uint2(l0, l1);
         }
     };
 
@@ -312,25 +269,25 @@ __global__ __launch_bounds__(kRTh) void key_ring_kernel(RingArgs a,
     issue(min(1, last), stg1);
     wait_vmcnt<kRLoads>();
     lds_barrier();
-    auto interval = [&](int k, const char* sa, char* refill, char* dw, char* xw) {
+    auto interval = [&](int k, const char* sa, char* refill, char* dw) {
       issue(min(k + 2, last), refill);
-      phase_a(k, fb[k], sa, dw, xw);
+      phase_a(sa, dw);
       // every interval issues one tile, so exactly one later tile's loads
       // may still be in flight once the next tile has landed
       wait_vmcnt<kRLoads>();
       lds_barrier();
     };
-    interval(0, stg0, stg2, dbuf0, xbuf0);
+    interval(0, stg0, stg2, dbuf0);
     int k = 1;
     for (; k + 4 <= ntiles; k += 4) {
-      interval(k + 0, stg1, stg3, dbuf1, xbuf1);
-      interval(k + 1, stg2, stg0, dbuf0, xbuf0);
-      interval(k + 2, stg3, stg1, dbuf1, xbuf1);
-      interval(k + 3, stg0, stg2, dbuf0, xbuf0);
+      interval(k + 0, stg1, stg3, dbuf1);
+      interval(k + 1, stg2, stg0, dbuf0);
+      interval(k + 2, stg3, stg1, dbuf1);
+      interval(k + 3, stg0, stg2, dbuf0);
     }
-    if (k < ntiles) interval(k, stg1, stg3, dbuf1, xbuf1);
-    if (k + 1 < ntiles) interval(k + 1, stg2, stg0, dbuf0, xbuf0);
-    if (k + 2 < ntiles) interval(k + 2, stg3, stg1, dbuf1, xbuf1);
+    if (k < ntiles) interval(k, stg1, stg3, dbuf1);
+    if (k + 1 < ntiles) interval(k + 1, stg2, stg0, dbuf0);
+    if (k + 2 < ntiles) interval(k + 2, stg3, stg1, dbuf1);
     // the clamped loads past the end land before the block's LDS is released
     wait_vmcnt<0>();
     return;
@@ -339,8 +296,8 @@ __global__ __launch_bounds__(kRTh) void key_ring_kernel(RingArgs a,
   // ------------------------------------------------------------------ phase B
   // kOp: W rows (B operand of A^T = D^T W), columns 32kb + 8g .. +7
   bf16x8 wh[FINAL ? 1 : 2][kRMP / 32], wl[FINAL ? 1 : 2][kRMP / 32];
-  // kFinal: Q columns 16 (2 rw + dd) + l16 at rows 32kb + 8g .. +7 (B operand
-  // of dK = D^T Q)
+  // kFinal: Q columns 16 (2 rw + dd) + l16 at rows 32kb + 8g .. +7 (A operand
+  // of dK^T = Q^T D)
   bf16x8 qt[FINAL ? 2 : 1][kRMP / 32];
   if constexpr (!FINAL) {
 #pragma unroll
@@ -375,7 +332,7 @@ __global__ __launch_bounds__(kRTh) void key_ring_kernel(RingArgs a,
     const int vr = 4 * g + e;
 #pragma unroll
     for (int dt = 0; dt < kRD / 16; ++dt)
-      vtofs[dt] = (uint32_t)(kRTB + vr * 256 + 16 * ((2 * dt + (qq >> 1)) ^ vswz(vr)) + 8 * (qq & 1));
+      vtofs[dt] = (uint32_t)(kRXB + vr * 256 + 16 * ((2 * dt + (qq >> 1)) ^ vswz(vr)) + 8 * (qq & 1));
   }
   // D transpose reads: row 8g + 4h + e (+32 per kb), keys 16kt + 4qq .. +3
   uint32_t dro[2][2];
@@ -401,9 +358,26 @@ __global__ __launch_bounds__(kRTh) void key_ring_kernel(RingArgs a,
     dh = cat8(ds_read_tr16(dp + dro[kt][0]), ds_read_tr16(dp + dro[kt][1]));
     dl = cat8(ds_read_tr16(dp + kRDB + dro[kt][0]), ds_read_tr16(dp + kRDB + dro[kt][1]));
   };
-  // Phase B of tile t: D_t from dr, X^T from xr, the tile's V* (or K0) from
-  // stage sb.
-  auto phase_b = [&](int t, const char* sb, const char* dr, const char* xr) {
+  // kFinal: K0 of the lane's four d columns at the keys of (kt, dd), for the
+  // tile in phase B.  Issued as inline assembly, ahead of the interval's tile
+  // loads, and completed by a counted wait that names these registers.
+  uint64_t k0r[2][2];
+  auto k0load = [&](int t) {
+    if constexpr (FINAL) {
+      const int tile0 = j0 + t * kRTK;
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int dd = 0; dd < 2; ++dd) {
+          const int key = min(tile0 + 16 * kt + l16, j1 - 1);
+          const u16* p = a.k0 + ((size_t)u * c + key) * kRD + 16 * (2 * rw + dd) + 4 * g;
+          asm volatile("global_load_dwordx2 %0, %1, off" : "=v"(k0r[kt][dd]) : "v"(p) : "memory");
+        }
+    }
+  };
+  // Phase B of tile t: D_t from dr, X^T and V* from stage sb (tail: the last
+  // interval, with no tile loads after the K0 loads).
+  auto phase_b = [&](int t, const char* sb, const char* dr, bool tail) {
     if constexpr (!FINAL) {
       // A^T = D^T W in the layout of X^T, steps (kb, kt), the D^T fragments
       // of the next step read before the MFMAs of this one
@@ -440,7 +414,7 @@ __global__ __launch_bounds__(kRTh) void key_ring_kernel(RingArgs a,
       for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt)
-          xv[kt][rt] = *reinterpret_cast<const f32x4*>(xr + xro + (2 * kt + rt) * 1024);
+          xv[kt][rt] = *reinterpret_cast<const f32x4*>(sb + xro + (2 * kt + rt) * 1024);
       vfrag(0, 0);
       // H^T = X^T o A^T as the B operand (keys 4g + j, then 16 + 4g + j)
       bf16x8 hh[2], hl[2];
@@ -472,8 +446,11 @@ __global__ __launch_bounds__(kRTh) void key_ring_kernel(RingArgs a,
         __builtin_amdgcn_sched_barrier(0);
       }
     } else {
-      // dK [keys x d] = D^T Q / sqrt(d) for the d columns 16 (2 rw + dd) + l16;
-      // K* = K0 + dK (fixed keys: D^T = 0, K* = K0 exactly)
+      // dK^T [d x keys] = Q^T D / sqrt(d) for the d columns 16 (2 rw + dd) + ..;
+      // lane holds dK[key 16kt + l16][d 16 (2 rw + dd) + 4g + i].  K* = K0 + dK
+      // (fixed keys: D = 0, K* = K0 exactly), K0 from the loads issued at the
+      // start of the interval (before the tile loads, so that only those may
+      // still be in flight once it has landed)
       f32x4 acc[2][2];
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
@@ -487,28 +464,34 @@ __global__ __launch_bounds__(kRTh) void key_ring_kernel(RingArgs a,
           dfrag(dr, kt, kb, dh, dl);
 #pragma unroll
           for (int dd = 0; dd < 2; ++dd) {
-            acc[kt][dd] = mfma_bf16(dh, qt[dd][kb], acc[kt][dd]);
-            acc[kt][dd] = mfma_bf16(dl, qt[dd][kb], acc[kt][dd]);
+            acc[kt][dd] = mfma_bf16(qt[dd][kb], dh, acc[kt][dd]);
+            acc[kt][dd] = mfma_bf16(qt[dd][kb], dl, acc[kt][dd]);
           }
         }
+      if (tail)
+        asm volatile("s_waitcnt vmcnt(0)" : "+v"(k0r[0][0]), "+v"(k0r[0][1]), "+v"(k0r[1][0]),
+                     "+v"(k0r[1][1]));
+      else
+        asm volatile("s_waitcnt vmcnt(%4)"
+                     : "+v"(k0r[0][0]), "+v"(k0r[0][1]), "+v"(k0r[1][0]), "+v"(k0r[1][1])
+                     : "n"(kRLoads));
       const int tile0 = j0 + t * kRTK;
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
+      for (int kt = 0; kt < 2; ++kt) {
+        const int key = tile0 + 16 * kt + l16;
+        if (key < j1) {
 #pragma unroll
-        for (int dd = 0; dd < 2; ++dd) {
-          const int col = 16 * (2 * rw + dd) + l16;
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int r = 16 * kt + 4 * g + i;
-            const int key = tile0 + r;
-            if (key < j1) {
-              const u16 k0v = *reinterpret_cast<const u16*>(
-                  sb + r * 256 + 16 * ((col >> 3) ^ kswz(r)) + 2 * (col & 7));
-              a.kstar[((size_t)u * c + key) * kRD + col] =
-                  bf16_to_f32(k0v) + acc[kt][dd][i] * a.inv_sqrt_d;
-            }
+          for (int dd = 0; dd < 2; ++dd) {
+            const uint64_t kv = k0r[kt][dd];
+            const f32x4 o = {bf16_to_f32((u16)kv) + acc[kt][dd][0] * a.inv_sqrt_d,
+                             bf16_to_f32((u16)(kv >> 16)) + acc[kt][dd][1] * a.inv_sqrt_d,
+                             bf16_to_f32((u16)(kv >> 32)) + acc[kt][dd][2] * a.inv_sqrt_d,
+                             bf16_to_f32((u16)(kv >> 48)) + acc[kt][dd][3] * a.inv_sqrt_d};
+            *reinterpret_cast<f32x4*>(a.kstar + ((size_t)u * c + key) * kRD + 16 * (2 * rw + dd) +
+                                      4 * g) = o;
           }
         }
+      }
     }
   };
 
@@ -522,30 +505,31 @@ __global__ __launch_bounds__(kRTh) void key_ring_kernel(RingArgs a,
   issue(min(2, last), stg2);
   wait_vmcnt<kRLoads>();
   lds_barrier();
-  auto interval = [&](int k, const char* sb, char* refill, const char* dr, const char* xr) {
+  auto interval = [&](int k, const char* sb, char* refill, const char* dr) {
+    k0load(k - 1);
     issue(min(k + 2, last), refill);
-    phase_b(k - 1, sb, dr, xr);
+    phase_b(k - 1, sb, dr, false);
     wait_vmcnt<kRLoads>();
     lds_barrier();
   };
   int k = 1;
   for (; k + 4 <= ntiles; k += 4) {
-    interval(k + 0, stg0, stg3, dbuf0, xbuf0);
-    interval(k + 1, stg1, stg0, dbuf1, xbuf1);
-    interval(k + 2, stg2, stg1, dbuf0, xbuf0);
-    interval(k + 3, stg3, stg2, dbuf1, xbuf1);
+    interval(k + 0, stg0, stg3, dbuf0);
+    interval(k + 1, stg1, stg0, dbuf1);
+    interval(k + 2, stg2, stg1, dbuf0);
+    interval(k + 3, stg3, stg2, dbuf1);
   }
-  if (k < ntiles) interval(k, stg0, stg3, dbuf0, xbuf0);
-  if (k + 1 < ntiles) interval(k + 1, stg1, stg0, dbuf1, xbuf1);
-  if (k + 2 < ntiles) interval(k + 2, stg2, stg1, dbuf0, xbuf0);
+  if (k < ntiles) interval(k, stg0, stg3, dbuf0);
+  if (k + 1 < ntiles) interval(k + 1, stg1, stg0, dbuf1);
+  if (k + 2 < ntiles) interval(k + 2, stg2, stg1, dbuf0);
   // the last interval: phase B of tile ntiles-1, after every load has landed
   // (its stage and buffers are picked at run time)
   wait_vmcnt<0>();
   {
     const char* sb = (last & 3) == 0 ? stg0 : (last & 3) == 1 ? stg1 : (last & 3) == 2 ? stg2 : stg3;
     const char* dr = (last & 1) ? dbuf1 : dbuf0;
-    const char* xr = (last & 1) ? xbuf1 : xbuf0;
-    phase_b(last, sb, dr, xr);
+    k0load(last);
+    phase_b(last, sb, dr, true);
   }
 
   if constexpr (!FINAL) {
@@ -566,30 +550,93 @@ __global__ __launch_bounds__(kRTh) void key_ring_kernel(RingArgs a,
   }
 }
 
-// V* to bf16 hi + lo, and the fixed flags to one bit per slot (bit j of word
-// t is slot 32t + j; slots past c count as fixed).
+// V* to bf16 hi + lo.
 __global__ __launch_bounds__(256) void key_prep_kernel(const float* __restrict__ v,
                                                        u16* __restrict__ vh, u16* __restrict__ vl,
-                                                       size_t n4, const uint8_t* __restrict__ fixed,
-                                                       uint32_t* __restrict__ bits, int U, int c,
-                                                       int nw) {
-  const size_t stride = (size_t)gridDim.x * blockDim.x;
-  const size_t t0 = blockIdx.x * (size_t)blockDim.x + threadIdx.x;
-  for (size_t i = t0; i < n4; i += stride) {
+                                                       size_t n4) {
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n4;
+       i += (size_t)gridDim.x * blockDim.x) {
     const float4 x = reinterpret_cast<const float4*>(v)[i];
     uint32_t l0, l1;
     const uint32_t h0 = pack_bf16x2(x.x, x.y, &l0), h1 = pack_bf16x2(x.z, x.w, &l1);
     reinterpret_cast<uint2*>(vh)[i] = make_uint2(h0, h1);
     reinterpret_cast<uint2*>(vl)[i] = make_uint2(l0, l1);
   }
-  for (size_t i = t0; i < (size_t)U * nw; i += stride) {
-    const int u = (int)(i / nw), t = (int)(i % nw);
-    uint32_t b = 0;
-    for (int j = 0; j < 32; ++j) {
-      const int slot = 32 * t + j;
-      if (slot >= c || fixed[(size_t)u * c + slot]) b |= 1u << j;
+}
+
+// X^T tiles of the retained set at K0: X = 2^(Q K0^T log2(e) / sqrt(d) - LSE)
+// against the retained log-sum-exp (the value step's retained-set softmax),
+// zero at slots a row cannot see (past c, or later window positions) and at
+// fixed slots.  Tile t of unit u holds keys 32t .. 32t+31 as 16 floats per
+// lane of the ring kernel's producer waves: float (((rw * 4 + 2kt + rt) * 64
+// + lane) * 4 + i) is X[row 32rw + 16rt + l16][key 32t + 16kt + 4g + i].
+// One block of 4 waves (32 rows each) per kXTiles tiles of a unit.
+constexpr int kXTiles = 1;
+
+__global__ __launch_bounds__(256) void key_x_kernel(const u16* __restrict__ q,
+                                                    const u16* __restrict__ k0,
+                                                    const float* __restrict__ lse2,
+                                                    const uint8_t* __restrict__ fixed,
+                                                    float* __restrict__ xs, int m, int w, int c,
+                                                    int ntc, int causal, float scale_log2) {
+  const int u = blockIdx.y, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int l16 = lane & 15, g = lane >> 4;
+  uint4 qb[2][kRD / 32];
+  float nl[2];
+  int vlim[2];
+#pragma unroll
+  for (int rt = 0; rt < 2; ++rt) {
+    const int row = 32 * wave + 16 * rt + l16;
+    const bool ok = row < m;
+    const u16* qr = q + ((size_t)u * m + row) * kRD;
+#pragma unroll
+    for (int ks = 0; ks < kRD / 32; ++ks)
+      qb[rt][ks] = ok ? *reinterpret_cast<const uint4*>(qr + ks * 32 + 8 * g) : make_uint4(0, 0, 0, 0);
+    nl[rt] = ok ? -lse2[(size_t)u * kRMP + row] : -__builtin_huge_valf();
+    // one past the last slot the row sees (the window is the last w slots)
+    vlim[rt] = causal ? min(c, c - w + row % w + 1) : c;
+  }
+  const int t0 = blockIdx.x * kXTiles;
+  for (int t = t0; t < min(t0 + kXTiles, ntc); ++t) {
+    const int tile0 = t * kRTK;
+    f32x4 st[2][2];
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+      const int key = min(tile0 + 16 * kt + l16, c - 1);
+      const u16* kr = k0 + ((size_t)u * c + key) * kRD;
+      uint4 kf[kRD / 32];
+#pragma unroll
+      for (int ks = 0; ks < kRD / 32; ++ks) kf[ks] = *reinterpret_cast<const uint4*>(kr + ks * 32 + 8 * g);
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt) {
+        st[kt][rt] = zero4();
+#pragma unroll
+        for (int ks = 0; ks < kRD / 32; ++ks)
+          st[kt][rt] = mfma_bf16(as_bf16x8(kf[ks]), as_bf16x8(qb[rt][ks]), st[kt][rt]);
+      }
     }
-    bits[i] = b;
+    float* xt = xs + ((size_t)u * ntc + t) * (kRXB / 4);
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+      bool fx[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int key = tile0 + 16 * kt + 4 * g + i;
+        fx[i] = key >= c || fixed[(size_t)u * c + min(key, c - 1)] != 0;
+      }
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt) {
+        f32x4 x;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int key = tile0 + 16 * kt + 4 * g + i;
+          x[i] = (!fx[i] && key < vlim[rt])
+                     ? __builtin_amdgcn_exp2f(fmaf(st[kt][rt][i], scale_log2, nl[rt]))
+                     : 0.f;
+        }
+        *reinterpret_cast<f32x4*>(xt + ((wave * 4 + 2 * kt + rt) * 64 + lane) * 4) = x;
+      }
+    }
   }
 }
 
@@ -599,15 +646,23 @@ bool key_ring_supported(const Plan& p) {
   return p.mp == kRMP && p.d == kRD && p.dtype == GRKV_BF16;
 }
 
-size_t key_fixbits_words(const Plan& p) { return (size_t)(p.c + kRTK - 1) / kRTK; }
+size_t key_x_bytes(const Plan& p) {
+  return (size_t)p.U * ((p.c + kRTK - 1) / kRTK) * kRXB;
+}
 
 hipError_t launch_key_prep(const Plan& p, const KeyArgs& a, hipStream_t s) {
   const size_t n4 = (size_t)p.U * p.c * p.d / 4;
   size_t blocks = (n4 + 255) / 256;
   if (blocks > 8192) blocks = 8192;
   if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(key_prep_kernel, dim3((unsigned)blocks), dim3(256), 0, s, a.vs, a.vh, a.vl,
-                     n4, a.fixed, a.fixbits, p.U, p.c, (int)key_fixbits_words(p));
+  hipLaunchKernelGGL(key_prep_kernel, dim3((unsigned)blocks), dim3(256), 0, s, a.vs, a.vh, a.vl, n4);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int ntc = (p.c + kRTK - 1) / kRTK;
+  hipLaunchKernelGGL(key_x_kernel, dim3((ntc + kXTiles - 1) / kXTiles, p.U), dim3(256), 0, s, a.q,
+                     a.k0, a.lse2, a.fixed, a.xs, p.m, p.w, p.c, ntc,
+                     p.opt.causal_window ? 1 : 0,
+                     (float)(1.4426950408889634 / sqrt((double)kRD)));
   return hipGetLastError();
 }
 
@@ -616,6 +671,7 @@ hipError_t launch_key_ring(const Plan& p, const KeyArgs& ka, bool final, int S, 
   RingArgs a;
   a.q = ka.q;
   a.k0 = ka.k0;
+  a.xs = ka.xs;
   a.vh = ka.vh;
   a.vl = ka.vl;
   a.lse2 = ka.lse2;
@@ -631,16 +687,17 @@ hipError_t launch_key_ring(const Plan& p, const KeyArgs& ka, bool final, int S, 
   a.m = p.m;
   a.w = p.w;
   a.c = p.c;
-  a.nw = (int)key_fixbits_words(p);
+  a.ntc = (p.c + kRTK - 1) / kRTK;
   a.S = S;
   a.chunk = chunk;
   a.causal = p.opt.causal_window ? 1 : 0;
   a.scale_log2 = (float)(1.4426950408889634 / sqrt((double)kRD));
   a.inv_sqrt_d = (float)(1.0 / sqrt((double)kRD));
+  if (chunk % kRTK != 0) return hipErrorInvalidValue;   // splits are whole tiles
   if (final)
-    hipLaunchKernelGGL(key_ring_kernel<true>, dim3(S, p.U), dim3(kRTh), 0, s, a, ka.fixbits);
+    hipLaunchKernelGGL(key_ring_kernel<true>, dim3(S, p.U), dim3(kRTh), 0, s, a);
   else
-    hipLaunchKernelGGL(key_ring_kernel<false>, dim3(S, p.U), dim3(kRTh), 0, s, a, ka.fixbits);
+    hipLaunchKernelGGL(key_ring_kernel<false>, dim3(S, p.U), dim3(kRTh), 0, s, a);
   return hipGetLastError();
 }
 
