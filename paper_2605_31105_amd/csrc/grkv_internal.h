@@ -247,7 +247,7 @@ bool key_ring_supported(const Plan& p);
 size_t key_x_bytes(const Plan& p);
 hipError_t launch_key_prep(const Plan& p, const KeyArgs& a, hipStream_t s);
 hipError_t launch_key_ring(const Plan& p, const KeyArgs& a, bool final, int S, int chunk,
-                           const float* dir, hipStream_t s);
+                           float* dir, bool fuse, hipStream_t s);
 hipError_t launch_to_f32(const uint16_t* src, float* dst, size_t n, hipStream_t s);
 
 // H2O accumulated-attention scores (bf16, d 64/128, G in {1, 2, 4, 8}): row

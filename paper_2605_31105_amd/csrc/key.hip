@@ -770,14 +770,19 @@ hipError_t launch_key_t(const Plan& p, const KeyPlan& kp, const KeyArgs& a, hipS
     for (int it = 0; it < a.max_iter; ++it) {
       const bool early = it < kKeyEarlyIters;
       const int S = early ? kp.S_full : kp.S4, chunk = early ? kp.chunk_full : kp.chunk4;
-      e = launch_key_ring(p, a, false, S, chunk, a.p, s);
+      // one split per unit: the CG update runs inside the pass
+      const bool fuse = S == 1;
+      e = launch_key_ring(p, a, false, S, chunk, a.p, fuse, s);
       if (e != hipSuccess) return e;
-      hipLaunchKernelGGL((key_cg_kernel<MP, D>), dim3(p.U), dim3(1024), 0, s, a.opart, a.hpart,
-                         S, a.Fm, a.alpha, a.r, a.p, a.sdot, a.cg, a.lam_k, a.tol, a.max_iter);
-      e = hipGetLastError();
-      if (e != hipSuccess) return e;
+      if (!fuse) {
+        hipLaunchKernelGGL((key_cg_kernel<MP, D>), dim3(p.U), dim3(1024), 0, s, a.opart,
+                           a.hpart, S, a.Fm, a.alpha, a.r, a.p, a.sdot, a.cg, a.lam_k, a.tol,
+                           a.max_iter);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+      }
     }
-    return launch_key_ring(p, a, true, kp.S_full, kp.chunk_full, a.alpha, s);
+    return launch_key_ring(p, a, true, kp.S_full, kp.chunk_full, a.alpha, false, s);
   }
   if constexpr (KF) {
     // a later alternating step: the right-hand side gains J_G (K_cur - K0)

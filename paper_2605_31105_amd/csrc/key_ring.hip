@@ -67,15 +67,21 @@ struct RingArgs {
   const float* lse2;   // [U][mp]
   const float* Fm;     // [U][mp][d]
   const float* W;      // [U][mp][mp]
-  const float* dir;    // [U][mp][d] direction p (kOp) or alpha (kFinal)
-  const float* sdot;   // [U][mp] rowdot(F, p) (kOp)
-  const double* cg;
+  float* dir;          // [U][mp][d] direction p (kOp) or alpha (kFinal)
+  float* sdot;         // [U][mp] rowdot(F, p) (kOp)
+  double* cg;          // [U][4] {r.r, r0.r0, iterations, state}
   float* opart;        // [U][S][mp][d]
   float* hpart;        // [U][S][mp]
   float* kstar;        // [U][c][d]
   float* cg_info;      // [U][4] or null
   int m, w, c, ntc, S, chunk, causal;   // ntc = ceil(c / 32)
   float scale_log2, inv_sqrt_d;
+  // kOp with one split per unit (fuse): the conjugate-gradient update of
+  // key_cg runs in the pass's epilogue, on alpha, r, p (= dir) and sdot
+  int fuse, max_iter;
+  float lam_k, tol;
+  float* alpha;        // [U][mp][d]
+  float* r;            // [U][mp][d]
 };
 
 __device__ __forceinline__ bf16x8 cat8(v4i16 a, v4i16 b) {
@@ -167,6 +173,14 @@ __global__ __launch_bounds__(kRTh) void key_ring_kernel(RingArgs a) {
       }
     }
   };
+
+  // consumers: out^T of their rows and the row sums of H (phase B)
+  f32x4 oacc[FINAL ? 1 : 2][kRD / 16];
+#pragma unroll
+  for (int rt = 0; rt < (FINAL ? 1 : 2); ++rt)
+#pragma unroll
+    for (int dt = 0; dt < kRD / 16; ++dt) oacc[rt][dt] = zero4();
+  float hs[2] = {0.f, 0.f};
 
   if (producer) {
     // ---------------------------------------------------------------- phase A
@@ -290,8 +304,7 @@ __global__ __launch_bounds__(kRTh) void key_ring_kernel(RingArgs a) {
     if (k + 2 < ntiles) interval(k + 2, stg3, stg1, dbuf1);
     // the clamped loads past the end land before the block's LDS is released
     wait_vmcnt<0>();
-    return;
-  }
+  } else {
 
   // ------------------------------------------------------------------ phase B
   // kOp: W rows (B operand of A^T = D^T W), columns 32kb + 8g .. +7
@@ -344,13 +357,6 @@ __global__ __launch_bounds__(kRTh) void key_ring_kernel(RingArgs a) {
       dro[kt][h] = (uint32_t)(R2 * 64 + 8 * ((4 * kt + qq) ^ dswz(R2)));
     }
   const uint32_t xro = (uint32_t)(rw * 4096 + lane * 16);
-
-  f32x4 oacc[FINAL ? 1 : 2][kRD / 16];
-#pragma unroll
-  for (int rt = 0; rt < (FINAL ? 1 : 2); ++rt)
-#pragma unroll
-    for (int dt = 0; dt < kRD / 16; ++dt) oacc[rt][dt] = zero4();
-  float hs[2] = {0.f, 0.f};
 
   // D^T fragments of row block kb (keys 16kt + l16, rows 32kb + 8g .. +7)
   auto dfrag = [&](const char* dr, int kt, int kb, bf16x8& dh, bf16x8& dl) {
@@ -531,21 +537,130 @@ __global__ __launch_bounds__(kRTh) void key_ring_kernel(RingArgs a) {
     k0load(last);
     phase_b(last, sb, dr, true);
   }
+  }   // roles
 
   if constexpr (!FINAL) {
-    // lane holds out^T [16dt + 4g + i][row 16rt + l16]
+    // row sums of H over the whole split (the lanes of a row hold parts)
+    float hrow[2];
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) {
-      const int row = row0 + 16 * rt + l16;
-      float* op = a.opart + (((size_t)u * a.S + s) * kRMP + row) * kRD;
-#pragma unroll
-      for (int dt = 0; dt < kRD / 16; ++dt)
-        *reinterpret_cast<float4*>(op + 16 * dt + 4 * g) =
-            make_float4(oacc[rt][dt][0], oacc[rt][dt][1], oacc[rt][dt][2], oacc[rt][dt][3]);
       float h = hs[rt];
       h += __shfl_xor(h, 16);
       h += __shfl_xor(h, 32);
-      if (g == 0) a.hpart[((size_t)u * a.S + s) * kRMP + row] = h;
+      hrow[rt] = h;
+    }
+    if (!a.fuse) {
+      if (!producer) {
+        // lane holds out^T [16dt + 4g + i][row 16rt + l16]
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt) {
+          const int row = row0 + 16 * rt + l16;
+          float* op = a.opart + (((size_t)u * a.S + s) * kRMP + row) * kRD;
+#pragma unroll
+          for (int dt = 0; dt < kRD / 16; ++dt)
+            *reinterpret_cast<float4*>(op + 16 * dt + 4 * g) =
+                make_float4(oacc[rt][dt][0], oacc[rt][dt][1], oacc[rt][dt][2], oacc[rt][dt][3]);
+          if (g == 0) a.hpart[((size_t)u * a.S + s) * kRMP + row] = hrow[rt];
+        }
+      }
+      return;
+    }
+    // One split holds the whole unit: the conjugate-gradient update of
+    // key_cg on the consumers' rows, with the block sums through LDS (the
+    // ring is no longer read).  Ap = out + lambda_k p - (H 1) o F;
+    // alpha += a p, r -= a Ap with a = r.r / p.Ap; p = r + (r'.r' / r.r) p and
+    // s = rowdot(F, p) for the next pass.  Sums in fp64.
+    double* red = reinterpret_cast<double*>(dbuf0);
+    auto block_sum8 = [&](double v, int slot) {
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+      if (lane == 0) red[slot * kRW + wave] = v;
+      lds_barrier();
+      double t = 0.0;
+#pragma unroll
+      for (int k = 0; k < kRW; ++k) t += red[slot * kRW + k];
+      return t;
+    };
+    lds_barrier();   // every wave is past its last ring access
+    double part = 0.0;
+    if (!producer) {
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt) {
+        const size_t ro = ((size_t)u * kRMP + row0 + 16 * rt + l16) * kRD + 4 * g;
+#pragma unroll
+        for (int dt = 0; dt < kRD / 16; ++dt) {
+          const f32x4 pv = *reinterpret_cast<const f32x4*>(a.dir + ro + 16 * dt);
+          const f32x4 fv = *reinterpret_cast<const f32x4*>(a.Fm + ro + 16 * dt);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const float ap = oacc[rt][dt][i] + a.lam_k * pv[i] - hrow[rt] * fv[i];
+            oacc[rt][dt][i] = ap;
+            part += (double)(pv[i] * ap);
+          }
+        }
+      }
+    }
+    const double pap = block_sum8(part, 0);
+    const double rr = a.cg[u * 4 + 0], rr0 = a.cg[u * 4 + 1];
+    const int it = (int)a.cg[u * 4 + 2] + 1;
+    if (!(pap > 0)) {
+      if (tid == 0) a.cg[u * 4 + 3] = kKeyBreakdown;
+      return;
+    }
+    const float step = (float)(rr / pap);
+    part = 0.0;
+    if (!producer) {
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt) {
+        const size_t ro = ((size_t)u * kRMP + row0 + 16 * rt + l16) * kRD + 4 * g;
+#pragma unroll
+        for (int dt = 0; dt < kRD / 16; ++dt) {
+          const f32x4 pv = *reinterpret_cast<const f32x4*>(a.dir + ro + 16 * dt);
+          f32x4 al = *reinterpret_cast<const f32x4*>(a.alpha + ro + 16 * dt);
+          f32x4 rv = *reinterpret_cast<const f32x4*>(a.r + ro + 16 * dt);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            al[i] += step * pv[i];
+            rv[i] -= step * oacc[rt][dt][i];
+            part += (double)(rv[i] * rv[i]);
+          }
+          *reinterpret_cast<f32x4*>(a.alpha + ro + 16 * dt) = al;
+          *reinterpret_cast<f32x4*>(a.r + ro + 16 * dt) = rv;
+          oacc[rt][dt] = rv;
+        }
+      }
+    }
+    const double rn = block_sum8(part, 1);
+    int st = kKeyRunning;
+    if (sqrt(rn) <= (double)a.tol * sqrt(rr0)) st = kKeyConverged;
+    else if (it >= a.max_iter) st = kKeyMaxIter;
+    if (st == kKeyRunning && !producer) {
+      const float beta = (float)(rn / rr);
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt) {
+        const int row = row0 + 16 * rt + l16;
+        const size_t ro = ((size_t)u * kRMP + row) * kRD + 4 * g;
+        float sdr = 0.f;
+#pragma unroll
+        for (int dt = 0; dt < kRD / 16; ++dt) {
+          f32x4 pv = *reinterpret_cast<const f32x4*>(a.dir + ro + 16 * dt);
+          const f32x4 fv = *reinterpret_cast<const f32x4*>(a.Fm + ro + 16 * dt);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            pv[i] = oacc[rt][dt][i] + beta * pv[i];
+            sdr += fv[i] * pv[i];
+          }
+          *reinterpret_cast<f32x4*>(a.dir + ro + 16 * dt) = pv;
+        }
+        sdr += __shfl_xor(sdr, 16);
+        sdr += __shfl_xor(sdr, 32);
+        if (g == 0) a.sdot[(size_t)u * kRMP + row] = sdr;
+      }
+    }
+    if (tid == 0) {
+      a.cg[u * 4 + 0] = rn;
+      a.cg[u * 4 + 2] = it;
+      a.cg[u * 4 + 3] = st;
     }
   }
 }
@@ -667,7 +782,7 @@ hipError_t launch_key_prep(const Plan& p, const KeyArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_key_ring(const Plan& p, const KeyArgs& ka, bool final, int S, int chunk,
-                           const float* dir, hipStream_t s) {
+                           float* dir, bool fuse, hipStream_t s) {
   RingArgs a;
   a.q = ka.q;
   a.k0 = ka.k0;
@@ -693,6 +808,12 @@ hipError_t launch_key_ring(const Plan& p, const KeyArgs& ka, bool final, int S, 
   a.causal = p.opt.causal_window ? 1 : 0;
   a.scale_log2 = (float)(1.4426950408889634 / sqrt((double)kRD));
   a.inv_sqrt_d = (float)(1.0 / sqrt((double)kRD));
+  a.fuse = fuse && !final && S == 1 ? 1 : 0;
+  a.max_iter = ka.max_iter;
+  a.lam_k = ka.lam_k;
+  a.tol = ka.tol;
+  a.alpha = ka.alpha;
+  a.r = ka.r;
   if (chunk % kRTK != 0) return hipErrorInvalidValue;   // splits are whole tiles
   if (final)
     hipLaunchKernelGGL(key_ring_kernel<true>, dim3(S, p.U), dim3(kRTh), 0, s, a);
