@@ -375,10 +375,12 @@ def key_step(args, cfg, G, hip, stream, qd, Kd, Vd, host=None):
         "cg_tol": 1e-5,
         "iteration_ms": it_ms,
         "ms_per_call_steps2": steps2_ms,
-        "roofline": {"bound": "mfma", "kernel": "key_pass + key_cg (one CG iteration)",
+        "roofline": {"bound": "mfma",
+                     "kernel": "key_ring_kernel operator pass with the CG update (one iteration)",
                      "achieved": tflops, "peak": 2500.0, "unit": "TFLOP/s",
                      "frac": tflops / 2500.0, "traffic": None,
-                     "note": "fp32-accurate products as three bf16 MFMAs each"},
+                     "note": "fp32-accurate products as three bf16 MFMAs each; X streamed from "
+                             "HBM (written once per key step by key_x)"},
         "cpu_baseline": cpu,
     }
 
