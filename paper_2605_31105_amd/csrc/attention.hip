@@ -401,41 +401,63 @@ __global__ __launch_bounds__(WAVES * 64) void prob_pass_kernel(PassK a) {
 // reduced in split order, so the result does not depend on the batching.
 constexpr int kCombineBatch = 16;
 
-__global__ void lse_combine_kernel(const float* pmax, const double* psum, int S, int mp,
-                                   int total, double* lse, float* lse_log2) {
-  int id = blockIdx.x * blockDim.x + threadIdx.x;
-  if (id >= total) return;
-  int u = id / mp, row = id % mp;
+// Log-sum-exp of split partials (max, sum of 2^(t - max)): one thread per
+// (row, split class s mod kLseLanes), which sums its splits against a running
+// maximum with all loads of a batch in flight; the classes of a row sit in
+// adjacent lanes and merge by shuffles.  Fixed order, so deterministic.
+constexpr int kLseLanes = 8;
+
+__device__ __forceinline__ double lse_rescale(double sum, float from, float to) {
+  return from == -INFINITY ? 0.0 : sum * exp2((double)from - (double)to);
+}
+
+__global__ __launch_bounds__(256) void lse_combine_kernel(const float* pmax, const double* psum,
+                                                          int S, int mp, int total, double* lse,
+                                                          float* lse_log2) {
+  const int gid = blockIdx.x * blockDim.x + threadIdx.x;
+  const int id = gid / kLseLanes, c = gid % kLseLanes;
+  const bool live = id < total;
+  const int u = live ? id / mp : 0, row = live ? id % mp : 0;
   const size_t base = (size_t)u * S * mp + row;
   float M = -INFINITY;
-  for (int s0 = 0; s0 < S; s0 += kCombineBatch) {
-    float ms[kCombineBatch];
+  double sum = 0.0;
+  if (live) {
+    for (int s0 = c; s0 < S; s0 += kLseLanes * kCombineBatch) {
+      float ms[kCombineBatch];
+      double ps[kCombineBatch];
 #pragma unroll
-    for (int k = 0; k < kCombineBatch; ++k)
-      ms[k] = s0 + k < S ? pmax[base + (size_t)(s0 + k) * mp] : -INFINITY;
+      for (int k = 0; k < kCombineBatch; ++k) {
+        const int sp = s0 + k * kLseLanes;
+        const bool in = sp < S;
+        ms[k] = in ? pmax[base + (size_t)sp * mp] : -INFINITY;
+        ps[k] = in ? psum[base + (size_t)sp * mp] : 0.0;
+      }
+      float bm = M;
 #pragma unroll
-    for (int k = 0; k < kCombineBatch; ++k) M = fmaxf(M, ms[k]);
+      for (int k = 0; k < kCombineBatch; ++k) bm = fmaxf(bm, ms[k]);
+      if (bm == -INFINITY) continue;
+      sum = lse_rescale(sum, M, bm);
+#pragma unroll
+      for (int k = 0; k < kCombineBatch; ++k)
+        if (ms[k] != -INFINITY) sum += ps[k] * exp2((double)ms[k] - (double)bm);
+      M = bm;
+    }
   }
+#pragma unroll
+  for (int off = 1; off < kLseLanes; off <<= 1) {
+    const float Mo = __shfl_xor(M, off);
+    const double so = __shfl_xor(sum, off);
+    const float Mn = fmaxf(M, Mo);
+    sum = lse_rescale(sum, M, Mn) + lse_rescale(so, Mo, Mn);
+    M = Mn;
+  }
+  if (!live || c != 0) return;
   if (M == -INFINITY) {  // padding row: no visible key
     lse[id] = -INFINITY;
     lse_log2[id] = 0.f;
     return;
   }
-  double sum = 0.0;
-  for (int s0 = 0; s0 < S; s0 += kCombineBatch) {
-    float ms[kCombineBatch];
-    double ps[kCombineBatch];
-#pragma unroll
-    for (int k = 0; k < kCombineBatch; ++k) {
-      const bool in = s0 + k < S;
-      ms[k] = in ? pmax[base + (size_t)(s0 + k) * mp] : -INFINITY;
-      ps[k] = in ? psum[base + (size_t)(s0 + k) * mp] : 0.0;
-    }
-#pragma unroll
-    for (int k = 0; k < kCombineBatch; ++k)
-      if (ms[k] != -INFINITY) sum += ps[k] * exp2((double)ms[k] - (double)M);
-  }
-  double l2 = (double)M + log2(sum);
+  const double l2 = (double)M + log2(sum);
   lse[id] = l2 * 0.69314718055994530942;
   lse_log2[id] = (float)l2;
 }
@@ -543,8 +565,9 @@ hipError_t launch_prob_pass(const Plan& p, const AttnPass& a, hipStream_t s) {
 
 hipError_t launch_lse_combine(const Plan& p, const float* pmax, const double* psum, int S,
                               double* lse, float* lse_log2, hipStream_t s) {
-  int total = p.U * p.mp;
-  hipLaunchKernelGGL(lse_combine_kernel, dim3((total + 255) / 256), dim3(256), 0, s, pmax, psum,
+  const int total = p.U * p.mp;
+  const int threads = total * kLseLanes;
+  hipLaunchKernelGGL(lse_combine_kernel, dim3((threads + 255) / 256), dim3(256), 0, s, pmax, psum,
                      S, p.mp, total, lse, lse_log2);
   return hipGetLastError();
 }

@@ -529,6 +529,11 @@ constexpr int kSmallThreads = 1024;
 constexpr int kSmallPer = 32;          // pooled scores per thread: prefixes up to 32768
 constexpr uint32_t kCandCap = 4096;    // candidates finished by one wave (64 per lane)
 
+// A value known to be the same in every lane, kept in a scalar register.
+__device__ __forceinline__ uint32_t uniform_u(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_readfirstlane((int)v);
+}
+
 // Sum over the 64 lanes of a wave, in every lane (DPP within 16-lane rows,
 // then the four row totals).
 __device__ __forceinline__ uint32_t wave_sum(uint32_t v) {
@@ -550,7 +555,52 @@ __device__ __forceinline__ uint32_t block_sum_small(uint32_t v, uint32_t (*part)
   uint32_t tot = 0;
 #pragma unroll
   for (int k = 0; k < kSmallThreads / 64; ++k) tot += part[parity][k];
-  return tot;
+  return uniform_u(tot);
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave: DPP shifts within each
+// 16-lane row, then the totals of the rows below, read from lanes 15, 31, 47.
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t v) {
+  int x = (int)v;
+  x += __builtin_amdgcn_update_dpp(0, x, 0x111, 0xF, 0xF, false);   // row_shr:1
+  x += __builtin_amdgcn_update_dpp(0, x, 0x112, 0xF, 0xF, false);   // row_shr:2
+  x += __builtin_amdgcn_update_dpp(0, x, 0x114, 0xF, 0xF, false);   // row_shr:4
+  x += __builtin_amdgcn_update_dpp(0, x, 0x118, 0xF, 0xF, false);   // row_shr:8
+  const int row = (threadIdx.x & 63) >> 4;
+  const int r0 = __builtin_amdgcn_readlane(x, 15), r1 = __builtin_amdgcn_readlane(x, 31),
+            r2 = __builtin_amdgcn_readlane(x, 47);
+  x += (row >= 1 ? r0 : 0) + (row >= 2 ? r1 : 0) + (row >= 3 ? r2 : 0);
+  return (uint32_t)x;
+}
+
+// Exclusive prefix sums over the block of two values per thread, and their
+// block totals, with one barrier: `scr` holds 2 x 32 words and alternates by
+// `parity` (shared with block_sum_small's), so consecutive calls need no
+// second barrier.
+__device__ __forceinline__ void block_scan2_small(uint32_t v0, uint32_t v1,
+                                                  uint32_t (*scr)[32], int parity,
+                                                  uint32_t& e0, uint32_t& e1, uint32_t& t0,
+                                                  uint32_t& t1) {
+  const uint32_t i0 = wave_incl_scan(v0), i1 = wave_incl_scan(v1);
+  const int wave = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 63) {
+    scr[parity][wave] = i0;
+    scr[parity][16 + wave] = i1;
+  }
+  __syncthreads();
+  uint32_t b0 = 0, b1 = 0, a0 = 0, a1 = 0;
+#pragma unroll
+  for (int k = 0; k < kSmallThreads / 64; ++k) {
+    const uint32_t s0 = scr[parity][k], s1 = scr[parity][16 + k];
+    b0 += k < wave ? s0 : 0u;
+    b1 += k < wave ? s1 : 0u;
+    a0 += s0;
+    a1 += s1;
+  }
+  e0 = b0 + i0 - v0;
+  e1 = b1 + i1 - v1;
+  t0 = uniform_u(a0);
+  t1 = uniform_u(a1);
 }
 
 // State of one k-th-largest search over the keys (fp32 bit patterns of
@@ -560,112 +610,51 @@ struct Bracket {
   uint32_t lo, hi, clo, chi;
 };
 
-// The positions taken at a threshold T, the k-th largest fp32 pooled score,
-// as a mask over the PER keys of this thread (key q <-> position j0 + q).
-//
-// The fp32 pooled sums round away differences that decide the order: two
-// overlapping windows share all but their edge terms, and when a large score
-// sits in both, their fp32 sums are equal while the edge terms differ.  So
-// the candidates whose fp32 sum lies within kBandUlps units in the last place
-// of T are ranked again by their sum recomputed in fp64 from the fp32 column
-// sums (in which the shared terms cancel exactly), then by position; the
-// keys above the band are taken, and the band fills the remaining places.
-// A band of more than kBandCap keys (scores equal over long runs) keeps the
-// fp32 order with ties to the lower position.  `work` is LDS of at least
-// kBandCap * (8 + 4 + 4) bytes.
-template <int PER>
-__device__ uint32_t refine_boundary(const uint32_t (&key)[PER], uint32_t T, uint32_t k,
-                                    const float* s, int j0, int P, int h, float* work,
-                                    uint32_t (*part)[16], uint32_t* scan_scratch, uint32_t* sh) {
-  const uint32_t lo = T > kBandUlps ? T - kBandUlps : 0u;
-  const uint32_t hi = T < 0x7F800000u - kBandUlps ? T + kBandUlps : 0x7F800000u;
-  uint32_t nabove = 0, nband = 0;
-#pragma unroll
-  for (int q = 0; q < PER; ++q) {
-    nabove += key[q] > hi;
-    nband += key[q] >= lo && key[q] <= hi;
-  }
-  // both counts in one scan (each total is at most PER * blockDim <= 32768)
-  uint32_t tot;
-  const uint32_t boff = block_exclusive_scan(nabove | (nband << 16), scan_scratch, &tot) >> 16;
-  const uint32_t tot_above = tot & 0xFFFFu, tot_band = tot >> 16;
-  const uint32_t need = k - tot_above;   // 1 <= need <= tot_band
-  uint32_t m = 0;
-  if (tot_band > kBandCap) {
-    // fp32 order, ties (key == T) to the lower position
-    uint32_t gt = 0, eq = 0;
-#pragma unroll
-    for (int q = 0; q < PER; ++q) {
-      gt += key[q] > T;
-      eq += key[q] == T;
-    }
-    uint32_t t2;
-    uint32_t e = block_exclusive_scan(gt | (eq << 16), scan_scratch, &t2) >> 16;
-    const uint32_t krem = k - (t2 & 0xFFFFu);
-#pragma unroll
-    for (int q = 0; q < PER; ++q) {
-      const bool take = key[q] > T || (key[q] == T && e < krem);
-      e += key[q] == T;
-      m |= (uint32_t)take << q;
-    }
-    return m;
-  }
-  double* v64 = reinterpret_cast<double*>(work);                       // [kBandCap]
-  int32_t* bpos = reinterpret_cast<int32_t*>(v64 + kBandCap);          // [kBandCap]
-  uint32_t* btake = reinterpret_cast<uint32_t*>(bpos + kBandCap);      // [kBandCap]
-  {
-    uint32_t o = boff;
-#pragma unroll
-    for (int q = 0; q < PER; ++q)
-      if (key[q] >= lo && key[q] <= hi) bpos[o++] = j0 + q;
-  }
-  __syncthreads();
-  for (uint32_t e = threadIdx.x; e < tot_band; e += blockDim.x) {
-    const int j = bpos[e];
-    const int t0 = j - h < 0 ? 0 : j - h, t1 = j + h > P - 1 ? P - 1 : j + h;
-    double acc = 0.0;
-    for (int t = t0; t <= t1; ++t) acc += (double)s[t];   // left to right
-    v64[e] = acc;
-  }
-  __syncthreads();
-  for (uint32_t e = threadIdx.x; e < tot_band; e += blockDim.x) {
-    const double v = v64[e];
-    const int j = bpos[e];
-    uint32_t rank = 0;
-    for (uint32_t f = 0; f < tot_band; ++f) {
-      const double w = v64[f];
-      rank += w > v || (w == v && bpos[f] < j);
-    }
-    btake[e] = rank < need;
-  }
-  __syncthreads();
-  {
-    uint32_t o = boff;
-#pragma unroll
-    for (int q = 0; q < PER; ++q) {
-      bool take = key[q] > hi;
-      if (key[q] >= lo && key[q] <= hi) take = btake[o++] != 0;
-      m |= (uint32_t)take << q;
-    }
-  }
-  __syncthreads();   // work is reused by the next call
-  return m;
-}
+// Boundary band of one threshold in the small kernel: positions, fp64 sums
+// and take flags of its keys (unordered), kBandCap * 16 bytes of LDS.
+struct SmallBand {
+  double* v64;
+  int32_t* pos;
+  uint32_t* take;
+  __device__ __forceinline__ explicit SmallBand(float* base)
+      : v64(reinterpret_cast<double*>(base)),
+        pos(reinterpret_cast<int32_t*>(v64 + kBandCap)),
+        take(reinterpret_cast<uint32_t*>(pos + kBandCap)) {}
+};
 
-// Same selection for prefixes of at most 32768 tokens, with each thread
-// keeping 32 consecutive pooled scores in registers.  The (c-w)-th largest
-// score T0 is found by bisection on the bit patterns: block-wide counts of
-// "score >= mid" from the [min, max] bracket until at most kCandCap keys
-// remain inside it; those candidates go to LDS and radix rounds (256 bins of
-// the bit pattern's offset in the bracket) finish.  The floor(beta*c)-th
-// largest T1 lies among the keys >= T0 (about c-w of them), so it starts
-// from the candidates directly.
+// Selection for prefixes of at most 32768 tokens, each thread keeping 32
+// consecutive pooled scores in registers.  Both thresholds (the (c-w)-th
+// largest score T0 and the floor(beta*c)-th largest T1) are searched
+// together, so every block-wide step serves both:
+//  * bisection on the bit patterns from the [min, max] bracket, the two
+//    counts "score >= mid" packed in one word per reduction, until at most
+//    kCandCap keys remain inside each bracket;
+//  * those candidates go to LDS, and radix rounds (256 bins of the bit
+//    pattern's offset in the bracket, one histogram per search) finish;
+//  * the fp32 pooled sums round away differences that decide the order (two
+//    overlapping windows share all but their edge terms), so the keys within
+//    kBandUlps units in the last place of each threshold are ranked again by
+//    their sums recomputed in fp64 from the fp32 column sums, then by
+//    position; the keys above the band are taken and the band fills the
+//    remaining places.  A band of more than kBandCap keys (scores equal over
+//    long runs) keeps the fp32 order with ties to the lower position.
+// Per-key work is written without branches (bounds by clamped addresses and
+// selects, compaction through per-lane spare slots), since a branch per key
+// costs far more than the key's arithmetic.  H = (pool width - 1) / 2 is a
+// template argument, so the pooling and the band sums unroll.
+constexpr int kSmallWords = kSmallThreads * kSmallPer + kSmallThreads * kSmallPer / 64;
+constexpr int kSpare = 2 * kCandCap;          // 64 per-lane spare slots after the candidates
+constexpr int kMaskWords = kSpare + 64;       // 2 x 1024 per-thread take masks of the bands
+
+template <int H>
 __global__ __launch_bounds__(kSmallThreads) void select_small_kernel(SelK a) {
-  __shared__ float sl[kSmallThreads * kSmallPer + kSmallThreads * kSmallPer / 64];
+  __shared__ __attribute__((aligned(16))) float sl[kSmallWords];
   __shared__ uint32_t part[2][16];
-  __shared__ uint32_t scan_scratch[16];
-  __shared__ uint32_t sh[8];
-  __shared__ uint32_t hist[256];
+  __shared__ uint32_t scr[2][32];
+  __shared__ uint32_t sh[2][4];
+  __shared__ uint32_t hist[2][256];
+  static_assert(kMaskWords + 2 * kSmallThreads <= kSmallWords, "LDS areas");
+  static_assert(2 * kBandCap * 4 <= kSpare, "band areas inside the candidate area");
   constexpr int PER = kSmallPer;
   const int u = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -676,60 +665,56 @@ __global__ __launch_bounds__(kSmallThreads) void select_small_kernel(SelK a) {
   int32_t* idx = a.idx + us.base;
   uint8_t* fixed = a.fixed + us.base;
   const int j0 = tid * PER;
+  uint32_t* slu = reinterpret_cast<uint32_t*>(sl);
+  uint32_t* mw = slu + kMaskWords;   // [2][kSmallThreads]
 
+  if (P > 0) {
   // Scores of the whole prefix into LDS (coalesced), one pad word per 64
   // entries so that the lanes of a wave, each reading its own contiguous
   // run, fall on distinct banks.  Each thread then pools its 32 positions
-  // (plus 8 on either side) in registers, summing s[j-h..j+h] left to right.
+  // (plus H on either side) in registers, summing s[j-H..j+H] left to right.
   // Positions past the prefix get key 0: they rank after every real position
   // with an equal score and are never taken while real positions are left.
   {
-    // all PER loads of a thread in flight at once
     float ld[PER];
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
       const int t = tid + k * kSmallThreads;
-      ld[k] = t < P ? s[t] : 0.f;
+      ld[k] = s[min(t, P - 1)];
     }
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
       const int t = tid + k * kSmallThreads;
-      sl[t + (t >> 6)] = ld[k];
+      sl[t + (t >> 6)] = t < P ? ld[k] : 0.f;
     }
   }
   __syncthreads();
   uint32_t key[PER];
   uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
   {
-    float v[PER + 16];
+    float v[PER + 2 * H];
 #pragma unroll
-    for (int q = 0; q < PER + 16; ++q) {
-      const int t = j0 - 8 + q;
-      v[q] = (t >= 0 && t < P) ? sl[t + (t >> 6)] : 0.f;
+    for (int q = 0; q < PER + 2 * H; ++q) {
+      const int t = j0 - H + q;
+      const int tc = min(max(t, 0), kSmallThreads * PER - 1);
+      const float x = sl[tc + (tc >> 6)];
+      v[q] = t >= 0 ? x : 0.f;   // past the prefix, sl holds zeros
     }
-    const int h = a.h;
 #pragma unroll
     for (int q = 0; q < PER; ++q) {
       const int j = j0 + q;
       float acc = 0.f;
 #pragma unroll
-      for (int t = -8; t <= 8; ++t)   // offsets -h..h in increasing order
-        if (t >= -h && t <= h) acc += v[q + 8 + t];
+      for (int t = 0; t <= 2 * H; ++t)   // offsets -H..H in increasing order
+        acc += v[q + t];
       key[q] = j < P ? __float_as_uint(acc) : 0u;
-      if (j < P) {
-        kmin = min(kmin, key[q]);
-        kmax = max(kmax, key[q]);
-      }
+      kmin = min(kmin, j < P ? key[q] : 0xFFFFFFFFu);
+      kmax = max(kmax, key[q]);
     }
   }
-  // the pooled scores (an intermediate the caller may inspect), coalesced
-  __syncthreads();
-#pragma unroll
-  for (int q = 0; q < PER; ++q) sl[j0 + q + ((j0 + q) >> 6)] = __uint_as_float(key[q]);
-  __syncthreads();
-  for (int t = tid; t < P; t += kSmallThreads) pg[t] = sl[t + (t >> 6)];
 
-  // key range of the real positions (block min and max)
+  // key range of the real positions (block min and max); the barrier also
+  // ends the pooling reads of sl, which is reused from here on
   {
     uint32_t mn = kmin, mx = kmax;
 #pragma unroll
@@ -749,125 +734,284 @@ __global__ __launch_bounds__(kSmallThreads) void select_small_kernel(SelK a) {
       kmin = min(kmin, part[0][k]);
       kmax = max(kmax, part[1][k]);
     }
+    mw[tid] = 0u;
+    mw[kSmallThreads + tid] = 0u;
     __syncthreads();   // part is reused below
   }
-  kmax = min(kmax, 0x7F800000u);   // +inf at most (no NaN scores)
-  uint32_t* cand = reinterpret_cast<uint32_t*>(sl);   // [kCandCap], reuses the staging area
+  kmin = uniform_u(kmin);
+  kmax = uniform_u(min(kmax, 0x7F800000u));   // +inf at most (no NaN scores)
   int parity = 0;
 
-  // k-th largest key from bracket b: block rounds while more than kCandCap
-  // keys lie in [lo, hi), then the candidates into LDS and radix rounds.
-  // Returns T with b.lo = T, b.hi = T + 1 (so b.chi = count(> T) and
-  // b.clo = count(>= T)).
-  auto kth = [&](uint32_t k, Bracket b) -> Bracket {
-#pragma unroll 1
-    for (int it = 0; it < 33 && b.hi - b.lo > 1 && b.clo - b.chi > kCandCap; ++it) {
-      const uint32_t mid = b.lo + (b.hi - b.lo) / 2;
-      uint32_t n = 0;
-#pragma unroll
-      for (int q = 0; q < PER; ++q) n += key[q] >= mid;
-      const uint32_t c = block_sum_small(n, part, parity);
-      parity ^= 1;
-      if (c >= k) { b.lo = mid; b.clo = c; }
-      else { b.hi = mid; b.chi = c; }
-    }
-    if (b.hi - b.lo <= 1) return b;
-    uint32_t n = 0;
-#pragma unroll
-    for (int q = 0; q < PER; ++q) n += key[q] >= b.lo && key[q] < b.hi;
-    uint32_t tot;
-    uint32_t o = block_exclusive_scan(n, scan_scratch, &tot);
-#pragma unroll
-    for (int q = 0; q < PER; ++q)
-      if (key[q] >= b.lo && key[q] < b.hi) {
-        if (o < kCandCap) cand[o] = key[q];
-        ++o;
-      }
-    __syncthreads();
-    // Radix rounds on the candidates: 256 bins of (x - lo) >> shift cover
-    // [lo, hi); the bin holding the k-th largest becomes the new bracket.  A
-    // 32-bit range takes at most four rounds.
-    const uint32_t L = min(b.clo - b.chi, kCandCap);
-#pragma unroll 1
-    for (int it = 0; it < 5 && b.hi - b.lo > 1; ++it) {
-      const uint32_t width = b.hi - b.lo;
-      const int bits = 32 - __builtin_clz(width - 1);   // width - 1 < 2^bits
-      const int shift = bits > 8 ? bits - 8 : 0;
-      if (tid < 256) hist[tid] = 0u;
-      __syncthreads();
-      for (uint32_t e = tid; e < L; e += kSmallThreads) {
-        const uint32_t x = cand[e];
-        if (x >= b.lo && x < b.hi) atomicAdd(&hist[(x - b.lo) >> shift], 1u);
-      }
-      __syncthreads();
-      if (wave == 0) {
-        // suffix sums over the bins: lane l holds bins 4l .. 4l+3
-        uint32_t h4[4], suf = 0;
-#pragma unroll
-        for (int i = 3; i >= 0; --i) {
-          h4[i] = hist[4 * lane + i];
-          suf += h4[i];
-        }
-        // inclusive suffix scan across lanes (lanes above l)
-        uint32_t incl = suf;
-#pragma unroll
-        for (int off = 1; off < 64; off <<= 1) {
-          const uint32_t o = (uint32_t)__shfl_down((int)incl, off);
-          if (lane + off < 64) incl += o;
-        }
-        // count(>= start of bin 4l + i) = chi + (bins above) ; the largest bin
-        // whose count reaches k holds the k-th largest
-        uint32_t above = b.chi + incl - suf;   // keys in bins > 4l+3, plus those >= hi
-        int best = -1;
-        uint32_t bc = 0, bh = 0;
-#pragma unroll
-        for (int i = 3; i >= 0; --i) {
-          const uint32_t c = above + h4[i];
-          if (best < 0 && c >= k) { best = 4 * lane + i; bc = c; bh = above; }
-          above = c;
-        }
-        // the highest lane with a hit owns the answer
-        const uint64_t hit = __ballot(best >= 0);
-        const int owner = 63 - __builtin_clzll(hit);
-        if (lane == owner) {
-          const uint32_t nlo = b.lo + ((uint32_t)best << shift);
-          const uint64_t nhi = (uint64_t)b.lo + ((uint64_t)(best + 1) << shift);
-          sh[0] = nlo;
-          sh[1] = nhi < b.hi ? (uint32_t)nhi : b.hi;
-          sh[2] = bc;
-          sh[3] = bh;
-        }
-      }
-      __syncthreads();
-      b.lo = sh[0]; b.hi = sh[1]; b.clo = sh[2]; b.chi = sh[3];
-      __syncthreads();   // hist and sh are rewritten by the next round
-    }
-    return b;
-  };
-
-  const uint32_t k0 = (uint32_t)us.s_sel, k1 = (uint32_t)us.n_top;
-  const bool any0 = k0 > 0, any1 = k1 > 0;
+  const uint32_t kk[2] = {(uint32_t)us.s_sel, (uint32_t)us.n_top};
+  const bool on[2] = {kk[0] > 0, kk[1] > 0};
   // count(>= kmin) = P (the padding keys, 0, count only when kmin is 0)
   const uint32_t all = kmin > 0 ? (uint32_t)P : (uint32_t)(kSmallThreads * PER);
-  Bracket b0 = {kmin, kmax + 1, all, 0u};
-  if (any0) b0 = kth(k0, b0);
-  // the n_top-th largest is at least T0 (n_top <= s_sel)
-  Bracket b1 = any0 ? Bracket{b0.lo, kmax + 1, b0.clo, 0u} : Bracket{kmin, kmax + 1, all, 0u};
-  if (any1) b1 = kth(k1, b1);
-  const uint32_t T0 = b0.lo, T1 = b1.lo;
-  uint32_t selm = any0 ? refine_boundary(key, T0, k0, s, j0, P, a.h, sl, part, scan_scratch, sh) : 0u;
-  uint32_t topm = any1 ? refine_boundary(key, T1, k1, s, j0, P, a.h, sl, part, scan_scratch, sh) : 0u;
-  uint32_t tot;
-  uint32_t off = block_exclusive_scan(__builtin_popcount(selm), scan_scratch, &tot);
-  // the selected positions in increasing order
-  while (selm) {
-    const int q = __builtin_ctz(selm);
-    const int j = j0 + q;
-    idx[off] = j;
-    fixed[off] = (j < a.n_sink || ((topm >> q) & 1)) ? 1 : 0;
-    ++off;
-    selm &= selm - 1;
+  Bracket b[2];
+  b[0] = b[1] = Bracket{kmin, kmax + 1, all, 0u};
+  auto wide = [&](int i) {
+    return on[i] && b[i].hi - b[i].lo > 1 && b[i].clo - b[i].chi > kCandCap;
+  };
+  auto open = [&](int i) { return on[i] && b[i].hi - b[i].lo > 1; };
+
+  // 1. bisection, both searches per reduction (each count <= 32768 < 2^16)
+#pragma unroll 1
+  for (int it = 0; it < 33 && (wide(0) || wide(1)); ++it) {
+    const uint32_t m0 = b[0].lo + (b[0].hi - b[0].lo) / 2;
+    const uint32_t m1 = b[1].lo + (b[1].hi - b[1].lo) / 2;
+    uint32_t n = 0;
+#pragma unroll
+    for (int q = 0; q < PER; ++q) n += (uint32_t)(key[q] >= m0) + ((uint32_t)(key[q] >= m1) << 16);
+    const uint32_t c = block_sum_small(n, part, parity);
+    parity ^= 1;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      if (!wide(i)) continue;
+      const uint32_t ci = i ? c >> 16 : c & 0xFFFFu;
+      const uint32_t mid = i ? m1 : m0;
+      if (ci >= kk[i]) { b[i].lo = mid; b[i].clo = ci; }
+      else { b[i].hi = mid; b[i].chi = ci; }
+    }
   }
+
+  // 2. the candidates of each open bracket into LDS (at most kCandCap each):
+  // a key is inside [lo, hi) when key - lo < hi - lo (unsigned); keys
+  // outside go to the lane's spare slot, so the stores need no branch
+  uint32_t* cand[2] = {slu, slu + kCandCap};
+  uint32_t L[2] = {0u, 0u};
+  if (open(0) || open(1)) {
+    const uint32_t w0 = open(0) ? b[0].hi - b[0].lo : 0u, w1 = open(1) ? b[1].hi - b[1].lo : 0u;
+    uint32_t in0 = 0, in1 = 0;   // bit q: key q inside bracket 0 / 1
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      in0 |= (uint32_t)(key[q] - b[0].lo < w0) << q;
+      in1 |= (uint32_t)(key[q] - b[1].lo < w1) << q;
+    }
+    uint32_t e0, e1, t0, t1;
+    block_scan2_small(__builtin_popcount(in0), __builtin_popcount(in1), scr, parity, e0, e1, t0, t1);
+    parity ^= 1;
+    const uint32_t spare = kSpare + lane;
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      const uint32_t f0 = (in0 >> q) & 1u, f1 = (in1 >> q) & 1u;
+      slu[f0 && e0 < kCandCap ? e0 : spare] = key[q];
+      slu[f1 && e1 < kCandCap ? kCandCap + e1 : spare] = key[q];
+      e0 += f0;
+      e1 += f1;
+    }
+    L[0] = min(t0, kCandCap);
+    L[1] = min(t1, kCandCap);
+    __syncthreads();
+  }
+
+  // 3. radix rounds on the candidates: 256 bins of (x - lo) >> shift cover
+  // [lo, hi); the bin holding the k-th largest becomes the new bracket.  A
+  // 32-bit range takes at most four rounds.  Wave i scans histogram i.
+#pragma unroll 1
+  for (int it = 0; it < 5 && (open(0) || open(1)); ++it) {
+    int shift[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const uint32_t width = b[i].hi - b[i].lo;
+      const int bits = width > 1 ? 32 - __builtin_clz(width - 1) : 1;   // width - 1 < 2^bits
+      shift[i] = bits > 8 ? bits - 8 : 0;
+    }
+    if (tid < 512) hist[tid >> 8][tid & 255] = 0u;
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      if (!open(i)) continue;
+      const uint32_t wi = b[i].hi - b[i].lo;
+      for (uint32_t e = tid; e < L[i]; e += kSmallThreads) {
+        const uint32_t x = cand[i][e];
+        if (x - b[i].lo < wi) atomicAdd(&hist[i][(x - b[i].lo) >> shift[i]], 1u);
+      }
+    }
+    __syncthreads();
+    if (wave < 2 && (wave == 0 ? open(0) : open(1))) {
+      const int i = wave;
+      const Bracket bi = i ? b[1] : b[0];
+      const uint32_t ki = i ? kk[1] : kk[0];
+      const int si = i ? shift[1] : shift[0];
+      // lane l holds bins 4(63 - l) .. 4(63 - l) + 3, so a prefix sum over
+      // the lanes counts the keys at or above each lane's bins
+      const int base = 4 * (63 - lane);
+      uint32_t h4[4], suf = 0;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        h4[r] = hist[i][base + r];
+        suf += h4[r];
+      }
+      const uint32_t incl = wave_incl_scan(suf);
+      uint32_t above = bi.chi + incl - suf;   // keys in higher bins, plus those >= hi
+      int best = -1;
+      uint32_t bc = 0, bh = 0;
+#pragma unroll
+      for (int r = 3; r >= 0; --r) {
+        const uint32_t c = above + h4[r];
+        const bool hit = best < 0 && c >= ki;
+        best = hit ? base + r : best;
+        bc = hit ? c : bc;
+        bh = hit ? above : bh;
+        above = c;
+      }
+      // the lowest lane with a hit (the highest bins) owns the answer
+      const uint64_t hit = __ballot(best >= 0);
+      const int owner = __builtin_ctzll(hit);
+      if (lane == owner) {
+        const uint32_t nlo = bi.lo + ((uint32_t)best << si);
+        const uint64_t nhi = (uint64_t)bi.lo + ((uint64_t)(best + 1) << si);
+        sh[i][0] = nlo;
+        sh[i][1] = nhi < bi.hi ? (uint32_t)nhi : bi.hi;
+        sh[i][2] = bc;
+        sh[i][3] = bh;
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+      if (open(i))
+        b[i] = Bracket{uniform_u(sh[i][0]), uniform_u(sh[i][1]), uniform_u(sh[i][2]), uniform_u(sh[i][3])};
+    // (hist and sh are rewritten after the next round's first barrier)
+  }
+  const uint32_t T[2] = {b[0].lo, b[1].lo};
+
+  // 4. the boundary bands [blo, bhi] around each threshold: masks of the keys
+  // above and inside them, and their counts in one scan
+  uint32_t m[2] = {0u, 0u}, inb[2] = {0u, 0u};
+  uint32_t eb[2] = {0u, 0u}, tb[2] = {0u, 0u}, need[2] = {0u, 0u};
+  {
+    uint32_t na[2] = {0u, 0u}, nb[2] = {0u, 0u};
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      if (!on[i]) continue;
+      const uint32_t blo = band_lo(T[i]), bw = band_hi(T[i]) - blo;
+#pragma unroll
+      for (int q = 0; q < PER; ++q) {
+        m[i] |= (uint32_t)(key[q] > blo + bw) << q;
+        inb[i] |= (uint32_t)(key[q] - blo <= bw) << q;
+      }
+      na[i] = __builtin_popcount(m[i]);
+      nb[i] = __builtin_popcount(inb[i]);
+    }
+    uint32_t e0, e1, t0, t1;
+    block_scan2_small(na[0] | (na[1] << 16), nb[0] | (nb[1] << 16), scr, parity, e0, e1, t0, t1);
+    parity ^= 1;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int sft = 16 * i;
+      eb[i] = (e1 >> sft) & 0xFFFFu;
+      tb[i] = on[i] ? (t1 >> sft) & 0xFFFFu : 0u;
+      need[i] = on[i] ? kk[i] - ((t0 >> sft) & 0xFFFFu) : 0u;   // 1 <= need <= tb
+    }
+  }
+  // bands too wide to rank: fp32 order, ties (key == T) to the lower position
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    if (!on[i] || tb[i] <= kBandCap) continue;
+    uint32_t gt = 0, eq = 0;
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      gt += key[q] > T[i];
+      eq += key[q] == T[i];
+    }
+    uint32_t e, dummy, tg, teq;
+    block_scan2_small(eq, gt, scr, parity, e, dummy, teq, tg);
+    parity ^= 1;
+    const uint32_t krem = kk[i] - tg;
+    uint32_t mm = 0;
+#pragma unroll
+    for (int q = 0; q < PER; ++q) {
+      const bool take = key[q] > T[i] || (key[q] == T[i] && e < krem);
+      e += key[q] == T[i];
+      mm |= (uint32_t)take << q;
+    }
+    m[i] = mm;
+  }
+  const bool rank0 = on[0] && tb[0] <= kBandCap, rank1 = on[1] && tb[1] <= kBandCap;
+  if (rank0 || rank1) {
+    const SmallBand band[2] = {SmallBand(sl), SmallBand(sl + kBandCap * 4)};
+    const bool rk[2] = {rank0, rank1};
+    // band positions (few keys: a loop over the set bits of the band mask)
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      if (!rk[i]) continue;
+      uint32_t o = eb[i], bits = inb[i];
+      while (bits) {
+        band[i].pos[o++] = j0 + __builtin_ctz(bits);
+        bits &= bits - 1;
+      }
+    }
+    __syncthreads();
+    // fp64 sums of the band entries, left to right (terms outside the prefix
+    // are zero), with all loads of an entry in flight
+    const uint32_t n0 = rank0 ? tb[0] : 0u, n1 = rank1 ? tb[1] : 0u;
+    for (uint32_t e = tid; e < n0 + n1; e += kSmallThreads) {
+      const bool second = e >= n0;
+      const uint32_t r = second ? e - n0 : e;
+      const SmallBand& bd = second ? band[1] : band[0];
+      const int j = bd.pos[r];
+      float st[2 * H + 1];
+#pragma unroll
+      for (int t = -H; t <= H; ++t) st[t + H] = s[min(max(j + t, 0), P - 1)];
+      double acc = 0.0;
+#pragma unroll
+      for (int t = -H; t <= H; ++t)
+        acc += (j + t >= 0 && j + t < P) ? (double)st[t + H] : 0.0;
+      bd.v64[r] = acc;
+    }
+    __syncthreads();
+    // rank inside the band; the taken entries set their bit in the owning
+    // thread's mask word (position j belongs to thread j / 32, bit j % 32)
+    for (uint32_t e = tid; e < n0 + n1; e += kSmallThreads) {
+      const bool second = e >= n0;
+      const uint32_t r = second ? e - n0 : e, nb = second ? n1 : n0;
+      const SmallBand& bd = second ? band[1] : band[0];
+      const double v = bd.v64[r];
+      const int j = bd.pos[r];
+      uint32_t rank = 0;
+      for (uint32_t f = 0; f < nb; ++f) {
+        const double w = bd.v64[f];
+        rank += w > v || (w == v && bd.pos[f] < j);
+      }
+      if (rank < (second ? need[1] : need[0]))
+        atomicOr(&mw[(second ? kSmallThreads : 0) + (j >> 5)], 1u << (j & 31));
+    }
+    __syncthreads();
+    if (rank0) m[0] |= mw[tid];
+    if (rank1) m[1] |= mw[kSmallThreads + tid];
+  }
+
+  // 5. the selected positions in increasing order, through LDS (position,
+  // and the fixed-subset flag in bit 31), then stored coalesced
+  {
+    uint32_t selm = m[0];
+    const uint32_t topm = m[1];
+    uint32_t off, dummy, tot, tdummy;
+    block_scan2_small(__builtin_popcount(selm), 0u, scr, parity, off, dummy, tot, tdummy);
+    parity ^= 1;
+    while (selm) {
+      const int q = __builtin_ctz(selm);
+      slu[off++] = (uint32_t)(j0 + q) | (((topm >> q) & 1u) << 31);
+      selm &= selm - 1;
+    }
+    __syncthreads();
+    for (uint32_t r = tid; r < (uint32_t)us.s_sel; r += kSmallThreads) {
+      const uint32_t v = slu[r];
+      const int j = (int)(v & 0x7FFFFFFFu);
+      idx[r] = j;
+      fixed[r] = (j < a.n_sink || (v >> 31)) ? 1 : 0;
+    }
+  }
+
+  // 6. the pooled scores (an intermediate the caller may inspect), through
+  // LDS so that the stores are coalesced
+  __syncthreads();   // the staged positions are no longer read
+#pragma unroll
+  for (int q = 0; q < PER; ++q) sl[j0 + q + ((j0 + q) >> 6)] = __uint_as_float(key[q]);
+  __syncthreads();
+  for (int t = tid; t < P; t += kSmallThreads) pg[t] = sl[t + (t >> 6)];
+  }   // P > 0
+
   for (int i = tid; i < a.w; i += kSmallThreads) {
     const int64_t pos = a.n - a.w + i;
     idx[us.s_sel + i] = (int32_t)pos;
@@ -914,9 +1058,16 @@ hipError_t launch_select(const Plan& p, const float* colsum, float* pooled, int3
   a.s_sel = p.s_sel; a.n_top = p.n_top_fixed; a.n_sink = p.opt.n_sink;
   a.fix_window = p.opt.fix_window ? 1 : 0; a.n = p.n;
   a.rag = p.rag;
-  if (p.prefix <= kSmallThreads * kSmallPer && p.k_pool <= 17)
-    hipLaunchKernelGGL(select_small_kernel, dim3(p.U), dim3(kSmallThreads), 0, s, a);
-  else
+  if (p.prefix <= kSmallThreads * kSmallPer && p.k_pool <= 17) {
+#define GRKV_SEL_SMALL(HV) \
+  case HV: hipLaunchKernelGGL(select_small_kernel<HV>, dim3(p.U), dim3(kSmallThreads), 0, s, a); break;
+    switch (a.h) {
+      GRKV_SEL_SMALL(0) GRKV_SEL_SMALL(1) GRKV_SEL_SMALL(2) GRKV_SEL_SMALL(3) GRKV_SEL_SMALL(4)
+      GRKV_SEL_SMALL(5) GRKV_SEL_SMALL(6) GRKV_SEL_SMALL(7) GRKV_SEL_SMALL(8)
+      default: return hipErrorInvalidValue;
+    }
+#undef GRKV_SEL_SMALL
+  } else
     hipLaunchKernelGGL(select_kernel, dim3(p.U), dim3(kSelectThreads), 0, s, a);
   return hipGetLastError();
 }
