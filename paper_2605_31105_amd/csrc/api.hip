@@ -277,7 +277,10 @@ int run_compress(const Plan& p, const void* q_obs, const void* K, const void* V,
   GRKV_STAGE(GRKV_STAGE_FULL_PROB, pass_b(full));
   // (the fast value step combines the Y partials inside its solve, again
   // unless there are many)
-  if (!p.fast_merge || pre)
+  // (with many retained splits too, the Y partials join the retained
+  // partials' combine below: one launch for both)
+  const bool pre2 = fast && p.fast_merge && !p.rag && p.S2 >= kPrecombineRetSplits;
+  if (!p.fast_merge || (pre && !pre2))
     GRKV_STAGE(GRKV_STAGE_FULL_Y, launch_combine_rows(p, F(p.ypart), p.S1, nullptr, F(p.y), s));
   // 2. pooled top-k retention and the fixed set; gather K0, V0
   uint8_t* fixed = (uint8_t*)(ws + p.fixed);
@@ -323,12 +326,13 @@ int run_compress(const Plan& p, const void* q_obs, const void* K, const void* V,
   if (fast_merge) {
     // many retained splits per unit (small uniform calls): their partials are
     // summed by one launch over all units first
-    const bool pre2 = direct && !p.rag && p.S2 >= kPrecombineRetSplits;
     if (pre2) {
-      const float* part[3] = {F(p.xvpart), F(p.npart), F(p.mpart)};
-      float* const outs[3] = {F(p.xvcomb), F(p.ncomb), F(p.mcomb)};
-      const size_t per[3] = {(size_t)p.mp * p.d, (size_t)p.mp * p.mp, (size_t)p.mp};
-      GRKV_STAGE(GRKV_STAGE_RESID, launch_combine_parts(p.U, p.S2, part, outs, per, s));
+      const float* part[kCombineSegs] = {F(p.xvpart), F(p.npart), F(p.mpart), F(p.ypart)};
+      float* const outs[kCombineSegs] = {F(p.xvcomb), F(p.ncomb), F(p.mcomb), F(p.y)};
+      const size_t per[kCombineSegs] = {(size_t)p.mp * p.d, (size_t)p.mp * p.mp, (size_t)p.mp,
+                                        pre ? (size_t)p.mp * p.d : 0};
+      const int S[kCombineSegs] = {p.S2, p.S2, p.S2, p.S1};
+      GRKV_STAGE(GRKV_STAGE_RESID, launch_combine_parts(p.U, S, part, outs, per, s));
     }
     GRKV_TRY(mark(GRKV_STAGE_SOLVE, 0));
     GRKV_TRY(launch_solve(p, pre ? F(p.y) : F(p.ypart), pre ? 1 : p.S1, pre2 ? 1 : p.S2,

@@ -480,23 +480,25 @@ __global__ void combine_rows_kernel(const float* part, int S, size_t per_unit, s
   out[id] = base ? base[id] - acc : acc;
 }
 
-// Up to three partial arrays summed over S splits in one launch: segment i
-// covers U * per_unit[i] consecutive ids.
+// Up to four partial arrays summed over their splits in one launch: segment
+// i covers U * per_unit[i] consecutive ids, each summing S[i] splits.
 struct CombineSeg {
-  const float* part[3];
-  float* out[3];
-  size_t per_unit[3];
+  const float* part[kCombineSegs];
+  float* out[kCombineSegs];
+  size_t per_unit[kCombineSegs];
+  int S[kCombineSegs];
 };
 
-__global__ void combine_segments_kernel(CombineSeg g, int S, int U, size_t total) {
+__global__ void combine_segments_kernel(CombineSeg g, int U, size_t total) {
   size_t id = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (id >= total) return;
   int i = 0;
-  while (i < 2 && id >= (size_t)U * g.per_unit[i]) {
+  while (i < kCombineSegs - 1 && id >= (size_t)U * g.per_unit[i]) {
     id -= (size_t)U * g.per_unit[i];
     ++i;
   }
   const size_t pu = g.per_unit[i], u = id / pu, e = id % pu;
+  const int S = g.S[i];
   const float* p0 = g.part[i] + u * S * pu + e;
   float acc = 0.f;
   for (int s0 = 0; s0 < S; s0 += kCombineBatch) {
@@ -580,18 +582,21 @@ hipError_t launch_combine_rows(const Plan& p, const float* part, int S, const fl
   return hipGetLastError();
 }
 
-hipError_t launch_combine_parts(int U, int S, const float* const part[3], float* const out[3],
-                                const size_t per_unit[3], hipStream_t s) {
+hipError_t launch_combine_parts(int U, const int S[kCombineSegs],
+                                const float* const part[kCombineSegs],
+                                float* const out[kCombineSegs],
+                                const size_t per_unit[kCombineSegs], hipStream_t s) {
   CombineSeg g;
   size_t total = 0;
-  for (int i = 0; i < 3; ++i) {
+  for (int i = 0; i < kCombineSegs; ++i) {
     g.part[i] = part[i];
     g.out[i] = out[i];
     g.per_unit[i] = per_unit[i];
+    g.S[i] = S[i];
     total += (size_t)U * per_unit[i];
   }
   hipLaunchKernelGGL(combine_segments_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s,
-                     g, S, U, total);
+                     g, U, total);
   return hipGetLastError();
 }
 

@@ -116,10 +116,13 @@ hipError_t launch_lse_combine(const Plan& p, const float* pmax,
                               const double* psum, int S, double* lse,
                               float* lse_log2, hipStream_t s);
 hipError_t launch_prob_pass(const Plan& p, const AttnPass& a, hipStream_t s);
-// out[i][u][e] = sum_s part[i][u][s][e], e < per_unit[i], for the three arrays i
-// (a per_unit of 0 leaves that array out); one launch.
-hipError_t launch_combine_parts(int U, int S, const float* const part[3], float* const out[3],
-                                const size_t per_unit[3], hipStream_t s);
+// out[i][u][e] = sum over s < S[i] of part[i][u][s][e], e < per_unit[i], for
+// up to four arrays i (a per_unit of 0 leaves that array out); one launch.
+constexpr int kCombineSegs = 4;
+hipError_t launch_combine_parts(int U, const int S[kCombineSegs],
+                                const float* const part[kCombineSegs],
+                                float* const out[kCombineSegs],
+                                const size_t per_unit[kCombineSegs], hipStream_t s);
 // out[u][r][c] = (base ? base[u][r][c] : 0) +/- sum_s part[u][s][r][c]
 hipError_t launch_combine_rows(const Plan& p, const float* part, int S,
                                const float* base, float* out, hipStream_t s);

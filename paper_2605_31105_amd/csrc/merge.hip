@@ -281,64 +281,101 @@ __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
 #pragma unroll
       for (int h = 0; h < 2; ++h) add4(acc[h], p[(size_t)s * stride + e[h]]);
   };
-  {
+  // R = Y - X V0 (scaled by the inverse retained masses) and Y for element
+  // e of the [MP][D] arrays (both sums given)
+  auto put_r = [&](int e, float4 yy, const float4 xv) {
+    const int r = e / (D / 4), c4 = (e % (D / 4)) * 4;
+    const float im = inv_mass[r];
+    float4 rv = make_float4(yy.x - im * xv.x, yy.y - im * xv.y, yy.z - im * xv.z, yy.w - im * xv.w);
+    if (r >= m) yy = rv = make_float4(0.f, 0.f, 0.f, 0.f);
+    reinterpret_cast<float4*>(y)[(size_t)u * (MP * D / 4) + e] = yy;
+    reinterpret_cast<float4*>(resid)[(size_t)u * (MP * D / 4) + e] = rv;
+    *reinterpret_cast<float4*>(B + r * BS + c4) = rv;
+    sy += (double)yy.x * yy.x + (double)yy.y * yy.y + (double)yy.z * yy.z + (double)yy.w * yy.w;
+    sr += (double)rv.x * rv.x + (double)rv.y * rv.y + (double)rv.z * rv.z + (double)rv.w * rv.w;
+  };
+  // N = Gram sum scaled by the inverse masses, + lambda I (padding: identity)
+  auto put_n = [&](int e, const float4 v) {
+    const int r = e / (MP / 4), c4 = (e % (MP / 4)) * 4;
+    float vv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int col = c4 + k;
+      vv[k] *= inv_mass[r] * inv_mass[col];
+      if (r >= m || col >= m) vv[k] = 0.f;
+      if (r == col) vv[k] += r < m ? lam : 1.f;
+    }
+    const float4 o = make_float4(vv[0], vv[1], vv[2], vv[3]);
+    reinterpret_cast<float4*>(gram)[(size_t)u * (MP * MP / 4) + e] = o;
+    *reinterpret_cast<float4*>(A + r * AS + c4) = o;
+  };
+  if (MP == D && S1 <= 4 && S2 == 1 && S3 == 1) {
+    // the usual shapes (one retained split, at most four full-cache splits):
+    // every load of two elements of Y, X V0 and N in flight together
     constexpr int E = MP * D / 4;
     const float4* __restrict__ yp = reinterpret_cast<const float4*>(ypart) + (size_t)u * S1 * E;
     const float4* __restrict__ xp = reinterpret_cast<const float4*>(xvpart) + sp0 * E;
-    float4* __restrict__ yo = reinterpret_cast<float4*>(y) + (size_t)u * E;
-    float4* __restrict__ ro = reinterpret_cast<float4*>(resid) + (size_t)u * E;
+    const float4* __restrict__ np = reinterpret_cast<const float4*>(npart) + sp3 * E;
     for (int e0 = tid; e0 < E; e0 += 2 * NTH) {
-      float4 yv[2], xv[2];
+      const int ee[2] = {e0, min(e0 + NTH, E - 1)};
+      float4 yv[4][2], xv[2], nv[2];
 #pragma unroll
-      for (int h = 0; h < 2; ++h) yv[h] = xv[h] = make_float4(0.f, 0.f, 0.f, 0.f);
-      const int e1 = min(e0 + NTH, E - 1);   // the second element, clamped (stored only if < E)
-      const int ee[2] = {e0, e1};
-      sum_parts(yp, E, S1, ee, yv);
-      sum_parts(xp, E, S2, ee, xv);
+      for (int sp = 0; sp < 4; ++sp)
+        if (sp < S1)
+#pragma unroll
+          for (int h = 0; h < 2; ++h) yv[sp][h] = yp[(size_t)sp * E + ee[h]];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        xv[h] = xp[ee[h]];
+        nv[h] = np[ee[h]];
+      }
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const int e = e0 + h * NTH;
         if (e >= E) break;
-        const int r = e / (D / 4), c4 = (e % (D / 4)) * 4;
-        const float im = inv_mass[r];
-        float4 rv = make_float4(yv[h].x - im * xv[h].x, yv[h].y - im * xv[h].y,
-                                yv[h].z - im * xv[h].z, yv[h].w - im * xv[h].w);
-        float4 yy = yv[h];
-        if (r >= m) yy = rv = make_float4(0.f, 0.f, 0.f, 0.f);
-        yo[e] = yy;
-        ro[e] = rv;
-        *reinterpret_cast<float4*>(B + r * BS + c4) = rv;
-        sy += (double)yy.x * yy.x + (double)yy.y * yy.y + (double)yy.z * yy.z + (double)yy.w * yy.w;
-        sr += (double)rv.x * rv.x + (double)rv.y * rv.y + (double)rv.z * rv.z + (double)rv.w * rv.w;
+        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+        for (int sp = 0; sp < 4; ++sp)   // in split order
+          if (sp < S1) add4(acc, yv[sp][h]);
+        put_r(e, acc, xv[h]);
+        put_n(e, nv[h]);
       }
     }
-  }
-  {
-    constexpr int E = MP * MP / 4;
-    const float4* __restrict__ np = reinterpret_cast<const float4*>(npart) + sp3 * E;
-    float4* __restrict__ go = reinterpret_cast<float4*>(gram) + (size_t)u * E;
-    for (int e2 = tid; e2 < E; e2 += 2 * NTH) {
-     float4 v2[2] = {make_float4(0.f, 0.f, 0.f, 0.f), make_float4(0.f, 0.f, 0.f, 0.f)};
-     const int ee[2] = {e2, min(e2 + NTH, E - 1)};
-     sum_parts(np, E, S3, ee, v2);
+  } else {
+    {
+      constexpr int E = MP * D / 4;
+      const float4* __restrict__ yp = reinterpret_cast<const float4*>(ypart) + (size_t)u * S1 * E;
+      const float4* __restrict__ xp = reinterpret_cast<const float4*>(xvpart) + sp0 * E;
+      for (int e0 = tid; e0 < E; e0 += 2 * NTH) {
+        float4 yv[2], xv[2];
 #pragma unroll
-     for (int h = 0; h < 2; ++h) {
-      const int e = e2 + h * NTH;
-      if (e >= E) break;
-      const float4 v = v2[h];
-      const int r = e / (MP / 4), c4 = (e % (MP / 4)) * 4;
-      float vv[4] = {v.x, v.y, v.z, v.w};
+        for (int h = 0; h < 2; ++h) yv[h] = xv[h] = make_float4(0.f, 0.f, 0.f, 0.f);
+        const int e1 = min(e0 + NTH, E - 1);   // the second element, clamped (stored only if < E)
+        const int ee[2] = {e0, e1};
+        sum_parts(yp, E, S1, ee, yv);
+        sum_parts(xp, E, S2, ee, xv);
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const int col = c4 + k;
-        vv[k] *= inv_mass[r] * inv_mass[col];
-        if (r >= m || col >= m) vv[k] = 0.f;
-        if (r == col) vv[k] += r < m ? lam : 1.f;
+        for (int h = 0; h < 2; ++h) {
+          const int e = e0 + h * NTH;
+          if (e >= E) break;
+          put_r(e, yv[h], xv[h]);
+        }
       }
-      const float4 o = make_float4(vv[0], vv[1], vv[2], vv[3]);
-      go[e] = o;
-      *reinterpret_cast<float4*>(A + r * AS + c4) = o;
-     }
+    }
+    {
+      constexpr int E = MP * MP / 4;
+      const float4* __restrict__ np = reinterpret_cast<const float4*>(npart) + sp3 * E;
+      for (int e2 = tid; e2 < E; e2 += 2 * NTH) {
+        float4 v2[2] = {make_float4(0.f, 0.f, 0.f, 0.f), make_float4(0.f, 0.f, 0.f, 0.f)};
+        const int ee[2] = {e2, min(e2 + NTH, E - 1)};
+        sum_parts(np, E, S3, ee, v2);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int e = e2 + h * NTH;
+          if (e >= E) break;
+          put_n(e, v2[h]);
+        }
+      }
     }
   }
   __syncthreads();
@@ -414,14 +451,21 @@ __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
       w = mfma_f32(lf.z, r[p][2], w);
       w = mfma_f32(lf.w, r[p][3], w);
       r[p] = w;
+      // the updates of the tiles below are independent chains: issued
+      // interleaved (k outer) so that the matrix unit is not left waiting on
+      // one chain; each tile still sums k = 0..3 in order
+      float4 af[NP];
 #pragma unroll
-      for (int t = p + 1; t < NP; ++t) {
-        const float4 af = *reinterpret_cast<const float4*>(A + (16 * t + l16) * AS + 16 * p + 4 * g);
-        r[t] = mfma_f32(-af.x, w[0], r[t]);
-        r[t] = mfma_f32(-af.y, w[1], r[t]);
-        r[t] = mfma_f32(-af.z, w[2], r[t]);
-        r[t] = mfma_f32(-af.w, w[3], r[t]);
-      }
+      for (int t = p + 1; t < NP; ++t)
+        af[t] = *reinterpret_cast<const float4*>(A + (16 * t + l16) * AS + 16 * p + 4 * g);
+#pragma unroll
+      for (int t = p + 1; t < NP; ++t) r[t] = mfma_f32(-af[t].x, w[0], r[t]);
+#pragma unroll
+      for (int t = p + 1; t < NP; ++t) r[t] = mfma_f32(-af[t].y, w[1], r[t]);
+#pragma unroll
+      for (int t = p + 1; t < NP; ++t) r[t] = mfma_f32(-af[t].z, w[2], r[t]);
+#pragma unroll
+      for (int t = p + 1; t < NP; ++t) r[t] = mfma_f32(-af[t].w, w[3], r[t]);
     }
     // backward: Z_p = L_pp^-T W_p, then W_i -= L_pi^T Z_p for i < p
 #pragma unroll
@@ -432,11 +476,10 @@ __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
         zt = mfma_f32(Li[(p * 16 + 4 * g + kb) * LS + l16], r[p][kb], zt);
       r[p] = zt;
 #pragma unroll
-      for (int t = 0; t < p; ++t) {
+      for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-        for (int kb = 0; kb < 4; ++kb)
+        for (int t = 0; t < p; ++t)
           r[t] = mfma_f32(-A[(16 * p + 4 * g + kb) * AS + 16 * t + l16], zt[kb], r[t]);
-      }
     }
     // Z^T out: row dd = c0 + l16, entries 16t + 4g .. +3
     const int dd = c0 + l16;
