@@ -152,6 +152,9 @@ static void make_key_plan(const Plan& p, int steps, KeyPlan* kp) {
   // keeps it short once only a few units are still converging
   split_range(p.c, ceil_div(256, p.U), 64, &kp->S_full, &kp->chunk_full);
   split_range(p.c, ceil_div(2048, p.U), 64, &kp->S4, &kp->chunk4);
+  // the ring passes' later iterations: about 1024 blocks (fewer partials for
+  // the separate CG update to combine, measured faster than 2048)
+  split_range(p.c, ceil_div(1024, p.U), 64, &kp->S4r, &kp->chunk4r);
   const int Smax = kp->S4 > kp->S_full ? kp->S4 : kp->S_full;
   const size_t U = p.U, mp = p.mp, d = p.d;
   size_t off = p.total;

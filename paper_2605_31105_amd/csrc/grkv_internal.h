@@ -205,6 +205,7 @@ enum { kKeyRunning = 0, kKeyConverged = 1, kKeyMaxIter = 2, kKeySkipped = 3, kKe
 
 struct KeyPlan {
   int S4, chunk4;           // splits of the retained keys per unit, later CG iterations
+  int S4r, chunk4r;         // the same for the ring passes (at most S4)
   int S_full, chunk_full;   // the same for the first iterations and the final pass
   size_t Fm, alpha, r, p, sdot, W, opart, hpart, cg;   // offsets after Plan::total
   // later alternating steps (steps > 1): fp32 copies of Q and V0, the compact

@@ -41,6 +41,7 @@ namespace {
 
 constexpr int kKT = 32;   // retained keys per tile (the key orders below assume 32)
 constexpr int kKeyEarlyIters = 13;  // CG iterations run with the fewest splits
+constexpr int kKeyRingEarlyIters = 16;  // the same for the ring passes
 
 // Position, inside a block of 32, of the index a lane holds as element j of an
 // MFMA operand when the operand comes from an MFMA result: elements
@@ -768,8 +769,8 @@ hipError_t launch_key_t(const Plan& p, const KeyPlan& kp, const KeyArgs& a, hipS
     e = launch_key_prep(p, a, s);
     if (e != hipSuccess) return e;
     for (int it = 0; it < a.max_iter; ++it) {
-      const bool early = it < kKeyEarlyIters;
-      const int S = early ? kp.S_full : kp.S4, chunk = early ? kp.chunk_full : kp.chunk4;
+      const bool early = it < kKeyRingEarlyIters;
+      const int S = early ? kp.S_full : kp.S4r, chunk = early ? kp.chunk_full : kp.chunk4r;
       // one split per unit: the CG update runs inside the pass
       const bool fuse = S == 1;
       e = launch_key_ring(p, a, false, S, chunk, a.p, fuse, s);

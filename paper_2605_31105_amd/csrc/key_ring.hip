@@ -566,11 +566,52 @@ __global__ __launch_bounds__(kRTh) void key_ring_kernel(RingArgs a) {
       return;
     }
     // One split holds the whole unit: the conjugate-gradient update of
-    // key_cg on the consumers' rows, with the block sums through LDS (the
-    // ring is no longer read).  Ap = out + lambda_k p - (H 1) o F;
-    // alpha += a p, r -= a Ap with a = r.r / p.Ap; p = r + (r'.r' / r.r) p and
-    // s = rowdot(F, p) for the next pass.  Sums in fp64.
-    double* red = reinterpret_cast<double*>(dbuf0);
+    // key_cg, spread over all eight waves.  Each thread takes 32 consecutive
+    // elements of one row (row tid / 4, columns 32 (tid % 4) ..) and loads
+    // its p, F, alpha and r at once, before the barrier; the consumers pass
+    // out (rows in stg0 / stg1, 16-byte chunks XOR-swizzled by the row) and
+    // the row sums of H (dbuf0) through the now idle ring.  Then
+    // Ap = out + lambda_k p - (H 1) o F; alpha += a p, r -= a Ap with
+    // a = r.r / p.Ap; p = r + (r'.r' / r.r) p and s = rowdot(F, p) for the
+    // next pass.  Sums in fp64, block sums through dbuf1.
+    constexpr int kEl = kRMP * kRD / kRTh;   // 32 elements per thread
+    const int er = tid >> 2, ec = (tid & 3) * kEl;
+    const size_t eo = ((size_t)u * kRMP + er) * kRD + ec;
+    f32x4 pv[kEl / 4], fv[kEl / 4], av[kEl / 4], rv[kEl / 4];
+    auto prefetch = [&]() {
+#pragma unroll
+      for (int k = 0; k < kEl / 4; ++k) {
+        pv[k] = *reinterpret_cast<const f32x4*>(a.dir + eo + 4 * k);
+        fv[k] = *reinterpret_cast<const f32x4*>(a.Fm + eo + 4 * k);
+        av[k] = *reinterpret_cast<const f32x4*>(a.alpha + eo + 4 * k);
+        rv[k] = *reinterpret_cast<const f32x4*>(a.r + eo + 4 * k);
+      }
+    };
+    const double rr = a.cg[u * 4 + 0], rr0 = a.cg[u * 4 + 1];
+    const int it = (int)a.cg[u * 4 + 2] + 1;
+    float* hbuf = reinterpret_cast<float*>(dbuf0);
+    double* red = reinterpret_cast<double*>(dbuf1);
+    // out[row][col] in stg0 (rows < 64) or stg1, at (row % 64) * kRD +
+    // 4 * ((col / 4) ^ (row % 16)) + col % 4
+    auto oaddr = [&](int row, int ch) {
+      float* base = reinterpret_cast<float*>(row < 64 ? stg0 : stg1);
+      return base + (row & 63) * kRD + 4 * (ch ^ (row & 15));
+    };
+    // (the producers, done first, load theirs while the consumers finish;
+    // the consumers load theirs once out has left their registers)
+    if (producer) prefetch();
+    lds_barrier();   // every wave is past its last ring access
+    if (!producer) {
+#pragma unroll
+      for (int rt = 0; rt < 2; ++rt) {
+        const int row = row0 + 16 * rt + l16;
+#pragma unroll
+        for (int dt = 0; dt < kRD / 16; ++dt)
+          *reinterpret_cast<f32x4*>(oaddr(row, 4 * dt + g)) = oacc[rt][dt];
+        if (g == 0) hbuf[row] = hrow[rt];
+      }
+      prefetch();
+    }
     auto block_sum8 = [&](double v, int slot) {
 #pragma unroll
       for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
@@ -581,81 +622,59 @@ __global__ __launch_bounds__(kRTh) void key_ring_kernel(RingArgs a) {
       for (int k = 0; k < kRW; ++k) t += red[slot * kRW + k];
       return t;
     };
-    lds_barrier();   // every wave is past its last ring access
+    lds_barrier();
+    f32x4 ap[kEl / 4];
     double part = 0.0;
-    if (!producer) {
+    {
+      const float h = hbuf[er];
 #pragma unroll
-      for (int rt = 0; rt < 2; ++rt) {
-        const size_t ro = ((size_t)u * kRMP + row0 + 16 * rt + l16) * kRD + 4 * g;
+      for (int k = 0; k < kEl / 4; ++k) {
+        const f32x4 o = *reinterpret_cast<const f32x4*>(oaddr(er, ec / 4 + k));
 #pragma unroll
-        for (int dt = 0; dt < kRD / 16; ++dt) {
-          const f32x4 pv = *reinterpret_cast<const f32x4*>(a.dir + ro + 16 * dt);
-          const f32x4 fv = *reinterpret_cast<const f32x4*>(a.Fm + ro + 16 * dt);
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const float ap = oacc[rt][dt][i] + a.lam_k * pv[i] - hrow[rt] * fv[i];
-            oacc[rt][dt][i] = ap;
-            part += (double)(pv[i] * ap);
-          }
+        for (int i = 0; i < 4; ++i) {
+          ap[k][i] = o[i] + a.lam_k * pv[k][i] - h * fv[k][i];
+          part += (double)(pv[k][i] * ap[k][i]);
         }
       }
     }
     const double pap = block_sum8(part, 0);
-    const double rr = a.cg[u * 4 + 0], rr0 = a.cg[u * 4 + 1];
-    const int it = (int)a.cg[u * 4 + 2] + 1;
     if (!(pap > 0)) {
       if (tid == 0) a.cg[u * 4 + 3] = kKeyBreakdown;
       return;
     }
     const float step = (float)(rr / pap);
     part = 0.0;
-    if (!producer) {
 #pragma unroll
-      for (int rt = 0; rt < 2; ++rt) {
-        const size_t ro = ((size_t)u * kRMP + row0 + 16 * rt + l16) * kRD + 4 * g;
+    for (int k = 0; k < kEl / 4; ++k) {
 #pragma unroll
-        for (int dt = 0; dt < kRD / 16; ++dt) {
-          const f32x4 pv = *reinterpret_cast<const f32x4*>(a.dir + ro + 16 * dt);
-          f32x4 al = *reinterpret_cast<const f32x4*>(a.alpha + ro + 16 * dt);
-          f32x4 rv = *reinterpret_cast<const f32x4*>(a.r + ro + 16 * dt);
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            al[i] += step * pv[i];
-            rv[i] -= step * oacc[rt][dt][i];
-            part += (double)(rv[i] * rv[i]);
-          }
-          *reinterpret_cast<f32x4*>(a.alpha + ro + 16 * dt) = al;
-          *reinterpret_cast<f32x4*>(a.r + ro + 16 * dt) = rv;
-          oacc[rt][dt] = rv;
-        }
+      for (int i = 0; i < 4; ++i) {
+        av[k][i] += step * pv[k][i];
+        rv[k][i] -= step * ap[k][i];
+        part += (double)(rv[k][i] * rv[k][i]);
       }
+      *reinterpret_cast<f32x4*>(a.alpha + eo + 4 * k) = av[k];
+      *reinterpret_cast<f32x4*>(a.r + eo + 4 * k) = rv[k];
     }
     const double rn = block_sum8(part, 1);
     int st = kKeyRunning;
     if (sqrt(rn) <= (double)a.tol * sqrt(rr0)) st = kKeyConverged;
     else if (it >= a.max_iter) st = kKeyMaxIter;
-    if (st == kKeyRunning && !producer) {
+    if (st == kKeyRunning) {
       const float beta = (float)(rn / rr);
+      float sdr = 0.f;
 #pragma unroll
-      for (int rt = 0; rt < 2; ++rt) {
-        const int row = row0 + 16 * rt + l16;
-        const size_t ro = ((size_t)u * kRMP + row) * kRD + 4 * g;
-        float sdr = 0.f;
+      for (int k = 0; k < kEl / 4; ++k) {
 #pragma unroll
-        for (int dt = 0; dt < kRD / 16; ++dt) {
-          f32x4 pv = *reinterpret_cast<const f32x4*>(a.dir + ro + 16 * dt);
-          const f32x4 fv = *reinterpret_cast<const f32x4*>(a.Fm + ro + 16 * dt);
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            pv[i] = oacc[rt][dt][i] + beta * pv[i];
-            sdr += fv[i] * pv[i];
-          }
-          *reinterpret_cast<f32x4*>(a.dir + ro + 16 * dt) = pv;
+        for (int i = 0; i < 4; ++i) {
+          pv[k][i] = rv[k][i] + beta * pv[k][i];
+          sdr += fv[k][i] * pv[k][i];
         }
-        sdr += __shfl_xor(sdr, 16);
-        sdr += __shfl_xor(sdr, 32);
-        if (g == 0) a.sdot[(size_t)u * kRMP + row] = sdr;
+        *reinterpret_cast<f32x4*>(a.dir + eo + 4 * k) = pv[k];
       }
+      // the four threads of a row are adjacent lanes
+      sdr += __shfl_xor(sdr, 1);
+      sdr += __shfl_xor(sdr, 2);
+      if ((tid & 3) == 0) a.sdot[(size_t)u * kRMP + er] = sdr;
     }
     if (tid == 0) {
       a.cg[u * 4 + 0] = rn;
