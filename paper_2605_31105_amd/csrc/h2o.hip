@@ -6,229 +6,272 @@
 // 0..i:
 //   s_j = sum_g sum_{i >= j} 2^(t_{g,i,j} - LSE2_{g,i}),  t = q . k log2(e) / sqrt(d).
 // This is the work of a prefill attention without P.V (O(n^2 d) per head),
-// done in two MFMA passes with no atomics:
-//  * h2o_lse_kernel, one block per (unit, 32 prompt positions) with one wave
-//    per query head (two 16-row tiles): streams K tiles 0 .. (last position)
-//    through LDS and keeps, per row and lane, an integer reference exponent
-//    and an fp64 sum of 2^(t - ref) (as the window's pass A does); the four
-//    lanes of a row merge at the end into LSE2 (log2 domain);
-//  * h2o_colsum_kernel, one block per (unit, 128 prefix keys) with 4 waves of
-//    32 keys (K fragments in registers): streams the query tiles at or after
-//    its first key (Q rows and their LSE2 through LDS), forms
-//    P = 2^(t - LSE2) under the causal rule and accumulates each key's column
-//    sum, in fp32 within a query tile and in fp64 across tiles; a 16-lane
+// done in two MFMA passes with no atomics, each with 8 waves of 64 rows or
+// 32 keys so that a tile staged in LDS feeds many MFMAs per barrier:
+//  * h2o_lse_kernel: a block takes 512 / G prompt positions of all G query
+//    heads (512 rows, head-major; wave w owns rows 64w .. 64w + 63, four
+//    16-row tiles as MFMA B operands in registers) and streams the key tiles
+//    (64 keys) up to its last position through LDS, keeping per row and lane
+//    an integer reference exponent and an fp64 sum of 2^(t - ref) (as the
+//    window's pass A does); the four lanes of a row merge at the end into
+//    LSE2 (log2 domain).  Blocks run latest positions first (most keys);
+//  * h2o_colsum_kernel: a block takes 256 prefix keys (wave w: keys
+//    32w .. 32w + 31 as A operands in registers) and streams the query tiles
+//    (256 / G positions of all heads) at or after its first key, with their
+//    LSE2, through LDS; P = 2^(t - LSE2) under the causal rule is summed per
+//    key, in fp32 within a query tile and in fp64 across tiles; a 16-lane
 //    reduction at the end gives the key's score.
+// Causal masks are applied only on tiles that straddle the diagonal.
 // The scores then drive grkv_compress_scored (selection with pool width 1).
 #include "grkv_device.h"
 #include "grkv_internal.h"
 
+#include <type_traits>
+
 namespace grkv {
 namespace {
 
-constexpr int kH2oTQ = 32;          // prompt positions per query tile
-constexpr int kH2oKT = 32;          // keys per streamed key tile (LSE pass)
-constexpr int kH2oColWaves = 4;
-constexpr int kH2oColKeys = 32 * kH2oColWaves;   // keys per column-sum block
+constexpr int kH2oWaves = 8;
+constexpr int kH2oTh = kH2oWaves * 64;
+constexpr int kH2oRows = 512;       // rows (positions x heads) of an LSE block
+constexpr int kH2oKT = 64;          // keys per streamed key tile (LSE pass)
+constexpr int kH2oColKeys = 32 * kH2oWaves;   // keys per column-sum block
+constexpr int kH2oQRows = 256;      // rows (positions x heads) of a streamed query tile
 
 // ------------------------------------------------------------ row LSE ----
 template <int D, int G>
-__global__ __launch_bounds__(G * 64) void h2o_lse_kernel(const u16* __restrict__ q_all,
+__global__ __launch_bounds__(kH2oTh) void h2o_lse_kernel(const u16* __restrict__ q_all,
                                                          const u16* __restrict__ K, int n,
                                                          float scale_log2, float* __restrict__ lse2) {
+  constexpr int TQ = kH2oRows / G;          // prompt positions per block
   constexpr int KS = D + 8;                 // LDS row stride (bf16)
-  constexpr int NTH = G * 64;
   constexpr int CH = kH2oKT * D / 8;        // 16-byte chunks of a key tile
-  constexpr int PER = (CH + NTH - 1) / NTH;
+  constexpr int PER = (CH + kH2oTh - 1) / kH2oTh;
+  constexpr int RT = 4;                     // 16-row tiles per wave
+  constexpr int KT = kH2oKT / 16;           // 16-key tiles per key tile
+  constexpr float NINF = -__builtin_huge_valf();
   __shared__ __attribute__((aligned(16))) u16 kt_s[2][kH2oKT * KS];
-  const int u = blockIdx.y, p0 = blockIdx.x * kH2oTQ, tid = threadIdx.x;
-  const int lane = tid & 63, g = __builtin_amdgcn_readfirstlane(tid >> 6), l16 = lane & 15, gq = lane >> 4;
+  const int nb = (n + TQ - 1) / TQ;
+  const int u = blockIdx.y, p0 = (nb - 1 - (int)blockIdx.x) * TQ, tid = threadIdx.x;
+  const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l16 = lane & 15, gq = lane >> 4;
+  const int head = (64 * wave) / TQ, pw0 = p0 + (64 * wave) % TQ;   // the wave's head, first position
   const u16* ku = K + (size_t)u * n * D;
-  const u16* qh = q_all + ((size_t)u * G + g) * n * D;
+  const u16* qh = q_all + ((size_t)u * G + head) * n * D;
 
-  // the wave's rows: positions p0 + 16 rt + l16 of head g (B operand layout)
-  uint4 qb[2][D / 32];
-  int pos[2];
+  // the wave's rows: positions pw0 + 16 rt + l16 (B operand layout)
+  bf16x8 qb[RT][D / 32];
+  int pos[RT];
 #pragma unroll
-  for (int rt = 0; rt < 2; ++rt) {
-    pos[rt] = p0 + 16 * rt + l16;
+  for (int rt = 0; rt < RT; ++rt) {
+    pos[rt] = pw0 + 16 * rt + l16;
     const int pr = min(pos[rt], n - 1);
 #pragma unroll
     for (int ks = 0; ks < D / 32; ++ks)
-      qb[rt][ks] = *reinterpret_cast<const uint4*>(qh + (size_t)pr * D + ks * 32 + 8 * gq);
+      qb[rt][ks] = *reinterpret_cast<const bf16x8*>(qh + (size_t)pr * D + ks * 32 + 8 * gq);
   }
-  // keys 0 .. min(n, p0 + 32) - 1 in tiles of 32
-  const int kend = min(n, p0 + kH2oTQ);
+  // keys 0 .. min(n, p0 + TQ) - 1 in tiles of kH2oKT; a tile needs the
+  // causal test only where it reaches past the block's first position
+  const int kend = min(n, p0 + TQ);
   const int ntiles = (kend + kH2oKT - 1) / kH2oKT;
-  uint4 kr[PER];
-  auto load = [&](int t) {
+  static_assert(CH % kH2oTh == 0, "whole key tiles per block");
+  bf16x8 kr[PER];
+#define H2O_LOAD_K(T)                                                                     \
+  _Pragma("unroll") for (int k = 0; k < PER; ++k) {                                       \
+    const int e = tid + k * kH2oTh;                                                       \
+    const int key = min((T) * kH2oKT + e / (D / 8), n - 1), ch = e % (D / 8);           \
+    kr[k] = *reinterpret_cast<const bf16x8*>(ku + (size_t)key * D + ch * 8);              \
+  }
+  float mref[RT];
+  double srun[RT];
 #pragma unroll
-    for (int k = 0; k < PER; ++k) {
-      const int e = min(tid + k * NTH, CH - 1);
-      const int key = min(t * kH2oKT + e / (D / 8), n - 1), ch = e % (D / 8);
-      kr[k] = *reinterpret_cast<const uint4*>(ku + (size_t)key * D + ch * 8);
-    }
-  };
-  auto store = [&](u16* dst) {
-#pragma unroll
-    for (int k = 0; k < PER; ++k) {
-      const int e = tid + k * NTH;
-      if (e < CH) *reinterpret_cast<uint4*>(dst + (e / (D / 8)) * KS + (e % (D / 8)) * 8) = kr[k];
-    }
-  };
-  float mref[2] = {-__builtin_huge_valf(), -__builtin_huge_valf()};
-  double srun[2] = {0.0, 0.0};
-  load(0);
+  for (int rt = 0; rt < RT; ++rt) {
+    mref[rt] = NINF;
+    srun[rt] = 0.0;
+  }
+  H2O_LOAD_K(0)
   for (int t = 0; t < ntiles; ++t) {
     u16* cur = kt_s[t & 1];
-    store(cur);
-    __syncthreads();
-    if (t + 1 < ntiles) load(t + 1);
-    float tv[2][2][4];   // [rt][kt][i]: key 32t + 16kt + 4gq + i, row 16rt + l16
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt) {
-      uint4 kf[D / 32];
+    for (int k = 0; k < PER; ++k) {
+      const int e = tid + k * kH2oTh;
+      *reinterpret_cast<bf16x8*>(cur + (e / (D / 8)) * KS + (e % (D / 8)) * 8) = kr[k];
+    }
+    __syncthreads();
+    H2O_LOAD_K(t + 1)   // (past the last tile: clamped rows, never stored)
+    const bool edge = (t + 1) * kH2oKT - 1 > pw0 || (t + 1) * kH2oKT > n;   // wave-uniform
+    // tv[rt][kt][i]: key 64t + 16kt + 4gq + i, row 16rt + l16
+    float tv[RT][KT][4];
+#pragma unroll
+    for (int kt = 0; kt < KT; ++kt) {
+      bf16x8 kf[D / 32];
 #pragma unroll
       for (int ks = 0; ks < D / 32; ++ks)
-        kf[ks] = *reinterpret_cast<const uint4*>(cur + (16 * kt + l16) * KS + ks * 32 + 8 * gq);
+        kf[ks] = *reinterpret_cast<const bf16x8*>(cur + (16 * kt + l16) * KS + ks * 32 + 8 * gq);
 #pragma unroll
-      for (int rt = 0; rt < 2; ++rt) {
+      for (int rt = 0; rt < RT; ++rt) {
         f32x4 acc = zero4();
 #pragma unroll
-        for (int ks = 0; ks < D / 32; ++ks) acc = mfma_bf16(as_bf16x8(kf[ks]), as_bf16x8(qb[rt][ks]), acc);
+        for (int ks = 0; ks < D / 32; ++ks) acc = mfma_bf16(kf[ks], qb[rt][ks], acc);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int key = t * kH2oKT + 16 * kt + 4 * gq + i;
-          tv[rt][kt][i] = (key <= pos[rt] && key < n) ? acc[i] * scale_log2 : -__builtin_huge_valf();
+        for (int i = 0; i < 4; ++i) tv[rt][kt][i] = acc[i] * scale_log2;
+      }
+    }
+    if (edge) {
+#pragma unroll
+      for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+        for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int key = t * kH2oKT + 16 * kt + 4 * gq + i;
+            if (!(key <= pos[rt] && key < n)) tv[rt][kt][i] = NINF;
+          }
+    }
+    // per row tile: the tile's sum against the running reference (masked keys
+    // add nothing and never meet a -inf reference; only edge tiles have any)
+    auto accumulate = [&](auto edge_tag) {
+      constexpr bool EDGE = decltype(edge_tag)::value;
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+        auto tile_sum = [&](float ref) {
+          float a = 0.f;
+#pragma unroll
+          for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              if constexpr (EDGE)
+                a += tv[rt][kt][i] != NINF ? __builtin_amdgcn_exp2f(tv[rt][kt][i] - ref) : 0.f;
+              else
+                a += __builtin_amdgcn_exp2f(tv[rt][kt][i] - ref);
+            }
+          return a;
+        };
+        float a = tile_sum(mref[rt]);
+        // a new reference when the tile's sum leaves [0, 2^64] (also taken on
+        // the lane's first visible key, while the reference is still -inf)
+        if (!(a <= 0x1p64f)) {
+          float mx = NINF;
+#pragma unroll
+          for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) mx = fmaxf(mx, tv[rt][kt][i]);
+          const float ref = ceilf(mx);   // finite: a was not 0, so a key is visible
+          srun[rt] = mref[rt] == NINF ? 0.0 : ldexp(srun[rt], (int)(mref[rt] - ref));
+          mref[rt] = ref;
+          a = tile_sum(ref);
         }
+        srun[rt] += (double)a;
       }
-    }
-    constexpr float NINF = -__builtin_huge_valf();
-#pragma unroll
-    for (int rt = 0; rt < 2; ++rt) {
-      // masked keys add nothing (and never meet a -inf reference)
-      float a = 0.f;
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          a += tv[rt][kt][i] != NINF ? __builtin_amdgcn_exp2f(tv[rt][kt][i] - mref[rt]) : 0.f;
-      // a new reference when the tile's sum leaves [0, 2^64] (also taken on the
-      // lane's first visible key, while the reference is still -inf)
-      if (!(a <= 0x1p64f)) {
-        float mx = NINF;
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) mx = fmaxf(mx, tv[rt][kt][i]);
-        const float ref = ceilf(mx);   // finite: a was not 0, so a key is visible
-        srun[rt] = mref[rt] == NINF ? 0.0 : ldexp(srun[rt], (int)(mref[rt] - ref));
-        mref[rt] = ref;
-        a = 0.f;
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            a += tv[rt][kt][i] != NINF ? __builtin_amdgcn_exp2f(tv[rt][kt][i] - ref) : 0.f;
-      }
-      srun[rt] += (double)a;
-    }
+    };
+    if (edge)
+      accumulate(std::true_type{});
+    else
+      accumulate(std::false_type{});
     __syncthreads();   // the next store overwrites the other buffer only; this
                        // one is rewritten two tiles later
   }
   // merge the four lanes of each row (exact power-of-two rescales)
 #pragma unroll
-  for (int rt = 0; rt < 2; ++rt) {
+  for (int rt = 0; rt < RT; ++rt) {
     const float M = max_over_groups(mref[rt]);
-    const double part = mref[rt] == -__builtin_huge_valf() ? 0.0 : ldexp(srun[rt], (int)(mref[rt] - M));
+    const double part = mref[rt] == NINF ? 0.0 : ldexp(srun[rt], (int)(mref[rt] - M));
     const double tot = sum_over_groups(part);
     if (gq == 0 && pos[rt] < n)
-      lse2[((size_t)u * G + g) * n + pos[rt]] = (float)((double)M + log2(tot));
+      lse2[((size_t)u * G + head) * n + pos[rt]] = (float)((double)M + log2(tot));
   }
+#undef H2O_LOAD_K
 }
 
 // --------------------------------------------------------- column sums ----
 template <int D, int G>
-__global__ __launch_bounds__(kH2oColWaves * 64) void h2o_colsum_kernel(
+__global__ __launch_bounds__(kH2oTh) void h2o_colsum_kernel(
     const u16* __restrict__ q_all, const u16* __restrict__ K, const float* __restrict__ lse2,
     int n, int P, float scale_log2, float* __restrict__ scores) {
-  constexpr int QS = D + 8;                  // LDS row stride (bf16) of Q rows
-  constexpr int NR = G * kH2oTQ;             // rows of a query tile (head-major)
-  constexpr int NTH = kH2oColWaves * 64;
-  constexpr int CH = NR * D / 8;             // 16-byte chunks of a query tile
-  constexpr int PER = (CH + NTH - 1) / NTH;
+  constexpr int TQ = kH2oQRows / G;         // positions per query tile
+  constexpr int QS = D + 8;                 // LDS row stride (bf16) of Q rows
+  constexpr int NR = kH2oQRows;             // rows of a query tile (head-major)
+  constexpr int CH = NR * D / 8;            // 16-byte chunks of a query tile
+  constexpr int PER = (CH + kH2oTh - 1) / kH2oTh;
   __shared__ __attribute__((aligned(16))) u16 q_s[2][NR * QS];
   __shared__ float l_s[2][NR];
   const int u = blockIdx.y, k0 = blockIdx.x * kH2oColKeys, tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6, l16 = lane & 15, gq = lane >> 4;
+  const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int l16 = lane & 15, gq = lane >> 4;
   const u16* ku = K + (size_t)u * n * D;
   const u16* qu = q_all + (size_t)u * G * n * D;
   const float* lu = lse2 + (size_t)u * G * n;
 
   // this wave's 32 keys (two 16-key tiles) as A operands
   const int kb = k0 + 32 * wave;
-  uint4 kf[2][D / 32];
+  bf16x8 kf[2][D / 32];
 #pragma unroll
   for (int kt = 0; kt < 2; ++kt) {
     const int key = min(kb + 16 * kt + l16, n - 1);
 #pragma unroll
     for (int ks = 0; ks < D / 32; ++ks)
-      kf[kt][ks] = *reinterpret_cast<const uint4*>(ku + (size_t)key * D + ks * 32 + 8 * gq);
+      kf[kt][ks] = *reinterpret_cast<const bf16x8*>(ku + (size_t)key * D + ks * 32 + 8 * gq);
   }
   // query tiles at or after the block's first key
-  const int qt0 = k0 / kH2oTQ, qt1 = (n + kH2oTQ - 1) / kH2oTQ;
-  uint4 qr[PER];
+  const int qt0 = k0 / TQ, qt1 = (n + TQ - 1) / TQ;
+  static_assert(CH % kH2oTh == 0 && NR <= kH2oTh, "whole query tiles per block");
+  bf16x8 qr[PER];
   float lr = 0.f;
-  auto load = [&](int qt) {
-    const int p0 = qt * kH2oTQ;
-#pragma unroll
-    for (int k = 0; k < PER; ++k) {
-      const int e = min(tid + k * NTH, CH - 1);
-      const int row = e / (D / 8), ch = e % (D / 8);
-      const int hg = row / kH2oTQ, pos = min(p0 + row % kH2oTQ, n - 1);
-      qr[k] = *reinterpret_cast<const uint4*>(qu + ((size_t)hg * n + pos) * D + ch * 8);
-    }
-    if (tid < NR) {
-      const int hg = tid / kH2oTQ, pos = p0 + tid % kH2oTQ;
-      lr = pos < n ? lu[(size_t)hg * n + pos] : 0.f;
-    }
-  };
-  auto store = [&](int b) {
-#pragma unroll
-    for (int k = 0; k < PER; ++k) {
-      const int e = tid + k * NTH;
-      if (e < CH) *reinterpret_cast<uint4*>(&q_s[b][(e / (D / 8)) * QS + (e % (D / 8)) * 8]) = qr[k];
-    }
-    if (tid < NR) l_s[b][tid] = lr;
-  };
+#define H2O_LOAD_Q(QT)                                                                    \
+  {                                                                                       \
+    const int pl0 = (QT) * TQ;                                                            \
+    _Pragma("unroll") for (int k = 0; k < PER; ++k) {                                     \
+      const int e = tid + k * kH2oTh;                                                     \
+      const int row = e / (D / 8), ch = e % (D / 8);                                      \
+      const int hg = row / TQ, pos = min(pl0 + row % TQ, n - 1);                          \
+      qr[k] = *reinterpret_cast<const bf16x8*>(qu + ((size_t)hg * n + pos) * D + ch * 8);  \
+    }                                                                                     \
+    if (tid < NR) {                                                                       \
+      const int hg = tid / TQ, pos = pl0 + tid % TQ;                                      \
+      lr = pos < n ? lu[(size_t)hg * n + pos] : 0.f;                                      \
+    }                                                                                     \
+  }
   double col[2][4] = {{0.0, 0.0, 0.0, 0.0}, {0.0, 0.0, 0.0, 0.0}};
-  if (qt0 < qt1) load(qt0);
+  H2O_LOAD_Q(qt0)
   for (int qt = qt0; qt < qt1; ++qt) {
     const int b = (qt - qt0) & 1;
-    store(b);
-    __syncthreads();
-    if (qt + 1 < qt1) load(qt + 1);
-    const int p0 = qt * kH2oTQ;
-    float part[2][4] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
-    for (int rt = 0; rt < 2 * G; ++rt) {
-      // rows 16 rt .. : head rt / 2, positions p0 + 16 (rt % 2) + l16
-      uint4 qf[D / 32];
+    for (int k = 0; k < PER; ++k) {
+      const int e = tid + k * kH2oTh;
+      *reinterpret_cast<bf16x8*>(&q_s[b][(e / (D / 8)) * QS + (e % (D / 8)) * 8]) = qr[k];
+    }
+    if (tid < NR) l_s[b][tid] = lr;
+    __syncthreads();
+    H2O_LOAD_Q(qt + 1)   // (past the last tile: clamped rows, never stored)
+    const int p0 = qt * TQ;
+    // the causal test and the end of the prompt matter only on tiles that
+    // start before the wave's last key or run past n (wave-uniform)
+    const bool edge = p0 < kb + 31 || p0 + TQ > n;
+    float part[2][4] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+#pragma unroll 4
+    for (int rt = 0; rt < NR / 16; ++rt) {
+      // rows 16 rt .. : head 16 rt / TQ, positions p0 + (16 rt) % TQ + l16
+      bf16x8 qf[D / 32];
 #pragma unroll
       for (int ks = 0; ks < D / 32; ++ks)
-        qf[ks] = *reinterpret_cast<const uint4*>(&q_s[b][(16 * rt + l16) * QS + ks * 32 + 8 * gq]);
-      const int rpos = p0 + 16 * (rt & 1) + l16;
+        qf[ks] = *reinterpret_cast<const bf16x8*>(&q_s[b][(16 * rt + l16) * QS + ks * 32 + 8 * gq]);
+      const int rpos = p0 + (16 * rt) % TQ + l16;
       const float nl = -l_s[b][16 * rt + l16];
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt) {
         f32x4 acc = zero4();
 #pragma unroll
-        for (int ks = 0; ks < D / 32; ++ks) acc = mfma_bf16(as_bf16x8(kf[kt][ks]), as_bf16x8(qf[ks]), acc);
-        // lane: key kb + 16 kt + 4 gq + i, row (head rt / 2, position rpos)
+        for (int ks = 0; ks < D / 32; ++ks) acc = mfma_bf16(kf[kt][ks], qf[ks], acc);
+        // lane: key kb + 16 kt + 4 gq + i, row (head, position rpos)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int key = kb + 16 * kt + 4 * gq + i;
           const float x = __builtin_amdgcn_exp2f(fmaf(acc[i], scale_log2, nl));
-          part[kt][i] += (rpos < n && key <= rpos) ? x : 0.f;
+          if (edge) {
+            const int key = kb + 16 * kt + 4 * gq + i;
+            part[kt][i] += (rpos < n && key <= rpos) ? x : 0.f;
+          } else {
+            part[kt][i] += x;
+          }
         }
       }
     }
@@ -251,18 +294,20 @@ __global__ __launch_bounds__(kH2oColWaves * 64) void h2o_colsum_kernel(
       const int key = kb + 16 * kt + 4 * gq + i;
       if (l16 == 0 && key < P) scores[(size_t)u * P + key] = (float)v;
     }
+#undef H2O_LOAD_Q
 }
 
 template <int D, int G>
 hipError_t launch_h2o_t(const u16* q_all, const u16* K, int U, int n, int P, float* lse2,
                         float* scores, hipStream_t s) {
   const float scale_log2 = (float)(1.4426950408889634 / __builtin_sqrt((double)D));
-  hipLaunchKernelGGL((h2o_lse_kernel<D, G>), dim3((n + kH2oTQ - 1) / kH2oTQ, U), dim3(G * 64), 0,
-                     s, q_all, K, n, scale_log2, lse2);
+  constexpr int TQ = kH2oRows / G;
+  hipLaunchKernelGGL((h2o_lse_kernel<D, G>), dim3((n + TQ - 1) / TQ, U), dim3(kH2oTh), 0, s, q_all,
+                     K, n, scale_log2, lse2);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || P < 1) return e;
   hipLaunchKernelGGL((h2o_colsum_kernel<D, G>), dim3((P + kH2oColKeys - 1) / kH2oColKeys, U),
-                     dim3(kH2oColWaves * 64), 0, s, q_all, K, lse2, n, P, scale_log2, scores);
+                     dim3(kH2oTh), 0, s, q_all, K, lse2, n, P, scale_log2, scores);
   return hipGetLastError();
 }
 
