@@ -309,36 +309,43 @@ __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
     reinterpret_cast<float4*>(gram)[(size_t)u * (MP * MP / 4) + e] = o;
     *reinterpret_cast<float4*>(A + r * AS + c4) = o;
   };
-  if (MP == D && S1 <= 4 && S2 == 1 && S3 == 1) {
-    // the usual shapes (one retained split, at most four full-cache splits):
-    // every load of two elements of Y, X V0 and N in flight together
+  if (MP == D && S1 <= 4 && S2 <= 2 && S3 <= 2) {
+    // the usual shapes (at most two retained splits, at most four full-cache
+    // splits): every load of two elements of Y, X V0 and N in flight together
     constexpr int E = MP * D / 4;
     const float4* __restrict__ yp = reinterpret_cast<const float4*>(ypart) + (size_t)u * S1 * E;
     const float4* __restrict__ xp = reinterpret_cast<const float4*>(xvpart) + sp0 * E;
     const float4* __restrict__ np = reinterpret_cast<const float4*>(npart) + sp3 * E;
     for (int e0 = tid; e0 < E; e0 += 2 * NTH) {
       const int ee[2] = {e0, min(e0 + NTH, E - 1)};
-      float4 yv[4][2], xv[2], nv[2];
+      float4 yv[4][2], xv[2][2], nv[2][2];
 #pragma unroll
       for (int sp = 0; sp < 4; ++sp)
         if (sp < S1)
 #pragma unroll
           for (int h = 0; h < 2; ++h) yv[sp][h] = yp[(size_t)sp * E + ee[h]];
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        xv[h] = xp[ee[h]];
-        nv[h] = np[ee[h]];
-      }
+      for (int sp = 0; sp < 2; ++sp)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          if (sp < S2) xv[sp][h] = xp[(size_t)sp * E + ee[h]];
+          if (sp < S3) nv[sp][h] = np[(size_t)sp * E + ee[h]];
+        }
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const int e = e0 + h * NTH;
         if (e >= E) break;
-        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f), xa = acc, na = acc;
 #pragma unroll
         for (int sp = 0; sp < 4; ++sp)   // in split order
           if (sp < S1) add4(acc, yv[sp][h]);
-        put_r(e, acc, xv[h]);
-        put_n(e, nv[h]);
+#pragma unroll
+        for (int sp = 0; sp < 2; ++sp) {
+          if (sp < S2) add4(xa, xv[sp][h]);
+          if (sp < S3) add4(na, nv[sp][h]);
+        }
+        put_r(e, acc, xa);
+        put_n(e, na);
       }
     }
   } else {
