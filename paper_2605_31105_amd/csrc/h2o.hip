@@ -6,8 +6,8 @@
 // 0..i:
 //   s_j = sum_g sum_{i >= j} 2^(t_{g,i,j} - LSE2_{g,i}),  t = q . k log2(e) / sqrt(d).
 // This is the work of a prefill attention without P.V (O(n^2 d) per head),
-// done in two MFMA passes with no atomics, each with 8 waves of 64 rows or
-// 32 keys so that a tile staged in LDS feeds many MFMAs per barrier:
+// done in two MFMA passes with no atomics, each with 8 waves, so that a tile
+// staged in LDS feeds many MFMAs per barrier:
 //  * h2o_lse_kernel: a block takes 512 / G prompt positions of all G query
 //    heads (512 rows, head-major; wave w owns rows 64w .. 64w + 63, four
 //    16-row tiles as MFMA B operands in registers) and streams the key tiles
@@ -15,8 +15,10 @@
 //    an integer reference exponent and an fp64 sum of 2^(t - ref) (as the
 //    window's pass A does); the four lanes of a row merge at the end into
 //    LSE2 (log2 domain).  Blocks run latest positions first (most keys);
-//  * h2o_colsum_kernel: a block takes 256 prefix keys (wave w: keys
-//    32w .. 32w + 31 as A operands in registers) and streams the query tiles
+//  * h2o_colsum_kernel: a block takes 128 prefix keys (wave w: keys
+//    16w .. 16w + 15 as A operands in registers; more keys per block re-read
+//    the queries less but balance the causal triangle worse, measured slower)
+//    and streams the query tiles
 //    (256 / G positions of all heads) at or after its first key, with their
 //    LSE2, through LDS; P = 2^(t - LSE2) under the causal rule is summed per
 //    key, in fp32 within a query tile and in fp64 across tiles; a 16-lane
@@ -35,7 +37,8 @@ constexpr int kH2oWaves = 8;
 constexpr int kH2oTh = kH2oWaves * 64;
 constexpr int kH2oRows = 512;       // rows (positions x heads) of an LSE block
 constexpr int kH2oKT = 64;          // keys per streamed key tile (LSE pass)
-constexpr int kH2oColKeys = 32 * kH2oWaves;   // keys per column-sum block
+constexpr int kH2oColKT = 1;       // 16-key tiles per wave (column sums)
+constexpr int kH2oColKeys = 16 * kH2oColKT * kH2oWaves;   // keys per column-sum block
 constexpr int kH2oQRows = 256;      // rows (positions x heads) of a streamed query tile
 
 // ------------------------------------------------------------ row LSE ----
@@ -202,11 +205,12 @@ __global__ __launch_bounds__(kH2oTh) void h2o_colsum_kernel(
   const u16* qu = q_all + (size_t)u * G * n * D;
   const float* lu = lse2 + (size_t)u * G * n;
 
-  // this wave's 32 keys (two 16-key tiles) as A operands
-  const int kb = k0 + 32 * wave;
-  bf16x8 kf[2][D / 32];
+  // this wave's keys (kH2oColKT 16-key tiles) as A operands
+  constexpr int KT = kH2oColKT;
+  const int kb = k0 + 16 * KT * wave;
+  bf16x8 kf[KT][D / 32];
 #pragma unroll
-  for (int kt = 0; kt < 2; ++kt) {
+  for (int kt = 0; kt < KT; ++kt) {
     const int key = min(kb + 16 * kt + l16, n - 1);
 #pragma unroll
     for (int ks = 0; ks < D / 32; ++ks)
@@ -231,7 +235,11 @@ __global__ __launch_bounds__(kH2oTh) void h2o_colsum_kernel(
       lr = pos < n ? lu[(size_t)hg * n + pos] : 0.f;                                      \
     }                                                                                     \
   }
-  double col[2][4] = {{0.0, 0.0, 0.0, 0.0}, {0.0, 0.0, 0.0, 0.0}};
+  double col[KT][4];
+#pragma unroll
+  for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) col[kt][i] = 0.0;
   H2O_LOAD_Q(qt0)
   for (int qt = qt0; qt < qt1; ++qt) {
     const int b = (qt - qt0) & 1;
@@ -246,8 +254,12 @@ __global__ __launch_bounds__(kH2oTh) void h2o_colsum_kernel(
     const int p0 = qt * TQ;
     // the causal test and the end of the prompt matter only on tiles that
     // start before the wave's last key or run past n (wave-uniform)
-    const bool edge = p0 < kb + 31 || p0 + TQ > n;
-    float part[2][4] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+    const bool edge = p0 < kb + 16 * KT - 1 || p0 + TQ > n;
+    float part[KT][4];
+#pragma unroll
+    for (int kt = 0; kt < KT; ++kt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) part[kt][i] = 0.f;
 #pragma unroll 4
     for (int rt = 0; rt < NR / 16; ++rt) {
       // rows 16 rt .. : head 16 rt / TQ, positions p0 + (16 rt) % TQ + l16
@@ -258,7 +270,7 @@ __global__ __launch_bounds__(kH2oTh) void h2o_colsum_kernel(
       const int rpos = p0 + (16 * rt) % TQ + l16;
       const float nl = -l_s[b][16 * rt + l16];
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
+      for (int kt = 0; kt < KT; ++kt) {
         f32x4 acc = zero4();
 #pragma unroll
         for (int ks = 0; ks < D / 32; ++ks) acc = mfma_bf16(kf[kt][ks], qf[ks], acc);
@@ -276,14 +288,14 @@ __global__ __launch_bounds__(kH2oTh) void h2o_colsum_kernel(
       }
     }
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
+    for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
       for (int i = 0; i < 4; ++i) col[kt][i] += (double)part[kt][i];
     __syncthreads();   // the tile in buffer b is read before it is rewritten
   }
   // sum over the 16 lanes (rows) sharing each key, in fp64
 #pragma unroll
-  for (int kt = 0; kt < 2; ++kt)
+  for (int kt = 0; kt < KT; ++kt)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       double v = col[kt][i];
