@@ -89,6 +89,10 @@ int make_plan(const grkv_problem* prob, int64_t n, int32_t window, int32_t budge
     split_range(budget, want, 128, &p->S2, &p->chunk2);
     if (p->chunk2 > 8192) split_range(budget, ceil_div(budget, 8192), 128, &p->S2, &p->chunk2);
   }
+  // calls with few units split the solve's right-hand-side columns over up
+  // to d / 16 blocks per unit (one per compute unit at most)
+  p->csplit = 1;
+  if (p->fast_merge && (size_t)p->U * (p->d / 16) <= 256) p->csplit = p->d / 16;
   if (p->fast_merge) {
     p->S3 = p->S2;
     p->chunk3 = p->chunk2;
@@ -140,6 +144,7 @@ static void layout_plan(Plan* p, size_t slots, size_t splits2, size_t splits3, s
   p->zhi = take(U * d * mp * 2);
   p->zlo = take(U * d * mp * 2);
   p->stats_ws = take(U * 4 * sizeof(float));
+  p->zpart = take(U * kZParts * sizeof(double));
   p->rag_tab = take(tab);
   p->total = off;
 }
@@ -343,7 +348,7 @@ int run_compress(const Plan& p, const void* q_obs, const void* K, const void* V,
                           direct ? (pre2 ? F(p.mcomb) : F(p.mpart)) : nullptr, F(p.lse1_log2),
                           kRetainedBias, F(p.lse2_log2), F(p.y), F(p.resid), F(p.gram), F(p.z),
                           (uint16_t*)(ws + p.zhi), (uint16_t*)(ws + p.zlo), F(p.stats_ws),
-                          out->stats, s));
+                          out->stats, Dd(p.zpart), s));
     // units whose retained mass the pass above could not resolve against the
     // full-cache log-sum-exp: the whole value step again, against the
     // retained set's own row maxima (the other blocks return at once)
@@ -351,13 +356,13 @@ int run_compress(const Plan& p, const void* q_obs, const void* K, const void* V,
       GRKV_TRY(launch_range_fix(p, q_obs, out->k_out, V, out->idx, fixed, F(p.y),
                                 F(p.lse2_log2), F(p.resid), F(p.gram), F(p.z),
                                 (uint16_t*)(ws + p.zhi), (uint16_t*)(ws + p.zlo),
-                                F(p.stats_ws), out->stats, s));
+                                F(p.stats_ws), out->stats, Dd(p.zpart), s));
     GRKV_TRY(mark(GRKV_STAGE_SOLVE, 1));
     GRKV_STAGE(GRKV_STAGE_UPDATE,
                launch_update(p, q_obs, out->k_out, F(p.lse2_log2), fixed,
                              (const uint16_t*)(ws + p.zhi),
                              (const uint16_t*)(ws + p.zlo), F(p.stats_ws),
-                             V, out->idx, out->v_out, s));
+                             V, out->idx, out->v_out, Dd(p.zpart), out->stats, s));
   } else {
     // 256 stacked rows: blocked MFMA factorisation (block-packed in LDS);
     // otherwise the column-by-column one

@@ -50,6 +50,10 @@ struct Plan {
   // on the fast value-step path, where that pass produces the Gram partials)
   int S3, chunk3;
   bool fast_merge;
+  // blocks per unit of the fast solve (column tiles of Z split between them,
+  // each block factoring N itself): more than one only for calls with few
+  // units, where one block per unit leaves most of the GPU idle
+  int csplit;
   // ragged budgets (bf16 fast path): device tables, null for one budget.
   // p.c is then the largest budget, chunk2 the uniform split length of the
   // retained pass and upd_spb the slots per update block.
@@ -64,11 +68,16 @@ struct Plan {
   // workspace offsets (bytes)
   size_t pmax1, psum1, lse1, lse1_log2, ypart, y, colsum, pooled, fixed, v0c, redo;
   size_t pmax2, psum2, lse2, lse2_log2, xvpart, x, resid, npart, mpart, gram, z, zhi, zlo, stats_ws;
+  // [U][kZParts] double (csplit > 1): ||Z||^2 of each solve block's columns,
+  // and ||Y||^2 in the last entry
+  size_t zpart;
   // retained-pass partials summed over the splits (small calls only)
   size_t xvcomb, ncomb, mcomb;
   size_t rag_tab;   // ragged tables: RagUnit [U], then the two block-to-unit maps
   size_t total;
 };
+
+constexpr int kZParts = 16;   // solve blocks per unit at most, plus ||Y||^2 (entry 15)
 
 // Fills `plan`; returns GRKV_OK or the error the call must report.
 int make_plan(const grkv_problem* prob, int64_t n, int32_t window,
@@ -155,7 +164,7 @@ hipError_t launch_solve(const Plan& p, const float* ypart, int S1, int S2, const
                         const float* npart, const float* mpart, const float* lse1_log2,
                         float lse_bias, float* lse2_log2, float* y, float* resid,
                         float* gram, float* z, uint16_t* zhi, uint16_t* zlo,
-                        float* stats_ws, float* stats_user, hipStream_t s);
+                        float* stats_ws, float* stats_user, double* zpart, hipStream_t s);
 // Units the solve marked GRKV_UNIT_RANGE (a window row's retained mass below
 // what P against the full-cache LSE resolves): the value step again in one
 // block per unit, against the retained set's own row maxima, writing the
@@ -164,7 +173,8 @@ hipError_t launch_solve(const Plan& p, const float* ypart, int S1, int S2, const
 hipError_t launch_range_fix(const Plan& p, const void* q, const void* k0, const void* V,
                             const int32_t* idx, const uint8_t* fixed, const float* y,
                             float* lse2_log2, float* resid, float* gram, float* z, uint16_t* zhi,
-                            uint16_t* zlo, float* stats_ws, float* stats_user, hipStream_t s);
+                            uint16_t* zlo, float* stats_ws, float* stats_user, double* zpart,
+                            hipStream_t s);
 // X is recomputed from q_obs, K0 (k_out) and the retained log-sum-exp; V0
 // rows are read from V [U][n][d] through idx.
 // Slots per update block for budget c (blocks per unit = ceil(c / spb)).
@@ -173,7 +183,7 @@ hipError_t launch_update(const Plan& p, const void* q, const void* k0,
                          const float* lse_log2, const uint8_t* fixed,
                          const uint16_t* zhi, const uint16_t* zlo,
                          const float* stats_ws, const void* V, const int32_t* idx,
-                         float* v_out, hipStream_t s);
+                         float* v_out, const double* zpart, float* stats_user, hipStream_t s);
 
 // Generic value step (any dtype, mp up to 256): Cholesky in LDS; the update
 // adds X_G^T Z into v_out, which the gather filled with V0.

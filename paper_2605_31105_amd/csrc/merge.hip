@@ -205,7 +205,7 @@ __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
     const float* ypart, int S1, const float* xvpart, int S2, const float* npart, int S3,
     const float* mpart, const float* lse1_log2, float lse_bias, float* lse2_log2,
     float* y, float* resid, float* gram, float* z, u16* zhi, u16* zlo, float* stats_ws,
-    float* stats_user, int m, float lam, const RagUnit* rag) {
+    float* stats_user, int m, float lam, const RagUnit* rag, int csplit, double* zpart) {
   constexpr int NP = MP / 16;   // panels
   constexpr int NC = D / 16;    // 16-column tiles of the right-hand side
   constexpr int AS = MP + 4;    // LDS row strides (floats); 16-byte aligned rows
@@ -221,6 +221,12 @@ __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
 
   const int u = blockIdx.x, tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, l16 = lane & 15, g = lane >> 4;
+  // With csplit > 1 the csplit blocks of a unit each factor N and solve
+  // their share of the right-hand-side columns; block 0 writes y, resid,
+  // gram and the stats, each block the ||Z||^2 of its columns to zpart (the
+  // update forms D after from them).
+  const int cblk = blockIdx.y;
+  const bool lead = cblk == 0;
   // this unit's retained-pass partials: splits sp0 .. sp0 + S2 - 1 (with
   // ragged budgets a unit's own split count, indexed by flat block)
   size_t sp0 = (size_t)u * S2, sp3 = (size_t)u * S3;
@@ -288,8 +294,10 @@ __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
     const float im = inv_mass[r];
     float4 rv = make_float4(yy.x - im * xv.x, yy.y - im * xv.y, yy.z - im * xv.z, yy.w - im * xv.w);
     if (r >= m) yy = rv = make_float4(0.f, 0.f, 0.f, 0.f);
-    reinterpret_cast<float4*>(y)[(size_t)u * (MP * D / 4) + e] = yy;
-    reinterpret_cast<float4*>(resid)[(size_t)u * (MP * D / 4) + e] = rv;
+    if (lead) {
+      reinterpret_cast<float4*>(y)[(size_t)u * (MP * D / 4) + e] = yy;
+      reinterpret_cast<float4*>(resid)[(size_t)u * (MP * D / 4) + e] = rv;
+    }
     *reinterpret_cast<float4*>(B + r * BS + c4) = rv;
     sy += (double)yy.x * yy.x + (double)yy.y * yy.y + (double)yy.z * yy.z + (double)yy.w * yy.w;
     sr += (double)rv.x * rv.x + (double)rv.y * rv.y + (double)rv.z * rv.z + (double)rv.w * rv.w;
@@ -306,7 +314,7 @@ __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
       if (r == col) vv[k] += r < m ? lam : 1.f;
     }
     const float4 o = make_float4(vv[0], vv[1], vv[2], vv[3]);
-    reinterpret_cast<float4*>(gram)[(size_t)u * (MP * MP / 4) + e] = o;
+    if (lead) reinterpret_cast<float4*>(gram)[(size_t)u * (MP * MP / 4) + e] = o;
     *reinterpret_cast<float4*>(A + r * AS + c4) = o;
   };
   if (MP == D && S1 <= 4 && S2 <= 2 && S3 <= 2) {
@@ -441,8 +449,9 @@ __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
 
   // 3. forward and backward substitution, 16 right-hand-side columns per wave;
   // tile rows 16t + 4g + i, column c0 + l16 live in r[t][i]
-  for (int cb = wave; cb < NC; cb += kSolveWaves) {
-    const int c0 = cb * 16;
+  const int tpb = NC / csplit;   // column tiles of this block
+  for (int ct = wave; ct < tpb; ct += kSolveWaves) {
+    const int c0 = (cblk * tpb + ct) * 16;
     f32x4 r[NP];
 #pragma unroll
     for (int t = 0; t < NP; ++t)
@@ -530,7 +539,12 @@ __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
     const double dafter = ok ? (double)lam * lam * Z2 / dn : dbefore;
     const float st[4] = {(float)Y2, (float)dbefore, (float)dafter,
                          range_fail ? (float)GRKV_UNIT_RANGE : ok ? 0.f : (float)GRKV_UNIT_SINGULAR};
+    if (csplit > 1) {
+      zpart[(size_t)u * kZParts + cblk] = Z2;
+      if (lead) zpart[(size_t)u * kZParts + kZParts - 1] = Y2;
+    }
     for (int k = 0; k < 4; ++k) {
+      if (!lead || (csplit > 1 && k == 2)) continue;   // D after: formed by the update
       stats_ws[u * 4 + k] = st[k];
       if (stats_user) stats_user[u * 4 + k] = st[k];
     }
@@ -565,7 +579,8 @@ __global__ __launch_bounds__(kUpdWaves * 64) void update_kernel(
     const u16* q, const u16* k0, const float* lse_log2, const uint8_t* fixed, const u16* zhi,
     const u16* zlo, const float* stats_ws, const u16* V, const int32_t* idx, int64_t n,
     float* v_out, int m, int w, int c, int spb, int causal, float scale_log2, const RagUnit* rag,
-    const int32_t* upd_unit, const int32_t* upd_order) {
+    const int32_t* upd_unit, const int32_t* upd_order, const double* zpart, int csplit, float lam,
+    float* stats_ws_w, float* stats_user) {
   constexpr int QS = D + 8;    // LDS row stride (bf16) of Q rows
   constexpr int ZS = MP + 8;   // LDS row stride (bf16) of Z^T rows
   constexpr int DT = D / 16;   // output tiles per slot row
@@ -593,6 +608,16 @@ __global__ __launch_bounds__(kUpdWaves * 64) void update_kernel(
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, l16 = lane & 15, g = lane >> 4;
   const bool singular = stats_ws[u * 4 + 3] != 0.f;
+  if (csplit > 1 && blk == 0 && tid == 0) {
+    // D after = lambda^2 ||Z||^2 / ||Y||^2 from the solve blocks' column
+    // shares, summed in block order
+    double Z2 = 0.0;
+    for (int k = 0; k < csplit; ++k) Z2 += zpart[(size_t)u * kZParts + k];
+    const double Y2 = zpart[(size_t)u * kZParts + kZParts - 1], dn = Y2 > 0 ? Y2 : 1.0;
+    const float dafter = singular ? stats_ws[u * 4 + 1] : (float)((double)lam * lam * Z2 / dn);
+    stats_ws_w[u * 4 + 2] = dafter;
+    if (stats_user) stats_user[u * 4 + 2] = dafter;
+  }
   const int win0 = c - w;   // first window slot of the retained set
   const int s0 = blk * spb;
   const int s1 = min(c, s0 + spb);
@@ -772,10 +797,13 @@ hipError_t launch_solve_t(const Plan& p, const float* ypart, int S1, int S2, con
                           const float* npart, const float* mpart, const float* lse1_log2,
                           float lse_bias, float* lse2_log2, float* y, float* resid, float* gram,
                           float* z, u16* zhi, u16* zlo, float* stats_ws, float* stats_user,
-                          hipStream_t s) {
-  hipLaunchKernelGGL((solve_kernel<MP, D>), dim3(p.U), dim3(kSolveWaves * 64), 0, s, ypart, S1,
-                     xvpart, S2, npart, S2, mpart, lse1_log2, lse_bias, lse2_log2, y, resid,
-                     gram, z, zhi, zlo, stats_ws, stats_user, p.m, p.lam, p.rag);
+                          double* zpart, hipStream_t s) {
+  const int csplit = p.rag ? 1 : p.csplit;
+  if (csplit < 1 || csplit > kZParts - 1 || (D / 16) % csplit != 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((solve_kernel<MP, D>), dim3(p.U, csplit), dim3(kSolveWaves * 64), 0, s,
+                     ypart, S1, xvpart, S2, npart, S2, mpart, lse1_log2, lse_bias, lse2_log2, y,
+                     resid, gram, z, zhi, zlo, stats_ws, stats_user, p.m, p.lam, p.rag, csplit,
+                     zpart);
   return hipGetLastError();
 }
 
@@ -783,7 +811,8 @@ template <int MP, int D>
 hipError_t launch_update_t(const Plan& p, const void* q, const void* k0, const float* lse_log2,
                            const uint8_t* fixed, const u16* zhi, const u16* zlo,
                            const float* stats_ws, const u16* V, const int32_t* idx,
-                           float* v_out, hipStream_t s) {
+                           float* v_out, const double* zpart, float* stats_ws_w,
+                           float* stats_user, hipStream_t s) {
   int spb = p.rag ? p.upd_spb : update_slots_per_block(p, p.c);
   if (spb < 32 || spb > kUpdMaxSlots ||
       (p.rag && (!p.rag_upd_unit || !p.rag_upd_order || p.rag_upd_blocks < 1)))
@@ -798,7 +827,8 @@ hipError_t launch_update_t(const Plan& p, const void* q, const void* k0, const f
   hipLaunchKernelGGL((update_kernel<MP, D>), grid, dim3(kUpdWaves * 64), lds, s,
                      (const u16*)q, (const u16*)k0, lse_log2, fixed, zhi, zlo, stats_ws, V, idx,
                      p.n, v_out, p.m, p.w, p.c, spb, p.opt.causal_window ? 1 : 0, scale_log2,
-                     p.rag, p.rag_upd_unit, p.rag_upd_order);
+                     p.rag, p.rag_upd_unit, p.rag_upd_order, zpart, p.rag ? 1 : p.csplit, p.lam,
+                     stats_ws_w, stats_user);
   return hipGetLastError();
 }
 
@@ -837,12 +867,13 @@ hipError_t launch_solve(const Plan& p, const float* ypart, int S1, int S2, const
                         const float* npart,
                         const float* mpart, const float* lse1_log2, float lse_bias,
                         float* lse2_log2, float* y, float* resid, float* gram, float* z, u16* zhi,
-                        u16* zlo, float* stats_ws, float* stats_user, hipStream_t s) {
+                        u16* zlo, float* stats_ws, float* stats_user, double* zpart,
+                        hipStream_t s) {
 #define GRKV_SOLVE(MPV, DV)                                                                   \
   if (p.mp == MPV && p.d == DV)                                                               \
     return launch_solve_t<MPV, DV>(p, ypart, S1, S2, xvpart, npart, mpart, lse1_log2, lse_bias, \
                                    lse2_log2, y, resid, gram, z, zhi, zlo, stats_ws,            \
-                                   stats_user, s);
+                                   stats_user, zpart, s);
   GRKV_SOLVE(32, 64) GRKV_SOLVE(32, 128) GRKV_SOLVE(64, 64) GRKV_SOLVE(64, 128)
   GRKV_SOLVE(128, 64) GRKV_SOLVE(128, 128)
 #undef GRKV_SOLVE
@@ -852,11 +883,12 @@ hipError_t launch_solve(const Plan& p, const float* ypart, int S1, int S2, const
 hipError_t launch_update(const Plan& p, const void* q, const void* k0, const float* lse_log2,
                          const uint8_t* fixed, const u16* zhi, const u16* zlo,
                          const float* stats_ws, const void* V, const int32_t* idx, float* v_out,
-                         hipStream_t s) {
+                         const double* zpart, float* stats_user, hipStream_t s) {
 #define GRKV_UPD(MPV, DV)                                                                     \
   if (p.mp == MPV && p.d == DV)                                                               \
     return launch_update_t<MPV, DV>(p, q, k0, lse_log2, fixed, zhi, zlo, stats_ws,             \
-                                    (const u16*)V, idx, v_out, s);
+                                    (const u16*)V, idx, v_out, zpart,                          \
+                                    const_cast<float*>(stats_ws), stats_user, s);
   GRKV_UPD(32, 64) GRKV_UPD(32, 128) GRKV_UPD(64, 64) GRKV_UPD(64, 128)
   GRKV_UPD(128, 64) GRKV_UPD(128, 128)
 #undef GRKV_UPD

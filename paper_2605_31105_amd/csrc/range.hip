@@ -59,7 +59,7 @@ __global__ __launch_bounds__(kFixThreads) void range_fix_kernel(
     const u16* q, const u16* k0, const u16* V, const int32_t* idx, const uint8_t* fixed,
     const float* y, int64_t n, int m, int w, int c, int causal, float scale_log2, float lam,
     float* lse2_log2, float* resid, float* gram, float* z, u16* zhi, u16* zlo, float* stats_ws,
-    float* stats_user, const RagUnit* rag) {
+    float* stats_user, const RagUnit* rag, int csplit, double* zpart) {
   using L = FixLds<MP, D>;
   constexpr int TPR = L::TPR, JPT = L::JPT;
   constexpr int NXV = D / TPR;    // columns of X V0 per thread
@@ -278,6 +278,11 @@ __global__ __launch_bounds__(kFixThreads) void range_fix_kernel(
       stats_ws[u * 4 + k] = st[k];
       if (stats_user) stats_user[u * 4 + k] = st[k];
     }
+    // the update forms D after again from the solve blocks' shares of ||Z||^2
+    if (csplit > 1) {
+      for (int k = 0; k < csplit; ++k) zpart[(size_t)u * kZParts + k] = k == 0 ? Z2 : 0.0;
+      zpart[(size_t)u * kZParts + kZParts - 1] = Y2;
+    }
   }
 }
 
@@ -285,7 +290,8 @@ template <int MP, int D>
 hipError_t launch_range_fix_t(const Plan& p, const void* q, const void* k0, const void* V,
                               const int32_t* idx, const uint8_t* fixed, const float* y,
                               float* lse2_log2, float* resid, float* gram, float* z, u16* zhi,
-                              u16* zlo, float* stats_ws, float* stats_user, hipStream_t s) {
+                              u16* zlo, float* stats_ws, float* stats_user, double* zpart,
+                              hipStream_t s) {
   const size_t lds = FixLds<MP, D>::bytes;
   hipError_t e = hipFuncSetAttribute((const void*)range_fix_kernel<MP, D>,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -294,7 +300,7 @@ hipError_t launch_range_fix_t(const Plan& p, const void* q, const void* k0, cons
   hipLaunchKernelGGL((range_fix_kernel<MP, D>), dim3(p.U), dim3(kFixThreads), lds, s,
                      (const u16*)q, (const u16*)k0, (const u16*)V, idx, fixed, y, p.n, p.m, p.w,
                      p.c, p.opt.causal_window ? 1 : 0, scale_log2, p.lam, lse2_log2, resid, gram,
-                     z, zhi, zlo, stats_ws, stats_user, p.rag);
+                     z, zhi, zlo, stats_ws, stats_user, p.rag, p.rag ? 1 : p.csplit, zpart);
   return hipGetLastError();
 }
 
@@ -303,11 +309,12 @@ hipError_t launch_range_fix_t(const Plan& p, const void* q, const void* k0, cons
 hipError_t launch_range_fix(const Plan& p, const void* q, const void* k0, const void* V,
                             const int32_t* idx, const uint8_t* fixed, const float* y,
                             float* lse2_log2, float* resid, float* gram, float* z, uint16_t* zhi,
-                            uint16_t* zlo, float* stats_ws, float* stats_user, hipStream_t s) {
+                            uint16_t* zlo, float* stats_ws, float* stats_user, double* zpart,
+                            hipStream_t s) {
 #define GRKV_FIX(MPV, DV)                                                                     \
   if (p.mp == MPV && p.d == DV)                                                               \
     return launch_range_fix_t<MPV, DV>(p, q, k0, V, idx, fixed, y, lse2_log2, resid, gram, z, \
-                                       zhi, zlo, stats_ws, stats_user, s);
+                                       zhi, zlo, stats_ws, stats_user, zpart, s);
   GRKV_FIX(32, 64) GRKV_FIX(32, 128) GRKV_FIX(64, 64) GRKV_FIX(64, 128)
   GRKV_FIX(128, 64) GRKV_FIX(128, 128)
 #undef GRKV_FIX
