@@ -468,8 +468,8 @@ def path_bytes_per_unit(cfg):
 
 
 def other_configs(args, G, hip, stream, want_cpu):
-    """The other workloads of the benchmark spec, each timed as one call over all
-    of its units (the same measurement as the headline, at their sizes): the
+    """The other workloads, each timed as one call over all of its units (the
+    same measurement as the headline, at their sizes): the
     one-layer 32k cache at budgets 1024 and 2048, and the 4-layer 128k cache
     (window 64, so m = 256 stacked rows), with the oracle timed on a bounded
     sample of each."""

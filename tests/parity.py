@@ -11,7 +11,7 @@ import numpy as np
 import workloads as W
 from oracle import grkv_oracle as O
 
-# spec tolerances: merged values and the post-merge discrepancy
+# parity tolerances: merged values and the post-merge discrepancy (relative)
 V_TOL = 2e-3
 D_TOL = 2e-3
 
