@@ -366,14 +366,30 @@ int run_compress(const Plan& p, const void* q_obs, const void* K, const void* V,
   } else {
     // 256 stacked rows: blocked MFMA factorisation (block-packed in LDS);
     // otherwise the column-by-column one
-    if (solve_big_supported(p))
-      GRKV_STAGE(GRKV_STAGE_SOLVE, launch_solve_big(p, F(p.npart), F(p.y), F(p.resid),
-                                                    F(p.gram), F(p.z), F(p.stats_ws),
-                                                    out->stats, s));
-    else
+    if (solve_big_supported(p)) {
+      // the Gram partials summed over all units first (one wide launch, in
+      // split order: the solve's own sum, spread over the GPU), into gram,
+      // which the solve then reads and overwrites with N
+      const float* Np = F(p.npart);
+      int S3 = p.S3;
+      GRKV_TRY(mark(GRKV_STAGE_SOLVE, 0));
+      if (S3 > 1) {
+        const float* part[kCombineSegs] = {F(p.npart), nullptr, nullptr, nullptr};
+        float* const outs[kCombineSegs] = {F(p.gram), nullptr, nullptr, nullptr};
+        const size_t per[kCombineSegs] = {(size_t)p.mp * p.mp, 0, 0, 0};
+        const int Sc[kCombineSegs] = {p.S3, 0, 0, 0};
+        GRKV_TRY(launch_combine_parts(p.U, Sc, part, outs, per, s));
+        Np = F(p.gram);
+        S3 = 1;
+      }
+      GRKV_TRY(launch_solve_big(p, Np, S3, F(p.y), F(p.resid), F(p.gram), F(p.z), F(p.stats_ws),
+                                out->stats, s));
+      GRKV_TRY(mark(GRKV_STAGE_SOLVE, 1));
+    } else {
       GRKV_STAGE(GRKV_STAGE_SOLVE, launch_cholesky_solve(p, F(p.npart), F(p.y), F(p.resid),
                                                          F(p.gram), F(p.z), F(p.stats_ws),
                                                          out->stats, s));
+    }
     GRKV_STAGE(GRKV_STAGE_UPDATE,
                launch_update_gen(p, F(p.x), fixed, F(p.z), F(p.stats_ws), ws + p.v0c,
                                  out->v_out, s));

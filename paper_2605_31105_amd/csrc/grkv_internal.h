@@ -194,8 +194,10 @@ hipError_t launch_cholesky_solve(const Plan& p, const float* npart,
                                  float* stats_user, hipStream_t s);
 // The same solve for mp = 256 (G * w in (128, 256]) with d 64 or 128: blocked
 // MFMA factorisation of N held block-packed in LDS, one 8-wave block per unit.
+// npart holds S3 Gram partials per unit; it may be gram itself when S3 is 1
+// (each element is read before the same thread overwrites it with N).
 bool solve_big_supported(const Plan& p);
-hipError_t launch_solve_big(const Plan& p, const float* npart, const float* y,
+hipError_t launch_solve_big(const Plan& p, const float* npart, int S3, const float* y,
                             const float* resid, float* gram, float* z, float* stats_ws,
                             float* stats_user, hipStream_t s);
 // v_out = V0 + X_G^T Z over every retained slot from the stored X [U][mp][c],

@@ -42,6 +42,7 @@ namespace {
 constexpr int kKT = 32;   // retained keys per tile (the key orders below assume 32)
 constexpr int kKeyEarlyIters = 13;  // CG iterations run with the fewest splits
 constexpr int kKeyRingEarlyIters = 16;  // the same for the ring passes
+constexpr int kInitBatch = 8;           // key_init: elements a thread loads together
 
 // Position, inside a block of 32, of the index a lane holds as element j of an
 // MFMA operand when the operand comes from an MFMA result: elements
@@ -87,24 +88,40 @@ __global__ __launch_bounds__(256) void key_init_kernel(
   const int u = blockIdx.x, tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6, l16 = lane & 15, g = lane >> 4;
   const bool skip = stats_ws[u * 4 + 3] != 0.f;
-  // Z^T is [d][mp]: read along its rows (coalesced), store transposed
-  for (int e = tid; e < MP * D; e += 256) {
-    const int col = e / MP, row = e % MP;
-    Es[row * ES + col] = (!skip && row < m) ? lam_v * zt[(size_t)u * D * MP + e] : 0.f;
+  // Z^T is [d][mp]: read along its rows (coalesced), store transposed.  A
+  // thread loads kInitBatch elements before it uses them; every row of the
+  // [mp]-row arrays is read (in bounds) and rows past m are masked.
+  constexpr int NE = MP * D;
+  static_assert(NE % (256 * kInitBatch) == 0, "whole batches");
+  for (int e0 = tid; e0 < NE; e0 += 256 * kInitBatch) {
+    float zv[kInitBatch];
+#pragma unroll
+    for (int b = 0; b < kInitBatch; ++b) zv[b] = zt[(size_t)u * D * MP + e0 + 256 * b];
+#pragma unroll
+    for (int b = 0; b < kInitBatch; ++b) {
+      const int e = e0 + 256 * b, col = e / MP, row = e % MP;
+      Es[row * ES + col] = (!skip && row < m) ? lam_v * zv[b] : 0.f;
+    }
   }
   __syncthreads();
   double ee = 0;
-  for (int e = tid; e < MP * D; e += 256) {
-    const int row = e / D, col = e % D;
-    const size_t o = (size_t)u * MP * D + e;
-    const float E = Es[row * ES + col];
-    const float F = row < m ? y[o] - E : 0.f;
-    Fs[row * ES + col] = F;
-    Fm[o] = F;
-    alpha[o] = 0.f;
-    r[o] = E;
-    p[o] = E;
-    ee += (double)E * E;
+  for (int e0 = tid; e0 < NE; e0 += 256 * kInitBatch) {
+    float yv[kInitBatch];
+#pragma unroll
+    for (int b = 0; b < kInitBatch; ++b) yv[b] = y[(size_t)u * MP * D + e0 + 256 * b];
+#pragma unroll
+    for (int b = 0; b < kInitBatch; ++b) {
+      const int e = e0 + 256 * b, row = e / D, col = e % D;
+      const size_t o = (size_t)u * MP * D + e;
+      const float E = Es[row * ES + col];
+      const float F = row < m ? yv[b] - E : 0.f;
+      Fs[row * ES + col] = F;
+      Fm[o] = F;
+      alpha[o] = 0.f;
+      r[o] = E;
+      p[o] = E;
+      ee += (double)E * E;
+    }
   }
   __syncthreads();
   // s = rowdot(F, p) for the first direction p = E, summed over the columns
@@ -121,12 +138,17 @@ __global__ __launch_bounds__(256) void key_init_kernel(
     const int ta = t / (MP / 16), tb = t % (MP / 16);
     const int ra = ta * 16 + l16, rb = tb * 16 + l16;
     f32x4 acc = zero4();
+    // (rows past m read row m - 1 and are masked: no branches around the loads)
+    uint4 av[D / 32], bv[D / 32];
 #pragma unroll
     for (int ks = 0; ks < D / 32; ++ks) {
-      const uint4 a = ra < m ? *reinterpret_cast<const uint4*>(qu + (size_t)ra * D + ks * 32 + 8 * g)
-                             : make_uint4(0, 0, 0, 0);
-      const uint4 b = rb < m ? *reinterpret_cast<const uint4*>(qu + (size_t)rb * D + ks * 32 + 8 * g)
-                             : make_uint4(0, 0, 0, 0);
+      av[ks] = *reinterpret_cast<const uint4*>(qu + (size_t)min(ra, m - 1) * D + ks * 32 + 8 * g);
+      bv[ks] = *reinterpret_cast<const uint4*>(qu + (size_t)min(rb, m - 1) * D + ks * 32 + 8 * g);
+    }
+#pragma unroll
+    for (int ks = 0; ks < D / 32; ++ks) {
+      const uint4 a = ra < m ? av[ks] : make_uint4(0, 0, 0, 0);
+      const uint4 b = rb < m ? bv[ks] : make_uint4(0, 0, 0, 0);
       acc = mfma_bf16(as_bf16x8(a), as_bf16x8(b), acc);
     }
 #pragma unroll

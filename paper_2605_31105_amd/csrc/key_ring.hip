@@ -718,15 +718,20 @@ __global__ __launch_bounds__(256) void key_x_kernel(const u16* __restrict__ q,
   uint4 qb[2][kRD / 32];
   float nl[2];
   int vlim[2];
+  // (rows past m read row m - 1, in bounds, and are masked: loads without
+  // branches are in flight together)
 #pragma unroll
   for (int rt = 0; rt < 2; ++rt) {
     const int row = 32 * wave + 16 * rt + l16;
     const bool ok = row < m;
-    const u16* qr = q + ((size_t)u * m + row) * kRD;
+    const u16* qr = q + ((size_t)u * m + min(row, m - 1)) * kRD;
 #pragma unroll
-    for (int ks = 0; ks < kRD / 32; ++ks)
-      qb[rt][ks] = ok ? *reinterpret_cast<const uint4*>(qr + ks * 32 + 8 * g) : make_uint4(0, 0, 0, 0);
-    nl[rt] = ok ? -lse2[(size_t)u * kRMP + row] : -__builtin_huge_valf();
+    for (int ks = 0; ks < kRD / 32; ++ks) {
+      const uint4 v = *reinterpret_cast<const uint4*>(qr + ks * 32 + 8 * g);
+      qb[rt][ks] = ok ? v : make_uint4(0, 0, 0, 0);
+    }
+    const float l2 = lse2[(size_t)u * kRMP + row];   // row < kRMP: in bounds
+    nl[rt] = ok ? -l2 : -__builtin_huge_valf();
     // one past the last slot the row sees (the window is the last w slots)
     vlim[rt] = causal ? min(c, c - w + row % w + 1) : c;
   }
@@ -756,7 +761,8 @@ __global__ __launch_bounds__(256) void key_x_kernel(const u16* __restrict__ q,
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int key = tile0 + 16 * kt + 4 * g + i;
-        fx[i] = key >= c || fixed[(size_t)u * c + min(key, c - 1)] != 0;
+        const uint8_t f = fixed[(size_t)u * c + min(key, c - 1)];   // loaded without a branch
+        fx[i] = (key >= c) | (f != 0);
       }
 #pragma unroll
       for (int rt = 0; rt < 2; ++rt) {

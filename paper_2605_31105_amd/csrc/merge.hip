@@ -46,6 +46,7 @@ __global__ __launch_bounds__(WAVES * 64) void gram_kernel(const float* x, const 
     for (int bt = 0; bt < NT; ++bt) acc[rt][bt] = zero4();
 
   float4 rg[F4];
+  uint32_t fg[F4];   // the fixed flags of rg's four slots, one per byte
   auto load = [&](int tk) {
 #pragma unroll
     for (int i = 0; i < F4; ++i) {
@@ -62,6 +63,12 @@ __global__ __launch_bounds__(WAVES * 64) void gram_kernel(const float* x, const 
         v = make_float4(tmp[0], tmp[1], tmp[2], tmp[3]);
       }
       rg[i] = v;
+      // flags of slots past t1 read slot c - 1 (in bounds; those slots are
+      // masked by t1): loads without branches, in flight with the slab's
+      uint32_t f = 0;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) f |= (uint32_t)fu[min(t + q, c - 1)] << (8 * q);
+      fg[i] = f;
     }
   };
   if (t0 < t1) load(t0);
@@ -74,7 +81,7 @@ __global__ __launch_bounds__(WAVES * 64) void gram_kernel(const float* x, const 
       float v[4] = {rg[i].x, rg[i].y, rg[i].z, rg[i].w};
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const float xv = (t + q < t1 && !fu[t + q]) ? v[q] : 0.f;
+        const float xv = (t + q < t1 && ((fg[i] >> (8 * q)) & 0xffu) == 0) ? v[q] : 0.f;
         const __bf16 h = (__bf16)xv;
         const __bf16 l = (__bf16)(xv - (float)h);
         hi[r * RS + cc + q] = __builtin_bit_cast(u16, h);
@@ -246,13 +253,22 @@ __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
   for (int r = tid; r < MP; r += kSolveWaves * 64) {
     float inv = 1.f;
     if (mpart) {
+      // the full-cache LSE and the first four row masses loaded together
+      const float l1 = lse1_log2[(size_t)u * MP + r];
       float ms = 0.f;
-      for (int s2 = 0; s2 < S2; ++s2) ms += mpart[(sp0 + s2) * MP + r];
+      for (int s0 = 0; s0 < S2; s0 += 4) {
+        float mv[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) mv[k] = mpart[(sp0 + min(s0 + k, S2 - 1)) * MP + r];
+#pragma unroll
+        for (int k = 0; k < 4; ++k)   // in split order
+          if (s0 + k < S2) ms += mv[k];
+      }
       inv = 0.f;
       if (r < m) {
         if (ms >= 0x1p-60f && ms < __builtin_huge_valf()) {
           inv = 1.f / ms;
-          lse2_log2[(size_t)u * MP + r] = lse1_log2[(size_t)u * MP + r] - lse_bias + __log2f(ms);
+          lse2_log2[(size_t)u * MP + r] = l1 - lse_bias + __log2f(ms);
         } else {
           range_fail = 1;
           lse2_log2[(size_t)u * MP + r] = 0.f;
@@ -326,18 +342,19 @@ __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
     const float4* __restrict__ np = reinterpret_cast<const float4*>(npart) + sp3 * E;
     for (int e0 = tid; e0 < E; e0 += 2 * NTH) {
       const int ee[2] = {e0, min(e0 + NTH, E - 1)};
+      // splits past a count read that count's last split again (in bounds,
+      // not summed): loads without branches, all in flight together
       float4 yv[4][2], xv[2][2], nv[2][2];
 #pragma unroll
       for (int sp = 0; sp < 4; ++sp)
-        if (sp < S1)
 #pragma unroll
-          for (int h = 0; h < 2; ++h) yv[sp][h] = yp[(size_t)sp * E + ee[h]];
+        for (int h = 0; h < 2; ++h) yv[sp][h] = yp[(size_t)min(sp, S1 - 1) * E + ee[h]];
 #pragma unroll
       for (int sp = 0; sp < 2; ++sp)
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-          if (sp < S2) xv[sp][h] = xp[(size_t)sp * E + ee[h]];
-          if (sp < S3) nv[sp][h] = np[(size_t)sp * E + ee[h]];
+          xv[sp][h] = xp[(size_t)min(sp, S2 - 1) * E + ee[h]];
+          nv[sp][h] = np[(size_t)min(sp, S3 - 1) * E + ee[h]];
         }
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
@@ -622,38 +639,84 @@ __global__ __launch_bounds__(kUpdWaves * 64) void update_kernel(
   const int s0 = blk * spb;
   const int s1 = min(c, s0 + spb);
 
+  // Staging: every thread issues all of its loads (Q rows, Z^T hi/lo, -LSE,
+  // the slots' source rows and fixed flags) before its first LDS store, so
+  // that they are in flight together.  Q rows past m read row m - 1 (in
+  // bounds) and are stored as zeros.
+  constexpr int QE = MP * (D / 8), QB = (QE + NTH - 1) / NTH;
+  constexpr int ZE = D * (MP / 8), ZB = (ZE + NTH - 1) / NTH;
+  constexpr int TB = (kUpdMaxSlots + NTH - 1) / NTH;
+  const int ns = s1 - s0;
+  uint4 qv[QB], zvh[ZB], zvl[ZB];
+  float lv = 0.f;
+  int64_t iv[TB];
+  uint8_t fv[TB];
+  const u16* qu = q + (size_t)u * m * D;
+  const u16* zhu = zhi + (size_t)u * D * MP;
+  const u16* zlu = zlo + (size_t)u * D * MP;
   if (!singular) {
-    const u16* qu = q + (size_t)u * m * D;
-    for (int e = tid; e < MP * (D / 8); e += NTH) {
-      const int r = e / (D / 8), ch = e % (D / 8);
-      const uint4 v = r < m ? *reinterpret_cast<const uint4*>(qu + (size_t)r * D + ch * 8)
-                            : make_uint4(0, 0, 0, 0);
-      *reinterpret_cast<uint4*>(qs + r * QS + ch * 8) = v;
+#pragma unroll
+    for (int b = 0; b < QB; ++b) {
+      const int e = tid + b * NTH;
+      if (QE % NTH == 0 || e < QE) {
+        const int r = e / (D / 8), ch = e % (D / 8);
+        qv[b] = *reinterpret_cast<const uint4*>(qu + (size_t)min(r, m - 1) * D + ch * 8);
+      }
     }
-    const u16* zhu = zhi + (size_t)u * D * MP;
-    const u16* zlu = zlo + (size_t)u * D * MP;
+#pragma unroll
+    for (int b = 0; b < ZB; ++b) {
+      const int e = tid + b * NTH;
+      if (ZE % NTH == 0 || e < ZE) {
+        const int dd = e / (MP / 8), r0 = 8 * (e % (MP / 8));
+        zvh[b] = *reinterpret_cast<const uint4*>(zhu + (size_t)dd * MP + r0);
+        zvl[b] = *reinterpret_cast<const uint4*>(zlu + (size_t)dd * MP + r0);
+      }
+    }
+    if (tid < MP) lv = lse_log2[(size_t)u * MP + tid];
+  }
+#pragma unroll
+  for (int b = 0; b < TB; ++b) {   // (slots past ns read slot ns - 1: no branch)
+    const int t = min(tid + b * NTH, ns - 1);
+    fv[b] = fixed[slot0 + s0 + t];
+    iv[b] = idx[slot0 + s0 + t];
+  }
+  if (!singular) {
+#pragma unroll
+    for (int b = 0; b < QB; ++b) {
+      const int e = tid + b * NTH;
+      if (QE % NTH == 0 || e < QE) {
+        const int r = e / (D / 8), ch = e % (D / 8);
+        *reinterpret_cast<uint4*>(qs + r * QS + ch * 8) = r < m ? qv[b] : make_uint4(0, 0, 0, 0);
+      }
+    }
     // Z^T row dd goes to LDS row (dd mod DT) * 16 + dd / DT; within a row, Z
     // row r = 32rp + 16h + 4g + i sits at 32rp + 8g + 4h + i, the order in
     // which a lane of group g holds its eight X values (one 16-byte read)
-    for (int e = tid; e < D * (MP / 8); e += NTH) {
-      const int dd = e / (MP / 8), r0 = 8 * (e % (MP / 8));
-      const int row = (dd % DT) * 16 + dd / DT;
-      const int rp = r0 >> 5, h = (r0 >> 4) & 1, g0 = (r0 >> 2) & 3;   // rows r0..r0+7: groups g0, g0+1
-      const int p0 = row * ZS + 32 * rp + 8 * g0 + 4 * h, p1 = p0 + 8;
-      const uint4 vh = *reinterpret_cast<const uint4*>(zhu + (size_t)dd * MP + r0);
-      const uint4 vl = *reinterpret_cast<const uint4*>(zlu + (size_t)dd * MP + r0);
-      *reinterpret_cast<uint2*>(zh + p0) = make_uint2(vh.x, vh.y);
-      *reinterpret_cast<uint2*>(zh + p1) = make_uint2(vh.z, vh.w);
-      *reinterpret_cast<uint2*>(zl + p0) = make_uint2(vl.x, vl.y);
-      *reinterpret_cast<uint2*>(zl + p1) = make_uint2(vl.z, vl.w);
+#pragma unroll
+    for (int b = 0; b < ZB; ++b) {
+      const int e = tid + b * NTH;
+      if (ZE % NTH == 0 || e < ZE) {
+        const int dd = e / (MP / 8), r0 = 8 * (e % (MP / 8));
+        const int row = (dd % DT) * 16 + dd / DT;
+        const int rp = r0 >> 5, h = (r0 >> 4) & 1, g0 = (r0 >> 2) & 3;   // rows r0..r0+7: groups g0, g0+1
+        const int p0 = row * ZS + 32 * rp + 8 * g0 + 4 * h, p1 = p0 + 8;
+        *reinterpret_cast<uint2*>(zh + p0) = make_uint2(zvh[b].x, zvh[b].y);
+        *reinterpret_cast<uint2*>(zh + p1) = make_uint2(zvh[b].z, zvh[b].w);
+        *reinterpret_cast<uint2*>(zl + p0) = make_uint2(zvl[b].x, zvl[b].y);
+        *reinterpret_cast<uint2*>(zl + p1) = make_uint2(zvl[b].z, zvl[b].w);
+      }
     }
     // padding rows get -inf, hence probability zero
-    for (int r = tid; r < MP; r += NTH) nls[r] = r < m ? -lse_log2[(size_t)u * MP + r] : NEG_INF;
+    if (tid < MP) nls[tid] = tid < m ? -lv : NEG_INF;
   }
-  for (int t = tid; t < s1 - s0; t += NTH) {
-    fl[t] = fixed[slot0 + s0 + t];
-    const int64_t r = idx[slot0 + s0 + t];
-    ps[t] = (int32_t)(r < 0 ? 0 : r >= n ? n - 1 : r);   // in range by construction
+#pragma unroll
+  for (int b = 0; b < TB; ++b) {
+    const int t = tid + b * NTH;
+    if (t < ns) {
+      fl[t] = fv[b];
+      const int64_t r = iv[b];
+      ps[t] = (int32_t)(r < 0 ? 0 : r >= n ? n - 1 : r);   // in range by construction
+    }
   }
   __syncthreads();
 

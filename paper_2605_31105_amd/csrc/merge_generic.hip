@@ -136,9 +136,24 @@ __global__ __launch_bounds__(256) void update_add_kernel(const float* x, const u
   const int l16 = lane & 15, g = lane >> 4;
   const float* xu = x + (size_t)u * mp * c;
   const uint8_t* fu = fixed + (size_t)u * c;
-  for (int e = tid; e < mp * 64; e += blockDim.x) {
-    int r = e / 64, tt = e % 64, t = t0 + tt;
-    Xs[r * XS + tt] = (t < c && !fu[t]) ? xu[(size_t)r * c + t] : 0.f;
+  // X of the block's 64 slots to LDS, masked by the fixed flags; a thread
+  // loads four elements and their flags before it stores them (slots past c
+  // read slot c - 1, in bounds, and store zero).  mp is a multiple of 32, so
+  // the mp x 64 elements are whole batches of 4 x 256.
+  for (int e0 = tid; e0 < mp * 64; e0 += 4 * 256) {
+    float xv[4];
+    uint8_t fv[4];
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int e = e0 + 256 * b, r = e / 64, t = min(t0 + e % 64, c - 1);
+      xv[b] = xu[(size_t)r * c + t];
+      fv[b] = fu[t];
+    }
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int e = e0 + 256 * b, r = e / 64, tt = e % 64;
+      Xs[r * XS + tt] = (t0 + tt < c && !fv[b]) ? xv[b] : 0.f;
+    }
   }
   __syncthreads();
   const float* zu = z + (size_t)u * D * mp;
@@ -166,13 +181,32 @@ __global__ __launch_bounds__(256) void update_add_kernel(const float* x, const u
       acc[dt] = mfma_bf16(alo, bhi, acc[dt]);
     }
   }
+  // v_out += dV at the free slots: flags and old values loaded first (slots
+  // past c read slot c - 1 and are not written)
+  bool upd[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int t = t0 + wave * 16 + 4 * g + i;
+    const uint8_t f = fu[min(t, c - 1)];
+    upd[i] = t < c && !f;
+  }
+  float vo[8][4];
 #pragma unroll
   for (int dt = 0; dt < 8; ++dt) {
     if (dt >= ndt) break;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      int t = t0 + wave * 16 + 4 * g + i;
-      if (t < c && !fu[t]) v_out[((size_t)u * c + t) * D + dt * 16 + l16] += acc[dt][i];
+      const int t = min(t0 + wave * 16 + 4 * g + i, c - 1);
+      vo[dt][i] = v_out[((size_t)u * c + t) * D + dt * 16 + l16];
+    }
+  }
+#pragma unroll
+  for (int dt = 0; dt < 8; ++dt) {
+    if (dt >= ndt) break;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int t = t0 + wave * 16 + 4 * g + i;
+      if (upd[i]) v_out[((size_t)u * c + t) * D + dt * 16 + l16] = vo[dt][i] + acc[dt][i];
     }
   }
 }
@@ -205,23 +239,37 @@ __global__ __launch_bounds__(kUpdGenWaves * 64) void update_gen_kernel(
   const uint8_t* fu = fixed + (size_t)u * c;
 
   if (!singular) {
+    // Z^T to bf16 hi/lo in LDS; a thread's loads of ZB elements are issued
+    // before it converts them
     const float* zu = z + (size_t)u * D * MP;
-    for (int e = tid; e < D * (MP / 4); e += NTH) {
-      const int dd = e / (MP / 4), r0 = 4 * (e % (MP / 4));
-      const float4 v = *reinterpret_cast<const float4*>(zu + (size_t)dd * MP + r0);
-      const float vv[4] = {v.x, v.y, v.z, v.w};
-      u16 hh[4], ll[4];
+    constexpr int ZE = D * (MP / 4), ZB = ZE / NTH < 8 ? ZE / NTH : 8;
+    static_assert(ZB >= 1 && ZE % (ZB * NTH) == 0, "whole batches");
+    for (int e0 = tid; e0 < ZE; e0 += ZB * NTH) {
+      float4 zb[ZB];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const __bf16 h = (__bf16)vv[i];
-        hh[i] = __builtin_bit_cast(u16, h);
-        ll[i] = __builtin_bit_cast(u16, (__bf16)(vv[i] - (float)h));
+      for (int b = 0; b < ZB; ++b) {
+        const int e = e0 + b * NTH;
+        zb[b] = *reinterpret_cast<const float4*>(zu + (size_t)(e / (MP / 4)) * MP + 4 * (e % (MP / 4)));
       }
-      const int row = (dd % DT) * 16 + dd / DT;
-      *reinterpret_cast<uint2*>(zh + row * ZS + r0) =
-          make_uint2(hh[0] | ((uint32_t)hh[1] << 16), hh[2] | ((uint32_t)hh[3] << 16));
-      *reinterpret_cast<uint2*>(zl + row * ZS + r0) =
-          make_uint2(ll[0] | ((uint32_t)ll[1] << 16), ll[2] | ((uint32_t)ll[3] << 16));
+#pragma unroll
+      for (int b = 0; b < ZB; ++b) {
+        const int e = e0 + b * NTH;
+        const int dd = e / (MP / 4), r0 = 4 * (e % (MP / 4));
+        const float4 v = zb[b];
+        const float vv[4] = {v.x, v.y, v.z, v.w};
+        u16 hh[4], ll[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const __bf16 h = (__bf16)vv[i];
+          hh[i] = __builtin_bit_cast(u16, h);
+          ll[i] = __builtin_bit_cast(u16, (__bf16)(vv[i] - (float)h));
+        }
+        const int row = (dd % DT) * 16 + dd / DT;
+        *reinterpret_cast<uint2*>(zh + row * ZS + r0) =
+            make_uint2(hh[0] | ((uint32_t)hh[1] << 16), hh[2] | ((uint32_t)hh[3] << 16));
+        *reinterpret_cast<uint2*>(zl + row * ZS + r0) =
+            make_uint2(ll[0] | ((uint32_t)ll[1] << 16), ll[2] | ((uint32_t)ll[3] << 16));
+      }
     }
   }
   __syncthreads();
@@ -238,20 +286,26 @@ __global__ __launch_bounds__(kUpdGenWaves * 64) void update_gen_kernel(
 #pragma unroll
     for (int tt = 0; tt < 2; ++tt) {
       const int t = tb + 16 * tt + l16;
-      keep[tt] = (t < c && !fu[t]) ? 1.f : 0.f;
+      const uint8_t f = fu[min(t, c - 1)];   // in bounds, without a branch
+      keep[tt] = (t < c && !f) ? 1.f : 0.f;
     }
 #pragma unroll 1
     for (int r0 = 0; r0 < MP; r0 += 32) {
-      bf16x8 ah[2], al[2];
+      // every row of X is read (rows past m are in bounds) and masked
+      // afterwards, so the sixteen loads are in flight together
+      float xl[2][8];
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt) {
         const int t = min(tb + 16 * tt + l16, c - 1);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) xl[tt][e] = xu[(size_t)(r0 + 8 * g + e) * c + t];
+      }
+      bf16x8 ah[2], al[2];
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt) {
         float xv[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int r = r0 + 8 * g + e;
-          xv[e] = r < m ? keep[tt] * xu[(size_t)r * c + t] : 0.f;
-        }
+        for (int e = 0; e < 8; ++e) xv[e] = r0 + 8 * g + e < m ? keep[tt] * xl[tt][e] : 0.f;
         split8(xv, ah[tt], al[tt]);
       }
 #pragma unroll
@@ -269,20 +323,33 @@ __global__ __launch_bounds__(kUpdGenWaves * 64) void update_gen_kernel(
     }
   }
   // lane holds dV[slot = tb + 16tt + 4g + i][dd = l16 * DT + dt]; V0 from the
-  // compact copy, every slot of the block written
+  // compact copy, every slot of the block written.  The V0 rows and fixed
+  // flags of all eight slots are loaded first (slots past c read slot c - 1,
+  // in bounds, and are not written).
+  T v0r[2][4][DT];
+  uint8_t flr[2][4];
+#pragma unroll
+  for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int tc = min(tb + 16 * tt + 4 * g + i, c - 1);
+      flr[tt][i] = fu[tc];
+      const T* src = v0c + ((size_t)u * c + tc) * D + l16 * DT;
+#pragma unroll
+      for (int k = 0; k < DT; ++k) v0r[tt][i][k] = src[k];
+    }
 #pragma unroll
   for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int t = tb + 16 * tt + 4 * g + i;
       if (t >= c) continue;
-      const bool upd = !singular && !fu[t];
-      const T* src = v0c + ((size_t)u * c + t) * D + l16 * DT;
+      const bool upd = !singular && !flr[tt][i];
       float v[DT];
 #pragma unroll
       for (int k = 0; k < DT; ++k) {
-        if constexpr (sizeof(T) == 2) v[k] = bf16_to_f32(src[k]);
-        else v[k] = (float)src[k];
+        if constexpr (sizeof(T) == 2) v[k] = bf16_to_f32(v0r[tt][i][k]);
+        else v[k] = (float)v0r[tt][i][k];
       }
       if (upd) {
 #pragma unroll

@@ -15,8 +15,11 @@
 // (16 columns per wave) for the forward and backward substitutions.
 //
 // Inputs are the generic value step's: the Gram partials npart [U][S3][mp][mp]
-// of the stored X, and Y and R = Y - X V0 combined [U][mp][D].  Outputs: the
-// full N (gram), Z^T (z [U][D][mp]) and the stats, as the generic solve.
+// of the stored X (the caller sums them over all units with one wide launch
+// first and passes that sum, S3 = 1: read by one block per unit, 2 MB of
+// partials take longer than the factorisation), and Y and R = Y - X V0
+// combined [U][mp][D].  Outputs: the full N (gram), Z^T (z [U][D][mp]) and
+// the stats, as the generic solve.
 #include "grkv_device.h"
 #include "grkv_internal.h"
 
@@ -28,6 +31,7 @@ constexpr int kBigWaves = 8;
 constexpr int kBigNP = kBigMP / 16;                        // panels
 constexpr int kBigBlocks = kBigNP * (kBigNP + 1) / 2;      // lower 16 x 16 blocks
 constexpr int kBigLS = 20;                                 // row stride of the inverted diagonal factors
+constexpr int kBigBatch = 8;                               // N elements loaded together per thread
 
 __device__ __forceinline__ int blk_index(int I, int J) { return I * (I + 1) / 2 + J; }
 
@@ -113,30 +117,41 @@ __global__ __launch_bounds__(kBigWaves * 64) void solve_big_kernel(
   if (tid == 0) fail = 0;
 
   // 1. N = sum of the Gram partials + lambda I (padding rows and columns:
-  // identity), to LDS (lower blocks) and to gram (all of it)
+  // identity), to LDS (lower blocks) and to gram (all of it).  A thread
+  // issues the loads of kBigBatch elements before it uses them (with one
+  // partial, the usual case, they are all in flight together).
   {
     constexpr int E = MP * MP / 4;
-    const float4* __restrict__ np = reinterpret_cast<const float4*>(npart) + (size_t)u * S3 * E;
-    float4* __restrict__ go = reinterpret_cast<float4*>(gram) + (size_t)u * E;
-    for (int e = tid; e < E; e += NTH) {
-      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-      for (int s = 0; s < S3; ++s) {
-        const float4 t = np[(size_t)s * E + e];
-        v.x += t.x; v.y += t.y; v.z += t.z; v.w += t.w;
-      }
-      const int r = e / (MP / 4), c0 = (e % (MP / 4)) * 4;
-      float vv[4] = {v.x, v.y, v.z, v.w};
+    static_assert(E % (kBigBatch * NTH) == 0, "whole batches");
+    const float4* np = reinterpret_cast<const float4*>(npart) + (size_t)u * S3 * E;
+    float4* go = reinterpret_cast<float4*>(gram) + (size_t)u * E;
+    for (int e0 = tid; e0 < E; e0 += kBigBatch * NTH) {
+      float4 vb[kBigBatch];
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const int c = c0 + k;
-        if (r >= m || c >= m) vv[k] = 0.f;
-        if (r == c) vv[k] += r < m ? lam : 1.f;
+      for (int b = 0; b < kBigBatch; ++b) vb[b] = np[e0 + b * NTH];
+      for (int s = 1; s < S3; ++s)   // in split order
+#pragma unroll
+        for (int b = 0; b < kBigBatch; ++b) {
+          const float4 t = np[(size_t)s * E + e0 + b * NTH];
+          vb[b].x += t.x; vb[b].y += t.y; vb[b].z += t.z; vb[b].w += t.w;
+        }
+#pragma unroll
+      for (int b = 0; b < kBigBatch; ++b) {
+        const int e = e0 + b * NTH;
+        const int r = e / (MP / 4), c0 = (e % (MP / 4)) * 4;
+        float vv[4] = {vb[b].x, vb[b].y, vb[b].z, vb[b].w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int c = c0 + k;
+          if (r >= m || c >= m) vv[k] = 0.f;
+          if (r == c) vv[k] += r < m ? lam : 1.f;
+        }
+        go[e] = make_float4(vv[0], vv[1], vv[2], vv[3]);
+        const int I = r >> 4, J = c0 >> 4;
+        if (J <= I)
+          *reinterpret_cast<float4*>(A + blk_index(I, J) * 256 + blk_chunk(r & 15, (c0 & 15) >> 2)) =
+              make_float4(vv[0], vv[1], vv[2], vv[3]);
       }
-      go[e] = make_float4(vv[0], vv[1], vv[2], vv[3]);
-      const int I = r >> 4, J = c0 >> 4;
-      if (J <= I)
-        *reinterpret_cast<float4*>(A + blk_index(I, J) * 256 + blk_chunk(r & 15, (c0 & 15) >> 2)) =
-            make_float4(vv[0], vv[1], vv[2], vv[3]);
     }
   }
   __syncthreads();
@@ -202,17 +217,24 @@ __global__ __launch_bounds__(kBigWaves * 64) void solve_big_kernel(
     const int c0 = cb * 16;
     const float* ru = resid + (size_t)u * MP * D;
     const float* yu = y + (size_t)u * MP * D;
+    // every row of the [MP][D] arrays is read (rows past m are in bounds)
+    // and masked afterwards: loads without branches stay in flight together.
+    // Row 16t + 4g + i of column c0 + l16 is the uniform row base of 16t + i
+    // plus one 32-bit lane offset.
+    const uint32_t lo = (uint32_t)(4 * g * D + c0 + l16);
     f32x4 r[NP];
 #pragma unroll
     for (int t = 0; t < NP; ++t)
 #pragma unroll
+      for (int i = 0; i < 4; ++i) r[t][i] = (ru + (16 * t + i) * D)[lo];
+#pragma unroll
+    for (int t = 0; t < NP; ++t)
+#pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int row = 16 * t + 4 * g + i;
-        const float rv = row < m ? ru[(size_t)row * D + c0 + l16] : 0.f;
-        const float yv = row < m ? yu[(size_t)row * D + c0 + l16] : 0.f;
+        const bool in = 16 * t + 4 * g + i < m;
+        const float rv = in ? r[t][i] : 0.f;
         r[t][i] = rv;
         sr += (double)rv * rv;
-        sy += (double)yv * yv;
       }
 #pragma unroll
     for (int p = 0; p < NP; ++p) {
@@ -257,6 +279,20 @@ __global__ __launch_bounds__(kBigWaves * 64) void solve_big_kernel(
       }
       *reinterpret_cast<float4*>(zr + 16 * t + 4 * g) = make_float4(zv[0], zv[1], zv[2], zv[3]);
     }
+    // ||Y||^2 of these columns (after the substitution, whose registers are
+    // free again), all 64 loads in flight before the sum
+    float yv[NP][4];
+#pragma unroll
+    for (int t = 0; t < NP; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) yv[t][i] = (yu + (16 * t + i) * D)[lo];
+#pragma unroll
+    for (int t = 0; t < NP; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float yy = 16 * t + 4 * g + i < m ? yv[t][i] : 0.f;
+        sy += (double)yy * yy;
+      }
   }
 
   // 4. stats: ||Y||^2, D before = ||R||^2 / ||Y||^2, D after = lambda^2 ||Z||^2 / ||Y||^2
@@ -286,15 +322,16 @@ __global__ __launch_bounds__(kBigWaves * 64) void solve_big_kernel(
 
 bool solve_big_supported(const Plan& p) { return p.mp == kBigMP && (p.d == 64 || p.d == 128); }
 
-hipError_t launch_solve_big(const Plan& p, const float* npart, const float* y, const float* resid,
-                            float* gram, float* z, float* stats_ws, float* stats_user,
-                            hipStream_t s) {
-  if (!solve_big_supported(p)) return hipErrorInvalidValue;
+hipError_t launch_solve_big(const Plan& p, const float* npart, int S3, const float* y,
+                            const float* resid, float* gram, float* z, float* stats_ws,
+                            float* stats_user, hipStream_t s) {
+  if (!solve_big_supported(p) || S3 < 1) return hipErrorInvalidValue;
+  if (npart == gram && S3 != 1) return hipErrorInvalidValue;
   if (p.d == 128)
-    hipLaunchKernelGGL(solve_big_kernel<128>, dim3(p.U), dim3(kBigWaves * 64), 0, s, npart, p.S3,
+    hipLaunchKernelGGL(solve_big_kernel<128>, dim3(p.U), dim3(kBigWaves * 64), 0, s, npart, S3,
                        y, resid, gram, z, stats_ws, stats_user, p.m, p.lam);
   else
-    hipLaunchKernelGGL(solve_big_kernel<64>, dim3(p.U), dim3(kBigWaves * 64), 0, s, npart, p.S3,
+    hipLaunchKernelGGL(solve_big_kernel<64>, dim3(p.U), dim3(kBigWaves * 64), 0, s, npart, S3,
                        y, resid, gram, z, stats_ws, stats_user, p.m, p.lam);
   return hipGetLastError();
 }

@@ -90,6 +90,7 @@ constexpr int kTileElems = 4096;   // elements of one tensor per tile
 constexpr float kFullPBias = 15.f;
 constexpr float kFullPUnscale = 0x1p-15f;
 constexpr int kRetMaxSlots = 4096;  // retained pass: key slots per block (the plan's split bound)
+constexpr int kPrologueSplits = 8;  // pass B: split partials combined from one batch of loads
 constexpr int kTileBytes = kTileElems * 2;
 
 // Sum of each of NV values (8 or 16) over the 16 lanes of a DPP row, as a
@@ -828,28 +829,54 @@ __attribute__((amdgpu_waves_per_eu(MODE == kModeLse ? 4 : 2))) void stream_kerne
     const int row = sm.rtile(rt) * 16 + l16;
     S.rowok[rt] = row < a.m;
     S.rowwin[rt] = a.causal ? row % a.w : 0x3fffffff;
-    const u16* q = a.q + ((size_t)u * a.m + row) * D;
+    // rows past m read row m - 1 (in bounds) and are masked: the loads are
+    // issued without branches, in flight together
+    const u16* q = a.q + ((size_t)u * a.m + min(row, a.m - 1)) * D;
 #pragma unroll
-    for (int ks = 0; ks < D / 32; ++ks)
-      S.qb[rt][ks] = S.rowok[rt] ? *reinterpret_cast<const uint4*>(q + ks * 32 + 8 * g)
-                                 : make_uint4(0, 0, 0, 0);
+    for (int ks = 0; ks < D / 32; ++ks) {
+      const uint4 v = *reinterpret_cast<const uint4*>(q + ks * 32 + 8 * g);
+      S.qb[rt][ks] = S.rowok[rt] ? v : make_uint4(0, 0, 0, 0);
+    }
     if (is_full<MODE>() && a.lse_ready) {
       S.lse[rt] = a.lse_log2_out[(size_t)u * a.mp + row] - kFullPBias;
     } else if constexpr (is_full<MODE>()) {
       // fixed-order combine of pass A's split partials: M = max of the
       // integer reference exponents, sum = sum_s psum_s 2^(ref_s - M) (exact
-      // powers of two), LSE (log2) = M + log2(sum)
+      // powers of two), LSE (log2) = M + log2(sum).  Up to kPrologueSplits
+      // splits have all their partials loaded at once (indices past S
+      // clamped, not used).
       float M = -INFINITY;
-      for (int sp = 0; sp < a.S; ++sp) M = fmaxf(M, a.pmax[((size_t)u * a.S + sp) * a.mp + row]);
       double l2 = 0.0;
-      if (M != -INFINITY) {
-        double sum = 0.0;
-        for (int sp = 0; sp < a.S; ++sp) {
-          const size_t o = ((size_t)u * a.S + sp) * a.mp + row;
-          const float ms = a.pmax[o];
-          if (ms != -INFINITY) sum += a.psum[o] * exp2((double)ms - (double)M);
+      if (a.S <= kPrologueSplits) {
+        float pm[kPrologueSplits];
+        double pz[kPrologueSplits];
+#pragma unroll
+        for (int k = 0; k < kPrologueSplits; ++k) {
+          const size_t o = ((size_t)u * a.S + min(k, a.S - 1)) * a.mp + row;
+          pm[k] = a.pmax[o];
+          pz[k] = a.psum[o];
         }
-        l2 = (double)M + log2(sum);
+#pragma unroll
+        for (int k = 0; k < kPrologueSplits; ++k)
+          if (k < a.S) M = fmaxf(M, pm[k]);
+        if (M != -INFINITY) {
+          double sum = 0.0;
+#pragma unroll
+          for (int k = 0; k < kPrologueSplits; ++k)
+            if (k < a.S && pm[k] != -INFINITY) sum += pz[k] * exp2((double)pm[k] - (double)M);
+          l2 = (double)M + log2(sum);
+        }
+      } else {
+        for (int sp = 0; sp < a.S; ++sp) M = fmaxf(M, a.pmax[((size_t)u * a.S + sp) * a.mp + row]);
+        if (M != -INFINITY) {
+          double sum = 0.0;
+          for (int sp = 0; sp < a.S; ++sp) {
+            const size_t o = ((size_t)u * a.S + sp) * a.mp + row;
+            const float ms = a.pmax[o];
+            if (ms != -INFINITY) sum += a.psum[o] * exp2((double)ms - (double)M);
+          }
+          l2 = (double)M + log2(sum);
+        }
       }
       S.lse[rt] = (float)l2 - kFullPBias;
       if (s == 0 && g == 0) {
