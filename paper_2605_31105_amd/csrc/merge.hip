@@ -156,9 +156,10 @@ __device__ __forceinline__ float row_bcast_rt(int j, float v) {
 }
 
 // Factor the 16x16 SPD block at `blk` (LDS, row stride AS) as L L^T and write
-// L^-1 (lower triangular, zero above) to `inv` (row stride 20).  Every 16-lane
-// row of the calling wave computes the same result; lane i holds row i.
-// Returns false when a pivot is not positive and finite.
+// L^-1 (lower triangular, zero above) to `inv` (row stride 20).  Called by a
+// whole wave: every 16-lane row factors the block (lane i holds row i), then
+// each forms and stores four of the sixteen columns of L^-1.  Returns false
+// when a pivot is not positive and finite.
 template <int AS>
 __device__ __forceinline__ bool factor_diag(const float* blk, float* inv, int lane) {
   const int i = lane & 15;
@@ -187,23 +188,27 @@ __device__ __forceinline__ bool factor_diag(const float* blk, float* inv, int la
   float dii = 0.f;
 #pragma unroll
   for (int k = 0; k < 16; ++k) dii = (i == k) ? invd[k] : dii;
-  float x[16];
+  // Each 16-lane group g of the wave forms columns 4g .. 4g+3 of M^-1 (all
+  // groups hold the same factor).  Row k of M^-1 is zero right of its
+  // diagonal, so the update of a column j > k adds zero and needs no
+  // predicate.
+  const int g4 = 4 * (lane >> 4);
+  float x[4];
 #pragma unroll
-  for (int j = 0; j < 16; ++j) x[j] = (j == i) ? 1.f : 0.f;
+  for (int cc = 0; cc < 4; ++cc) x[cc] = (g4 + cc == i) ? 1.f : 0.f;
 #pragma unroll
   for (int k = 0; k < 15; ++k) {
     const float mik = (i > k) ? a[k] * dii : 0.f;   // M_ik for the rows below k
 #pragma unroll
-    for (int j = 0; j <= k; ++j) x[j] = fmaf(-mik, row_bcast_rt<0>(k, x[j]), x[j]);
+    for (int cc = 0; cc < 4; ++cc) x[cc] = fmaf(-mik, row_bcast_rt<0>(k, x[cc]), x[cc]);
   }
+  float sc[4] = {0.f, 0.f, 0.f, 0.f};   // 1 / L_jj of this group's columns
 #pragma unroll
-  for (int j = 0; j < 16; ++j) x[j] *= invd[j];
-  if (lane < 16) {
+  for (int j = 0; j < 16; ++j)
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-      *reinterpret_cast<float4*>(inv + i * 20 + 4 * q) =
-          make_float4(x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]);
-  }
+    for (int cc = 0; cc < 4; ++cc) sc[cc] = (g4 + cc == j) ? invd[j] : sc[cc];
+  *reinterpret_cast<float4*>(inv + i * 20 + g4) =
+      make_float4(x[0] * sc[0], x[1] * sc[1], x[2] * sc[2], x[3] * sc[3]);
   return ok;
 }
 
@@ -333,46 +338,59 @@ __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
     if (lead) reinterpret_cast<float4*>(gram)[(size_t)u * (MP * MP / 4) + e] = o;
     *reinterpret_cast<float4*>(A + r * AS + c4) = o;
   };
-  if (MP == D && S1 <= 4 && S2 <= 2 && S3 <= 2) {
-    // the usual shapes (at most two retained splits, at most four full-cache
-    // splits): every load of two elements of Y, X V0 and N in flight together
+  // the usual shapes (at most two retained splits, at most four full-cache
+  // splits): every load of two elements of Y, X V0 and N in flight together.
+  // C1, C2, C3 splits are loaded (indices past S1, S2, S3 read the last
+  // split again, in bounds, and are not summed): without branches around the
+  // loads; the common split counts get their exact load counts.
+  auto combine_small = [&](auto c1, auto c2, auto c3) {
+    constexpr int C1 = decltype(c1)::value, C2 = decltype(c2)::value, C3 = decltype(c3)::value;
     constexpr int E = MP * D / 4;
     const float4* __restrict__ yp = reinterpret_cast<const float4*>(ypart) + (size_t)u * S1 * E;
     const float4* __restrict__ xp = reinterpret_cast<const float4*>(xvpart) + sp0 * E;
     const float4* __restrict__ np = reinterpret_cast<const float4*>(npart) + sp3 * E;
     for (int e0 = tid; e0 < E; e0 += 2 * NTH) {
       const int ee[2] = {e0, min(e0 + NTH, E - 1)};
-      // splits past a count read that count's last split again (in bounds,
-      // not summed): loads without branches, all in flight together
-      float4 yv[4][2], xv[2][2], nv[2][2];
+      float4 yv[C1][2], xv[C2][2], nv[C3][2];
 #pragma unroll
-      for (int sp = 0; sp < 4; ++sp)
+      for (int sp = 0; sp < C1; ++sp)
 #pragma unroll
         for (int h = 0; h < 2; ++h) yv[sp][h] = yp[(size_t)min(sp, S1 - 1) * E + ee[h]];
 #pragma unroll
-      for (int sp = 0; sp < 2; ++sp)
+      for (int h = 0; h < 2; ++h) {
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          xv[sp][h] = xp[(size_t)min(sp, S2 - 1) * E + ee[h]];
-          nv[sp][h] = np[(size_t)min(sp, S3 - 1) * E + ee[h]];
-        }
+        for (int sp = 0; sp < C2; ++sp) xv[sp][h] = xp[(size_t)min(sp, S2 - 1) * E + ee[h]];
+#pragma unroll
+        for (int sp = 0; sp < C3; ++sp) nv[sp][h] = np[(size_t)min(sp, S3 - 1) * E + ee[h]];
+      }
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const int e = e0 + h * NTH;
         if (e >= E) break;
         float4 acc = make_float4(0.f, 0.f, 0.f, 0.f), xa = acc, na = acc;
 #pragma unroll
-        for (int sp = 0; sp < 4; ++sp)   // in split order
+        for (int sp = 0; sp < C1; ++sp)   // in split order
           if (sp < S1) add4(acc, yv[sp][h]);
 #pragma unroll
-        for (int sp = 0; sp < 2; ++sp) {
+        for (int sp = 0; sp < C2; ++sp)
           if (sp < S2) add4(xa, xv[sp][h]);
+#pragma unroll
+        for (int sp = 0; sp < C3; ++sp)
           if (sp < S3) add4(na, nv[sp][h]);
-        }
         put_r(e, acc, xa);
         put_n(e, na);
       }
     }
+  };
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I4 = std::integral_constant<int, 4>;
+  if (MP == D && S1 == 4 && S2 == 1 && S3 == 1) {
+    combine_small(I4{}, I1{}, I1{});   // many units: four full-cache splits
+  } else if (MP == D && S1 == 1 && S2 == 1 && S3 == 1) {
+    combine_small(I1{}, I1{}, I1{});   // few units: partials summed beforehand
+  } else if (MP == D && S1 <= 4 && S2 <= 2 && S3 <= 2) {
+    combine_small(I4{}, I2{}, I2{});
   } else {
     {
       constexpr int E = MP * D / 4;

@@ -57,8 +57,9 @@ __device__ __forceinline__ float bcast_row_rt(int j, float v) {
 }
 
 // L L^T of the SPD diagonal block `blk`; L^-1 (lower, zero above) to `inv`
-// (row stride kBigLS).  Every 16-lane row of the wave computes the same
-// result (lane i holds row i).  False when a pivot is not positive and finite.
+// (row stride kBigLS).  Called by a whole wave: every 16-lane row factors the
+// block (lane i holds row i), then each forms and stores four of the sixteen
+// columns of L^-1.  False when a pivot is not positive and finite.
 __device__ __forceinline__ bool factor_diag_blk(const float* blk, float* inv, int lane) {
   const int i = lane & 15;
   float a[16];
@@ -82,23 +83,27 @@ __device__ __forceinline__ bool factor_diag_blk(const float* blk, float* inv, in
   float dii = 0.f;
 #pragma unroll
   for (int k = 0; k < 16; ++k) dii = (i == k) ? invd[k] : dii;
-  float x[16];
+  // Each 16-lane group g of the wave forms columns 4g .. 4g+3 of M^-1 (all
+  // groups hold the same factor).  Row k of M^-1 is zero right of its
+  // diagonal, so the update of a column j > k adds zero and needs no
+  // predicate.
+  const int g4 = 4 * (lane >> 4);
+  float x[4];
 #pragma unroll
-  for (int j = 0; j < 16; ++j) x[j] = (j == i) ? 1.f : 0.f;
+  for (int cc = 0; cc < 4; ++cc) x[cc] = (g4 + cc == i) ? 1.f : 0.f;
 #pragma unroll
   for (int k = 0; k < 15; ++k) {
     const float mik = (i > k) ? a[k] * dii : 0.f;
 #pragma unroll
-    for (int j = 0; j <= k; ++j) x[j] = fmaf(-mik, bcast_row_rt<0>(k, x[j]), x[j]);
+    for (int cc = 0; cc < 4; ++cc) x[cc] = fmaf(-mik, bcast_row_rt<0>(k, x[cc]), x[cc]);
   }
+  float sc[4] = {0.f, 0.f, 0.f, 0.f};   // 1 / L_jj of this group's columns
 #pragma unroll
-  for (int j = 0; j < 16; ++j) x[j] *= invd[j];
-  if (lane < 16) {
+  for (int j = 0; j < 16; ++j)
 #pragma unroll
-    for (int q = 0; q < 4; ++q)
-      *reinterpret_cast<float4*>(inv + i * kBigLS + 4 * q) =
-          make_float4(x[4 * q], x[4 * q + 1], x[4 * q + 2], x[4 * q + 3]);
-  }
+    for (int cc = 0; cc < 4; ++cc) sc[cc] = (g4 + cc == j) ? invd[j] : sc[cc];
+  *reinterpret_cast<float4*>(inv + i * kBigLS + g4) =
+      make_float4(x[0] * sc[0], x[1] * sc[1], x[2] * sc[2], x[3] * sc[3]);
   return ok;
 }
 
