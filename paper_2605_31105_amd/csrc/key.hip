@@ -43,6 +43,7 @@ constexpr int kKT = 32;   // retained keys per tile (the key orders below assume
 constexpr int kKeyEarlyIters = 13;  // CG iterations run with the fewest splits
 constexpr int kKeyRingEarlyIters = 16;  // the same for the ring passes
 constexpr int kInitBatch = 8;           // key_init: elements a thread loads together
+constexpr int kCgBatch = 4;             // key_cg: split partials a thread loads together
 
 // Position, inside a block of 32, of the index a lane holds as element j of an
 // MFMA operand when the operand comes from an MFMA result: elements
@@ -613,9 +614,18 @@ __global__ __launch_bounds__(1024) void key_rhs_kernel(
   __shared__ double red[16];
   const int u = blockIdx.x, tid = threadIdx.x;
   if ((int)cg[u * 4 + 3] == kKeySkipped) return;
+  // split partials in batches of kCgBatch (clamped, summed in split order),
+  // as in key_cg
   for (int i = tid; i < MP; i += NTH) {
     float h = 0.f;
-    for (int k = 0; k < S; ++k) h += hpart[((size_t)u * S + k) * MP + i];
+    for (int k0 = 0; k0 < S; k0 += kCgBatch) {
+      float hv[kCgBatch];
+#pragma unroll
+      for (int j = 0; j < kCgBatch; ++j) hv[j] = hpart[((size_t)u * S + min(k0 + j, S - 1)) * MP + i];
+#pragma unroll
+      for (int j = 0; j < kCgBatch; ++j)
+        if (k0 + j < S) h += hv[j];
+    }
     hsum[i] = h;
   }
   __syncthreads();
@@ -624,17 +634,32 @@ __global__ __launch_bounds__(1024) void key_rhs_kernel(
   const float4* __restrict__ F4 = reinterpret_cast<const float4*>(Fm) + base;
   float4* __restrict__ r4 = reinterpret_cast<float4*>(r) + base;
   float4* __restrict__ p4 = reinterpret_cast<float4*>(p) + base;
+  float4 rs[PER];   // r + the partials, in split order
+#pragma unroll
+  for (int k = 0; k < PER; ++k) rs[k] = r4[min(tid + k * NTH, E4 - 1)];
+  for (int s0 = 0; s0 < S; s0 += kCgBatch) {
+    float4 ov[kCgBatch][PER];
+#pragma unroll
+    for (int j = 0; j < kCgBatch; ++j)
+#pragma unroll
+      for (int k = 0; k < PER; ++k)
+        ov[j][k] = op4[(size_t)min(s0 + j, S - 1) * E4 + min(tid + k * NTH, E4 - 1)];
+#pragma unroll
+    for (int j = 0; j < kCgBatch; ++j)
+      if (s0 + j < S)
+#pragma unroll
+        for (int k = 0; k < PER; ++k) {
+          rs[k].x += ov[j][k].x; rs[k].y += ov[j][k].y;
+          rs[k].z += ov[j][k].z; rs[k].w += ov[j][k].w;
+        }
+  }
   double rr = 0;
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
     const int e = tid + k * NTH;
     float4 re = make_float4(0.f, 0.f, 0.f, 0.f), f = re;
     if (e < E4) {
-      float4 v = r4[e];
-      for (int sp = 0; sp < S; ++sp) {
-        const float4 o = op4[(size_t)sp * E4 + e];
-        v.x += o.x; v.y += o.y; v.z += o.z; v.w += o.w;
-      }
+      const float4 v = rs[k];
       f = F4[e];
       const float h = hsum[e / RW];
       re = make_float4(v.x - h * f.x, v.y - h * f.y, v.z - h * f.z, v.w - h * f.w);
@@ -673,9 +698,19 @@ __global__ __launch_bounds__(1024) void key_cg_kernel(
   __shared__ double red[16];
   const int u = blockIdx.x, tid = threadIdx.x;
   if ((int)cg[u * 4 + 3] != kKeyRunning) return;
+  // the split partials are loaded kCgBatch splits at a time (indices past S
+  // read split S - 1, in bounds, and are not summed) and summed in split
+  // order: the loads of a batch are in flight together
   for (int i = tid; i < MP; i += NTH) {
     float h = 0.f;
-    for (int k = 0; k < S; ++k) h += hpart[((size_t)u * S + k) * MP + i];
+    for (int k0 = 0; k0 < S; k0 += kCgBatch) {
+      float hv[kCgBatch];
+#pragma unroll
+      for (int j = 0; j < kCgBatch; ++j) hv[j] = hpart[((size_t)u * S + min(k0 + j, S - 1)) * MP + i];
+#pragma unroll
+      for (int j = 0; j < kCgBatch; ++j)
+        if (k0 + j < S) h += hv[j];
+    }
     hsum[i] = h;
   }
   __syncthreads();
@@ -686,6 +721,25 @@ __global__ __launch_bounds__(1024) void key_cg_kernel(
   float4* __restrict__ r4 = reinterpret_cast<float4*>(r) + base;
   float4* __restrict__ p4 = reinterpret_cast<float4*>(p) + base;
   const float4 z4 = make_float4(0.f, 0.f, 0.f, 0.f);
+  float4 osum[PER];
+#pragma unroll
+  for (int k = 0; k < PER; ++k) osum[k] = z4;
+  for (int s0 = 0; s0 < S; s0 += kCgBatch) {
+    float4 ov[kCgBatch][PER];
+#pragma unroll
+    for (int j = 0; j < kCgBatch; ++j)
+#pragma unroll
+      for (int k = 0; k < PER; ++k)
+        ov[j][k] = op4[(size_t)min(s0 + j, S - 1) * E4 + min(tid + k * NTH, E4 - 1)];
+#pragma unroll
+    for (int j = 0; j < kCgBatch; ++j)
+      if (s0 + j < S)
+#pragma unroll
+        for (int k = 0; k < PER; ++k) {
+          osum[k].x += ov[j][k].x; osum[k].y += ov[j][k].y;
+          osum[k].z += ov[j][k].z; osum[k].w += ov[j][k].w;
+        }
+  }
   float4 ap[PER], pp[PER], fv[PER];
   double pap = 0;
 #pragma unroll
@@ -693,11 +747,7 @@ __global__ __launch_bounds__(1024) void key_cg_kernel(
     const int e = tid + k * NTH;
     ap[k] = pp[k] = fv[k] = z4;
     if (e < E4) {
-      float4 v = z4;
-      for (int sp = 0; sp < S; ++sp) {
-        const float4 o = op4[(size_t)sp * E4 + e];
-        v.x += o.x; v.y += o.y; v.z += o.z; v.w += o.w;
-      }
+      float4 v = osum[k];
       const float4 pe = p4[e], f = F4[e];
       const float h = hsum[e / RW];
       v.x += lam_k * pe.x - h * f.x;
