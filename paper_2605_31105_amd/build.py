@@ -16,7 +16,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libgrkv.so")
-SOURCES = ["attention.hip", "stream.hip", "selection.hip", "merge.hip", "range.hip", "solve_big.hip", "merge_generic.hip", "key.hip", "key_ring.hip", "carrier.hip", "frontend.hip",
+SOURCES = ["attention.hip", "stream.hip", "selection.hip", "merge.hip", "solve_big.hip", "merge_generic.hip", "key.hip", "key_ring.hip", "carrier.hip", "frontend.hip",
            "h2o.hip", "noalloc.hip", "api.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -348,15 +348,7 @@ int run_compress(const Plan& p, const void* q_obs, const void* K, const void* V,
                           direct ? (pre2 ? F(p.mcomb) : F(p.mpart)) : nullptr, F(p.lse1_log2),
                           kRetainedBias, F(p.lse2_log2), F(p.y), F(p.resid), F(p.gram), F(p.z),
                           (uint16_t*)(ws + p.zhi), (uint16_t*)(ws + p.zlo), F(p.stats_ws),
-                          out->stats, Dd(p.zpart), s));
-    // units whose retained mass the pass above could not resolve against the
-    // full-cache log-sum-exp: the whole value step again, against the
-    // retained set's own row maxima (the other blocks return at once)
-    if (direct)
-      GRKV_TRY(launch_range_fix(p, q_obs, out->k_out, V, out->idx, fixed, F(p.y),
-                                F(p.lse2_log2), F(p.resid), F(p.gram), F(p.z),
-                                (uint16_t*)(ws + p.zhi), (uint16_t*)(ws + p.zlo),
-                                F(p.stats_ws), out->stats, Dd(p.zpart), s));
+                          out->stats, Dd(p.zpart), q_obs, out->k_out, V, out->idx, fixed, s));
     GRKV_TRY(mark(GRKV_STAGE_SOLVE, 1));
     GRKV_STAGE(GRKV_STAGE_UPDATE,
                launch_update(p, q_obs, out->k_out, F(p.lse2_log2), fixed,

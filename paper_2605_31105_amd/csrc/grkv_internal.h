@@ -160,21 +160,19 @@ bool merge_fast_supported(const Plan& p);
 // the retained LSE is written to lse2_log2), or null when X itself was used.
 // ypart holds S1 partials per unit (p.S1, or 1 when Y was combined already);
 // xvpart, npart and mpart S2 (p.S2, or 1), unless p.rag gives each unit's own.
+// Units it marks GRKV_UNIT_RANGE (with mpart: a window row's retained mass
+// below what P against the full-cache LSE resolves) get the value step again
+// in the same launch, by their first block, against the retained set's own
+// row maxima (range_fix.h), from q_obs, K0 (k0 = k_out), V through idx and
+// the fixed flags; it writes the retained LSE, R, N, Z^T and the stats where
+// the solve does.
 hipError_t launch_solve(const Plan& p, const float* ypart, int S1, int S2, const float* xvpart,
                         const float* npart, const float* mpart, const float* lse1_log2,
                         float lse_bias, float* lse2_log2, float* y, float* resid,
                         float* gram, float* z, uint16_t* zhi, uint16_t* zlo,
-                        float* stats_ws, float* stats_user, double* zpart, hipStream_t s);
-// Units the solve marked GRKV_UNIT_RANGE (a window row's retained mass below
-// what P against the full-cache LSE resolves): the value step again in one
-// block per unit, against the retained set's own row maxima, writing the
-// retained LSE, R, N, Z^T and the stats where the solve does.  Blocks of
-// other units return at once.
-hipError_t launch_range_fix(const Plan& p, const void* q, const void* k0, const void* V,
-                            const int32_t* idx, const uint8_t* fixed, const float* y,
-                            float* lse2_log2, float* resid, float* gram, float* z, uint16_t* zhi,
-                            uint16_t* zlo, float* stats_ws, float* stats_user, double* zpart,
-                            hipStream_t s);
+                        float* stats_ws, float* stats_user, double* zpart, const void* q,
+                        const void* k0, const void* V, const int32_t* idx,
+                        const uint8_t* fixed, hipStream_t s);
 // X is recomputed from q_obs, K0 (k_out) and the retained log-sum-exp; V0
 // rows are read from V [U][n][d] through idx.
 // Slots per update block for budget c (blocks per unit = ceil(c / spb)).

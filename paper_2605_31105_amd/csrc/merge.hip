@@ -12,6 +12,7 @@
 
 #include "grkv_device.h"
 #include "grkv_internal.h"
+#include "range_fix.h"
 
 namespace grkv {
 namespace {
@@ -217,15 +218,23 @@ __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
     const float* ypart, int S1, const float* xvpart, int S2, const float* npart, int S3,
     const float* mpart, const float* lse1_log2, float lse_bias, float* lse2_log2,
     float* y, float* resid, float* gram, float* z, u16* zhi, u16* zlo, float* stats_ws,
-    float* stats_user, int m, float lam, const RagUnit* rag, int csplit, double* zpart) {
+    float* stats_user, int m, float lam, const RagUnit* rag, int csplit, double* zpart,
+    const u16* q, const u16* k0, const u16* V, const int32_t* idx, const uint8_t* fixed,
+    int64_t n, int w, int c, int causal, float scale_log2) {
   constexpr int NP = MP / 16;   // panels
   constexpr int NC = D / 16;    // 16-column tiles of the right-hand side
   constexpr int AS = MP + 4;    // LDS row strides (floats); 16-byte aligned rows
   constexpr int BS = D + 4;
   constexpr int LS = 20;
   constexpr int NTH = kSolveWaves * 64;
-  __shared__ __attribute__((aligned(16))) float A[MP * AS];
-  __shared__ __attribute__((aligned(16))) float B[MP * BS];
+  // A (N, row stride AS) then B (right-hand sides, row stride BS); a unit
+  // marked GRKV_UNIT_RANGE reuses the same LDS for the range fix
+  constexpr size_t kAB = (size_t)MP * AS + (size_t)MP * BS;
+  constexpr size_t kSolveLds = kAB > FixLds<MP, D>::floats ? kAB : FixLds<MP, D>::floats;
+  static_assert(kSolveWaves * 64 == kFixThreads, "the range fix runs on the solve's block");
+  __shared__ __attribute__((aligned(16))) float AB[kSolveLds];
+  float* const A = AB;
+  float* const B = AB + MP * AS;
   __shared__ __attribute__((aligned(16))) float Li[NP * 16 * LS];
   __shared__ double red[3][kSolveWaves];
   __shared__ float inv_mass[MP];
@@ -283,6 +292,10 @@ __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
     inv_mass[r] = inv;
   }
   __syncthreads();
+  // a unit marked GRKV_UNIT_RANGE is solved again by its first block (at the
+  // end of this kernel), which writes every column of Z^T: the other blocks
+  // of the unit have nothing to add
+  if (range_fail && !lead) return;   // (LDS flag after the barrier: block-uniform)
 
   // 1. combine the partials; every thread issues the loads of two elements
   // and four splits at a time before it sums them (in split order), which
@@ -584,6 +597,12 @@ __global__ __launch_bounds__(kSolveWaves * 64) void solve_kernel(
       if (stats_user) stats_user[u * 4 + k] = st[k];
     }
   }
+  if (range_fail) {   // only the unit's first block gets here (block-uniform)
+    __syncthreads();   // every write above is done, A and B are free
+    range_fix_unit<MP, D>(AB, u, q, k0, V, idx, fixed, y, n, m, w, c, causal, scale_log2, lam,
+                          lse2_log2, resid, gram, z, zhi, zlo, stats_ws, stats_user, rag, csplit,
+                          zpart);
+  }
 }
 
 // ---------------------------------------------------------------- update ----
@@ -878,13 +897,18 @@ hipError_t launch_solve_t(const Plan& p, const float* ypart, int S1, int S2, con
                           const float* npart, const float* mpart, const float* lse1_log2,
                           float lse_bias, float* lse2_log2, float* y, float* resid, float* gram,
                           float* z, u16* zhi, u16* zlo, float* stats_ws, float* stats_user,
-                          double* zpart, hipStream_t s) {
+                          double* zpart, const void* q, const void* k0, const void* V,
+                          const int32_t* idx, const uint8_t* fixed, hipStream_t s) {
   const int csplit = p.rag ? 1 : p.csplit;
   if (csplit < 1 || csplit > kZParts - 1 || (D / 16) % csplit != 0) return hipErrorInvalidValue;
+  // the range fix (with mpart) reads q_obs, K0, V and the retained set
+  if (mpart && (!q || !k0 || !V || !idx || !fixed)) return hipErrorInvalidValue;
+  const float scale_log2 = (float)(1.4426950408889634 / __builtin_sqrt((double)D));
   hipLaunchKernelGGL((solve_kernel<MP, D>), dim3(p.U, csplit), dim3(kSolveWaves * 64), 0, s,
                      ypart, S1, xvpart, S2, npart, S2, mpart, lse1_log2, lse_bias, lse2_log2, y,
                      resid, gram, z, zhi, zlo, stats_ws, stats_user, p.m, p.lam, p.rag, csplit,
-                     zpart);
+                     zpart, (const u16*)q, (const u16*)k0, (const u16*)V, idx, fixed, p.n, p.w,
+                     p.c, p.opt.causal_window ? 1 : 0, scale_log2);
   return hipGetLastError();
 }
 
@@ -949,12 +973,13 @@ hipError_t launch_solve(const Plan& p, const float* ypart, int S1, int S2, const
                         const float* mpart, const float* lse1_log2, float lse_bias,
                         float* lse2_log2, float* y, float* resid, float* gram, float* z, u16* zhi,
                         u16* zlo, float* stats_ws, float* stats_user, double* zpart,
-                        hipStream_t s) {
+                        const void* q, const void* k0, const void* V, const int32_t* idx,
+                        const uint8_t* fixed, hipStream_t s) {
 #define GRKV_SOLVE(MPV, DV)                                                                   \
   if (p.mp == MPV && p.d == DV)                                                               \
     return launch_solve_t<MPV, DV>(p, ypart, S1, S2, xvpart, npart, mpart, lse1_log2, lse_bias, \
                                    lse2_log2, y, resid, gram, z, zhi, zlo, stats_ws,            \
-                                   stats_user, zpart, s);
+                                   stats_user, zpart, q, k0, V, idx, fixed, s);
   GRKV_SOLVE(32, 64) GRKV_SOLVE(32, 128) GRKV_SOLVE(64, 64) GRKV_SOLVE(64, 128)
   GRKV_SOLVE(128, 64) GRKV_SOLVE(128, 128)
 #undef GRKV_SOLVE

@@ -17,16 +17,19 @@
 // exactly where the solve writes them, so the update kernel that follows
 // forms V* = V0 + X_G^T Z as for every other unit.
 //
-// One block of 1024 threads per unit; a unit the solve did not mark leaves at
-// once, so in a call without such units the launch costs one flag read per
-// block.  The arithmetic is plain fp32 on the vector ALUs (products of bf16
-// inputs are exact in fp32), the Cholesky factorisation a right-looking
-// column sweep in LDS: this path trades speed for range.
+// Run by the solve kernel's first block of a marked unit, after that block's
+// own solve (the other blocks of the unit return early), so a call without
+// marked units pays nothing for it.  One block of 1024 threads; the LDS
+// scratch (FixLds<MP, D>::floats) is the solve's own, reused.  The
+// arithmetic is plain fp32 on the vector ALUs (products of bf16 inputs are
+// exact in fp32), the Cholesky factorisation a right-looking column sweep in
+// LDS: this path trades speed for range.
+#pragma once
+
 #include "grkv_device.h"
 #include "grkv_internal.h"
 
 namespace grkv {
-namespace {
 
 constexpr int kFixThreads = 1024;
 constexpr int kFixChunk = 32;   // retained keys per step
@@ -50,31 +53,32 @@ struct FixLds {
   static constexpr size_t a_off = 0;
   static constexpr size_t b_off = a_off + (size_t)MP * AS;
   static constexpr size_t solve_floats = b_off + (size_t)MP * BS;
-  static constexpr size_t bytes =
-      (stream_floats > solve_floats ? stream_floats : solve_floats) * sizeof(float);
+  static constexpr size_t floats = stream_floats > solve_floats ? stream_floats : solve_floats;
+  static constexpr size_t bytes = floats * sizeof(float);
 };
 
+// The value step of unit u (GRKV_UNIT_RANGE) against the retained row maxima,
+// by the whole calling block (kFixThreads threads); fsm: FixLds<MP, D>::floats
+// of LDS that no other code of the block uses meanwhile.
 template <int MP, int D>
-__global__ __launch_bounds__(kFixThreads) void range_fix_kernel(
-    const u16* q, const u16* k0, const u16* V, const int32_t* idx, const uint8_t* fixed,
-    const float* y, int64_t n, int m, int w, int c, int causal, float scale_log2, float lam,
-    float* lse2_log2, float* resid, float* gram, float* z, u16* zhi, u16* zlo, float* stats_ws,
-    float* stats_user, const RagUnit* rag, int csplit, double* zpart) {
+__device__ __forceinline__ void range_fix_unit(
+    float* fsm, int u, const u16* q, const u16* k0, const u16* V, const int32_t* idx,
+    const uint8_t* fixed, const float* y, int64_t n, int m, int w, int c, int causal,
+    float scale_log2, float lam, float* lse2_log2, float* resid, float* gram, float* z, u16* zhi,
+    u16* zlo, float* stats_ws, float* stats_user, const RagUnit* rag, int csplit, double* zpart) {
   using L = FixLds<MP, D>;
   constexpr int TPR = L::TPR, JPT = L::JPT;
   constexpr int NXV = D / TPR;    // columns of X V0 per thread
   constexpr int NN = MP / TPR;    // columns of N per thread
   static_assert(kFixThreads % MP == 0 && kFixChunk % TPR == 0, "thread mapping");
   static_assert(D % TPR == 0 && MP % TPR == 0, "thread mapping");
-  extern __shared__ __attribute__((aligned(16))) float fsm[];
   __shared__ float rowmax[MP], rowinv[MP];
   __shared__ int32_t kpos[kFixChunk];
   __shared__ float kfree[kFixChunk];
   __shared__ double red[3][kFixThreads / 64];
   __shared__ int fail;
 
-  const int u = blockIdx.x, tid = threadIdx.x;
-  if (stats_ws[u * 4 + 3] != (float)GRKV_UNIT_RANGE) return;   // block-uniform
+  const int tid = threadIdx.x;
   size_t slot0 = (size_t)u * c;
   if (rag) {
     slot0 = (size_t)rag[u].off;
@@ -284,41 +288,6 @@ __global__ __launch_bounds__(kFixThreads) void range_fix_kernel(
       zpart[(size_t)u * kZParts + kZParts - 1] = Y2;
     }
   }
-}
-
-template <int MP, int D>
-hipError_t launch_range_fix_t(const Plan& p, const void* q, const void* k0, const void* V,
-                              const int32_t* idx, const uint8_t* fixed, const float* y,
-                              float* lse2_log2, float* resid, float* gram, float* z, u16* zhi,
-                              u16* zlo, float* stats_ws, float* stats_user, double* zpart,
-                              hipStream_t s) {
-  const size_t lds = FixLds<MP, D>::bytes;
-  hipError_t e = hipFuncSetAttribute((const void*)range_fix_kernel<MP, D>,
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (e != hipSuccess) return e;
-  const float scale_log2 = (float)(1.4426950408889634 / __builtin_sqrt((double)D));
-  hipLaunchKernelGGL((range_fix_kernel<MP, D>), dim3(p.U), dim3(kFixThreads), lds, s,
-                     (const u16*)q, (const u16*)k0, (const u16*)V, idx, fixed, y, p.n, p.m, p.w,
-                     p.c, p.opt.causal_window ? 1 : 0, scale_log2, p.lam, lse2_log2, resid, gram,
-                     z, zhi, zlo, stats_ws, stats_user, p.rag, p.rag ? 1 : p.csplit, zpart);
-  return hipGetLastError();
-}
-
-}  // namespace
-
-hipError_t launch_range_fix(const Plan& p, const void* q, const void* k0, const void* V,
-                            const int32_t* idx, const uint8_t* fixed, const float* y,
-                            float* lse2_log2, float* resid, float* gram, float* z, uint16_t* zhi,
-                            uint16_t* zlo, float* stats_ws, float* stats_user, double* zpart,
-                            hipStream_t s) {
-#define GRKV_FIX(MPV, DV)                                                                     \
-  if (p.mp == MPV && p.d == DV)                                                               \
-    return launch_range_fix_t<MPV, DV>(p, q, k0, V, idx, fixed, y, lse2_log2, resid, gram, z, \
-                                       zhi, zlo, stats_ws, stats_user, zpart, s);
-  GRKV_FIX(32, 64) GRKV_FIX(32, 128) GRKV_FIX(64, 64) GRKV_FIX(64, 128)
-  GRKV_FIX(128, 64) GRKV_FIX(128, 128)
-#undef GRKV_FIX
-  return hipErrorInvalidValue;
 }
 
 }  // namespace grkv
