@@ -292,13 +292,17 @@ def _planted_far_key(cfg):
     return q, K, V
 
 
+@pytest.mark.parametrize("kv_heads", [2, 40], ids=["solve-column-split", "one-solve-block-per-unit"])
 @pytest.mark.parametrize("fix_window", [1, 0], ids=["window-fixed", "window-free"])
-def test_retained_mass_far_below_full_cache(fix_window):
+def test_retained_mass_far_below_full_cache(fix_window, kv_heads):
     # every retained key of every window row lies ~200 nats below an evicted
     # key: the retained pass against the full-cache LSE cannot resolve the
     # retained softmax, and the value step is redone against the retained
-    # set's own row maxima; the result must match the oracle like any other
-    cfg = W.config(2, layers=1, kv_heads=2, n=2048, budget=32)
+    # set's own row maxima; the result must match the oracle like any other.
+    # With 2 units the solve splits each unit's right-hand-side columns over
+    # several blocks (the first redoes the unit, the others stand down); with
+    # 40 units it runs one block per unit.
+    cfg = W.config(2, layers=1, kv_heads=kv_heads, n=2048, budget=32)
     q, K, V = _planted_far_key(cfg)
     opt = O.Options(fix_window=bool(fix_window))
     from tests.parity import oracle_unit
@@ -308,10 +312,10 @@ def test_retained_mass_far_below_full_cache(fix_window):
     lret = (Q @ r0["K0"].T) / np.sqrt(cfg.head_dim)
     lret = np.where(r0["idx"][None, :] <= r0["pos"][:, None], lret, -np.inf)
     assert np.min(r0["lse"] - lret.max(axis=1)) > 120.0
-    print("case far-key fix_window", fix_window, flush=True)
+    print("case far-key fix_window", fix_window, "units", cfg.units, flush=True)
     gpu = run_gpu(cfg, q, K, V, fix_window=fix_window)
     rep = []
-    for u in range(cfg.units):
+    for u in sorted({0, 1, cfg.units // 2, cfg.units - 1}):
         check_unit(cfg, q, K, V, gpu, u, opt=opt, report=rep)
     for rr in rep:
         print(rr, flush=True)
