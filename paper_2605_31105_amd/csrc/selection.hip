@@ -165,10 +165,139 @@ __device__ void radix_finish(Search& b, const uint32_t* cand, uint32_t L, KthWor
   }
 }
 
+// A first bracket for each search from a sample of the keys: every stride-th
+// key (kSample of them at most, the rest key 0), eight per thread in
+// registers; the samples about 4 sqrt(r) + 16 ranks either side of rank
+// r = k / stride bound T, found by one joint bisection of the four order
+// statistics (counts of two of them packed per word, one barrier per step).
+// One sweep then counts the keys at or above both bounds of both searches
+// exactly; a bracket is taken only when it provably holds T
+// (count(>= lo) >= k > count(>= hi)), so a poor sample costs that sweep and
+// the searches start from the full range as before.
+constexpr int kSample = 2 * kLargeCand;
+constexpr int kSamplePer = kSample / kSelectThreads;
+
+__device__ void sampled_bracket(const float* p, int P, Search (&b)[2], KthWork& wk) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  constexpr int NW = kSelectThreads / 64;
+  static_assert(kSample % kSelectThreads == 0 && kSample < 65536, "packed 16-bit counts");
+  const int stride = (P + kSample - 1) / kSample;   // >= 1
+  const int ns = (P + stride - 1) / stride;         // real samples
+  uint32_t sv[kSamplePer];
+#pragma unroll
+  for (int m = 0; m < kSamplePer; ++m) {
+    const int i = tid + m * kSelectThreads;
+    const int64_t j = min((int64_t)i * stride, (int64_t)P - 1);
+    const uint32_t x = __float_as_uint(p[j]);
+    sv[m] = i < ns ? x : 0u;
+  }
+  // targets 2t (rank jh: the bound above T) and 2t + 1 (rank jl: below T)
+  int J[4];
+  bool act[4];
+  uint32_t lo[2], hi[2];
+  bool try_[2];
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    lo[t] = b[t].lo;
+    hi[t] = b[t].hi;
+    const bool w = b[t].wide();
+    const int r = w ? (int)(b[t].k / (uint32_t)stride) : 0;
+    const int delta = 4 * (int)sqrtf((float)r) + 16;
+    J[2 * t] = r - delta;
+    J[2 * t + 1] = r + delta;
+    act[2 * t] = w && r - delta >= 0;
+    act[2 * t + 1] = w && r + delta < ns;
+    try_[t] = act[2 * t] || act[2 * t + 1];
+  }
+  // the J-th largest sample (0-based) is the largest x with count(>= x) > J:
+  // L keeps count(>= L) > J, H count(>= H) <= J (key 0 counts every sample)
+  uint32_t L[4], H[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) { L[i] = 0u; H[i] = 0x7F800001u; }
+  int parity = 0;
+#pragma unroll 1
+  for (int it = 0; it < 32; ++it) {
+    bool more = false;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) more |= act[i] && H[i] - L[i] > 1;
+    if (!more) break;   // uniform
+    uint32_t mid[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) mid[i] = L[i] + (H[i] - L[i]) / 2;
+    uint32_t c01 = 0, c23 = 0;
+#pragma unroll
+    for (int m = 0; m < kSamplePer; ++m) {
+      c01 += (uint32_t)(sv[m] >= mid[0]) + ((uint32_t)(sv[m] >= mid[1]) << 16);
+      c23 += (uint32_t)(sv[m] >= mid[2]) + ((uint32_t)(sv[m] >= mid[3]) << 16);
+    }
+    c01 = wave_sum_u(c01);
+    c23 = wave_sum_u(c23);
+    if (lane == 0) { wk.part[wave][2 * parity] = c01; wk.part[wave][2 * parity + 1] = c23; }
+    __syncthreads();
+    uint32_t t01 = 0, t23 = 0;
+#pragma unroll
+    for (int q = 0; q < NW; ++q) { t01 += wk.part[q][2 * parity]; t23 += wk.part[q][2 * parity + 1]; }
+    parity ^= 1;   // (the other pair of words next step: one barrier per step)
+    const uint32_t cnt[4] = {t01 & 0xFFFFu, t01 >> 16, t23 & 0xFFFFu, t23 >> 16};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      if (!(act[i] && H[i] - L[i] > 1)) continue;
+      if (cnt[i] > (uint32_t)J[i]) L[i] = mid[i];
+      else H[i] = mid[i];
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    if (act[2 * t]) hi[t] = __builtin_amdgcn_readfirstlane(L[2 * t]);
+    if (act[2 * t + 1]) lo[t] = __builtin_amdgcn_readfirstlane(L[2 * t + 1]);
+    if (!(lo[t] < hi[t])) try_[t] = false;
+  }
+  __syncthreads();   // the last step's words are read before part is reused
+  if (!try_[0] && !try_[1]) return;
+  uint32_t cl[2] = {0u, 0u}, ch[2] = {0u, 0u};
+  for (int j0 = tid; j0 < P; j0 += kLoadBatch * kSelectThreads) {
+    uint32_t kk[kLoadBatch];
+    load_strided(p, j0, P, kk);
+#pragma unroll
+    for (int q = 0; q < kLoadBatch; ++q) {
+      const bool in = j0 + q * kSelectThreads < P;
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        cl[t] += in && kk[q] >= lo[t];
+        ch[t] += in && kk[q] >= hi[t];
+      }
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const uint32_t x = wave_sum_u(cl[t]), y = wave_sum_u(ch[t]);
+    if (lane == 0) { wk.part[wave][2 * t] = x; wk.part[wave][2 * t + 1] = y; }
+  }
+  __syncthreads();
+  if (tid < 4) {
+    uint32_t v = 0;
+    for (int q = 0; q < NW; ++q) v += wk.part[q][tid];
+    wk.tot[tid] = v;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const uint32_t clo = wk.tot[2 * t], chi = wk.tot[2 * t + 1];
+    if (try_[t] && clo >= b[t].k && chi < b[t].k) {
+      b[t].lo = __builtin_amdgcn_readfirstlane(lo[t]);
+      b[t].hi = __builtin_amdgcn_readfirstlane(hi[t]);
+      b[t].clo = __builtin_amdgcn_readfirstlane(clo);
+      b[t].chi = __builtin_amdgcn_readfirstlane(chi);
+    }
+  }
+  __syncthreads();   // part and tot are reused
+}
+
 // The k-th largest keys of both searches (each found exactly: T = lo).
 __device__ void kth_pair(const float* p, int P, Search (&b)[2], KthWork& wk) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   constexpr int NW = kSelectThreads / 64;
+  if (b[0].wide() || b[1].wide()) sampled_bracket(p, P, b, wk);
 #pragma unroll 1
   while (b[0].wide() || b[1].wide()) {
     uint32_t piv[2][kWays - 1], cnt[2][kWays - 1];
