@@ -433,22 +433,32 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(SelK a) {
   const int h = a.h;
   const int CH = kStageFloats - 2 * h >= 2048 ? min(16384, kStageFloats - 2 * h) : 0;
   if (CH > 0) {
+    // a round's CH + 2h scores fit one batch of kLoadBatch per thread; the
+    // next round's are loaded (clamped into the prefix, masked) while this
+    // round pools
+    static_assert(kStageFloats <= kLoadBatch * kSelectThreads, "one load batch per round");
+    float nv[kLoadBatch];
+    auto fetch = [&](int base) {
+#pragma unroll
+      for (int q = 0; q < kLoadBatch; ++q) {
+        const int t = tid + q * kSelectThreads, j = base - h + t;
+        const uint32_t x = __float_as_uint(s[min(max(j, 0), P - 1)]);
+        // masked with an AND, not a select: a select of a load is turned
+        // into a branch around the load, which then waits alone
+        const uint32_t keep = (t < CH + 2 * h && j >= 0 && j < P) ? 0xFFFFFFFFu : 0u;
+        nv[q] = __uint_as_float(x & keep);
+      }
+    };
+    fetch(0);
     for (int base = 0; base < P; base += CH) {
       __syncthreads();
-      for (int t0 = tid; t0 < CH + 2 * h; t0 += kLoadBatch * kSelectThreads) {
-        float v[kLoadBatch];
 #pragma unroll
-        for (int q = 0; q < kLoadBatch; ++q) {
-          const int t = t0 + q * kSelectThreads, j = base - h + t;
-          v[q] = (t < CH + 2 * h && j >= 0 && j < P) ? s[j] : 0.f;
-        }
-#pragma unroll
-        for (int q = 0; q < kLoadBatch; ++q) {
-          const int t = t0 + q * kSelectThreads;
-          if (t < CH + 2 * h) stage[t] = v[q];
-        }
+      for (int q = 0; q < kLoadBatch; ++q) {
+        const int t = tid + q * kSelectThreads;
+        if (t < CH + 2 * h) stage[t] = nv[q];
       }
       __syncthreads();
+      if (base + CH < P) fetch(base + CH);
       for (int q = tid; q < CH && base + q < P; q += kSelectThreads) {
         float acc = 0.f;
         for (int t = 0; t <= 2 * h; ++t) acc += stage[q + t];
@@ -463,7 +473,14 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(SelK a) {
       const int lo = j - h < 0 ? 0 : j - h;
       const int hi = j + h > P - 1 ? P - 1 : j + h;
       float acc = 0.f;
-      for (int t = lo; t <= hi; ++t) acc += s[t];
+      for (int t0 = lo; t0 <= hi; t0 += 8) {   // eight loads in flight, summed left to right
+        float v[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = s[min(t0 + i, hi)];
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+          if (t0 + i <= hi) acc += v[i];
+      }
       p[j] = acc;
       kmin = min(kmin, __float_as_uint(acc));
       kmax = max(kmax, __float_as_uint(acc));
@@ -543,7 +560,14 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(SelK a) {
       const int j = band[t].pos[e];
       const int t0 = j - h < 0 ? 0 : j - h, t1 = j + h > P - 1 ? P - 1 : j + h;
       double acc = 0.0;
-      for (int x = t0; x <= t1; ++x) acc += (double)s[x];
+      for (int x0 = t0; x0 <= t1; x0 += 8) {   // eight loads in flight, summed left to right
+        float v[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) v[i] = s[min(x0 + i, t1)];
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+          if (x0 + i <= t1) acc += (double)v[i];
+      }
       band[t].v64[e] = acc;
     }
   }
