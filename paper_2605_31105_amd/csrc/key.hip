@@ -54,12 +54,6 @@ __device__ __forceinline__ int kperm(int x) {
   return b + ((o & 15) >> 2) * 8 + (o >> 4) * 4 + (o & 3);
 }
 
-// Order of the 32 keys of a tile in the transposed V* rows and in a wave's H
-// rows: key k sits at 2 (k mod 16) + k / 16, so a lane's two keys {k, k + 16}
-// are adjacent, and the eight positions 8g .. 8g + 7 a lane reads as an MFMA
-// operand hold keys {4g + j/2 (+16 for odd j)} in both.
-__device__ __forceinline__ int tpos(int key) { return 2 * (key & 15) + (key >> 4); }
-
 __device__ __forceinline__ float dot4(float4 a, float4 b) {
   return a.x * b.x + a.y * b.y + a.z * b.z + a.w * b.w;
 }

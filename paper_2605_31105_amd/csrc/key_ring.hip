@@ -47,11 +47,10 @@ constexpr int kRStage = kRXB + 2 * kRTB;          // X^T, V* hi, V* lo
 constexpr int kRDB = kRMP * kRTK * 2;             // one D tile, hi or lo (8 KB)
 constexpr int kRLoads = kRStage / 1024 / kRW;     // tile loads per wave per tile (4)
 
-// 16-byte chunk permutations inside a 256-byte tile row (key row r).  K rows
-// are read 16 rows x one chunk (r mod 16 keeps those on distinct banks); V*
-// rows are read that way and also by the transpose read as 8 rows x two
-// adjacent chunks per half wave, which 2 (r mod 8) + (r / 8 mod 2) serves both.
-__device__ __forceinline__ int kswz(int r) { return r & 15; }
+// 16-byte chunk permutation inside a 256-byte V* tile row (key row r): the
+// rows are read 16 rows x one chunk and also by the transpose read as 8 rows x
+// two adjacent chunks per half wave, which 2 (r mod 8) + (r / 8 mod 2) keeps
+// on distinct banks in both.
 __device__ __forceinline__ int vswz(int r) { return ((r & 7) << 1) | ((r >> 3) & 1); }
 // 8-byte unit permutation inside a 64-byte D row (query row R): the row
 // writes (16 rows x 2 units per half wave) and the transpose reads (8 rows x
