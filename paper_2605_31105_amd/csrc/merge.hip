@@ -941,10 +941,12 @@ hipError_t launch_update_t(const Plan& p, const void* q, const void* k0, const f
 
 int update_slots_per_block(const Plan& p, int c) {
   // about one block per compute unit: split a unit's slots over several
-  // blocks only when there are fewer units than that
-  const int pair_rows = 32 * kUpdWaves;
+  // blocks only when there are fewer units than that, down to 128 slots per
+  // block (half of the waves' 32-slot pairs: a one-layer call at c = 2048
+  // measured 156 us per call with 128 or 64 slots per block, 158 with 256)
+  const int least_slots = 16 * kUpdWaves;
   int bpu = (256 + p.U - 1) / p.U;
-  const int most = (c + pair_rows - 1) / pair_rows;
+  const int most = (c + least_slots - 1) / least_slots;
   if (bpu > most) bpu = most;
   const int least = (c + kUpdMaxSlots - 1) / kUpdMaxSlots;
   if (bpu < least) bpu = least;
