@@ -106,3 +106,33 @@ def test_h2o_end_to_end_against_oracle(pool):
         v_err = np.abs(res.v_out[u].cpu().numpy() - r["Vstar"]).max() / np.abs(r["Vstar"]).max()
         print("pool", pool, "unit", u, "v_err %.2e" % v_err, flush=True)
         assert v_err <= 2e-3
+
+
+def test_compress_scored_long_prefix_sample_misses_the_top():
+    # a prefix past 32768 positions takes the long-prefix selection, whose
+    # first brackets come from every 5th score (stride = ceil(P / 8192)); here
+    # every sampled position holds a low score and the top-k lies among the
+    # others, so the brackets fail their exact count check and both searches
+    # run from the full range: the selection must still equal the oracle's
+    import paper_2605_31105_amd as G
+    cfg = W.config(2, layers=1, kv_heads=2, n=40000, budget=2048, pool_kernel=1)
+    q, K, V = W.make_batch(cfg)
+    P = cfg.n - cfg.window
+    stride = -(-P // 8192)
+    assert stride == 5
+    rng = np.random.default_rng(11)
+    s = (1.0 + rng.random((cfg.units, P))).astype(np.float32)
+    s[:, ::stride] = (1e-3 * (1.0 + rng.random((cfg.units, (P + stride - 1) // stride)))).astype(np.float32)
+    qd, Kd, Vd = (to_device(a, cfg.dtype) for a in (q, K, V))
+    print("case scored long prefix, sampled positions low", flush=True)
+    res = G.compress_scored(qd, Kd, Vd, cfg.window, cfg.budget, 1, cfg.lam,
+                            torch.from_numpy(s).cuda())
+    torch.cuda.synchronize()
+    gpu = dict(idx=res.idx.cpu().numpy(), v_out=res.v_out.cpu().numpy(),
+               stats=res.stats.cpu().numpy(),
+               **{k: v.cpu().numpy() for k, v in G.intermediates(res).items()})
+    gpu["k_out"] = res.k_out.cpu().view(torch.int16).numpy().view(np.uint16)
+    for u in range(cfg.units):
+        kept = gpu["idx"][u][: cfg.budget - cfg.window]
+        assert np.all(kept % stride != 0)   # no sampled (low) position is kept
+        print(check_unit(cfg, q, K, V, gpu, u, scores=s[u].astype(np.float64)), flush=True)
